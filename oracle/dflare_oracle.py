@@ -1,0 +1,295 @@
+"""Plain fp64 CPU oracle of the DFlare draft step (arXiv 2606.02091).
+
+TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and bench.py's
+cpu_baseline leg may import this module.  The HIP library and its Python binding
+never import, call or link it, and it imports nothing from them.
+
+What is computed (all floating point in fp64; inputs are bfloat16 bit patterns
+(uint16) up-cast exactly):
+
+* fusion weights  alpha^(i) = softmax(W^fuse_{i,:})        -- Sec. 4.1, Eq. 3, first line;
+                                                              cached once (Sec. 4.1, text after Eq. 3)
+* fused rows      f_t^(i) = RMSNorm(sum_j alpha_j^(i) h_t^(j)) -- Sec. 4.1, Eq. 3, second line
+* context K/V     K = F^(i) W_K^t,  V = F^(i) W_V^t           -- Sec. 4.2, Eq. 4, first block
+* block K/V/Q     x W_K^d, x W_V^d, x W_Q for the B block rows -- Sec. 4.2, Eq. 4, other blocks
+* attention       bidirectional inside the block and over the full context;
+                  only the B block rows go on to the next layer, the context is
+                  fixed across layers                           -- Sec. 3.2 (drafting phase)
+* MLP sub-layer, final LM head, one token per block position    -- Sec. 3.2 (drafting phase)
+
+Readings where the paper is silent (each is listed in the design doc):
+  pre-norm block with residuals around attention and MLP, SwiGLU MLP, no biases,
+  final RMSNorm before the LM head; RMSNorm(x; g) = x / sqrt(mean(x^2) + eps) * g;
+  rotary position embedding in the rotate-half convention on Q and K (context K
+  rotated at its own position when appended, V never rotated); context row r sits
+  at position r and block row b at position L + b; scale 1/sqrt(head_dim); query
+  head h reads KV head floor(h / (n_q / n_kv)); the block's own K/V are not kept
+  in the cache; greedy argmax with ties going to the lowest token id.
+
+Weights use the [out, in] row-major convention: y = x @ W.T (the paper writes x W
+with W in R^{d x d_kv}; it is the same map).
+
+Parity pins: see tests/test_oracle_pins.py (closed forms, invariants, brute force,
+library routines).  Parity unpinned: the readings above that the paper leaves
+open (layer internals, rotary convention, positions) -- any consistent reading
+satisfies the paper's equations, so nothing in the paper can fix them.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+__all__ = [
+    "bf16_to_f64", "fusion_weights", "rms_norm", "rope", "silu", "fuse_rows",
+    "context_kv", "block_attention", "draft_layer", "lm_head_logits", "argmax_lowest",
+    "DraftOracle",
+]
+
+
+def bf16_to_f64(u16) -> np.ndarray:
+    """bfloat16 bit patterns -> float64 (exact: bf16 is a prefix of fp32)."""
+    u = np.asarray(u16, dtype=np.uint16)
+    return (u.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def fusion_weights(fusion_logits) -> np.ndarray:
+    """alpha^(i) = softmax over target layers of row i of W^fuse  (Sec. 4.1, Eq. 3).
+
+    fusion_logits: [D, S] real.  Returns [D, S] fp64 with rows summing to 1.
+    The maximum of each row is subtracted first so that large logits do not
+    overflow; this does not change the softmax.  Raises ValueError for a row with
+    a NaN, +inf, or no finite entry.
+    """
+    lg = np.asarray(fusion_logits, dtype=np.float64)
+    if lg.ndim != 2:
+        raise ValueError("fusion logits must be [D, S]")
+    if np.isnan(lg).any() or np.isposinf(lg).any():
+        raise ValueError("fusion logits must not contain NaN or +inf")
+    if not np.isfinite(lg).any(axis=1).all():
+        raise ValueError("each fusion-logit row needs a finite entry")
+    m = lg.max(axis=1, keepdims=True)
+    e = np.exp(lg - m)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def rms_norm(x: np.ndarray, gain, eps: float) -> np.ndarray:
+    """RMSNorm over the last axis: x / sqrt(mean(x^2) + eps), times gain if given."""
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    y = x / np.sqrt(ms + eps)
+    return y if gain is None else y * gain
+
+
+def rope(x: np.ndarray, positions, base: float) -> np.ndarray:
+    """Rotary embedding, rotate-half convention.
+
+    x: [n, heads, hd]; positions: [n].  For m < hd/2, theta = p * base^(-2m/hd) and
+    (x_m, x_{m+hd/2}) -> (x_m cos - x_{m+hd/2} sin, x_{m+hd/2} cos + x_m sin).
+    """
+    hd = x.shape[-1]
+    half = hd // 2
+    inv_freq = base ** (-(2.0 * np.arange(half, dtype=np.float64)) / hd)
+    theta = np.asarray(positions, dtype=np.float64)[:, None] * inv_freq[None, :]
+    c = np.cos(theta)[:, None, :]
+    s = np.sin(theta)[:, None, :]
+    x1, x2 = x[..., :half], x[..., half:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def silu(z: np.ndarray) -> np.ndarray:
+    return z / (1.0 + np.exp(-z))
+
+
+def fuse_rows(alpha: np.ndarray, hidden: np.ndarray, gains, eps: float) -> np.ndarray:
+    """Layer-specific fused rows f^(i)  (Sec. 4.1, Eq. 3).
+
+    alpha: [D, S]; hidden: [S, n, H] fp64; gains: [D, H] or None.
+    u^(i) = sum_j alpha[i, j] h^(j) is accumulated in j order, one row at a time,
+    so a row's value does not depend on which other rows are fused with it.
+    Returns [D, n, H].
+    """
+    D, S = alpha.shape
+    out = np.empty((D,) + hidden.shape[1:], dtype=np.float64)
+    for i in range(D):
+        u = np.zeros(hidden.shape[1:], dtype=np.float64)
+        for j in range(S):
+            u += alpha[i, j] * hidden[j]
+        out[i] = rms_norm(u, None if gains is None else gains[i], eps)
+    return out
+
+
+def context_kv(f_i: np.ndarray, wk_t: np.ndarray, wv_t: np.ndarray, positions,
+               n_kv: int, hd: int, base: float):
+    """Context keys/values of one draft layer  (Sec. 4.2, Eq. 4, first block).
+
+    f_i: [n, H] fused rows; wk_t, wv_t: [n_kv*hd, H].  K is rotated at the rows'
+    own positions; V is not rotated.  Returns K, V as [n, n_kv, hd].
+    """
+    n = f_i.shape[0]
+    k = (f_i @ wk_t.T).reshape(n, n_kv, hd)
+    v = (f_i @ wv_t.T).reshape(n, n_kv, hd)
+    return rope(k, positions, base), v
+
+
+def block_attention(q, k_ctx, v_ctx, k_blk, v_blk) -> np.ndarray:
+    """Block attention without any mask  (Sec. 3.2, drafting phase; Sec. 4.2).
+
+    q: [B, n_q, hd]; k_ctx/v_ctx: [L, n_kv, hd]; k_blk/v_blk: [B, n_kv, hd].
+    Every block row attends to all L context keys and all B block keys (itself
+    included).  Query head h uses KV head h // (n_q / n_kv).  Returns [B, n_q, hd].
+    """
+    B, nq, hd = q.shape
+    nkv = k_blk.shape[1]
+    group = nq // nkv
+    keys = np.concatenate([k_ctx, k_blk], axis=0)
+    vals = np.concatenate([v_ctx, v_blk], axis=0)
+    out = np.empty_like(q)
+    for h in range(nq):
+        g = h // group
+        s = (q[:, h, :] @ keys[:, g, :].T) / math.sqrt(hd)
+        s = s - s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        p = p / p.sum(axis=1, keepdims=True)
+        out[:, h, :] = p @ vals[:, g, :]
+    return out
+
+
+def draft_layer(X, lw: dict, k_ctx, v_ctx, positions, cfg) -> np.ndarray:
+    """One draft Transformer layer over the B block rows.
+
+    lw holds this layer's fp64 weights: attn_norm, mlp_norm [H]; wq, wk_d, wv_d,
+    wo, w_gate, w_up, w_down as [out, in].  Queries and block keys/values come from
+    the block rows through W_Q, W_K^d, W_V^d (Eq. 4); the context K/V come from the
+    cache.  Returns the new block rows [B, H].
+    """
+    B = X.shape[0]
+    nq, nkv, hd = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    a = rms_norm(X, lw["attn_norm"], cfg.rms_eps)
+    q = rope((a @ lw["wq"].T).reshape(B, nq, hd), positions, cfg.rope_base)
+    kb = rope((a @ lw["wk_d"].T).reshape(B, nkv, hd), positions, cfg.rope_base)
+    vb = (a @ lw["wv_d"].T).reshape(B, nkv, hd)
+    o = block_attention(q, k_ctx, v_ctx, kb, vb).reshape(B, nq * hd)
+    X = X + o @ lw["wo"].T
+    m = rms_norm(X, lw["mlp_norm"], cfg.rms_eps)
+    return X + (silu(m @ lw["w_gate"].T) * (m @ lw["w_up"].T)) @ lw["w_down"].T
+
+
+def lm_head_logits(X, final_norm, lm_head_bf16, eps: float, chunk: int = 16384) -> np.ndarray:
+    """Logits z = RMSNorm(X; g_final) W_lm^T over the full vocabulary (Sec. 3.2).
+
+    lm_head_bf16: [V, H] bf16 bits, converted in vocabulary chunks.
+    """
+    xn = rms_norm(X, final_norm, eps)
+    V = lm_head_bf16.shape[0]
+    z = np.empty((X.shape[0], V), dtype=np.float64)
+    for v0 in range(0, V, chunk):
+        z[:, v0:v0 + chunk] = xn @ bf16_to_f64(lm_head_bf16[v0:v0 + chunk]).T
+    return z
+
+
+def argmax_lowest(z: np.ndarray) -> np.ndarray:
+    """Greedy token per row: the lowest index among the maxima."""
+    return np.argmax(z, axis=-1).astype(np.int32)
+
+
+_LAYER_KINDS = ("attn_norm", "mlp_norm", "wq", "wk_d", "wv_d", "wo", "w_gate", "w_up", "w_down")
+
+
+class DraftOracle:
+    """Stateful fp64 draft model: a context cache per draft layer plus block passes.
+
+    cfg: any object with the attributes hidden, n_q_heads, n_kv_heads, head_dim,
+    ffn, vocab, n_draft_layers, n_target_layers, block_size, rope_base, rms_eps.
+    weights: dict of bf16 bit arrays as laid out by the input generator
+    (embed, lm_head [V, H]; final_norm [H]; fuse/attn/mlp_norm [D, H]; linear
+    weights [D, out, in]); a norm entry may be None for unit gains.
+    fusion_logits: [D, S].
+    """
+
+    def __init__(self, cfg, weights: dict, fusion_logits, max_context: int = 1 << 16,
+                 cache_weights: bool = False):
+        self.cfg = cfg
+        self.w = weights
+        self.alpha = fusion_weights(fusion_logits)
+        D = cfg.n_draft_layers
+        if self.alpha.shape != (D, cfg.n_target_layers):
+            raise ValueError("fusion logits must be [D, S]")
+        self.max_context = max_context
+        self.L = 0
+        self.k_cache = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(D)]
+        self.v_cache = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(D)]
+        self._cache_weights = cache_weights
+        self._lw: dict[int, dict] = {}
+        self.last_fused = None
+
+    # -- weights -------------------------------------------------------------
+    def _gain(self, kind, i=None):
+        g = self.w.get(kind)
+        if g is None:
+            return None
+        return bf16_to_f64(g if i is None else g[i])
+
+    def layer_weights(self, i: int) -> dict:
+        if i in self._lw:
+            return self._lw[i]
+        lw = {k: (self._gain(k, i) if k.endswith("norm") else bf16_to_f64(self.w[k][i]))
+              for k in _LAYER_KINDS}
+        if self._cache_weights:
+            self._lw[i] = lw
+        return lw
+
+    # -- context -------------------------------------------------------------
+    def append(self, hidden_bf16, positions=None) -> np.ndarray:
+        """Fuse n new target rows [S, n, H] and append their K/V to every layer.
+
+        Returns the fused rows [D, n, H] (Eq. 3).  Positions default to L..L+n-1.
+        """
+        cfg = self.cfg
+        h = bf16_to_f64(hidden_bf16)
+        S, n, H = h.shape
+        if S != cfg.n_target_layers or H != cfg.hidden:
+            raise ValueError("target hidden rows must be [S, n, H]")
+        if self.L + n > self.max_context:
+            raise ValueError("context full")
+        pos = np.arange(self.L, self.L + n) if positions is None else np.asarray(positions)
+        fuse_g = self.w.get("fuse_norm")
+        gains = None if fuse_g is None else bf16_to_f64(fuse_g)
+        f = fuse_rows(self.alpha, h, gains, cfg.rms_eps)
+        for i in range(cfg.n_draft_layers):
+            k, v = context_kv(f[i], bf16_to_f64(self.w["wk_t"][i]), bf16_to_f64(self.w["wv_t"][i]),
+                              pos, cfg.n_kv_heads, cfg.head_dim, cfg.rope_base)
+            self.k_cache[i] = np.concatenate([self.k_cache[i], k], axis=0)
+            self.v_cache[i] = np.concatenate([self.v_cache[i], v], axis=0)
+        self.L += n
+        self.last_fused = f
+        return f
+
+    def truncate(self, new_len: int) -> None:
+        if not 0 <= new_len <= self.L:
+            raise ValueError("truncate length out of range")
+        for i in range(self.cfg.n_draft_layers):
+            self.k_cache[i] = self.k_cache[i][:new_len]
+            self.v_cache[i] = self.v_cache[i][:new_len]
+        self.L = new_len
+
+    # -- block pass ----------------------------------------------------------
+    def draft_block(self, ids, positions=None, keep_logits: bool = True) -> dict:
+        """One drafting forward pass over the block ids [B]  (Sec. 3.2).
+
+        Returns dict(tokens [B] int32, logits [B, V] (if keep_logits),
+        hidden [D, B, H] = block rows after each layer).
+        """
+        cfg = self.cfg
+        ids = np.asarray(ids, dtype=np.int64)
+        B = ids.shape[0]
+        pos = np.arange(self.L, self.L + B) if positions is None else np.asarray(positions)
+        X = bf16_to_f64(self.w["embed"][ids])
+        hs = []
+        for i in range(cfg.n_draft_layers):
+            X = draft_layer(X, self.layer_weights(i), self.k_cache[i], self.v_cache[i], pos, cfg)
+            hs.append(X)
+        z = lm_head_logits(X, self._gain("final_norm"), self.w["lm_head"], cfg.rms_eps)
+        out = {"tokens": argmax_lowest(z), "hidden": np.stack(hs)}
+        if keep_logits:
+            out["logits"] = z
+        return out
