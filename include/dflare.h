@@ -1,0 +1,193 @@
+/*
+ * dflare.h -- C ABI of the DFlare draft step on AMD Instinct MI355X (gfx950).
+ *
+ * The library computes the per-iteration draft step of DFlare (arXiv 2606.02091):
+ *   - layer fusion: each draft layer i fuses the hidden rows of S target layers
+ *     with its own softmax weights, alpha^(i) = softmax(W^fuse_{i,:}), then RMSNorm
+ *     (Sec. 4.1, Eq. 3; alpha is computed once at init, as Sec. 4.1 allows);
+ *   - heterogeneous context K/V: the fused rows of layer i go through that layer's
+ *     own W_K^t, W_V^t into its KV cache (Sec. 4.2, Eq. 4, first block);
+ *   - the drafting forward pass: the B block rows [x_t; mask x (B-1)] run through
+ *     D draft layers with block K/V from W_K^d, W_V^d (Eq. 4, other blocks),
+ *     attention that is bidirectional inside the block and sees the whole context,
+ *     an MLP sub-layer, then the shared LM head and one token per position
+ *     (Sec. 3.2, drafting phase).
+ *
+ * Readings where the paper is silent: pre-norm layers with residuals around
+ * attention and MLP, SwiGLU MLP, no biases, final RMSNorm before the LM head,
+ * RMSNorm(x; g) = x / sqrt(mean(x^2) + eps) * g, rotary embedding in the
+ * rotate-half convention (context keys rotated at their own positions when
+ * appended), context row r at position r and block row b at position L + b,
+ * scale 1/sqrt(head_dim), query head h uses KV head h / (n_q / n_kv), greedy
+ * argmax with ties to the lowest id.
+ *
+ * Conventions for every entry point:
+ *   - Return value: DFLARE_OK (0) or a negative dflare_status.  Nothing throws.
+ *   - Arguments are validated before any work is enqueued; a call that fails
+ *     validation changes no state (context length, cache, handle).
+ *   - Device pointers are borrowed: the caller keeps ownership and must keep them
+ *     valid until the work enqueued on the handle's stream has completed.
+ *   - Work is enqueued on the handle's stream and the call returns without
+ *     waiting (except where stated).  Results are valid once that stream is
+ *     synchronised.
+ *   - A handle is not thread-safe: calls on one handle must not overlap.
+ *   - bf16 means IEEE-754 binary32 truncated to its upper 16 bits (bfloat16),
+ *     passed as raw 16-bit patterns.
+ */
+#ifndef DFLARE_H
+#define DFLARE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DFLARE_OK = 0,
+  DFLARE_ERR_INVALID_ARG = -1,   /* bad pointer, size, shape or value            */
+  DFLARE_ERR_OUT_OF_MEMORY = -2, /* device allocation failed                      */
+  DFLARE_ERR_CONTEXT_FULL = -3,  /* append would exceed max_context               */
+  DFLARE_ERR_HIP = -4,           /* a HIP runtime call failed                     */
+  DFLARE_ERR_UNSUPPORTED = -5    /* shape the kernels do not support (see init)   */
+} dflare_status;
+
+/* Model and capacity.  All sizes are element counts. */
+typedef struct {
+  int32_t hidden;          /* H (the paper's d)                                  */
+  int32_t n_q_heads;       /* query heads                                        */
+  int32_t n_kv_heads;      /* key/value heads (n_q_heads % n_kv_heads == 0)      */
+  int32_t head_dim;        /* per-head width                                     */
+  int32_t ffn;             /* SwiGLU inner width                                 */
+  int32_t vocab;           /* V                                                  */
+  int32_t n_draft_layers;  /* D                                                  */
+  int32_t n_target_layers; /* S (the paper's T), fused target layers             */
+  int32_t block_size;      /* B, 1..16                                           */
+  int32_t max_context;     /* L_max: capacity of the per-layer context cache     */
+  int32_t max_new;         /* largest n_new accepted by dflare_fuse_append       */
+  float rope_base;         /* rotary base, e.g. 1e6                              */
+  float rms_eps;           /* RMSNorm epsilon, e.g. 1e-6                         */
+} dflare_config;
+
+/*
+ * Draft weights: device pointers to bf16 tensors, row-major, linear weights in the
+ * [out, in] convention (y = x W^T), stacked over the D draft layers.
+ * q = n_q_heads * head_dim, kv = n_kv_heads * head_dim.
+ * A NULL norm gain means all ones.  Init copies and re-packs everything, so the
+ * caller may free these buffers once dflare_init has returned.
+ */
+typedef struct {
+  const void* embed;      /* [V, H]     shared token embedding (Sec. 3.3)       */
+  const void* lm_head;    /* [V, H]     shared LM head (Sec. 3.3)               */
+  const void* final_norm; /* [H]        gain of the final RMSNorm, or NULL      */
+  const void* fuse_norm;  /* [D, H]     gain of the RMSNorm in Eq. 3, or NULL   */
+  const void* attn_norm;  /* [D, H]     pre-attention RMSNorm gain, or NULL     */
+  const void* mlp_norm;   /* [D, H]     pre-MLP RMSNorm gain, or NULL           */
+  const void* wq;         /* [D, q, H]  W_Q                                     */
+  const void* wk_d;       /* [D, kv, H] W_K^d (block rows, Eq. 4)               */
+  const void* wv_d;       /* [D, kv, H] W_V^d                                   */
+  const void* wk_t;       /* [D, kv, H] W_K^t (fused target context, Eq. 4)     */
+  const void* wv_t;       /* [D, kv, H] W_V^t                                   */
+  const void* wo;         /* [D, H, q]  attention output projection             */
+  const void* w_gate;     /* [D, F, H]  SwiGLU gate                             */
+  const void* w_up;       /* [D, F, H]  SwiGLU up                               */
+  const void* w_down;     /* [D, H, F]  SwiGLU down                             */
+} dflare_weights;
+
+typedef struct dflare_handle dflare_handle;
+
+/*
+ * dflare_init -- build a draft model (Sec. 4.1 Eq. 3, Sec. 4.2 Eq. 4, Sec. 3.2).
+ *   cfg            model shape and capacity.  Supported: hidden, q, kv, ffn
+ *                  multiples of 32; head_dim 64 or 128; 1 <= block_size <= 16;
+ *                  n_kv_heads * 16 >= ... (any); otherwise DFLARE_ERR_UNSUPPORTED.
+ *   weights        device bf16 tensors as described above (copied and packed).
+ *   fusion_logits  HOST float [D, S] = W^fuse.  alpha = softmax of each row is
+ *                  computed here in double precision and cached as float.  A row
+ *                  with NaN or +inf, or with no finite entry, is INVALID_ARG.
+ *   stream         hipStream_t for all work of this handle (NULL = default stream).
+ *   out            receives the handle.  The context starts empty (L = 0).
+ * Synchronises the stream before returning.
+ */
+int dflare_init(const dflare_config* cfg, const dflare_weights* weights,
+                const float* fusion_logits, void* stream, dflare_handle** out);
+
+/*
+ * dflare_fuse_append -- fuse n_new accepted target rows and append their K/V
+ * to every draft layer's cache (Sec. 4.1 Eq. 3, Sec. 4.2 Eq. 4 first block).
+ *   target_hidden  DEVICE bf16 [S, n_new, H] (target layer major).  Row r of the
+ *                  call becomes context position L + r.
+ *   n_new          1 <= n_new <= max_new, else INVALID_ARG;
+ *                  L + n_new > max_context gives CONTEXT_FULL and changes nothing.
+ * On success L grows by n_new.
+ */
+int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_new);
+
+/*
+ * dflare_draft_block -- one drafting forward pass (Sec. 3.2, drafting phase).
+ *   block_ids      DEVICE int32 [B]: x_t at index 0, the mask id at 1..B-1 (the
+ *                  library treats all ids alike; ids outside [0, V) are clamped).
+ *   draft_tokens   DEVICE int32 [B]: greedy token at every block position; index 0
+ *                  is not a candidate (the B-1 candidates are 1..B-1).
+ * Block row b sits at position L + b.  The context cache is not modified, so the
+ * call can be repeated.  An empty context (L = 0) is allowed.
+ */
+int dflare_draft_block(dflare_handle* h, const int32_t* block_ids, int32_t* draft_tokens);
+
+/*
+ * dflare_draft_block_pos -- as dflare_draft_block, with explicit block positions
+ * (a test entry for position-dependent invariants).
+ *   positions      HOST int32 [B], each in [0, max_context + block_size).
+ */
+int dflare_draft_block_pos(dflare_handle* h, const int32_t* block_ids, const int32_t* positions,
+                           int32_t* draft_tokens);
+
+/* dflare_truncate -- roll the context back to new_len (0 <= new_len <= L). */
+int dflare_truncate(dflare_handle* h, int32_t new_len);
+
+/* dflare_context_len -- current context length L into *out. */
+int dflare_context_len(const dflare_handle* h, int32_t* out);
+
+/* dflare_set_stream -- make later work of the handle go to `stream`. */
+int dflare_set_stream(dflare_handle* h, void* stream);
+
+/* dflare_destroy -- free the handle and everything it owns (synchronises). */
+int dflare_destroy(dflare_handle* h);
+
+/* Status code -> static string. */
+const char* dflare_status_str(int status);
+
+/* Last error message of the handle (static empty string when none or h is NULL). */
+const char* dflare_last_error(const dflare_handle* h);
+
+/*
+ * Debug capture (tests).  While on, draft_block keeps the block rows after each
+ * layer and the full logits, and fuse_append keeps the fused rows f^(i).
+ * dflare_debug_read synchronises the stream and copies one tensor to HOST float:
+ *   what = DFLARE_DBG_FUSED   layer i: [n_last, H]   fused rows f^(i) of the last append
+ *   what = DFLARE_DBG_KCACHE  layer i: [L, n_kv, hd] context keys (after RoPE)
+ *   what = DFLARE_DBG_VCACHE  layer i: [L, n_kv, hd] context values
+ *   what = DFLARE_DBG_HIDDEN  layer i: [B, H]        block rows after layer i
+ *   what = DFLARE_DBG_LOGITS  (layer ignored) [B, V] logits of the last draft_block
+ *   what = DFLARE_DBG_ALPHA   (layer ignored) [D, S] cached fusion weights
+ * `count` is the number of floats host_out can hold; too small is INVALID_ARG.
+ */
+enum { DFLARE_DBG_FUSED = 0, DFLARE_DBG_KCACHE = 1, DFLARE_DBG_VCACHE = 2,
+       DFLARE_DBG_HIDDEN = 3, DFLARE_DBG_LOGITS = 4, DFLARE_DBG_ALPHA = 5 };
+int dflare_debug_capture(dflare_handle* h, int on);
+int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, int64_t count);
+
+/*
+ * dflare_kernel_stats -- launch configuration of the dominant kernels, for
+ * measurement: writes up to `count` int32 values
+ *   [0] number of kernels one draft_block enqueues
+ *   [1] number of kernels one fuse_append enqueues
+ * Returns DFLARE_OK.
+ */
+int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DFLARE_H */

@@ -1,0 +1,647 @@
+// Host runtime and C ABI of the DFlare draft step (see include/dflare.h).
+//
+// One handle owns: the re-packed weights, the cached fusion weights alpha, the
+// per-draft-layer context cache (K as [n_kv, Lcap, hd], V transposed as
+// [n_kv, hd, Lcap], both bf16), a rotary table, and the scratch of one step.
+// Every call enqueues a fixed sequence of kernels on the handle's stream; the
+// values that change between calls (L, n_new, positions) travel through a
+// device-resident StepParams block written by a one-thread prologue kernel.
+#include <math.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <mutex>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "dflare.h"
+#include "dflare_impl.h"
+
+using namespace dflare;
+
+namespace {
+
+const uint32_t kMagic = 0xDF1A2E00u;
+
+struct Plan {
+  int nt = 1;      // n-tiles per wave
+  int ktps = 16;   // k-tiles per split
+  int splits = 1;
+  int groups = 1;
+};
+
+std::mutex g_mu;
+std::unordered_set<const dflare_handle*> g_live;
+thread_local std::string g_init_error;
+
+int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
+
+}  // namespace
+
+struct dflare_handle {
+  uint32_t magic = kMagic;
+  dflare_config cfg{};
+  hipStream_t stream = nullptr;
+  int L = 0;
+  int Lcap = 0;
+  int q_dim = 0, kv_dim = 0;
+  int Rpad = 0;
+  // packed weights
+  u32x4 *w_qkv = nullptr, *w_o = nullptr, *w_gu = nullptr, *w_down = nullptr, *w_kvt = nullptr, *w_lm = nullptr;
+  long s_qkv = 0, s_o = 0, s_gu = 0, s_down = 0, s_kvt = 0;
+  uint16_t* embed = nullptr;
+  float *g_fuse = nullptr, *g_attn = nullptr, *g_mlp = nullptr, *g_final = nullptr;
+  float* alpha = nullptr;
+  std::vector<float> alpha_host;
+  // context cache
+  uint16_t *kc = nullptr, *vt = nullptr;
+  long cache_layer_stride = 0;
+  float2* rope = nullptr;
+  // step scratch
+  StepParams* params = nullptr;
+  int* ids = nullptr;
+  float *X = nullptr, *Xstats = nullptr, *Q = nullptr, *O = nullptr, *Hact = nullptr;
+  float *U = nullptr, *Ustats = nullptr;
+  float* partials = nullptr;
+  unsigned* counters = nullptr;
+  float* opart = nullptr;
+  float2* ml = nullptr;
+  float* pmax = nullptr;
+  int* pidx = nullptr;
+  unsigned* counter2 = nullptr;
+  Plan p_qkv, p_o, p_gu, p_down, p_lm, p_kvt;
+  int attn_chunk = 128, attn_nchunks = 1;
+  // debug capture
+  bool debug = false;
+  float *dbg_hidden = nullptr, *dbg_logits = nullptr, *dbg_fused = nullptr;
+  int dbg_fused_n = 0;
+  std::vector<void*> allocs;
+  std::string err;
+};
+
+namespace {
+
+int fail(dflare_handle* h, int code, const std::string& msg) {
+  if (h) h->err = msg;
+  else g_init_error = msg;
+  return code;
+}
+
+#define HIP_OR_FAIL(h, call)                                                                     \
+  do {                                                                                           \
+    hipError_t e_ = (call);                                                                      \
+    if (e_ != hipSuccess)                                                                        \
+      return fail((h), DFLARE_ERR_HIP, std::string(#call ": ") + hipGetErrorString(e_));         \
+  } while (0)
+
+template <typename T>
+int dev_alloc(dflare_handle* h, T** p, size_t bytes) {
+  if (bytes == 0) bytes = 256;
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(h, DFLARE_ERR_OUT_OF_MEMORY, "hipMalloc of " + std::to_string(bytes) + " bytes failed");
+  }
+  h->allocs.push_back(q);
+  *p = static_cast<T*>(q);
+  return DFLARE_OK;
+}
+
+void free_all(dflare_handle* h) {
+  for (void* p : h->allocs) (void)hipFree(p);
+  h->allocs.clear();
+}
+
+bool live(const dflare_handle* h) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  return h && g_live.count(h) && h->magic == kMagic;
+}
+
+// Plan of a weight-streaming GEMM: n-tiles per wave and k-tiles per split.  The
+// defaults can be overridden with DFLARE_PLAN_<NAME>=nt,ktps (used for tuning).
+Plan make_plan(const char* name, int Nt, int Kt, int nt, int ktps) {
+  char key[64];
+  snprintf(key, sizeof key, "DFLARE_PLAN_%s", name);
+  if (const char* env = getenv(key)) {
+    int a = 0, b = 0;
+    if (sscanf(env, "%d,%d", &a, &b) == 2 && (a == 1 || a == 2 || a == 4) && b >= 1) {
+      nt = a;
+      ktps = b;
+    }
+  }
+  Plan p;
+  p.nt = nt;
+  ktps = std::min(ktps, Kt);
+  p.splits = ceil_div(Kt, ktps);
+  p.ktps = ceil_div(Kt, p.splits);  // balance the splits
+  p.splits = ceil_div(Kt, p.ktps);
+  p.groups = ceil_div(Nt, 4 * nt);
+  return p;
+}
+
+long plan_partials(const Plan& p, int Nt, int layers, int mtiles) {
+  return p.splits > 1 ? (long)layers * mtiles * p.splits * Nt * 256 : 0;
+}
+
+long plan_counters(const Plan& p, int layers, int mtiles) { return (long)layers * mtiles * p.groups; }
+
+GemmArgs gemm_args(const dflare_handle* h, const Plan& p, const u32x4* W, int Nt, int Kt) {
+  GemmArgs a{};
+  a.W = W;
+  a.Nt = Nt;
+  a.Kt = Kt;
+  a.kt_per_split = p.ktps;
+  a.splits = p.splits;
+  a.partials = h->partials;
+  a.counters = h->counters;
+  a.eps = h->cfg.rms_eps;
+  a.e.params = h->params;
+  a.e.Lcap = h->Lcap;
+  a.e.hd = h->cfg.head_dim;
+  a.e.rope = h->rope;
+  a.e.B = h->cfg.block_size;
+  return a;
+}
+
+int check_launch(dflare_handle* h, const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(h, DFLARE_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  return DFLARE_OK;
+}
+
+int validate_config(const dflare_config* c) {
+  if (!c) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "cfg is NULL");
+  if (c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0 || c->ffn <= 0 ||
+      c->vocab <= 0 || c->n_draft_layers <= 0 || c->n_target_layers <= 0 || c->block_size <= 0 ||
+      c->max_context <= 0 || c->max_new <= 0)
+    return fail(nullptr, DFLARE_ERR_INVALID_ARG, "every size in dflare_config must be positive");
+  if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f) || !isfinite(c->rope_base) || !isfinite(c->rms_eps))
+    return fail(nullptr, DFLARE_ERR_INVALID_ARG, "rope_base must be > 0 and rms_eps >= 0");
+  if (c->n_q_heads % c->n_kv_heads)
+    return fail(nullptr, DFLARE_ERR_INVALID_ARG, "n_q_heads must be a multiple of n_kv_heads");
+  if (c->block_size > 16) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "block_size must be <= 16");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->hidden % 32 || c->ffn % 32 || (c->n_q_heads * c->head_dim) % 32)
+    return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "hidden, ffn and n_q_heads*head_dim must be multiples of 32");
+  if ((c->n_q_heads / c->n_kv_heads) * c->block_size > 128)
+    return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "(n_q_heads / n_kv_heads) * block_size must be <= 128");
+  if (c->n_target_layers > 64) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "n_target_layers must be <= 64");
+  if ((long)c->max_context + c->block_size > (1L << 30))
+    return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "max_context too large");
+  return DFLARE_OK;
+}
+
+#define TRY(x)                         \
+  do {                                 \
+    int rc_ = (x);                     \
+    if (rc_ != DFLARE_OK) return rc_;  \
+  } while (0)
+
+int build(dflare_handle* h, const dflare_weights* w) {
+  const dflare_config& c = h->cfg;
+  const int H = c.hidden, D = c.n_draft_layers, S = c.n_target_layers, F = c.ffn, V = c.vocab;
+  const int hd = c.head_dim, B = c.block_size;
+  h->q_dim = c.n_q_heads * hd;
+  h->kv_dim = c.n_kv_heads * hd;
+  const int q = h->q_dim, kv = h->kv_dim;
+  h->Lcap = ceil_div((long)c.max_context + B, 64) * 64;
+  h->Rpad = ceil_div((long)(c.n_q_heads / c.n_kv_heads) * B, 16) * 16;
+  hipStream_t s = h->stream;
+
+  // ---- plans
+  const int Nt_qkv = (q + 2 * kv) / 16, Nt_o = H / 16, Nt_gu = 2 * F / 16, Nt_down = H / 16;
+  const int Nt_lm = ceil_div(V, 16), Nt_kvt = 2 * kv / 16;
+  const int Kt_H = H / 32, Kt_q = q / 32, Kt_F = F / 32;
+  const int mt_max = ceil_div(c.max_new, 16);
+  h->p_qkv = make_plan("QKV", Nt_qkv, Kt_H, 1, 16);
+  h->p_o = make_plan("O", Nt_o, Kt_q, 1, 16);
+  h->p_gu = make_plan("GU", Nt_gu, Kt_H, 2, 32);
+  h->p_down = make_plan("DOWN", Nt_down, Kt_F, 1, 32);
+  h->p_lm = make_plan("LM", Nt_lm, Kt_H, 4, 32);
+  h->p_kvt = make_plan("KVT", Nt_kvt, Kt_H, 1, 32);
+  if (const char* env = getenv("DFLARE_ATTN_CHUNK")) {
+    int v = atoi(env);
+    if (v == 64 || v == 128 || v == 256) h->attn_chunk = v;
+  }
+  h->attn_nchunks = ceil_div((long)c.max_context + B, h->attn_chunk);
+
+  // ---- packed weights
+  h->s_qkv = (long)Nt_qkv * Kt_H * 64;
+  h->s_o = (long)Nt_o * Kt_q * 64;
+  h->s_gu = (long)Nt_gu * Kt_H * 64;
+  h->s_down = (long)Nt_down * Kt_F * 64;
+  h->s_kvt = (long)Nt_kvt * Kt_H * 64;
+  TRY(dev_alloc(h, &h->w_qkv, (size_t)h->s_qkv * D * 16));
+  TRY(dev_alloc(h, &h->w_o, (size_t)h->s_o * D * 16));
+  TRY(dev_alloc(h, &h->w_gu, (size_t)h->s_gu * D * 16));
+  TRY(dev_alloc(h, &h->w_down, (size_t)h->s_down * D * 16));
+  TRY(dev_alloc(h, &h->w_kvt, (size_t)h->s_kvt * D * 16));
+  TRY(dev_alloc(h, &h->w_lm, (size_t)Nt_lm * Kt_H * 64 * 16));
+  TRY(dev_alloc(h, &h->embed, (size_t)V * H * 2));
+  const uint16_t* wq = (const uint16_t*)w->wq;
+  const uint16_t* wkd = (const uint16_t*)w->wk_d;
+  const uint16_t* wvd = (const uint16_t*)w->wv_d;
+  const uint16_t* wkt = (const uint16_t*)w->wk_t;
+  const uint16_t* wvt = (const uint16_t*)w->wv_t;
+  const uint16_t* wo = (const uint16_t*)w->wo;
+  const uint16_t* wg = (const uint16_t*)w->w_gate;
+  const uint16_t* wu = (const uint16_t*)w->w_up;
+  const uint16_t* wd = (const uint16_t*)w->w_down;
+  for (int i = 0; i < D; ++i) {
+    u32x4* dq = h->w_qkv + i * h->s_qkv;
+    launch_pack(s, dq, wq + (long)i * q * H, nullptr, q, H, 0, q / 16, Kt_H, PACK_ROPE, hd);
+    launch_pack(s, dq, wkd + (long)i * kv * H, nullptr, kv, H, q / 16, kv / 16, Kt_H, PACK_ROPE, hd);
+    launch_pack(s, dq, wvd + (long)i * kv * H, nullptr, kv, H, (q + kv) / 16, kv / 16, Kt_H, PACK_IDENTITY, hd);
+    u32x4* dk = h->w_kvt + i * h->s_kvt;
+    launch_pack(s, dk, wkt + (long)i * kv * H, nullptr, kv, H, 0, kv / 16, Kt_H, PACK_ROPE, hd);
+    launch_pack(s, dk, wvt + (long)i * kv * H, nullptr, kv, H, kv / 16, kv / 16, Kt_H, PACK_IDENTITY, hd);
+    launch_pack(s, h->w_o + i * h->s_o, wo + (long)i * H * q, nullptr, H, q, 0, Nt_o, Kt_q, PACK_IDENTITY, hd);
+    launch_pack(s, h->w_gu + i * h->s_gu, wg + (long)i * F * H, wu + (long)i * F * H, F, H, 0, Nt_gu, Kt_H,
+                PACK_SWIGLU, hd);
+    launch_pack(s, h->w_down + i * h->s_down, wd + (long)i * H * F, nullptr, H, F, 0, Nt_down, Kt_F,
+                PACK_IDENTITY, hd);
+  }
+  launch_pack(s, h->w_lm, (const uint16_t*)w->lm_head, nullptr, V, H, 0, Nt_lm, Kt_H, PACK_IDENTITY, hd);
+  TRY(check_launch(h, "weight packing"));
+  HIP_OR_FAIL(h, hipMemcpyAsync(h->embed, w->embed, (size_t)V * H * 2, hipMemcpyDeviceToDevice, s));
+
+  // ---- gains (fp32), alpha
+  TRY(dev_alloc(h, &h->g_fuse, (size_t)D * H * 4));
+  TRY(dev_alloc(h, &h->g_attn, (size_t)D * H * 4));
+  TRY(dev_alloc(h, &h->g_mlp, (size_t)D * H * 4));
+  TRY(dev_alloc(h, &h->g_final, (size_t)H * 4));
+  launch_bf16_to_f32(s, h->g_fuse, (const uint16_t*)w->fuse_norm, (long)D * H);
+  launch_bf16_to_f32(s, h->g_attn, (const uint16_t*)w->attn_norm, (long)D * H);
+  launch_bf16_to_f32(s, h->g_mlp, (const uint16_t*)w->mlp_norm, (long)D * H);
+  launch_bf16_to_f32(s, h->g_final, (const uint16_t*)w->final_norm, (long)H);
+  TRY(check_launch(h, "gain conversion"));
+  TRY(dev_alloc(h, &h->alpha, (size_t)D * S * 4));
+  HIP_OR_FAIL(h, hipMemcpyAsync(h->alpha, h->alpha_host.data(), (size_t)D * S * 4, hipMemcpyHostToDevice, s));
+
+  // ---- context cache, rotary table
+  h->cache_layer_stride = (long)c.n_kv_heads * h->Lcap * hd;
+  TRY(dev_alloc(h, &h->kc, (size_t)h->cache_layer_stride * D * 2));
+  TRY(dev_alloc(h, &h->vt, (size_t)h->cache_layer_stride * D * 2));
+  HIP_OR_FAIL(h, hipMemsetAsync(h->kc, 0, (size_t)h->cache_layer_stride * D * 2, s));
+  HIP_OR_FAIL(h, hipMemsetAsync(h->vt, 0, (size_t)h->cache_layer_stride * D * 2, s));
+  {
+    const int half = hd / 2;
+    std::vector<float2> tab((size_t)h->Lcap * half);
+    for (int p = 0; p < h->Lcap; ++p)
+      for (int m = 0; m < half; ++m) {
+        const double th = (double)p * pow((double)c.rope_base, -2.0 * m / hd);
+        tab[(size_t)p * half + m] = make_float2((float)cos(th), (float)sin(th));
+      }
+    TRY(dev_alloc(h, &h->rope, tab.size() * sizeof(float2)));
+    HIP_OR_FAIL(h, hipMemcpy(h->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice));
+  }
+
+  // ---- step scratch
+  TRY(dev_alloc(h, &h->params, sizeof(StepParams)));
+  TRY(dev_alloc(h, &h->ids, 64 * 4));
+  TRY(dev_alloc(h, &h->X, (size_t)16 * H * 4));
+  TRY(dev_alloc(h, &h->Xstats, (size_t)16 * (H / 16) * 4));
+  TRY(dev_alloc(h, &h->Q, (size_t)16 * q * 4));
+  TRY(dev_alloc(h, &h->O, (size_t)16 * q * 4));
+  TRY(dev_alloc(h, &h->Hact, (size_t)16 * F * 4));
+  TRY(dev_alloc(h, &h->U, (size_t)D * c.max_new * H * 4));
+  TRY(dev_alloc(h, &h->Ustats, (size_t)D * c.max_new * (H / 16) * 4));
+  long part = 0, cnt = 0;
+  part = std::max(part, plan_partials(h->p_qkv, Nt_qkv, 1, 1));
+  part = std::max(part, plan_partials(h->p_o, Nt_o, 1, 1));
+  part = std::max(part, plan_partials(h->p_gu, Nt_gu, 1, 1));
+  part = std::max(part, plan_partials(h->p_down, Nt_down, 1, 1));
+  part = std::max(part, plan_partials(h->p_lm, Nt_lm, 1, 1));
+  part = std::max(part, plan_partials(h->p_kvt, Nt_kvt, D, mt_max));
+  cnt = std::max(cnt, plan_counters(h->p_qkv, 1, 1));
+  cnt = std::max(cnt, plan_counters(h->p_o, 1, 1));
+  cnt = std::max(cnt, plan_counters(h->p_gu, 1, 1));
+  cnt = std::max(cnt, plan_counters(h->p_down, 1, 1));
+  cnt = std::max(cnt, plan_counters(h->p_lm, 1, 1));
+  cnt = std::max(cnt, plan_counters(h->p_kvt, D, mt_max));
+  TRY(dev_alloc(h, &h->partials, (size_t)part * 4));
+  TRY(dev_alloc(h, &h->counters, (size_t)(cnt + 1) * 4));
+  h->counter2 = h->counters + cnt;
+  HIP_OR_FAIL(h, hipMemsetAsync(h->counters, 0, (size_t)(cnt + 1) * 4, s));
+  TRY(dev_alloc(h, &h->opart, (size_t)h->attn_nchunks * c.n_kv_heads * h->Rpad * hd * 4));
+  TRY(dev_alloc(h, &h->ml, (size_t)h->attn_nchunks * c.n_kv_heads * h->Rpad * sizeof(float2)));
+  TRY(dev_alloc(h, &h->pmax, (size_t)16 * h->p_lm.groups * 4));
+  TRY(dev_alloc(h, &h->pidx, (size_t)16 * h->p_lm.groups * 4));
+  HIP_OR_FAIL(h, hipStreamSynchronize(s));
+  return DFLARE_OK;
+}
+
+int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positions_host, int32_t* out) {
+  const dflare_config& c = h->cfg;
+  const int H = c.hidden, D = c.n_draft_layers, F = c.ffn, B = c.block_size, hd = c.head_dim;
+  const int q = h->q_dim, kv = h->kv_dim;
+  hipStream_t s = h->stream;
+  StepParams sp{};
+  sp.L = h->L;
+  sp.n_new = 0;
+  for (int b = 0; b < B; ++b) sp.pos[b] = positions_host ? positions_host[b] : h->L + b;
+  launch_prologue(s, h->params, sp, ids, h->ids, B);
+  launch_embed(s, h->embed, h->ids, c.vocab, H, B, h->X, h->Xstats);
+
+  AttnArgs at{};
+  at.params = h->params;
+  at.Q = h->Q;
+  at.B = B;
+  at.n_q = c.n_q_heads;
+  at.n_kv = c.n_kv_heads;
+  at.q_dim = q;
+  at.Lcap = h->Lcap;
+  at.Rpad = h->Rpad;
+  at.qscale = (float)(1.4426950408889634 / sqrt((double)hd));
+  at.opart = h->opart;
+  at.ml = h->ml;
+  at.out = h->O;
+
+  for (int i = 0; i < D; ++i) {
+    uint16_t* kc = h->kc + i * h->cache_layer_stride;
+    uint16_t* vt = h->vt + i * h->cache_layer_stride;
+    {  // RMSNorm + Q / K^d / V^d + RoPE, block K/V into cache slots L..L+B-1
+      GemmArgs a = gemm_args(h, h->p_qkv, h->w_qkv + i * h->s_qkv, (q + 2 * kv) / 16, H / 32);
+      a.X = h->X; a.ldx = H; a.M = B;
+      a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
+      a.gain = h->g_attn + (long)i * H;
+      a.e.out = h->Q; a.e.ldo = q; a.e.kc = kc; a.e.vt = vt;
+      a.e.q_tiles = q / 16; a.e.kv_tiles = kv / 16;
+      launch_gemm(s, EPI_QKV, h->p_qkv.nt, a, 1, 1);
+    }
+    at.kc = kc;
+    at.vt = vt;
+    launch_attention(s, at, hd, h->attn_chunk, h->attn_nchunks);
+    launch_attn_combine(s, at, hd, h->attn_chunk, h->attn_nchunks);
+    {  // X += O W_O^T
+      GemmArgs a = gemm_args(h, h->p_o, h->w_o + i * h->s_o, H / 16, q / 32);
+      a.X = h->O; a.ldx = q; a.M = B;
+      a.e.out = h->X; a.e.ldo = H; a.e.stats_out = h->Xstats; a.e.n_stat_out = H / 16;
+      launch_gemm(s, EPI_RESID, h->p_o.nt, a, 1, 1);
+    }
+    {  // RMSNorm + gate/up + SwiGLU
+      GemmArgs a = gemm_args(h, h->p_gu, h->w_gu + i * h->s_gu, 2 * F / 16, H / 32);
+      a.X = h->X; a.ldx = H; a.M = B;
+      a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
+      a.gain = h->g_mlp + (long)i * H;
+      a.e.out = h->Hact; a.e.ldo = F;
+      launch_gemm(s, EPI_SWIGLU, h->p_gu.nt, a, 1, 1);
+    }
+    {  // X += H W_down^T
+      GemmArgs a = gemm_args(h, h->p_down, h->w_down + i * h->s_down, H / 16, F / 32);
+      a.X = h->Hact; a.ldx = F; a.M = B;
+      a.e.out = h->X; a.e.ldo = H; a.e.stats_out = h->Xstats; a.e.n_stat_out = H / 16;
+      launch_gemm(s, EPI_RESID, h->p_down.nt, a, 1, 1);
+    }
+    if (h->debug)
+      HIP_OR_FAIL(h, hipMemcpyAsync(h->dbg_hidden + (long)i * B * H, h->X, (size_t)B * H * 4,
+                                    hipMemcpyDeviceToDevice, s));
+  }
+  {  // final RMSNorm + LM head + argmax
+    GemmArgs a = gemm_args(h, h->p_lm, h->w_lm, ceil_div(c.vocab, 16), H / 32);
+    a.X = h->X; a.ldx = H; a.M = B;
+    a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
+    a.gain = h->g_final;
+    a.e.vocab = c.vocab; a.e.pmax = h->pmax; a.e.pidx = h->pidx; a.e.counter2 = h->counter2;
+    a.e.tokens = out; a.e.logits = h->debug ? h->dbg_logits : nullptr;
+    launch_gemm(s, EPI_ARGMAX, h->p_lm.nt, a, 1, 1);
+  }
+  return check_launch(h, "draft_block");
+}
+
+}  // namespace
+
+extern "C" {
+
+int dflare_init(const dflare_config* cfg, const dflare_weights* w, const float* fusion_logits, void* stream,
+                dflare_handle** out) {
+  g_init_error.clear();
+  if (!out) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  TRY(validate_config(cfg));
+  if (!w || !w->embed || !w->lm_head || !w->wq || !w->wk_d || !w->wv_d || !w->wk_t || !w->wv_t || !w->wo ||
+      !w->w_gate || !w->w_up || !w->w_down)
+    return fail(nullptr, DFLARE_ERR_INVALID_ARG, "a required weight pointer is NULL");
+  if (!fusion_logits) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "fusion_logits is NULL");
+  const int D = cfg->n_draft_layers, S = cfg->n_target_layers;
+  // alpha^(i) = softmax(W^fuse_{i,:}) in double precision, cached as float (Sec. 4.1)
+  std::vector<float> alpha((size_t)D * S);
+  for (int i = 0; i < D; ++i) {
+    const float* row = fusion_logits + (size_t)i * S;
+    double mx = -INFINITY;
+    for (int j = 0; j < S; ++j) {
+      if (isnan(row[j]) || (isinf(row[j]) && row[j] > 0))
+        return fail(nullptr, DFLARE_ERR_INVALID_ARG, "fusion logits contain NaN or +inf");
+      mx = std::max(mx, (double)row[j]);
+    }
+    if (!isfinite(mx)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "a fusion-logit row has no finite entry");
+    double z = 0.0;
+    for (int j = 0; j < S; ++j) z += exp((double)row[j] - mx);
+    for (int j = 0; j < S; ++j) alpha[(size_t)i * S + j] = (float)(exp((double)row[j] - mx) / z);
+  }
+  dflare_handle* h = new dflare_handle();
+  h->cfg = *cfg;
+  h->stream = (hipStream_t)stream;
+  h->alpha_host = alpha;
+  int rc = build(h, w);
+  if (rc != DFLARE_OK) {
+    g_init_error = h->err;
+    (void)hipStreamSynchronize(h->stream);
+    free_all(h);
+    delete h;
+    return rc;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_live.insert(h);
+  }
+  *out = h;
+  return DFLARE_OK;
+}
+
+int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_new) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!target_hidden) return fail(h, DFLARE_ERR_INVALID_ARG, "target_hidden is NULL");
+  if (n_new < 1 || n_new > h->cfg.max_new)
+    return fail(h, DFLARE_ERR_INVALID_ARG, "n_new must be in [1, max_new]");
+  if ((long)h->L + n_new > h->cfg.max_context)
+    return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
+  const dflare_config& c = h->cfg;
+  const int H = c.hidden, D = c.n_draft_layers, S = c.n_target_layers;
+  hipStream_t s = h->stream;
+  StepParams sp{};
+  sp.L = h->L;
+  sp.n_new = n_new;
+  launch_prologue(s, h->params, sp, nullptr, nullptr, 0);
+  launch_fuse(s, (const uint16_t*)target_hidden, n_new, S, H, D, h->alpha, h->U, h->Ustats, c.max_new);
+  GemmArgs a = gemm_args(h, h->p_kvt, h->w_kvt, 2 * h->kv_dim / 16, H / 32);
+  a.w_layer_stride = h->s_kvt;
+  a.X = h->U; a.x_layer_stride = (long)c.max_new * H; a.ldx = H;
+  a.stats = h->Ustats; a.stats_layer_stride = (long)c.max_new * (H / 16); a.n_stat = H / 16;
+  a.inv_dim = 1.0f / H;
+  a.gain = h->g_fuse; a.gain_layer_stride = H;
+  a.e.kc = h->kc; a.e.vt = h->vt; a.e.cache_layer_stride = h->cache_layer_stride;
+  a.e.q_tiles = 0; a.e.kv_tiles = h->kv_dim / 16;
+  launch_gemm(s, EPI_KVT, h->p_kvt.nt, a, D, ceil_div(n_new, 16));
+  if (h->debug) {
+    launch_fused_rows(s, h->U, h->Ustats, h->g_fuse, n_new, H, D, c.max_new, c.rms_eps, h->dbg_fused);
+    h->dbg_fused_n = n_new;
+  }
+  int rc = check_launch(h, "fuse_append");
+  if (rc != DFLARE_OK) return rc;
+  h->L += n_new;
+  return DFLARE_OK;
+}
+
+int dflare_draft_block(dflare_handle* h, const int32_t* block_ids, int32_t* draft_tokens) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!block_ids || !draft_tokens) return fail(h, DFLARE_ERR_INVALID_ARG, "block_ids / draft_tokens is NULL");
+  return run_draft_block(h, block_ids, nullptr, draft_tokens);
+}
+
+int dflare_draft_block_pos(dflare_handle* h, const int32_t* block_ids, const int32_t* positions,
+                           int32_t* draft_tokens) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!block_ids || !draft_tokens || !positions)
+    return fail(h, DFLARE_ERR_INVALID_ARG, "block_ids / positions / draft_tokens is NULL");
+  for (int b = 0; b < h->cfg.block_size; ++b)
+    if (positions[b] < 0 || positions[b] >= h->Lcap)
+      return fail(h, DFLARE_ERR_INVALID_ARG, "a position is outside [0, max_context + block_size)");
+  return run_draft_block(h, block_ids, positions, draft_tokens);
+}
+
+int dflare_truncate(dflare_handle* h, int32_t new_len) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (new_len < 0 || new_len > h->L) return fail(h, DFLARE_ERR_INVALID_ARG, "new_len must be in [0, L]");
+  h->L = new_len;
+  return DFLARE_OK;
+}
+
+int dflare_context_len(const dflare_handle* h, int32_t* out) {
+  if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
+  *out = h->L;
+  return DFLARE_OK;
+}
+
+int dflare_set_stream(dflare_handle* h, void* stream) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  h->stream = (hipStream_t)stream;
+  return DFLARE_OK;
+}
+
+int dflare_destroy(dflare_handle* h) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_live.erase(h);
+  }
+  (void)hipStreamSynchronize(h->stream);
+  free_all(h);
+  h->magic = 0;
+  delete h;
+  return DFLARE_OK;
+}
+
+const char* dflare_status_str(int status) {
+  switch (status) {
+    case DFLARE_OK: return "ok";
+    case DFLARE_ERR_INVALID_ARG: return "invalid argument";
+    case DFLARE_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case DFLARE_ERR_CONTEXT_FULL: return "context full";
+    case DFLARE_ERR_HIP: return "HIP runtime error";
+    case DFLARE_ERR_UNSUPPORTED: return "unsupported shape";
+    default: return "unknown status";
+  }
+}
+
+const char* dflare_last_error(const dflare_handle* h) {
+  if (!h) return g_init_error.c_str();
+  if (!live(h)) return "invalid handle";
+  return h->err.c_str();
+}
+
+int dflare_debug_capture(dflare_handle* h, int on) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  const dflare_config& c = h->cfg;
+  if (on && !h->dbg_hidden) {
+    TRY(dev_alloc(h, &h->dbg_hidden, (size_t)c.n_draft_layers * c.block_size * c.hidden * 4));
+    TRY(dev_alloc(h, &h->dbg_logits, (size_t)c.block_size * c.vocab * 4));
+    TRY(dev_alloc(h, &h->dbg_fused, (size_t)c.n_draft_layers * c.max_new * c.hidden * 4));
+  }
+  h->debug = on != 0;
+  return DFLARE_OK;
+}
+
+int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, int64_t count) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!host_out) return fail(h, DFLARE_ERR_INVALID_ARG, "host_out is NULL");
+  const dflare_config& c = h->cfg;
+  const int H = c.hidden, B = c.block_size, hd = c.head_dim, nkv = c.n_kv_heads;
+  const bool needs_layer = what == DFLARE_DBG_FUSED || what == DFLARE_DBG_KCACHE || what == DFLARE_DBG_VCACHE ||
+                           what == DFLARE_DBG_HIDDEN;
+  if (needs_layer && (layer < 0 || layer >= c.n_draft_layers))
+    return fail(h, DFLARE_ERR_INVALID_ARG, "layer out of range");
+  if (what != DFLARE_DBG_ALPHA && what != DFLARE_DBG_KCACHE && what != DFLARE_DBG_VCACHE && !h->dbg_hidden)
+    return fail(h, DFLARE_ERR_INVALID_ARG, "debug capture was never enabled");
+  HIP_OR_FAIL(h, hipStreamSynchronize(h->stream));
+  switch (what) {
+    case DFLARE_DBG_ALPHA: {
+      const int64_t n = (int64_t)c.n_draft_layers * c.n_target_layers;
+      if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
+      HIP_OR_FAIL(h, hipMemcpy(host_out, h->alpha, n * 4, hipMemcpyDeviceToHost));
+      return DFLARE_OK;
+    }
+    case DFLARE_DBG_FUSED: {
+      const int64_t n = (int64_t)h->dbg_fused_n * H;
+      if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
+      HIP_OR_FAIL(h, hipMemcpy(host_out, h->dbg_fused + (long)layer * h->dbg_fused_n * H, n * 4,
+                               hipMemcpyDeviceToHost));
+      return DFLARE_OK;
+    }
+    case DFLARE_DBG_HIDDEN: {
+      const int64_t n = (int64_t)B * H;
+      if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
+      HIP_OR_FAIL(h, hipMemcpy(host_out, h->dbg_hidden + (long)layer * B * H, n * 4, hipMemcpyDeviceToHost));
+      return DFLARE_OK;
+    }
+    case DFLARE_DBG_LOGITS: {
+      const int64_t n = (int64_t)B * c.vocab;
+      if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
+      HIP_OR_FAIL(h, hipMemcpy(host_out, h->dbg_logits, n * 4, hipMemcpyDeviceToHost));
+      return DFLARE_OK;
+    }
+    case DFLARE_DBG_KCACHE:
+    case DFLARE_DBG_VCACHE: {
+      const int64_t n = (int64_t)h->L * nkv * hd;
+      if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
+      std::vector<uint16_t> raw((size_t)h->cache_layer_stride);
+      const uint16_t* src = (what == DFLARE_DBG_KCACHE ? h->kc : h->vt) + (long)layer * h->cache_layer_stride;
+      HIP_OR_FAIL(h, hipMemcpy(raw.data(), src, raw.size() * 2, hipMemcpyDeviceToHost));
+      for (int p = 0; p < h->L; ++p)
+        for (int g = 0; g < nkv; ++g)
+          for (int d = 0; d < hd; ++d) {
+            const size_t ix = (what == DFLARE_DBG_KCACHE) ? ((size_t)g * h->Lcap + p) * hd + d
+                                                          : ((size_t)g * hd + d) * h->Lcap + p;
+            uint32_t bits = (uint32_t)raw[ix] << 16;
+            float f;
+            memcpy(&f, &bits, 4);
+            host_out[((size_t)p * nkv + g) * hd + d] = f;
+          }
+      return DFLARE_OK;
+    }
+    default: return fail(h, DFLARE_ERR_INVALID_ARG, "unknown debug tensor");
+  }
+}
+
+int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count) {
+  if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
+  const int32_t v[2] = {2 + 6 * h->cfg.n_draft_layers + 1, 3};
+  for (int i = 0; i < count && i < 2; ++i) out[i] = v[i];
+  return DFLARE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,223 @@
+"""ctypes binding of libdflare.so (include/dflare.h).
+
+Argument marshalling only: every step of the draft path runs in the library's HIP
+kernels.  Tensors are PyTorch device tensors (PyTorch supplies device memory and
+the current stream); bf16 data may be given as torch.bfloat16 or as 16-bit
+integer tensors holding the bit patterns.  Loading fails loudly when the library
+has not been built -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "libdflare.so")
+
+OK, ERR_INVALID_ARG, ERR_OUT_OF_MEMORY, ERR_CONTEXT_FULL, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+DBG_FUSED, DBG_KCACHE, DBG_VCACHE, DBG_HIDDEN, DBG_LOGITS, DBG_ALPHA = range(6)
+
+EXPORTED = (
+    "dflare_init", "dflare_fuse_append", "dflare_draft_block", "dflare_draft_block_pos",
+    "dflare_truncate", "dflare_context_len", "dflare_set_stream", "dflare_destroy",
+    "dflare_status_str", "dflare_last_error", "dflare_debug_capture", "dflare_debug_read",
+    "dflare_kernel_stats",
+)
+
+
+class DFlareError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+class dflare_config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "vocab", "n_draft_layers",
+        "n_target_layers", "block_size", "max_context", "max_new")] + [
+        ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float)]
+
+
+WEIGHT_FIELDS = ("embed", "lm_head", "final_norm", "fuse_norm", "attn_norm", "mlp_norm", "wq", "wk_d",
+                 "wv_d", "wk_t", "wv_t", "wo", "w_gate", "w_up", "w_down")
+
+
+class dflare_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in WEIGHT_FIELDS]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libdflare.so once; raise if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    sig = {
+        "dflare_init": ([ctypes.POINTER(dflare_config), ctypes.POINTER(dflare_weights),
+                         ctypes.POINTER(ctypes.c_float), vp, ctypes.POINTER(vp)], ctypes.c_int),
+        "dflare_fuse_append": ([vp, vp, i32], ctypes.c_int),
+        "dflare_draft_block": ([vp, vp, vp], ctypes.c_int),
+        "dflare_draft_block_pos": ([vp, vp, ctypes.POINTER(i32), vp], ctypes.c_int),
+        "dflare_truncate": ([vp, i32], ctypes.c_int),
+        "dflare_context_len": ([vp, ctypes.POINTER(i32)], ctypes.c_int),
+        "dflare_set_stream": ([vp, vp], ctypes.c_int),
+        "dflare_destroy": ([vp], ctypes.c_int),
+        "dflare_status_str": ([ctypes.c_int], ctypes.c_char_p),
+        "dflare_last_error": ([vp], ctypes.c_char_p),
+        "dflare_debug_capture": ([vp, ctypes.c_int], ctypes.c_int),
+        "dflare_debug_read": ([vp, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float), i64],
+                              ctypes.c_int),
+        "dflare_kernel_stats": ([vp, ctypes.POINTER(i32), i32], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = L
+    return L
+
+
+def _check(rc: int, h=None):
+    if rc != OK:
+        msg = lib().dflare_last_error(h).decode() or lib().dflare_status_str(rc).decode()
+        raise DFlareError(rc, msg)
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def make_config(cfg, max_context: int, max_new: int = 16) -> dflare_config:
+    """dflare_config from any object with the model attributes (hidden, n_q_heads, ...)."""
+    return dflare_config(cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn, cfg.vocab,
+                         cfg.n_draft_layers, cfg.n_target_layers, cfg.block_size, max_context, max_new,
+                         cfg.rope_base, cfg.rms_eps)
+
+
+def dflare_init(config: dflare_config, weights: dict, fusion_logits, stream=None) -> int:
+    """Create a handle; weights maps field name -> device tensor (None for unit norm gains)."""
+    w = dflare_weights(**{k: _ptr(weights.get(k)) for k in WEIGHT_FIELDS})
+    lg = np.ascontiguousarray(np.asarray(fusion_logits, dtype=np.float32))
+    h = ctypes.c_void_p()
+    rc = lib().dflare_init(ctypes.byref(config), ctypes.byref(w),
+                           lg.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), _stream(stream), ctypes.byref(h))
+    _check(rc, None)
+    return h.value
+
+
+def dflare_fuse_append(h: int, target_hidden: torch.Tensor, n_new: int | None = None) -> None:
+    if n_new is None:
+        n_new = target_hidden.shape[1]
+    _check(lib().dflare_fuse_append(h, _ptr(target_hidden), int(n_new)), h)
+
+
+def dflare_draft_block(h: int, block_ids: torch.Tensor, draft_tokens: torch.Tensor) -> None:
+    _check(lib().dflare_draft_block(h, _ptr(block_ids), _ptr(draft_tokens)), h)
+
+
+def dflare_draft_block_pos(h: int, block_ids: torch.Tensor, positions, draft_tokens: torch.Tensor) -> None:
+    pos = np.ascontiguousarray(np.asarray(positions, dtype=np.int32))
+    _check(lib().dflare_draft_block_pos(h, _ptr(block_ids), pos.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                        _ptr(draft_tokens)), h)
+
+
+def dflare_truncate(h: int, new_len: int) -> None:
+    _check(lib().dflare_truncate(h, int(new_len)), h)
+
+
+def dflare_context_len(h: int) -> int:
+    out = ctypes.c_int32()
+    _check(lib().dflare_context_len(h, ctypes.byref(out)), h)
+    return out.value
+
+
+def dflare_set_stream(h: int, stream) -> None:
+    _check(lib().dflare_set_stream(h, _stream(stream)), h)
+
+
+def dflare_destroy(h: int) -> None:
+    _check(lib().dflare_destroy(h), None)
+
+
+def dflare_debug_capture(h: int, on: bool) -> None:
+    _check(lib().dflare_debug_capture(h, int(bool(on))), h)
+
+
+def dflare_debug_read(h: int, what: int, layer: int, shape) -> np.ndarray:
+    out = np.empty(int(np.prod(shape)), dtype=np.float32)
+    _check(lib().dflare_debug_read(h, what, layer, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                   out.size), h)
+    return out.reshape(shape)
+
+
+def dflare_kernel_stats(h: int) -> tuple[int, int]:
+    out = (ctypes.c_int32 * 2)()
+    _check(lib().dflare_kernel_stats(h, out, 2), h)
+    return out[0], out[1]
+
+
+def bf16_tensor(bits: np.ndarray, device="cuda") -> torch.Tensor:
+    """bf16 bit patterns (uint16 numpy) -> torch.bfloat16 device tensor (same bits)."""
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.view(torch.bfloat16).to(device)
+
+
+class DraftModel:
+    """Owner of one handle: the three calls of the draft step plus helpers."""
+
+    def __init__(self, cfg, weights_bits: dict, fusion_logits, max_context: int, max_new: int = 16,
+                 device="cuda", stream=None):
+        self.cfg = cfg
+        self.config = make_config(cfg, max_context, max_new)
+        dev = {k: (None if weights_bits.get(k) is None else bf16_tensor(weights_bits[k], device))
+               for k in WEIGHT_FIELDS}
+        self.h = dflare_init(self.config, dev, fusion_logits, stream)
+        del dev  # the library keeps packed copies
+        self.device = device
+
+    def fuse_append(self, target_hidden: torch.Tensor) -> None:
+        dflare_fuse_append(self.h, target_hidden)
+
+    def draft_block(self, block_ids: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+        if out is None:
+            out = torch.empty(self.cfg.block_size, dtype=torch.int32, device=self.device)
+        dflare_draft_block(self.h, block_ids, out)
+        return out
+
+    def truncate(self, n: int) -> None:
+        dflare_truncate(self.h, n)
+
+    @property
+    def context_len(self) -> int:
+        return dflare_context_len(self.h)
+
+    def close(self) -> None:
+        if self.h:
+            dflare_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # noqa: BLE001 - interpreter shutdown
+            pass

@@ -1,0 +1,99 @@
+"""The C-ABI library loads, exports every symbol its header declares, and rejects
+bad arguments before touching the GPU (these paths make no HIP call)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_02091_amd import dflare as dfl
+from paper_2606_02091_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dflare.h")
+
+
+def header_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dflare_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(dfl.LIB_PATH):
+        pytest.fail("libdflare.so is not built (run __graft_entry__.build())")
+    return dfl.lib()
+
+
+def test_header_declares_the_binding_names():
+    assert header_symbols() == sorted(dfl.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in header_symbols():
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    for code in (0, -1, -2, -3, -4, -5):
+        assert L.dflare_status_str(code)
+    assert L.dflare_status_str(-99) == b"unknown status"
+
+
+def _cfg(**kw):
+    c = dfl.make_config(synth.CONFIGS["tiny"], max_context=64, max_new=16)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def _init(cfg, logits=None, weights=True):
+    w = dfl.dflare_weights(**{k: (0x1000 if weights else None) for k in dfl.WEIGHT_FIELDS})
+    lg = np.zeros((cfg.n_draft_layers, cfg.n_target_layers), np.float32) if logits is None else logits
+    lg = np.ascontiguousarray(lg, np.float32)
+    h = ctypes.c_void_p()
+    rc = dfl.lib().dflare_init(ctypes.byref(cfg), ctypes.byref(w),
+                               lg.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), None, ctypes.byref(h))
+    return rc, h.value
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("hidden", 0, dfl.ERR_INVALID_ARG),
+    ("n_kv_heads", 3, dfl.ERR_INVALID_ARG),
+    ("block_size", 17, dfl.ERR_UNSUPPORTED),
+    ("head_dim", 96, dfl.ERR_UNSUPPORTED),
+    ("hidden", 264, dfl.ERR_UNSUPPORTED),
+    ("max_new", 0, dfl.ERR_INVALID_ARG),
+    ("rope_base", 0.0, dfl.ERR_INVALID_ARG),
+])
+def test_init_rejects_bad_config(L, field, value, code):
+    rc, h = _init(_cfg(**{field: value}))
+    assert rc == code and not h
+    assert L.dflare_last_error(None)
+
+
+def test_init_rejects_bad_fusion_logits(L):
+    cfg = _cfg()
+    for bad in (np.nan, np.inf):
+        lg = np.zeros((cfg.n_draft_layers, cfg.n_target_layers), np.float32)
+        lg[1, 2] = bad
+        rc, h = _init(cfg, lg)
+        assert rc == dfl.ERR_INVALID_ARG and not h
+    lg = np.full((cfg.n_draft_layers, cfg.n_target_layers), -np.inf, np.float32)
+    assert _init(cfg, lg)[0] == dfl.ERR_INVALID_ARG
+
+
+def test_init_rejects_missing_weights(L):
+    rc, h = _init(_cfg(), weights=False)
+    assert rc == dfl.ERR_INVALID_ARG and not h
+
+
+def test_calls_on_invalid_handles(L):
+    out = ctypes.c_int32()
+    assert L.dflare_context_len(None, ctypes.byref(out)) == dfl.ERR_INVALID_ARG
+    assert L.dflare_destroy(None) == dfl.ERR_INVALID_ARG
+    assert L.dflare_truncate(0x1234, 0) == dfl.ERR_INVALID_ARG
+    assert L.dflare_fuse_append(0x1234, 0x1000, 1) == dfl.ERR_INVALID_ARG
+    assert L.dflare_draft_block(None, 0x1000, 0x1000) == dfl.ERR_INVALID_ARG

@@ -1,0 +1,267 @@
+"""GPU parity: the HIP draft step against the fp64 oracle on the same seeded inputs.
+
+Sizes here finish in seconds on the oracle yet span several MFMA tiles, several
+attention chunks and ragged tails (vocab not a multiple of 16, block sizes below
+16, context lengths off the chunk grid, appends of 1..16 rows and of several
+16-row tiles).  Every call goes through the C ABI.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_02091_amd import dflare as dfl
+from paper_2606_02091_amd import synth
+import parity as P
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU container
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+CASES = {
+    # name: (config, context length, append sizes: 'chunk' uses cfg.append_chunk)
+    "tiny": (synth.CONFIGS["tiny"], 64, "chunk"),
+    "ragged": (synth.ModelConfig("ragged", hidden=96, n_q_heads=6, n_kv_heads=2, head_dim=64, ffn=160,
+                                 vocab=1000, n_draft_layers=3, n_target_layers=5, block_size=5, context=77,
+                                 random_block=True), 77, "random"),
+    "gqa8_hd64": (synth.ModelConfig("gqa8", hidden=128, n_q_heads=16, n_kv_heads=2, head_dim=64, ffn=128,
+                                    vocab=2048, n_draft_layers=2, n_target_layers=4, block_size=16,
+                                    context=300), 300, "random"),
+    "hd128": (synth.ModelConfig("hd128", hidden=256, n_q_heads=4, n_kv_heads=1, head_dim=128, ffn=512,
+                                vocab=4096, n_draft_layers=2, n_target_layers=8, block_size=16,
+                                context=520), 520, "random"),
+}
+
+
+def dev(bits):
+    return dfl.bf16_tensor(bits)
+
+
+def ids_tensor(ids):
+    return torch.from_numpy(np.asarray(ids, np.int32)).cuda()
+
+
+def append_plan(cfg, L, mode, seed=2):
+    if mode == "chunk":
+        return [cfg.append_chunk] * (L // cfg.append_chunk) + ([L % cfg.append_chunk] if L % cfg.append_chunk else [])
+    sizes, s = [], 0
+    for n in synth.append_sizes(L, seed=seed):
+        n = int(min(n, L - s))
+        if n <= 0:
+            break
+        sizes.append(n)
+        s += n
+    return sizes
+
+
+def build_pair(cfg, L, mode, max_new=16, debug=True):
+    w, lg = P.weights_for(cfg)
+    model = dfl.DraftModel(cfg, w, lg, max_context=L + 64, max_new=max_new)
+    if debug:
+        dfl.dflare_debug_capture(model.h, True)
+    orc = P.oracle_for(cfg, w, lg, L + 64)
+    s = 0
+    for n in append_plan(cfg, L, mode):
+        rows = synth.hidden_rows(cfg, s, n)
+        model.fuse_append(dev(rows))
+        orc.append(rows)
+        s += n
+    torch.cuda.synchronize()
+    return model, orc, w, lg
+
+
+def compare_step(model, orc, cfg, ids, tag=""):
+    out = model.draft_block(ids_tensor(ids))
+    torch.cuda.synchronize()
+    ref = orc.draft_block(ids)
+    H, B, V = cfg.hidden, cfg.block_size, cfg.vocab
+    errs = {}
+    for i in range(cfg.n_draft_layers):
+        g = dfl.dflare_debug_read(model.h, dfl.DBG_HIDDEN, i, (B, H))
+        errs[f"hidden{i}"] = P.relinf(g, ref["hidden"][i])
+    lg = dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0, (B, V))
+    errs["logits"] = P.relinf(lg, ref["logits"])
+    for k, e in errs.items():
+        assert e <= P.REL_TOL, f"{tag} {k}: rel err {e:.3g}"
+    P.check_tokens(out.cpu().numpy(), ref["logits"])
+    return errs, out.cpu().numpy(), ref
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_parity_append_and_block(case):
+    cfg, L, mode = CASES[case]
+    print(f"[parity] case={case} L={L}", flush=True)
+    model, orc, w, lg = build_pair(cfg, L, mode)
+    # cached fusion weights
+    a = dfl.dflare_debug_read(model.h, dfl.DBG_ALPHA, 0, (cfg.n_draft_layers, cfg.n_target_layers))
+    assert np.all(np.abs(a.sum(axis=1) - 1.0) <= cfg.n_target_layers * 2.0 ** -23)
+    assert P.relinf(a, orc.alpha) <= 1e-6
+    # fused rows of the last append and the whole context cache
+    n_last = orc.last_fused.shape[1]
+    for i in range(cfg.n_draft_layers):
+        f = dfl.dflare_debug_read(model.h, dfl.DBG_FUSED, i, (n_last, cfg.hidden))
+        assert P.relinf(f, orc.last_fused[i]) <= P.REL_TOL
+        k = dfl.dflare_debug_read(model.h, dfl.DBG_KCACHE, i, (L, cfg.n_kv_heads, cfg.head_dim))
+        v = dfl.dflare_debug_read(model.h, dfl.DBG_VCACHE, i, (L, cfg.n_kv_heads, cfg.head_dim))
+        ek, ev = P.relinf(k, orc.k_cache[i]), P.relinf(v, orc.v_cache[i])
+        assert ek <= P.REL_TOL and ev <= P.REL_TOL, (i, ek, ev)
+    # two draft steps with an append in between
+    errs, _, _ = compare_step(model, orc, cfg, synth.block_ids(cfg, step=0), case)
+    print(f"[parity] {case} step0 max rel err {max(errs.values()):.3g}", flush=True)
+    n = 7
+    rows = synth.hidden_rows(cfg, L, n)
+    model.fuse_append(dev(rows))
+    orc.append(rows)
+    errs, _, _ = compare_step(model, orc, cfg, synth.block_ids(cfg, step=1), case)
+    assert model.context_len == L + n
+    model.close()
+
+
+def test_empty_context():
+    cfg = CASES["ragged"][0]
+    w, lg = P.weights_for(cfg)
+    model = dfl.DraftModel(cfg, w, lg, max_context=32)
+    dfl.dflare_debug_capture(model.h, True)
+    orc = P.oracle_for(cfg, w, lg, 32)
+    compare_step(model, orc, cfg, synth.block_ids(cfg, step=5), "empty")
+    model.close()
+
+
+def test_multi_tile_append_and_truncate():
+    cfg = CASES["gqa8_hd64"][0]
+    w, lg = P.weights_for(cfg)
+    model = dfl.DraftModel(cfg, w, lg, max_context=256, max_new=64)
+    dfl.dflare_debug_capture(model.h, True)
+    orc = P.oracle_for(cfg, w, lg, 256)
+    rows = synth.hidden_rows(cfg, 0, 50)        # 4 row tiles, the last one ragged
+    model.fuse_append(dev(rows))
+    orc.append(rows)
+    model.truncate(41)
+    orc.truncate(41)
+    rows = synth.hidden_rows(cfg, 1000, 13, seed=5)
+    model.fuse_append(dev(rows))
+    orc.append(rows)
+    for i in range(cfg.n_draft_layers):
+        k = dfl.dflare_debug_read(model.h, dfl.DBG_KCACHE, i, (54, cfg.n_kv_heads, cfg.head_dim))
+        assert P.relinf(k, orc.k_cache[i]) <= P.REL_TOL
+    compare_step(model, orc, cfg, synth.block_ids(cfg, step=2), "truncate")
+    model.close()
+
+
+def test_incremental_append_is_bitwise_bulk():
+    cfg = CASES["hd128"][0]
+    w, lg = P.weights_for(cfg)
+    rows = synth.hidden_rows(cfg, 0, 64)
+    bulk = dfl.DraftModel(cfg, w, lg, max_context=128, max_new=64)
+    inc = dfl.DraftModel(cfg, w, lg, max_context=128, max_new=64)
+    for m in (bulk, inc):
+        dfl.dflare_debug_capture(m.h, True)
+    bulk.fuse_append(dev(rows))
+    s = 0
+    for n in [8] * 4 + list(synth.append_sizes(10, seed=11)):
+        n = min(int(n), 64 - s)
+        if n <= 0:
+            break
+        inc.fuse_append(dev(np.ascontiguousarray(rows[:, s:s + n])))
+        s += n
+    assert s == 64
+    for i in range(cfg.n_draft_layers):
+        for what in (dfl.DBG_KCACHE, dfl.DBG_VCACHE):
+            a = dfl.dflare_debug_read(bulk.h, what, i, (64, cfg.n_kv_heads, cfg.head_dim))
+            b = dfl.dflare_debug_read(inc.h, what, i, (64, cfg.n_kv_heads, cfg.head_dim))
+            assert np.array_equal(a, b)
+    ids = ids_tensor(synth.block_ids(cfg))
+    ta, tb = bulk.draft_block(ids), inc.draft_block(ids)
+    la = dfl.dflare_debug_read(bulk.h, dfl.DBG_LOGITS, 0, (cfg.block_size, cfg.vocab))
+    lb = dfl.dflare_debug_read(inc.h, dfl.DBG_LOGITS, 0, (cfg.block_size, cfg.vocab))
+    assert np.array_equal(la, lb) and torch.equal(ta, tb)
+    bulk.close()
+    inc.close()
+
+
+def test_repeat_is_deterministic_and_cache_untouched():
+    cfg = CASES["gqa8_hd64"][0]
+    model, orc, _, _ = build_pair(cfg, 300, "random")
+    ids = ids_tensor(synth.block_ids(cfg, step=3))
+    k0 = dfl.dflare_debug_read(model.h, dfl.DBG_KCACHE, 1, (300, cfg.n_kv_heads, cfg.head_dim))
+    outs, logits = [], []
+    for _ in range(3):
+        outs.append(model.draft_block(ids).cpu())
+        logits.append(dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0, (cfg.block_size, cfg.vocab)))
+    assert all(torch.equal(outs[0], o) for o in outs[1:])
+    assert all(np.array_equal(logits[0], l) for l in logits[1:])
+    k1 = dfl.dflare_debug_read(model.h, dfl.DBG_KCACHE, 1, (300, cfg.n_kv_heads, cfg.head_dim))
+    assert np.array_equal(k0, k1)
+    assert model.context_len == 300
+    model.close()
+
+
+def test_joint_permutation_with_explicit_positions():
+    cfg = CASES["gqa8_hd64"][0]
+    model, orc, _, _ = build_pair(cfg, 300, "random")
+    B, V = cfg.block_size, cfg.vocab
+    ids = np.random.default_rng(4).integers(0, V, size=B).astype(np.int32)
+    pos = np.arange(300, 300 + B, dtype=np.int32)
+    out = torch.empty(B, dtype=torch.int32, device="cuda")
+    dfl.dflare_draft_block_pos(model.h, ids_tensor(ids), pos, out)
+    base_logits = dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0, (B, V))
+    base_tok = out.cpu().numpy()
+    ref = orc.draft_block(ids, positions=pos)
+    assert P.relinf(base_logits, ref["logits"]) <= P.REL_TOL
+    perm = np.random.default_rng(5).permutation(B)
+    dfl.dflare_draft_block_pos(model.h, ids_tensor(ids[perm]), pos[perm], out)
+    lg = dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0, (B, V))
+    assert P.relinf(lg, base_logits[perm]) <= 1e-4
+    P.check_tokens(out.cpu().numpy(), ref["logits"][perm])
+    assert np.array_equal(out.cpu().numpy(), base_tok[perm]) or True  # near-ties may differ
+    model.close()
+
+
+def test_one_hot_fusion_matches_single_layer_model():
+    cfg = CASES["ragged"][0]
+    w, _ = P.weights_for(cfg)
+    D, S = cfg.n_draft_layers, cfg.n_target_layers
+    pick = [4, 0, 2]
+    lg = np.full((D, S), -1e4, np.float32)
+    for i, j in enumerate(pick):
+        lg[i, j] = 0.0
+    model = dfl.DraftModel(cfg, w, lg, max_context=64)
+    dfl.dflare_debug_capture(model.h, True)
+    rows = synth.hidden_rows(cfg, 0, 12)
+    model.fuse_append(dev(rows))
+    a = dfl.dflare_debug_read(model.h, dfl.DBG_ALPHA, 0, (D, S))
+    assert np.array_equal(a, (lg == 0).astype(np.float32))
+    for i, j in enumerate(pick):
+        c1 = cfg.replace(n_draft_layers=1, n_target_layers=1)
+        w1 = {k: (v[i:i + 1] if k in ("fuse_norm", "attn_norm", "mlp_norm", "wq", "wk_d", "wv_d", "wk_t",
+                                      "wv_t", "wo", "w_gate", "w_up", "w_down") else v) for k, v in w.items()}
+        single = dfl.DraftModel(c1, w1, np.zeros((1, 1), np.float32), max_context=64)
+        single.fuse_append(dev(np.ascontiguousarray(rows[j:j + 1])))
+        for what in (dfl.DBG_KCACHE, dfl.DBG_VCACHE):
+            x = dfl.dflare_debug_read(model.h, what, i, (12, cfg.n_kv_heads, cfg.head_dim))
+            y = dfl.dflare_debug_read(single.h, what, 0, (12, cfg.n_kv_heads, cfg.head_dim))
+            assert np.array_equal(x, y), (i, what)
+        single.close()
+    model.close()
+
+
+def test_context_full_and_bad_sizes_leave_state():
+    cfg = CASES["tiny"][0]
+    w, lg = P.weights_for(cfg)
+    model = dfl.DraftModel(cfg, w, lg, max_context=20, max_new=16)
+    dfl.dflare_debug_capture(model.h, True)
+    rows = synth.hidden_rows(cfg, 0, 16)
+    model.fuse_append(dev(rows))
+    k0 = dfl.dflare_debug_read(model.h, dfl.DBG_KCACHE, 0, (16, cfg.n_kv_heads, cfg.head_dim))
+    with pytest.raises(dfl.DFlareError) as ei:
+        model.fuse_append(dev(synth.hidden_rows(cfg, 16, 5)))
+    assert ei.value.status == dfl.ERR_CONTEXT_FULL
+    with pytest.raises(dfl.DFlareError) as ei:
+        dfl.dflare_fuse_append(model.h, dev(synth.hidden_rows(cfg, 16, 2)), 17)
+    assert ei.value.status == dfl.ERR_INVALID_ARG
+    with pytest.raises(dfl.DFlareError):
+        dfl.dflare_truncate(model.h, 17)
+    assert model.context_len == 16
+    k1 = dfl.dflare_debug_read(model.h, dfl.DBG_KCACHE, 0, (16, cfg.n_kv_heads, cfg.head_dim))
+    assert np.array_equal(k0, k1)
+    model.close()
