@@ -1,0 +1,213 @@
+#!/usr/bin/env python3
+"""Benchmark of the DFlare draft step on one MI355X.
+
+One step = dflare_fuse_append(n_new ~ U{1..16} accepted target rows) followed by
+dflare_draft_block(B = 16) at a fixed context length L: before each step the
+context is truncated by n_new so that every step sees exactly L context rows.
+Default workload: Qwen3-8B-shaped draft (H 4096, 32 q / 8 kv heads x 128,
+SwiGLU 12288, vocab 151936, D = 8 draft layers fusing S = 36 target layers),
+L = 4096, batch 1.  Weights and inputs are seeded synthetic data (no trained
+weights exist here); all inputs are resident in HBM before the timed region.
+
+Prints one JSON line.  Per-kernel durations come from hipEvents placed by the
+library around the launches of one kernel kind at a time (a separate pass after
+the timed region, so the headline number carries no event overhead).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "draft blocks/sec (B=16, Qwen3-8B shape, batch 1) + % HBM roofline"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="qwen3_8b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-context", type=int, default=256,
+                    help="context rows of the oracle's timed sample")
+    ap.add_argument("--profile-steps", type=int, default=20)
+    return ap.parse_args()
+
+
+def kernel_bytes(cfg, L, n_mean):
+    """Algorithmic HBM bytes per launch of each kernel kind (bf16 storage)."""
+    H, F, V, D, S = cfg.hidden, cfg.ffn, cfg.vocab, cfg.n_draft_layers, cfg.n_target_layers
+    q, kv = cfg.q_dim, cfg.kv_dim
+    return {
+        "qkv": (q + 2 * kv) * H * 2,          # W_Q, W_K^d, W_V^d of one layer
+        "attn": 2 * L * kv * 2,               # context K and V of one layer
+        "o": H * q * 2,
+        "gate_up": 2 * F * H * 2,
+        "down": H * F * 2,
+        "lm_head": V * H * 2,
+        "fuse": S * n_mean * H * 2,           # the target rows, read once
+        "kv_t": D * 2 * kv * H * 2,           # W_K^t, W_V^t of all layers (one launch)
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs the draft step on one GPU only; "
+                                   "bench.py --gpus N with N > 1 is not supported"}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_02091_amd import dflare as dfl
+    from paper_2606_02091_amd import synth
+
+    cfg = synth.CONFIGS[args.config]
+    L, B, S, H = cfg.context, cfg.block_size, cfg.n_target_layers, cfg.hidden
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    w = synth.make_weights(cfg)
+    fusion_logits = w.pop("fusion_logits")
+    print(f"[bench] weights generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    model = dfl.DraftModel(cfg, w, fusion_logits, max_context=L + 16, max_new=512)
+    h = model.h
+    chunk = 512
+    for s in range(0, L, chunk):
+        n = min(chunk, L - s)
+        model.fuse_append(dfl.bf16_tensor(synth.hidden_rows(cfg, s, n)))
+    torch.cuda.synchronize()
+    print(f"[bench] context prefilled to {model.context_len} rows", file=sys.stderr, flush=True)
+
+    total = args.warmup + args.steps
+    sizes = [int(x) for x in synth.append_sizes(total)]
+    hid = {n: dfl.bf16_tensor(synth.hidden_rows(cfg, L - n, n)) for n in range(1, 17)}
+    ids = torch.from_numpy(synth.block_ids(cfg)).cuda()
+    out = torch.empty(B, dtype=torch.int32, device="cuda")
+
+    def step(k):
+        n = sizes[k % len(sizes)]
+        dfl.dflare_truncate(h, L - n)
+        dfl.dflare_fuse_append(h, hid[n], n)
+        dfl.dflare_draft_block(h, ids, out)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for k in range(args.warmup, total):
+        step(k)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    n_mean = float(np.mean(sizes[args.warmup:total]))
+    print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # draft_block alone
+    for _ in range(5):
+        dfl.dflare_draft_block(h, ids, out)
+    e0.record(stream)
+    for _ in range(args.steps):
+        dfl.dflare_draft_block(h, ids, out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    block_ms = e0.elapsed_time(e1) / args.steps
+
+    # per-kernel durations (hipEvents in the library, one kind per pass)
+    kb = kernel_bytes(cfg, L, n_mean)
+    kinds = {"qkv": dfl.K_QKV, "attn": dfl.K_ATTN, "o": dfl.K_O, "gate_up": dfl.K_GATE_UP,
+             "down": dfl.K_DOWN, "lm_head": dfl.K_LM_HEAD, "fuse": dfl.K_FUSE, "kv_t": dfl.K_KV_T}
+    kern = {}
+    for name, kind in kinds.items():
+        dfl.dflare_profile_begin(h, kind)
+        for k in range(args.profile_steps):
+            step(k)
+        tot, launches = dfl.dflare_profile_end(h)
+        avg_us = 1000.0 * tot / max(launches, 1)
+        per_step_us = 1000.0 * tot / args.profile_steps
+        gbs = kb[name] / (avg_us * 1e-6) / 1e9 if avg_us > 0 else 0.0
+        kern[name] = {"avg_us": round(avg_us, 3), "launches_per_step": launches / args.profile_steps,
+                      "us_per_step": round(per_step_us, 2), "bytes_per_launch": int(kb[name]),
+                      "achieved_GBs": round(gbs, 1)}
+    dom = max(kern, key=lambda k: kern[k]["us_per_step"])
+    d = kern[dom]
+
+    step_bytes = cfg.block_bytes(L) + cfg.append_bytes(n_mean)
+    step_gbs = step_bytes / (ms * 1e-3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": round(1000.0 / ms, 2),
+        "unit": "blocks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-shaped draft step: H={H}, {cfg.n_q_heads}q/{cfg.n_kv_heads}kv x "
+                               f"{cfg.head_dim}, F={cfg.ffn}, V={cfg.vocab}, D={cfg.n_draft_layers}, S={S}, "
+                               f"L={L}, B={B}, batch 1, n_new~U{{1..16}}",
+                   "global_batch": 1, "seq_len": L, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": round(d["achieved_GBs"], 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(d["achieved_GBs"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": dom, "bytes_per_launch": d["bytes_per_launch"], "avg_us": d["avg_us"]},
+        "step_roofline": {"bytes_per_step": int(step_bytes), "achieved_GBs": round(step_gbs, 1),
+                          "frac": round(step_gbs / HBM_PEAK_GBS, 4)},
+        "draft_block_ms": round(block_ms, 5),
+        "kernels": kern,
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context)
+    print(json.dumps(result), flush=True)
+    model.close()
+
+
+def cpu_baseline(cfg, w, fusion_logits, ctx):
+    """The fp64 oracle, as it stands, timed on this host for one draft step."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import dflare_oracle as orc
+    from paper_2606_02091_amd import synth
+
+    o = orc.DraftOracle(cfg, w, fusion_logits, max_context=ctx + 64)
+    o.append(synth.hidden_rows(cfg, 0, ctx))
+    rows = synth.hidden_rows(cfg, ctx, 8)
+    ids = synth.block_ids(cfg)
+    t = time.perf_counter()
+    o.append(rows)
+    o.draft_block(ids, keep_logits=False)
+    sec = time.perf_counter() - t
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": round(1.0 / sec, 5), "unit": "blocks/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"1 step (fuse_append of 8 rows + draft_block) of the same model at context {ctx}; "
+                      f"{sec:.2f} s on {cpu} ({platform.machine()})",
+            "seconds": round(sec, 3)}
+
+
+if __name__ == "__main__":
+    main()

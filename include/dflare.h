@@ -178,13 +178,30 @@ int dflare_debug_capture(dflare_handle* h, int on);
 int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, int64_t count);
 
 /*
- * dflare_kernel_stats -- launch configuration of the dominant kernels, for
- * measurement: writes up to `count` int32 values
+ * dflare_kernel_stats -- launch counts, for measurement: writes up to `count`
+ * int32 values
  *   [0] number of kernels one draft_block enqueues
  *   [1] number of kernels one fuse_append enqueues
- * Returns DFLARE_OK.
  */
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count);
+
+/*
+ * Kernel timing (measurement).  dflare_profile_begin(h, kind) brackets every later
+ * launch of one kernel kind with a pair of hipEvents on the handle's stream, up to
+ * 8192 launches; kind = 0 stops.  dflare_profile_end synchronises the stream and
+ * returns the summed event-measured duration (ms) and the number of launches
+ * timed since the last begin, then stops.  Kinds:
+ */
+enum { DFLARE_K_QKV = 1,       /* RMSNorm + Q/K^d/V^d projection + RoPE           */
+       DFLARE_K_ATTN = 2,      /* block attention (split over keys) + combine      */
+       DFLARE_K_O = 3,         /* output projection + residual                     */
+       DFLARE_K_GATE_UP = 4,   /* RMSNorm + gate/up projection + SwiGLU            */
+       DFLARE_K_DOWN = 5,      /* down projection + residual                       */
+       DFLARE_K_LM_HEAD = 6,   /* final RMSNorm + LM head + argmax                 */
+       DFLARE_K_FUSE = 7,      /* layer fusion (Eq. 3)                             */
+       DFLARE_K_KV_T = 8 };    /* context K/V projection + RoPE + append (Eq. 4)   */
+int dflare_profile_begin(dflare_handle* h, int kind);
+int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches);
 
 #ifdef __cplusplus
 }

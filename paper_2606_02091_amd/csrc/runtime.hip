@@ -78,6 +78,10 @@ struct dflare_handle {
   bool debug = false;
   float *dbg_hidden = nullptr, *dbg_logits = nullptr, *dbg_fused = nullptr;
   int dbg_fused_n = 0;
+  // kernel timing
+  int prof_kind = 0;
+  std::vector<hipEvent_t> prof_ev;  // pairs
+  int prof_n = 0;
   std::vector<void*> allocs;
   std::string err;
 };
@@ -114,6 +118,26 @@ int dev_alloc(dflare_handle* h, T** p, size_t bytes) {
 void free_all(dflare_handle* h) {
   for (void* p : h->allocs) (void)hipFree(p);
   h->allocs.clear();
+  for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
+  h->prof_ev.clear();
+}
+
+const int kProfMax = 8192;
+
+// bracket one launch of kernel kind `k` with events when it is the profiled kind
+void prof_mark(dflare_handle* h, int k, bool start) {
+  if (h->prof_kind != k || h->prof_n >= kProfMax) return;
+  const size_t ix = 2 * (size_t)h->prof_n + (start ? 0 : 1);
+  while (h->prof_ev.size() <= ix) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) {
+      h->prof_kind = 0;
+      return;
+    }
+    h->prof_ev.push_back(e);
+  }
+  (void)hipEventRecord(h->prof_ev[ix], h->stream);
+  if (!start) ++h->prof_n;
 }
 
 bool live(const dflare_handle* h) {
@@ -371,17 +395,23 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
       a.gain = h->g_attn + (long)i * H;
       a.e.out = h->Q; a.e.ldo = q; a.e.kc = kc; a.e.vt = vt;
       a.e.q_tiles = q / 16; a.e.kv_tiles = kv / 16;
+      prof_mark(h, DFLARE_K_QKV, true);
       launch_gemm(s, EPI_QKV, h->p_qkv.nt, a, 1, 1);
+      prof_mark(h, DFLARE_K_QKV, false);
     }
     at.kc = kc;
     at.vt = vt;
+    prof_mark(h, DFLARE_K_ATTN, true);
     launch_attention(s, at, hd, h->attn_chunk, h->attn_nchunks);
     launch_attn_combine(s, at, hd, h->attn_chunk, h->attn_nchunks);
+    prof_mark(h, DFLARE_K_ATTN, false);
     {  // X += O W_O^T
       GemmArgs a = gemm_args(h, h->p_o, h->w_o + i * h->s_o, H / 16, q / 32);
       a.X = h->O; a.ldx = q; a.M = B;
       a.e.out = h->X; a.e.ldo = H; a.e.stats_out = h->Xstats; a.e.n_stat_out = H / 16;
+      prof_mark(h, DFLARE_K_O, true);
       launch_gemm(s, EPI_RESID, h->p_o.nt, a, 1, 1);
+      prof_mark(h, DFLARE_K_O, false);
     }
     {  // RMSNorm + gate/up + SwiGLU
       GemmArgs a = gemm_args(h, h->p_gu, h->w_gu + i * h->s_gu, 2 * F / 16, H / 32);
@@ -389,13 +419,17 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
       a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
       a.gain = h->g_mlp + (long)i * H;
       a.e.out = h->Hact; a.e.ldo = F;
+      prof_mark(h, DFLARE_K_GATE_UP, true);
       launch_gemm(s, EPI_SWIGLU, h->p_gu.nt, a, 1, 1);
+      prof_mark(h, DFLARE_K_GATE_UP, false);
     }
     {  // X += H W_down^T
       GemmArgs a = gemm_args(h, h->p_down, h->w_down + i * h->s_down, H / 16, F / 32);
       a.X = h->Hact; a.ldx = F; a.M = B;
       a.e.out = h->X; a.e.ldo = H; a.e.stats_out = h->Xstats; a.e.n_stat_out = H / 16;
+      prof_mark(h, DFLARE_K_DOWN, true);
       launch_gemm(s, EPI_RESID, h->p_down.nt, a, 1, 1);
+      prof_mark(h, DFLARE_K_DOWN, false);
     }
     if (h->debug)
       HIP_OR_FAIL(h, hipMemcpyAsync(h->dbg_hidden + (long)i * B * H, h->X, (size_t)B * H * 4,
@@ -408,7 +442,9 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
     a.gain = h->g_final;
     a.e.vocab = c.vocab; a.e.pmax = h->pmax; a.e.pidx = h->pidx; a.e.counter2 = h->counter2;
     a.e.tokens = out; a.e.logits = h->debug ? h->dbg_logits : nullptr;
+    prof_mark(h, DFLARE_K_LM_HEAD, true);
     launch_gemm(s, EPI_ARGMAX, h->p_lm.nt, a, 1, 1);
+    prof_mark(h, DFLARE_K_LM_HEAD, false);
   }
   return check_launch(h, "draft_block");
 }
@@ -477,7 +513,9 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   sp.L = h->L;
   sp.n_new = n_new;
   launch_prologue(s, h->params, sp, nullptr, nullptr, 0);
+  prof_mark(h, DFLARE_K_FUSE, true);
   launch_fuse(s, (const uint16_t*)target_hidden, n_new, S, H, D, h->alpha, h->U, h->Ustats, c.max_new);
+  prof_mark(h, DFLARE_K_FUSE, false);
   GemmArgs a = gemm_args(h, h->p_kvt, h->w_kvt, 2 * h->kv_dim / 16, H / 32);
   a.w_layer_stride = h->s_kvt;
   a.X = h->U; a.x_layer_stride = (long)c.max_new * H; a.ldx = H;
@@ -486,7 +524,9 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   a.gain = h->g_fuse; a.gain_layer_stride = H;
   a.e.kc = h->kc; a.e.vt = h->vt; a.e.cache_layer_stride = h->cache_layer_stride;
   a.e.q_tiles = 0; a.e.kv_tiles = h->kv_dim / 16;
+  prof_mark(h, DFLARE_K_KV_T, true);
   launch_gemm(s, EPI_KVT, h->p_kvt.nt, a, D, ceil_div(n_new, 16));
+  prof_mark(h, DFLARE_K_KV_T, false);
   if (h->debug) {
     launch_fused_rows(s, h->U, h->Ustats, h->g_fuse, n_new, H, D, c.max_new, c.rms_eps, h->dbg_fused);
     h->dbg_fused_n = n_new;
@@ -635,6 +675,31 @@ int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, in
     }
     default: return fail(h, DFLARE_ERR_INVALID_ARG, "unknown debug tensor");
   }
+}
+
+int dflare_profile_begin(dflare_handle* h, int kind) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (kind < 0 || kind > DFLARE_K_KV_T) return fail(h, DFLARE_ERR_INVALID_ARG, "unknown kernel kind");
+  h->prof_kind = kind;
+  h->prof_n = 0;
+  return DFLARE_OK;
+}
+
+int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!total_ms || !launches) return fail(h, DFLARE_ERR_INVALID_ARG, "NULL output");
+  HIP_OR_FAIL(h, hipStreamSynchronize(h->stream));
+  double t = 0.0;
+  for (int i = 0; i < h->prof_n; ++i) {
+    float ms = 0.f;
+    HIP_OR_FAIL(h, hipEventElapsedTime(&ms, h->prof_ev[2 * i], h->prof_ev[2 * i + 1]));
+    t += ms;
+  }
+  *total_ms = t;
+  *launches = h->prof_n;
+  h->prof_kind = 0;
+  h->prof_n = 0;
+  return DFLARE_OK;
 }
 
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count) {

@@ -23,8 +23,9 @@ EXPORTED = (
     "dflare_init", "dflare_fuse_append", "dflare_draft_block", "dflare_draft_block_pos",
     "dflare_truncate", "dflare_context_len", "dflare_set_stream", "dflare_destroy",
     "dflare_status_str", "dflare_last_error", "dflare_debug_capture", "dflare_debug_read",
-    "dflare_kernel_stats",
+    "dflare_kernel_stats", "dflare_profile_begin", "dflare_profile_end",
 )
+K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T = range(1, 9)
 
 
 class DFlareError(RuntimeError):
@@ -76,6 +77,8 @@ def lib() -> ctypes.CDLL:
         "dflare_debug_read": ([vp, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float), i64],
                               ctypes.c_int),
         "dflare_kernel_stats": ([vp, ctypes.POINTER(i32), i32], ctypes.c_int),
+        "dflare_profile_begin": ([vp, ctypes.c_int], ctypes.c_int),
+        "dflare_profile_end": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -174,6 +177,17 @@ def dflare_kernel_stats(h: int) -> tuple[int, int]:
     out = (ctypes.c_int32 * 2)()
     _check(lib().dflare_kernel_stats(h, out, 2), h)
     return out[0], out[1]
+
+
+def dflare_profile_begin(h: int, kind: int) -> None:
+    _check(lib().dflare_profile_begin(h, int(kind)), h)
+
+
+def dflare_profile_end(h: int) -> tuple[float, int]:
+    """(summed kernel milliseconds, launches) since dflare_profile_begin."""
+    ms, n = ctypes.c_double(), ctypes.c_int32()
+    _check(lib().dflare_profile_end(h, ctypes.byref(ms), ctypes.byref(n)), h)
+    return ms.value, n.value
 
 
 def bf16_tensor(bits: np.ndarray, device="cuda") -> torch.Tensor:

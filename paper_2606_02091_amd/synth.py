@@ -95,12 +95,20 @@ WEIGHT_KINDS = (
 )
 
 
-def round_bf16(x: np.ndarray) -> np.ndarray:
-    """float32 -> bfloat16 bit patterns (uint16), round to nearest even."""
+def round_bf16(x: np.ndarray, out: np.ndarray | None = None) -> np.ndarray:
+    """float32 -> bfloat16 bit patterns (uint16), round to nearest even.
+
+    NaN maps to the quiet NaN 0x7FC0.  `out` (uint16, same size) may be given.
+    """
     x = np.ascontiguousarray(x, dtype=np.float32)
     u = x.view(np.uint32)
-    bias = ((u >> 16) & 1) + np.uint32(0x7FFF)
-    out = ((u + bias) >> 16).astype(np.uint16)
+    r = (u >> np.uint32(16)) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= np.uint32(16)
+    if out is None:
+        out = np.empty(x.shape, np.uint16)
+    np.copyto(out, r, casting="unsafe")
     nan = np.isnan(x)
     if nan.any():
         out[nan] = 0x7FC0
@@ -124,19 +132,17 @@ def _shape(cfg: ModelConfig, kind: str) -> tuple[int, ...]:
     }[kind]
 
 
-def _draw(cfg: ModelConfig, kind: str, seed: int) -> np.ndarray:
-    idx = WEIGHT_KINDS.index(kind)
-    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, idx])))
-    shape = _shape(cfg, kind)
-    z = rng.standard_normal(size=shape, dtype=np.float32)
-    if kind == "fusion_logits":
-        return z.astype(np.float32)          # host fp32 logits, N(0, 1)
+_CHUNK = 1 << 22  # values per independently seeded chunk
+
+
+def _draw_chunk(kind: str, idx: int, seed: int, c: int, flat_out: np.ndarray) -> None:
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, idx, c])))
+    n = flat_out.size
+    z = rng.standard_normal(size=n, dtype=np.float32)
+    z *= np.float32(0.02)
     if kind.endswith("norm"):
-        z *= np.float32(0.02)
         z += np.float32(1.0)                 # gains 1 + N(0, 0.02)
-    else:
-        z *= np.float32(0.02)                # N(0, 0.02)
-    return round_bf16(z)
+    round_bf16(z, out=flat_out)
 
 
 def make_weights(cfg: ModelConfig, seed: int = 0, kinds=WEIGHT_KINDS,
@@ -144,11 +150,31 @@ def make_weights(cfg: ModelConfig, seed: int = 0, kinds=WEIGHT_KINDS,
     """All draft weights as bf16 bit arrays (uint16); fusion logits as float32.
 
     Linear weights use the [out, in] row-major convention, stacked over the D
-    draft layers: y = x @ W.T.
+    draft layers: y = x @ W.T.  Each tensor is drawn in chunks of 2^22 values,
+    chunk c of tensor kind k seeded by (seed, k, c), so the result does not
+    depend on the thread count.
     """
-    with ThreadPoolExecutor(max_workers=threads) as ex:
-        arrs = list(ex.map(lambda k: _draw(cfg, k, seed), kinds))
-    return dict(zip(kinds, arrs))
+    out: dict[str, np.ndarray] = {}
+    jobs = []
+    for kind in kinds:
+        idx = WEIGHT_KINDS.index(kind)
+        shape = _shape(cfg, kind)
+        if kind == "fusion_logits":           # host fp32 logits, N(0, 1)
+            rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, idx])))
+            out[kind] = rng.standard_normal(size=shape, dtype=np.float32)
+            continue
+        arr = np.empty(shape, np.uint16)
+        flat = arr.reshape(-1)
+        for c, lo in enumerate(range(0, flat.size, _CHUNK)):
+            jobs.append((kind, idx, c, flat[lo:lo + _CHUNK]))
+        out[kind] = arr
+    if threads <= 1:
+        for kind, idx, c, view in jobs:
+            _draw_chunk(kind, idx, seed, c, view)
+    else:
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(lambda j: _draw_chunk(j[0], j[1], seed, j[2], j[3]), jobs))
+    return {k: out[k] for k in kinds}
 
 
 _ROW_BLOCK = 64
