@@ -26,7 +26,7 @@ enum Epi {
   EPI_SWIGLU = 1,  // out[row, f] = silu(gate_f) * up_f
   EPI_QKV = 2,     // block Q (RoPE, fp32), block K (RoPE) and V into cache slots L + row
   EPI_KVT = 3,     // context K (RoPE) and V of appended rows into cache slots L + row
-  EPI_ARGMAX = 4   // vocabulary-parallel argmax, final combine by the last block
+  EPI_ARGMAX = 4   // vocabulary-parallel argmax: best (logit, id) of the block per row
 };
 
 struct StepParams {  // device-resident, rewritten by a prologue kernel each call
@@ -52,30 +52,29 @@ struct EpiArgs {
   int B;                  // block rows (QKV / ARGMAX)
   // ARGMAX
   int vocab;
-  float* pmax;            // [16, n_groups]
-  int* pidx;
-  unsigned* counter2;
-  int* tokens;            // [B]
+  float* pmax;            // [16, blocks]: best logit of each block per row
+  int* pidx;              // [16, blocks]: its token id
   float* logits;          // optional debug [B, vocab]
+  // RESID / SWIGLU: A fragments of the next GEMM's input (RESID: x * next_gain)
+  uint32_t* na_hi;
+  uint32_t* na_lo;
+  int na_Kt;
+  const float* next_gain;
 };
 
 struct GemmArgs {
   const u32x4* W;          // packed tiles of layer 0
   long w_layer_stride;     // in u32x4 units (layer = blockIdx.y)
   int Nt, Kt;              // output tiles (16 wide), k tiles (32 deep)
-  int kt_per_split, splits;
-  const float* X;          // activations [M, ldx] fp32 of layer 0
-  long x_layer_stride;
-  int ldx;
+  const u32x4* zero;       // one zero tile (64 x 16 bytes)
+  const u32x4* Ahi;        // activation A fragments (hi / lo planes) of layer 0, [m-tiles, Kt, 64]
+  const u32x4* Alo;
+  long a_layer_stride;     // in u32x4 units
   int M;                   // rows (ignored for KVT, which reads n_new)
-  const float* stats;      // optional: per-row partial sums of squares [M, n_stat]
-  long stats_layer_stride;
+  const float* stats;      // optional: per-row partial sums of squares [M, n_stat]; when set the
+  long stats_layer_stride; // output rows are scaled by 1/sqrt(sum * inv_dim + eps) (RMSNorm)
   int n_stat;
   float inv_dim, eps;
-  const float* gain;       // optional fp32 gain [K]
-  long gain_layer_stride;
-  float* partials;         // split-K partial tiles
-  unsigned* counters;      // arrival counters, zero between launches
   EpiArgs e;
 };
 
@@ -88,7 +87,9 @@ struct AttnArgs {
   float qscale;            // log2(e) / sqrt(hd)
   float* opart;            // [chunks, n_kv, Rpad, hd]
   float2* ml;              // [chunks, n_kv, Rpad]
-  float* out;              // combine: O [B, q_dim]
+  u32x4* oa_hi;            // combine: A fragments of O [B, q_dim] for the output projection
+  u32x4* oa_lo;
+  int oa_Kt;
 };
 
 // ---- launchers (kernels.hip) ----
@@ -98,14 +99,15 @@ void launch_bf16_to_f32(hipStream_t s, float* dst, const uint16_t* src, long n);
 void launch_prologue(hipStream_t s, StepParams* p, const StepParams& host, const int* ids_src,
                      int* ids_dst, int B);
 void launch_embed(hipStream_t s, const uint16_t* embed, const int* ids, int vocab, int H, int B,
-                  float* X, float* stats);
+                  float* X, float* stats, const float* gain, u32x4* a_hi, u32x4* a_lo);
 void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
-                 float* U, float* ustats, int n_max);
-void launch_fused_rows(hipStream_t s, const float* U, const float* ustats, const float* gain, int n,
-                       int H, int D, int n_max, float eps, float* out);
-void launch_gemm(hipStream_t s, int epi, int nt_per_wave, const GemmArgs& a, int layers, int mtiles);
+                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max);
+void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n,
+                       int H, int D, int n_max, int mt_max, float eps, float* out);
+void launch_gemm(hipStream_t s, int epi, int nt_per_block, int waves, const GemmArgs& a, int layers, int mtiles);
+bool gemm_shape_supported(int nt_per_block, int waves);
+void launch_argmax_combine(hipStream_t s, const float* pmax, const int* pidx, int groups, int B, int* tokens);
 void launch_attention(hipStream_t s, const AttnArgs& a, int hd, int chunk, int n_chunks);
 void launch_attn_combine(hipStream_t s, const AttnArgs& a, int hd, int chunk, int n_chunks);
-size_t gemm_lds_bytes(int kt_per_split);
 
 }  // namespace dflare

@@ -35,6 +35,24 @@ __device__ __forceinline__ void split_pack8(const float* v, u32x4& hi, u32x4& lo
   }
 }
 
+// Activations handed from one kernel to the next are stored directly in the A-operand
+// layout of v_mfma_f32_16x16x32_bf16, as two bf16 planes hi and lo (x ~= hi + lo):
+//   element (row, k) of a [rows, K] matrix sits in 16-row tile row/16, k-tile k/32,
+//   lane (row % 16) + 16 * ((k % 32) / 8), slot k % 8; a (row-tile, k-tile) is 1 KiB.
+__device__ __forceinline__ long frag_off(int row, int k, int Kt) {
+  return ((((long)(row >> 4) * Kt + (k >> 5)) * 64 + (row & 15) + ((k & 31) >> 3) * 16) << 3) + (k & 7);
+}
+
+// store the hi/lo planes of two consecutive elements (k even) as one 32-bit word each
+__device__ __forceinline__ void store_frag_pair(uint32_t* hi, uint32_t* lo, int row, int k, int Kt, float v0,
+                                                float v1) {
+  const uint32_t h0 = f2bf(v0), h1 = f2bf(v1);
+  const uint32_t l0 = f2bf(v0 - bf2f(h0)), l1 = f2bf(v1 - bf2f(h1));
+  const long o = frag_off(row, k, Kt) >> 1;
+  hi[o] = h0 | (h1 << 16);
+  lo[o] = l0 | (l1 << 16);
+}
+
 __device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
@@ -95,17 +113,20 @@ __global__ void k_prologue(StepParams* p, StepParams host, const int* ids_src, i
 }
 
 // ------------------------------------------------------------------------------------------
-// embedding gather: X[b, :] = E[id_b, :] (fp32) and per-16-column sums of squares
+// embedding gather: X[b, :] = E[id_b, :] (fp32), per-16-column sums of squares, and the
+// A fragments of X * g (g = gain of the first pre-attention RMSNorm)
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, const int* __restrict__ ids,
-                                               int vocab, int H, float* X, float* stats) {
+                                               int vocab, int H, float* X, float* stats,
+                                               const float* __restrict__ gain, u32x4* a_hi, u32x4* a_lo) {
   const int b = blockIdx.x;
   int id = ids[b];
   id = id < 0 ? 0 : (id >= vocab ? vocab - 1 : id);
   const uint16_t* row = E + (long)id * H;
+  const int Kt = H / 32;
   for (int k0 = threadIdx.x * 8; k0 < H; k0 += blockDim.x * 8) {
     const u32x4 v = *reinterpret_cast<const u32x4*>(row + k0);
-    float f[8];
+    float f[8], y[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       f[2 * e] = bf2f(v[e] & 0xFFFFu);
@@ -113,10 +134,18 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, c
     }
     float sq = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) sq += f[e] * f[e];
+    for (int e = 0; e < 8; ++e) {
+      sq += f[e] * f[e];
+      y[e] = f[e] * gain[k0 + e];
+    }
     float* xo = X + (long)b * H + k0;
     *reinterpret_cast<float4*>(xo) = make_float4(f[0], f[1], f[2], f[3]);
     *reinterpret_cast<float4*>(xo + 4) = make_float4(f[4], f[5], f[6], f[7]);
+    u32x4 hi, lo;
+    split_pack8(y, hi, lo);
+    const long fo = frag_off(b, k0, Kt) >> 3;
+    a_hi[fo] = hi;
+    a_lo[fo] = lo;
     sq += __shfl_xor(sq, 1);
     if ((threadIdx.x & 1) == 0) stats[(long)b * (H / 16) + k0 / 16] = sq;
   }
@@ -124,21 +153,32 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, c
 
 // ------------------------------------------------------------------------------------------
 // layer fusion (Eq. 3): u^(i)[r, k] = sum_j alpha[i, j] h^(j)[r, k] for all D draft layers from
-// one read of the S target rows; the RMS statistics are kept as per-16-column partial sums.
+// one read of the S target rows.  Writes the A fragments of u^(i) * g_fuse^(i) and per-16-
+// column sums of squares of u^(i); the 1/rms of Eq. 3 is applied in the K/V projection.
 // grid (ceil(H / 512), n), block 64, LDS S * 1 KiB.
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int n, int S, int H, int D,
-                                             const float* __restrict__ alpha, float* U, float* ustats,
-                                             int n_max) {
+                                             const float* __restrict__ alpha, const float* __restrict__ gain,
+                                             float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
   extern __shared__ u32x4 sh[];
   const int lane = threadIdx.x;
   const int r = blockIdx.y;
   const int k0 = blockIdx.x * 512 + lane * 8;
   const bool ok = k0 < H;
-  for (int j = 0; j < S; ++j) {
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (ok) v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(hidden + ((long)j * n + r) * H + k0));
-    sh[j * 64 + lane] = v;
+  const int Kt = H / 32;
+  // all S loads of this lane in flight together, 8 at a time
+  for (int j0 = 0; j0 < S; j0 += 8) {
+    u32x4 v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      v[q] = u32x4{0u, 0u, 0u, 0u};
+      if (ok && j0 + q < S)
+        v[q] = __builtin_nontemporal_load(
+            reinterpret_cast<const u32x4*>(hidden + ((long)(j0 + q) * n + r) * H + k0));
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (j0 + q < S) sh[(j0 + q) * 64 + lane] = v[q];
   }
   // each lane reads back only its own slots: no barrier needed
   for (int i = 0; i < D; ++i) {
@@ -157,18 +197,24 @@ __global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden
     for (int e = 0; e < 8; ++e) sq += u[e] * u[e];
     sq += __shfl_xor(sq, 1);
     if (ok) {
-      float* o = U + ((long)i * n_max + r) * H + k0;
-      *reinterpret_cast<float4*>(o) = make_float4(u[0], u[1], u[2], u[3]);
-      *reinterpret_cast<float4*>(o + 4) = make_float4(u[4], u[5], u[6], u[7]);
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = u[e] * gain[(long)i * H + k0 + e];
+      u32x4 hi, lo;
+      split_pack8(y, hi, lo);
+      const long fo = ((long)i * mt_max * Kt * 64 * 8 + frag_off(r, k0, Kt)) >> 3;
+      ua_hi[fo] = hi;
+      ua_lo[fo] = lo;
       if ((lane & 1) == 0) ustats[((long)i * n_max + r) * (H / 16) + k0 / 16] = sq;
     }
   }
 }
 
-// debug: materialise f^(i) = u * rstd * g (fp32), [D, n, H]
-__global__ void k_fused_rows(const float* U, const float* ustats, const float* gain, int n, int H, int D,
-                             int n_max, float eps, float* out) {
+// debug: materialise f^(i) = (hi + lo) * rstd, [D, n, H] fp32 (the gain is already applied)
+__global__ void k_fused_rows(const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n, int H, int D,
+                             int n_max, int mt_max, float eps, float* out) {
   const int r = blockIdx.x, i = blockIdx.y;
+  const int Kt = H / 32;
   __shared__ float s_r;
   if (threadIdx.x == 0) {
     float s = 0.f;
@@ -176,169 +222,176 @@ __global__ void k_fused_rows(const float* U, const float* ustats, const float* g
     s_r = rsqrtf(s / H + eps);
   }
   __syncthreads();
-  for (int k = threadIdx.x; k < H; k += blockDim.x)
-    out[((long)i * n + r) * H + k] = U[((long)i * n_max + r) * H + k] * s_r * gain[(long)i * H + k];
+  const uint16_t* hi = reinterpret_cast<const uint16_t*>(ua_hi);
+  const uint16_t* lo = reinterpret_cast<const uint16_t*>(ua_lo);
+  for (int k = threadIdx.x; k < H; k += blockDim.x) {
+    const long o = (long)i * mt_max * Kt * 64 * 8 + frag_off(r, k, Kt);
+    out[((long)i * n + r) * H + k] = (bf2f(hi[o]) + bf2f(lo[o])) * s_r;
+  }
 }
 
 // ------------------------------------------------------------------------------------------
-// weight-streaming GEMM, y[M<=16 per m-tile, N] = x[M, K] W^T, split-K over blocks.
-// Block = 4 waves; block (group, split) owns n-tiles [group*4*NT, +4*NT) and k-tiles
-// [split*kt_per_split, +kt_per_split).  Activations of the k range are normalised (optional
-// RMSNorm from partial statistics), split into bf16 hi/lo and staged in LDS in A-operand
-// order; each wave streams its NT weight tiles.  The last block of a group to arrive sums
-// the split partials in fixed order (deterministic) and runs the fused epilogue.
+// weight-streaming GEMM, y[M<=16 per m-tile, N] = x[M, K] W^T.
+// Block `group` owns output tiles [group*NT, +NT) over the whole K; its WAVES waves split the
+// k range, each streaming its NT weight tiles per k-tile from HBM together with the A
+// fragments of the same k-tile (hi and lo planes, from L2: they are shared by every block).
+// Two register sets alternate so that one batch of loads is always in flight while the
+// previous batch goes through the matrix cores.  The waves' partial sums are added in LDS in
+// wave order (fixed, so results do not depend on timing), and wave w < NT then holds output
+// tile group*NT + w for the epilogue.  No block ever waits on another: there is no split-K
+// across blocks, because making partial sums of one XCD visible to another takes agent-scope
+// fences that write back and invalidate the L2 -- far costlier than these kernels.
 // ------------------------------------------------------------------------------------------
-template <int NT, int EPI>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
-  constexpr int U = (8 / NT) < 2 ? 2 : (8 / NT);
-  extern __shared__ u32x4 lds[];
+template <int NT, int WAVES, int EPI>
+__global__ __launch_bounds__(64 * WAVES) void k_gemm(GemmArgs a) {
+  constexpr int U = 2;  // k-tiles per batch
+  __shared__ f32x4 red[WAVES][NT][64];
   __shared__ float s_rstd[16];
-  __shared__ int s_last;
-  __shared__ float s_bv[4][16];
-  __shared__ int s_bi[4][16];
+  __shared__ float s_bv[NT][16];
+  __shared__ int s_bi[NT][16];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int quad = lane >> 4, col = lane & 15;
-  const int groups = (a.Nt + 4 * NT - 1) / (4 * NT);
-  const int group = blockIdx.x % groups, split = blockIdx.x / groups;
+  const int groups = gridDim.x;
+  const int group = blockIdx.x;
   const int layer = blockIdx.y, mt = blockIdx.z;
-  const int kt0 = split * a.kt_per_split;
-  const int kt1 = min(a.Kt, kt0 + a.kt_per_split);
-  const int nk = kt1 - kt0;
   const int M = (EPI == EPI_KVT) ? a.e.params->n_new : a.M;
-  if (mt * 16 >= M) return;  // whole m-tile idle: every split of it leaves together
+  if (mt * 16 >= M) return;  // whole m-tile idle: every block of it leaves together
 
-  // 1. per-row 1/rms from the producer's partial sums of squares
-  if (a.stats) {
-    const int row = tid >> 4, part = tid & 15;
-    float s = 0.f;
-    if (mt * 16 + row < M) {
-      const float* st = a.stats + layer * a.stats_layer_stride + (long)(mt * 16 + row) * a.n_stat;
-      for (int t = part; t < a.n_stat; t += 16) s += st[t];
-    }
-    s += __shfl_xor(s, 8);
-    s += __shfl_xor(s, 4);
-    s += __shfl_xor(s, 2);
-    s += __shfl_xor(s, 1);
-    if (part == 0) s_rstd[row] = rsqrtf(s * a.inv_dim + a.eps);
-  }
-  __syncthreads();
+  const int kw0 = (a.Kt * wave) / WAVES;
+  const int nk = (a.Kt * (wave + 1)) / WAVES - kw0;
+  const int nb = (nk + U - 1) / U;
+  const int nb2 = (nb + 1) & ~1;
+  const int nt0 = group * NT;
 
-  // 2. stage the activation slice as bf16 hi/lo A fragments
-  u32x4* lhi = lds;
-  u32x4* llo = lds + a.kt_per_split * 64;
-  {
-    const float* X = a.X + layer * a.x_layer_stride;
-    const float* G = a.gain ? a.gain + layer * a.gain_layer_stride : nullptr;
-    for (int idx = tid; idx < nk * 64; idx += 256) {
-      const int t = idx >> 6, l = idx & 63, r = l & 15;
-      const int row = mt * 16 + r;
-      const int k = (kt0 + t) * 32 + (l >> 4) * 8;
-      float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      if (row < M) {
-        const float4 x0 = *reinterpret_cast<const float4*>(X + (long)row * a.ldx + k);
-        const float4 x1 = *reinterpret_cast<const float4*>(X + (long)row * a.ldx + k + 4);
-        v[0] = x0.x; v[1] = x0.y; v[2] = x0.z; v[3] = x0.w;
-        v[4] = x1.x; v[5] = x1.y; v[6] = x1.z; v[7] = x1.w;
-        const float sc = a.stats ? s_rstd[r] : 1.0f;
-        if (G) {
-          const float4 g0 = *reinterpret_cast<const float4*>(G + k);
-          const float4 g1 = *reinterpret_cast<const float4*>(G + k + 4);
-          v[0] *= sc * g0.x; v[1] *= sc * g0.y; v[2] *= sc * g0.z; v[3] *= sc * g0.w;
-          v[4] *= sc * g1.x; v[5] *= sc * g1.y; v[6] *= sc * g1.z; v[7] *= sc * g1.w;
-        } else if (a.stats) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) v[e] *= sc;
-        }
-      }
-      u32x4 hi, lo;
-      split_pack8(v, hi, lo);
-      lhi[idx] = hi;
-      llo[idx] = lo;
-    }
-  }
-  __syncthreads();
-
-  // 3. stream the weight tiles through the matrix cores
-  const int nt_base = group * 4 * NT + wave * NT;
-  f32x4 acc[NT];
-#pragma unroll
-  for (int j = 0; j < NT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // Tile addresses; a tile past the wave's range or a padding output tile reads the zero
+  // tile instead, so the streaming loop has no branches.
+  const u32x4* zt = a.zero + lane;
   const u32x4* Wl = a.W + layer * a.w_layer_stride;
-  for (int t = 0; t < nk; t += U) {
-    u32x4 b[U][NT];
+  const u32x4* wrow[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) wrow[j] = Wl + ((long)(nt0 + j) * a.Kt + kw0) * 64 + lane;
+  const long abase = layer * a.a_layer_stride + ((long)mt * a.Kt + kw0) * 64 + lane;
+  const u32x4* ah_row = a.Ahi + abase;
+  const u32x4* al_row = a.Alo + abase;
+  auto wptr = [&](int j, int t) -> const u32x4* {
+    return (t < nk && nt0 + j < a.Nt) ? wrow[j] + (long)t * 64 : zt;
+  };
+  auto ahp = [&](int t) -> const u32x4* { return (t < nk) ? ah_row + (long)t * 64 : zt; };
+  auto alp = [&](int t) -> const u32x4* { return (t < nk) ? al_row + (long)t * 64 : zt; };
+
+  u32x4 wA[U][NT], hA[U], lA[U], wB[U][NT], hB[U], lB[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+#pragma unroll
+    for (int j = 0; j < NT; ++j) wA[u][j] = __builtin_nontemporal_load(wptr(j, u));
+    hA[u] = *ahp(u);
+    lA[u] = *alp(u);
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+#pragma unroll
+    for (int j = 0; j < NT; ++j) wB[u][j] = __builtin_nontemporal_load(wptr(j, U + u));
+    hB[u] = *ahp(U + u);
+    lB[u] = *alp(U + u);
+  }
+  f32x4 acc_h[NT], acc_l[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    acc_h[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    acc_l[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int b = 0; b < nb2; b += 2) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
-        const int nt = nt_base + j;
-        b[u][j] = u32x4{0u, 0u, 0u, 0u};
-        if (t + u < nk && nt < a.Nt)
-          b[u][j] = __builtin_nontemporal_load(Wl + ((long)nt * a.Kt + kt0 + t + u) * 64 + lane);
+        acc_h[j] = mfma(hA[u], wA[u][j], acc_h[j]);
+        acc_l[j] = mfma(lA[u], wA[u][j], acc_l[j]);
       }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (t + u < nk) {
-        const u32x4 ah = lhi[(t + u) * 64 + lane];
-        const u32x4 al = llo[(t + u) * 64 + lane];
+      const int t = (b + 2) * U + u;
 #pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          acc[j] = mfma(ah, b[u][j], acc[j]);
-          acc[j] = mfma(al, b[u][j], acc[j]);
+      for (int j = 0; j < NT; ++j) wA[u][j] = __builtin_nontemporal_load(wptr(j, t));
+      hA[u] = *ahp(t);
+      lA[u] = *alp(t);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        acc_h[j] = mfma(hB[u], wB[u][j], acc_h[j]);
+        acc_l[j] = mfma(lB[u], wB[u][j], acc_l[j]);
+      }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = (b + 3) * U + u;
+#pragma unroll
+      for (int j = 0; j < NT; ++j) wB[u][j] = __builtin_nontemporal_load(wptr(j, t));
+      hB[u] = *ahp(t);
+      lB[u] = *alp(t);
+    }
+  }
+
+  // waves -> tiles: wave w < NT receives tile w summed over the waves in wave order
+#pragma unroll
+  for (int j = 0; j < NT; ++j) red[wave][j][lane] = acc_h[j] + acc_l[j];
+  __syncthreads();
+  const bool owner = wave < NT;
+  const int nt = nt0 + (owner ? wave : 0);
+  const bool has_tile = owner && nt < a.Nt;  // wave-uniform
+  f32x4 v = {0.f, 0.f, 0.f, 0.f};
+  if (owner) {
+    v = red[0][wave][lane];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) v += red[w][wave][lane];
+  }
+
+  // 1/rms of the rows (RMSNorm consumers): (x*g/rms) W^T = (1/rms) (x*g) W^T
+  if (a.stats) {
+    if (tid < 256) {
+      const int row = tid >> 4, part = tid & 15;
+      float s = 0.f;
+      if (mt * 16 + row < M) {
+        const float* st = a.stats + layer * a.stats_layer_stride + (long)(mt * 16 + row) * a.n_stat;
+#pragma unroll
+        for (int q = 0; q < 32; ++q) {
+          const int t = part + 16 * q;
+          if (t < a.n_stat) s += st[t];
         }
       }
-    }
-  }
-
-  // 4. split-K: last arriving block sums the partials in split order
-  if (a.splits > 1) {
-    const long ptile = (long)(layer * gridDim.z + mt) * a.splits;  // (layer, m-tile) slab
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int nt = nt_base + j;
-      if (nt < a.Nt)
-        *reinterpret_cast<f32x4*>(a.partials + (((ptile + split) * a.Nt + nt) * 64 + lane) * 4) = acc[j];
-    }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-      unsigned* c = a.counters + (long)(layer * gridDim.z + mt) * groups + group;
-      const unsigned prev = atomicAdd(c, 1u);
-      s_last = (prev == (unsigned)(a.splits - 1));
-      if (s_last) *c = 0u;  // every split has arrived: reset for the next launch
+      s += __shfl_xor(s, 8);
+      s += __shfl_xor(s, 4);
+      s += __shfl_xor(s, 2);
+      s += __shfl_xor(s, 1);
+      if (part == 0) s_rstd[row] = rsqrtf(s * a.inv_dim + a.eps);
     }
     __syncthreads();
-    if (!s_last) return;
-    __threadfence();
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int nt = nt_base + j;
-      f32x4 s = {0.f, 0.f, 0.f, 0.f};
-      if (nt < a.Nt)
-        for (int sp = 0; sp < a.splits; ++sp)
-          s += *reinterpret_cast<const f32x4*>(a.partials + (((ptile + sp) * a.Nt + nt) * 64 + lane) * 4);
-      acc[j] = s;
-    }
+    for (int i = 0; i < 4; ++i) v[i] *= s_rstd[quad * 4 + i];
   }
 
-  // 5. epilogues.  Lane holds rows mt*16 + 4*quad + i (i < 4) of output column nt*16 + col.
+  // epilogues.  The owner lane holds rows mt*16 + 4*quad + i (i < 4) of output column nt*16 + col.
   const EpiArgs& e = a.e;
   if constexpr (EPI == EPI_RESID) {
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int nt = nt_base + j;
-      if (nt >= a.Nt) continue;  // wave-uniform
+    if (has_tile) {
+      const int k = nt * 16 + col;
+      const float gn = e.next_gain[k];
       float sq[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = mt * 16 + quad * 4 + i;
         float x = 0.f;
         if (row < M) {
-          float* p = e.out + (long)row * e.ldo + nt * 16 + col;
-          x = *p + acc[j][i];
+          float* p = e.out + (long)row * e.ldo + k;
+          x = *p + v[i];
           *p = x;
         }
         sq[i] = x * x;
+        const float y = x * gn;
+        const float y1 = __shfl_xor(y, 1);
+        if ((col & 1) == 0 && row < M) store_frag_pair(e.na_hi, e.na_lo, row, k, e.na_Kt, y, y1);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -355,27 +408,23 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
         }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int nt = nt_base + j;
-      if (nt >= a.Nt) continue;
+    if (has_tile) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float v = acc[j][i];
-        const float up = __shfl_xor(v, 8);
+        const float g = v[i];
+        const float up = __shfl_xor(g, 8);
+        const float hv = (col < 8) ? g / (1.0f + expf(-g)) * up : 0.f;
+        const float h1 = __shfl_xor(hv, 1);
         const int row = mt * 16 + quad * 4 + i;
-        if (col < 8 && row < M) e.out[(long)row * e.ldo + nt * 8 + col] = v / (1.0f + expf(-v)) * up;
+        if (col < 8 && (col & 1) == 0 && row < M) store_frag_pair(e.na_hi, e.na_lo, row, nt * 8 + col, e.na_Kt, hv, h1);
       }
     }
   } else if constexpr (EPI == EPI_QKV || EPI == EPI_KVT) {
-    const int L = e.params->L;
-    const int tph = e.hd / 16, half = e.hd / 2;
-    uint16_t* kc = e.kc + (EPI == EPI_KVT ? layer * e.cache_layer_stride : 0);
-    uint16_t* vt = e.vt + (EPI == EPI_KVT ? layer * e.cache_layer_stride : 0);
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int nt = nt_base + j;
-      if (nt >= a.Nt) continue;
+    if (has_tile) {
+      const int L = e.params->L;
+      const int tph = e.hd / 16, half = e.hd / 2;
+      uint16_t* kc = e.kc + (EPI == EPI_KVT ? layer * e.cache_layer_stride : 0);
+      uint16_t* vt = e.vt + (EPI == EPI_KVT ? layer * e.cache_layer_stride : 0);
       int region, t;  // 0 = Q, 1 = K, 2 = V
       if (nt < e.q_tiles) { region = 0; t = nt; }
       else if (nt < e.q_tiles + e.kv_tiles) { region = 1; t = nt - e.q_tiles; }
@@ -387,13 +436,13 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
         const bool valid = (EPI == EPI_QKV) ? (row < e.B) : (row < M);
         const int pos = valid ? ((EPI == EPI_QKV) ? e.params->pos[row] : L + row) : 0;
         const int slot = L + row;
-        const float v = acc[j][i];
-        const float partner = __shfl_xor(v, 8);
+        const float x = v[i];
+        const float partner = __shfl_xor(x, 8);
         if (region < 2) {
           const int m = 8 * jj + (col & 7);
           const int dim = (col < 8) ? m : half + m;
           const float2 cs = e.rope[(long)pos * half + m];
-          const float y = (col < 8) ? (v * cs.x - partner * cs.y) : (v * cs.x + partner * cs.y);
+          const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
           if (valid) {
             if (region == 0)
               e.out[(long)row * e.ldo + head * e.hd + dim] = y;
@@ -402,77 +451,78 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
           }
         } else if (valid) {
           const int dim = jj * 16 + col;
-          vt[((long)head * e.hd + dim) * e.Lcap + slot] = (uint16_t)f2bf(v);
+          vt[((long)head * e.hd + dim) * e.Lcap + slot] = (uint16_t)f2bf(x);
         }
       }
     }
   } else if constexpr (EPI == EPI_ARGMAX) {
-    float bv[4];
-    int bi[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) { bv[i] = -INFINITY; bi[i] = 0x7FFFFFFF; }
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int nt = nt_base + j;
+    if (owner) {
       const int c = nt * 16 + col;
-      const bool ok = nt < a.Nt && c < e.vocab;
+      const bool ok = has_tile && c < e.vocab;
+      float bv[4];
+      int bi[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = quad * 4 + i;
-        const float v = acc[j][i];
-        if (ok && e.logits && row < e.B) e.logits[(long)row * e.vocab + c] = v;
-        if (ok && (v > bv[i] || (v == bv[i] && c < bi[i]))) { bv[i] = v; bi[i] = c; }
+        if (ok && e.logits && row < e.B) e.logits[(long)row * e.vocab + c] = v[i];
+        bv[i] = ok ? v[i] : -INFINITY;
+        bi[i] = ok ? c : 0x7FFFFFFF;
       }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) {
+          const float ov = __shfl_xor(bv[i], off);
+          const int oi = __shfl_xor(bi[i], off);
+          if (ov > bv[i] || (ov == bv[i] && oi < bi[i])) { bv[i] = ov; bi[i] = oi; }
+        }
+      if (col == 0)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { s_bv[wave][quad * 4 + i] = bv[i]; s_bi[wave][quad * 4 + i] = bi[i]; }
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) {
-        const float ov = __shfl_xor(bv[i], off);
-        const int oi = __shfl_xor(bi[i], off);
-        if (ov > bv[i] || (ov == bv[i] && oi < bi[i])) { bv[i] = ov; bi[i] = oi; }
-      }
-    if (col == 0)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { s_bv[wave][quad * 4 + i] = bv[i]; s_bi[wave][quad * 4 + i] = bi[i]; }
     __syncthreads();
-    if (tid < 16) {
-      float v = s_bv[0][tid];
+    if (tid < 16) {  // this block's best per row; the combine kernel picks across blocks
+      float bvv = s_bv[0][tid];
       int ix = s_bi[0][tid];
-      for (int w = 1; w < 4; ++w) {
+      for (int w = 1; w < NT; ++w) {
         const float ov = s_bv[w][tid];
         const int oi = s_bi[w][tid];
-        if (ov > v || (ov == v && oi < ix)) { v = ov; ix = oi; }
+        if (ov > bvv || (ov == bvv && oi < ix)) { bvv = ov; ix = oi; }
       }
-      e.pmax[(long)tid * groups + group] = v;
+      e.pmax[(long)tid * groups + group] = bvv;
       e.pidx[(long)tid * groups + group] = ix;
     }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-      const unsigned prev = atomicAdd(e.counter2, 1u);
-      s_last = (prev == (unsigned)(groups - 1));
-      if (s_last) *e.counter2 = 0u;
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    // final combine: 16 threads per row
-    const int row = tid >> 4, part = tid & 15;
-    float v = -INFINITY;
-    int ix = 0x7FFFFFFF;
-    for (int g = part; g < groups; g += 16) {
-      const float ov = e.pmax[(long)row * groups + g];
-      const int oi = e.pidx[(long)row * groups + g];
-      if (ov > v || (ov == v && oi < ix)) { v = ov; ix = oi; }
-    }
+  }
+}
+
+// per-row argmax over the blocks' partial results (ties: lowest token id)
+__global__ __launch_bounds__(256) void k_argmax_combine(const float* pmax, const int* pidx, int groups,
+                                                        int* tokens) {
+  __shared__ float s_v[4];
+  __shared__ int s_i[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  float v = -INFINITY;
+  int ix = 0x7FFFFFFF;
+  for (int g = tid; g < groups; g += 256) {
+    const float ov = pmax[(long)row * groups + g];
+    const int oi = pidx[(long)row * groups + g];
+    if (ov > v || (ov == v && oi < ix)) { v = ov; ix = oi; }
+  }
 #pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      const float ov = __shfl_xor(v, off);
-      const int oi = __shfl_xor(ix, off);
-      if (ov > v || (ov == v && oi < ix)) { v = ov; ix = oi; }
-    }
-    if (part == 0 && row < e.B) e.tokens[row] = (ix == 0x7FFFFFFF) ? 0 : ix;
+  for (int off = 1; off < 64; off <<= 1) {
+    const float ov = __shfl_xor(v, off);
+    const int oi = __shfl_xor(ix, off);
+    if (ov > v || (ov == v && oi < ix)) { v = ov; ix = oi; }
+  }
+  if ((tid & 63) == 0) {
+    s_v[tid >> 6] = v;
+    s_i[tid >> 6] = ix;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < 4; ++w)
+      if (s_v[w] > v || (s_v[w] == v && s_i[w] < ix)) { v = s_v[w]; ix = s_i[w]; }
+    tokens[row] = (ix == 0x7FFFFFFF) ? 0 : ix;
   }
 }
 
@@ -607,28 +657,42 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
   }
 }
 
-// combine the chunk partials: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c
+// combine the chunk partials: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as the
+// A fragments of the output projection.  One thread per (query row, 8 consecutive dims).
 template <int HD, int CK>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
   const int g = blockIdx.y;
   const int idx = blockIdx.x * 256 + threadIdx.x;
-  const int r = idx / HD, d = idx % HD;
+  const int r = idx / (HD / 8), d0 = (idx % (HD / 8)) * 8;
   const int G = a.n_q / a.n_kv;
   const int R = G * a.B;
   if (r >= R) return;
   const int nch = (a.params->L + a.B + CK - 1) / CK;
   float M = -INFINITY;
+#pragma unroll 4
   for (int c = 0; c < nch; ++c) M = fmaxf(M, a.ml[((long)c * a.n_kv + g) * a.Rpad + r].x);
-  float num = 0.f, den = 0.f;
+  float num[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float den = 0.f;
+#pragma unroll 4
   for (int c = 0; c < nch; ++c) {
     const long base = ((long)c * a.n_kv + g) * a.Rpad + r;
     const float2 ml = a.ml[base];
     const float wgt = exp2f(ml.x - M);
     den += wgt * ml.y;
-    num += wgt * a.opart[base * HD + d];
+    const float4 o0 = *reinterpret_cast<const float4*>(a.opart + base * HD + d0);
+    const float4 o1 = *reinterpret_cast<const float4*>(a.opart + base * HD + d0 + 4);
+    num[0] += wgt * o0.x; num[1] += wgt * o0.y; num[2] += wgt * o0.z; num[3] += wgt * o0.w;
+    num[4] += wgt * o1.x; num[5] += wgt * o1.y; num[6] += wgt * o1.z; num[7] += wgt * o1.w;
   }
+  const float inv = 1.0f / den;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) num[e] *= inv;
   const int b = r % a.B, h = g * G + r / a.B;
-  a.out[(long)b * a.q_dim + h * HD + d] = num / den;
+  u32x4 hi, lo;
+  split_pack8(num, hi, lo);
+  const long fo = frag_off(b, h * HD + d0, a.oa_Kt) >> 3;
+  a.oa_hi[fo] = hi;
+  a.oa_lo[fo] = lo;
 }
 
 // ------------------------------------------------------------------------------------------
@@ -655,43 +719,55 @@ void launch_prologue(hipStream_t s, StepParams* p, const StepParams& host, const
 }
 
 void launch_embed(hipStream_t s, const uint16_t* embed, const int* ids, int vocab, int H, int B, float* X,
-                  float* stats) {
-  hipLaunchKernelGGL(k_embed, dim3(B), dim3(256), 0, s, embed, ids, vocab, H, X, stats);
+                  float* stats, const float* gain, u32x4* a_hi, u32x4* a_lo) {
+  hipLaunchKernelGGL(k_embed, dim3(B), dim3(256), 0, s, embed, ids, vocab, H, X, stats, gain, a_hi, a_lo);
 }
 
-void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha, float* U,
-                 float* ustats, int n_max) {
+void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
+                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
   hipLaunchKernelGGL(k_fuse, dim3((H + 511) / 512, n), dim3(64), (size_t)S * 1024, s, hidden, n, S, H, D, alpha,
-                     U, ustats, n_max);
+                     gain, ustats, ua_hi, ua_lo, n_max, mt_max);
 }
 
-void launch_fused_rows(hipStream_t s, const float* U, const float* ustats, const float* gain, int n, int H, int D,
-                       int n_max, float eps, float* out) {
-  hipLaunchKernelGGL(k_fused_rows, dim3(n, D), dim3(256), 0, s, U, ustats, gain, n, H, D, n_max, eps, out);
+void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n, int H,
+                       int D, int n_max, int mt_max, float eps, float* out) {
+  hipLaunchKernelGGL(k_fused_rows, dim3(n, D), dim3(256), 0, s, ua_hi, ua_lo, ustats, n, H, D, n_max, mt_max, eps,
+                     out);
 }
 
-size_t gemm_lds_bytes(int kt_per_split) { return (size_t)kt_per_split * 64 * 16 * 2; }
-
-template <int NT>
-static void gemm_nt(hipStream_t s, int epi, const GemmArgs& a, dim3 grid, size_t lds) {
+template <int NT, int WAVES>
+static void gemm_nw(hipStream_t s, int epi, const GemmArgs& a, dim3 grid) {
+  const dim3 block(64 * WAVES);
   switch (epi) {
-    case EPI_RESID: hipLaunchKernelGGL((k_gemm<NT, EPI_RESID>), grid, dim3(256), lds, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((k_gemm<NT, EPI_SWIGLU>), grid, dim3(256), lds, s, a); break;
-    case EPI_QKV: hipLaunchKernelGGL((k_gemm<NT, EPI_QKV>), grid, dim3(256), lds, s, a); break;
-    case EPI_KVT: hipLaunchKernelGGL((k_gemm<NT, EPI_KVT>), grid, dim3(256), lds, s, a); break;
-    case EPI_ARGMAX: hipLaunchKernelGGL((k_gemm<NT, EPI_ARGMAX>), grid, dim3(256), lds, s, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_RESID>), grid, block, 0, s, a); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_SWIGLU>), grid, block, 0, s, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_QKV>), grid, block, 0, s, a); break;
+    case EPI_KVT: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_KVT>), grid, block, 0, s, a); break;
+    case EPI_ARGMAX: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_ARGMAX>), grid, block, 0, s, a); break;
   }
 }
 
-void launch_gemm(hipStream_t s, int epi, int nt_per_wave, const GemmArgs& a, int layers, int mtiles) {
-  const int groups = (a.Nt + 4 * nt_per_wave - 1) / (4 * nt_per_wave);
-  const dim3 grid(groups * a.splits, layers, mtiles);
-  const size_t lds = gemm_lds_bytes(a.kt_per_split);
-  switch (nt_per_wave) {
-    case 1: gemm_nt<1>(s, epi, a, grid, lds); break;
-    case 2: gemm_nt<2>(s, epi, a, grid, lds); break;
-    case 4: gemm_nt<4>(s, epi, a, grid, lds); break;
+bool gemm_shape_supported(int nt_per_block, int waves) {
+  return (nt_per_block == 1 && (waves == 8 || waves == 16)) || (nt_per_block == 2 && (waves == 8 || waves == 16)) ||
+         (nt_per_block == 4 && (waves == 4 || waves == 8));
+}
+
+void launch_gemm(hipStream_t s, int epi, int nt_per_block, int waves, const GemmArgs& a, int layers, int mtiles) {
+  const dim3 grid((a.Nt + nt_per_block - 1) / nt_per_block, layers, mtiles);
+  if (nt_per_block == 1) {
+    if (waves == 16) gemm_nw<1, 16>(s, epi, a, grid);
+    else gemm_nw<1, 8>(s, epi, a, grid);
+  } else if (nt_per_block == 2) {
+    if (waves == 16) gemm_nw<2, 16>(s, epi, a, grid);
+    else gemm_nw<2, 8>(s, epi, a, grid);
+  } else {
+    if (waves == 8) gemm_nw<4, 8>(s, epi, a, grid);
+    else gemm_nw<4, 4>(s, epi, a, grid);
   }
+}
+
+void launch_argmax_combine(hipStream_t s, const float* pmax, const int* pidx, int groups, int B, int* tokens) {
+  hipLaunchKernelGGL(k_argmax_combine, dim3(B), dim3(256), 0, s, pmax, pidx, groups, tokens);
 }
 
 template <int HD>
@@ -705,7 +781,7 @@ static void attn_hd(hipStream_t s, const AttnArgs& a, int chunk, int n_chunks, b
       case 256: hipLaunchKernelGGL((k_attn<HD, 256>), grid, dim3(threads), 0, s, a); break;
     }
   } else {
-    const dim3 grid((a.Rpad * HD + 255) / 256, a.n_kv);
+    const dim3 grid((a.Rpad * (HD / 8) + 255) / 256, a.n_kv);
     switch (chunk) {
       case 64: hipLaunchKernelGGL((k_attn_combine<HD, 64>), grid, dim3(256), 0, s, a); break;
       case 128: hipLaunchKernelGGL((k_attn_combine<HD, 128>), grid, dim3(256), 0, s, a); break;

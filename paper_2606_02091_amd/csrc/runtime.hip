@@ -27,10 +27,9 @@ namespace {
 const uint32_t kMagic = 0xDF1A2E00u;
 
 struct Plan {
-  int nt = 1;      // n-tiles per wave
-  int ktps = 16;   // k-tiles per split
-  int splits = 1;
-  int groups = 1;
+  int nt = 4;      // output tiles per block
+  int waves = 4;   // waves per block (they split K)
+  int groups = 1;  // blocks per layer and row tile
 };
 
 std::mutex g_mu;
@@ -63,15 +62,19 @@ struct dflare_handle {
   // step scratch
   StepParams* params = nullptr;
   int* ids = nullptr;
-  float *X = nullptr, *Xstats = nullptr, *Q = nullptr, *O = nullptr, *Hact = nullptr;
-  float *U = nullptr, *Ustats = nullptr;
-  float* partials = nullptr;
-  unsigned* counters = nullptr;
+  float *X = nullptr, *Xstats = nullptr, *Q = nullptr;
+  float* Ustats = nullptr;
+  // activations in A-fragment layout (hi / lo bf16 planes), each padded by 64 tiles
+  u32x4 *xa_hi = nullptr, *xa_lo = nullptr;  // x * gain of the next RMSNorm consumer, [Kt_H]
+  u32x4 *oa_hi = nullptr, *oa_lo = nullptr;  // attention output, [Kt_q]
+  u32x4 *ha_hi = nullptr, *ha_lo = nullptr;  // SwiGLU output, [Kt_F]
+  u32x4 *ua_hi = nullptr, *ua_lo = nullptr;  // fused rows u * g_fuse, [D, mt_max, Kt_H]
+  int mt_max = 1;
   float* opart = nullptr;
   float2* ml = nullptr;
   float* pmax = nullptr;
   int* pidx = nullptr;
-  unsigned* counter2 = nullptr;
+  u32x4* zero_tile = nullptr;
   Plan p_qkv, p_o, p_gu, p_down, p_lm, p_kvt;
   int attn_chunk = 128, attn_nchunks = 1;
   // debug capture
@@ -145,43 +148,31 @@ bool live(const dflare_handle* h) {
   return h && g_live.count(h) && h->magic == kMagic;
 }
 
-// Plan of a weight-streaming GEMM: n-tiles per wave and k-tiles per split.  The
-// defaults can be overridden with DFLARE_PLAN_<NAME>=nt,ktps (used for tuning).
-Plan make_plan(const char* name, int Nt, int Kt, int nt, int ktps) {
+// Plan of a weight-streaming GEMM: output tiles per block and waves per block.  The defaults
+// can be overridden with DFLARE_PLAN_<NAME>=nt,waves (used for tuning).
+Plan make_plan(const char* name, int Nt, int nt, int waves) {
   char key[64];
   snprintf(key, sizeof key, "DFLARE_PLAN_%s", name);
   if (const char* env = getenv(key)) {
-    int a = 0, b = 0;
-    if (sscanf(env, "%d,%d", &a, &b) == 2 && (a == 1 || a == 2 || a == 4) && b >= 1) {
-      nt = a;
-      ktps = b;
+    int x = 0, y = 0;
+    if (sscanf(env, "%d,%d", &x, &y) == 2 && gemm_shape_supported(x, y)) {
+      nt = x;
+      waves = y;
     }
   }
   Plan p;
   p.nt = nt;
-  ktps = std::min(ktps, Kt);
-  p.splits = ceil_div(Kt, ktps);
-  p.ktps = ceil_div(Kt, p.splits);  // balance the splits
-  p.splits = ceil_div(Kt, p.ktps);
-  p.groups = ceil_div(Nt, 4 * nt);
+  p.waves = waves;
+  p.groups = ceil_div(Nt, nt);
   return p;
 }
 
-long plan_partials(const Plan& p, int Nt, int layers, int mtiles) {
-  return p.splits > 1 ? (long)layers * mtiles * p.splits * Nt * 256 : 0;
-}
-
-long plan_counters(const Plan& p, int layers, int mtiles) { return (long)layers * mtiles * p.groups; }
-
-GemmArgs gemm_args(const dflare_handle* h, const Plan& p, const u32x4* W, int Nt, int Kt) {
+GemmArgs gemm_args(const dflare_handle* h, const u32x4* W, int Nt, int Kt) {
   GemmArgs a{};
   a.W = W;
   a.Nt = Nt;
   a.Kt = Kt;
-  a.kt_per_split = p.ktps;
-  a.splits = p.splits;
-  a.partials = h->partials;
-  a.counters = h->counters;
+  a.zero = h->zero_tile;
   a.eps = h->cfg.rms_eps;
   a.e.params = h->params;
   a.e.Lcap = h->Lcap;
@@ -214,6 +205,7 @@ int validate_config(const dflare_config* c) {
   if ((c->n_q_heads / c->n_kv_heads) * c->block_size > 128)
     return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "(n_q_heads / n_kv_heads) * block_size must be <= 128");
   if (c->n_target_layers > 64) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "n_target_layers must be <= 64");
+  if (c->hidden > 8192) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "hidden must be <= 8192");
   if ((long)c->max_context + c->block_size > (1L << 30))
     return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "max_context too large");
   return DFLARE_OK;
@@ -241,12 +233,12 @@ int build(dflare_handle* h, const dflare_weights* w) {
   const int Nt_lm = ceil_div(V, 16), Nt_kvt = 2 * kv / 16;
   const int Kt_H = H / 32, Kt_q = q / 32, Kt_F = F / 32;
   const int mt_max = ceil_div(c.max_new, 16);
-  h->p_qkv = make_plan("QKV", Nt_qkv, Kt_H, 1, 16);
-  h->p_o = make_plan("O", Nt_o, Kt_q, 1, 16);
-  h->p_gu = make_plan("GU", Nt_gu, Kt_H, 2, 32);
-  h->p_down = make_plan("DOWN", Nt_down, Kt_F, 1, 32);
-  h->p_lm = make_plan("LM", Nt_lm, Kt_H, 4, 32);
-  h->p_kvt = make_plan("KVT", Nt_kvt, Kt_H, 1, 32);
+  h->p_qkv = make_plan("QKV", Nt_qkv, 2, 16);
+  h->p_o = make_plan("O", Nt_o, 1, 16);
+  h->p_gu = make_plan("GU", Nt_gu, 4, 4);
+  h->p_down = make_plan("DOWN", Nt_down, 1, 16);
+  h->p_lm = make_plan("LM", Nt_lm, 4, 4);
+  h->p_kvt = make_plan("KVT", Nt_kvt, 1, 16);
   if (const char* env = getenv("DFLARE_ATTN_CHUNK")) {
     int v = atoi(env);
     if (v == 64 || v == 128 || v == 256) h->attn_chunk = v;
@@ -326,31 +318,25 @@ int build(dflare_handle* h, const dflare_weights* w) {
 
   // ---- step scratch
   TRY(dev_alloc(h, &h->params, sizeof(StepParams)));
+  TRY(dev_alloc(h, &h->zero_tile, 64 * 16));
+  HIP_OR_FAIL(h, hipMemsetAsync(h->zero_tile, 0, 64 * 16, s));
   TRY(dev_alloc(h, &h->ids, 64 * 4));
   TRY(dev_alloc(h, &h->X, (size_t)16 * H * 4));
   TRY(dev_alloc(h, &h->Xstats, (size_t)16 * (H / 16) * 4));
   TRY(dev_alloc(h, &h->Q, (size_t)16 * q * 4));
-  TRY(dev_alloc(h, &h->O, (size_t)16 * q * 4));
-  TRY(dev_alloc(h, &h->Hact, (size_t)16 * F * 4));
-  TRY(dev_alloc(h, &h->U, (size_t)D * c.max_new * H * 4));
   TRY(dev_alloc(h, &h->Ustats, (size_t)D * c.max_new * (H / 16) * 4));
-  long part = 0, cnt = 0;
-  part = std::max(part, plan_partials(h->p_qkv, Nt_qkv, 1, 1));
-  part = std::max(part, plan_partials(h->p_o, Nt_o, 1, 1));
-  part = std::max(part, plan_partials(h->p_gu, Nt_gu, 1, 1));
-  part = std::max(part, plan_partials(h->p_down, Nt_down, 1, 1));
-  part = std::max(part, plan_partials(h->p_lm, Nt_lm, 1, 1));
-  part = std::max(part, plan_partials(h->p_kvt, Nt_kvt, D, mt_max));
-  cnt = std::max(cnt, plan_counters(h->p_qkv, 1, 1));
-  cnt = std::max(cnt, plan_counters(h->p_o, 1, 1));
-  cnt = std::max(cnt, plan_counters(h->p_gu, 1, 1));
-  cnt = std::max(cnt, plan_counters(h->p_down, 1, 1));
-  cnt = std::max(cnt, plan_counters(h->p_lm, 1, 1));
-  cnt = std::max(cnt, plan_counters(h->p_kvt, D, mt_max));
-  TRY(dev_alloc(h, &h->partials, (size_t)part * 4));
-  TRY(dev_alloc(h, &h->counters, (size_t)(cnt + 1) * 4));
-  h->counter2 = h->counters + cnt;
-  HIP_OR_FAIL(h, hipMemsetAsync(h->counters, 0, (size_t)(cnt + 1) * 4, s));
+  h->mt_max = mt_max;
+  {
+    const size_t pad = 64;
+    const size_t nx = (size_t)Kt_H + pad, no = (size_t)Kt_q + pad, nh = (size_t)Kt_F + pad;
+    const size_t nu = (size_t)D * mt_max * Kt_H + pad;
+    u32x4** bufs[8] = {&h->xa_hi, &h->xa_lo, &h->oa_hi, &h->oa_lo, &h->ha_hi, &h->ha_lo, &h->ua_hi, &h->ua_lo};
+    const size_t tiles[8] = {nx, nx, no, no, nh, nh, nu, nu};
+    for (int b = 0; b < 8; ++b) {
+      TRY(dev_alloc(h, bufs[b], tiles[b] * 1024));
+      HIP_OR_FAIL(h, hipMemsetAsync(*bufs[b], 0, tiles[b] * 1024, s));
+    }
+  }
   TRY(dev_alloc(h, &h->opart, (size_t)h->attn_nchunks * c.n_kv_heads * h->Rpad * hd * 4));
   TRY(dev_alloc(h, &h->ml, (size_t)h->attn_nchunks * c.n_kv_heads * h->Rpad * sizeof(float2)));
   TRY(dev_alloc(h, &h->pmax, (size_t)16 * h->p_lm.groups * 4));
@@ -369,7 +355,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   sp.n_new = 0;
   for (int b = 0; b < B; ++b) sp.pos[b] = positions_host ? positions_host[b] : h->L + b;
   launch_prologue(s, h->params, sp, ids, h->ids, B);
-  launch_embed(s, h->embed, h->ids, c.vocab, H, B, h->X, h->Xstats);
+  launch_embed(s, h->embed, h->ids, c.vocab, H, B, h->X, h->Xstats, h->g_attn, h->xa_hi, h->xa_lo);
 
   AttnArgs at{};
   at.params = h->params;
@@ -383,20 +369,21 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   at.qscale = (float)(1.4426950408889634 / sqrt((double)hd));
   at.opart = h->opart;
   at.ml = h->ml;
-  at.out = h->O;
+  at.oa_hi = h->oa_hi;
+  at.oa_lo = h->oa_lo;
+  at.oa_Kt = q / 32;
 
   for (int i = 0; i < D; ++i) {
     uint16_t* kc = h->kc + i * h->cache_layer_stride;
     uint16_t* vt = h->vt + i * h->cache_layer_stride;
     {  // RMSNorm + Q / K^d / V^d + RoPE, block K/V into cache slots L..L+B-1
-      GemmArgs a = gemm_args(h, h->p_qkv, h->w_qkv + i * h->s_qkv, (q + 2 * kv) / 16, H / 32);
-      a.X = h->X; a.ldx = H; a.M = B;
+      GemmArgs a = gemm_args(h, h->w_qkv + i * h->s_qkv, (q + 2 * kv) / 16, H / 32);
+      a.Ahi = h->xa_hi; a.Alo = h->xa_lo; a.M = B;
       a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
-      a.gain = h->g_attn + (long)i * H;
       a.e.out = h->Q; a.e.ldo = q; a.e.kc = kc; a.e.vt = vt;
       a.e.q_tiles = q / 16; a.e.kv_tiles = kv / 16;
       prof_mark(h, DFLARE_K_QKV, true);
-      launch_gemm(s, EPI_QKV, h->p_qkv.nt, a, 1, 1);
+      launch_gemm(s, EPI_QKV, h->p_qkv.nt, h->p_qkv.waves, a, 1, 1);
       prof_mark(h, DFLARE_K_QKV, false);
     }
     at.kc = kc;
@@ -406,29 +393,32 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
     launch_attn_combine(s, at, hd, h->attn_chunk, h->attn_nchunks);
     prof_mark(h, DFLARE_K_ATTN, false);
     {  // X += O W_O^T
-      GemmArgs a = gemm_args(h, h->p_o, h->w_o + i * h->s_o, H / 16, q / 32);
-      a.X = h->O; a.ldx = q; a.M = B;
+      GemmArgs a = gemm_args(h, h->w_o + i * h->s_o, H / 16, q / 32);
+      a.Ahi = h->oa_hi; a.Alo = h->oa_lo; a.M = B;
       a.e.out = h->X; a.e.ldo = H; a.e.stats_out = h->Xstats; a.e.n_stat_out = H / 16;
+      a.e.na_hi = (uint32_t*)h->xa_hi; a.e.na_lo = (uint32_t*)h->xa_lo; a.e.na_Kt = H / 32;
+      a.e.next_gain = h->g_mlp + (long)i * H;
       prof_mark(h, DFLARE_K_O, true);
-      launch_gemm(s, EPI_RESID, h->p_o.nt, a, 1, 1);
+      launch_gemm(s, EPI_RESID, h->p_o.nt, h->p_o.waves, a, 1, 1);
       prof_mark(h, DFLARE_K_O, false);
     }
     {  // RMSNorm + gate/up + SwiGLU
-      GemmArgs a = gemm_args(h, h->p_gu, h->w_gu + i * h->s_gu, 2 * F / 16, H / 32);
-      a.X = h->X; a.ldx = H; a.M = B;
+      GemmArgs a = gemm_args(h, h->w_gu + i * h->s_gu, 2 * F / 16, H / 32);
+      a.Ahi = h->xa_hi; a.Alo = h->xa_lo; a.M = B;
       a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
-      a.gain = h->g_mlp + (long)i * H;
-      a.e.out = h->Hact; a.e.ldo = F;
+      a.e.na_hi = (uint32_t*)h->ha_hi; a.e.na_lo = (uint32_t*)h->ha_lo; a.e.na_Kt = F / 32;
       prof_mark(h, DFLARE_K_GATE_UP, true);
-      launch_gemm(s, EPI_SWIGLU, h->p_gu.nt, a, 1, 1);
+      launch_gemm(s, EPI_SWIGLU, h->p_gu.nt, h->p_gu.waves, a, 1, 1);
       prof_mark(h, DFLARE_K_GATE_UP, false);
     }
     {  // X += H W_down^T
-      GemmArgs a = gemm_args(h, h->p_down, h->w_down + i * h->s_down, H / 16, F / 32);
-      a.X = h->Hact; a.ldx = F; a.M = B;
+      GemmArgs a = gemm_args(h, h->w_down + i * h->s_down, H / 16, F / 32);
+      a.Ahi = h->ha_hi; a.Alo = h->ha_lo; a.M = B;
       a.e.out = h->X; a.e.ldo = H; a.e.stats_out = h->Xstats; a.e.n_stat_out = H / 16;
+      a.e.na_hi = (uint32_t*)h->xa_hi; a.e.na_lo = (uint32_t*)h->xa_lo; a.e.na_Kt = H / 32;
+      a.e.next_gain = (i + 1 < D) ? h->g_attn + (long)(i + 1) * H : h->g_final;
       prof_mark(h, DFLARE_K_DOWN, true);
-      launch_gemm(s, EPI_RESID, h->p_down.nt, a, 1, 1);
+      launch_gemm(s, EPI_RESID, h->p_down.nt, h->p_down.waves, a, 1, 1);
       prof_mark(h, DFLARE_K_DOWN, false);
     }
     if (h->debug)
@@ -436,14 +426,14 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
                                     hipMemcpyDeviceToDevice, s));
   }
   {  // final RMSNorm + LM head + argmax
-    GemmArgs a = gemm_args(h, h->p_lm, h->w_lm, ceil_div(c.vocab, 16), H / 32);
-    a.X = h->X; a.ldx = H; a.M = B;
+    GemmArgs a = gemm_args(h, h->w_lm, ceil_div(c.vocab, 16), H / 32);
+    a.Ahi = h->xa_hi; a.Alo = h->xa_lo; a.M = B;
     a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
-    a.gain = h->g_final;
-    a.e.vocab = c.vocab; a.e.pmax = h->pmax; a.e.pidx = h->pidx; a.e.counter2 = h->counter2;
-    a.e.tokens = out; a.e.logits = h->debug ? h->dbg_logits : nullptr;
+    a.e.vocab = c.vocab; a.e.pmax = h->pmax; a.e.pidx = h->pidx;
+    a.e.logits = h->debug ? h->dbg_logits : nullptr;
     prof_mark(h, DFLARE_K_LM_HEAD, true);
-    launch_gemm(s, EPI_ARGMAX, h->p_lm.nt, a, 1, 1);
+    launch_gemm(s, EPI_ARGMAX, h->p_lm.nt, h->p_lm.waves, a, 1, 1);
+    launch_argmax_combine(s, h->pmax, h->pidx, h->p_lm.groups, B, out);
     prof_mark(h, DFLARE_K_LM_HEAD, false);
   }
   return check_launch(h, "draft_block");
@@ -514,21 +504,22 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   sp.n_new = n_new;
   launch_prologue(s, h->params, sp, nullptr, nullptr, 0);
   prof_mark(h, DFLARE_K_FUSE, true);
-  launch_fuse(s, (const uint16_t*)target_hidden, n_new, S, H, D, h->alpha, h->U, h->Ustats, c.max_new);
+  launch_fuse(s, (const uint16_t*)target_hidden, n_new, S, H, D, h->alpha, h->g_fuse, h->Ustats, h->ua_hi,
+              h->ua_lo, c.max_new, h->mt_max);
   prof_mark(h, DFLARE_K_FUSE, false);
-  GemmArgs a = gemm_args(h, h->p_kvt, h->w_kvt, 2 * h->kv_dim / 16, H / 32);
+  GemmArgs a = gemm_args(h, h->w_kvt, 2 * h->kv_dim / 16, H / 32);
   a.w_layer_stride = h->s_kvt;
-  a.X = h->U; a.x_layer_stride = (long)c.max_new * H; a.ldx = H;
+  a.Ahi = h->ua_hi; a.Alo = h->ua_lo; a.a_layer_stride = (long)h->mt_max * (H / 32) * 64;
   a.stats = h->Ustats; a.stats_layer_stride = (long)c.max_new * (H / 16); a.n_stat = H / 16;
   a.inv_dim = 1.0f / H;
-  a.gain = h->g_fuse; a.gain_layer_stride = H;
   a.e.kc = h->kc; a.e.vt = h->vt; a.e.cache_layer_stride = h->cache_layer_stride;
   a.e.q_tiles = 0; a.e.kv_tiles = h->kv_dim / 16;
   prof_mark(h, DFLARE_K_KV_T, true);
-  launch_gemm(s, EPI_KVT, h->p_kvt.nt, a, D, ceil_div(n_new, 16));
+  launch_gemm(s, EPI_KVT, h->p_kvt.nt, h->p_kvt.waves, a, D, ceil_div(n_new, 16));
   prof_mark(h, DFLARE_K_KV_T, false);
   if (h->debug) {
-    launch_fused_rows(s, h->U, h->Ustats, h->g_fuse, n_new, H, D, c.max_new, c.rms_eps, h->dbg_fused);
+    launch_fused_rows(s, h->ua_hi, h->ua_lo, h->Ustats, n_new, H, D, c.max_new, h->mt_max, c.rms_eps,
+                      h->dbg_fused);
     h->dbg_fused_n = n_new;
   }
   int rc = check_launch(h, "fuse_append");
@@ -704,7 +695,7 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches) {
 
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count) {
   if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
-  const int32_t v[2] = {2 + 6 * h->cfg.n_draft_layers + 1, 3};
+  const int32_t v[2] = {2 + 6 * h->cfg.n_draft_layers + 2, 3};
   for (int i = 0; i < count && i < 2; ++i) out[i] = v[i];
   return DFLARE_OK;
 }
