@@ -75,6 +75,9 @@ def main():
     cfg = synth.CONFIGS[args.config]
     L, B, S, H = cfg.context, cfg.block_size, cfg.n_target_layers, cfg.hidden
     torch.cuda.set_device(0)
+    # a non-default stream (default priority): the library replays its draft block as a HIP graph
+    side = torch.cuda.Stream()
+    torch.cuda.set_stream(side)
     t0 = time.time()
     w = synth.make_weights(cfg)
     fusion_logits = w.pop("fusion_logits")

@@ -216,11 +216,33 @@ class DraftOracle:
             raise ValueError("fusion logits must be [D, S]")
         self.max_context = max_context
         self.L = 0
-        self.k_cache = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(D)]
-        self.v_cache = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(D)]
+        # context keys/values per draft layer, grown by doubling; rows [0, L) are live
+        self._k = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(D)]
+        self._v = [np.zeros((0, cfg.n_kv_heads, cfg.head_dim)) for _ in range(D)]
         self._cache_weights = cache_weights
         self._lw: dict[int, dict] = {}
         self.last_fused = None
+
+    @property
+    def k_cache(self):
+        """Context keys per draft layer, each [L, n_kv, hd] (after RoPE)."""
+        return [k[:self.L] for k in self._k]
+
+    @property
+    def v_cache(self):
+        """Context values per draft layer, each [L, n_kv, hd]."""
+        return [v[:self.L] for v in self._v]
+
+    def _reserve(self, n: int) -> None:
+        cap = self._k[0].shape[0]
+        if n <= cap:
+            return
+        cap = max(n, 2 * cap)
+        for lst in (self._k, self._v):
+            for i, a in enumerate(lst):
+                b = np.zeros((cap,) + a.shape[1:])
+                b[:self.L] = a[:self.L]
+                lst[i] = b
 
     # -- weights -------------------------------------------------------------
     def _gain(self, kind, i=None):
@@ -255,11 +277,12 @@ class DraftOracle:
         fuse_g = self.w.get("fuse_norm")
         gains = None if fuse_g is None else bf16_to_f64(fuse_g)
         f = fuse_rows(self.alpha, h, gains, cfg.rms_eps)
+        self._reserve(self.L + n)
         for i in range(cfg.n_draft_layers):
             k, v = context_kv(f[i], bf16_to_f64(self.w["wk_t"][i]), bf16_to_f64(self.w["wv_t"][i]),
                               pos, cfg.n_kv_heads, cfg.head_dim, cfg.rope_base)
-            self.k_cache[i] = np.concatenate([self.k_cache[i], k], axis=0)
-            self.v_cache[i] = np.concatenate([self.v_cache[i], v], axis=0)
+            self._k[i][self.L:self.L + n] = k
+            self._v[i][self.L:self.L + n] = v
         self.L += n
         self.last_fused = f
         return f
@@ -267,9 +290,6 @@ class DraftOracle:
     def truncate(self, new_len: int) -> None:
         if not 0 <= new_len <= self.L:
             raise ValueError("truncate length out of range")
-        for i in range(self.cfg.n_draft_layers):
-            self.k_cache[i] = self.k_cache[i][:new_len]
-            self.v_cache[i] = self.v_cache[i][:new_len]
         self.L = new_len
 
     # -- block pass ----------------------------------------------------------
@@ -286,7 +306,7 @@ class DraftOracle:
         X = bf16_to_f64(self.w["embed"][ids])
         hs = []
         for i in range(cfg.n_draft_layers):
-            X = draft_layer(X, self.layer_weights(i), self.k_cache[i], self.v_cache[i], pos, cfg)
+            X = draft_layer(X, self.layer_weights(i), self._k[i][:self.L], self._v[i][:self.L], pos, cfg)
             hs.append(X)
         z = lm_head_logits(X, self._gain("final_norm"), self.w["lm_head"], cfg.rms_eps)
         out = {"tokens": argmax_lowest(z), "hidden": np.stack(hs)}

@@ -101,7 +101,8 @@ void launch_prologue(hipStream_t s, StepParams* p, const StepParams& host, const
 void launch_embed(hipStream_t s, const uint16_t* embed, const int* ids, int vocab, int H, int B,
                   float* X, float* stats, const float* gain, u32x4* a_hi, u32x4* a_lo);
 void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
-                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max);
+                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max,
+                 StepParams* params, int L);
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n,
                        int H, int D, int n_max, int mt_max, float eps, float* out);
 void launch_gemm(hipStream_t s, int epi, int nt_per_block, int waves, const GemmArgs& a, int layers, int mtiles);

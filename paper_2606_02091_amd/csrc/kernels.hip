@@ -152,61 +152,59 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, c
 }
 
 // ------------------------------------------------------------------------------------------
-// layer fusion (Eq. 3): u^(i)[r, k] = sum_j alpha[i, j] h^(j)[r, k] for all D draft layers from
-// one read of the S target rows.  Writes the A fragments of u^(i) * g_fuse^(i) and per-16-
-// column sums of squares of u^(i); the 1/rms of Eq. 3 is applied in the K/V projection.
-// grid (ceil(H / 512), n), block 64, LDS S * 1 KiB.
+// layer fusion (Eq. 3): u^(i)[r, k] = sum_j alpha[i, j] h^(j)[r, k], accumulated in j order.
+// Block (512 columns, row r, draft layer i); a lane owns 8 columns and keeps twelve 16-byte
+// loads in flight.  Writes the A fragments of u^(i) * g_fuse^(i) and per-16-column sums of
+// squares of u^(i); the 1/rms of Eq. 3 is applied in the K/V projection.  The S target rows
+// are read from HBM once; the blocks of the other draft layers find them in L2.
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int n, int S, int H, int D,
+__global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int n, int S, int H,
                                              const float* __restrict__ alpha, const float* __restrict__ gain,
-                                             float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
-  extern __shared__ u32x4 sh[];
+                                             float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max,
+                                             StepParams* params, int L) {
   const int lane = threadIdx.x;
-  const int r = blockIdx.y;
+  const int r = blockIdx.y, i = blockIdx.z;
+  if (blockIdx.x == 0 && r == 0 && i == 0 && lane == 0) {  // step parameters for the K/V projection
+    params->L = L;
+    params->n_new = n;
+  }
   const int k0 = blockIdx.x * 512 + lane * 8;
   const bool ok = k0 < H;
   const int Kt = H / 32;
-  // all S loads of this lane in flight together, 8 at a time
-  for (int j0 = 0; j0 < S; j0 += 8) {
-    u32x4 v[8];
+  float u[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int j0 = 0; j0 < S; j0 += 12) {
+    u32x4 v[12];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      v[q] = u32x4{0u, 0u, 0u, 0u};
-      if (ok && j0 + q < S)
-        v[q] = __builtin_nontemporal_load(
-            reinterpret_cast<const u32x4*>(hidden + ((long)(j0 + q) * n + r) * H + k0));
+    for (int qq = 0; qq < 12; ++qq) {
+      v[qq] = u32x4{0u, 0u, 0u, 0u};
+      if (ok && j0 + qq < S) v[qq] = *reinterpret_cast<const u32x4*>(hidden + ((long)(j0 + qq) * n + r) * H + k0);
     }
 #pragma unroll
-    for (int q = 0; q < 8; ++q)
-      if (j0 + q < S) sh[(j0 + q) * 64 + lane] = v[q];
-  }
-  // each lane reads back only its own slots: no barrier needed
-  for (int i = 0; i < D; ++i) {
-    float u[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < S; ++j) {
-      const float a = alpha[i * S + j];
-      const u32x4 v = sh[j * 64 + lane];
+    for (int qq = 0; qq < 12; ++qq) {
+      if (j0 + qq < S) {
+        const float a = alpha[i * S + j0 + qq];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        u[2 * e] = fmaf(a, bf2f(v[e] & 0xFFFFu), u[2 * e]);
-        u[2 * e + 1] = fmaf(a, bf2f(v[e] >> 16), u[2 * e + 1]);
+        for (int e = 0; e < 4; ++e) {
+          u[2 * e] = fmaf(a, bf2f(v[qq][e] & 0xFFFFu), u[2 * e]);
+          u[2 * e + 1] = fmaf(a, bf2f(v[qq][e] >> 16), u[2 * e + 1]);
+        }
       }
     }
-    float sq = 0.f;
+  }
+  float sq = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) sq += u[e] * u[e];
-    sq += __shfl_xor(sq, 1);
-    if (ok) {
-      float y[8];
+  for (int e = 0; e < 8; ++e) sq += u[e] * u[e];
+  sq += __shfl_xor(sq, 1);
+  if (ok) {
+    float y[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = u[e] * gain[(long)i * H + k0 + e];
-      u32x4 hi, lo;
-      split_pack8(y, hi, lo);
-      const long fo = ((long)i * mt_max * Kt * 64 * 8 + frag_off(r, k0, Kt)) >> 3;
-      ua_hi[fo] = hi;
-      ua_lo[fo] = lo;
-      if ((lane & 1) == 0) ustats[((long)i * n_max + r) * (H / 16) + k0 / 16] = sq;
-    }
+    for (int e = 0; e < 8; ++e) y[e] = u[e] * gain[(long)i * H + k0 + e];
+    u32x4 hi, lo;
+    split_pack8(y, hi, lo);
+    const long fo = ((long)i * mt_max * Kt * 64 * 8 + frag_off(r, k0, Kt)) >> 3;
+    ua_hi[fo] = hi;
+    ua_lo[fo] = lo;
+    if ((lane & 1) == 0) ustats[((long)i * n_max + r) * (H / 16) + k0 / 16] = sq;
   }
 }
 
@@ -528,171 +526,221 @@ __global__ __launch_bounds__(256) void k_argmax_combine(const float* pmax, const
 
 // ------------------------------------------------------------------------------------------
 // block attention, split over the key axis (Sec. 3.2: no mask, every block row sees the
-// whole context and the whole block).  Block (chunk c, KV head g); wave w takes 16 query rows
-// r = w*16 + lane%16 of the G*B rows that share head g (r -> query head g*G + r/B, block
+// whole context and the whole block).  Block (chunk c, KV head g): the CK keys of the chunk
+// (K rows and V^T rows, the block's own B keys sit in cache slots L..L+B-1) are copied to LDS
+// with every load in flight at once; then each wave takes 16-row query tiles
+// r = tile*16 + lane%16 of the G*B rows that share head g (r -> query head g*G + r/B, block
 // position r%B).  Scores are formed transposed, S^T = K Q^T, so that the probabilities land
 // in exactly the B-operand layout of the P V product and never leave registers.
 // ------------------------------------------------------------------------------------------
-template <int HD, int CK>
-__global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+template <int HD, int CK, int QTW>
+__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+  constexpr int CKM = CK + 32;  // the last chunk also holds the B <= 16 block keys
+  constexpr int KP = HD + 8;    // padded LDS row of K (elements): spreads rows over the banks
+  constexpr int VP = CKM + 8;   // padded LDS row of V^T
+  __shared__ __attribute__((aligned(16))) uint16_t sK[CKM * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[HD * VP];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int quad = lane >> 4, q = lane & 15;
   const int g = blockIdx.y, c = blockIdx.x;
-  const int Lk = a.params->L + a.B;
+  const int L = a.params->L;
+  const int nch = max(1, (L + CK - 1) / CK);
+  if (c >= nch) return;
   const int kbeg = c * CK;
-  if (kbeg >= Lk) return;
-  const int kend = min(Lk, kbeg + CK);
-  const int nkeys = kend - kbeg;
+  const int kend = (c == nch - 1) ? L + a.B : kbeg + CK;
+  const int nkeys = kend - kbeg;  // <= CK + B
   const int G = a.n_q / a.n_kv;
   const int R = G * a.B;
-  const int r = w * 16 + q;
-  const bool rv = r < R;
-  const int b = rv ? r % a.B : 0;
-  const int h = g * G + (rv ? r / a.B : 0);
 
-  u32x4 qh[HD / 32], ql[HD / 32];
-#pragma unroll
-  for (int ks = 0; ks < HD / 32; ++ks) {
-    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if (rv) {
-      const float* src = a.Q + (long)b * a.q_dim + h * HD + ks * 32 + quad * 8;
-      const float4 x0 = *reinterpret_cast<const float4*>(src);
-      const float4 x1 = *reinterpret_cast<const float4*>(src + 4);
-      v[0] = x0.x * a.qscale; v[1] = x0.y * a.qscale; v[2] = x0.z * a.qscale; v[3] = x0.w * a.qscale;
-      v[4] = x1.x * a.qscale; v[5] = x1.y * a.qscale; v[6] = x1.z * a.qscale; v[7] = x1.w * a.qscale;
-    }
-    split_pack8(v, qh[ks], ql[ks]);
-  }
-
+  // 1. issue the K chunk [keys, HD], the V^T chunk [HD, keys] and this wave's query rows
+  constexpr int KPIECES = (CKM * HD / 8 + 255) / 256;  // 16-byte pieces per thread, per matrix
+  u32x4 kv[KPIECES], vv[KPIECES];
   const uint16_t* Kg = a.kc + (long)g * a.Lcap * HD;
-  f32x4 s[CK / 16];
-#pragma unroll
-  for (int kt = 0; kt < CK / 16; ++kt) {
-    const int key = kbeg + kt * 16 + q;
-    u32x4 kv[HD / 32];
-#pragma unroll
-    for (int ks = 0; ks < HD / 32; ++ks) {
-      kv[ks] = u32x4{0u, 0u, 0u, 0u};
-      if (key < kend) kv[ks] = *reinterpret_cast<const u32x4*>(Kg + (long)key * HD + ks * 32 + quad * 8);
-    }
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < HD / 32; ++ks) {
-      acc = mfma(kv[ks], qh[ks], acc);
-      acc = mfma(kv[ks], ql[ks], acc);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (kt * 16 + quad * 4 + i >= nkeys) acc[i] = -INFINITY;
-    s[kt] = acc;
-  }
-  // softmax statistics per query row (column q), in the log2 domain
-  float m = -INFINITY;
-#pragma unroll
-  for (int kt = 0; kt < CK / 16; ++kt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) m = fmaxf(m, s[kt][i]);
-  m = fmaxf(m, __shfl_xor(m, 16));
-  m = fmaxf(m, __shfl_xor(m, 32));
-  float l = 0.f;
-#pragma unroll
-  for (int kt = 0; kt < CK / 16; ++kt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float p = exp2f(s[kt][i] - m);
-      s[kt][i] = p;
-      l += p;
-    }
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
-
-  // O^T = V^T P^T over the chunk
   const uint16_t* Vg = a.vt + (long)g * HD * a.Lcap;
-  f32x4 o[HD / 16];
 #pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < KPIECES; ++i) {
+    const int p = i * 256 + tid;
+    const int kr = p / (HD / 8), kc8 = p % (HD / 8);
+    kv[i] = u32x4{0u, 0u, 0u, 0u};
+    if (kr < nkeys) kv[i] = *reinterpret_cast<const u32x4*>(Kg + (long)(kbeg + kr) * HD + kc8 * 8);
+    const int vr = p / (CKM / 8), vc8 = p % (CKM / 8);
+    vv[i] = u32x4{0u, 0u, 0u, 0u};
+    if (vr < HD && vc8 * 8 < nkeys) vv[i] = *reinterpret_cast<const u32x4*>(Vg + (long)vr * a.Lcap + kbeg + vc8 * 8);
+  }
+  float4 qx[QTW][HD / 16];
 #pragma unroll
-  for (int kk = 0; kk < CK / 32; ++kk) {
-    float pv[8] = {s[2 * kk][0], s[2 * kk][1], s[2 * kk][2], s[2 * kk][3],
-                   s[2 * kk + 1][0], s[2 * kk + 1][1], s[2 * kk + 1][2], s[2 * kk + 1][3]};
-    u32x4 ph, pl;
-    split_pack8(pv, ph, pl);
-    const int k0 = kbeg + kk * 32 + quad * 4;  // keys k0..k0+3 and k0+16..k0+19
+  for (int j = 0; j < QTW; ++j) {
+    const int r = (w + 4 * j) * 16 + q;
+    const bool rv = r < R;
+    const int b = rv ? r % a.B : 0;
+    const int h = g * G + (rv ? r / a.B : 0);
 #pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) {
-      const uint16_t* vp = Vg + (long)(dt * 16 + q) * a.Lcap;
-      u32x2 v0 = {0u, 0u}, v1 = {0u, 0u};
-      if (k0 < kend) v0 = *reinterpret_cast<const u32x2*>(vp + k0);
-      if (k0 + 16 < kend) v1 = *reinterpret_cast<const u32x2*>(vp + k0 + 16);
-      // zero values of keys past the end (their p is 0, but stale memory may hold non-finite bits)
-      if (k0 + 4 > kend) {
-        const int nv = kend - k0;
-        if (nv <= 0) v0 = u32x2{0u, 0u};
-        else {
-          if (nv < 2) v0[0] &= 0xFFFFu;
-          if (nv < 3) v0[1] = 0u;
-          if (nv < 4) v0[1] &= 0xFFFFu;
-        }
-      }
-      if (k0 + 20 > kend) {
-        const int nv = kend - (k0 + 16);
-        if (nv <= 0) v1 = u32x2{0u, 0u};
-        else {
-          if (nv < 2) v1[0] &= 0xFFFFu;
-          if (nv < 3) v1[1] = 0u;
-          if (nv < 4) v1[1] &= 0xFFFFu;
-        }
-      }
-      const u32x4 av = {v0[0], v0[1], v1[0], v1[1]};
-      o[dt] = mfma(av, ph, o[dt]);
-      o[dt] = mfma(av, pl, o[dt]);
+    for (int ks = 0; ks < HD / 32; ++ks) {
+      const float* src = a.Q + (long)b * a.q_dim + h * HD + ks * 32 + quad * 8;
+      qx[j][2 * ks] = rv ? *reinterpret_cast<const float4*>(src) : make_float4(0.f, 0.f, 0.f, 0.f);
+      qx[j][2 * ks + 1] = rv ? *reinterpret_cast<const float4*>(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
-  if (rv) {
-    const long base = ((long)c * a.n_kv + g) * a.Rpad + r;
+  // 2. K/V to LDS (keys past the end become zeros)
 #pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt)
-      *reinterpret_cast<f32x4*>(a.opart + base * HD + dt * 16 + quad * 4) = o[dt];
-    if (quad == 0) a.ml[base] = make_float2(m, l);
+  for (int i = 0; i < KPIECES; ++i) {
+    const int p = i * 256 + tid;
+    const int kr = p / (HD / 8), kc8 = p % (HD / 8);
+    if (kr < CKM) *reinterpret_cast<u32x4*>(sK + kr * KP + kc8 * 8) = kv[i];
+    const int vr = p / (CKM / 8), vc8 = p % (CKM / 8);
+    u32x4 v = vv[i];
+    const int nv = nkeys - vc8 * 8;  // valid keys in this piece
+    if (nv < 8) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (2 * e >= nv) v[e] = 0u;
+        else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;
+      }
+    }
+    if (vr < HD) *reinterpret_cast<u32x4*>(sV + vr * VP + vc8 * 8) = v;
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int j = 0; j < QTW; ++j) {
+    const int qt = w + 4 * j;
+    if (qt * 16 >= R) break;  // wave-uniform
+    const int r = qt * 16 + q;
+    u32x4 qh[HD / 32], ql[HD / 32];
+#pragma unroll
+    for (int ks = 0; ks < HD / 32; ++ks) {
+      const float4 x0 = qx[j][2 * ks], x1 = qx[j][2 * ks + 1];
+      float v[8] = {x0.x * a.qscale, x0.y * a.qscale, x0.z * a.qscale, x0.w * a.qscale,
+                    x1.x * a.qscale, x1.y * a.qscale, x1.z * a.qscale, x1.w * a.qscale};
+      split_pack8(v, qh[ks], ql[ks]);
+    }
+    f32x4 s[CKM / 16];
+#pragma unroll
+    for (int kt = 0; kt < CKM / 16; ++kt) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        const u32x4 kf = *reinterpret_cast<const u32x4*>(sK + (kt * 16 + q) * KP + ks * 32 + quad * 8);
+        acc = mfma(kf, qh[ks], acc);
+        acc = mfma(kf, ql[ks], acc);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (kt * 16 + quad * 4 + i >= nkeys) acc[i] = -INFINITY;
+      s[kt] = acc;
+    }
+    // softmax statistics per query row (column q), in the log2 domain
+    float m = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < CKM / 16; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) m = fmaxf(m, s[kt][i]);
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    float l = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < CKM / 16; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p = exp2f(s[kt][i] - m);
+        s[kt][i] = p;
+        l += p;
+      }
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    // O^T = V^T P^T over the chunk
+    f32x4 o[HD / 16];
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < CKM / 32; ++kk) {
+      float pv[8] = {s[2 * kk][0], s[2 * kk][1], s[2 * kk][2], s[2 * kk][3],
+                     s[2 * kk + 1][0], s[2 * kk + 1][1], s[2 * kk + 1][2], s[2 * kk + 1][3]};
+      u32x4 ph, pl;
+      split_pack8(pv, ph, pl);
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt) {
+        const uint16_t* vp = sV + (dt * 16 + q) * VP + kk * 32 + quad * 4;
+        const u32x2 v0 = *reinterpret_cast<const u32x2*>(vp);       // keys kk*32 + 4*quad + 0..3
+        const u32x2 v1 = *reinterpret_cast<const u32x2*>(vp + 16);  // keys kk*32 + 16 + 4*quad + 0..3
+        const u32x4 av = {v0[0], v0[1], v1[0], v1[1]};
+        o[dt] = mfma(av, ph, o[dt]);
+        o[dt] = mfma(av, pl, o[dt]);
+      }
+    }
+    if (r < R) {
+      const long base = ((long)c * a.n_kv + g) * a.Rpad + r;
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt)
+        *reinterpret_cast<f32x4*>(a.opart + base * HD + dt * 16 + quad * 4) = o[dt];
+      if (quad == 0) a.ml[base] = make_float2(m, l);
+    }
   }
 }
 
-// combine the chunk partials: O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as the
-// A fragments of the output projection.  One thread per (query row, 8 consecutive dims).
+// combine the chunk partials of one query row r of KV head g:
+// O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as the A fragments of the output
+// projection.  Block (r, g); thread (chunk slot cs, 8 dims d0..d0+7).
 template <int HD, int CK>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
-  const int g = blockIdx.y;
-  const int idx = blockIdx.x * 256 + threadIdx.x;
-  const int r = idx / (HD / 8), d0 = (idx % (HD / 8)) * 8;
+  constexpr int DG = HD / 8, CS = 256 / DG;
+  __shared__ float s_red[256];
+  __shared__ float s_num[CS][HD];
+  const int r = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
   const int G = a.n_q / a.n_kv;
   const int R = G * a.B;
   if (r >= R) return;
-  const int nch = (a.params->L + a.B + CK - 1) / CK;
-  float M = -INFINITY;
-#pragma unroll 4
-  for (int c = 0; c < nch; ++c) M = fmaxf(M, a.ml[((long)c * a.n_kv + g) * a.Rpad + r].x);
+  const int nch = max(1, (a.params->L + CK - 1) / CK);  // the last chunk also holds the block keys
+  const float2* ml = a.ml + (long)g * a.Rpad + r;  // chunk c at ml[c * n_kv * Rpad]
+  const long mstride = (long)a.n_kv * a.Rpad;
+  // 1. M = max_c m_c
+  float m = -INFINITY;
+  for (int c = tid; c < nch; c += 256) m = fmaxf(m, ml[c * mstride].x);
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((tid & 63) == 0) s_red[tid >> 6] = m;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
+  // 2. weighted sums; chunk slots in a fixed order
+  const int dg = tid % DG, cs = tid / DG, d0 = dg * 8;
   float num[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float den = 0.f;
 #pragma unroll 4
-  for (int c = 0; c < nch; ++c) {
-    const long base = ((long)c * a.n_kv + g) * a.Rpad + r;
-    const float2 ml = a.ml[base];
-    const float wgt = exp2f(ml.x - M);
-    den += wgt * ml.y;
-    const float4 o0 = *reinterpret_cast<const float4*>(a.opart + base * HD + d0);
-    const float4 o1 = *reinterpret_cast<const float4*>(a.opart + base * HD + d0 + 4);
+  for (int c = cs; c < nch; c += CS) {
+    const float2 mc = ml[c * mstride];
+    const float wgt = exp2f(mc.x - M);
+    den += wgt * mc.y;
+    const float* op = a.opart + (((long)c * a.n_kv + g) * a.Rpad + r) * HD + d0;
+    const float4 o0 = *reinterpret_cast<const float4*>(op);
+    const float4 o1 = *reinterpret_cast<const float4*>(op + 4);
     num[0] += wgt * o0.x; num[1] += wgt * o0.y; num[2] += wgt * o0.z; num[3] += wgt * o0.w;
     num[4] += wgt * o1.x; num[5] += wgt * o1.y; num[6] += wgt * o1.z; num[7] += wgt * o1.w;
   }
-  const float inv = 1.0f / den;
+  __syncthreads();
 #pragma unroll
-  for (int e = 0; e < 8; ++e) num[e] *= inv;
-  const int b = r % a.B, h = g * G + r / a.B;
-  u32x4 hi, lo;
-  split_pack8(num, hi, lo);
-  const long fo = frag_off(b, h * HD + d0, a.oa_Kt) >> 3;
-  a.oa_hi[fo] = hi;
-  a.oa_lo[fo] = lo;
+  for (int e = 0; e < 8; ++e) s_num[cs][d0 + e] = num[e];
+  if (dg == 0) s_red[cs] = den;
+  __syncthreads();
+  if (tid < DG) {
+    float acc[8];
+    float dsum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+    for (int k = 0; k < CS; ++k) {
+      dsum += s_red[k];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += s_num[k][tid * 8 + e];
+    }
+    const float inv = 1.0f / dsum;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] *= inv;
+    const int b = r % a.B, h = g * G + r / a.B;
+    u32x4 hi, lo;
+    split_pack8(acc, hi, lo);
+    const long fo = frag_off(b, h * HD + tid * 8, a.oa_Kt) >> 3;
+    a.oa_hi[fo] = hi;
+    a.oa_lo[fo] = lo;
+  }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -724,9 +772,10 @@ void launch_embed(hipStream_t s, const uint16_t* embed, const int* ids, int voca
 }
 
 void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
-                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
-  hipLaunchKernelGGL(k_fuse, dim3((H + 511) / 512, n), dim3(64), (size_t)S * 1024, s, hidden, n, S, H, D, alpha,
-                     gain, ustats, ua_hi, ua_lo, n_max, mt_max);
+                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max,
+                 StepParams* params, int L) {
+  hipLaunchKernelGGL(k_fuse, dim3((H + 511) / 512, n, D), dim3(64), 0, s, hidden, n, S, H, alpha, gain, ustats,
+                     ua_hi, ua_lo, n_max, mt_max, params, L);
 }
 
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n, int H,
@@ -772,20 +821,21 @@ void launch_argmax_combine(hipStream_t s, const float* pmax, const int* pidx, in
 
 template <int HD>
 static void attn_hd(hipStream_t s, const AttnArgs& a, int chunk, int n_chunks, bool combine) {
-  const int threads = a.Rpad / 16 * 64;
   if (!combine) {
     const dim3 grid(n_chunks, a.n_kv);
-    switch (chunk) {
-      case 64: hipLaunchKernelGGL((k_attn<HD, 64>), grid, dim3(threads), 0, s, a); break;
-      case 128: hipLaunchKernelGGL((k_attn<HD, 128>), grid, dim3(threads), 0, s, a); break;
-      case 256: hipLaunchKernelGGL((k_attn<HD, 256>), grid, dim3(threads), 0, s, a); break;
+    const bool two = a.Rpad > 64;  // more than 4 query tiles: two per wave
+    if (chunk == 64) {
+      if (two) hipLaunchKernelGGL((k_attn<HD, 64, 2>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn<HD, 64, 1>), grid, dim3(256), 0, s, a);
+    } else {
+      if (two) hipLaunchKernelGGL((k_attn<HD, 128, 2>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn<HD, 128, 1>), grid, dim3(256), 0, s, a);
     }
   } else {
-    const dim3 grid((a.Rpad * (HD / 8) + 255) / 256, a.n_kv);
+    const dim3 grid(a.Rpad, a.n_kv);
     switch (chunk) {
       case 64: hipLaunchKernelGGL((k_attn_combine<HD, 64>), grid, dim3(256), 0, s, a); break;
-      case 128: hipLaunchKernelGGL((k_attn_combine<HD, 128>), grid, dim3(256), 0, s, a); break;
-      case 256: hipLaunchKernelGGL((k_attn_combine<HD, 256>), grid, dim3(256), 0, s, a); break;
+      default: hipLaunchKernelGGL((k_attn_combine<HD, 128>), grid, dim3(256), 0, s, a); break;
     }
   }
 }

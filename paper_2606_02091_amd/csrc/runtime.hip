@@ -81,6 +81,13 @@ struct dflare_handle {
   bool debug = false;
   float *dbg_hidden = nullptr, *dbg_logits = nullptr, *dbg_fused = nullptr;
   int dbg_fused_n = 0;
+  // captured draft blocks, keyed by the output buffer
+  struct BlockGraph {
+    int32_t* out;
+    hipGraphExec_t exec;
+  };
+  std::vector<BlockGraph> graphs;
+  bool use_graphs = true;
   // kernel timing
   int prof_kind = 0;
   std::vector<hipEvent_t> prof_ev;  // pairs
@@ -118,7 +125,10 @@ int dev_alloc(dflare_handle* h, T** p, size_t bytes) {
   return DFLARE_OK;
 }
 
+void drop_graphs(dflare_handle* h);
+
 void free_all(dflare_handle* h) {
+  drop_graphs(h);
   for (void* p : h->allocs) (void)hipFree(p);
   h->allocs.clear();
   for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
@@ -239,11 +249,13 @@ int build(dflare_handle* h, const dflare_weights* w) {
   h->p_down = make_plan("DOWN", Nt_down, 1, 16);
   h->p_lm = make_plan("LM", Nt_lm, 4, 4);
   h->p_kvt = make_plan("KVT", Nt_kvt, 1, 16);
+  if (const char* env = getenv("DFLARE_GRAPH")) h->use_graphs = atoi(env) != 0;
   if (const char* env = getenv("DFLARE_ATTN_CHUNK")) {
     int v = atoi(env);
-    if (v == 64 || v == 128 || v == 256) h->attn_chunk = v;
+    if (v == 64 || v == 128) h->attn_chunk = v;
   }
-  h->attn_nchunks = ceil_div((long)c.max_context + B, h->attn_chunk);
+  // chunk c holds keys [c*chunk, (c+1)*chunk); the last one also the B block keys
+  h->attn_nchunks = std::max(1, ceil_div((long)c.max_context, h->attn_chunk));
 
   // ---- packed weights
   h->s_qkv = (long)Nt_qkv * Kt_H * 64;
@@ -345,16 +357,13 @@ int build(dflare_handle* h, const dflare_weights* w) {
   return DFLARE_OK;
 }
 
-int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positions_host, int32_t* out) {
+// Every kernel of a draft block after the prologue.  The launch sequence and its arguments
+// depend only on the handle and `out`, so it can be captured once in a HIP graph and replayed.
+int enqueue_block_body(dflare_handle* h, int32_t* out) {
   const dflare_config& c = h->cfg;
   const int H = c.hidden, D = c.n_draft_layers, F = c.ffn, B = c.block_size, hd = c.head_dim;
   const int q = h->q_dim, kv = h->kv_dim;
   hipStream_t s = h->stream;
-  StepParams sp{};
-  sp.L = h->L;
-  sp.n_new = 0;
-  for (int b = 0; b < B; ++b) sp.pos[b] = positions_host ? positions_host[b] : h->L + b;
-  launch_prologue(s, h->params, sp, ids, h->ids, B);
   launch_embed(s, h->embed, h->ids, c.vocab, H, B, h->X, h->Xstats, h->g_attn, h->xa_hi, h->xa_lo);
 
   AttnArgs at{};
@@ -439,6 +448,50 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   return check_launch(h, "draft_block");
 }
 
+void drop_graphs(dflare_handle* h) {
+  for (auto& g : h->graphs) (void)hipGraphExecDestroy(g.exec);
+  h->graphs.clear();
+}
+
+int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positions_host, int32_t* out) {
+  const int B = h->cfg.block_size;
+  hipStream_t s = h->stream;
+  StepParams sp{};
+  sp.L = h->L;
+  sp.n_new = 0;
+  for (int b = 0; b < B; ++b) sp.pos[b] = positions_host ? positions_host[b] : h->L + b;
+  launch_prologue(s, h->params, sp, ids, h->ids, B);
+  // Graph replay needs a capturable (non-null) stream; debug capture and kernel timing
+  // insert extra work between the kernels, so they run eagerly.
+  const bool graph = h->use_graphs && s != nullptr && !h->debug && h->prof_kind == 0;
+  if (!graph) return enqueue_block_body(h, out);
+  for (auto& g : h->graphs)
+    if (g.out == out) {
+      HIP_OR_FAIL(h, hipGraphLaunch(g.exec, s));
+      return DFLARE_OK;
+    }
+  hipGraph_t graph_def = nullptr;
+  HIP_OR_FAIL(h, hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal));
+  const int rc = enqueue_block_body(h, out);
+  const hipError_t ce = hipStreamEndCapture(s, &graph_def);
+  if (rc != DFLARE_OK) {
+    if (graph_def) (void)hipGraphDestroy(graph_def);
+    return rc;
+  }
+  if (ce != hipSuccess) return fail(h, DFLARE_ERR_HIP, std::string("graph capture: ") + hipGetErrorString(ce));
+  hipGraphExec_t exec = nullptr;
+  const hipError_t ie = hipGraphInstantiate(&exec, graph_def, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(graph_def);
+  if (ie != hipSuccess) return fail(h, DFLARE_ERR_HIP, std::string("graph instantiate: ") + hipGetErrorString(ie));
+  if (h->graphs.size() >= 4) {  // keep the four most recent output buffers
+    (void)hipGraphExecDestroy(h->graphs.front().exec);
+    h->graphs.erase(h->graphs.begin());
+  }
+  h->graphs.push_back({out, exec});
+  HIP_OR_FAIL(h, hipGraphLaunch(exec, s));
+  return DFLARE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -499,13 +552,9 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   const dflare_config& c = h->cfg;
   const int H = c.hidden, D = c.n_draft_layers, S = c.n_target_layers;
   hipStream_t s = h->stream;
-  StepParams sp{};
-  sp.L = h->L;
-  sp.n_new = n_new;
-  launch_prologue(s, h->params, sp, nullptr, nullptr, 0);
   prof_mark(h, DFLARE_K_FUSE, true);
   launch_fuse(s, (const uint16_t*)target_hidden, n_new, S, H, D, h->alpha, h->g_fuse, h->Ustats, h->ua_hi,
-              h->ua_lo, c.max_new, h->mt_max);
+              h->ua_lo, c.max_new, h->mt_max, h->params, h->L);
   prof_mark(h, DFLARE_K_FUSE, false);
   GemmArgs a = gemm_args(h, h->w_kvt, 2 * h->kv_dim / 16, H / 32);
   a.w_layer_stride = h->s_kvt;
@@ -695,7 +744,7 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches) {
 
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count) {
   if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
-  const int32_t v[2] = {2 + 6 * h->cfg.n_draft_layers + 2, 3};
+  const int32_t v[2] = {2 + 6 * h->cfg.n_draft_layers + 2, 2};
   for (int i = 0; i < count && i < 2; ++i) out[i] = v[i];
   return DFLARE_OK;
 }

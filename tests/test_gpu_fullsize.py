@@ -1,0 +1,84 @@
+"""GPU parity at the workloads' full sizes, in the launch configuration bench.py times.
+
+For each model shape (Qwen3-8B, Qwen3-4B and GPT-OSS-20B shaped drafts at their full
+context lengths) the library and the fp64 oracle prefill the same seeded context in
+512-row appends, then run draft steps.  Checked against the oracle: the whole
+context K/V cache of every draft layer, the block rows after every layer, the logits
+and the draft tokens (the bar of tests/parity.py).  The bench's configuration --
+a non-default stream, the draft block replayed as a HIP graph -- must then produce
+the very same tokens, bitwise, as the eager debug run.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_02091_amd import dflare as dfl
+from paper_2606_02091_amd import synth
+import parity as P
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU container
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+NAMES = os.environ.get("DFLARE_FULLSIZE", "qwen3_8b,qwen3_4b,gpt_oss_20b").split(",")
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", NAMES)
+def test_fullsize_parity(name):
+    cfg = synth.CONFIGS[name]
+    L = cfg.context
+    print(f"[fullsize] {name}: generating weights", flush=True)
+    w, lg = P.weights_for(cfg)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        model = dfl.DraftModel(cfg, w, lg, max_context=L + 64, max_new=512)
+        orc = P.oracle_for(cfg, w, lg, L + 64)
+        for s in range(0, L, 512):
+            n = min(512, L - s)
+            rows = synth.hidden_rows(cfg, s, n)
+            model.fuse_append(dfl.bf16_tensor(rows))
+            orc.append(rows)
+        print(f"[fullsize] {name}: context {L} appended", flush=True)
+        side.synchronize()
+        for i in range(cfg.n_draft_layers):
+            for what, ref in ((dfl.DBG_KCACHE, orc.k_cache[i]), (dfl.DBG_VCACHE, orc.v_cache[i])):
+                got = dfl.dflare_debug_read(model.h, what, i, (L, cfg.n_kv_heads, cfg.head_dim))
+                e = P.relinf(got, ref)
+                assert e <= P.REL_TOL, (name, i, what, e)
+        ids = synth.block_ids(cfg, step=0)
+        ids_t = torch.from_numpy(ids).cuda()
+        out = torch.empty(cfg.block_size, dtype=torch.int32, device="cuda")
+        for step in range(2):
+            # bench configuration first: graph replay on the side stream, no debug capture
+            model.draft_block(ids_t, out)
+            model.draft_block(ids_t, out)
+            side.synchronize()
+            graph_tokens = out.cpu().numpy().copy()
+            dfl.dflare_debug_capture(model.h, True)
+            eager = model.draft_block(ids_t).cpu().numpy()
+            side.synchronize()
+            dfl.dflare_debug_capture(model.h, False)
+            assert np.array_equal(graph_tokens, eager)
+            ref = orc.draft_block(ids)
+            print(f"[fullsize] {name}: step {step} oracle done", flush=True)
+            for i in range(cfg.n_draft_layers):
+                g = dfl.dflare_debug_read(model.h, dfl.DBG_HIDDEN, i, (cfg.block_size, cfg.hidden))
+                e = P.relinf(g, ref["hidden"][i])
+                assert e <= P.REL_TOL, (name, step, i, e)
+            zl = dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0, (cfg.block_size, cfg.vocab))
+            e = P.relinf(zl, ref["logits"])
+            assert e <= P.REL_TOL, (name, step, "logits", e)
+            stats = P.check_tokens(eager, ref["logits"])
+            print(f"[fullsize] {name}: step {step} logits rel err {e:.2e} tokens {stats}", flush=True)
+            # next step: append accepted rows, as in the bench's draft loop
+            n = int(synth.append_sizes(1, seed=10 + step)[0])
+            rows = synth.hidden_rows(cfg, L + 100 * step, n, seed=4)
+            model.fuse_append(dfl.bf16_tensor(rows))
+            orc.append(rows)
+            ids = synth.block_ids(cfg, step=step + 1)
+            ids_t = torch.from_numpy(ids).cuda()
+        model.close()

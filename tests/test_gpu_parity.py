@@ -265,3 +265,32 @@ def test_context_full_and_bad_sizes_leave_state():
     k1 = dfl.dflare_debug_read(model.h, dfl.DBG_KCACHE, 0, (16, cfg.n_kv_heads, cfg.head_dim))
     assert np.array_equal(k0, k1)
     model.close()
+
+
+def test_graph_replay_matches_eager():
+    """The captured draft block (non-default stream) equals the eager one bitwise, on every
+    replay, with eager work (appends, syncs, an eager block) between the replays."""
+    cfg = CASES["gqa8_hd64"][0]
+    w, lg = P.weights_for(cfg)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        model = dfl.DraftModel(cfg, w, lg, max_context=400)
+        rows = synth.hidden_rows(cfg, 0, 300)
+        for s in range(0, 300, 16):
+            model.fuse_append(dev(np.ascontiguousarray(rows[:, s:s + 16])))
+        ids = ids_tensor(synth.block_ids(cfg, step=7))
+        out = torch.empty(cfg.block_size, dtype=torch.int32, device="cuda")
+        outs = []
+        for k in range(4):
+            model.draft_block(ids, out)          # graph captured on the first call, replayed after
+            side.synchronize()
+            outs.append(out.cpu().clone())
+            extra = synth.hidden_rows(cfg, 300 + k, 1)
+            model.fuse_append(dev(extra))          # eager work between replays
+            model.truncate(300)
+        dfl.dflare_debug_capture(model.h, True)  # debug capture runs the block eagerly
+        eager = model.draft_block(ids).cpu()
+        side.synchronize()
+    for o in outs:
+        assert torch.equal(o, eager)
+    model.close()
