@@ -43,6 +43,7 @@ struct EpiArgs {
   int n_stat_out;
   uint16_t* kc;           // K cache of the layer (QKV) or of layer 0 (KVT): [n_kv, Lcap, hd]
   uint16_t* vt;           // V cache, transposed: [n_kv, hd, Lcap]
+  long plane;             // elements from the hi plane of a cache to its lo plane
   long cache_layer_stride;  // elements between consecutive layers' caches (KVT)
   int Lcap;
   int hd;
@@ -81,8 +82,9 @@ struct GemmArgs {
 struct AttnArgs {
   const StepParams* params;
   const float* Q;          // [B, q_dim] fp32, rotated
-  const uint16_t* kc;      // [n_kv, Lcap, hd] of the layer
+  const uint16_t* kc;      // [n_kv, Lcap, hd] of the layer (hi plane; lo plane at +plane)
   const uint16_t* vt;      // [n_kv, hd, Lcap]
+  long plane;
   int B, n_q, n_kv, q_dim, Lcap, Rpad;
   float qscale;            // log2(e) / sqrt(hd)
   float* opart;            // [chunks, n_kv, Rpad, hd]

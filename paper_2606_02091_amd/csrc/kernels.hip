@@ -442,14 +442,21 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm(GemmArgs a) {
           const float2 cs = e.rope[(long)pos * half + m];
           const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
           if (valid) {
-            if (region == 0)
+            if (region == 0) {
               e.out[(long)row * e.ldo + head * e.hd + dim] = y;
-            else
-              kc[((long)head * e.Lcap + slot) * e.hd + dim] = (uint16_t)f2bf(y);
+            } else {  // the cache keeps y as two bf16 planes, y ~= hi + lo
+              const long ix = ((long)head * e.Lcap + slot) * e.hd + dim;
+              const uint32_t hb = f2bf(y);
+              kc[ix] = (uint16_t)hb;
+              kc[ix + e.plane] = (uint16_t)f2bf(y - bf2f(hb));
+            }
           }
         } else if (valid) {
           const int dim = jj * 16 + col;
-          vt[((long)head * e.hd + dim) * e.Lcap + slot] = (uint16_t)f2bf(x);
+          const long ix = ((long)head * e.hd + dim) * e.Lcap + slot;
+          const uint32_t hb = f2bf(x);
+          vt[ix] = (uint16_t)hb;
+          vt[ix + e.plane] = (uint16_t)f2bf(x - bf2f(hb));
         }
       }
     }
@@ -526,20 +533,26 @@ __global__ __launch_bounds__(256) void k_argmax_combine(const float* pmax, const
 
 // ------------------------------------------------------------------------------------------
 // block attention, split over the key axis (Sec. 3.2: no mask, every block row sees the
-// whole context and the whole block).  Block (chunk c, KV head g): the CK keys of the chunk
-// (K rows and V^T rows, the block's own B keys sit in cache slots L..L+B-1) are copied to LDS
-// with every load in flight at once; then each wave takes 16-row query tiles
-// r = tile*16 + lane%16 of the G*B rows that share head g (r -> query head g*G + r/B, block
-// position r%B).  Scores are formed transposed, S^T = K Q^T, so that the probabilities land
-// in exactly the B-operand layout of the P V product and never leave registers.
+// whole context and the whole block).  Block (chunk c, KV head g) of 8 waves: chunk c holds
+// keys [c*CK, (c+1)*CK) of the context, the last chunk also the B block keys (cache slots
+// L..L+B-1).  K rows and V^T rows of the chunk, both bf16 planes (hi, lo), are copied to LDS
+// with every load in flight at once (16-byte pieces, XOR-swizzled columns so that the
+// fragment reads of 16 different rows hit different banks).  Wave w then takes query tile w:
+// rows r = w*16 + lane%16 of the G*B rows that share head g (r -> query head g*G + r/B, block
+// position r%B).  Scores are formed transposed, S^T = K Q^T, so that the probabilities land in
+// exactly the B-operand layout of the P V product and never leave registers.  Products of
+// two hi/lo pairs keep the three terms above 2^-16 relative: hi*hi + hi*lo + lo*hi.
 // ------------------------------------------------------------------------------------------
-template <int HD, int CK, int QTW>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  constexpr int CKM = CK + 32;  // the last chunk also holds the B <= 16 block keys
-  constexpr int KP = HD + 8;    // padded LDS row of K (elements): spreads rows over the banks
-  constexpr int VP = CKM + 8;   // padded LDS row of V^T
-  __shared__ __attribute__((aligned(16))) uint16_t sK[CKM * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[HD * VP];
+template <int HD, int CK>
+__global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
+  constexpr int CKM = CK + 32;   // keys held by a block (room for the B <= 16 block keys)
+  constexpr int KC = HD / 8;     // 16-byte columns of a K row
+  constexpr int VC = CKM / 8;    // 16-byte columns of a V^T row (a multiple of 4)
+  constexpr int KPC = 2 * CKM * KC, VPC = 2 * HD * VC;  // pieces of both planes
+  constexpr int PER = (KPC + VPC) / 512;                 // pieces per thread
+  static_assert(KPC % 512 == 0 && VPC % 512 == 0, "piece counts must split evenly over the block");
+  __shared__ u32x4 sK[2][CKM * KC];  // (row r, column c) at r*KC + (c ^ (r & 7))
+  __shared__ u32x4 sV[2][HD * VC];   // (row d, column c) at d*VC + (c ^ (d & 3))
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int quad = lane >> 4, q = lane & 15;
   const int g = blockIdx.y, c = blockIdx.x;
@@ -552,129 +565,143 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int G = a.n_q / a.n_kv;
   const int R = G * a.B;
 
-  // 1. issue the K chunk [keys, HD], the V^T chunk [HD, keys] and this wave's query rows
-  constexpr int KPIECES = (CKM * HD / 8 + 255) / 256;  // 16-byte pieces per thread, per matrix
-  u32x4 kv[KPIECES], vv[KPIECES];
-  const uint16_t* Kg = a.kc + (long)g * a.Lcap * HD;
-  const uint16_t* Vg = a.vt + (long)g * HD * a.Lcap;
+  // 1. issue every piece of the chunk and this wave's query row
+  u32x4 pc[PER];
 #pragma unroll
-  for (int i = 0; i < KPIECES; ++i) {
-    const int p = i * 256 + tid;
-    const int kr = p / (HD / 8), kc8 = p % (HD / 8);
-    kv[i] = u32x4{0u, 0u, 0u, 0u};
-    if (kr < nkeys) kv[i] = *reinterpret_cast<const u32x4*>(Kg + (long)(kbeg + kr) * HD + kc8 * 8);
-    const int vr = p / (CKM / 8), vc8 = p % (CKM / 8);
-    vv[i] = u32x4{0u, 0u, 0u, 0u};
-    if (vr < HD && vc8 * 8 < nkeys) vv[i] = *reinterpret_cast<const u32x4*>(Vg + (long)vr * a.Lcap + kbeg + vc8 * 8);
+  for (int i = 0; i < PER; ++i) {
+    const int p = i * 512 + tid;
+    pc[i] = u32x4{0u, 0u, 0u, 0u};
+    if (p < KPC) {  // uniform for a given i
+      const int pl = p / (CKM * KC), rem = p % (CKM * KC);
+      const int r = rem / KC, col = rem % KC;
+      if (r < nkeys)
+        pc[i] = *reinterpret_cast<const u32x4*>(a.kc + pl * a.plane + ((long)g * a.Lcap + kbeg + r) * HD + col * 8);
+    } else {
+      const int pv = p - KPC;
+      const int pl = pv / (HD * VC), rem = pv % (HD * VC);
+      const int d = rem / VC, col = rem % VC;
+      if (col * 8 < nkeys)
+        pc[i] = *reinterpret_cast<const u32x4*>(a.vt + pl * a.plane + ((long)g * HD + d) * a.Lcap + kbeg + col * 8);
+    }
   }
-  float4 qx[QTW][HD / 16];
-#pragma unroll
-  for (int j = 0; j < QTW; ++j) {
-    const int r = (w + 4 * j) * 16 + q;
-    const bool rv = r < R;
+  const int r = w * 16 + q;
+  const bool active = w * 16 < R;  // wave-uniform
+  const bool rv = r < R;
+  float4 qx[HD / 16];
+  {
     const int b = rv ? r % a.B : 0;
     const int h = g * G + (rv ? r / a.B : 0);
 #pragma unroll
     for (int ks = 0; ks < HD / 32; ++ks) {
       const float* src = a.Q + (long)b * a.q_dim + h * HD + ks * 32 + quad * 8;
-      qx[j][2 * ks] = rv ? *reinterpret_cast<const float4*>(src) : make_float4(0.f, 0.f, 0.f, 0.f);
-      qx[j][2 * ks + 1] = rv ? *reinterpret_cast<const float4*>(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+      qx[2 * ks] = (active && rv) ? *reinterpret_cast<const float4*>(src) : make_float4(0.f, 0.f, 0.f, 0.f);
+      qx[2 * ks + 1] = (active && rv) ? *reinterpret_cast<const float4*>(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   }
-  // 2. K/V to LDS (keys past the end become zeros)
+  // 2. pieces to LDS (keys past the end become zeros)
 #pragma unroll
-  for (int i = 0; i < KPIECES; ++i) {
-    const int p = i * 256 + tid;
-    const int kr = p / (HD / 8), kc8 = p % (HD / 8);
-    if (kr < CKM) *reinterpret_cast<u32x4*>(sK + kr * KP + kc8 * 8) = kv[i];
-    const int vr = p / (CKM / 8), vc8 = p % (CKM / 8);
-    u32x4 v = vv[i];
-    const int nv = nkeys - vc8 * 8;  // valid keys in this piece
-    if (nv < 8) {
+  for (int i = 0; i < PER; ++i) {
+    const int p = i * 512 + tid;
+    if (p < KPC) {
+      const int pl = p / (CKM * KC), rem = p % (CKM * KC);
+      const int rr = rem / KC, col = rem % KC;
+      sK[pl][rr * KC + (col ^ (rr & 7))] = pc[i];
+    } else {
+      const int pv = p - KPC;
+      const int pl = pv / (HD * VC), rem = pv % (HD * VC);
+      const int d = rem / VC, col = rem % VC;
+      u32x4 v = pc[i];
+      const int nv = nkeys - col * 8;  // valid keys in this piece
+      if (nv < 8) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (2 * e >= nv) v[e] = 0u;
-        else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;
+        for (int e = 0; e < 4; ++e) {
+          if (2 * e >= nv) v[e] = 0u;
+          else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;
+        }
       }
+      sV[pl][d * VC + (col ^ (d & 3))] = v;
     }
-    if (vr < HD) *reinterpret_cast<u32x4*>(sV + vr * VP + vc8 * 8) = v;
   }
   __syncthreads();
+  if (!active) return;
 
+  u32x4 qh[HD / 32], ql[HD / 32];
 #pragma unroll
-  for (int j = 0; j < QTW; ++j) {
-    const int qt = w + 4 * j;
-    if (qt * 16 >= R) break;  // wave-uniform
-    const int r = qt * 16 + q;
-    u32x4 qh[HD / 32], ql[HD / 32];
+  for (int ks = 0; ks < HD / 32; ++ks) {
+    const float4 x0 = qx[2 * ks], x1 = qx[2 * ks + 1];
+    float v[8] = {x0.x * a.qscale, x0.y * a.qscale, x0.z * a.qscale, x0.w * a.qscale,
+                  x1.x * a.qscale, x1.y * a.qscale, x1.z * a.qscale, x1.w * a.qscale};
+    split_pack8(v, qh[ks], ql[ks]);
+  }
+  f32x4 s[CKM / 16];
+#pragma unroll
+  for (int kt = 0; kt < CKM / 16; ++kt) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    const int rr = kt * 16 + q;
 #pragma unroll
     for (int ks = 0; ks < HD / 32; ++ks) {
-      const float4 x0 = qx[j][2 * ks], x1 = qx[j][2 * ks + 1];
-      float v[8] = {x0.x * a.qscale, x0.y * a.qscale, x0.z * a.qscale, x0.w * a.qscale,
-                    x1.x * a.qscale, x1.y * a.qscale, x1.z * a.qscale, x1.w * a.qscale};
-      split_pack8(v, qh[ks], ql[ks]);
+      const int slot = rr * KC + ((ks * 4 + quad) ^ (rr & 7));
+      const u32x4 kh = sK[0][slot], kl = sK[1][slot];
+      acc = mfma(kh, qh[ks], acc);
+      acc = mfma(kh, ql[ks], acc);
+      acc = mfma(kl, qh[ks], acc);
     }
-    f32x4 s[CKM / 16];
 #pragma unroll
-    for (int kt = 0; kt < CKM / 16; ++kt) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < 4; ++i)
+      if (kt * 16 + quad * 4 + i >= nkeys) acc[i] = -INFINITY;
+    s[kt] = acc;
+  }
+  // softmax statistics per query row (column q), in the log2 domain
+  float m = -INFINITY;
 #pragma unroll
-      for (int ks = 0; ks < HD / 32; ++ks) {
-        const u32x4 kf = *reinterpret_cast<const u32x4*>(sK + (kt * 16 + q) * KP + ks * 32 + quad * 8);
-        acc = mfma(kf, qh[ks], acc);
-        acc = mfma(kf, ql[ks], acc);
-      }
+  for (int kt = 0; kt < CKM / 16; ++kt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (kt * 16 + quad * 4 + i >= nkeys) acc[i] = -INFINITY;
-      s[kt] = acc;
+    for (int i = 0; i < 4; ++i) m = fmaxf(m, s[kt][i]);
+  m = fmaxf(m, __shfl_xor(m, 16));
+  m = fmaxf(m, __shfl_xor(m, 32));
+  float l = 0.f;
+#pragma unroll
+  for (int kt = 0; kt < CKM / 16; ++kt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float p = exp2f(s[kt][i] - m);
+      s[kt][i] = p;
+      l += p;
     }
-    // softmax statistics per query row (column q), in the log2 domain
-    float m = -INFINITY;
+  l += __shfl_xor(l, 16);
+  l += __shfl_xor(l, 32);
+  // O^T = V^T P^T over the chunk
+  f32x4 o[HD / 16];
 #pragma unroll
-    for (int kt = 0; kt < CKM / 16; ++kt)
+  for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const u32x2* v2h = reinterpret_cast<const u32x2*>(sV[0]);
+  const u32x2* v2l = reinterpret_cast<const u32x2*>(sV[1]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) m = fmaxf(m, s[kt][i]);
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
-    float l = 0.f;
+  for (int kk = 0; kk < CKM / 32; ++kk) {
+    float pv[8] = {s[2 * kk][0], s[2 * kk][1], s[2 * kk][2], s[2 * kk][3],
+                   s[2 * kk + 1][0], s[2 * kk + 1][1], s[2 * kk + 1][2], s[2 * kk + 1][3]};
+    u32x4 ph, pl;
+    split_pack8(pv, ph, pl);
+    const int c0 = kk * 4 + (quad >> 1), half = quad & 1;  // keys kk*32 + 4*quad + 0..3 (+16)
 #pragma unroll
-    for (int kt = 0; kt < CKM / 16; ++kt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = exp2f(s[kt][i] - m);
-        s[kt][i] = p;
-        l += p;
-      }
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    // O^T = V^T P^T over the chunk
-    f32x4 o[HD / 16];
-#pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < CKM / 32; ++kk) {
-      float pv[8] = {s[2 * kk][0], s[2 * kk][1], s[2 * kk][2], s[2 * kk][3],
-                     s[2 * kk + 1][0], s[2 * kk + 1][1], s[2 * kk + 1][2], s[2 * kk + 1][3]};
-      u32x4 ph, pl;
-      split_pack8(pv, ph, pl);
-#pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) {
-        const uint16_t* vp = sV + (dt * 16 + q) * VP + kk * 32 + quad * 4;
-        const u32x2 v0 = *reinterpret_cast<const u32x2*>(vp);       // keys kk*32 + 4*quad + 0..3
-        const u32x2 v1 = *reinterpret_cast<const u32x2*>(vp + 16);  // keys kk*32 + 16 + 4*quad + 0..3
-        const u32x4 av = {v0[0], v0[1], v1[0], v1[1]};
-        o[dt] = mfma(av, ph, o[dt]);
-        o[dt] = mfma(av, pl, o[dt]);
-      }
+    for (int dt = 0; dt < HD / 16; ++dt) {
+      const int d = dt * 16 + q;
+      const int i0 = (d * VC + (c0 ^ (d & 3))) * 2 + half;
+      const int i1 = (d * VC + ((c0 + 2) ^ (d & 3))) * 2 + half;
+      const u32x2 h0 = v2h[i0], h1 = v2h[i1], l0 = v2l[i0], l1 = v2l[i1];
+      const u32x4 vh = {h0[0], h0[1], h1[0], h1[1]};
+      const u32x4 vl = {l0[0], l0[1], l1[0], l1[1]};
+      o[dt] = mfma(vh, ph, o[dt]);
+      o[dt] = mfma(vh, pl, o[dt]);
+      o[dt] = mfma(vl, ph, o[dt]);
     }
-    if (r < R) {
-      const long base = ((long)c * a.n_kv + g) * a.Rpad + r;
+  }
+  if (rv) {
+    const long base = ((long)c * a.n_kv + g) * a.Rpad + r;
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt)
-        *reinterpret_cast<f32x4*>(a.opart + base * HD + dt * 16 + quad * 4) = o[dt];
-      if (quad == 0) a.ml[base] = make_float2(m, l);
-    }
+    for (int dt = 0; dt < HD / 16; ++dt)
+      *reinterpret_cast<f32x4*>(a.opart + base * HD + dt * 16 + quad * 4) = o[dt];
+    if (quad == 0) a.ml[base] = make_float2(m, l);
   }
 }
 
@@ -823,20 +850,12 @@ template <int HD>
 static void attn_hd(hipStream_t s, const AttnArgs& a, int chunk, int n_chunks, bool combine) {
   if (!combine) {
     const dim3 grid(n_chunks, a.n_kv);
-    const bool two = a.Rpad > 64;  // more than 4 query tiles: two per wave
-    if (chunk == 64) {
-      if (two) hipLaunchKernelGGL((k_attn<HD, 64, 2>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_attn<HD, 64, 1>), grid, dim3(256), 0, s, a);
-    } else {
-      if (two) hipLaunchKernelGGL((k_attn<HD, 128, 2>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_attn<HD, 128, 1>), grid, dim3(256), 0, s, a);
-    }
+    if (chunk == 64) hipLaunchKernelGGL((k_attn<HD, 64>), grid, dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((k_attn<HD, 128>), grid, dim3(512), 0, s, a);
   } else {
     const dim3 grid(a.Rpad, a.n_kv);
-    switch (chunk) {
-      case 64: hipLaunchKernelGGL((k_attn_combine<HD, 64>), grid, dim3(256), 0, s, a); break;
-      default: hipLaunchKernelGGL((k_attn_combine<HD, 128>), grid, dim3(256), 0, s, a); break;
-    }
+    if (chunk == 64) hipLaunchKernelGGL((k_attn_combine<HD, 64>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_combine<HD, 128>), grid, dim3(256), 0, s, a);
   }
 }
 

@@ -58,6 +58,7 @@ struct dflare_handle {
   // context cache
   uint16_t *kc = nullptr, *vt = nullptr;
   long cache_layer_stride = 0;
+  long cache_plane = 0;
   float2* rope = nullptr;
   // step scratch
   StepParams* params = nullptr;
@@ -186,6 +187,7 @@ GemmArgs gemm_args(const dflare_handle* h, const u32x4* W, int Nt, int Kt) {
   a.eps = h->cfg.rms_eps;
   a.e.params = h->params;
   a.e.Lcap = h->Lcap;
+  a.e.plane = h->cache_plane;
   a.e.hd = h->cfg.head_dim;
   a.e.rope = h->rope;
   a.e.B = h->cfg.block_size;
@@ -311,7 +313,9 @@ int build(dflare_handle* h, const dflare_weights* w) {
   HIP_OR_FAIL(h, hipMemcpyAsync(h->alpha, h->alpha_host.data(), (size_t)D * S * 4, hipMemcpyHostToDevice, s));
 
   // ---- context cache, rotary table
-  h->cache_layer_stride = (long)c.n_kv_heads * h->Lcap * hd;
+  // per layer: K (or V^T) as two bf16 planes, hi then lo (value ~= hi + lo)
+  h->cache_plane = (long)c.n_kv_heads * h->Lcap * hd;
+  h->cache_layer_stride = 2 * h->cache_plane;
   TRY(dev_alloc(h, &h->kc, (size_t)h->cache_layer_stride * D * 2));
   TRY(dev_alloc(h, &h->vt, (size_t)h->cache_layer_stride * D * 2));
   HIP_OR_FAIL(h, hipMemsetAsync(h->kc, 0, (size_t)h->cache_layer_stride * D * 2, s));
@@ -374,6 +378,7 @@ int enqueue_block_body(dflare_handle* h, int32_t* out) {
   at.n_kv = c.n_kv_heads;
   at.q_dim = q;
   at.Lcap = h->Lcap;
+  at.plane = h->cache_plane;
   at.Rpad = h->Rpad;
   at.qscale = (float)(1.4426950408889634 / sqrt((double)hd));
   at.opart = h->opart;
@@ -706,10 +711,11 @@ int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, in
           for (int d = 0; d < hd; ++d) {
             const size_t ix = (what == DFLARE_DBG_KCACHE) ? ((size_t)g * h->Lcap + p) * hd + d
                                                           : ((size_t)g * hd + d) * h->Lcap + p;
-            uint32_t bits = (uint32_t)raw[ix] << 16;
-            float f;
-            memcpy(&f, &bits, 4);
-            host_out[((size_t)p * nkv + g) * hd + d] = f;
+            const uint32_t hb = (uint32_t)raw[ix] << 16, lb = (uint32_t)raw[ix + h->cache_plane] << 16;
+            float fh, fl;
+            memcpy(&fh, &hb, 4);
+            memcpy(&fl, &lb, 4);
+            host_out[((size_t)p * nkv + g) * hd + d] = fh + fl;
           }
       return DFLARE_OK;
     }
