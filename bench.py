@@ -39,7 +39,23 @@ def parse():
     ap.add_argument("--cpu-context", type=int, default=256,
                     help="context rows of the oracle's timed sample")
     ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
+
+
+def calibrate_copy():
+    """A plain device-to-device copy of known size: the byte counters of the profiler
+    read against it give the scale from counter units to bytes."""
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "launches": 3}), flush=True)
 
 
 def kernel_bytes(cfg, L, n_mean):
@@ -58,8 +74,28 @@ def kernel_bytes(cfg, L, n_mean):
     }
 
 
+def counter_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` measured with rocprofv3 byte counters, if the
+    recorded measurement belongs to the kernel source of this build; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_counters_qwen3_8b.json")
+    src = os.path.join(ROOT, "paper_2606_02091_amd", "csrc", "kernels.hip")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except (OSError, ValueError):
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    if rec.get("kernels_hip_sha256_16") != sha or k is None:
+        return None
+    return int(k["fetch_kib"] * 1024 * rec["fetch_scale"] + k["write_kib"] * 1024 * rec["write_scale"])
+
+
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build runs the draft step on one GPU only; "
@@ -166,7 +202,8 @@ def main():
                                f"L={L}, B={B}, batch 1, n_new~U{{1..16}}",
                    "global_batch": 1, "seq_len": L, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(d["achieved_GBs"], 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(d["achieved_GBs"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(d["achieved_GBs"] / HBM_PEAK_GBS, 4),
+                     "traffic": counter_traffic(dom),
                      "kernel": dom, "bytes_per_launch": d["bytes_per_launch"], "avg_us": d["avg_us"]},
         "step_roofline": {"bytes_per_step": int(step_bytes), "achieved_GBs": round(step_gbs, 1),
                           "frac": round(step_gbs / HBM_PEAK_GBS, 4)},
