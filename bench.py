@@ -9,9 +9,11 @@ SwiGLU 12288, vocab 151936, D = 8 draft layers fusing S = 36 target layers),
 L = 4096, batch 1.  Weights and inputs are seeded synthetic data (no trained
 weights exist here); all inputs are resident in HBM before the timed region.
 
-Prints one JSON line.  Per-kernel durations come from hipEvents placed by the
-library around the launches of one kernel kind at a time (a separate pass after
-the timed region, so the headline number carries no event overhead).
+The draft block runs as one persistent launch (its phases wait at grid barriers),
+fuse_append as two kernels.  Prints one JSON line.  Per-kernel durations come from
+hipEvents placed by the library around the launches of one kernel kind at a time (a
+separate pass after the timed region, so the headline number carries no event
+overhead); per-phase times come from the kernel's own wall-clock trace.
 """
 from __future__ import annotations
 
@@ -63,6 +65,7 @@ def kernel_bytes(cfg, L, n_mean):
     H, F, V, D, S = cfg.hidden, cfg.ffn, cfg.vocab, cfg.n_draft_layers, cfg.n_target_layers
     q, kv = cfg.q_dim, cfg.kv_dim
     return {
+        "draft_block": cfg.block_bytes(L),    # every draft-layer weight, LM head, context K/V
         "qkv": (q + 2 * kv) * H * 2,          # W_Q, W_K^d, W_V^d of one layer
         "attn": 2 * L * kv * 2,               # context K and V of one layer
         "o": H * q * 2,
@@ -111,7 +114,7 @@ def main():
     cfg = synth.CONFIGS[args.config]
     L, B, S, H = cfg.context, cfg.block_size, cfg.n_target_layers, cfg.hidden
     torch.cuda.set_device(0)
-    # a non-default stream (default priority): the library replays its draft block as a HIP graph
+    # a non-default stream of default priority, as a serving loop would use
     side = torch.cuda.Stream()
     torch.cuda.set_stream(side)
     t0 = time.time()
@@ -163,24 +166,32 @@ def main():
     torch.cuda.synchronize()
     block_ms = e0.elapsed_time(e1) / args.steps
 
-    # per-kernel durations (hipEvents in the library, one kind per pass)
+    # per-kernel durations (hipEvents in the library, one kind per pass).  The kernels of a
+    # step: the persistent draft-block kernel, fusion and context K/V projection.
     kb = kernel_bytes(cfg, L, n_mean)
-    kinds = {"qkv": dfl.K_QKV, "attn": dfl.K_ATTN, "o": dfl.K_O, "gate_up": dfl.K_GATE_UP,
-             "down": dfl.K_DOWN, "lm_head": dfl.K_LM_HEAD, "fuse": dfl.K_FUSE, "kv_t": dfl.K_KV_T}
-    kern = {}
-    for name, kind in kinds.items():
-        dfl.dflare_profile_begin(h, kind)
-        for k in range(args.profile_steps):
-            step(k)
-        tot, launches = dfl.dflare_profile_end(h)
-        avg_us = 1000.0 * tot / max(launches, 1)
-        per_step_us = 1000.0 * tot / args.profile_steps
-        gbs = kb[name] / (avg_us * 1e-6) / 1e9 if avg_us > 0 else 0.0
-        kern[name] = {"avg_us": round(avg_us, 3), "launches_per_step": launches / args.profile_steps,
-                      "us_per_step": round(per_step_us, 2), "bytes_per_launch": int(kb[name]),
-                      "achieved_GBs": round(gbs, 1)}
+
+    def profile(kinds):
+        res = {}
+        for name, kind in kinds.items():
+            dfl.dflare_profile_begin(h, kind)
+            for k in range(args.profile_steps):
+                step(k)
+            tot, launches = dfl.dflare_profile_end(h)
+            avg_us = 1000.0 * tot / max(launches, 1)
+            per_step_us = 1000.0 * tot / args.profile_steps
+            gbs = kb[name] / (avg_us * 1e-6) / 1e9 if avg_us > 0 else 0.0
+            res[name] = {"avg_us": round(avg_us, 3), "launches_per_step": launches / args.profile_steps,
+                         "us_per_step": round(per_step_us, 2), "bytes_per_launch": int(kb[name]),
+                         "achieved_GBs": round(gbs, 1)}
+        return res
+
+    kern = profile({"draft_block": dfl.K_DRAFT, "fuse": dfl.K_FUSE, "kv_t": dfl.K_KV_T})
     dom = max(kern, key=lambda k: kern[k]["us_per_step"])
     d = kern[dom]
+    # the same phases launched one kernel each (what the persistent launch saves)
+    per_phase = profile({"qkv": dfl.K_QKV, "attn": dfl.K_ATTN, "o": dfl.K_O, "gate_up": dfl.K_GATE_UP,
+                         "down": dfl.K_DOWN, "lm_head": dfl.K_LM_HEAD})
+    phases = phase_trace(dfl, h, step, cfg, kb, args.profile_steps)
 
     step_bytes = cfg.block_bytes(L) + cfg.append_bytes(n_mean)
     step_gbs = step_bytes / (ms * 1e-3) / 1e9
@@ -209,12 +220,51 @@ def main():
                           "frac": round(step_gbs / HBM_PEAK_GBS, 4)},
         "draft_block_ms": round(block_ms, 5),
         "kernels": kern,
+        "phases": phases,
+        "per_phase_launches": per_phase,
     }
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context)
     print(json.dumps(result), flush=True)
     model.close()
+
+
+def phase_trace(dfl, h, step, cfg, kb, steps):
+    """Per-phase time inside the persistent draft-block kernel, from its wall-clock trace
+    (100 MHz).  For each phase kind, microseconds per step (summed over layers): "us" from
+    the moment the work-groups pass the grid barrier into the phase to the moment they pass
+    into the next one, split into "body" (until the work-group's stores are complete) and
+    "wait" (at the next barrier); medians over work-groups; "body_max" is the slowest
+    work-group.  "GBs" relates "us" to the phase's algorithmic bytes."""
+    import numpy as np
+    n_launch, _, blocks, n_phase, _ = dfl.dflare_kernel_stats(h)
+    if n_launch != 1:
+        return None
+    dfl.dflare_set_option(h, dfl.OPT_TRACE, 1)
+    names = ["embed"] + ["qkv", "attn", "comb", "o", "gate_up", "down"] * cfg.n_draft_layers + ["lm_head"]
+    acc = {}
+    for k in range(steps):
+        step(k)
+        t = dfl.dflare_debug_read(h, dfl.DBG_TRACE, 0, (blocks, n_phase, 2)).astype(np.float64)
+        start, end = t[:, :, 0], t[:, :, 1]
+        nxt = np.concatenate([start[:, 1:], end[:, -1:]], axis=1)
+        for p, name in enumerate(names):
+            a = acc.setdefault(name, np.zeros(4))
+            a += [np.median(nxt[:, p] - start[:, p]), np.median(end[:, p] - start[:, p]),
+                  np.max(end[:, p] - start[:, p]), np.median(nxt[:, p] - end[:, p])]
+    dfl.dflare_set_option(h, dfl.OPT_TRACE, 0)
+    layer_bytes = {"qkv": kb["qkv"], "attn": kb["attn"], "o": kb["o"], "gate_up": kb["gate_up"],
+                   "down": kb["down"]}
+    out = {}
+    for name, a in acc.items():
+        us, body, body_max, wait = (a / steps).tolist()
+        reps = cfg.n_draft_layers if name in layer_bytes else 1
+        nbytes = layer_bytes.get(name, kb["lm_head"] if name == "lm_head" else 0) * reps
+        out[name] = {"us": round(us, 2), "body": round(body, 2), "body_max": round(body_max, 2),
+                     "wait": round(wait, 2),
+                     "GBs": round(nbytes / (us * 1e-6) / 1e9, 1) if nbytes and us > 0 else None}
+    return out
 
 
 def cpu_baseline(cfg, w, fusion_logits, ctx):

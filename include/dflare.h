@@ -98,9 +98,10 @@ typedef struct dflare_handle dflare_handle;
 
 /*
  * dflare_init -- build a draft model (Sec. 4.1 Eq. 3, Sec. 4.2 Eq. 4, Sec. 3.2).
- *   cfg            model shape and capacity.  Supported: hidden, q, kv, ffn
- *                  multiples of 32; head_dim 64 or 128; 1 <= block_size <= 16;
- *                  n_kv_heads * 16 >= ... (any); otherwise DFLARE_ERR_UNSUPPORTED.
+ *   cfg            model shape and capacity.  Supported: hidden, q and ffn
+ *                  multiples of 32, hidden <= 8192; head_dim 64 or 128;
+ *                  1 <= block_size <= 16; (n_q_heads / n_kv_heads) * block_size
+ *                  <= 128; n_target_layers <= 64; otherwise DFLARE_ERR_UNSUPPORTED.
  *   weights        device bf16 tensors as described above (copied and packed).
  *   fusion_logits  HOST float [D, S] = W^fuse.  alpha = softmax of each row is
  *                  computed here in double precision and cached as float.  A row
@@ -131,6 +132,11 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
  *                  is not a candidate (the B-1 candidates are 1..B-1).
  * Block row b sits at position L + b.  The context cache is not modified, so the
  * call can be repeated.  An empty context (L = 0) is allowed.
+ * By default the whole pass is one cooperative launch of one work-group per CU
+ * whose phases are separated by grid barriers (see DFLARE_OPT_PERSISTENT).  If a
+ * grid barrier of an earlier call timed out (the work-groups were not all
+ * resident), this call returns DFLARE_ERR_HIP without enqueuing work and the
+ * handle switches to one launch per phase.
  */
 int dflare_draft_block(dflare_handle* h, const int32_t* block_ids, int32_t* draft_tokens);
 
@@ -170,18 +176,29 @@ const char* dflare_last_error(const dflare_handle* h);
  *   what = DFLARE_DBG_HIDDEN  layer i: [B, H]        block rows after layer i
  *   what = DFLARE_DBG_LOGITS  (layer ignored) [B, V] logits of the last draft_block
  *   what = DFLARE_DBG_ALPHA   (layer ignored) [D, S] cached fusion weights
+ *   what = DFLARE_DBG_TRACE   (layer ignored) [blocks, phases, 2] microseconds at which
+ *                             each work-group of the last draft_block began each phase
+ *                             (after its grid barrier) and finished it (its stores
+ *                             complete), relative to the earliest start; needs
+ *                             DFLARE_OPT_TRACE (sizes from dflare_kernel_stats)
  * `count` is the number of floats host_out can hold; too small is INVALID_ARG.
+ * Debug capture makes draft_block run one launch per phase.
  */
 enum { DFLARE_DBG_FUSED = 0, DFLARE_DBG_KCACHE = 1, DFLARE_DBG_VCACHE = 2,
-       DFLARE_DBG_HIDDEN = 3, DFLARE_DBG_LOGITS = 4, DFLARE_DBG_ALPHA = 5 };
+       DFLARE_DBG_HIDDEN = 3, DFLARE_DBG_LOGITS = 4, DFLARE_DBG_ALPHA = 5,
+       DFLARE_DBG_TRACE = 6 };
 int dflare_debug_capture(dflare_handle* h, int on);
 int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, int64_t count);
 
 /*
- * dflare_kernel_stats -- launch counts, for measurement: writes up to `count`
+ * dflare_kernel_stats -- launch shape, for measurement: writes up to `count`
  * int32 values
  *   [0] number of kernels one draft_block enqueues
  *   [1] number of kernels one fuse_append enqueues
+ *   [2] work-groups of the draft-block kernel
+ *   [3] phases of a draft block (embedding; per layer QKV, attention, combine,
+ *       output projection, gate/up, down; LM head)
+ *   [4] grid barriers one draft_block waits at (0 with one launch per phase)
  */
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count);
 
@@ -190,7 +207,9 @@ int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count);
  * launch of one kernel kind with a pair of hipEvents on the handle's stream, up to
  * 8192 launches; kind = 0 stops.  dflare_profile_end synchronises the stream and
  * returns the summed event-measured duration (ms) and the number of launches
- * timed since the last begin, then stops.  Kinds:
+ * timed since the last begin, then stops.  Kinds 1-6 are phases of the draft
+ * block: while one of them is profiled, draft_block runs one launch per phase.
+ * Kinds:
  */
 enum { DFLARE_K_QKV = 1,       /* RMSNorm + Q/K^d/V^d projection + RoPE           */
        DFLARE_K_ATTN = 2,      /* block attention (split over keys) + combine      */
@@ -199,9 +218,21 @@ enum { DFLARE_K_QKV = 1,       /* RMSNorm + Q/K^d/V^d projection + RoPE         
        DFLARE_K_DOWN = 5,      /* down projection + residual                       */
        DFLARE_K_LM_HEAD = 6,   /* final RMSNorm + LM head + argmax                 */
        DFLARE_K_FUSE = 7,      /* layer fusion (Eq. 3)                             */
-       DFLARE_K_KV_T = 8 };    /* context K/V projection + RoPE + append (Eq. 4)   */
+       DFLARE_K_KV_T = 8,      /* context K/V projection + RoPE + append (Eq. 4)   */
+       DFLARE_K_DRAFT = 9 };   /* a whole draft_block, as configured               */
 int dflare_profile_begin(dflare_handle* h, int kind);
 int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches);
+
+/*
+ * dflare_set_option -- execution options of a handle (they do not change results):
+ *   DFLARE_OPT_PERSISTENT  1 (default): a draft_block is one cooperative launch whose
+ *                          phases wait at grid barriers; 0: one launch per phase.
+ *                          1 is refused (UNSUPPORTED) when the device cannot keep one
+ *                          work-group per CU resident.
+ *   DFLARE_OPT_TRACE       1: record per-work-group phase start times (DFLARE_DBG_TRACE).
+ */
+enum { DFLARE_OPT_PERSISTENT = 1, DFLARE_OPT_TRACE = 2 };
+int dflare_set_option(dflare_handle* h, int option, int value);
 
 #ifdef __cplusplus
 }

@@ -17,7 +17,7 @@ What is computed (all floating point in fp64; inputs are bfloat16 bit patterns
                   fixed across layers                           -- Sec. 3.2 (drafting phase)
 * MLP sub-layer, final LM head, one token per block position    -- Sec. 3.2 (drafting phase)
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
   pre-norm block with residuals around attention and MLP, SwiGLU MLP, no biases,
   final RMSNorm before the LM head; RMSNorm(x; g) = x / sqrt(mean(x^2) + eps) * g;
   rotary position embedding in the rotate-half convention on Q and K (context K

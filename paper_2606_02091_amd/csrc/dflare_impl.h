@@ -20,97 +20,146 @@ enum PackMode {
   PACK_SWIGLU = 2     // each 16-column tile holds 8 gate rows then the 8 matching up rows
 };
 
-// Epilogue selected by the GEMM template.
-enum Epi {
-  EPI_RESID = 0,   // out[row, col] += y; per-16-column sums of squares of the result
-  EPI_SWIGLU = 1,  // out[row, f] = silu(gate_f) * up_f
-  EPI_QKV = 2,     // block Q (RoPE, fp32), block K (RoPE) and V into cache slots L + row
-  EPI_KVT = 3,     // context K (RoPE) and V of appended rows into cache slots L + row
-  EPI_ARGMAX = 4   // vocabulary-parallel argmax: best (logit, id) of the block per row
+constexpr int kThreads = 512;   // draft-block work-group: 8 waves, one work-group per CU
+constexpr int kWaves = kThreads / 64;
+constexpr int kStatsPad = 32;   // floats per 16-column tile in the sums-of-squares arrays (one 128 B line)
+constexpr int kBarCounters = 16;  // grid-barrier arrival counters, each on its own 128 B line
+constexpr int kMaxBlock = 16;     // draft block rows (one 16-row MFMA tile)
+constexpr int kTNMax = 8;         // output tiles a GEMM work-group accumulates at once
+constexpr int kMaxSplit = 8;      // work-groups that split one GEMM output range along K
+constexpr int kMaxBlocks = 1024;  // work-groups of the draft-block kernel
+// Split-K arrival counters: one per (GEMM phase kind, output range), each on its own
+// 128 B line, after the grid-barrier counters and the LM-head completion counter.
+constexpr int kSplitKinds = 4;    // QKV, O, gate/up, down
+constexpr long kSyncBytes = 4096 + (long)kSplitKinds * kMaxBlocks * 128;
+// Zero k-tiles after the K real ones in every draft-block activation (A-fragment) plane:
+// a GEMM wave's run of k-tiles may reach past K, by less than 2 * 8 + 1 batches of 4.
+constexpr int kKtPad = 72;
+// Spare bytes after every packed weight matrix: the last batch of a row may reach past K.
+constexpr long kWeightSpare = 64 * 1024;
+
+// The draft block is one sequence of phases; between two phases every work-group waits
+// at a grid barrier (one persistent launch) or the phases are separate launches.
+//   EMBED, then for each draft layer QKV, ATTN, COMB, O, GU, DOWN, then LM.
+enum Phase { PH_EMBED = 0, PH_QKV, PH_ATTN, PH_COMB, PH_O, PH_GU, PH_DOWN, PH_LM, PH_COUNT };
+__host__ __device__ inline int phase_count(int D) { return 2 + 6 * D; }
+__host__ __device__ inline void phase_of(int p, int D, int& kind, int& layer) {
+  if (p == 0) {
+    kind = PH_EMBED;
+    layer = 0;
+  } else if (p == 1 + 6 * D) {
+    kind = PH_LM;
+    layer = D;
+  } else {
+    kind = PH_QKV + (p - 1) % 6;
+    layer = (p - 1) / 6;
+  }
+}
+
+// What changes from one draft block to the next: passed by value at every launch.
+struct DraftCall {
+  int L;                // context length
+  int pos[kMaxBlock];   // positions of the block rows
+  const int* ids;       // [B] block token ids
+  int* tokens;          // [B] output: greedy draft tokens
+  float* logits;        // optional [B, V]
+  unsigned bar_epoch;   // grid barriers completed by earlier launches
+  unsigned done_epoch;  // launches that ran the LM phase before this one
+  unsigned long long* trace;  // optional [blocks][phases][2] wall clock at each phase's start and end
 };
 
-struct StepParams {  // device-resident, rewritten by a prologue kernel each call
-  int L;             // context length before this call
-  int n_new;         // rows appended by this call (fuse_append)
-  int pos[16];       // block positions (draft_block)
+// Everything else the draft-block kernel needs; written to device memory once at init and
+// read through a pointer, so that the kernel loads each field where a phase uses it instead
+// of holding all of them in scalar registers for the whole launch.  Data that one phase
+// hands to a later one is written with write-through (agent-coherent) stores and is either
+// written once per launch (per-stage and per-layer buffers, read with ordinary cached
+// loads) or read back with coherent loads (the residual stream, the attention partials,
+// the LM-head partial maxima); see the kernel source for the rule.
+struct DraftArgs {
+  // shapes
+  int H, F, V, D, B, hd, n_q, n_kv, Lcap, Rpad, chunk, nch;
+  float eps, qscale;
+  // GEMM plan of each phase kind: the work-groups form blocks / kg output ranges of
+  // consecutive n-tiles, kg work-groups per range each taking 1/kg of K; a work-group
+  // accumulates up to tn (2, 4, 6 or 8) n-tiles at once.
+  int tn[PH_COUNT], kg[PH_COUNT];
+  // weights: packed tiles; strides between layers in u32x4 units
+  const uint16_t* embed;
+  const u32x4 *w_qkv, *w_o, *w_gu, *w_down, *w_lm;
+  long s_qkv, s_o, s_gu, s_down;
+  const float *g_attn, *g_mlp, *g_final;  // RMSNorm gains [D, H], [D, H], [H]
+  const u32x4* zero;                      // one zero tile
+  const float2* rope;                     // [Lcap, hd/2] (cos, sin)
+  // context cache of layer 0: K [n_kv, Lcap, hd], V^T [n_kv, hd, Lcap], hi plane then lo plane
+  uint16_t *kc, *vt;
+  long plane, cache_layer;
+  // activations
+  float* X;              // residual stream [16, H] fp32, updated in place
+  float* XS;             // per stage: sums of squares [H/16][kStatsPad]
+  long xs_stride;
+  u32x4* XA;             // per stage: A fragments of x * gain, hi plane then lo plane (K + kKtPad k-tiles each)
+  long xa_stride;
+  float* Q;              // per layer: rotated queries [16, q_dim]
+  long q_stride;
+  float* OP;             // attention partials [nch, n_kv, Rpad, hd]
+  float2* ML;            // [nch, n_kv, Rpad] (running max, sum), log2 domain
+  u32x4* OA;             // per layer: A fragments of the attention output
+  long oa_stride;
+  u32x4* HA;             // per layer: A fragments of the SwiGLU output
+  long ha_stride;
+  float* pmax;           // [blocks][kStatsPad] best logit of each work-group per row
+  int* pidx;
+  float* part;           // split-K partial sums [blocks][kTNMax][64 lanes][4]
+  unsigned* kcnt;        // split-K arrival counters [kSplitKinds][kMaxBlocks], 32 words apart
+  // synchronisation
+  unsigned* bar;          // kBarCounters counters, 32 words apart, monotonic across launches
+  unsigned* done;         // LM-head completion counter, monotonic across launches
+  int* err;               // host-mapped flag, set when a grid barrier times out
 };
 
-struct EpiArgs {
-  const StepParams* params;
-  float* out;             // RESID: X [M, ldo]; SWIGLU: H [M, ldo]; QKV: Q [B, ldo]
-  int ldo;
-  float* stats_out;       // RESID: [M, n_stat_out]
-  int n_stat_out;
-  uint16_t* kc;           // K cache of the layer (QKV) or of layer 0 (KVT): [n_kv, Lcap, hd]
-  uint16_t* vt;           // V cache, transposed: [n_kv, hd, Lcap]
-  long plane;             // elements from the hi plane of a cache to its lo plane
-  long cache_layer_stride;  // elements between consecutive layers' caches (KVT)
-  int Lcap;
-  int hd;
-  int q_tiles;            // QKV: number of Q tiles; KVT: 0
-  int kv_tiles;           // tiles of the K region (== tiles of the V region)
-  const float2* rope;     // [positions, hd/2] (cos, sin)
-  int B;                  // block rows (QKV / ARGMAX)
-  // ARGMAX
-  int vocab;
-  float* pmax;            // [16, blocks]: best logit of each block per row
-  int* pidx;              // [16, blocks]: its token id
-  float* logits;          // optional debug [B, vocab]
-  // RESID / SWIGLU: A fragments of the next GEMM's input (RESID: x * next_gain)
-  uint32_t* na_hi;
-  uint32_t* na_lo;
-  int na_Kt;
-  const float* next_gain;
+// The draft kernel's one argument: phases [p0, p1) of a draft block.
+struct DraftKernArgs {
+  const DraftArgs* a;  // device copy of the fixed arguments
+  DraftCall c;
+  int p0, p1;
 };
 
-struct GemmArgs {
-  const u32x4* W;          // packed tiles of layer 0
-  long w_layer_stride;     // in u32x4 units (layer = blockIdx.y)
-  int Nt, Kt;              // output tiles (16 wide), k tiles (32 deep)
-  const u32x4* zero;       // one zero tile (64 x 16 bytes)
-  const u32x4* Ahi;        // activation A fragments (hi / lo planes) of layer 0, [m-tiles, Kt, 64]
+// Arguments of the context K/V projection of fuse_append (Eq. 4, W^t): fused rows of every
+// draft layer -> RoPE(K) and V written into cache slots L .. L + n_new - 1.
+struct KvtArgs {
+  const u32x4* W;          // packed [K^t ; V^t] tiles of layer 0
+  long w_layer_stride;
+  int Nt, Kt;
+  const u32x4* zero;
+  const u32x4* Ahi;        // A fragments of u * g_fuse, [D][mt_max][Kt][64]
   const u32x4* Alo;
-  long a_layer_stride;     // in u32x4 units
-  int M;                   // rows (ignored for KVT, which reads n_new)
-  const float* stats;      // optional: per-row partial sums of squares [M, n_stat]; when set the
-  long stats_layer_stride; // output rows are scaled by 1/sqrt(sum * inv_dim + eps) (RMSNorm)
+  long a_layer_stride;
+  const float* stats;      // sums of squares [D][max_new][H/16]
+  long stats_layer_stride;
   int n_stat;
   float inv_dim, eps;
-  EpiArgs e;
-};
-
-struct AttnArgs {
-  const StepParams* params;
-  const float* Q;          // [B, q_dim] fp32, rotated
-  const uint16_t* kc;      // [n_kv, Lcap, hd] of the layer (hi plane; lo plane at +plane)
-  const uint16_t* vt;      // [n_kv, hd, Lcap]
-  long plane;
-  int B, n_q, n_kv, q_dim, Lcap, Rpad;
-  float qscale;            // log2(e) / sqrt(hd)
-  float* opart;            // [chunks, n_kv, Rpad, hd]
-  float2* ml;              // [chunks, n_kv, Rpad]
-  u32x4* oa_hi;            // combine: A fragments of O [B, q_dim] for the output projection
-  u32x4* oa_lo;
-  int oa_Kt;
+  int L, n_new;
+  uint16_t *kc, *vt;
+  long plane, cache_layer_stride;
+  int Lcap, hd, kv_tiles;
+  const float2* rope;
 };
 
 // ---- launchers (kernels.hip) ----
 void launch_pack(hipStream_t s, u32x4* dst, const uint16_t* src0, const uint16_t* src1,
                  int n_src_rows, int K, int nt_begin, int nt_count, int Kt_total, int mode, int hd);
 void launch_bf16_to_f32(hipStream_t s, float* dst, const uint16_t* src, long n);
-void launch_prologue(hipStream_t s, StepParams* p, const StepParams& host, const int* ids_src,
-                     int* ids_dst, int B);
-void launch_embed(hipStream_t s, const uint16_t* embed, const int* ids, int vocab, int H, int B,
-                  float* X, float* stats, const float* gain, u32x4* a_hi, u32x4* a_lo);
 void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
-                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max,
-                 StepParams* params, int L);
+                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max);
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n,
                        int H, int D, int n_max, int mt_max, float eps, float* out);
-void launch_gemm(hipStream_t s, int epi, int nt_per_block, int waves, const GemmArgs& a, int layers, int mtiles);
-bool gemm_shape_supported(int nt_per_block, int waves);
-void launch_argmax_combine(hipStream_t s, const float* pmax, const int* pidx, int groups, int B, int* tokens);
-void launch_attention(hipStream_t s, const AttnArgs& a, int hd, int chunk, int n_chunks);
-void launch_attn_combine(hipStream_t s, const AttnArgs& a, int hd, int chunk, int n_chunks);
+bool kvt_shape_supported(int nt_per_block, int waves);
+void launch_kvt(hipStream_t s, int nt_per_block, int waves, const KvtArgs& a, int layers, int mtiles);
+// Phases [p0, p1) of a draft block on `blocks` work-groups of kThreads threads.  With
+// cooperative = true the work-groups are guaranteed co-resident and wait at grid barriers
+// between phases; otherwise p1 must be p0 + 1.
+hipError_t launch_draft(hipStream_t s, const DraftArgs* a_dev, const DraftCall& c, int hd, int blocks, int p0,
+                        int p1, bool cooperative);
+int draft_blocks_per_cu(int hd);
 
 }  // namespace dflare

@@ -6,6 +6,22 @@
 // lo = bf16(x - hi)), so each product carries about 16 mantissa bits of the
 // activation against the exact bf16 weight; the doubled MFMA work is free
 // because every GEMM here streams its weights from HBM (batch-1, 16 rows).
+//
+// A draft block (Sec. 3.2, Eq. 4, and the LM head) runs as one persistent launch of one
+// 8-wave work-group per CU.  Its phases are separated by grid barriers, and each phase
+// issues the loads that do not depend on the previous phase (its first weight tiles, the
+// context K/V of attention) before it waits, so HBM keeps streaming across the barrier.
+//
+// Cross-phase data and the per-XCD L2 caches.  Each XCD has its own L2, and ordinary
+// stores stay in the writer's L2 until the kernel ends.  So within a launch:
+//   - everything a later phase reads is stored write-through (agent-scope atomic stores,
+//     which reach the device-coherent level before they complete), and every work-group
+//     waits for its stores before it arrives at a barrier;
+//   - a line is read with ordinary (L2-cached) loads only if it is written at most once
+//     per launch, before any read of it: the per-stage and per-layer buffers below.  At
+//     launch start the L2s hold no copy of such a line, so the first read fetches the
+//     written value.  Buffers that are rewritten within a launch (the residual stream,
+//     the attention partials, the LM-head maxima) are read with coherent loads.
 #include "dflare_impl.h"
 
 #include <math.h>
@@ -15,6 +31,13 @@ namespace dflare {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define GLOBAL __attribute__((address_space(1)))
+#define CONSTANT __attribute__((address_space(4)))
+
+constexpr int kLdsBytes = 160 * 1024;
+constexpr int kChunk = 128;  // context keys per attention work item
+constexpr long long kBarrierTimeout = 25000000;  // wall-clock ticks (100 MHz): 0.25 s
 
 __device__ __forceinline__ float bf2f(uint32_t b) { return __uint_as_float(b << 16); }
 
@@ -35,7 +58,65 @@ __device__ __forceinline__ void split_pack8(const float* v, u32x4& hi, u32x4& lo
   }
 }
 
-// Activations handed from one kernel to the next are stored directly in the A-operand
+__device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Every buffer lives in device (global) memory; pointers that come from memory rather than
+// from kernel arguments are cast to the global address space so that the compiler emits
+// global rather than flat memory instructions.
+template <typename T>
+__device__ __forceinline__ GLOBAL T* gbl(T* p) {
+  return (GLOBAL T*)p;
+}
+template <typename T>
+__device__ __forceinline__ const GLOBAL T* gbl(const T* p) {
+  return (const GLOBAL T*)p;
+}
+
+// ---- write-through stores and coherent loads ----
+__device__ __forceinline__ void st_wt(float* p, float v) {
+  __hip_atomic_store(gbl(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_wt(uint32_t* p, uint32_t v) {
+  __hip_atomic_store(gbl(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_wt(int* p, int v) {
+  __hip_atomic_store(gbl(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_wt(uint16_t* p, uint16_t v) {
+  __hip_atomic_store(gbl(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_wt8(void* p, uint64_t v) {
+  __hip_atomic_store(gbl(reinterpret_cast<uint64_t*>(p)), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_wt16(void* p, u32x4 v) {
+  uint64_t* q = reinterpret_cast<uint64_t*>(p);
+  st_wt8(q, (uint64_t)v[0] | ((uint64_t)v[1] << 32));
+  st_wt8(q + 1, (uint64_t)v[2] | ((uint64_t)v[3] << 32));
+}
+__device__ __forceinline__ float ld_coh(const float* p) {
+  return __hip_atomic_load(gbl(const_cast<float*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int ld_coh(const int* p) {
+  return __hip_atomic_load(gbl(const_cast<int*>(p)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 ld_coh2(const void* p) {
+  const uint64_t v = __hip_atomic_load(gbl(reinterpret_cast<uint64_t*>(const_cast<void*>(p))), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+// an integer the compiler cannot see through (keeps address arithmetic where it is written)
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// wait until this wave's memory operations (stores included) have completed
+__device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Activations handed from one GEMM to the next are stored directly in the A-operand
 // layout of v_mfma_f32_16x16x32_bf16, as two bf16 planes hi and lo (x ~= hi + lo):
 //   element (row, k) of a [rows, K] matrix sits in 16-row tile row/16, k-tile k/32,
 //   lane (row % 16) + 16 * ((k % 32) / 8), slot k % 8; a (row-tile, k-tile) is 1 KiB.
@@ -43,19 +124,27 @@ __device__ __forceinline__ long frag_off(int row, int k, int Kt) {
   return ((((long)(row >> 4) * Kt + (k >> 5)) * 64 + (row & 15) + ((k & 31) >> 3) * 16) << 3) + (k & 7);
 }
 
-// store the hi/lo planes of two consecutive elements (k even) as one 32-bit word each
+// hi/lo planes of two consecutive elements (k even), one 32-bit word per plane
+__device__ __forceinline__ void frag_pair(float v0, float v1, uint32_t& hi, uint32_t& lo) {
+  const uint32_t h0 = f2bf(v0), h1 = f2bf(v1);
+  hi = h0 | (h1 << 16);
+  lo = f2bf(v0 - bf2f(h0)) | (f2bf(v1 - bf2f(h1)) << 16);
+}
 __device__ __forceinline__ void store_frag_pair(uint32_t* hi, uint32_t* lo, int row, int k, int Kt, float v0,
                                                 float v1) {
-  const uint32_t h0 = f2bf(v0), h1 = f2bf(v1);
-  const uint32_t l0 = f2bf(v0 - bf2f(h0)), l1 = f2bf(v1 - bf2f(h1));
+  uint32_t h, l;
+  frag_pair(v0, v1, h, l);
   const long o = frag_off(row, k, Kt) >> 1;
-  hi[o] = h0 | (h1 << 16);
-  lo[o] = l0 | (l1 << 16);
+  hi[o] = h;
+  lo[o] = l;
 }
-
-__device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+__device__ __forceinline__ void store_frag_pair_wt(uint32_t* hi, uint32_t* lo, int row, int k, int Kt, float v0,
+                                                   float v1) {
+  uint32_t h, l;
+  frag_pair(v0, v1, h, l);
+  const long o = frag_off(row, k, Kt) >> 1;
+  st_wt(hi + o, h);
+  st_wt(lo + o, l);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -100,58 +189,6 @@ __global__ void k_bf16_to_f32(float* dst, const uint16_t* src, long n) {
 }
 
 // ------------------------------------------------------------------------------------------
-// per-call prologue: step parameters and a private copy of the block ids
-// ------------------------------------------------------------------------------------------
-__global__ void k_prologue(StepParams* p, StepParams host, const int* ids_src, int* ids_dst, int B) {
-  const int t = threadIdx.x;
-  if (t == 0) {
-    p->L = host.L;
-    p->n_new = host.n_new;
-  }
-  if (t < 16) p->pos[t] = host.pos[t];
-  if (ids_src && t < B) ids_dst[t] = ids_src[t];
-}
-
-// ------------------------------------------------------------------------------------------
-// embedding gather: X[b, :] = E[id_b, :] (fp32), per-16-column sums of squares, and the
-// A fragments of X * g (g = gain of the first pre-attention RMSNorm)
-// ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, const int* __restrict__ ids,
-                                               int vocab, int H, float* X, float* stats,
-                                               const float* __restrict__ gain, u32x4* a_hi, u32x4* a_lo) {
-  const int b = blockIdx.x;
-  int id = ids[b];
-  id = id < 0 ? 0 : (id >= vocab ? vocab - 1 : id);
-  const uint16_t* row = E + (long)id * H;
-  const int Kt = H / 32;
-  for (int k0 = threadIdx.x * 8; k0 < H; k0 += blockDim.x * 8) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(row + k0);
-    float f[8], y[8];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      f[2 * e] = bf2f(v[e] & 0xFFFFu);
-      f[2 * e + 1] = bf2f(v[e] >> 16);
-    }
-    float sq = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      sq += f[e] * f[e];
-      y[e] = f[e] * gain[k0 + e];
-    }
-    float* xo = X + (long)b * H + k0;
-    *reinterpret_cast<float4*>(xo) = make_float4(f[0], f[1], f[2], f[3]);
-    *reinterpret_cast<float4*>(xo + 4) = make_float4(f[4], f[5], f[6], f[7]);
-    u32x4 hi, lo;
-    split_pack8(y, hi, lo);
-    const long fo = frag_off(b, k0, Kt) >> 3;
-    a_hi[fo] = hi;
-    a_lo[fo] = lo;
-    sq += __shfl_xor(sq, 1);
-    if ((threadIdx.x & 1) == 0) stats[(long)b * (H / 16) + k0 / 16] = sq;
-  }
-}
-
-// ------------------------------------------------------------------------------------------
 // layer fusion (Eq. 3): u^(i)[r, k] = sum_j alpha[i, j] h^(j)[r, k], accumulated in j order.
 // Block (512 columns, row r, draft layer i); a lane owns 8 columns and keeps twelve 16-byte
 // loads in flight.  Writes the A fragments of u^(i) * g_fuse^(i) and per-16-column sums of
@@ -160,14 +197,9 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* __restrict__ E, c
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int n, int S, int H,
                                              const float* __restrict__ alpha, const float* __restrict__ gain,
-                                             float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max,
-                                             StepParams* params, int L) {
+                                             float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
   const int lane = threadIdx.x;
   const int r = blockIdx.y, i = blockIdx.z;
-  if (blockIdx.x == 0 && r == 0 && i == 0 && lane == 0) {  // step parameters for the K/V projection
-    params->L = L;
-    params->n_new = n;
-  }
   const int k0 = blockIdx.x * 512 + lane * 8;
   const bool ok = k0 < H;
   const int Kt = H / 32;
@@ -229,31 +261,23 @@ __global__ void k_fused_rows(const u32x4* ua_hi, const u32x4* ua_lo, const float
 }
 
 // ------------------------------------------------------------------------------------------
-// weight-streaming GEMM, y[M<=16 per m-tile, N] = x[M, K] W^T.
-// Block `group` owns output tiles [group*NT, +NT) over the whole K; its WAVES waves split the
-// k range, each streaming its NT weight tiles per k-tile from HBM together with the A
-// fragments of the same k-tile (hi and lo planes, from L2: they are shared by every block).
-// Two register sets alternate so that one batch of loads is always in flight while the
-// previous batch goes through the matrix cores.  The waves' partial sums are added in LDS in
-// wave order (fixed, so results do not depend on timing), and wave w < NT then holds output
-// tile group*NT + w for the epilogue.  No block ever waits on another: there is no split-K
-// across blocks, because making partial sums of one XCD visible to another takes agent-scope
-// fences that write back and invalidate the L2 -- far costlier than these kernels.
+// context K/V projection of fuse_append (Eq. 4, W^t): RoPE(f W_K^t) and f W_V^t for every
+// appended row of every draft layer, into cache slots L + row.  Weight-streaming GEMM:
+// block (group of NT output tiles, layer, 16-row m-tile); its WAVES waves split the k range
+// and add their partial sums in LDS in wave order.  Two register sets alternate so that one
+// batch of loads is in flight while the previous one goes through the matrix cores.
 // ------------------------------------------------------------------------------------------
-template <int NT, int WAVES, int EPI>
-__global__ __launch_bounds__(64 * WAVES) void k_gemm(GemmArgs a) {
+template <int NT, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_kvt(KvtArgs a) {
   constexpr int U = 2;  // k-tiles per batch
   __shared__ f32x4 red[WAVES][NT][64];
   __shared__ float s_rstd[16];
-  __shared__ float s_bv[NT][16];
-  __shared__ int s_bi[NT][16];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int quad = lane >> 4, col = lane & 15;
-  const int groups = gridDim.x;
   const int group = blockIdx.x;
   const int layer = blockIdx.y, mt = blockIdx.z;
-  const int M = (EPI == EPI_KVT) ? a.e.params->n_new : a.M;
+  const int M = a.n_new;
   if (mt * 16 >= M) return;  // whole m-tile idle: every block of it leaves together
 
   const int kw0 = (a.Kt * wave) / WAVES;
@@ -262,8 +286,6 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm(GemmArgs a) {
   const int nb2 = (nb + 1) & ~1;
   const int nt0 = group * NT;
 
-  // Tile addresses; a tile past the wave's range or a padding output tile reads the zero
-  // tile instead, so the streaming loop has no branches.
   const u32x4* zt = a.zero + lane;
   const u32x4* Wl = a.W + layer * a.w_layer_stride;
   const u32x4* wrow[NT];
@@ -332,441 +354,998 @@ __global__ __launch_bounds__(64 * WAVES) void k_gemm(GemmArgs a) {
     }
   }
 
-  // waves -> tiles: wave w < NT receives tile w summed over the waves in wave order
 #pragma unroll
   for (int j = 0; j < NT; ++j) red[wave][j][lane] = acc_h[j] + acc_l[j];
   __syncthreads();
   const bool owner = wave < NT;
   const int nt = nt0 + (owner ? wave : 0);
-  const bool has_tile = owner && nt < a.Nt;  // wave-uniform
+  const bool has_tile = owner && nt < a.Nt;
   f32x4 v = {0.f, 0.f, 0.f, 0.f};
   if (owner) {
     v = red[0][wave][lane];
 #pragma unroll
     for (int w = 1; w < WAVES; ++w) v += red[w][wave][lane];
   }
-
-  // 1/rms of the rows (RMSNorm consumers): (x*g/rms) W^T = (1/rms) (x*g) W^T
-  if (a.stats) {
-    if (tid < 256) {
-      const int row = tid >> 4, part = tid & 15;
-      float s = 0.f;
-      if (mt * 16 + row < M) {
-        const float* st = a.stats + layer * a.stats_layer_stride + (long)(mt * 16 + row) * a.n_stat;
+  // 1/rms of the fused rows (Eq. 3): (u*g/rms) W^T = (1/rms) (u*g) W^T
+  if (tid < 256) {
+    const int row = tid >> 4, part = tid & 15;
+    float s = 0.f;
+    if (mt * 16 + row < M) {
+      const float* st = a.stats + layer * a.stats_layer_stride + (long)(mt * 16 + row) * a.n_stat;
+      for (int t = part; t < a.n_stat; t += 16) s += st[t];
+    }
+    s += __shfl_xor(s, 8);
+    s += __shfl_xor(s, 4);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 1);
+    if (part == 0) s_rstd[row] = (mt * 16 + row < M) ? rsqrtf(s * a.inv_dim + a.eps) : 0.f;
+  }
+  __syncthreads();
 #pragma unroll
-        for (int q = 0; q < 32; ++q) {
-          const int t = part + 16 * q;
-          if (t < a.n_stat) s += st[t];
+  for (int i = 0; i < 4; ++i) v[i] *= s_rstd[quad * 4 + i];
+
+  if (has_tile) {
+    const int tph = a.hd / 16, half = a.hd / 2;
+    uint16_t* kc = a.kc + layer * a.cache_layer_stride;
+    uint16_t* vt = a.vt + layer * a.cache_layer_stride;
+    const bool is_k = nt < a.kv_tiles;
+    const int t = is_k ? nt : nt - a.kv_tiles;
+    const int head = t / tph, jj = t % tph;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = mt * 16 + quad * 4 + i;
+      const bool valid = row < M;
+      const int slot = a.L + row;
+      const float x = v[i];
+      const float partner = __shfl_xor(x, 8);
+      if (is_k) {
+        const int m = 8 * jj + (col & 7);
+        const int dim = (col < 8) ? m : half + m;
+        const float2 cs = a.rope[(long)(valid ? slot : 0) * half + m];
+        const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
+        if (valid) {  // the cache keeps y as two bf16 planes, y ~= hi + lo
+          const long ix = ((long)head * a.Lcap + slot) * a.hd + dim;
+          const uint32_t hb = f2bf(y);
+          kc[ix] = (uint16_t)hb;
+          kc[ix + a.plane] = (uint16_t)f2bf(y - bf2f(hb));
+        }
+      } else if (valid) {
+        const int dim = jj * 16 + col;
+        const long ix = ((long)head * a.hd + dim) * a.Lcap + slot;
+        const uint32_t hb = f2bf(x);
+        vt[ix] = (uint16_t)hb;
+        vt[ix + a.plane] = (uint16_t)f2bf(x - bf2f(hb));
+      }
+    }
+  }
+}
+
+// ==========================================================================================
+// the draft block
+// ==========================================================================================
+
+// The draft kernel reads its fixed arguments through the constant address space: they are
+// never written during a launch, so every field is a scalar load where a phase uses it.
+typedef const CONSTANT DraftArgs* Args;
+typedef const CONSTANT DraftCall* Call;
+
+// ---- grid barrier ----
+// Arrival: every wave waits for its own stores, then one atomic add per work-group on one
+// of kBarCounters counters (spreading the arrivals keeps same-address atomics from
+// serialising).  Wait: lanes of wave 0 poll the counters with coherent loads until each
+// holds its share of arrivals times the barrier's epoch.  A wait that exceeds the time
+// limit raises the host-visible error flag and lets the work-group go on (results are then
+// wrong, and the host reports the failure), so a launch always terminates.
+__device__ __forceinline__ void grid_arrive(Args a) {
+  wait_vm();
+  __syncthreads();
+  if (threadIdx.x == 0)
+    __hip_atomic_fetch_add(a->bar + (blockIdx.x % kBarCounters) * 32, 1u, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void trace_mark(Call c, int slot, int nslots) {
+  if (c->trace && threadIdx.x == 0) c->trace[(long)blockIdx.x * nslots + slot] = wall_clock64();
+}
+
+__device__ __forceinline__ void grid_wait(Args a, unsigned epoch, bool& failed) {
+  if (threadIdx.x < 64 && !failed) {
+    const int lane = threadIdx.x;
+    const unsigned n = gridDim.x;
+    const unsigned share = n / kBarCounters + ((unsigned)lane < n % kBarCounters ? 1u : 0u);
+    const unsigned target = share * epoch;
+    unsigned* c = a->bar + (lane % kBarCounters) * 32;
+    const long long t0 = wall_clock64();
+    while (true) {
+      const bool ok = lane >= kBarCounters ||
+                      __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target;
+      if (__all(ok)) break;
+      __builtin_amdgcn_s_sleep(1);
+      if (wall_clock64() - t0 > kBarrierTimeout) {
+        failed = true;
+        if (lane == 0) __hip_atomic_store(a->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        break;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+struct PhaseCtl {
+  bool wait;        // wait at the grid barrier before the phase body
+  unsigned epoch;   // that barrier's epoch
+  int slot, nslots; // trace slot of the body start
+};
+
+__device__ __forceinline__ void phase_begin(Args a, Call c, const PhaseCtl& pc,
+                                            bool& failed) {
+  if (pc.wait) grid_wait(a, pc.epoch, failed);
+  trace_mark(c, pc.slot, pc.nslots);
+}
+
+// ---- EMBED: X = E[ids] (fp32), sums of squares and A fragments of X * g_attn^(0) (stage 0)
+__device__ void phase_embed(Args a, Call c) {
+  const int H = a->H, Kt = H / 32, per_row = H / 8;
+  const int total = a->B * per_row;
+  const float* gain = a->g_attn;
+  float* XS = a->XS;
+  uint32_t* xhi = reinterpret_cast<uint32_t*>(a->XA);
+  uint32_t* xlo = reinterpret_cast<uint32_t*>(a->XA + (long)(Kt + kKtPad) * 64);
+  // Item = 8 columns of one row.  total is even and so is the stride, so the two lanes of
+  // a 16-column tile (items 2j, 2j+1) always run the loop body together.
+  for (int item = blockIdx.x * kThreads + opaque(threadIdx.x); item < total; item += gridDim.x * kThreads) {
+    const int row = item / per_row, k0 = (item % per_row) * 8;
+    int id = gbl(c->ids)[row];
+    id = id < 0 ? 0 : (id >= a->V ? a->V - 1 : id);
+    const u32x4 v = *gbl(reinterpret_cast<const u32x4*>(a->embed + (long)id * H + k0));
+    float f[8], y[8], sq = 0.f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f[2 * e] = bf2f(v[e] & 0xFFFFu);
+      f[2 * e + 1] = bf2f(v[e] >> 16);
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      sq += f[e] * f[e];
+      y[e] = f[e] * gbl(gain)[k0 + e];
+    }
+    sq += __shfl_xor(sq, 1);
+    float* xo = a->X + (long)row * H + k0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) st_wt(xo + e, f[e]);
+    u32x4 hi, lo;
+    split_pack8(y, hi, lo);
+    const long fo = frag_off(row, k0, Kt);  // in bf16 elements
+    st_wt16(reinterpret_cast<uint16_t*>(xhi) + fo, hi);
+    st_wt16(reinterpret_cast<uint16_t*>(xlo) + fo, lo);
+    if ((item & 1) == 0) st_wt(XS + (k0 / 16) * kStatsPad + row, sq);
+  }
+}
+
+// ---- weight-streaming GEMM phases ----
+enum Epi { EPI_RESID = 0, EPI_SWIGLU = 1, EPI_QKV = 2, EPI_ARGMAX = 3 };
+
+struct GemmJob {
+  const u32x4* W;      // packed tiles of this layer
+  int Nt, Kt;
+  const u32x4* Ahi;    // A fragments of the input rows (one 16-row tile)
+  const u32x4* Alo;
+  const float* stats;  // sums of squares [H/16][kStatsPad] of an RMSNorm input, or null
+  // RESID
+  float* xs_out;       // [H/16][kStatsPad]
+  uint32_t* na_hi;     // A fragments of the next consumer
+  uint32_t* na_lo;
+  int na_Kt;
+  const float* gain;   // RESID: gain of the next RMSNorm
+  // QKV
+  float* q_out;        // [16, q_dim]
+  uint16_t* kc;        // cache of this layer
+  uint16_t* vt;
+  // split-K
+  unsigned* cnt;       // arrival counters of this phase kind, 32 words apart
+  unsigned target;     // counter value once every work-group of a range has arrived
+};
+
+// LDS of a GEMM phase: partial tiles [kWaves][TN][64 lanes] (64 KiB at most), then the
+// row scales, the argmax scratch and a flag.
+constexpr int kLdsRedBytes = kWaves * kTNMax * 1024;
+
+// 16-byte coherent load (two 8-byte agent-scope loads)
+__device__ __forceinline__ f32x4 ld_coh16(const f32x4* p) {
+  const float2 x = ld_coh2(p), y = ld_coh2(reinterpret_cast<const float*>(p) + 2);
+  return f32x4{x.x, x.y, y.x, y.y};
+}
+
+// Epilogue of one finished 16 x 16 output tile nt (lane holds rows quad*4 .. +3 of column
+// col); v already carries the RMSNorm row scale.  ARGMAX leaves the tile's best (logit,
+// id) per row in s_bv / s_bi at slot j.
+template <int EPI>
+__device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, int nt, f32x4 v, int j,
+                                              float* s_bv, int* s_bi) {
+  const int lane = opaque(threadIdx.x) & 63;  // epilogue values are not hoisted above the main loop
+  const int quad = lane >> 4, col = lane & 15;
+  const int M = a->B;
+  if constexpr (EPI == EPI_RESID) {
+    const int k = nt * 16 + col;
+    const float gn = gbl(g.gain)[k];
+    float sq[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = quad * 4 + i;
+      float x = 0.f;
+      if (row < M) {
+        float* p = a->X + (long)row * a->H + k;
+        x = ld_coh(p) + v[i];
+        st_wt(p, x);
+      }
+      sq[i] = x * x;
+      const float y = x * gn;
+      const float y1 = __shfl_xor(y, 1);
+      if ((col & 1) == 0 && row < M) store_frag_pair_wt(g.na_hi, g.na_lo, row, k, g.na_Kt, y, y1);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sq[i] += __shfl_xor(sq[i], 1);
+      sq[i] += __shfl_xor(sq[i], 2);
+      sq[i] += __shfl_xor(sq[i], 4);
+      sq[i] += __shfl_xor(sq[i], 8);
+    }
+    if (col == 0)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) st_wt(g.xs_out + nt * kStatsPad + quad * 4 + i, sq[i]);
+  } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float gt = v[i];
+      const float up = __shfl_xor(gt, 8);
+      const float hv = (col < 8) ? gt / (1.0f + expf(-gt)) * up : 0.f;
+      const float h1 = __shfl_xor(hv, 1);
+      const int row = quad * 4 + i;
+      if (col < 8 && (col & 1) == 0 && row < M) store_frag_pair_wt(g.na_hi, g.na_lo, row, nt * 8 + col, g.na_Kt, hv, h1);
+    }
+  } else if constexpr (EPI == EPI_QKV) {
+    const int L = c->L, hd = a->hd;
+    const int tph = hd / 16, half = hd / 2;
+    const int q_tiles = a->n_q * tph, kv_tiles = a->n_kv * tph;
+    int region, t;  // 0 = Q, 1 = K, 2 = V
+    if (nt < q_tiles) {
+      region = 0;
+      t = nt;
+    } else if (nt < q_tiles + kv_tiles) {
+      region = 1;
+      t = nt - q_tiles;
+    } else {
+      region = 2;
+      t = nt - q_tiles - kv_tiles;
+    }
+    const int head = t / tph, jj = t % tph;
+    const int q_dim = a->n_q * hd;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = quad * 4 + i;
+      const bool valid = row < M;
+      const int pos = valid ? c->pos[row] : 0;
+      const int slot = L + row;
+      const float x = v[i];
+      const float partner = __shfl_xor(x, 8);
+      if (region < 2) {
+        const int m = 8 * jj + (col & 7);
+        const int dim = (col < 8) ? m : half + m;
+        const uint64_t csb = gbl(reinterpret_cast<const uint64_t*>(a->rope))[(long)pos * half + m];
+        const float2 cs = make_float2(__uint_as_float((uint32_t)csb), __uint_as_float((uint32_t)(csb >> 32)));
+        const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
+        if (valid) {
+          if (region == 0) {
+            st_wt(g.q_out + (long)row * q_dim + head * hd + dim, y);
+          } else {  // block keys go to cache slots L + row as two bf16 planes, y ~= hi + lo
+            const long ix = ((long)head * a->Lcap + slot) * hd + dim;
+            const uint32_t hb = f2bf(y);
+            st_wt(g.kc + ix, (uint16_t)hb);
+            st_wt(g.kc + ix + a->plane, (uint16_t)f2bf(y - bf2f(hb)));
+          }
+        }
+      } else if (valid) {
+        const int dim = jj * 16 + col;
+        const long ix = ((long)head * hd + dim) * a->Lcap + slot;
+        const uint32_t hb = f2bf(x);
+        st_wt(g.vt + ix, (uint16_t)hb);
+        st_wt(g.vt + ix + a->plane, (uint16_t)f2bf(x - bf2f(hb)));
+      }
+    }
+  } else if constexpr (EPI == EPI_ARGMAX) {
+    const int vc = nt * 16 + col;
+    const bool ok = vc < a->V;
+    float bv[4];
+    int bix[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = quad * 4 + i;
+      if (ok && c->logits && row < M) c->logits[(long)row * a->V + vc] = v[i];
+      bv[i] = ok ? v[i] : -INFINITY;
+      bix[i] = ok ? vc : 0x7FFFFFFF;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) {
+        const float ov = __shfl_xor(bv[i], off);
+        const int oi = __shfl_xor(bix[i], off);
+        if (ov > bv[i] || (ov == bv[i] && oi < bix[i])) {
+          bv[i] = ov;
+          bix[i] = oi;
         }
       }
+    if (col == 0)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s_bv[j * 16 + quad * 4 + i] = bv[i];
+        s_bi[j * 16 + quad * 4 + i] = bix[i];
+      }
+  }
+}
+
+// One GEMM phase, y = x W^T for the 16 block rows.  The work-groups form R = blocks / kg
+// output ranges of consecutive n-tiles (sizes differ by at most one tile), kg work-groups
+// per range, work-group k of a range taking the k-th of kg near-equal parts of the K
+// range.  A work-group walks its n-tiles in chunks of TN; its 8 waves split its K part
+// into 8 contiguous slices, and a wave accumulates all TN tiles of a chunk over its slice,
+// so each A fragment it loads serves TN weight tiles.  Loads form one stream per wave,
+// one k-tile (TN weight tiles and the hi/lo A fragments) per step, NS steps in flight in
+// NS register sets that rotate; slices are padded to a multiple of NS steps with zero A
+// fragments (the weight loads of padding steps re-read a real tile).  The loop body has
+// no conditional loads, so the compiler's memory wait counts stay exact.  At the end of a
+// chunk the waves' sums meet in LDS and are added in wave order; with kg = 1 wave j then
+// finishes tile j of the chunk, otherwise it stores the work-group's partial tile and the
+// last work-group of the range to arrive adds the kg partials in K order and finishes the
+// range's tiles, so results never depend on timing.  The first NS steps of weights are
+// requested before the grid barrier: they do not depend on the previous phase.
+template <int EPI, int TN>
+__device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const PhaseCtl& pc, bool& failed,
+                           u32x4* smem) {
+  constexpr int NS = TN >= 8 ? 2 : 4;
+  static_assert(TN <= kTNMax && TN <= kWaves, "one tile per wave in the chunk epilogue");
+  f32x4* red = reinterpret_cast<f32x4*>(smem);
+  float* s_rstd = reinterpret_cast<float*>(reinterpret_cast<char*>(smem) + kLdsRedBytes);
+  float* s_bv = s_rstd + 16;                        // ARGMAX: [TN][16]
+  int* s_bi = reinterpret_cast<int*>(s_bv + kTNMax * 16);
+  int* s_flag = s_bi + kTNMax * 16;
+
+  // every lane-dependent value of a phase derives from a laundered thread index, so that the
+  // compiler cannot hoist it out of the phase loop and keep it in registers for all phases
+  const int tid = opaque(threadIdx.x), lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nblk = gridDim.x, b = blockIdx.x;
+  const int R = nblk / kg, kgi = b % kg, rg = b / kg;
+  const int Nt = g.Nt, Kt = g.Kt;
+  const int t0 = (int)((long)rg * Nt / R), t1 = (int)((long)(rg + 1) * Nt / R);
+  const int T = t1 - t0;
+  const int nch = (T + TN - 1) / TN;
+  const int kb = (int)((long)kgi * Kt / kg), ke = (int)((long)(kgi + 1) * Kt / kg);
+  const int k0 = kb + (wave * (ke - kb)) / kWaves, k1 = kb + ((wave + 1) * (ke - kb)) / kWaves;
+  // steps per chunk: the longest slice rounded up to a multiple of NS (the same for every
+  // wave, so that all waves reach each chunk end together)
+  const int slice = (ke - kb + kWaves - 1) / kWaves;
+  const int nbr = max(NS, ((slice + NS - 1) / NS) * NS);
+  const int total = T > 0 ? nch * nbr : 0;
+  const int M = a->B;
+  const int kw_last = max(k1 - 1, 0);
+
+  const GLOBAL u32x4* Wg = gbl(g.W) + lane;
+  const GLOBAL u32x4* Ah = gbl(g.Ahi) + lane;
+  const GLOBAL u32x4* Al = gbl(g.Alo) + lane;
+  const GLOBAL u32x4* Zt = gbl(a->zero) + lane;
+
+  // step s of the stream: chunk s / nbr, k-tile k0 + s % nbr.  Steps past the stream's end
+  // (the loop's look-ahead) re-read the last real tile with zero A fragments.
+  auto load_w = [&](u32x4 (&w)[TN], int s) {
+    const int ch = min(s / nbr, nch - 1);
+    const int k = min(k0 + (s - ch * nbr), kw_last);
+    const int tl = min(TN, T - ch * TN) - 1;  // last real tile of the chunk
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int nt = t0 + ch * TN + min(j, tl);
+      w[j] = __builtin_nontemporal_load(Wg + ((long)nt * Kt + k) * 64);
+    }
+  };
+  auto load_a = [&](u32x4& hv, u32x4& lv, int s) {
+    const int ch = s / nbr;
+    const int k = k0 + (s - ch * nbr);
+    const bool real = k < k1 && s < total;
+    hv = *(real ? Ah + (long)k * 64 : Zt);
+    lv = *(real ? Al + (long)k * 64 : Zt);
+  };
+
+  float best_v = -INFINITY;  // ARGMAX: running best of the work-group per row (threads < 16)
+  int best_i = 0x7FFFFFFF;
+
+  u32x4 w[NS][TN], ah[NS], al[NS];
+  if (total > 0) {
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      load_w(w[i], i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  phase_begin(a, c, pc, failed);
+  if (total > 0) {
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      load_a(ah[i], al[i], i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  // sums of squares of the RMSNorm input: thread (row, part) sums tiles part, part+16, ...
+  // (threads 256.. repeat 0..255); loads unconditional with clamped indices, so that no
+  // branch precedes the loop; values past the last tile are dropped when summed.
+  const int n_st = a->H / 16;
+  float stv[16];
+  if (g.stats) {
+    const int row = (tid >> 4) & 15, part = tid & 15;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) stv[q] = gbl(g.stats)[min(part + 16 * q, n_st - 1) * kStatsPad + row];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  f32x4 acc[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // end of chunk ch: the waves' partial sums meet in LDS; wave j finishes tile j
+  auto chunk_end = [&](int ch) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      red[(wave * TN + j) * 64 + lane] = acc[j];
+      acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (ch == 0 && g.stats && tid < 256) {  // 1/rms of the rows: (x*g/rms) W^T = (1/rms) (x*g) W^T
+      const int row = tid >> 4;
+      float s = 0.f;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) s += ((tid & 15) + 16 * q < n_st) ? stv[q] : 0.f;
+      for (int t = (tid & 15) + 256; t < n_st; t += 16) s += gbl(g.stats)[t * kStatsPad + row];
       s += __shfl_xor(s, 8);
       s += __shfl_xor(s, 4);
       s += __shfl_xor(s, 2);
       s += __shfl_xor(s, 1);
-      if (part == 0) s_rstd[row] = rsqrtf(s * a.inv_dim + a.eps);
+      if ((tid & 15) == 0) s_rstd[row] = (row < M) ? rsqrtf(s / a->H + a->eps) : 0.f;
     }
     __syncthreads();
+    const int tn_c = min(TN, T - ch * TN);
+    if (wave < tn_c) {
+      const f32x4* rp = red + wave * 64 + lane;
+      f32x4 v = rp[0];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] *= s_rstd[quad * 4 + i];
-  }
-
-  // epilogues.  The owner lane holds rows mt*16 + 4*quad + i (i < 4) of output column nt*16 + col.
-  const EpiArgs& e = a.e;
-  if constexpr (EPI == EPI_RESID) {
-    if (has_tile) {
-      const int k = nt * 16 + col;
-      const float gn = e.next_gain[k];
-      float sq[4];
+      for (int q = 1; q < kWaves; ++q) v += rp[q * TN * 64];
+      if (g.stats) {
+        const int quad = (opaque(threadIdx.x) & 63) >> 4;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = mt * 16 + quad * 4 + i;
-        float x = 0.f;
-        if (row < M) {
-          float* p = e.out + (long)row * e.ldo + k;
-          x = *p + v[i];
-          *p = x;
-        }
-        sq[i] = x * x;
-        const float y = x * gn;
-        const float y1 = __shfl_xor(y, 1);
-        if ((col & 1) == 0 && row < M) store_frag_pair(e.na_hi, e.na_lo, row, k, e.na_Kt, y, y1);
+        for (int i = 0; i < 4; ++i) v[i] *= s_rstd[quad * 4 + i];
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sq[i] += __shfl_xor(sq[i], 1);
-        sq[i] += __shfl_xor(sq[i], 2);
-        sq[i] += __shfl_xor(sq[i], 4);
-        sq[i] += __shfl_xor(sq[i], 8);
-      }
-      if (col == 0)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = mt * 16 + quad * 4 + i;
-          if (row < M) e.stats_out[(long)row * e.n_stat_out + nt] = sq[i];
-        }
-    }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    if (has_tile) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float g = v[i];
-        const float up = __shfl_xor(g, 8);
-        const float hv = (col < 8) ? g / (1.0f + expf(-g)) * up : 0.f;
-        const float h1 = __shfl_xor(hv, 1);
-        const int row = mt * 16 + quad * 4 + i;
-        if (col < 8 && (col & 1) == 0 && row < M) store_frag_pair(e.na_hi, e.na_lo, row, nt * 8 + col, e.na_Kt, hv, h1);
+      if (kg > 1) {
+        f32x4* pp = reinterpret_cast<f32x4*>(a->part) + (((long)b * kTNMax + wave) * 64 + lane);
+        st_wt16(pp, __builtin_bit_cast(u32x4, v));
+      } else {
+        gemm_epilogue<EPI>(a, c, g, t0 + ch * TN + wave, v, wave, s_bv, s_bi);
       }
     }
-  } else if constexpr (EPI == EPI_QKV || EPI == EPI_KVT) {
-    if (has_tile) {
-      const int L = e.params->L;
-      const int tph = e.hd / 16, half = e.hd / 2;
-      uint16_t* kc = e.kc + (EPI == EPI_KVT ? layer * e.cache_layer_stride : 0);
-      uint16_t* vt = e.vt + (EPI == EPI_KVT ? layer * e.cache_layer_stride : 0);
-      int region, t;  // 0 = Q, 1 = K, 2 = V
-      if (nt < e.q_tiles) { region = 0; t = nt; }
-      else if (nt < e.q_tiles + e.kv_tiles) { region = 1; t = nt - e.q_tiles; }
-      else { region = 2; t = nt - e.q_tiles - e.kv_tiles; }
-      const int head = t / tph, jj = t % tph;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = mt * 16 + quad * 4 + i;
-        const bool valid = (EPI == EPI_QKV) ? (row < e.B) : (row < M);
-        const int pos = valid ? ((EPI == EPI_QKV) ? e.params->pos[row] : L + row) : 0;
-        const int slot = L + row;
-        const float x = v[i];
-        const float partner = __shfl_xor(x, 8);
-        if (region < 2) {
-          const int m = 8 * jj + (col & 7);
-          const int dim = (col < 8) ? m : half + m;
-          const float2 cs = e.rope[(long)pos * half + m];
-          const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
-          if (valid) {
-            if (region == 0) {
-              e.out[(long)row * e.ldo + head * e.hd + dim] = y;
-            } else {  // the cache keeps y as two bf16 planes, y ~= hi + lo
-              const long ix = ((long)head * e.Lcap + slot) * e.hd + dim;
-              const uint32_t hb = f2bf(y);
-              kc[ix] = (uint16_t)hb;
-              kc[ix + e.plane] = (uint16_t)f2bf(y - bf2f(hb));
-            }
+    if constexpr (EPI == EPI_ARGMAX) {
+      __syncthreads();
+      if (tid < 16)
+        for (int j = 0; j < tn_c; ++j) {  // tile order: ties keep the lowest token id
+          const float ov = s_bv[j * 16 + tid];
+          const int oi = s_bi[j * 16 + tid];
+          if (ov > best_v || (ov == best_v && oi < best_i)) {
+            best_v = ov;
+            best_i = oi;
           }
-        } else if (valid) {
-          const int dim = jj * 16 + col;
-          const long ix = ((long)head * e.hd + dim) * e.Lcap + slot;
-          const uint32_t hb = f2bf(x);
-          vt[ix] = (uint16_t)hb;
-          vt[ix + e.plane] = (uint16_t)f2bf(x - bf2f(hb));
         }
-      }
     }
-  } else if constexpr (EPI == EPI_ARGMAX) {
-    if (owner) {
-      const int c = nt * 16 + col;
-      const bool ok = has_tile && c < e.vocab;
-      float bv[4];
-      int bi[4];
+    __syncthreads();  // LDS is reused by the next chunk
+  };
+
+  // The scheduling barriers keep each set's reload right after its MFMAs: left alone, the
+  // compiler sinks a reload past the other sets' MFMAs, and the wait for the next set then
+  // drains every load in flight.
+  for (int s0 = 0; s0 < total; s0 += NS) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = quad * 4 + i;
-        if (ok && e.logits && row < e.B) e.logits[(long)row * e.vocab + c] = v[i];
-        bv[i] = ok ? v[i] : -INFINITY;
-        bi[i] = ok ? c : 0x7FFFFFFF;
+    for (int i = 0; i < NS; ++i) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        acc[j] = mfma(ah[i], w[i][j], acc[j]);
+        acc[j] = mfma(al[i], w[i][j], acc[j]);
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) {
-          const float ov = __shfl_xor(bv[i], off);
-          const int oi = __shfl_xor(bi[i], off);
-          if (ov > bv[i] || (ov == bv[i] && oi < bi[i])) { bv[i] = ov; bi[i] = oi; }
-        }
-      if (col == 0)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) { s_bv[wave][quad * 4 + i] = bv[i]; s_bi[wave][quad * 4 + i] = bi[i]; }
+      __builtin_amdgcn_sched_barrier(0);
+      load_w(w[i], s0 + NS + i);
+      load_a(ah[i], al[i], s0 + NS + i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const int done = s0 + NS;
+    if (done % nbr == 0) chunk_end(done / nbr - 1);
+  }
+
+  if (kg > 1 && total > 0) {
+    // split K: the last work-group of the range to arrive adds the partials in K order
+    wait_vm();
+    __syncthreads();
+    if (tid == 0) {
+      const unsigned old = __hip_atomic_fetch_add(g.cnt + rg * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *s_flag = (old + 1u == g.target) ? 1 : 0;
     }
     __syncthreads();
-    if (tid < 16) {  // this block's best per row; the combine kernel picks across blocks
-      float bvv = s_bv[0][tid];
-      int ix = s_bi[0][tid];
-      for (int w = 1; w < NT; ++w) {
-        const float ov = s_bv[w][tid];
-        const int oi = s_bi[w][tid];
-        if (ov > bvv || (ov == bvv && oi < ix)) { bvv = ov; ix = oi; }
-      }
-      e.pmax[(long)tid * groups + group] = bvv;
-      e.pidx[(long)tid * groups + group] = ix;
+    if (*s_flag && wave < T) {
+      const f32x4* pp = reinterpret_cast<const f32x4*>(a->part) + (((long)rg * kg * kTNMax + wave) * 64 + lane);
+      f32x4 v = ld_coh16(pp);
+      for (int q = 1; q < kg; ++q) v += ld_coh16(pp + (long)q * kTNMax * 64);
+      gemm_epilogue<EPI>(a, c, g, t0 + wave, v, wave, s_bv, s_bi);
     }
   }
-}
 
-// per-row argmax over the blocks' partial results (ties: lowest token id)
-__global__ __launch_bounds__(256) void k_argmax_combine(const float* pmax, const int* pidx, int groups,
-                                                        int* tokens) {
-  __shared__ float s_v[4];
-  __shared__ int s_i[4];
-  const int row = blockIdx.x, tid = threadIdx.x;
-  float v = -INFINITY;
-  int ix = 0x7FFFFFFF;
-  for (int g = tid; g < groups; g += 256) {
-    const float ov = pmax[(long)row * groups + g];
-    const int oi = pidx[(long)row * groups + g];
-    if (ov > v || (ov == v && oi < ix)) { v = ov; ix = oi; }
-  }
+  if constexpr (EPI == EPI_ARGMAX) {
+    // The work-group's best per row; the last work-group to finish picks across all of them.
+    if (tid < 16) {
+      st_wt(a->pmax + b * kStatsPad + tid, best_v);
+      st_wt(a->pidx + b * kStatsPad + tid, best_i);
+    }
+    wait_vm();
+    __syncthreads();
+    if (tid == 0) {
+      const unsigned old = __hip_atomic_fetch_add(a->done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *s_flag = (old == (c->done_epoch + 1u) * (unsigned)nblk - 1u) ? 1 : 0;
+    }
+    __syncthreads();
+    if (*s_flag)  // wave w reduces rows w, w + 8 over the work-groups
+      for (int row = wave; row < M; row += kWaves) {
+        float v = -INFINITY;
+        int ix = 0x7FFFFFFF;
+        for (int w2 = lane; w2 < nblk; w2 += 64) {
+          const float ov = ld_coh(a->pmax + w2 * kStatsPad + row);
+          const int oi = ld_coh(a->pidx + w2 * kStatsPad + row);
+          if (ov > v || (ov == v && oi < ix)) {
+            v = ov;
+            ix = oi;
+          }
+        }
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float ov = __shfl_xor(v, off);
-    const int oi = __shfl_xor(ix, off);
-    if (ov > v || (ov == v && oi < ix)) { v = ov; ix = oi; }
-  }
-  if ((tid & 63) == 0) {
-    s_v[tid >> 6] = v;
-    s_i[tid >> 6] = ix;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    for (int w = 1; w < 4; ++w)
-      if (s_v[w] > v || (s_v[w] == v && s_i[w] < ix)) { v = s_v[w]; ix = s_i[w]; }
-    tokens[row] = (ix == 0x7FFFFFFF) ? 0 : ix;
+        for (int off = 1; off < 64; off <<= 1) {
+          const float ov = __shfl_xor(v, off);
+          const int oi = __shfl_xor(ix, off);
+          if (ov > v || (ov == v && oi < ix)) {
+            v = ov;
+            ix = oi;
+          }
+        }
+        if (lane == 0) c->tokens[row] = (ix == 0x7FFFFFFF) ? 0 : ix;
+      }
   }
 }
 
-// ------------------------------------------------------------------------------------------
-// block attention, split over the key axis (Sec. 3.2: no mask, every block row sees the
-// whole context and the whole block).  Block (chunk c, KV head g) of 8 waves: chunk c holds
-// keys [c*CK, (c+1)*CK) of the context, the last chunk also the B block keys (cache slots
-// L..L+B-1).  K rows and V^T rows of the chunk, both bf16 planes (hi, lo), are copied to LDS
-// with every load in flight at once (16-byte pieces, XOR-swizzled columns so that the
-// fragment reads of 16 different rows hit different banks).  Wave w then takes query tile w:
-// rows r = w*16 + lane%16 of the G*B rows that share head g (r -> query head g*G + r/B, block
-// position r%B).  Scores are formed transposed, S^T = K Q^T, so that the probabilities land in
-// exactly the B-operand layout of the P V product and never leave registers.  Products of
-// two hi/lo pairs keep the three terms above 2^-16 relative: hi*hi + hi*lo + lo*hi.
-// ------------------------------------------------------------------------------------------
-template <int HD, int CK>
-__global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
-  constexpr int CKM = CK + 32;   // keys held by a block (room for the B <= 16 block keys)
+// ---- ATTN: block attention, split over the key axis ----
+// Sec. 3.2: no mask; every block row attends to the whole context and the whole block.
+// Work item (chunk c, KV head g): keys [c*CK, (c+1)*CK) of the context, the last chunk also
+// the B block keys (cache slots L .. L+B-1, written by the QKV phase).  K rows and V^T rows
+// of the chunk, both bf16 planes (hi, lo), are staged in LDS (16-byte pieces, XOR-swizzled
+// columns so that fragment reads of 16 different rows hit different banks).  The pieces of
+// context keys are requested before the grid barrier; only the block keys and the queries
+// depend on the QKV phase, and the early requests never touch a cache line that the QKV
+// phase writes (K rows are whole lines; a V^T line is requested early only if all its 64
+// slots are context).  Wave w < QT then takes query tile w: rows r = w*16 + lane%16 of
+// the G*B rows that share head g (r -> query head g*G + r/B, block row r%B).  Scores are
+// formed transposed, S^T = K Q^T, so that the probabilities land in exactly the B-operand
+// layout of the P V product and never leave registers.  Products of two hi/lo pairs keep
+// the three terms above 2^-16 relative: hi*hi + hi*lo + lo*hi.
+template <int HD>
+__device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed,
+                           u32x4* smem) {
+  constexpr int CK = kChunk;
+  constexpr int CKM = CK + 32;   // keys held by a work-group (room for the B <= 16 block keys)
   constexpr int KC = HD / 8;     // 16-byte columns of a K row
   constexpr int VC = CKM / 8;    // 16-byte columns of a V^T row (a multiple of 4)
   constexpr int KPC = 2 * CKM * KC, VPC = 2 * HD * VC;  // pieces of both planes
-  constexpr int PER = (KPC + VPC) / 512;                 // pieces per thread
-  static_assert(KPC % 512 == 0 && VPC % 512 == 0, "piece counts must split evenly over the block");
-  __shared__ u32x4 sK[2][CKM * KC];  // (row r, column c) at r*KC + (c ^ (r & 7))
-  __shared__ u32x4 sV[2][HD * VC];   // (row d, column c) at d*VC + (c ^ (d & 3))
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int quad = lane >> 4, q = lane & 15;
-  const int g = blockIdx.y, c = blockIdx.x;
-  const int L = a.params->L;
-  const int nch = max(1, (L + CK - 1) / CK);
-  if (c >= nch) return;
-  const int kbeg = c * CK;
-  const int kend = (c == nch - 1) ? L + a.B : kbeg + CK;
-  const int nkeys = kend - kbeg;  // <= CK + B
-  const int G = a.n_q / a.n_kv;
-  const int R = G * a.B;
+  constexpr int PER = (KPC + VPC) / kThreads;          // pieces per thread
+  static_assert((KPC + VPC) % kThreads == 0, "pieces must split evenly over the work-group");
+  u32x4* sK = smem;                 // [2][CKM * KC]: (row r, column c) at r*KC + (c ^ (r & 7))
+  u32x4* sV = smem + 2 * CKM * KC;  // [2][HD * VC]:  (row d, column c) at d*VC + (c ^ (d & 3))
 
-  // 1. issue every piece of the chunk and this wave's query row
-  u32x4 pc[PER];
+  const int tid = opaque(threadIdx.x), lane = tid & 63, w = tid >> 6;
+  const int quad = lane >> 4, q = lane & 15;
+  const int L = dc->L;
+  const int nch = max(1, (L + CK - 1) / CK);
+  const int items = nch * a->n_kv;
+  const int G = a->n_q / a->n_kv;
+  const int R = G * a->B;
+  const uint16_t* kc = a->kc + layer * a->cache_layer;
+  const uint16_t* vt = a->vt + layer * a->cache_layer;
+  const float* Q = a->Q + layer * a->q_stride;
+  const int q_dim = a->n_q * HD;
+
+  // request the pieces of item j: pass 0 = context keys only, pass 1 = the rest.  The thread
+  // index is laundered through an empty asm statement so that the compiler recomputes the
+  // piece coordinates here instead of keeping them in registers for the whole kernel.
+  auto issue = [&](int j, int pass, u32x4 (&pcs)[PER]) {
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int c = j / a->n_kv, g = j % a->n_kv;
+    const int kbeg = c * CK;
+    const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + CK) - kbeg;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int p = i * 512 + tid;
-    pc[i] = u32x4{0u, 0u, 0u, 0u};
-    if (p < KPC) {  // uniform for a given i
-      const int pl = p / (CKM * KC), rem = p % (CKM * KC);
-      const int r = rem / KC, col = rem % KC;
-      if (r < nkeys)
-        pc[i] = *reinterpret_cast<const u32x4*>(a.kc + pl * a.plane + ((long)g * a.Lcap + kbeg + r) * HD + col * 8);
-    } else {
-      const int pv = p - KPC;
-      const int pl = pv / (HD * VC), rem = pv % (HD * VC);
-      const int d = rem / VC, col = rem % VC;
-      if (col * 8 < nkeys)
-        pc[i] = *reinterpret_cast<const u32x4*>(a.vt + pl * a.plane + ((long)g * HD + d) * a.Lcap + kbeg + col * 8);
+    for (int i = 0; i < PER; ++i) {
+      const int p = i * kThreads + tid;
+      if (p < KPC) {
+        const int pl = p / (CKM * KC), rem = p % (CKM * KC);
+        const int r = rem / KC, col = rem % KC;
+        const bool ctx = kbeg + r < L;
+        if (r < nkeys && (pass == 0 ? ctx : !ctx))
+          pcs[i] = *gbl(reinterpret_cast<const u32x4*>(kc + pl * a->plane + ((long)g * a->Lcap + kbeg + r) * HD + col * 8));
+      } else {
+        const int pv = p - KPC;
+        const int pl = pv / (HD * VC), rem = pv % (HD * VC);
+        const int d = rem / VC, col = rem % VC;
+        // requested early only if its whole 128-byte line (64 keys) precedes slot L: the line
+        // holding slot L also receives the block's values in the QKV phase
+        const bool ctx = ((kbeg + col * 8) & ~63) + 64 <= L;
+        if (col * 8 < nkeys && (pass == 0 ? ctx : !ctx))
+          pcs[i] = *gbl(reinterpret_cast<const u32x4*>(vt + pl * a->plane + ((long)g * HD + d) * a->Lcap + kbeg + col * 8));
+      }
     }
-  }
-  const int r = w * 16 + q;
-  const bool active = w * 16 < R;  // wave-uniform
-  const bool rv = r < R;
-  float4 qx[HD / 16];
-  {
-    const int b = rv ? r % a.B : 0;
-    const int h = g * G + (rv ? r / a.B : 0);
+  };
+
+  // everything of item j after its context pieces were requested
+  auto finish = [&](int j, u32x4 (&pcs)[PER]) {
+    issue(j, 1, pcs);
+    const int c = j / a->n_kv, g = j % a->n_kv;
+    const int kbeg = c * CK;
+    const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + CK) - kbeg;
+    const int r = w * 16 + q;
+    const bool active = w * 16 < R;  // wave-uniform
+    const bool rv = r < R;
+    float4 qx[HD / 16];
+    {
+      const int bb = rv ? r % a->B : 0;
+      const int h = g * G + (rv ? r / a->B : 0);
 #pragma unroll
-    for (int ks = 0; ks < HD / 32; ++ks) {
-      const float* src = a.Q + (long)b * a.q_dim + h * HD + ks * 32 + quad * 8;
-      qx[2 * ks] = (active && rv) ? *reinterpret_cast<const float4*>(src) : make_float4(0.f, 0.f, 0.f, 0.f);
-      qx[2 * ks + 1] = (active && rv) ? *reinterpret_cast<const float4*>(src + 4) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-  }
-  // 2. pieces to LDS (keys past the end become zeros)
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int p = i * 512 + tid;
-    if (p < KPC) {
-      const int pl = p / (CKM * KC), rem = p % (CKM * KC);
-      const int rr = rem / KC, col = rem % KC;
-      sK[pl][rr * KC + (col ^ (rr & 7))] = pc[i];
-    } else {
-      const int pv = p - KPC;
-      const int pl = pv / (HD * VC), rem = pv % (HD * VC);
-      const int d = rem / VC, col = rem % VC;
-      u32x4 v = pc[i];
-      const int nv = nkeys - col * 8;  // valid keys in this piece
-      if (nv < 8) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          if (2 * e >= nv) v[e] = 0u;
-          else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        const float* src = Q + (long)bb * q_dim + h * HD + ks * 32 + quad * 8;
+        qx[2 * ks] = make_float4(0.f, 0.f, 0.f, 0.f);
+        qx[2 * ks + 1] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (active && rv) {
+          const u32x4 q0 = *gbl(reinterpret_cast<const u32x4*>(src));
+          const u32x4 q1 = *gbl(reinterpret_cast<const u32x4*>(src + 4));
+          qx[2 * ks] = make_float4(__uint_as_float(q0[0]), __uint_as_float(q0[1]), __uint_as_float(q0[2]),
+                                   __uint_as_float(q0[3]));
+          qx[2 * ks + 1] = make_float4(__uint_as_float(q1[0]), __uint_as_float(q1[1]), __uint_as_float(q1[2]),
+                                       __uint_as_float(q1[3]));
         }
       }
-      sV[pl][d * VC + (col ^ (d & 3))] = v;
     }
-  }
-  __syncthreads();
-  if (!active) return;
+    // pieces to LDS (keys past the end become zeros)
+    int tid2 = threadIdx.x;
+    asm volatile("" : "+v"(tid2));
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int p = i * kThreads + tid2;
+      if (p < KPC) {
+        const int pl = p / (CKM * KC), rem = p % (CKM * KC);
+        const int rr = rem / KC, col = rem % KC;
+        sK[pl * CKM * KC + rr * KC + (col ^ (rr & 7))] = pcs[i];
+      } else {
+        const int pv = p - KPC;
+        const int pl = pv / (HD * VC), rem = pv % (HD * VC);
+        const int d = rem / VC, col = rem % VC;
+        u32x4 v = pcs[i];
+        const int nv = nkeys - col * 8;  // valid keys in this piece
+        if (nv < 8) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (2 * e >= nv) v[e] = 0u;
+            else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;
+          }
+        }
+        sV[pl * HD * VC + d * VC + (col ^ (d & 3))] = v;
+      }
+    }
+    __syncthreads();
+    if (active) {
+      u32x4 qh[HD / 32], ql[HD / 32];
+#pragma unroll
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        const float4 x0 = qx[2 * ks], x1 = qx[2 * ks + 1];
+        float v[8] = {x0.x * a->qscale, x0.y * a->qscale, x0.z * a->qscale, x0.w * a->qscale,
+                      x1.x * a->qscale, x1.y * a->qscale, x1.z * a->qscale, x1.w * a->qscale};
+        split_pack8(v, qh[ks], ql[ks]);
+      }
+      // LDS read addresses: per-lane byte bases plus compile-time offsets below 64 KiB, so
+      // that every read takes its offset as an immediate (row kt*16 + q has swizzle key
+      // q & 7; row d = dt*16 + q has key q & 3).  The bases are laundered so that the
+      // compiler neither folds the large plane offsets into per-read registers nor keeps
+      // them alive outside this block.
+      const char* lds = reinterpret_cast<const char*>(smem);
+      const int ln = opaque(threadIdx.x & 63);
+      const int q = ln & 15, quad = ln >> 4;
+      int kh_at[HD / 32], kl_at[HD / 32];
+#pragma unroll
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        kh_at[ks] = opaque((q * KC + ((ks * 4 + quad) ^ (q & 7))) * 16);
+        kl_at[ks] = opaque(kh_at[ks] + CKM * KC * 16);
+      }
+      const int vx = (quad >> 1) ^ (q & 3);
+      const int vbase = 2 * CKM * KC * 16 + (quad & 1) * 8;  // sV, half of a 16-byte column
+      const int vh0 = opaque(vbase + (q * VC + vx) * 16), vh1 = opaque(vbase + (q * VC + (vx ^ 2)) * 16);
+      const int vl0 = opaque(vh0 + HD * VC * 16), vl1 = opaque(vh1 + HD * VC * 16);
+      f32x4 s[CKM / 16];
+#pragma unroll
+      for (int kt = 0; kt < CKM / 16; ++kt) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < HD / 32; ++ks) {
+          const u32x4 kh = *reinterpret_cast<const u32x4*>(lds + kh_at[ks] + kt * 16 * KC * 16);
+          const u32x4 kl = *reinterpret_cast<const u32x4*>(lds + kl_at[ks] + kt * 16 * KC * 16);
+          acc = mfma(kh, qh[ks], acc);
+          acc = mfma(kh, ql[ks], acc);
+          acc = mfma(kl, qh[ks], acc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (kt * 16 + quad * 4 + i >= nkeys) acc[i] = -INFINITY;
+        s[kt] = acc;
+        __builtin_amdgcn_sched_barrier(0);  // bound how far LDS reads are hoisted (registers)
+      }
+      // softmax statistics per query row (column q), in the log2 domain
+      float m = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < CKM / 16; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m = fmaxf(m, s[kt][i]);
+      m = fmaxf(m, __shfl_xor(m, 16));
+      m = fmaxf(m, __shfl_xor(m, 32));
+      float l = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < CKM / 16; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float p = exp2f(s[kt][i] - m);
+          s[kt][i] = p;
+          l += p;
+        }
+      l += __shfl_xor(l, 16);
+      l += __shfl_xor(l, 32);
+      // O^T = V^T P^T over the chunk
+      f32x4 o[HD / 16];
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < CKM / 32; ++kk) {
+        float pv[8] = {s[2 * kk][0], s[2 * kk][1], s[2 * kk][2], s[2 * kk][3],
+                       s[2 * kk + 1][0], s[2 * kk + 1][1], s[2 * kk + 1][2], s[2 * kk + 1][3]};
+        u32x4 ph, pl;
+        split_pack8(pv, ph, pl);
+        // keys kk*32 + 4*quad + 0..3 and + 16: 16-byte columns kk*4 + quad/2 and + 2, halves quad & 1
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt) {
+          const int off = (dt * 16 * VC + kk * 4) * 16;
+          const u32x2 h0 = *reinterpret_cast<const u32x2*>(lds + vh0 + off);
+          const u32x2 h1 = *reinterpret_cast<const u32x2*>(lds + vh1 + off);
+          const u32x2 l0 = *reinterpret_cast<const u32x2*>(lds + vl0 + off);
+          const u32x2 l1 = *reinterpret_cast<const u32x2*>(lds + vl1 + off);
+          const u32x4 vh = {h0[0], h0[1], h1[0], h1[1]};
+          const u32x4 vl = {l0[0], l0[1], l1[0], l1[1]};
+          o[dt] = mfma(vh, ph, o[dt]);
+          o[dt] = mfma(vh, pl, o[dt]);
+          o[dt] = mfma(vl, ph, o[dt]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (rv) {
+        const long base = ((long)c * a->n_kv + g) * a->Rpad + r;
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt)
+          st_wt16(a->OP + base * HD + dt * 16 + quad * 4, __builtin_bit_cast(u32x4, o[dt]));
+        if (quad == 0)
+          st_wt8(a->ML + base, (uint64_t)__float_as_uint(m) | ((uint64_t)__float_as_uint(l) << 32));
+      }
+    }
+    __syncthreads();  // LDS is refilled by the next item
+  };
 
-  u32x4 qh[HD / 32], ql[HD / 32];
+  // The first item's context pieces are requested before the barrier.  Each item keeps its
+  // pieces in a register array of its own scope, so none stays live across items.
+  const int j0 = blockIdx.x;
+  {
+    u32x4 pcs[PER];
 #pragma unroll
-  for (int ks = 0; ks < HD / 32; ++ks) {
-    const float4 x0 = qx[2 * ks], x1 = qx[2 * ks + 1];
-    float v[8] = {x0.x * a.qscale, x0.y * a.qscale, x0.z * a.qscale, x0.w * a.qscale,
-                  x1.x * a.qscale, x1.y * a.qscale, x1.z * a.qscale, x1.w * a.qscale};
-    split_pack8(v, qh[ks], ql[ks]);
+    for (int i = 0; i < PER; ++i) pcs[i] = u32x4{0u, 0u, 0u, 0u};
+    if (j0 < items) issue(j0, 0, pcs);
+    phase_begin(a, dc, pc, failed);
+    if (j0 < items) finish(j0, pcs);
   }
-  f32x4 s[CKM / 16];
+  for (int j = j0 + gridDim.x; j < items; j += gridDim.x) {
+    u32x4 pcs[PER];
 #pragma unroll
-  for (int kt = 0; kt < CKM / 16; ++kt) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    const int rr = kt * 16 + q;
-#pragma unroll
-    for (int ks = 0; ks < HD / 32; ++ks) {
-      const int slot = rr * KC + ((ks * 4 + quad) ^ (rr & 7));
-      const u32x4 kh = sK[0][slot], kl = sK[1][slot];
-      acc = mfma(kh, qh[ks], acc);
-      acc = mfma(kh, ql[ks], acc);
-      acc = mfma(kl, qh[ks], acc);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (kt * 16 + quad * 4 + i >= nkeys) acc[i] = -INFINITY;
-    s[kt] = acc;
-  }
-  // softmax statistics per query row (column q), in the log2 domain
-  float m = -INFINITY;
-#pragma unroll
-  for (int kt = 0; kt < CKM / 16; ++kt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) m = fmaxf(m, s[kt][i]);
-  m = fmaxf(m, __shfl_xor(m, 16));
-  m = fmaxf(m, __shfl_xor(m, 32));
-  float l = 0.f;
-#pragma unroll
-  for (int kt = 0; kt < CKM / 16; ++kt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float p = exp2f(s[kt][i] - m);
-      s[kt][i] = p;
-      l += p;
-    }
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
-  // O^T = V^T P^T over the chunk
-  f32x4 o[HD / 16];
-#pragma unroll
-  for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const u32x2* v2h = reinterpret_cast<const u32x2*>(sV[0]);
-  const u32x2* v2l = reinterpret_cast<const u32x2*>(sV[1]);
-#pragma unroll
-  for (int kk = 0; kk < CKM / 32; ++kk) {
-    float pv[8] = {s[2 * kk][0], s[2 * kk][1], s[2 * kk][2], s[2 * kk][3],
-                   s[2 * kk + 1][0], s[2 * kk + 1][1], s[2 * kk + 1][2], s[2 * kk + 1][3]};
-    u32x4 ph, pl;
-    split_pack8(pv, ph, pl);
-    const int c0 = kk * 4 + (quad >> 1), half = quad & 1;  // keys kk*32 + 4*quad + 0..3 (+16)
-#pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) {
-      const int d = dt * 16 + q;
-      const int i0 = (d * VC + (c0 ^ (d & 3))) * 2 + half;
-      const int i1 = (d * VC + ((c0 + 2) ^ (d & 3))) * 2 + half;
-      const u32x2 h0 = v2h[i0], h1 = v2h[i1], l0 = v2l[i0], l1 = v2l[i1];
-      const u32x4 vh = {h0[0], h0[1], h1[0], h1[1]};
-      const u32x4 vl = {l0[0], l0[1], l1[0], l1[1]};
-      o[dt] = mfma(vh, ph, o[dt]);
-      o[dt] = mfma(vh, pl, o[dt]);
-      o[dt] = mfma(vl, ph, o[dt]);
-    }
-  }
-  if (rv) {
-    const long base = ((long)c * a.n_kv + g) * a.Rpad + r;
-#pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt)
-      *reinterpret_cast<f32x4*>(a.opart + base * HD + dt * 16 + quad * 4) = o[dt];
-    if (quad == 0) a.ml[base] = make_float2(m, l);
+    for (int i = 0; i < PER; ++i) pcs[i] = u32x4{0u, 0u, 0u, 0u};
+    issue(j, 0, pcs);
+    finish(j, pcs);
   }
 }
 
-// combine the chunk partials of one query row r of KV head g:
-// O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as the A fragments of the output
-// projection.  Block (r, g); thread (chunk slot cs, 8 dims d0..d0+7).
-template <int HD, int CK>
-__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
-  constexpr int DG = HD / 8, CS = 256 / DG;
-  __shared__ float s_red[256];
-  __shared__ float s_num[CS][HD];
-  const int r = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
-  const int G = a.n_q / a.n_kv;
-  const int R = G * a.B;
-  if (r >= R) return;
-  const int nch = max(1, (a.params->L + CK - 1) / CK);  // the last chunk also holds the block keys
-  const float2* ml = a.ml + (long)g * a.Rpad + r;  // chunk c at ml[c * n_kv * Rpad]
-  const long mstride = (long)a.n_kv * a.Rpad;
-  // 1. M = max_c m_c
-  float m = -INFINITY;
-  for (int c = tid; c < nch; c += 256) m = fmaxf(m, ml[c * mstride].x);
+// ---- COMB: merge the chunk partials of query row r of KV head g (one wave per row):
+// O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as the A fragments of the
+// output projection.  Chunks are added in ascending order.
+template <int HD>
+__device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed) {
+  constexpr int DPL = HD / 64;  // dims per lane
+  phase_begin(a, dc, pc, failed);
+  const int lane = opaque(threadIdx.x) & 63;
+  const int G = a->n_q / a->n_kv, R = G * a->B;
+  const int nch = max(1, (dc->L + kChunk - 1) / kChunk);
+  const int items = a->n_kv * R;
+  const int q_Kt = a->n_q * HD / 32;
+  uint32_t* ohi = reinterpret_cast<uint32_t*>(a->OA + layer * a->oa_stride);
+  uint32_t* olo = reinterpret_cast<uint32_t*>(a->OA + layer * a->oa_stride + (long)(q_Kt + kKtPad) * 64);
+  const long cstride = (long)a->n_kv * a->Rpad;
+  // item i goes to wave i / blocks of work-group i % blocks: the items spread over all CUs
+  for (int it = blockIdx.x + (threadIdx.x >> 6) * gridDim.x; it < items; it += gridDim.x * kWaves) {
+    const int g = it / R, r = it % R;
+    const float2* ml = a->ML + (long)g * a->Rpad + r;
+    float M = -INFINITY;
+    for (int c = lane; c < nch; c += 64) M = fmaxf(M, ld_coh2(ml + c * cstride).x);
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
-  if ((tid & 63) == 0) s_red[tid >> 6] = m;
-  __syncthreads();
-  const float M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
-  // 2. weighted sums; chunk slots in a fixed order
-  const int dg = tid % DG, cs = tid / DG, d0 = dg * 8;
-  float num[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  float den = 0.f;
-#pragma unroll 4
-  for (int c = cs; c < nch; c += CS) {
-    const float2 mc = ml[c * mstride];
-    const float wgt = exp2f(mc.x - M);
-    den += wgt * mc.y;
-    const float* op = a.opart + (((long)c * a.n_kv + g) * a.Rpad + r) * HD + d0;
-    const float4 o0 = *reinterpret_cast<const float4*>(op);
-    const float4 o1 = *reinterpret_cast<const float4*>(op + 4);
-    num[0] += wgt * o0.x; num[1] += wgt * o0.y; num[2] += wgt * o0.z; num[3] += wgt * o0.w;
-    num[4] += wgt * o1.x; num[5] += wgt * o1.y; num[6] += wgt * o1.z; num[7] += wgt * o1.w;
-  }
-  __syncthreads();
+    for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
+    float num[DPL], den = 0.f;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) s_num[cs][d0 + e] = num[e];
-  if (dg == 0) s_red[cs] = den;
-  __syncthreads();
-  if (tid < DG) {
-    float acc[8];
-    float dsum = 0.f;
+    for (int e = 0; e < DPL; ++e) num[e] = 0.f;
+    const float* op = a->OP + ((long)g * a->Rpad + r) * HD + lane * DPL;
+    // 32 chunks per batch, all their loads in flight together (one memory round trip)
+    for (int c0 = 0; c0 < nch; c0 += 32) {
+      float2 mc[32];
+      float ov[32][DPL];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-    for (int k = 0; k < CS; ++k) {
-      dsum += s_red[k];
+      for (int u = 0; u < 32; ++u) {
+        const int c = min(c0 + u, nch - 1);
+        mc[u] = ld_coh2(ml + c * cstride);
+        if constexpr (DPL == 2) {
+          const float2 t = ld_coh2(op + c * cstride * HD);
+          ov[u][0] = t.x;
+          ov[u][1] = t.y;
+        } else {
+          ov[u][0] = ld_coh(op + c * cstride * HD);
+        }
+      }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += s_num[k][tid * 8 + e];
+      for (int u = 0; u < 32; ++u) {
+        if (c0 + u < nch) {
+          const float wgt = exp2f(mc[u].x - M);
+          den += wgt * mc[u].y;
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) num[e] += wgt * ov[u][e];
+        }
+      }
     }
-    const float inv = 1.0f / dsum;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] *= inv;
-    const int b = r % a.B, h = g * G + r / a.B;
-    u32x4 hi, lo;
-    split_pack8(acc, hi, lo);
-    const long fo = frag_off(b, h * HD + tid * 8, a.oa_Kt) >> 3;
-    a.oa_hi[fo] = hi;
-    a.oa_lo[fo] = lo;
+    const float inv = 1.0f / den;
+    const int bb = r % a->B, h = g * G + r / a->B;
+    if constexpr (DPL == 2) {
+      store_frag_pair_wt(ohi, olo, bb, h * HD + 2 * lane, q_Kt, num[0] * inv, num[1] * inv);
+    } else {
+      const float y = num[0] * inv;
+      const float y1 = __shfl_xor(y, 1);
+      if ((lane & 1) == 0) store_frag_pair_wt(ohi, olo, bb, h * HD + lane, q_Kt, y, y1);
+    }
+  }
+}
+
+// GEMM phase with the plan's chunk width (the LM head always uses 8)
+template <int EPI>
+__device__ __forceinline__ void gemm_dispatch(Args a, Call c, GemmJob& g, int kind, int layer, const PhaseCtl& pc,
+                                              bool& failed, u32x4* smem) {
+  const int kg = a->kg[kind];
+  const int slot = kind == PH_QKV ? 0 : kind == PH_O ? 1 : kind == PH_GU ? 2 : 3;
+  g.cnt = a->kcnt + (long)slot * kMaxBlocks * 32;
+  g.target = (c->done_epoch * (unsigned)a->D + (unsigned)layer + 1u) * (unsigned)kg;
+  if constexpr (EPI == EPI_ARGMAX) {
+    gemm_phase<EPI, 8>(a, c, g, 1, pc, failed, smem);
+  } else {
+    switch (a->tn[kind]) {
+      case 2: gemm_phase<EPI, 2>(a, c, g, kg, pc, failed, smem); break;
+      case 4: gemm_phase<EPI, 4>(a, c, g, kg, pc, failed, smem); break;
+      case 6: gemm_phase<EPI, 6>(a, c, g, kg, pc, failed, smem); break;
+      default: gemm_phase<EPI, 8>(a, c, g, kg, pc, failed, smem); break;
+    }
+  }
+}
+
+// The single kernel argument is read in place through the kernel-argument pointer, so each
+// field is loaded where it is used instead of being held in scalar registers (or copied to
+// scratch memory, as a by-reference use of a parameter would) for the whole launch.
+template <int HD>
+__global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
+  __shared__ u32x4 smem[kLdsBytes / 16];
+  const CONSTANT DraftKernArgs* ka = (const CONSTANT DraftKernArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  const Args a = (const CONSTANT DraftArgs*)ka->a;
+  const Call c = &ka->c;
+  const int p0 = ka->p0, p1 = ka->p1;
+  const int nphase = phase_count(a->D);
+  const int nslots = 2 * nphase;  // trace: body start, then arrival (stores done), per phase
+  const int H = a->H, Kt_H = H / 32, q_Kt = a->n_q * a->hd / 32, F_Kt = a->F / 32;
+  bool failed = false;
+  for (int p = p0; p < p1; ++p) {
+    int kind, layer;
+    phase_of(p, a->D, kind, layer);
+    PhaseCtl pc;
+    pc.wait = p > p0;
+    pc.epoch = c->bar_epoch + (unsigned)(p - p0);
+    pc.slot = 2 * p;
+    pc.nslots = nslots;
+    GemmJob g{};
+    switch (kind) {
+      case PH_EMBED:
+        phase_begin(a, c, pc, failed);
+        phase_embed(a, c);
+        break;
+      case PH_QKV: {
+        const int s = 2 * layer;
+        g.W = a->w_qkv + layer * a->s_qkv;
+        g.Nt = (a->n_q + 2 * a->n_kv) * a->hd / 16;
+        g.Kt = Kt_H;
+        g.Ahi = a->XA + s * a->xa_stride;
+        g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
+        g.stats = a->XS + s * a->xs_stride;
+        g.q_out = a->Q + layer * a->q_stride;
+        g.kc = a->kc + layer * a->cache_layer;
+        g.vt = a->vt + layer * a->cache_layer;
+        gemm_dispatch<EPI_QKV>(a, c, g, kind, layer, pc, failed, smem);
+        break;
+      }
+      case PH_ATTN:
+        phase_attn<HD>(a, c, layer, pc, failed, smem);
+        break;
+      case PH_COMB:
+        phase_comb<HD>(a, c, layer, pc, failed);
+        break;
+      case PH_O:
+      case PH_DOWN: {
+        const bool o = kind == PH_O;
+        const int s = o ? 2 * layer + 1 : 2 * layer + 2;
+        g.W = o ? a->w_o + layer * a->s_o : a->w_down + layer * a->s_down;
+        g.Nt = H / 16;
+        g.Kt = o ? q_Kt : F_Kt;
+        g.Ahi = o ? a->OA + layer * a->oa_stride : a->HA + layer * a->ha_stride;
+        g.Alo = g.Ahi + (long)(g.Kt + kKtPad) * 64;
+        g.stats = nullptr;
+        g.xs_out = a->XS + s * a->xs_stride;
+        g.na_hi = reinterpret_cast<uint32_t*>(a->XA + s * a->xa_stride);
+        g.na_lo = reinterpret_cast<uint32_t*>(a->XA + s * a->xa_stride + (long)(Kt_H + kKtPad) * 64);
+        g.na_Kt = Kt_H;
+        g.gain = o ? a->g_mlp + (long)layer * H : (layer + 1 < a->D ? a->g_attn + (long)(layer + 1) * H : a->g_final);
+        gemm_dispatch<EPI_RESID>(a, c, g, kind, layer, pc, failed, smem);
+        break;
+      }
+      case PH_GU: {
+        const int s = 2 * layer + 1;
+        g.W = a->w_gu + layer * a->s_gu;
+        g.Nt = 2 * a->F / 16;
+        g.Kt = Kt_H;
+        g.Ahi = a->XA + s * a->xa_stride;
+        g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
+        g.stats = a->XS + s * a->xs_stride;
+        g.na_hi = reinterpret_cast<uint32_t*>(a->HA + layer * a->ha_stride);
+        g.na_lo = reinterpret_cast<uint32_t*>(a->HA + layer * a->ha_stride + (long)(F_Kt + kKtPad) * 64);
+        g.na_Kt = F_Kt;
+        gemm_dispatch<EPI_SWIGLU>(a, c, g, kind, layer, pc, failed, smem);
+        break;
+      }
+      case PH_LM: {
+        const int s = 2 * a->D;
+        g.W = a->w_lm;
+        g.Nt = (a->V + 15) / 16;
+        g.Kt = Kt_H;
+        g.Ahi = a->XA + s * a->xa_stride;
+        g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
+        g.stats = a->XS + s * a->xs_stride;
+        gemm_dispatch<EPI_ARGMAX>(a, c, g, kind, layer, pc, failed, smem);
+        break;
+      }
+    }
+    if (p + 1 < p1) grid_arrive(a);
+    else wait_vm();
+    trace_mark(c, 2 * p + 1, nslots);
   }
 }
 
@@ -788,21 +1367,10 @@ void launch_bf16_to_f32(hipStream_t s, float* dst, const uint16_t* src, long n) 
   hipLaunchKernelGGL(k_bf16_to_f32, dim3(blocks), dim3(256), 0, s, dst, src, n);
 }
 
-void launch_prologue(hipStream_t s, StepParams* p, const StepParams& host, const int* ids_src, int* ids_dst,
-                     int B) {
-  hipLaunchKernelGGL(k_prologue, dim3(1), dim3(64), 0, s, p, host, ids_src, ids_dst, B);
-}
-
-void launch_embed(hipStream_t s, const uint16_t* embed, const int* ids, int vocab, int H, int B, float* X,
-                  float* stats, const float* gain, u32x4* a_hi, u32x4* a_lo) {
-  hipLaunchKernelGGL(k_embed, dim3(B), dim3(256), 0, s, embed, ids, vocab, H, X, stats, gain, a_hi, a_lo);
-}
-
 void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
-                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max,
-                 StepParams* params, int L) {
+                 const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
   hipLaunchKernelGGL(k_fuse, dim3((H + 511) / 512, n, D), dim3(64), 0, s, hidden, n, S, H, alpha, gain, ustats,
-                     ua_hi, ua_lo, n_max, mt_max, params, L);
+                     ua_hi, ua_lo, n_max, mt_max);
 }
 
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n, int H,
@@ -811,62 +1379,36 @@ void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, co
                      out);
 }
 
-template <int NT, int WAVES>
-static void gemm_nw(hipStream_t s, int epi, const GemmArgs& a, dim3 grid) {
-  const dim3 block(64 * WAVES);
-  switch (epi) {
-    case EPI_RESID: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_RESID>), grid, block, 0, s, a); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_SWIGLU>), grid, block, 0, s, a); break;
-    case EPI_QKV: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_QKV>), grid, block, 0, s, a); break;
-    case EPI_KVT: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_KVT>), grid, block, 0, s, a); break;
-    case EPI_ARGMAX: hipLaunchKernelGGL((k_gemm<NT, WAVES, EPI_ARGMAX>), grid, block, 0, s, a); break;
-  }
+bool kvt_shape_supported(int nt_per_block, int waves) {
+  return (nt_per_block == 1 && waves == 16) || (nt_per_block == 2 && waves == 8);
 }
 
-bool gemm_shape_supported(int nt_per_block, int waves) {
-  return (nt_per_block == 1 && (waves == 8 || waves == 16)) || (nt_per_block == 2 && (waves == 8 || waves == 16)) ||
-         (nt_per_block == 4 && (waves == 4 || waves == 8));
-}
-
-void launch_gemm(hipStream_t s, int epi, int nt_per_block, int waves, const GemmArgs& a, int layers, int mtiles) {
+void launch_kvt(hipStream_t s, int nt_per_block, int waves, const KvtArgs& a, int layers, int mtiles) {
   const dim3 grid((a.Nt + nt_per_block - 1) / nt_per_block, layers, mtiles);
-  if (nt_per_block == 1) {
-    if (waves == 16) gemm_nw<1, 16>(s, epi, a, grid);
-    else gemm_nw<1, 8>(s, epi, a, grid);
-  } else if (nt_per_block == 2) {
-    if (waves == 16) gemm_nw<2, 16>(s, epi, a, grid);
-    else gemm_nw<2, 8>(s, epi, a, grid);
-  } else {
-    if (waves == 8) gemm_nw<4, 8>(s, epi, a, grid);
-    else gemm_nw<4, 4>(s, epi, a, grid);
-  }
+  if (nt_per_block == 2 && waves == 8) hipLaunchKernelGGL((k_kvt<2, 8>), grid, dim3(512), 0, s, a);
+  else hipLaunchKernelGGL((k_kvt<1, 16>), grid, dim3(1024), 0, s, a);
 }
 
-void launch_argmax_combine(hipStream_t s, const float* pmax, const int* pidx, int groups, int B, int* tokens) {
-  hipLaunchKernelGGL(k_argmax_combine, dim3(B), dim3(256), 0, s, pmax, pidx, groups, tokens);
+static const void* draft_kernel(int hd) {
+  return hd == 64 ? reinterpret_cast<const void*>(&k_draft<64>) : reinterpret_cast<const void*>(&k_draft<128>);
 }
 
-template <int HD>
-static void attn_hd(hipStream_t s, const AttnArgs& a, int chunk, int n_chunks, bool combine) {
-  if (!combine) {
-    const dim3 grid(n_chunks, a.n_kv);
-    if (chunk == 64) hipLaunchKernelGGL((k_attn<HD, 64>), grid, dim3(512), 0, s, a);
-    else hipLaunchKernelGGL((k_attn<HD, 128>), grid, dim3(512), 0, s, a);
-  } else {
-    const dim3 grid(a.Rpad, a.n_kv);
-    if (chunk == 64) hipLaunchKernelGGL((k_attn_combine<HD, 64>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_attn_combine<HD, 128>), grid, dim3(256), 0, s, a);
-  }
+hipError_t launch_draft(hipStream_t s, const DraftArgs* a_dev, const DraftCall& c, int hd, int blocks, int p0,
+                        int p1, bool cooperative) {
+  DraftKernArgs ka;
+  ka.a = a_dev;
+  ka.c = c;
+  ka.p0 = p0;
+  ka.p1 = p1;
+  void* kargs[] = {&ka};
+  if (cooperative) return hipLaunchCooperativeKernel(draft_kernel(hd), dim3(blocks), dim3(kThreads), kargs, 0, s);
+  return hipLaunchKernel(draft_kernel(hd), dim3(blocks), dim3(kThreads), kargs, 0, s);
 }
 
-void launch_attention(hipStream_t s, const AttnArgs& a, int hd, int chunk, int n_chunks) {
-  if (hd == 64) attn_hd<64>(s, a, chunk, n_chunks, false);
-  else attn_hd<128>(s, a, chunk, n_chunks, false);
-}
-
-void launch_attn_combine(hipStream_t s, const AttnArgs& a, int hd, int chunk, int n_chunks) {
-  if (hd == 64) attn_hd<64>(s, a, chunk, n_chunks, true);
-  else attn_hd<128>(s, a, chunk, n_chunks, true);
+int draft_blocks_per_cu(int hd) {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, draft_kernel(hd), kThreads, 0) != hipSuccess) return 0;
+  return n;
 }
 
 }  // namespace dflare

@@ -2,10 +2,11 @@
 //
 // One handle owns: the re-packed weights, the cached fusion weights alpha, the
 // per-draft-layer context cache (K as [n_kv, Lcap, hd], V transposed as
-// [n_kv, hd, Lcap], both bf16), a rotary table, and the scratch of one step.
-// Every call enqueues a fixed sequence of kernels on the handle's stream; the
-// values that change between calls (L, n_new, positions) travel through a
-// device-resident StepParams block written by a one-thread prologue kernel.
+// [n_kv, hd, Lcap], each as two bf16 planes hi + lo), a rotary table, and the
+// activation buffers of one draft block.  fuse_append enqueues two kernels (fusion,
+// context K/V projection); draft_block enqueues one persistent cooperative kernel (or,
+// on request, the same kernel once per phase).  Values that change between calls (L,
+// n_new, positions, the block ids pointer) travel as kernel arguments.
 #include <math.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -26,12 +27,6 @@ namespace {
 
 const uint32_t kMagic = 0xDF1A2E00u;
 
-struct Plan {
-  int nt = 4;      // output tiles per block
-  int waves = 4;   // waves per block (they split K)
-  int groups = 1;  // blocks per layer and row tile
-};
-
 std::mutex g_mu;
 std::unordered_set<const dflare_handle*> g_live;
 thread_local std::string g_init_error;
@@ -40,10 +35,17 @@ int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
 
 }  // namespace
 
+namespace {
+struct GemmPlan {  // chunk width and K split of one GEMM phase kind
+  int tn = 8, kg = 1;
+};
+}  // namespace
+
 struct dflare_handle {
   uint32_t magic = kMagic;
   dflare_config cfg{};
   hipStream_t stream = nullptr;
+  int device = 0;
   int L = 0;
   int Lcap = 0;
   int q_dim = 0, kv_dim = 0;
@@ -60,35 +62,46 @@ struct dflare_handle {
   long cache_layer_stride = 0;
   long cache_plane = 0;
   float2* rope = nullptr;
-  // step scratch
-  StepParams* params = nullptr;
-  int* ids = nullptr;
-  float *X = nullptr, *Xstats = nullptr, *Q = nullptr;
+  u32x4* zero_tile = nullptr;
+  // fuse_append scratch
   float* Ustats = nullptr;
-  // activations in A-fragment layout (hi / lo bf16 planes), each padded by 64 tiles
-  u32x4 *xa_hi = nullptr, *xa_lo = nullptr;  // x * gain of the next RMSNorm consumer, [Kt_H]
-  u32x4 *oa_hi = nullptr, *oa_lo = nullptr;  // attention output, [Kt_q]
-  u32x4 *ha_hi = nullptr, *ha_lo = nullptr;  // SwiGLU output, [Kt_F]
   u32x4 *ua_hi = nullptr, *ua_lo = nullptr;  // fused rows u * g_fuse, [D, mt_max, Kt_H]
   int mt_max = 1;
-  float* opart = nullptr;
-  float2* ml = nullptr;
+  int kvt_nt = 2, kvt_waves = 8;
+  // draft block
+  int blocks = 0;          // work-groups of the draft kernel
+  int phases = 0;
+  bool persistent = true;
+  bool coop_ok = false;    // the device keeps one work-group per CU resident
+  GemmPlan plan[PH_COUNT];
+  int attn_nch = 1;
+  float* X = nullptr;
+  float* XS = nullptr;
+  long xs_stride = 0;
+  u32x4* XA = nullptr;
+  long xa_stride = 0;
+  float* Q = nullptr;
+  long q_stride = 0;
+  float* OP = nullptr;
+  float2* ML = nullptr;
+  u32x4* OA = nullptr;
+  long oa_stride = 0;
+  u32x4* HA = nullptr;
+  long ha_stride = 0;
   float* pmax = nullptr;
   int* pidx = nullptr;
-  u32x4* zero_tile = nullptr;
-  Plan p_qkv, p_o, p_gu, p_down, p_lm, p_kvt;
-  int attn_chunk = 128, attn_nchunks = 1;
+  float* part = nullptr;
+  DraftArgs* args_dev = nullptr;  // device copy of the draft kernel's fixed arguments
+  unsigned* sync = nullptr;  // barrier counters, the LM-head completion counter, split-K counters
+  unsigned bar_epoch = 0, done_epoch = 0;
+  int* err_host = nullptr;   // host-mapped barrier time-out flag
+  int* err_dev = nullptr;
+  bool trace = false;
+  unsigned long long* trace_buf = nullptr;
   // debug capture
   bool debug = false;
   float *dbg_hidden = nullptr, *dbg_logits = nullptr, *dbg_fused = nullptr;
   int dbg_fused_n = 0;
-  // captured draft blocks, keyed by the output buffer
-  struct BlockGraph {
-    int32_t* out;
-    hipGraphExec_t exec;
-  };
-  std::vector<BlockGraph> graphs;
-  bool use_graphs = true;
   // kernel timing
   int prof_kind = 0;
   std::vector<hipEvent_t> prof_ev;  // pairs
@@ -112,6 +125,12 @@ int fail(dflare_handle* h, int code, const std::string& msg) {
       return fail((h), DFLARE_ERR_HIP, std::string(#call ": ") + hipGetErrorString(e_));         \
   } while (0)
 
+#define TRY(x)                         \
+  do {                                 \
+    int rc_ = (x);                     \
+    if (rc_ != DFLARE_OK) return rc_;  \
+  } while (0)
+
 template <typename T>
 int dev_alloc(dflare_handle* h, T** p, size_t bytes) {
   if (bytes == 0) bytes = 256;
@@ -126,12 +145,19 @@ int dev_alloc(dflare_handle* h, T** p, size_t bytes) {
   return DFLARE_OK;
 }
 
-void drop_graphs(dflare_handle* h);
+// zero-filled device allocation
+template <typename T>
+int dev_zalloc(dflare_handle* h, T** p, size_t bytes) {
+  TRY(dev_alloc(h, p, bytes));
+  HIP_OR_FAIL(h, hipMemsetAsync(*p, 0, bytes, h->stream));
+  return DFLARE_OK;
+}
 
 void free_all(dflare_handle* h) {
-  drop_graphs(h);
   for (void* p : h->allocs) (void)hipFree(p);
   h->allocs.clear();
+  if (h->err_host) (void)hipHostFree(h->err_host);
+  h->err_host = nullptr;
   for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
   h->prof_ev.clear();
 }
@@ -159,41 +185,6 @@ bool live(const dflare_handle* h) {
   return h && g_live.count(h) && h->magic == kMagic;
 }
 
-// Plan of a weight-streaming GEMM: output tiles per block and waves per block.  The defaults
-// can be overridden with DFLARE_PLAN_<NAME>=nt,waves (used for tuning).
-Plan make_plan(const char* name, int Nt, int nt, int waves) {
-  char key[64];
-  snprintf(key, sizeof key, "DFLARE_PLAN_%s", name);
-  if (const char* env = getenv(key)) {
-    int x = 0, y = 0;
-    if (sscanf(env, "%d,%d", &x, &y) == 2 && gemm_shape_supported(x, y)) {
-      nt = x;
-      waves = y;
-    }
-  }
-  Plan p;
-  p.nt = nt;
-  p.waves = waves;
-  p.groups = ceil_div(Nt, nt);
-  return p;
-}
-
-GemmArgs gemm_args(const dflare_handle* h, const u32x4* W, int Nt, int Kt) {
-  GemmArgs a{};
-  a.W = W;
-  a.Nt = Nt;
-  a.Kt = Kt;
-  a.zero = h->zero_tile;
-  a.eps = h->cfg.rms_eps;
-  a.e.params = h->params;
-  a.e.Lcap = h->Lcap;
-  a.e.plane = h->cache_plane;
-  a.e.hd = h->cfg.head_dim;
-  a.e.rope = h->rope;
-  a.e.B = h->cfg.block_size;
-  return a;
-}
-
 int check_launch(dflare_handle* h, const char* what) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(h, DFLARE_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
@@ -210,7 +201,7 @@ int validate_config(const dflare_config* c) {
     return fail(nullptr, DFLARE_ERR_INVALID_ARG, "rope_base must be > 0 and rms_eps >= 0");
   if (c->n_q_heads % c->n_kv_heads)
     return fail(nullptr, DFLARE_ERR_INVALID_ARG, "n_q_heads must be a multiple of n_kv_heads");
-  if (c->block_size > 16) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "block_size must be <= 16");
+  if (c->block_size > kMaxBlock) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "block_size must be <= 16");
   if (c->head_dim != 64 && c->head_dim != 128) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   if (c->hidden % 32 || c->ffn % 32 || (c->n_q_heads * c->head_dim) % 32)
     return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "hidden, ffn and n_q_heads*head_dim must be multiples of 32");
@@ -223,11 +214,56 @@ int validate_config(const dflare_config* c) {
   return DFLARE_OK;
 }
 
-#define TRY(x)                         \
-  do {                                 \
-    int rc_ = (x);                     \
-    if (rc_ != DFLARE_OK) return rc_;  \
-  } while (0)
+// GEMM plan of a phase kind (see DraftArgs::tn / kg).  Candidates: kg in {1, 2, 4, 8}
+// dividing the work-group count (kg > 1 only where the epilogue is linear in the sum and
+// a range fits one chunk of <= 8 tiles), tn the smallest of 2, 4, 6, 8 that holds a range
+// (8 when a range needs several chunks).  Cost, in KiB streamed by the busiest work-group:
+// its weight tiles, plus a quarter of its A-fragment and padding re-reads (L2 hits), plus
+// for a split the partial tiles the last work-group reads back and a fixed 16 for the
+// extra round trip.  DFLARE_PLAN_<NAME>=tn,kg overrides the choice (tuning, tests).
+bool plan_ok(int tn, int kg, int Nt, int blocks, bool allow_split) {
+  if (tn != 2 && tn != 4 && tn != 6 && tn != 8) return false;
+  if (kg < 1 || kg > kMaxSplit || (kg & (kg - 1)) || blocks % kg) return false;
+  if (kg > 1 && (!allow_split || ceil_div(Nt, blocks / kg) > tn)) return false;
+  return true;
+}
+
+GemmPlan choose_plan(const char* name, int Nt, int Kt, int blocks, bool allow_split) {
+  GemmPlan best;
+  double best_cost = 1e300;
+  for (int kg = 1; kg <= kMaxSplit; kg *= 2) {
+    if (blocks % kg || (kg > 1 && !allow_split)) continue;
+    const int T = ceil_div(Nt, blocks / kg);
+    if (kg > 1 && T > kTNMax) continue;
+    int tn = kTNMax;
+    for (int c : {2, 4, 6, 8})
+      if (c >= T) {
+        tn = c;
+        break;
+      }
+    const int nch = ceil_div(T, tn);
+    const int kpart = ceil_div(Kt, kg);
+    const double cost = (double)T * kpart + 0.25 * ((double)nch * 2 * kpart + (double)(nch * tn - T) * kpart) +
+                        (kg > 1 ? 16.0 + 2.0 * (kg - 1) * T : 0.0);
+    if (cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best.tn = tn;
+      best.kg = kg;
+    }
+  }
+  char key[64];
+  snprintf(key, sizeof key, "DFLARE_PLAN_%s", name);
+  if (const char* env = getenv(key)) {
+    int tn = 0, kg = 0;
+    if (sscanf(env, "%d,%d", &tn, &kg) == 2 && plan_ok(tn, kg, Nt, blocks, allow_split)) {
+      best.tn = tn;
+      best.kg = kg;
+    }
+  }
+  return best;
+}
+
+DraftArgs draft_args(const dflare_handle* h);
 
 int build(dflare_handle* h, const dflare_weights* w) {
   const dflare_config& c = h->cfg;
@@ -236,28 +272,52 @@ int build(dflare_handle* h, const dflare_weights* w) {
   h->q_dim = c.n_q_heads * hd;
   h->kv_dim = c.n_kv_heads * hd;
   const int q = h->q_dim, kv = h->kv_dim;
-  h->Lcap = ceil_div((long)c.max_context + B, 64) * 64;
+  // 8 spare slots: a 16-byte V^T piece that starts at the last block key stays inside a row
+  h->Lcap = ceil_div((long)c.max_context + B + 8, 64) * 64;
   h->Rpad = ceil_div((long)(c.n_q_heads / c.n_kv_heads) * B, 16) * 16;
   hipStream_t s = h->stream;
+  HIP_OR_FAIL(h, hipGetDevice(&h->device));
 
-  // ---- plans
   const int Nt_qkv = (q + 2 * kv) / 16, Nt_o = H / 16, Nt_gu = 2 * F / 16, Nt_down = H / 16;
   const int Nt_lm = ceil_div(V, 16), Nt_kvt = 2 * kv / 16;
   const int Kt_H = H / 32, Kt_q = q / 32, Kt_F = F / 32;
   const int mt_max = ceil_div(c.max_new, 16);
-  h->p_qkv = make_plan("QKV", Nt_qkv, 2, 16);
-  h->p_o = make_plan("O", Nt_o, 1, 16);
-  h->p_gu = make_plan("GU", Nt_gu, 4, 4);
-  h->p_down = make_plan("DOWN", Nt_down, 1, 16);
-  h->p_lm = make_plan("LM", Nt_lm, 4, 4);
-  h->p_kvt = make_plan("KVT", Nt_kvt, 1, 16);
-  if (const char* env = getenv("DFLARE_GRAPH")) h->use_graphs = atoi(env) != 0;
-  if (const char* env = getenv("DFLARE_ATTN_CHUNK")) {
-    int v = atoi(env);
-    if (v == 64 || v == 128) h->attn_chunk = v;
+
+  // ---- launch shape of the draft block: one work-group of kThreads per CU
+  int cus = 0;
+  HIP_OR_FAIL(h, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device));
+  int coop = 0;
+  HIP_OR_FAIL(h, hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device));
+  const int per_cu = draft_blocks_per_cu(hd);
+  h->coop_ok = coop != 0 && per_cu >= 1;
+  h->blocks = cus;
+  if (const char* env = getenv("DFLARE_BLOCKS")) {
+    const int v = atoi(env);
+    if (v >= 16 && v <= cus) h->blocks = v;
   }
-  // chunk c holds keys [c*chunk, (c+1)*chunk); the last one also the B block keys
-  h->attn_nchunks = std::max(1, ceil_div((long)c.max_context, h->attn_chunk));
+  if (h->blocks > kMaxBlocks) h->blocks = kMaxBlocks;
+  h->persistent = h->coop_ok;
+  if (const char* env = getenv("DFLARE_PERSISTENT"))
+    if (atoi(env) == 0) h->persistent = false;
+  h->phases = phase_count(D);
+  h->plan[PH_QKV] = choose_plan("QKV", Nt_qkv, Kt_H, h->blocks, true);
+  h->plan[PH_O] = choose_plan("O", Nt_o, Kt_q, h->blocks, true);
+  h->plan[PH_GU] = choose_plan("GU", Nt_gu, Kt_H, h->blocks, true);
+  h->plan[PH_DOWN] = choose_plan("DOWN", Nt_down, Kt_F, h->blocks, true);
+  h->plan[PH_LM] = choose_plan("LM", Nt_lm, Kt_H, h->blocks, false);
+  if (getenv("DFLARE_VERBOSE"))
+    fprintf(stderr, "dflare: %d work-groups; GEMM plans (tn,kg) qkv %d,%d o %d,%d gate/up %d,%d down %d,%d lm %d,%d\n",
+            h->blocks, h->plan[PH_QKV].tn, h->plan[PH_QKV].kg, h->plan[PH_O].tn, h->plan[PH_O].kg,
+            h->plan[PH_GU].tn, h->plan[PH_GU].kg, h->plan[PH_DOWN].tn, h->plan[PH_DOWN].kg, h->plan[PH_LM].tn,
+            h->plan[PH_LM].kg);
+  if (const char* env = getenv("DFLARE_PLAN_KVT")) {
+    int x = 0, y = 0;
+    if (sscanf(env, "%d,%d", &x, &y) == 2 && kvt_shape_supported(x, y)) {
+      h->kvt_nt = x;
+      h->kvt_waves = y;
+    }
+  }
+  h->attn_nch = std::max(1, ceil_div((long)c.max_context, 128));
 
   // ---- packed weights
   h->s_qkv = (long)Nt_qkv * Kt_H * 64;
@@ -265,12 +325,12 @@ int build(dflare_handle* h, const dflare_weights* w) {
   h->s_gu = (long)Nt_gu * Kt_H * 64;
   h->s_down = (long)Nt_down * Kt_F * 64;
   h->s_kvt = (long)Nt_kvt * Kt_H * 64;
-  TRY(dev_alloc(h, &h->w_qkv, (size_t)h->s_qkv * D * 16));
-  TRY(dev_alloc(h, &h->w_o, (size_t)h->s_o * D * 16));
-  TRY(dev_alloc(h, &h->w_gu, (size_t)h->s_gu * D * 16));
-  TRY(dev_alloc(h, &h->w_down, (size_t)h->s_down * D * 16));
+  TRY(dev_zalloc(h, &h->w_qkv, (size_t)h->s_qkv * D * 16 + kWeightSpare));
+  TRY(dev_zalloc(h, &h->w_o, (size_t)h->s_o * D * 16 + kWeightSpare));
+  TRY(dev_zalloc(h, &h->w_gu, (size_t)h->s_gu * D * 16 + kWeightSpare));
+  TRY(dev_zalloc(h, &h->w_down, (size_t)h->s_down * D * 16 + kWeightSpare));
   TRY(dev_alloc(h, &h->w_kvt, (size_t)h->s_kvt * D * 16));
-  TRY(dev_alloc(h, &h->w_lm, (size_t)Nt_lm * Kt_H * 64 * 16));
+  TRY(dev_zalloc(h, &h->w_lm, (size_t)Nt_lm * Kt_H * 64 * 16 + kWeightSpare));
   TRY(dev_alloc(h, &h->embed, (size_t)V * H * 2));
   const uint16_t* wq = (const uint16_t*)w->wq;
   const uint16_t* wkd = (const uint16_t*)w->wk_d;
@@ -316,10 +376,8 @@ int build(dflare_handle* h, const dflare_weights* w) {
   // per layer: K (or V^T) as two bf16 planes, hi then lo (value ~= hi + lo)
   h->cache_plane = (long)c.n_kv_heads * h->Lcap * hd;
   h->cache_layer_stride = 2 * h->cache_plane;
-  TRY(dev_alloc(h, &h->kc, (size_t)h->cache_layer_stride * D * 2));
-  TRY(dev_alloc(h, &h->vt, (size_t)h->cache_layer_stride * D * 2));
-  HIP_OR_FAIL(h, hipMemsetAsync(h->kc, 0, (size_t)h->cache_layer_stride * D * 2, s));
-  HIP_OR_FAIL(h, hipMemsetAsync(h->vt, 0, (size_t)h->cache_layer_stride * D * 2, s));
+  TRY(dev_zalloc(h, &h->kc, (size_t)h->cache_layer_stride * D * 2));
+  TRY(dev_zalloc(h, &h->vt, (size_t)h->cache_layer_stride * D * 2));
   {
     const int half = hd / 2;
     std::vector<float2> tab((size_t)h->Lcap * half);
@@ -331,170 +389,182 @@ int build(dflare_handle* h, const dflare_weights* w) {
     TRY(dev_alloc(h, &h->rope, tab.size() * sizeof(float2)));
     HIP_OR_FAIL(h, hipMemcpy(h->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice));
   }
+  TRY(dev_zalloc(h, &h->zero_tile, 64 * 16));
 
-  // ---- step scratch
-  TRY(dev_alloc(h, &h->params, sizeof(StepParams)));
-  TRY(dev_alloc(h, &h->zero_tile, 64 * 16));
-  HIP_OR_FAIL(h, hipMemsetAsync(h->zero_tile, 0, 64 * 16, s));
-  TRY(dev_alloc(h, &h->ids, 64 * 4));
-  TRY(dev_alloc(h, &h->X, (size_t)16 * H * 4));
-  TRY(dev_alloc(h, &h->Xstats, (size_t)16 * (H / 16) * 4));
-  TRY(dev_alloc(h, &h->Q, (size_t)16 * q * 4));
-  TRY(dev_alloc(h, &h->Ustats, (size_t)D * c.max_new * (H / 16) * 4));
+  // ---- fuse_append scratch
   h->mt_max = mt_max;
+  TRY(dev_zalloc(h, &h->Ustats, (size_t)D * c.max_new * (H / 16) * 4));
+  TRY(dev_zalloc(h, &h->ua_hi, (size_t)D * mt_max * Kt_H * 1024));
+  TRY(dev_zalloc(h, &h->ua_lo, (size_t)D * mt_max * Kt_H * 1024));
+
+  // ---- draft-block activations.  Rows >= B of every A-fragment and stats buffer stay zero.
+  const int stages = 2 * D + 1;
+  TRY(dev_zalloc(h, &h->X, (size_t)kMaxBlock * H * 4));
+  h->xs_stride = (long)(H / 16) * kStatsPad;
+  TRY(dev_zalloc(h, &h->XS, (size_t)stages * h->xs_stride * 4));
+  h->xa_stride = 2L * (Kt_H + kKtPad) * 64;
+  TRY(dev_zalloc(h, &h->XA, (size_t)stages * h->xa_stride * 16));
+  h->q_stride = (long)kMaxBlock * q;
+  TRY(dev_zalloc(h, &h->Q, (size_t)D * h->q_stride * 4));
+  TRY(dev_zalloc(h, &h->OP, (size_t)h->attn_nch * c.n_kv_heads * h->Rpad * hd * 4));
+  TRY(dev_zalloc(h, &h->ML, (size_t)h->attn_nch * c.n_kv_heads * h->Rpad * sizeof(float2)));
+  h->oa_stride = 2L * (Kt_q + kKtPad) * 64;
+  TRY(dev_zalloc(h, &h->OA, (size_t)D * h->oa_stride * 16));
+  h->ha_stride = 2L * (Kt_F + kKtPad) * 64;
+  TRY(dev_zalloc(h, &h->HA, (size_t)D * h->ha_stride * 16));
+  TRY(dev_zalloc(h, &h->pmax, (size_t)h->blocks * kStatsPad * 4));
+  TRY(dev_zalloc(h, &h->pidx, (size_t)h->blocks * kStatsPad * 4));
+  TRY(dev_zalloc(h, &h->part, (size_t)h->blocks * kTNMax * 1024));
+  TRY(dev_zalloc(h, &h->sync, kSyncBytes));
+  HIP_OR_FAIL(h, hipHostMalloc((void**)&h->err_host, 64, hipHostMallocMapped | hipHostMallocCoherent));
+  *(volatile int*)h->err_host = 0;
+  HIP_OR_FAIL(h, hipHostGetDevicePointer((void**)&h->err_dev, h->err_host, 0));
   {
-    const size_t pad = 64;
-    const size_t nx = (size_t)Kt_H + pad, no = (size_t)Kt_q + pad, nh = (size_t)Kt_F + pad;
-    const size_t nu = (size_t)D * mt_max * Kt_H + pad;
-    u32x4** bufs[8] = {&h->xa_hi, &h->xa_lo, &h->oa_hi, &h->oa_lo, &h->ha_hi, &h->ha_lo, &h->ua_hi, &h->ua_lo};
-    const size_t tiles[8] = {nx, nx, no, no, nh, nh, nu, nu};
-    for (int b = 0; b < 8; ++b) {
-      TRY(dev_alloc(h, bufs[b], tiles[b] * 1024));
-      HIP_OR_FAIL(h, hipMemsetAsync(*bufs[b], 0, tiles[b] * 1024, s));
-    }
+    const DraftArgs a = draft_args(h);
+    TRY(dev_alloc(h, &h->args_dev, sizeof(DraftArgs)));
+    HIP_OR_FAIL(h, hipMemcpy(h->args_dev, &a, sizeof(DraftArgs), hipMemcpyHostToDevice));
   }
-  TRY(dev_alloc(h, &h->opart, (size_t)h->attn_nchunks * c.n_kv_heads * h->Rpad * hd * 4));
-  TRY(dev_alloc(h, &h->ml, (size_t)h->attn_nchunks * c.n_kv_heads * h->Rpad * sizeof(float2)));
-  TRY(dev_alloc(h, &h->pmax, (size_t)16 * h->p_lm.groups * 4));
-  TRY(dev_alloc(h, &h->pidx, (size_t)16 * h->p_lm.groups * 4));
   HIP_OR_FAIL(h, hipStreamSynchronize(s));
   return DFLARE_OK;
 }
 
-// Every kernel of a draft block after the prologue.  The launch sequence and its arguments
-// depend only on the handle and `out`, so it can be captured once in a HIP graph and replayed.
-int enqueue_block_body(dflare_handle* h, int32_t* out) {
+DraftArgs draft_args(const dflare_handle* h) {
   const dflare_config& c = h->cfg;
-  const int H = c.hidden, D = c.n_draft_layers, F = c.ffn, B = c.block_size, hd = c.head_dim;
-  const int q = h->q_dim, kv = h->kv_dim;
-  hipStream_t s = h->stream;
-  launch_embed(s, h->embed, h->ids, c.vocab, H, B, h->X, h->Xstats, h->g_attn, h->xa_hi, h->xa_lo);
-
-  AttnArgs at{};
-  at.params = h->params;
-  at.Q = h->Q;
-  at.B = B;
-  at.n_q = c.n_q_heads;
-  at.n_kv = c.n_kv_heads;
-  at.q_dim = q;
-  at.Lcap = h->Lcap;
-  at.plane = h->cache_plane;
-  at.Rpad = h->Rpad;
-  at.qscale = (float)(1.4426950408889634 / sqrt((double)hd));
-  at.opart = h->opart;
-  at.ml = h->ml;
-  at.oa_hi = h->oa_hi;
-  at.oa_lo = h->oa_lo;
-  at.oa_Kt = q / 32;
-
-  for (int i = 0; i < D; ++i) {
-    uint16_t* kc = h->kc + i * h->cache_layer_stride;
-    uint16_t* vt = h->vt + i * h->cache_layer_stride;
-    {  // RMSNorm + Q / K^d / V^d + RoPE, block K/V into cache slots L..L+B-1
-      GemmArgs a = gemm_args(h, h->w_qkv + i * h->s_qkv, (q + 2 * kv) / 16, H / 32);
-      a.Ahi = h->xa_hi; a.Alo = h->xa_lo; a.M = B;
-      a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
-      a.e.out = h->Q; a.e.ldo = q; a.e.kc = kc; a.e.vt = vt;
-      a.e.q_tiles = q / 16; a.e.kv_tiles = kv / 16;
-      prof_mark(h, DFLARE_K_QKV, true);
-      launch_gemm(s, EPI_QKV, h->p_qkv.nt, h->p_qkv.waves, a, 1, 1);
-      prof_mark(h, DFLARE_K_QKV, false);
-    }
-    at.kc = kc;
-    at.vt = vt;
-    prof_mark(h, DFLARE_K_ATTN, true);
-    launch_attention(s, at, hd, h->attn_chunk, h->attn_nchunks);
-    launch_attn_combine(s, at, hd, h->attn_chunk, h->attn_nchunks);
-    prof_mark(h, DFLARE_K_ATTN, false);
-    {  // X += O W_O^T
-      GemmArgs a = gemm_args(h, h->w_o + i * h->s_o, H / 16, q / 32);
-      a.Ahi = h->oa_hi; a.Alo = h->oa_lo; a.M = B;
-      a.e.out = h->X; a.e.ldo = H; a.e.stats_out = h->Xstats; a.e.n_stat_out = H / 16;
-      a.e.na_hi = (uint32_t*)h->xa_hi; a.e.na_lo = (uint32_t*)h->xa_lo; a.e.na_Kt = H / 32;
-      a.e.next_gain = h->g_mlp + (long)i * H;
-      prof_mark(h, DFLARE_K_O, true);
-      launch_gemm(s, EPI_RESID, h->p_o.nt, h->p_o.waves, a, 1, 1);
-      prof_mark(h, DFLARE_K_O, false);
-    }
-    {  // RMSNorm + gate/up + SwiGLU
-      GemmArgs a = gemm_args(h, h->w_gu + i * h->s_gu, 2 * F / 16, H / 32);
-      a.Ahi = h->xa_hi; a.Alo = h->xa_lo; a.M = B;
-      a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
-      a.e.na_hi = (uint32_t*)h->ha_hi; a.e.na_lo = (uint32_t*)h->ha_lo; a.e.na_Kt = F / 32;
-      prof_mark(h, DFLARE_K_GATE_UP, true);
-      launch_gemm(s, EPI_SWIGLU, h->p_gu.nt, h->p_gu.waves, a, 1, 1);
-      prof_mark(h, DFLARE_K_GATE_UP, false);
-    }
-    {  // X += H W_down^T
-      GemmArgs a = gemm_args(h, h->w_down + i * h->s_down, H / 16, F / 32);
-      a.Ahi = h->ha_hi; a.Alo = h->ha_lo; a.M = B;
-      a.e.out = h->X; a.e.ldo = H; a.e.stats_out = h->Xstats; a.e.n_stat_out = H / 16;
-      a.e.na_hi = (uint32_t*)h->xa_hi; a.e.na_lo = (uint32_t*)h->xa_lo; a.e.na_Kt = H / 32;
-      a.e.next_gain = (i + 1 < D) ? h->g_attn + (long)(i + 1) * H : h->g_final;
-      prof_mark(h, DFLARE_K_DOWN, true);
-      launch_gemm(s, EPI_RESID, h->p_down.nt, h->p_down.waves, a, 1, 1);
-      prof_mark(h, DFLARE_K_DOWN, false);
-    }
-    if (h->debug)
-      HIP_OR_FAIL(h, hipMemcpyAsync(h->dbg_hidden + (long)i * B * H, h->X, (size_t)B * H * 4,
-                                    hipMemcpyDeviceToDevice, s));
+  DraftArgs a{};
+  a.H = c.hidden;
+  a.F = c.ffn;
+  a.V = c.vocab;
+  a.D = c.n_draft_layers;
+  a.B = c.block_size;
+  a.hd = c.head_dim;
+  a.n_q = c.n_q_heads;
+  a.n_kv = c.n_kv_heads;
+  a.Lcap = h->Lcap;
+  a.Rpad = h->Rpad;
+  a.chunk = 128;
+  a.nch = h->attn_nch;
+  a.eps = c.rms_eps;
+  a.qscale = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
+  for (int k = 0; k < PH_COUNT; ++k) {
+    a.tn[k] = h->plan[k].tn;
+    a.kg[k] = h->plan[k].kg;
   }
-  {  // final RMSNorm + LM head + argmax
-    GemmArgs a = gemm_args(h, h->w_lm, ceil_div(c.vocab, 16), H / 32);
-    a.Ahi = h->xa_hi; a.Alo = h->xa_lo; a.M = B;
-    a.stats = h->Xstats; a.n_stat = H / 16; a.inv_dim = 1.0f / H;
-    a.e.vocab = c.vocab; a.e.pmax = h->pmax; a.e.pidx = h->pidx;
-    a.e.logits = h->debug ? h->dbg_logits : nullptr;
-    prof_mark(h, DFLARE_K_LM_HEAD, true);
-    launch_gemm(s, EPI_ARGMAX, h->p_lm.nt, h->p_lm.waves, a, 1, 1);
-    launch_argmax_combine(s, h->pmax, h->pidx, h->p_lm.groups, B, out);
-    prof_mark(h, DFLARE_K_LM_HEAD, false);
-  }
-  return check_launch(h, "draft_block");
+  a.embed = h->embed;
+  a.w_qkv = h->w_qkv;
+  a.w_o = h->w_o;
+  a.w_gu = h->w_gu;
+  a.w_down = h->w_down;
+  a.w_lm = h->w_lm;
+  a.s_qkv = h->s_qkv;
+  a.s_o = h->s_o;
+  a.s_gu = h->s_gu;
+  a.s_down = h->s_down;
+  a.g_attn = h->g_attn;
+  a.g_mlp = h->g_mlp;
+  a.g_final = h->g_final;
+  a.zero = h->zero_tile;
+  a.rope = h->rope;
+  a.kc = h->kc;
+  a.vt = h->vt;
+  a.plane = h->cache_plane;
+  a.cache_layer = h->cache_layer_stride;
+  a.X = h->X;
+  a.XS = h->XS;
+  a.xs_stride = h->xs_stride;
+  a.XA = h->XA;
+  a.xa_stride = h->xa_stride;
+  a.Q = h->Q;
+  a.q_stride = h->q_stride;
+  a.OP = h->OP;
+  a.ML = h->ML;
+  a.OA = h->OA;
+  a.oa_stride = h->oa_stride;
+  a.HA = h->HA;
+  a.ha_stride = h->ha_stride;
+  a.pmax = h->pmax;
+  a.pidx = h->pidx;
+  a.bar = h->sync;
+  a.done = h->sync + kBarCounters * 32;
+  a.part = h->part;
+  a.kcnt = h->sync + 1024;
+  a.err = h->err_dev;
+  return a;
 }
 
-void drop_graphs(dflare_handle* h) {
-  for (auto& g : h->graphs) (void)hipGraphExecDestroy(g.exec);
-  h->graphs.clear();
+DraftCall draft_call(const dflare_handle* h, const int32_t* ids, const int32_t* positions_host, int32_t* out) {
+  const dflare_config& c = h->cfg;
+  DraftCall d{};
+  d.L = h->L;
+  for (int b = 0; b < kMaxBlock; ++b) d.pos[b] = (b < c.block_size) ? (positions_host ? positions_host[b] : h->L + b) : 0;
+  d.ids = ids;
+  d.tokens = out;
+  d.logits = h->debug ? h->dbg_logits : nullptr;
+  d.bar_epoch = h->bar_epoch;
+  d.done_epoch = h->done_epoch;
+  d.trace = h->trace ? h->trace_buf : nullptr;
+  return d;
+}
+
+int prof_kind_of(int phase_kind) {
+  switch (phase_kind) {
+    case PH_QKV: return DFLARE_K_QKV;
+    case PH_ATTN:
+    case PH_COMB: return DFLARE_K_ATTN;
+    case PH_O: return DFLARE_K_O;
+    case PH_GU: return DFLARE_K_GATE_UP;
+    case PH_DOWN: return DFLARE_K_DOWN;
+    case PH_LM: return DFLARE_K_LM_HEAD;
+    default: return 0;
+  }
 }
 
 int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positions_host, int32_t* out) {
-  const int B = h->cfg.block_size;
+  const dflare_config& c = h->cfg;
   hipStream_t s = h->stream;
-  StepParams sp{};
-  sp.L = h->L;
-  sp.n_new = 0;
-  for (int b = 0; b < B; ++b) sp.pos[b] = positions_host ? positions_host[b] : h->L + b;
-  launch_prologue(s, h->params, sp, ids, h->ids, B);
-  // Graph replay needs a capturable (non-null) stream; debug capture and kernel timing
-  // insert extra work between the kernels, so they run eagerly.
-  const bool graph = h->use_graphs && s != nullptr && !h->debug && h->prof_kind == 0;
-  if (!graph) return enqueue_block_body(h, out);
-  for (auto& g : h->graphs)
-    if (g.out == out) {
-      HIP_OR_FAIL(h, hipGraphLaunch(g.exec, s));
-      return DFLARE_OK;
+  if (*(volatile int*)h->err_host) {  // an earlier persistent launch timed out at a grid barrier
+    HIP_OR_FAIL(h, hipStreamSynchronize(s));
+    HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
+    HIP_OR_FAIL(h, hipStreamSynchronize(s));
+    h->bar_epoch = h->done_epoch = 0;
+    *(volatile int*)h->err_host = 0;
+    h->persistent = false;
+    return fail(h, DFLARE_ERR_HIP,
+                "a grid barrier of an earlier draft_block timed out; its tokens are invalid and the handle "
+                "now runs one launch per phase");
+  }
+  const int P = h->phases;
+  // counters are monotonic across launches; start again from zero long before they wrap
+  // (split-K counters reach (done_epoch + 1) * D * kg <= (done_epoch + 1) * D * 8)
+  if (h->bar_epoch + (unsigned)P > (1u << 24) || h->done_epoch + 1u > (1u << 22) ||
+      ((uint64_t)h->done_epoch + 1u) * (uint64_t)c.n_draft_layers * kMaxSplit >= (1ull << 31)) {
+    HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
+    h->bar_epoch = h->done_epoch = 0;
+  }
+  if (h->trace && !h->trace_buf) TRY(dev_zalloc(h, &h->trace_buf, (size_t)h->blocks * 2 * P * 8));
+  const DraftCall dc = draft_call(h, ids, positions_host, out);
+  const int hd = c.head_dim;
+  const bool split = !h->persistent || h->debug || (h->prof_kind >= DFLARE_K_QKV && h->prof_kind <= DFLARE_K_LM_HEAD);
+  prof_mark(h, DFLARE_K_DRAFT, true);
+  if (!split) {
+    HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, h->blocks, 0, P, true));
+    h->bar_epoch += (unsigned)(P - 1);
+  } else {
+    for (int p = 0; p < P; ++p) {
+      int kind, layer;
+      phase_of(p, c.n_draft_layers, kind, layer);
+      const int pk = prof_kind_of(kind);
+      const bool open = pk && (kind != PH_COMB);  // attention + combine are timed together
+      if (open) prof_mark(h, pk, true);
+      HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, h->blocks, p, p + 1, false));
+      if (pk && kind != PH_ATTN) prof_mark(h, pk, false);
+      if (h->debug && kind == PH_DOWN)
+        HIP_OR_FAIL(h, hipMemcpyAsync(h->dbg_hidden + (long)layer * c.block_size * c.hidden, h->X,
+                                      (size_t)c.block_size * c.hidden * 4, hipMemcpyDeviceToDevice, s));
     }
-  hipGraph_t graph_def = nullptr;
-  HIP_OR_FAIL(h, hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal));
-  const int rc = enqueue_block_body(h, out);
-  const hipError_t ce = hipStreamEndCapture(s, &graph_def);
-  if (rc != DFLARE_OK) {
-    if (graph_def) (void)hipGraphDestroy(graph_def);
-    return rc;
   }
-  if (ce != hipSuccess) return fail(h, DFLARE_ERR_HIP, std::string("graph capture: ") + hipGetErrorString(ce));
-  hipGraphExec_t exec = nullptr;
-  const hipError_t ie = hipGraphInstantiate(&exec, graph_def, nullptr, nullptr, 0);
-  (void)hipGraphDestroy(graph_def);
-  if (ie != hipSuccess) return fail(h, DFLARE_ERR_HIP, std::string("graph instantiate: ") + hipGetErrorString(ie));
-  if (h->graphs.size() >= 4) {  // keep the four most recent output buffers
-    (void)hipGraphExecDestroy(h->graphs.front().exec);
-    h->graphs.erase(h->graphs.begin());
-  }
-  h->graphs.push_back({out, exec});
-  HIP_OR_FAIL(h, hipGraphLaunch(exec, s));
-  return DFLARE_OK;
+  h->done_epoch += 1;
+  prof_mark(h, DFLARE_K_DRAFT, false);
+  return check_launch(h, "draft_block");
 }
 
 }  // namespace
@@ -559,17 +629,34 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   hipStream_t s = h->stream;
   prof_mark(h, DFLARE_K_FUSE, true);
   launch_fuse(s, (const uint16_t*)target_hidden, n_new, S, H, D, h->alpha, h->g_fuse, h->Ustats, h->ua_hi,
-              h->ua_lo, c.max_new, h->mt_max, h->params, h->L);
+              h->ua_lo, c.max_new, h->mt_max);
   prof_mark(h, DFLARE_K_FUSE, false);
-  GemmArgs a = gemm_args(h, h->w_kvt, 2 * h->kv_dim / 16, H / 32);
+  KvtArgs a{};
+  a.W = h->w_kvt;
   a.w_layer_stride = h->s_kvt;
-  a.Ahi = h->ua_hi; a.Alo = h->ua_lo; a.a_layer_stride = (long)h->mt_max * (H / 32) * 64;
-  a.stats = h->Ustats; a.stats_layer_stride = (long)c.max_new * (H / 16); a.n_stat = H / 16;
+  a.Nt = 2 * h->kv_dim / 16;
+  a.Kt = H / 32;
+  a.zero = h->zero_tile;
+  a.Ahi = h->ua_hi;
+  a.Alo = h->ua_lo;
+  a.a_layer_stride = (long)h->mt_max * (H / 32) * 64;
+  a.stats = h->Ustats;
+  a.stats_layer_stride = (long)c.max_new * (H / 16);
+  a.n_stat = H / 16;
   a.inv_dim = 1.0f / H;
-  a.e.kc = h->kc; a.e.vt = h->vt; a.e.cache_layer_stride = h->cache_layer_stride;
-  a.e.q_tiles = 0; a.e.kv_tiles = h->kv_dim / 16;
+  a.eps = c.rms_eps;
+  a.L = h->L;
+  a.n_new = n_new;
+  a.kc = h->kc;
+  a.vt = h->vt;
+  a.plane = h->cache_plane;
+  a.cache_layer_stride = h->cache_layer_stride;
+  a.Lcap = h->Lcap;
+  a.hd = c.head_dim;
+  a.kv_tiles = h->kv_dim / 16;
+  a.rope = h->rope;
   prof_mark(h, DFLARE_K_KV_T, true);
-  launch_gemm(s, EPI_KVT, h->p_kvt.nt, h->p_kvt.waves, a, D, ceil_div(n_new, 16));
+  launch_kvt(s, h->kvt_nt, h->kvt_waves, a, D, ceil_div(n_new, 16));
   prof_mark(h, DFLARE_K_KV_T, false);
   if (h->debug) {
     launch_fused_rows(s, h->ua_hi, h->ua_lo, h->Ustats, n_new, H, D, c.max_new, h->mt_max, c.rms_eps,
@@ -594,7 +681,7 @@ int dflare_draft_block_pos(dflare_handle* h, const int32_t* block_ids, const int
   if (!block_ids || !draft_tokens || !positions)
     return fail(h, DFLARE_ERR_INVALID_ARG, "block_ids / positions / draft_tokens is NULL");
   for (int b = 0; b < h->cfg.block_size; ++b)
-    if (positions[b] < 0 || positions[b] >= h->Lcap)
+    if (positions[b] < 0 || positions[b] >= h->cfg.max_context + h->cfg.block_size)
       return fail(h, DFLARE_ERR_INVALID_ARG, "a position is outside [0, max_context + block_size)");
   return run_draft_block(h, block_ids, positions, draft_tokens);
 }
@@ -670,8 +757,9 @@ int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, in
                            what == DFLARE_DBG_HIDDEN;
   if (needs_layer && (layer < 0 || layer >= c.n_draft_layers))
     return fail(h, DFLARE_ERR_INVALID_ARG, "layer out of range");
-  if (what != DFLARE_DBG_ALPHA && what != DFLARE_DBG_KCACHE && what != DFLARE_DBG_VCACHE && !h->dbg_hidden)
+  if ((what == DFLARE_DBG_FUSED || what == DFLARE_DBG_HIDDEN || what == DFLARE_DBG_LOGITS) && !h->dbg_hidden)
     return fail(h, DFLARE_ERR_INVALID_ARG, "debug capture was never enabled");
+  if (what == DFLARE_DBG_TRACE && !h->trace_buf) return fail(h, DFLARE_ERR_INVALID_ARG, "tracing was never enabled");
   HIP_OR_FAIL(h, hipStreamSynchronize(h->stream));
   switch (what) {
     case DFLARE_DBG_ALPHA: {
@@ -719,13 +807,23 @@ int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, in
           }
       return DFLARE_OK;
     }
+    case DFLARE_DBG_TRACE: {
+      const int64_t n = (int64_t)h->blocks * 2 * h->phases;
+      if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
+      std::vector<unsigned long long> raw((size_t)n);
+      HIP_OR_FAIL(h, hipMemcpy(raw.data(), h->trace_buf, n * 8, hipMemcpyDeviceToHost));
+      unsigned long long t0 = ~0ull;
+      for (int b = 0; b < h->blocks; ++b) t0 = std::min(t0, raw[(size_t)b * 2 * h->phases]);
+      for (int64_t i = 0; i < n; ++i) host_out[i] = (float)((double)(raw[i] - t0) * 0.01);  // 100 MHz ticks -> us
+      return DFLARE_OK;
+    }
     default: return fail(h, DFLARE_ERR_INVALID_ARG, "unknown debug tensor");
   }
 }
 
 int dflare_profile_begin(dflare_handle* h, int kind) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
-  if (kind < 0 || kind > DFLARE_K_KV_T) return fail(h, DFLARE_ERR_INVALID_ARG, "unknown kernel kind");
+  if (kind < 0 || kind > DFLARE_K_DRAFT) return fail(h, DFLARE_ERR_INVALID_ARG, "unknown kernel kind");
   h->prof_kind = kind;
   h->prof_n = 0;
   return DFLARE_OK;
@@ -750,9 +848,24 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches) {
 
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count) {
   if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
-  const int32_t v[2] = {2 + 6 * h->cfg.n_draft_layers + 2, 2};
-  for (int i = 0; i < count && i < 2; ++i) out[i] = v[i];
+  const int32_t v[5] = {h->persistent ? 1 : h->phases, 2, h->blocks, h->phases, h->persistent ? h->phases - 1 : 0};
+  for (int i = 0; i < count && i < 5; ++i) out[i] = v[i];
   return DFLARE_OK;
+}
+
+int dflare_set_option(dflare_handle* h, int option, int value) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  switch (option) {
+    case DFLARE_OPT_PERSISTENT:
+      if (value && !h->coop_ok)
+        return fail(h, DFLARE_ERR_UNSUPPORTED, "the device cannot keep one draft work-group per CU resident");
+      h->persistent = value != 0;
+      return DFLARE_OK;
+    case DFLARE_OPT_TRACE:
+      h->trace = value != 0;
+      return DFLARE_OK;
+    default: return fail(h, DFLARE_ERR_INVALID_ARG, "unknown option");
+  }
 }
 
 }  // extern "C"

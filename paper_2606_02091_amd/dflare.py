@@ -17,15 +17,16 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "libdflare.so")
 
 OK, ERR_INVALID_ARG, ERR_OUT_OF_MEMORY, ERR_CONTEXT_FULL, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-DBG_FUSED, DBG_KCACHE, DBG_VCACHE, DBG_HIDDEN, DBG_LOGITS, DBG_ALPHA = range(6)
+DBG_FUSED, DBG_KCACHE, DBG_VCACHE, DBG_HIDDEN, DBG_LOGITS, DBG_ALPHA, DBG_TRACE = range(7)
+OPT_PERSISTENT, OPT_TRACE = 1, 2
 
 EXPORTED = (
     "dflare_init", "dflare_fuse_append", "dflare_draft_block", "dflare_draft_block_pos",
     "dflare_truncate", "dflare_context_len", "dflare_set_stream", "dflare_destroy",
     "dflare_status_str", "dflare_last_error", "dflare_debug_capture", "dflare_debug_read",
-    "dflare_kernel_stats", "dflare_profile_begin", "dflare_profile_end",
+    "dflare_kernel_stats", "dflare_profile_begin", "dflare_profile_end", "dflare_set_option",
 )
-K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T = range(1, 9)
+K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T, K_DRAFT = range(1, 10)
 
 
 class DFlareError(RuntimeError):
@@ -79,6 +80,7 @@ def lib() -> ctypes.CDLL:
         "dflare_kernel_stats": ([vp, ctypes.POINTER(i32), i32], ctypes.c_int),
         "dflare_profile_begin": ([vp, ctypes.c_int], ctypes.c_int),
         "dflare_profile_end": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)], ctypes.c_int),
+        "dflare_set_option": ([vp, ctypes.c_int, ctypes.c_int], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -173,10 +175,15 @@ def dflare_debug_read(h: int, what: int, layer: int, shape) -> np.ndarray:
     return out.reshape(shape)
 
 
-def dflare_kernel_stats(h: int) -> tuple[int, int]:
-    out = (ctypes.c_int32 * 2)()
-    _check(lib().dflare_kernel_stats(h, out, 2), h)
-    return out[0], out[1]
+def dflare_kernel_stats(h: int) -> tuple[int, ...]:
+    """(kernels per draft_block, kernels per fuse_append, work-groups, phases, grid barriers)."""
+    out = (ctypes.c_int32 * 5)()
+    _check(lib().dflare_kernel_stats(h, out, 5), h)
+    return tuple(out)
+
+
+def dflare_set_option(h: int, option: int, value: int) -> None:
+    _check(lib().dflare_set_option(h, int(option), int(value)), h)
 
 
 def dflare_profile_begin(h: int, kind: int) -> None:

@@ -62,7 +62,7 @@ class ModelConfig:
     def replace(self, **kw) -> "ModelConfig":
         return dataclasses.replace(self, **kw)
 
-    # algorithmic bytes of one draft step (bf16 storage), see the design doc
+    # algorithmic HBM bytes of one draft block and of one append (bf16 storage)
     def block_bytes(self, L: int | None = None) -> int:
         L = self.context if L is None else L
         H, F, V, D = self.hidden, self.ffn, self.vocab, self.n_draft_layers

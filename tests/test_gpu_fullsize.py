@@ -4,9 +4,10 @@ For each model shape (Qwen3-8B, Qwen3-4B and GPT-OSS-20B shaped drafts at their 
 context lengths) the library and the fp64 oracle prefill the same seeded context in
 512-row appends, then run draft steps.  Checked against the oracle: the whole
 context K/V cache of every draft layer, the block rows after every layer, the logits
-and the draft tokens (the bar of tests/parity.py).  The bench's configuration --
-a non-default stream, the draft block replayed as a HIP graph -- must then produce
-the very same tokens, bitwise, as the eager debug run.
+and the draft tokens (the bar of tests/parity.py).  The bench's configuration -- a
+non-default stream, the draft block as one persistent launch whose phases wait at grid
+barriers -- must produce the very same tokens, bitwise, as the debug run with one
+launch per phase.
 """
 import os
 
@@ -53,16 +54,17 @@ def test_fullsize_parity(name):
         ids_t = torch.from_numpy(ids).cuda()
         out = torch.empty(cfg.block_size, dtype=torch.int32, device="cuda")
         for step in range(2):
-            # bench configuration first: graph replay on the side stream, no debug capture
+            # bench configuration first: persistent launch on the side stream, no debug capture
             model.draft_block(ids_t, out)
             model.draft_block(ids_t, out)
             side.synchronize()
-            graph_tokens = out.cpu().numpy().copy()
+            assert dfl.dflare_kernel_stats(model.h)[0] == 1
+            persistent_tokens = out.cpu().numpy().copy()
             dfl.dflare_debug_capture(model.h, True)
             eager = model.draft_block(ids_t).cpu().numpy()
             side.synchronize()
             dfl.dflare_debug_capture(model.h, False)
-            assert np.array_equal(graph_tokens, eager)
+            assert np.array_equal(persistent_tokens, eager)
             ref = orc.draft_block(ids)
             print(f"[fullsize] {name}: step {step} oracle done", flush=True)
             for i in range(cfg.n_draft_layers):

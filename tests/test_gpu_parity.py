@@ -267,30 +267,83 @@ def test_context_full_and_bad_sizes_leave_state():
     model.close()
 
 
-def test_graph_replay_matches_eager():
-    """The captured draft block (non-default stream) equals the eager one bitwise, on every
-    replay, with eager work (appends, syncs, an eager block) between the replays."""
-    cfg = CASES["gqa8_hd64"][0]
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_persistent_matches_per_phase(case):
+    """The persistent launch (phases separated by grid barriers, non-default stream) gives
+    the very tokens of one launch per phase, bitwise, step after step, with eager work
+    (appends, truncation, synchronisation) between the calls; both agree with the oracle."""
+    cfg, L, mode = CASES[case]
+    print(f"[persistent] case={case}", flush=True)
     w, lg = P.weights_for(cfg)
     side = torch.cuda.Stream()
     with torch.cuda.stream(side):
-        model = dfl.DraftModel(cfg, w, lg, max_context=400)
-        rows = synth.hidden_rows(cfg, 0, 300)
-        for s in range(0, 300, 16):
-            model.fuse_append(dev(np.ascontiguousarray(rows[:, s:s + 16])))
-        ids = ids_tensor(synth.block_ids(cfg, step=7))
+        model = dfl.DraftModel(cfg, w, lg, max_context=L + 64, max_new=16)
+        n_blocks = dfl.dflare_kernel_stats(model.h)[2]
+        orc = P.oracle_for(cfg, w, lg, L + 64)
+        s = 0
+        for n in append_plan(cfg, L, mode):
+            rows = synth.hidden_rows(cfg, s, n)
+            model.fuse_append(dev(rows))
+            orc.append(rows)
+            s += n
         out = torch.empty(cfg.block_size, dtype=torch.int32, device="cuda")
-        outs = []
-        for k in range(4):
-            model.draft_block(ids, out)          # graph captured on the first call, replayed after
+        for k in range(3):
+            ids_np = synth.block_ids(cfg, step=k)
+            ids = ids_tensor(ids_np)
+            dfl.dflare_set_option(model.h, dfl.OPT_PERSISTENT, 1)
+            assert dfl.dflare_kernel_stats(model.h)[0] == 1
+            model.draft_block(ids, out)
+            model.draft_block(ids, out)  # repeated: the block slots are rewritten, the context is not
             side.synchronize()
-            outs.append(out.cpu().clone())
-            extra = synth.hidden_rows(cfg, 300 + k, 1)
-            model.fuse_append(dev(extra))          # eager work between replays
-            model.truncate(300)
-        dfl.dflare_debug_capture(model.h, True)  # debug capture runs the block eagerly
-        eager = model.draft_block(ids).cpu()
-        side.synchronize()
-    for o in outs:
-        assert torch.equal(o, eager)
+            persistent = out.cpu().numpy().copy()
+            dfl.dflare_set_option(model.h, dfl.OPT_PERSISTENT, 0)
+            per_phase = model.draft_block(ids).cpu().numpy()
+            side.synchronize()
+            assert np.array_equal(persistent, per_phase), (case, k, persistent, per_phase)
+            ref = orc.draft_block(ids_np)
+            P.check_tokens(persistent, ref["logits"])
+            extra = synth.hidden_rows(cfg, s, 3, seed=9 + k)  # eager work between the calls
+            model.fuse_append(dev(extra))
+            orc.append(extra)
+            s += 3
+    assert n_blocks >= 16
+    model.close()
+
+
+SPLIT_CFG = synth.ModelConfig("splits", hidden=256, n_q_heads=4, n_kv_heads=2, head_dim=128, ffn=640,
+                              vocab=8000, n_draft_layers=2, n_target_layers=6, block_size=16, context=300,
+                              random_block=True)
+
+
+# GEMM plans (chunk width tn, K split kg) per phase kind for SPLIT_CFG on 16 work-groups:
+# QKV 64 x 8 tiles, O 16 x 16, gate/up 80 x 8, down 16 x 20, LM head 500 x 8 (n x k).
+PLANS = {
+    "chunks2": {"QKV": "2,1", "O": "2,1", "GU": "2,1", "DOWN": "2,1"},   # several chunks per work-group
+    "chunks8": {"QKV": "8,1", "O": "8,1", "GU": "8,1", "DOWN": "8,1"},   # padding tiles in every chunk
+    "split": {"QKV": "8,2", "O": "8,8", "GU": "6,1", "DOWN": "4,4"},     # K split over 2, 8, 4 work-groups
+    "split_thin": {"QKV": "4,1", "O": "4,4", "GU": "4,1", "DOWN": "8,8"},  # K parts of 2-3 tiles: idle waves
+}
+
+
+@pytest.mark.parametrize("plan", sorted(PLANS))
+def test_gemm_plans(plan, monkeypatch):
+    """Every way a GEMM phase can lay out its work: 16 work-groups, so each owns many output
+    tiles; chunks of 2 to 8 tiles with padding; K split over 2 to 8 work-groups, including
+    parts so thin that some waves hold no k-tile; the LM head in many chunks.  Per-phase
+    launches match the oracle; the persistent launch matches them bitwise."""
+    cfg = SPLIT_CFG
+    print(f"[plans] {plan}", flush=True)
+    monkeypatch.setenv("DFLARE_BLOCKS", "16")
+    for name, v in PLANS[plan].items():
+        monkeypatch.setenv(f"DFLARE_PLAN_{name}", v)
+    model, orc, w, lg = build_pair(cfg, cfg.context, "random")
+    assert dfl.dflare_kernel_stats(model.h)[2] == 16
+    for k in range(2):
+        ids = synth.block_ids(cfg, step=k)
+        _, per_phase, _ = compare_step(model, orc, cfg, ids, tag=f"plan={plan} step={k}")
+        dfl.dflare_debug_capture(model.h, False)
+        persistent = model.draft_block(ids_tensor(ids)).cpu().numpy()
+        torch.cuda.synchronize()
+        dfl.dflare_debug_capture(model.h, True)
+        assert np.array_equal(persistent, per_phase), (plan, k)
     model.close()
