@@ -90,9 +90,9 @@ struct DraftArgs {
   const float *g_attn, *g_mlp, *g_final;  // RMSNorm gains [D, H], [D, H], [H]
   const u32x4* zero;                      // one zero tile
   const float2* rope;                     // [Lcap, hd/2] (cos, sin)
-  // context cache of layer 0: K [n_kv, Lcap, hd], V^T [n_kv, hd, Lcap], hi plane then lo plane
+  // context cache of layer 0 (fp16): K [n_kv, Lcap, hd], V^T [n_kv, hd, Lcap]
   uint16_t *kc, *vt;
-  long plane, cache_layer;
+  long cache_layer;
   // activations
   float* X;              // residual stream [16, H] fp32, updated in place
   float* XS;             // per stage: sums of squares [H/16][kStatsPad]
@@ -140,7 +140,7 @@ struct KvtArgs {
   float inv_dim, eps;
   int L, n_new;
   uint16_t *kc, *vt;
-  long plane, cache_layer_stride;
+  long cache_layer_stride;
   int Lcap, hd, kv_tiles;
   const float2* rope;
 };

@@ -29,6 +29,7 @@
 namespace dflare {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -61,6 +62,27 @@ __device__ __forceinline__ void split_pack8(const float* v, u32x4& hi, u32x4& lo
 __device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_h(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+// float -> fp16 bits, round to nearest even, saturated to +-65504 (the KV cache format)
+__device__ __forceinline__ uint16_t f2h(float x) {
+  return __builtin_bit_cast(uint16_t, (_Float16)fminf(fmaxf(x, -65504.f), 65504.f));
+}
+__device__ __forceinline__ float h2f(uint32_t b) { return (float)__builtin_bit_cast(_Float16, (uint16_t)b); }
+
+// fp16 hi/lo split of 8 floats (x ~= hi + lo with about 22 significant bits)
+__device__ __forceinline__ void split_pack8_h(const float* v, u32x4& hi, u32x4& lo) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t h0 = f2h(v[2 * e]), h1 = f2h(v[2 * e + 1]);
+    const uint32_t l0 = f2h(v[2 * e] - h2f(h0)), l1 = f2h(v[2 * e + 1] - h2f(h1));
+    hi[e] = h0 | (h1 << 16);
+    lo[e] = l0 | (l1 << 16);
+  }
 }
 
 // Every buffer lives in device (global) memory; pointers that come from memory rather than
@@ -403,18 +425,10 @@ __global__ __launch_bounds__(64 * WAVES) void k_kvt(KvtArgs a) {
         const int dim = (col < 8) ? m : half + m;
         const float2 cs = a.rope[(long)(valid ? slot : 0) * half + m];
         const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
-        if (valid) {  // the cache keeps y as two bf16 planes, y ~= hi + lo
-          const long ix = ((long)head * a.Lcap + slot) * a.hd + dim;
-          const uint32_t hb = f2bf(y);
-          kc[ix] = (uint16_t)hb;
-          kc[ix + a.plane] = (uint16_t)f2bf(y - bf2f(hb));
-        }
+        if (valid) kc[((long)head * a.Lcap + slot) * a.hd + dim] = f2h(y);
       } else if (valid) {
         const int dim = jj * 16 + col;
-        const long ix = ((long)head * a.hd + dim) * a.Lcap + slot;
-        const uint32_t hb = f2bf(x);
-        vt[ix] = (uint16_t)hb;
-        vt[ix + a.plane] = (uint16_t)f2bf(x - bf2f(hb));
+        vt[((long)head * a.hd + dim) * a.Lcap + slot] = f2h(x);
       }
     }
   }
@@ -637,19 +651,13 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
         if (valid) {
           if (region == 0) {
             st_wt(g.q_out + (long)row * q_dim + head * hd + dim, y);
-          } else {  // block keys go to cache slots L + row as two bf16 planes, y ~= hi + lo
-            const long ix = ((long)head * a->Lcap + slot) * hd + dim;
-            const uint32_t hb = f2bf(y);
-            st_wt(g.kc + ix, (uint16_t)hb);
-            st_wt(g.kc + ix + a->plane, (uint16_t)f2bf(y - bf2f(hb)));
+          } else {  // block keys go to cache slots L + row
+            st_wt(g.kc + ((long)head * a->Lcap + slot) * hd + dim, f2h(y));
           }
         }
       } else if (valid) {
         const int dim = jj * 16 + col;
-        const long ix = ((long)head * hd + dim) * a->Lcap + slot;
-        const uint32_t hb = f2bf(x);
-        st_wt(g.vt + ix, (uint16_t)hb);
-        st_wt(g.vt + ix + a->plane, (uint16_t)f2bf(x - bf2f(hb)));
+        st_wt(g.vt + ((long)head * hd + dim) * a->Lcap + slot, f2h(x));
       }
     }
   } else if constexpr (EPI == EPI_ARGMAX) {
@@ -845,8 +853,9 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
 
   // The scheduling barriers keep each set's reload right after its MFMAs: left alone, the
   // compiler sinks a reload past the other sets' MFMAs, and the wait for the next set then
-  // drains every load in flight.
-  for (int s0 = 0; s0 < total; s0 += NS) {
+  // drains every load in flight.  The last NS steps (total is a multiple of NS) request
+  // nothing more.
+  for (int s0 = 0; s0 + NS < total; s0 += NS) {
 #pragma unroll
     for (int i = 0; i < NS; ++i) {
 #pragma unroll
@@ -861,6 +870,16 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
     }
     const int done = s0 + NS;
     if (done % nbr == 0) chunk_end(done / nbr - 1);
+  }
+  if (total > 0) {
+#pragma unroll
+    for (int i = 0; i < NS; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        acc[j] = mfma(ah[i], w[i][j], acc[j]);
+        acc[j] = mfma(al[i], w[i][j], acc[j]);
+      }
+    chunk_end(nch - 1);
   }
 
   if (kg > 1 && total > 0) {
@@ -923,36 +942,46 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
 // Sec. 3.2: no mask; every block row attends to the whole context and the whole block.
 // Work item (chunk c, KV head g): keys [c*CK, (c+1)*CK) of the context, the last chunk also
 // the B block keys (cache slots L .. L+B-1, written by the QKV phase).  K rows and V^T rows
-// of the chunk, both bf16 planes (hi, lo), are staged in LDS (16-byte pieces, XOR-swizzled
-// columns so that fragment reads of 16 different rows hit different banks).  The pieces of
-// context keys are requested before the grid barrier; only the block keys and the queries
-// depend on the QKV phase, and the early requests never touch a cache line that the QKV
-// phase writes (K rows are whole lines; a V^T line is requested early only if all its 64
-// slots are context).  Wave w < QT then takes query tile w: rows r = w*16 + lane%16 of
-// the G*B rows that share head g (r -> query head g*G + r/B, block row r%B).  Scores are
-// formed transposed, S^T = K Q^T, so that the probabilities land in exactly the B-operand
-// layout of the P V product and never leave registers.  Products of two hi/lo pairs keep
-// the three terms above 2^-16 relative: hi*hi + hi*lo + lo*hi.
+// of the chunk (fp16) are staged in LDS (16-byte pieces, XOR-swizzled columns so that
+// fragment reads of 16 different rows hit different banks).  The pieces of context keys
+// are requested before the grid barrier; only the block keys and the queries depend on the
+// QKV phase, and the early requests never touch a cache line that the QKV phase writes (K
+// rows are whole lines; a V^T line is requested early only if all its 64 slots are
+// context).  The G*B query rows that share head g form QT tiles of 16 (row r -> query head
+// g*G + r/B, block row r%B); the waves form KS = 8 / QT groups of QT, group k taking the
+// k-th of KS runs of 32-key blocks, so that all waves share the work.  Scores are formed
+// transposed, S^T = K Q^T, so that the probabilities land in exactly the B-operand layout
+// of the P V product and never leave registers.  Queries and probabilities enter the fp16
+// matrix cores as hi/lo pairs (about 22 significant bits) against the fp16 keys and values.
+// The KS partial results of a query tile (running max, sum, unnormalised output) are
+// merged through LDS in group order.
 template <int HD>
 __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed,
                            u32x4* smem) {
   constexpr int CK = kChunk;
   constexpr int CKM = CK + 32;   // keys held by a work-group (room for the B <= 16 block keys)
+  constexpr int NKB = CKM / 32;  // 32-key blocks of a work item
   constexpr int KC = HD / 8;     // 16-byte columns of a K row
   constexpr int VC = CKM / 8;    // 16-byte columns of a V^T row (a multiple of 4)
-  constexpr int KPC = 2 * CKM * KC, VPC = 2 * HD * VC;  // pieces of both planes
-  constexpr int PER = (KPC + VPC) / kThreads;          // pieces per thread
-  static_assert((KPC + VPC) % kThreads == 0, "pieces must split evenly over the work-group");
-  u32x4* sK = smem;                 // [2][CKM * KC]: (row r, column c) at r*KC + (c ^ (r & 7))
-  u32x4* sV = smem + 2 * CKM * KC;  // [2][HD * VC]:  (row d, column c) at d*VC + (c ^ (d & 3))
+  constexpr int KP = CKM * KC, VP = HD * VC;
+  constexpr int PER = (KP + VP) / kThreads;  // pieces per thread
+  constexpr int DT = HD / 16;                // 16-dim tiles of an output row
+  static_assert((KP + VP) % kThreads == 0, "pieces must split evenly over the work-group");
+  static_assert(KC >= 8, "K swizzle needs 8 columns");
+  u32x4* sK = smem;                                        // (row r, column c) at r*KC + (c ^ (r & 7))
+  u32x4* sV = smem + KP;                                   // (row d, column c) at d*VC + (c ^ (d & 3))
+  f32x4* sO = reinterpret_cast<f32x4*>(smem + KP + VP);    // merge: [kWaves][DT][64]
+  float2* sML = reinterpret_cast<float2*>(sO + kWaves * DT * 64);  // [kWaves][16]
+  static_assert((KP + VP) * 16 + kWaves * DT * 64 * 16 + kWaves * 16 * 8 <= kLdsBytes, "LDS");
 
-  const int tid = opaque(threadIdx.x), lane = tid & 63, w = tid >> 6;
-  const int quad = lane >> 4, q = lane & 15;
+  const int tid = opaque(threadIdx.x), lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = dc->L;
   const int nch = max(1, (L + CK - 1) / CK);
   const int items = nch * a->n_kv;
   const int G = a->n_q / a->n_kv;
   const int R = G * a->B;
+  const int QT = (R + 15) / 16, KS = kWaves / QT;
   const uint16_t* kc = a->kc + layer * a->cache_layer;
   const uint16_t* vt = a->vt + layer * a->cache_layer;
   const float* Q = a->Q + layer * a->q_stride;
@@ -962,29 +991,27 @@ __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
   // index is laundered through an empty asm statement so that the compiler recomputes the
   // piece coordinates here instead of keeping them in registers for the whole kernel.
   auto issue = [&](int j, int pass, u32x4 (&pcs)[PER]) {
-    int tid = threadIdx.x;
-    asm volatile("" : "+v"(tid));
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
     const int c = j / a->n_kv, g = j % a->n_kv;
     const int kbeg = c * CK;
     const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + CK) - kbeg;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int p = i * kThreads + tid;
-      if (p < KPC) {
-        const int pl = p / (CKM * KC), rem = p % (CKM * KC);
-        const int r = rem / KC, col = rem % KC;
+      const int p = i * kThreads + t;
+      if (p < KP) {
+        const int r = p / KC, col = p % KC;
         const bool ctx = kbeg + r < L;
         if (r < nkeys && (pass == 0 ? ctx : !ctx))
-          pcs[i] = *gbl(reinterpret_cast<const u32x4*>(kc + pl * a->plane + ((long)g * a->Lcap + kbeg + r) * HD + col * 8));
+          pcs[i] = *gbl(reinterpret_cast<const u32x4*>(kc + ((long)g * a->Lcap + kbeg + r) * HD + col * 8));
       } else {
-        const int pv = p - KPC;
-        const int pl = pv / (HD * VC), rem = pv % (HD * VC);
-        const int d = rem / VC, col = rem % VC;
+        const int pv = p - KP;
+        const int d = pv / VC, col = pv % VC;
         // requested early only if its whole 128-byte line (64 keys) precedes slot L: the line
         // holding slot L also receives the block's values in the QKV phase
         const bool ctx = ((kbeg + col * 8) & ~63) + 64 <= L;
         if (col * 8 < nkeys && (pass == 0 ? ctx : !ctx))
-          pcs[i] = *gbl(reinterpret_cast<const u32x4*>(vt + pl * a->plane + ((long)g * HD + d) * a->Lcap + kbeg + col * 8));
+          pcs[i] = *gbl(reinterpret_cast<const u32x4*>(vt + ((long)g * HD + d) * a->Lcap + kbeg + col * 8));
       }
     }
   };
@@ -993,11 +1020,15 @@ __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
   auto finish = [&](int j, u32x4 (&pcs)[PER]) {
     issue(j, 1, pcs);
     const int c = j / a->n_kv, g = j % a->n_kv;
-    const int kbeg = c * CK;
-    const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + CK) - kbeg;
-    const int r = w * 16 + q;
-    const bool active = w * 16 < R;  // wave-uniform
+    const int nkeys = ((c == nch - 1) ? L + a->B : c * CK + CK) - c * CK;
+    const int qt = w % QT, kh = w / QT;
+    const bool active = kh < KS;  // wave-uniform
+    const int q = lane & 15, quad = lane >> 4;
+    const int r = qt * 16 + q;
     const bool rv = r < R;
+    // this wave's 32-key blocks [kb0, kb1)
+    const int nkb = (nkeys + 31) / 32, bps = (nkb + KS - 1) / KS;
+    const int kb0 = min(kh * bps, nkb), kb1 = min(kb0 + bps, nkb);
     float4 qx[HD / 16];
     {
       const int bb = rv ? r % a->B : 0;
@@ -1017,20 +1048,18 @@ __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
         }
       }
     }
-    // pieces to LDS (keys past the end become zeros)
+    // pieces to LDS (values of keys past the end become zeros)
     int tid2 = threadIdx.x;
     asm volatile("" : "+v"(tid2));
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int p = i * kThreads + tid2;
-      if (p < KPC) {
-        const int pl = p / (CKM * KC), rem = p % (CKM * KC);
-        const int rr = rem / KC, col = rem % KC;
-        sK[pl * CKM * KC + rr * KC + (col ^ (rr & 7))] = pcs[i];
+      if (p < KP) {
+        const int rr = p / KC, col = p % KC;
+        sK[rr * KC + (col ^ (rr & 7))] = pcs[i];
       } else {
-        const int pv = p - KPC;
-        const int pl = pv / (HD * VC), rem = pv % (HD * VC);
-        const int d = rem / VC, col = rem % VC;
+        const int pv = p - KP;
+        const int d = pv / VC, col = pv % VC;
         u32x4 v = pcs[i];
         const int nv = nkeys - col * 8;  // valid keys in this piece
         if (nv < 8) {
@@ -1040,108 +1069,127 @@ __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
             else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;
           }
         }
-        sV[pl * HD * VC + d * VC + (col ^ (d & 3))] = v;
+        sV[d * VC + (col ^ (d & 3))] = v;
       }
     }
     __syncthreads();
-    if (active) {
+    float m = -INFINITY, l = 0.f;
+    f32x4 o[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (active && kb1 > kb0) {
       u32x4 qh[HD / 32], ql[HD / 32];
 #pragma unroll
       for (int ks = 0; ks < HD / 32; ++ks) {
         const float4 x0 = qx[2 * ks], x1 = qx[2 * ks + 1];
         float v[8] = {x0.x * a->qscale, x0.y * a->qscale, x0.z * a->qscale, x0.w * a->qscale,
                       x1.x * a->qscale, x1.y * a->qscale, x1.z * a->qscale, x1.w * a->qscale};
-        split_pack8(v, qh[ks], ql[ks]);
+        split_pack8_h(v, qh[ks], ql[ks]);
       }
-      // LDS read addresses: per-lane byte bases plus compile-time offsets below 64 KiB, so
-      // that every read takes its offset as an immediate (row kt*16 + q has swizzle key
-      // q & 7; row d = dt*16 + q has key q & 3).  The bases are laundered so that the
-      // compiler neither folds the large plane offsets into per-read registers nor keeps
-      // them alive outside this block.
+      // LDS read addresses: per-lane byte bases plus compile-time offsets, so that every read
+      // takes its offset as an immediate (row kt*16 + q has swizzle key q & 7; row
+      // d = dt*16 + q has key q & 3).  The bases are laundered so that the compiler neither
+      // folds them into per-read registers nor keeps them alive outside this block.
       const char* lds = reinterpret_cast<const char*>(smem);
       const int ln = opaque(threadIdx.x & 63);
-      const int q = ln & 15, quad = ln >> 4;
-      int kh_at[HD / 32], kl_at[HD / 32];
+      const int qq = ln & 15, qd = ln >> 4;
+      int k_at[HD / 32];
 #pragma unroll
-      for (int ks = 0; ks < HD / 32; ++ks) {
-        kh_at[ks] = opaque((q * KC + ((ks * 4 + quad) ^ (q & 7))) * 16);
-        kl_at[ks] = opaque(kh_at[ks] + CKM * KC * 16);
-      }
-      const int vx = (quad >> 1) ^ (q & 3);
-      const int vbase = 2 * CKM * KC * 16 + (quad & 1) * 8;  // sV, half of a 16-byte column
-      const int vh0 = opaque(vbase + (q * VC + vx) * 16), vh1 = opaque(vbase + (q * VC + (vx ^ 2)) * 16);
-      const int vl0 = opaque(vh0 + HD * VC * 16), vl1 = opaque(vh1 + HD * VC * 16);
-      f32x4 s[CKM / 16];
+      for (int ks = 0; ks < HD / 32; ++ks) k_at[ks] = opaque((qq * KC + ((ks * 4 + qd) ^ (qq & 7))) * 16);
+      const int vx = (qd >> 1) ^ (qq & 3);
+      const int vbase = KP * 16 + (qd & 1) * 8;  // sV, half of a 16-byte column
+      const int v0 = opaque(vbase + (qq * VC + vx) * 16), v1 = opaque(vbase + (qq * VC + (vx ^ 2)) * 16);
+      // scores of the wave's blocks (blocks outside [kb0, kb1) and keys past the end: -inf)
+      f32x4 sc[2 * NKB];
 #pragma unroll
-      for (int kt = 0; kt < CKM / 16; ++kt) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int kt = 0; kt < 2 * NKB; ++kt) {
+        f32x4 acc = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+        if (kt / 2 >= kb0 && kt / 2 < kb1) {
+          acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < HD / 32; ++ks) {
-          const u32x4 kh = *reinterpret_cast<const u32x4*>(lds + kh_at[ks] + kt * 16 * KC * 16);
-          const u32x4 kl = *reinterpret_cast<const u32x4*>(lds + kl_at[ks] + kt * 16 * KC * 16);
-          acc = mfma(kh, qh[ks], acc);
-          acc = mfma(kh, ql[ks], acc);
-          acc = mfma(kl, qh[ks], acc);
+          for (int ks = 0; ks < HD / 32; ++ks) {
+            const u32x4 kv = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + kt * 16 * KC * 16);
+            acc = mfma_h(kv, qh[ks], acc);
+            acc = mfma_h(kv, ql[ks], acc);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (kt * 16 + qd * 4 + i >= nkeys) acc[i] = -INFINITY;
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (kt * 16 + quad * 4 + i >= nkeys) acc[i] = -INFINITY;
-        s[kt] = acc;
+        sc[kt] = acc;
         __builtin_amdgcn_sched_barrier(0);  // bound how far LDS reads are hoisted (registers)
       }
       // softmax statistics per query row (column q), in the log2 domain
-      float m = -INFINITY;
 #pragma unroll
-      for (int kt = 0; kt < CKM / 16; ++kt)
+      for (int kt = 0; kt < 2 * NKB; ++kt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) m = fmaxf(m, s[kt][i]);
+        for (int i = 0; i < 4; ++i) m = fmaxf(m, sc[kt][i]);
       m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
-      float l = 0.f;
 #pragma unroll
-      for (int kt = 0; kt < CKM / 16; ++kt)
+      for (int kt = 0; kt < 2 * NKB; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float p = exp2f(s[kt][i] - m);
-          s[kt][i] = p;
+          const float p = exp2f(sc[kt][i] - m);
+          sc[kt][i] = p;
           l += p;
         }
       l += __shfl_xor(l, 16);
       l += __shfl_xor(l, 32);
-      // O^T = V^T P^T over the chunk
-      f32x4 o[HD / 16];
+      // O^T = V^T P^T over the wave's blocks
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kk = 0; kk < NKB; ++kk) {
+        if (kk >= kb0 && kk < kb1) {
+          float pv[8] = {sc[2 * kk][0], sc[2 * kk][1], sc[2 * kk][2], sc[2 * kk][3],
+                         sc[2 * kk + 1][0], sc[2 * kk + 1][1], sc[2 * kk + 1][2], sc[2 * kk + 1][3]};
+          u32x4 ph, pl;
+          split_pack8_h(pv, ph, pl);
+          // keys kk*32 + 4*qd + 0..3 and + 16: 16-byte columns kk*4 + qd/2 and + 2, halves qd & 1
 #pragma unroll
-      for (int kk = 0; kk < CKM / 32; ++kk) {
-        float pv[8] = {s[2 * kk][0], s[2 * kk][1], s[2 * kk][2], s[2 * kk][3],
-                       s[2 * kk + 1][0], s[2 * kk + 1][1], s[2 * kk + 1][2], s[2 * kk + 1][3]};
-        u32x4 ph, pl;
-        split_pack8(pv, ph, pl);
-        // keys kk*32 + 4*quad + 0..3 and + 16: 16-byte columns kk*4 + quad/2 and + 2, halves quad & 1
-#pragma unroll
-        for (int dt = 0; dt < HD / 16; ++dt) {
-          const int off = (dt * 16 * VC + kk * 4) * 16;
-          const u32x2 h0 = *reinterpret_cast<const u32x2*>(lds + vh0 + off);
-          const u32x2 h1 = *reinterpret_cast<const u32x2*>(lds + vh1 + off);
-          const u32x2 l0 = *reinterpret_cast<const u32x2*>(lds + vl0 + off);
-          const u32x2 l1 = *reinterpret_cast<const u32x2*>(lds + vl1 + off);
-          const u32x4 vh = {h0[0], h0[1], h1[0], h1[1]};
-          const u32x4 vl = {l0[0], l0[1], l1[0], l1[1]};
-          o[dt] = mfma(vh, ph, o[dt]);
-          o[dt] = mfma(vh, pl, o[dt]);
-          o[dt] = mfma(vl, ph, o[dt]);
+          for (int dt = 0; dt < DT; ++dt) {
+            const int off = (dt * 16 * VC + kk * 4) * 16;
+            const u32x2 h0 = *reinterpret_cast<const u32x2*>(lds + v0 + off);
+            const u32x2 h1 = *reinterpret_cast<const u32x2*>(lds + v1 + off);
+            const u32x4 vv = {h0[0], h0[1], h1[0], h1[1]};
+            o[dt] = mfma_h(vv, ph, o[dt]);
+            o[dt] = mfma_h(vv, pl, o[dt]);
+          }
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      if (rv) {
-        const long base = ((long)c * a->n_kv + g) * a->Rpad + r;
+    }
+    // merge the KS key runs of each query tile (group order), then store the item's partial
+    if (KS > 1) {
+      if (active) {
 #pragma unroll
-        for (int dt = 0; dt < HD / 16; ++dt)
-          st_wt16(a->OP + base * HD + dt * 16 + quad * 4, __builtin_bit_cast(u32x4, o[dt]));
-        if (quad == 0)
-          st_wt8(a->ML + base, (uint64_t)__float_as_uint(m) | ((uint64_t)__float_as_uint(l) << 32));
+        for (int dt = 0; dt < DT; ++dt) sO[(w * DT + dt) * 64 + lane] = o[dt];
+        if (quad == 0) sML[w * 16 + q] = make_float2(m, l);
       }
+      __syncthreads();
+      if (active && kh == 0) {
+        float M = -INFINITY;
+        for (int k = 0; k < KS; ++k) M = fmaxf(M, sML[(qt + k * QT) * 16 + q].x);
+        float lt = 0.f;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int k = 0; k < KS; ++k) {
+          const int wk = qt + k * QT;
+          const float2 mlk = sML[wk * 16 + q];
+          const float f = exp2f(mlk.x - M);  // 0 for a run without keys
+          lt += f * mlk.y;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[dt] += f * sO[(wk * DT + dt) * 64 + lane];
+        }
+        m = M;
+        l = lt;
+      }
+    }
+    if (active && kh == 0 && rv) {
+      const long base = ((long)c * a->n_kv + g) * a->Rpad + r;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        st_wt16(a->OP + base * HD + dt * 16 + quad * 4, __builtin_bit_cast(u32x4, o[dt]));
+      if (quad == 0) st_wt8(a->ML + base, (uint64_t)__float_as_uint(m) | ((uint64_t)__float_as_uint(l) << 32));
     }
     __syncthreads();  // LDS is refilled by the next item
   };

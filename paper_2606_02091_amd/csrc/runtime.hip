@@ -33,6 +33,20 @@ thread_local std::string g_init_error;
 
 int ceil_div(long a, long b) { return (int)((a + b - 1) / b); }
 
+// IEEE binary16 bits -> float (exact)
+float half_to_float(uint16_t hbits) {
+  const uint32_t sign = (uint32_t)(hbits >> 15) << 31, e = (hbits >> 10) & 31u, m = hbits & 1023u;
+  float v;
+  if (e == 0) v = ldexpf((float)m, -24);                        // zero, subnormal
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = ldexpf((float)(m | 1024u), (int)e - 25);
+  uint32_t u;
+  memcpy(&u, &v, 4);
+  u |= sign;
+  memcpy(&v, &u, 4);
+  return v;
+}
+
 }  // namespace
 
 namespace {
@@ -60,7 +74,6 @@ struct dflare_handle {
   // context cache
   uint16_t *kc = nullptr, *vt = nullptr;
   long cache_layer_stride = 0;
-  long cache_plane = 0;
   float2* rope = nullptr;
   u32x4* zero_tile = nullptr;
   // fuse_append scratch
@@ -373,9 +386,8 @@ int build(dflare_handle* h, const dflare_weights* w) {
   HIP_OR_FAIL(h, hipMemcpyAsync(h->alpha, h->alpha_host.data(), (size_t)D * S * 4, hipMemcpyHostToDevice, s));
 
   // ---- context cache, rotary table
-  // per layer: K (or V^T) as two bf16 planes, hi then lo (value ~= hi + lo)
-  h->cache_plane = (long)c.n_kv_heads * h->Lcap * hd;
-  h->cache_layer_stride = 2 * h->cache_plane;
+  // per layer: K (or V^T) in fp16
+  h->cache_layer_stride = (long)c.n_kv_heads * h->Lcap * hd;
   TRY(dev_zalloc(h, &h->kc, (size_t)h->cache_layer_stride * D * 2));
   TRY(dev_zalloc(h, &h->vt, (size_t)h->cache_layer_stride * D * 2));
   {
@@ -466,7 +478,6 @@ DraftArgs draft_args(const dflare_handle* h) {
   a.rope = h->rope;
   a.kc = h->kc;
   a.vt = h->vt;
-  a.plane = h->cache_plane;
   a.cache_layer = h->cache_layer_stride;
   a.X = h->X;
   a.XS = h->XS;
@@ -649,7 +660,6 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   a.n_new = n_new;
   a.kc = h->kc;
   a.vt = h->vt;
-  a.plane = h->cache_plane;
   a.cache_layer_stride = h->cache_layer_stride;
   a.Lcap = h->Lcap;
   a.hd = c.head_dim;
@@ -799,11 +809,7 @@ int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, in
           for (int d = 0; d < hd; ++d) {
             const size_t ix = (what == DFLARE_DBG_KCACHE) ? ((size_t)g * h->Lcap + p) * hd + d
                                                           : ((size_t)g * hd + d) * h->Lcap + p;
-            const uint32_t hb = (uint32_t)raw[ix] << 16, lb = (uint32_t)raw[ix + h->cache_plane] << 16;
-            float fh, fl;
-            memcpy(&fh, &hb, 4);
-            memcpy(&fl, &lb, 4);
-            host_out[((size_t)p * nkv + g) * hd + d] = fh + fl;
+            host_out[((size_t)p * nkv + g) * hd + d] = half_to_float(raw[ix]);
           }
       return DFLARE_OK;
     }
