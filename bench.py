@@ -232,11 +232,13 @@ def main():
 
 def phase_trace(dfl, h, step, cfg, kb, steps):
     """Per-phase time inside the persistent draft-block kernel, from its wall-clock trace
-    (100 MHz).  For each phase kind, microseconds per step (summed over layers): "us" from
-    the moment the work-groups pass the grid barrier into the phase to the moment they pass
-    into the next one, split into "body" (until the work-group's stores are complete) and
-    "wait" (at the next barrier); medians over work-groups; "body_max" is the slowest
-    work-group.  "GBs" relates "us" to the phase's algorithmic bytes."""
+    (100 MHz, four marks per phase).  For each phase kind, microseconds per step (summed
+    over layers), medians over work-groups: "us" from the moment the work-groups pass the
+    grid barrier into the phase to the moment they pass into the next one; "body" until the
+    work-group's stores are complete, "body_max" for the slowest work-group; "wait" at the
+    next barrier.  "seg" splits the body at the phase's inner marks (GEMM: main loop, chunk
+    epilogues, split-K combine and final epilogue; attention: key staging, scores and
+    values, merge and stores).  "GBs" relates "us" to the phase's algorithmic bytes."""
     import numpy as np
     n_launch, _, blocks, n_phase, _ = dfl.dflare_kernel_stats(h)
     if n_launch != 1:
@@ -246,24 +248,32 @@ def phase_trace(dfl, h, step, cfg, kb, steps):
     acc = {}
     for k in range(steps):
         step(k)
-        t = dfl.dflare_debug_read(h, dfl.DBG_TRACE, 0, (blocks, n_phase, 2)).astype(np.float64)
-        start, end = t[:, :, 0], t[:, :, 1]
+        t = dfl.dflare_debug_read(h, dfl.DBG_TRACE, 0, (blocks, n_phase, 4)).astype(np.float64)
+        start, end = t[:, :, 0], t[:, :, 3]
         nxt = np.concatenate([start[:, 1:], end[:, -1:]], axis=1)
         for p, name in enumerate(names):
-            a = acc.setdefault(name, np.zeros(4))
+            a = acc.setdefault(name, np.zeros(7))
+            m1, m2 = t[:, p, 1], t[:, p, 2]
+            seg = [np.nan, np.nan, np.nan]
+            ok1, ok2 = m1 >= 0, m2 >= 0
+            if ok1.any() and ok2.any():
+                seg = [np.median((m1 - start[:, p])[ok1]), np.median((m2 - m1)[ok1 & ok2]),
+                       np.median((end[:, p] - m2)[ok2])]
             a += [np.median(nxt[:, p] - start[:, p]), np.median(end[:, p] - start[:, p]),
-                  np.max(end[:, p] - start[:, p]), np.median(nxt[:, p] - end[:, p])]
+                  np.max(end[:, p] - start[:, p]), np.median(nxt[:, p] - end[:, p])] + seg
     dfl.dflare_set_option(h, dfl.OPT_TRACE, 0)
     layer_bytes = {"qkv": kb["qkv"], "attn": kb["attn"], "o": kb["o"], "gate_up": kb["gate_up"],
                    "down": kb["down"]}
     out = {}
     for name, a in acc.items():
-        us, body, body_max, wait = (a / steps).tolist()
+        us, body, body_max, wait, s1, s2, s3 = (a / steps).tolist()
         reps = cfg.n_draft_layers if name in layer_bytes else 1
         nbytes = layer_bytes.get(name, kb["lm_head"] if name == "lm_head" else 0) * reps
         out[name] = {"us": round(us, 2), "body": round(body, 2), "body_max": round(body_max, 2),
                      "wait": round(wait, 2),
                      "GBs": round(nbytes / (us * 1e-6) / 1e9, 1) if nbytes and us > 0 else None}
+        if not np.isnan(s1):
+            out[name]["seg"] = [round(s1, 2), round(s2, 2), round(s3, 2)]
     return out
 
 

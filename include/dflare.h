@@ -176,11 +176,14 @@ const char* dflare_last_error(const dflare_handle* h);
  *   what = DFLARE_DBG_HIDDEN  layer i: [B, H]        block rows after layer i
  *   what = DFLARE_DBG_LOGITS  (layer ignored) [B, V] logits of the last draft_block
  *   what = DFLARE_DBG_ALPHA   (layer ignored) [D, S] cached fusion weights
- *   what = DFLARE_DBG_TRACE   (layer ignored) [blocks, phases, 2] microseconds at which
- *                             each work-group of the last draft_block began each phase
- *                             (after its grid barrier) and finished it (its stores
- *                             complete), relative to the earliest start; needs
- *                             DFLARE_OPT_TRACE (sizes from dflare_kernel_stats)
+ *   what = DFLARE_DBG_TRACE   (layer ignored) [blocks, phases, 4] microseconds, relative to
+ *                             the earliest mark, at which each work-group of the last
+ *                             draft_block reached four marks of each phase: body start
+ *                             (after its grid barrier), two inner marks (GEMM phases: main
+ *                             loop done, chunk epilogues done; attention: keys staged in LDS,
+ *                             scores and values done), stores complete; -1 where a phase sets
+ *                             no such mark.  Needs DFLARE_OPT_TRACE (sizes from
+ *                             dflare_kernel_stats)
  * `count` is the number of floats host_out can hold; too small is INVALID_ARG.
  * Debug capture makes draft_block run one launch per phase.
  */

@@ -25,6 +25,10 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kStatsPad = 32;   // floats per 16-column tile in the sums-of-squares arrays (one 128 B line)
 constexpr int kBarCounters = 16;  // grid-barrier arrival counters, each on its own 128 B line
 constexpr int kMaxBlock = 16;     // draft block rows (one 16-row MFMA tile)
+// wall-clock marks per phase: body start (after the grid barrier), two inner marks
+// (GEMM: main loop done, chunk epilogues done; attention: keys staged, scores and
+// values done; combine: partials loaded), stores complete
+constexpr int kTraceSlots = 4;
 constexpr int kTNMax = 8;         // output tiles a GEMM work-group accumulates at once
 constexpr int kMaxSplit = 8;      // work-groups that split one GEMM output range along K
 constexpr int kMaxBlocks = 1024;  // work-groups of the draft-block kernel
@@ -65,7 +69,7 @@ struct DraftCall {
   float* logits;        // optional [B, V]
   unsigned bar_epoch;   // grid barriers completed by earlier launches
   unsigned done_epoch;  // launches that ran the LM phase before this one
-  unsigned long long* trace;  // optional [blocks][phases][2] wall clock at each phase's start and end
+  unsigned long long* trace;  // optional [blocks][phases][kTraceSlots] wall clock at marks of each phase
 };
 
 // Everything else the draft-block kernel needs; written to device memory once at init and

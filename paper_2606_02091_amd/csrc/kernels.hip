@@ -692,6 +692,157 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
   }
 }
 
+// Registers carried from one phase into the next: the QKV phase issues the context pieces
+// of the first attention item as soon as its own weight streaming is done, so that they are
+// in flight during its epilogue, its stores and the grid barrier.  GEMM phases use the same
+// registers for their first weight tiles.  Every prefetch writes all kPf entries (zeros
+// where it loads nothing), so that the registers are free inside the phases that do not
+// carry anything.
+constexpr int kPf = 16;
+typedef u32x4 Carry[kPf];
+
+__host__ __device__ constexpr int gemm_ns(int TN) { return TN >= 8 ? 2 : 4; }  // steps in flight
+
+// The GEMM job of phase (kind, layer): weights, input fragments and epilogue targets.
+__device__ __forceinline__ GemmJob make_job(Args a, int kind, int layer) {
+  GemmJob g{};
+  const int H = a->H, Kt_H = H / 32, q_Kt = a->n_q * a->hd / 32, F_Kt = a->F / 32;
+  switch (kind) {
+    case PH_QKV: {
+      const int s = 2 * layer;
+      g.W = a->w_qkv + layer * a->s_qkv;
+      g.Nt = (a->n_q + 2 * a->n_kv) * a->hd / 16;
+      g.Kt = Kt_H;
+      g.Ahi = a->XA + s * a->xa_stride;
+      g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
+      g.stats = a->XS + s * a->xs_stride;
+      g.q_out = a->Q + layer * a->q_stride;
+      g.kc = a->kc + layer * a->cache_layer;
+      g.vt = a->vt + layer * a->cache_layer;
+      break;
+    }
+    case PH_O:
+    case PH_DOWN: {
+      const bool o = kind == PH_O;
+      const int s = o ? 2 * layer + 1 : 2 * layer + 2;
+      g.W = o ? a->w_o + layer * a->s_o : a->w_down + layer * a->s_down;
+      g.Nt = H / 16;
+      g.Kt = o ? q_Kt : F_Kt;
+      g.Ahi = o ? a->OA + layer * a->oa_stride : a->HA + layer * a->ha_stride;
+      g.Alo = g.Ahi + (long)(g.Kt + kKtPad) * 64;
+      g.stats = nullptr;
+      g.xs_out = a->XS + s * a->xs_stride;
+      g.na_hi = reinterpret_cast<uint32_t*>(a->XA + s * a->xa_stride);
+      g.na_lo = reinterpret_cast<uint32_t*>(a->XA + s * a->xa_stride + (long)(Kt_H + kKtPad) * 64);
+      g.na_Kt = Kt_H;
+      g.gain = o ? a->g_mlp + (long)layer * H : (layer + 1 < a->D ? a->g_attn + (long)(layer + 1) * H : a->g_final);
+      break;
+    }
+    case PH_GU: {
+      const int s = 2 * layer + 1;
+      g.W = a->w_gu + layer * a->s_gu;
+      g.Nt = 2 * a->F / 16;
+      g.Kt = Kt_H;
+      g.Ahi = a->XA + s * a->xa_stride;
+      g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
+      g.stats = a->XS + s * a->xs_stride;
+      g.na_hi = reinterpret_cast<uint32_t*>(a->HA + layer * a->ha_stride);
+      g.na_lo = reinterpret_cast<uint32_t*>(a->HA + layer * a->ha_stride + (long)(F_Kt + kKtPad) * 64);
+      g.na_Kt = F_Kt;
+      break;
+    }
+    default: {  // PH_LM
+      const int s = 2 * a->D;
+      g.W = a->w_lm;
+      g.Nt = (a->V + 15) / 16;
+      g.Kt = Kt_H;
+      g.Ahi = a->XA + s * a->xa_stride;
+      g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
+      g.stats = a->XS + s * a->xs_stride;
+      break;
+    }
+  }
+  return g;
+}
+
+// A work-group's share of a GEMM phase (see gemm_phase): output range rg (n-tiles
+// [t0, t0 + T), chunks of TN), K part kgi, this wave's k-tiles [k0, k1), nbr steps per
+// chunk and total steps of its stream.
+struct GemmGeom {
+  int rg, kgi, t0, T, nch, k0, k1, nbr, total, kw_last;
+};
+template <int TN>
+__device__ __forceinline__ GemmGeom gemm_geom(const GemmJob& g, int kg, int wave) {
+  constexpr int NS = gemm_ns(TN);
+  GemmGeom q;
+  const int R = gridDim.x / kg;
+  q.kgi = blockIdx.x % kg;
+  q.rg = blockIdx.x / kg;
+  q.t0 = (int)((long)q.rg * g.Nt / R);
+  q.T = (int)((long)(q.rg + 1) * g.Nt / R) - q.t0;
+  q.nch = (q.T + TN - 1) / TN;
+  const int kb = (int)((long)q.kgi * g.Kt / kg), ke = (int)((long)(q.kgi + 1) * g.Kt / kg);
+  q.k0 = kb + (wave * (ke - kb)) / kWaves;
+  q.k1 = kb + ((wave + 1) * (ke - kb)) / kWaves;
+  // steps per chunk: the longest slice rounded up to a multiple of NS (the same for every
+  // wave, so that all waves reach each chunk end together)
+  const int slice = (ke - kb + kWaves - 1) / kWaves;
+  q.nbr = max(NS, ((slice + NS - 1) / NS) * NS);
+  q.total = q.T > 0 ? q.nch * q.nbr : 0;
+  q.kw_last = max(q.k1 - 1, 0);
+  return q;
+}
+
+// weight tile j of step s of a wave's stream (chunk s / nbr, k-tile k0 + s % nbr); steps
+// past the stream's end re-read the last real tile (their A fragments are zero)
+template <int TN>
+__device__ __forceinline__ u32x4 gemm_tile(const GemmJob& g, const GemmGeom& q, int lane, int s, int j) {
+  const int ch = min(s / q.nbr, q.nch - 1);
+  const int k = min(q.k0 + (s - ch * q.nbr), q.kw_last);
+  const int tl = min(TN, q.T - ch * TN) - 1;  // last real tile of the chunk
+  const int nt = q.t0 + ch * TN + min(j, tl);
+  return __builtin_nontemporal_load(gbl(g.W) + lane + ((long)nt * g.Kt + k) * 64);
+}
+
+// The weight tiles of a wave's first NS steps, numbered t = step * TN + j: tiles t < kPf
+// travel in the carry registers, the others (TN = 6) in registers of the phase itself.
+// gemm_prefetch requests the carried ones.
+template <int TN>
+__device__ __forceinline__ void gemm_prefetch(const GemmJob& g, int kg, Carry& pf) {
+  constexpr int NS = gemm_ns(TN);
+  constexpr int NPF = NS * TN < kPf ? NS * TN : kPf;
+  const int lane = opaque(threadIdx.x) & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(opaque(threadIdx.x) >> 6);
+  const GemmGeom q = gemm_geom<TN>(g, kg, wave);
+#pragma unroll
+  for (int t = NPF; t < kPf; ++t) pf[t] = u32x4{0u, 0u, 0u, 0u};
+  if (q.total > 0) {
+#pragma unroll
+    for (int t = 0; t < NPF; ++t) {
+      pf[t] = gemm_tile<TN>(g, q, lane, t / TN, t % TN);
+      if (t % TN == TN - 1) __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < NPF; ++t) pf[t] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+__device__ __forceinline__ void prefetch_gemm(Args a, int kind, int layer, Carry& pf) {
+  const GemmJob g = make_job(a, kind, layer);
+  if (kind == PH_LM) {
+    gemm_prefetch<8>(g, 1, pf);
+    return;
+  }
+  const int kg = a->kg[kind];
+  switch (a->tn[kind]) {
+    case 2: gemm_prefetch<2>(g, kg, pf); break;
+    case 4: gemm_prefetch<4>(g, kg, pf); break;
+    case 6: gemm_prefetch<6>(g, kg, pf); break;
+    default: gemm_prefetch<8>(g, kg, pf); break;
+  }
+}
+
 // One GEMM phase, y = x W^T for the 16 block rows.  The work-groups form R = blocks / kg
 // output ranges of consecutive n-tiles (sizes differ by at most one tile), kg work-groups
 // per range, work-group k of a range taking the k-th of kg near-equal parts of the K
@@ -707,10 +858,10 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
 // last work-group of the range to arrive adds the kg partials in K order and finishes the
 // range's tiles, so results never depend on timing.  The first NS steps of weights are
 // requested before the grid barrier: they do not depend on the previous phase.
-template <int EPI, int TN>
-__device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const PhaseCtl& pc, bool& failed,
-                           u32x4* smem) {
-  constexpr int NS = TN >= 8 ? 2 : 4;
+template <int EPI, int TN, typename Tail>
+__device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const PhaseCtl& pc,
+                                           bool& failed, u32x4* smem, Carry& pf, bool have_pf, Tail tail) {
+  constexpr int NS = gemm_ns(TN);
   static_assert(TN <= kTNMax && TN <= kWaves, "one tile per wave in the chunk epilogue");
   f32x4* red = reinterpret_cast<f32x4*>(smem);
   float* s_rstd = reinterpret_cast<float*>(reinterpret_cast<char*>(smem) + kLdsRedBytes);
@@ -723,38 +874,15 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
   const int tid = opaque(threadIdx.x), lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int nblk = gridDim.x, b = blockIdx.x;
-  const int R = nblk / kg, kgi = b % kg, rg = b / kg;
-  const int Nt = g.Nt, Kt = g.Kt;
-  const int t0 = (int)((long)rg * Nt / R), t1 = (int)((long)(rg + 1) * Nt / R);
-  const int T = t1 - t0;
-  const int nch = (T + TN - 1) / TN;
-  const int kb = (int)((long)kgi * Kt / kg), ke = (int)((long)(kgi + 1) * Kt / kg);
-  const int k0 = kb + (wave * (ke - kb)) / kWaves, k1 = kb + ((wave + 1) * (ke - kb)) / kWaves;
-  // steps per chunk: the longest slice rounded up to a multiple of NS (the same for every
-  // wave, so that all waves reach each chunk end together)
-  const int slice = (ke - kb + kWaves - 1) / kWaves;
-  const int nbr = max(NS, ((slice + NS - 1) / NS) * NS);
-  const int total = T > 0 ? nch * nbr : 0;
+  const GemmGeom geo = gemm_geom<TN>(g, kg, wave);
+  const int rg = geo.rg, t0 = geo.t0, T = geo.T, nch = geo.nch, k0 = geo.k0, k1 = geo.k1, nbr = geo.nbr,
+            total = geo.total;
   const int M = a->B;
-  const int kw_last = max(k1 - 1, 0);
 
-  const GLOBAL u32x4* Wg = gbl(g.W) + lane;
   const GLOBAL u32x4* Ah = gbl(g.Ahi) + lane;
   const GLOBAL u32x4* Al = gbl(g.Alo) + lane;
   const GLOBAL u32x4* Zt = gbl(a->zero) + lane;
 
-  // step s of the stream: chunk s / nbr, k-tile k0 + s % nbr.  Steps past the stream's end
-  // (the loop's look-ahead) re-read the last real tile with zero A fragments.
-  auto load_w = [&](u32x4 (&w)[TN], int s) {
-    const int ch = min(s / nbr, nch - 1);
-    const int k = min(k0 + (s - ch * nbr), kw_last);
-    const int tl = min(TN, T - ch * TN) - 1;  // last real tile of the chunk
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int nt = t0 + ch * TN + min(j, tl);
-      w[j] = __builtin_nontemporal_load(Wg + ((long)nt * Kt + k) * 64);
-    }
-  };
   auto load_a = [&](u32x4& hv, u32x4& lv, int s) {
     const int ch = s / nbr;
     const int k = k0 + (s - ch * nbr);
@@ -766,14 +894,19 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
   float best_v = -INFINITY;  // ARGMAX: running best of the work-group per row (threads < 16)
   int best_i = 0x7FFFFFFF;
 
-  u32x4 w[NS][TN], ah[NS], al[NS];
+  // Weight storage of the NS steps in flight: tile t = step * TN + j in pf[t] (t < kPf) or
+  // in ext.  The first NS steps' carried tiles come from the previous phase's tail, else they
+  // are requested here; the others are requested here.  Both go out before the grid barrier
+  // (they do not depend on the previous phase).
+  constexpr int NALL = NS * TN, NPF = NALL < kPf ? NALL : kPf, NEXT = NALL - NPF;
+  u32x4 ext[NEXT > 0 ? NEXT : 1];
+  auto wt = [&](int t) -> u32x4& { return t < kPf ? pf[t] : ext[t - kPf]; };
+  if (!have_pf) gemm_prefetch<TN>(g, kg, pf);
   if (total > 0) {
 #pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      load_w(w[i], i);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    for (int t = NPF; t < NALL; ++t) ext[t - NPF] = gemm_tile<TN>(g, geo, lane, t / TN, t % TN);
   }
+  u32x4 ah[NS], al[NS];
   phase_begin(a, c, pc, failed);
   if (total > 0) {
 #pragma unroll
@@ -782,15 +915,15 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-  // sums of squares of the RMSNorm input: thread (row, part) sums tiles part, part+16, ...
-  // (threads 256.. repeat 0..255); loads unconditional with clamped indices, so that no
-  // branch precedes the loop; values past the last tile are dropped when summed.
+  // sums of squares of the RMSNorm input: thread (row, part) = (tid / 32, tid % 32) sums
+  // tiles part, part+32, ...; loads unconditional with clamped indices, so that no branch
+  // precedes the loop; values past the last tile are dropped when summed.
   const int n_st = a->H / 16;
-  float stv[16];
+  float stv[8];
   if (g.stats) {
-    const int row = (tid >> 4) & 15, part = tid & 15;
+    const int row = tid >> 5, part = tid & 31;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) stv[q] = gbl(g.stats)[min(part + 16 * q, n_st - 1) * kStatsPad + row];
+    for (int qq = 0; qq < 8; ++qq) stv[qq] = gbl(g.stats)[min(part + 32 * qq, n_st - 1) * kStatsPad + row];
   }
   __builtin_amdgcn_sched_barrier(0);
 
@@ -805,17 +938,18 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
       red[(wave * TN + j) * 64 + lane] = acc[j];
       acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    if (ch == 0 && g.stats && tid < 256) {  // 1/rms of the rows: (x*g/rms) W^T = (1/rms) (x*g) W^T
-      const int row = tid >> 4;
+    if (ch == 0 && g.stats) {  // 1/rms of the rows: (x*g/rms) W^T = (1/rms) (x*g) W^T
+      const int row = tid >> 5;
       float s = 0.f;
 #pragma unroll
-      for (int q = 0; q < 16; ++q) s += ((tid & 15) + 16 * q < n_st) ? stv[q] : 0.f;
-      for (int t = (tid & 15) + 256; t < n_st; t += 16) s += gbl(g.stats)[t * kStatsPad + row];
+      for (int q = 0; q < 8; ++q) s += ((tid & 31) + 32 * q < n_st) ? stv[q] : 0.f;
+      for (int t = (tid & 31) + 256; t < n_st; t += 32) s += gbl(g.stats)[t * kStatsPad + row];
+      s += __shfl_xor(s, 16);
       s += __shfl_xor(s, 8);
       s += __shfl_xor(s, 4);
       s += __shfl_xor(s, 2);
       s += __shfl_xor(s, 1);
-      if ((tid & 15) == 0) s_rstd[row] = (row < M) ? rsqrtf(s / a->H + a->eps) : 0.f;
+      if ((tid & 31) == 0) s_rstd[row] = (row < M) ? rsqrtf(s / a->H + a->eps) : 0.f;
     }
     __syncthreads();
     const int tn_c = min(TN, T - ch * TN);
@@ -860,11 +994,12 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
     for (int i = 0; i < NS; ++i) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        acc[j] = mfma(ah[i], w[i][j], acc[j]);
-        acc[j] = mfma(al[i], w[i][j], acc[j]);
+        acc[j] = mfma(ah[i], wt(i * TN + j), acc[j]);
+        acc[j] = mfma(al[i], wt(i * TN + j), acc[j]);
       }
       __builtin_amdgcn_sched_barrier(0);
-      load_w(w[i], s0 + NS + i);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) wt(i * TN + j) = gemm_tile<TN>(g, geo, lane, s0 + NS + i, j);
       load_a(ah[i], al[i], s0 + NS + i);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -876,10 +1011,16 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
     for (int i = 0; i < NS; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        acc[j] = mfma(ah[i], w[i][j], acc[j]);
-        acc[j] = mfma(al[i], w[i][j], acc[j]);
+        acc[j] = mfma(ah[i], wt(i * TN + j), acc[j]);
+        acc[j] = mfma(al[i], wt(i * TN + j), acc[j]);
       }
+    trace_mark(c, pc.slot + 1, pc.nslots);
+  }
+  // the next phase's first loads go out now, ahead of this phase's epilogue and stores
+  tail();
+  if (total > 0) {
     chunk_end(nch - 1);
+    trace_mark(c, pc.slot + 2, pc.nslots);
   }
 
   if (kg > 1 && total > 0) {
@@ -955,24 +1096,79 @@ __device__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const Phase
 // matrix cores as hi/lo pairs (about 22 significant bits) against the fp16 keys and values.
 // The KS partial results of a query tile (running max, sum, unnormalised output) are
 // merged through LDS in group order.
+// Shape of an attention work item.
 template <int HD>
-__device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed,
-                           u32x4* smem) {
-  constexpr int CK = kChunk;
-  constexpr int CKM = CK + 32;   // keys held by a work-group (room for the B <= 16 block keys)
-  constexpr int NKB = CKM / 32;  // 32-key blocks of a work item
-  constexpr int KC = HD / 8;     // 16-byte columns of a K row
-  constexpr int VC = CKM / 8;    // 16-byte columns of a V^T row (a multiple of 4)
-  constexpr int KP = CKM * KC, VP = HD * VC;
-  constexpr int PER = (KP + VP) / kThreads;  // pieces per thread
-  constexpr int DT = HD / 16;                // 16-dim tiles of an output row
+struct AttnShape {
+  static constexpr int CK = kChunk;
+  static constexpr int CKM = CK + 32;   // keys held by a work-group (room for the B <= 16 block keys)
+  static constexpr int NKB = CKM / 32;  // 32-key blocks of a work item
+  static constexpr int KC = HD / 8;     // 16-byte columns of a K row
+  static constexpr int VC = CKM / 8;    // 16-byte columns of a V^T row (a multiple of 4)
+  static constexpr int KP = CKM * KC, VP = HD * VC;
+  static constexpr int PER = (KP + VP) / kThreads;  // pieces per thread
   static_assert((KP + VP) % kThreads == 0, "pieces must split evenly over the work-group");
+  static_assert(PER <= kPf, "the first item's pieces travel in the carry registers");
+};
+
+// Request the pieces of attention item j (chunk j / n_kv, KV head j % n_kv) of a layer:
+// pass 0 = context keys only, pass 1 = the rest.  Pieces that a pass does not load keep
+// their value.  The thread index is laundered so that the compiler recomputes the piece
+// coordinates here instead of keeping them in registers for the whole kernel.
+template <int HD>
+__device__ __forceinline__ void attn_issue(Args a, Call dc, int layer, int j, int pass, u32x4* pcs) {
+  using A = AttnShape<HD>;
+  int t = threadIdx.x;
+  asm volatile("" : "+v"(t));
+  const int L = dc->L;
+  const int nch = max(1, (L + A::CK - 1) / A::CK);
+  const int c = j / a->n_kv, g = j % a->n_kv;
+  const int kbeg = c * A::CK;
+  const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + A::CK) - kbeg;
+  const uint16_t* kc = a->kc + layer * a->cache_layer;
+  const uint16_t* vt = a->vt + layer * a->cache_layer;
+#pragma unroll
+  for (int i = 0; i < A::PER; ++i) {
+    const int p = i * kThreads + t;
+    if (p < A::KP) {
+      const int r = p / A::KC, col = p % A::KC;
+      const bool ctx = kbeg + r < L;
+      if (r < nkeys && (pass == 0 ? ctx : !ctx))
+        pcs[i] = *gbl(reinterpret_cast<const u32x4*>(kc + ((long)g * a->Lcap + kbeg + r) * HD + col * 8));
+    } else {
+      const int pv = p - A::KP;
+      const int d = pv / A::VC, col = pv % A::VC;
+      // requested early only if its whole 128-byte line (64 keys) precedes slot L: the line
+      // holding slot L also receives the block's values in the QKV phase
+      const bool ctx = ((kbeg + col * 8) & ~63) + 64 <= L;
+      if (col * 8 < nkeys && (pass == 0 ? ctx : !ctx))
+        pcs[i] = *gbl(reinterpret_cast<const u32x4*>(vt + ((long)g * HD + d) * a->Lcap + kbeg + col * 8));
+    }
+  }
+}
+
+// the context pieces of this work-group's first attention item, into the carry registers
+template <int HD>
+__device__ __forceinline__ void attn_prefetch(Args a, Call dc, int layer, Carry& pf) {
+  const int nch = max(1, (dc->L + kChunk - 1) / kChunk);
+#pragma unroll
+  for (int i = 0; i < kPf; ++i) pf[i] = u32x4{0u, 0u, 0u, 0u};
+  if ((int)blockIdx.x < nch * a->n_kv) attn_issue<HD>(a, dc, layer, blockIdx.x, 0, pf);
+}
+
+template <int HD>
+__device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed,
+                                           u32x4* smem, Carry& pf, bool have_pf) {
+  using A = AttnShape<HD>;
+  constexpr int CK = A::CK, CKM = A::CKM, NKB = A::NKB, KC = A::KC, VC = A::VC, KP = A::KP, VP = A::VP,
+                PER = A::PER;
+  constexpr int DT = HD / 16;                // 16-dim tiles of an output row
   static_assert(KC >= 8, "K swizzle needs 8 columns");
   u32x4* sK = smem;                                        // (row r, column c) at r*KC + (c ^ (r & 7))
   u32x4* sV = smem + KP;                                   // (row d, column c) at d*VC + (c ^ (d & 3))
   f32x4* sO = reinterpret_cast<f32x4*>(smem + KP + VP);    // merge: [kWaves][DT][64]
   float2* sML = reinterpret_cast<float2*>(sO + kWaves * DT * 64);  // [kWaves][16]
   static_assert((KP + VP) * 16 + kWaves * DT * 64 * 16 + kWaves * 16 * 8 <= kLdsBytes, "LDS");
+  (void)CKM;
 
   const int tid = opaque(threadIdx.x), lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -982,42 +1178,12 @@ __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
   const int G = a->n_q / a->n_kv;
   const int R = G * a->B;
   const int QT = (R + 15) / 16, KS = kWaves / QT;
-  const uint16_t* kc = a->kc + layer * a->cache_layer;
-  const uint16_t* vt = a->vt + layer * a->cache_layer;
   const float* Q = a->Q + layer * a->q_stride;
   const int q_dim = a->n_q * HD;
-
-  // request the pieces of item j: pass 0 = context keys only, pass 1 = the rest.  The thread
-  // index is laundered through an empty asm statement so that the compiler recomputes the
-  // piece coordinates here instead of keeping them in registers for the whole kernel.
-  auto issue = [&](int j, int pass, u32x4 (&pcs)[PER]) {
-    int t = threadIdx.x;
-    asm volatile("" : "+v"(t));
-    const int c = j / a->n_kv, g = j % a->n_kv;
-    const int kbeg = c * CK;
-    const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + CK) - kbeg;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int p = i * kThreads + t;
-      if (p < KP) {
-        const int r = p / KC, col = p % KC;
-        const bool ctx = kbeg + r < L;
-        if (r < nkeys && (pass == 0 ? ctx : !ctx))
-          pcs[i] = *gbl(reinterpret_cast<const u32x4*>(kc + ((long)g * a->Lcap + kbeg + r) * HD + col * 8));
-      } else {
-        const int pv = p - KP;
-        const int d = pv / VC, col = pv % VC;
-        // requested early only if its whole 128-byte line (64 keys) precedes slot L: the line
-        // holding slot L also receives the block's values in the QKV phase
-        const bool ctx = ((kbeg + col * 8) & ~63) + 64 <= L;
-        if (col * 8 < nkeys && (pass == 0 ? ctx : !ctx))
-          pcs[i] = *gbl(reinterpret_cast<const u32x4*>(vt + ((long)g * HD + d) * a->Lcap + kbeg + col * 8));
-      }
-    }
-  };
+  auto issue = [&](int j, int pass, u32x4* pcs) { attn_issue<HD>(a, dc, layer, j, pass, pcs); };
 
   // everything of item j after its context pieces were requested
-  auto finish = [&](int j, u32x4 (&pcs)[PER]) {
+  auto finish = [&](int j, u32x4* pcs) {
     issue(j, 1, pcs);
     const int c = j / a->n_kv, g = j % a->n_kv;
     const int nkeys = ((c == nch - 1) ? L + a->B : c * CK + CK) - c * CK;
@@ -1073,6 +1239,7 @@ __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
       }
     }
     __syncthreads();
+    if (j == (int)blockIdx.x) trace_mark(dc, pc.slot + 1, pc.nslots);
     float m = -INFINITY, l = 0.f;
     f32x4 o[DT];
 #pragma unroll
@@ -1158,6 +1325,7 @@ __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    if (j == (int)blockIdx.x && w == 0) trace_mark(dc, pc.slot + 2, pc.nslots);
     // merge the KS key runs of each query tile (group order), then store the item's partial
     if (KS > 1) {
       if (active) {
@@ -1194,17 +1362,13 @@ __device__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
     __syncthreads();  // LDS is refilled by the next item
   };
 
-  // The first item's context pieces are requested before the barrier.  Each item keeps its
-  // pieces in a register array of its own scope, so none stays live across items.
+  // The first item's context pieces come in the carry registers (requested by the QKV
+  // phase's tail) or are requested here, before the barrier.  Later items keep their pieces
+  // in a register array of their own scope, so none stays live across items.
   const int j0 = blockIdx.x;
-  {
-    u32x4 pcs[PER];
-#pragma unroll
-    for (int i = 0; i < PER; ++i) pcs[i] = u32x4{0u, 0u, 0u, 0u};
-    if (j0 < items) issue(j0, 0, pcs);
-    phase_begin(a, dc, pc, failed);
-    if (j0 < items) finish(j0, pcs);
-  }
+  if (!have_pf) attn_prefetch<HD>(a, dc, layer, pf);
+  phase_begin(a, dc, pc, failed);
+  if (j0 < items) finish(j0, pf);
   for (int j = j0 + gridDim.x; j < items; j += gridDim.x) {
     u32x4 pcs[PER];
 #pragma unroll
@@ -1241,12 +1405,12 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
 #pragma unroll
     for (int e = 0; e < DPL; ++e) num[e] = 0.f;
     const float* op = a->OP + ((long)g * a->Rpad + r) * HD + lane * DPL;
-    // 32 chunks per batch, all their loads in flight together (one memory round trip)
-    for (int c0 = 0; c0 < nch; c0 += 32) {
-      float2 mc[32];
-      float ov[32][DPL];
+    // 16 chunks per batch, all their loads in flight together (one memory round trip)
+    for (int c0 = 0; c0 < nch; c0 += 16) {
+      float2 mc[16];
+      float ov[16][DPL];
 #pragma unroll
-      for (int u = 0; u < 32; ++u) {
+      for (int u = 0; u < 16; ++u) {
         const int c = min(c0 + u, nch - 1);
         mc[u] = ld_coh2(ml + c * cstride);
         if constexpr (DPL == 2) {
@@ -1258,7 +1422,7 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
         }
       }
 #pragma unroll
-      for (int u = 0; u < 32; ++u) {
+      for (int u = 0; u < 16; ++u) {
         if (c0 + u < nch) {
           const float wgt = exp2f(mc[u].x - M);
           den += wgt * mc[u].y;
@@ -1280,21 +1444,22 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
 }
 
 // GEMM phase with the plan's chunk width (the LM head always uses 8)
-template <int EPI>
-__device__ __forceinline__ void gemm_dispatch(Args a, Call c, GemmJob& g, int kind, int layer, const PhaseCtl& pc,
-                                              bool& failed, u32x4* smem) {
-  const int kg = a->kg[kind];
+template <int EPI, typename Tail>
+__device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int layer, const PhaseCtl& pc, bool& failed,
+                                              u32x4* smem, Carry& pf, bool have_pf, Tail tail) {
+  GemmJob g = make_job(a, kind, layer);
+  const int kg = kind == PH_LM ? 1 : a->kg[kind];
   const int slot = kind == PH_QKV ? 0 : kind == PH_O ? 1 : kind == PH_GU ? 2 : 3;
   g.cnt = a->kcnt + (long)slot * kMaxBlocks * 32;
   g.target = (c->done_epoch * (unsigned)a->D + (unsigned)layer + 1u) * (unsigned)kg;
   if constexpr (EPI == EPI_ARGMAX) {
-    gemm_phase<EPI, 8>(a, c, g, 1, pc, failed, smem);
+    gemm_phase<EPI, 8>(a, c, g, 1, pc, failed, smem, pf, have_pf, tail);
   } else {
     switch (a->tn[kind]) {
-      case 2: gemm_phase<EPI, 2>(a, c, g, kg, pc, failed, smem); break;
-      case 4: gemm_phase<EPI, 4>(a, c, g, kg, pc, failed, smem); break;
-      case 6: gemm_phase<EPI, 6>(a, c, g, kg, pc, failed, smem); break;
-      default: gemm_phase<EPI, 8>(a, c, g, kg, pc, failed, smem); break;
+      case 2: gemm_phase<EPI, 2>(a, c, g, kg, pc, failed, smem, pf, have_pf, tail); break;
+      case 4: gemm_phase<EPI, 4>(a, c, g, kg, pc, failed, smem, pf, have_pf, tail); break;
+      case 6: gemm_phase<EPI, 6>(a, c, g, kg, pc, failed, smem, pf, have_pf, tail); break;
+      default: gemm_phase<EPI, 8>(a, c, g, kg, pc, failed, smem, pf, have_pf, tail); break;
     }
   }
 }
@@ -1310,90 +1475,55 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
   const Call c = &ka->c;
   const int p0 = ka->p0, p1 = ka->p1;
   const int nphase = phase_count(a->D);
-  const int nslots = 2 * nphase;  // trace: body start, then arrival (stores done), per phase
-  const int H = a->H, Kt_H = H / 32, q_Kt = a->n_q * a->hd / 32, F_Kt = a->F / 32;
+  const int nslots = kTraceSlots * nphase;
   bool failed = false;
+  Carry pf;
   for (int p = p0; p < p1; ++p) {
     int kind, layer;
     phase_of(p, a->D, kind, layer);
     PhaseCtl pc;
     pc.wait = p > p0;
     pc.epoch = c->bar_epoch + (unsigned)(p - p0);
-    pc.slot = 2 * p;
+    pc.slot = kTraceSlots * p;
     pc.nslots = nslots;
-    GemmJob g{};
+    // The QKV phase's tail requests the context pieces of the first attention item (into the
+    // carry registers), ahead of its epilogue, its stores and the grid barrier; the attention
+    // phase uses them when that tail ran in this launch.  Other phases request their first
+    // loads themselves: a tail load ahead of an epilogue that reads memory (the residual
+    // stream, split-K partials, counters) would hold that epilogue up, since a wave's loads
+    // complete in order.
+    const bool prev = p > p0;
     switch (kind) {
       case PH_EMBED:
         phase_begin(a, c, pc, failed);
         phase_embed(a, c);
         break;
-      case PH_QKV: {
-        const int s = 2 * layer;
-        g.W = a->w_qkv + layer * a->s_qkv;
-        g.Nt = (a->n_q + 2 * a->n_kv) * a->hd / 16;
-        g.Kt = Kt_H;
-        g.Ahi = a->XA + s * a->xa_stride;
-        g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
-        g.stats = a->XS + s * a->xs_stride;
-        g.q_out = a->Q + layer * a->q_stride;
-        g.kc = a->kc + layer * a->cache_layer;
-        g.vt = a->vt + layer * a->cache_layer;
-        gemm_dispatch<EPI_QKV>(a, c, g, kind, layer, pc, failed, smem);
+      case PH_QKV:
+        gemm_dispatch<EPI_QKV>(a, c, kind, layer, pc, failed, smem, pf, false,
+                               [&]() { attn_prefetch<HD>(a, c, layer, pf); });
         break;
-      }
       case PH_ATTN:
-        phase_attn<HD>(a, c, layer, pc, failed, smem);
+        phase_attn<HD>(a, c, layer, pc, failed, smem, pf, prev);
         break;
       case PH_COMB:
         phase_comb<HD>(a, c, layer, pc, failed);
         break;
       case PH_O:
-      case PH_DOWN: {
-        const bool o = kind == PH_O;
-        const int s = o ? 2 * layer + 1 : 2 * layer + 2;
-        g.W = o ? a->w_o + layer * a->s_o : a->w_down + layer * a->s_down;
-        g.Nt = H / 16;
-        g.Kt = o ? q_Kt : F_Kt;
-        g.Ahi = o ? a->OA + layer * a->oa_stride : a->HA + layer * a->ha_stride;
-        g.Alo = g.Ahi + (long)(g.Kt + kKtPad) * 64;
-        g.stats = nullptr;
-        g.xs_out = a->XS + s * a->xs_stride;
-        g.na_hi = reinterpret_cast<uint32_t*>(a->XA + s * a->xa_stride);
-        g.na_lo = reinterpret_cast<uint32_t*>(a->XA + s * a->xa_stride + (long)(Kt_H + kKtPad) * 64);
-        g.na_Kt = Kt_H;
-        g.gain = o ? a->g_mlp + (long)layer * H : (layer + 1 < a->D ? a->g_attn + (long)(layer + 1) * H : a->g_final);
-        gemm_dispatch<EPI_RESID>(a, c, g, kind, layer, pc, failed, smem);
+        gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem, pf, false, []() {});
         break;
-      }
-      case PH_GU: {
-        const int s = 2 * layer + 1;
-        g.W = a->w_gu + layer * a->s_gu;
-        g.Nt = 2 * a->F / 16;
-        g.Kt = Kt_H;
-        g.Ahi = a->XA + s * a->xa_stride;
-        g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
-        g.stats = a->XS + s * a->xs_stride;
-        g.na_hi = reinterpret_cast<uint32_t*>(a->HA + layer * a->ha_stride);
-        g.na_lo = reinterpret_cast<uint32_t*>(a->HA + layer * a->ha_stride + (long)(F_Kt + kKtPad) * 64);
-        g.na_Kt = F_Kt;
-        gemm_dispatch<EPI_SWIGLU>(a, c, g, kind, layer, pc, failed, smem);
+      case PH_GU:
+        gemm_dispatch<EPI_SWIGLU>(a, c, kind, layer, pc, failed, smem, pf, false, []() {});
         break;
-      }
-      case PH_LM: {
-        const int s = 2 * a->D;
-        g.W = a->w_lm;
-        g.Nt = (a->V + 15) / 16;
-        g.Kt = Kt_H;
-        g.Ahi = a->XA + s * a->xa_stride;
-        g.Alo = g.Ahi + (long)(Kt_H + kKtPad) * 64;
-        g.stats = a->XS + s * a->xs_stride;
-        gemm_dispatch<EPI_ARGMAX>(a, c, g, kind, layer, pc, failed, smem);
+      case PH_DOWN:
+        gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem, pf, false, []() {});
         break;
-      }
+      default:  // PH_LM
+        gemm_dispatch<EPI_ARGMAX>(a, c, kind, layer, pc, failed, smem, pf, false, []() {});
+        break;
     }
     if (p + 1 < p1) grid_arrive(a);
     else wait_vm();
-    trace_mark(c, 2 * p + 1, nslots);
+    trace_mark(c, kTraceSlots * p + kTraceSlots - 1, nslots);
   }
 }
 

@@ -551,7 +551,8 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
     HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
     h->bar_epoch = h->done_epoch = 0;
   }
-  if (h->trace && !h->trace_buf) TRY(dev_zalloc(h, &h->trace_buf, (size_t)h->blocks * 2 * P * 8));
+  if (h->trace && !h->trace_buf) TRY(dev_zalloc(h, &h->trace_buf, (size_t)h->blocks * kTraceSlots * P * 8));
+  if (h->trace) HIP_OR_FAIL(h, hipMemsetAsync(h->trace_buf, 0, (size_t)h->blocks * kTraceSlots * P * 8, s));
   const DraftCall dc = draft_call(h, ids, positions_host, out);
   const int hd = c.head_dim;
   const bool split = !h->persistent || h->debug || (h->prof_kind >= DFLARE_K_QKV && h->prof_kind <= DFLARE_K_LM_HEAD);
@@ -814,13 +815,15 @@ int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, in
       return DFLARE_OK;
     }
     case DFLARE_DBG_TRACE: {
-      const int64_t n = (int64_t)h->blocks * 2 * h->phases;
+      const int64_t n = (int64_t)h->blocks * kTraceSlots * h->phases;
       if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
       std::vector<unsigned long long> raw((size_t)n);
       HIP_OR_FAIL(h, hipMemcpy(raw.data(), h->trace_buf, n * 8, hipMemcpyDeviceToHost));
       unsigned long long t0 = ~0ull;
-      for (int b = 0; b < h->blocks; ++b) t0 = std::min(t0, raw[(size_t)b * 2 * h->phases]);
-      for (int64_t i = 0; i < n; ++i) host_out[i] = (float)((double)(raw[i] - t0) * 0.01);  // 100 MHz ticks -> us
+      for (int64_t i = 0; i < n; ++i)
+        if (raw[i]) t0 = std::min(t0, raw[i]);
+      for (int64_t i = 0; i < n; ++i)  // 100 MHz ticks -> us; marks a phase does not set: -1
+        host_out[i] = raw[i] ? (float)((double)(raw[i] - t0) * 0.01) : -1.0f;
       return DFLARE_OK;
     }
     default: return fail(h, DFLARE_ERR_INVALID_ARG, "unknown debug tensor");
