@@ -87,6 +87,9 @@ struct DraftArgs {
   // consecutive n-tiles, kg work-groups per range each taking 1/kg of K; a work-group
   // accumulates up to tn (2, 4, 6 or 8) n-tiles at once.
   int tn[PH_COUNT], kg[PH_COUNT];
+  // the partition, precomputed: output range r holds nq + (r < nr) n-tiles starting at
+  // r * nq + min(r, nr); K part k holds kq + (k < kr) k-tiles starting at k * kq + min(k, kr)
+  int nq[PH_COUNT], nr[PH_COUNT], kq[PH_COUNT], kr[PH_COUNT];
   // weights: packed tiles; strides between layers in u32x4 units
   const uint16_t* embed;
   const u32x4 *w_qkv, *w_o, *w_gu, *w_down, *w_lm;

@@ -35,6 +35,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 #define GLOBAL __attribute__((address_space(1)))
 #define CONSTANT __attribute__((address_space(4)))
+#define LDSP __attribute__((address_space(3)))
 
 constexpr int kLdsBytes = 160 * 1024;
 constexpr int kChunk = 128;  // context keys per attention work item
@@ -563,6 +564,11 @@ struct GemmJob {
 // LDS of a GEMM phase: partial tiles [kWaves][TN][64 lanes] (64 KiB at most), then the
 // row scales, the argmax scratch and a flag.
 constexpr int kLdsRedBytes = kWaves * kTNMax * 1024;
+// LDS of the attention phase: the merge area at 0 (shared with the GEMM reduction area), the
+// K / V^T staging area from kStageOff to the end.  GEMM phases never touch the staging
+// area, so the next layer's context pieces can be streamed into it during them.
+constexpr int kStageOff = 80 * 1024;
+static_assert(kLdsRedBytes + 2048 <= kStageOff, "GEMM scratch stays below the attention staging area");
 
 // 16-byte coherent load (two 8-byte agent-scope loads)
 __device__ __forceinline__ f32x4 ld_coh16(const f32x4* p) {
@@ -692,15 +698,6 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
   }
 }
 
-// Registers carried from one phase into the next: the QKV phase issues the context pieces
-// of the first attention item as soon as its own weight streaming is done, so that they are
-// in flight during its epilogue, its stores and the grid barrier.  GEMM phases use the same
-// registers for their first weight tiles.  Every prefetch writes all kPf entries (zeros
-// where it loads nothing), so that the registers are free inside the phases that do not
-// carry anything.
-constexpr int kPf = 16;
-typedef u32x4 Carry[kPf];
-
 __host__ __device__ constexpr int gemm_ns(int TN) { return TN >= 8 ? 2 : 4; }  // steps in flight
 
 // The GEMM job of phase (kind, layer): weights, input fragments and epilogue targets.
@@ -772,75 +769,28 @@ struct GemmGeom {
   int rg, kgi, t0, T, nch, k0, k1, nbr, total, kw_last;
 };
 template <int TN>
-__device__ __forceinline__ GemmGeom gemm_geom(const GemmJob& g, int kg, int wave) {
+__device__ __forceinline__ GemmGeom gemm_geom(Args a, int kind, int kg, int wave) {
   constexpr int NS = gemm_ns(TN);
   GemmGeom q;
-  const int R = gridDim.x / kg;
   q.kgi = blockIdx.x % kg;
   q.rg = blockIdx.x / kg;
-  q.t0 = (int)((long)q.rg * g.Nt / R);
-  q.T = (int)((long)(q.rg + 1) * g.Nt / R) - q.t0;
+  const int nq = a->nq[kind], nr = a->nr[kind], kq = a->kq[kind], kr = a->kr[kind];
+  q.t0 = q.rg * nq + min(q.rg, nr);
+  q.T = nq + (q.rg < nr ? 1 : 0);
   q.nch = (q.T + TN - 1) / TN;
-  const int kb = (int)((long)q.kgi * g.Kt / kg), ke = (int)((long)(q.kgi + 1) * g.Kt / kg);
-  q.k0 = kb + (wave * (ke - kb)) / kWaves;
-  q.k1 = kb + ((wave + 1) * (ke - kb)) / kWaves;
+  const int kb = q.kgi * kq + min(q.kgi, kr);
+  const int TK = kq + (q.kgi < kr ? 1 : 0);
+  // wave w takes TK / 8 k-tiles, the first TK % 8 waves one more
+  const int kw = TK / kWaves, kx = TK % kWaves;
+  q.k0 = kb + wave * kw + min(wave, kx);
+  q.k1 = q.k0 + kw + (wave < kx ? 1 : 0);
   // steps per chunk: the longest slice rounded up to a multiple of NS (the same for every
   // wave, so that all waves reach each chunk end together)
-  const int slice = (ke - kb + kWaves - 1) / kWaves;
+  const int slice = kw + (kx > 0 ? 1 : 0);
   q.nbr = max(NS, ((slice + NS - 1) / NS) * NS);
   q.total = q.T > 0 ? q.nch * q.nbr : 0;
   q.kw_last = max(q.k1 - 1, 0);
   return q;
-}
-
-// weight tile j of step s of a wave's stream (chunk s / nbr, k-tile k0 + s % nbr); steps
-// past the stream's end re-read the last real tile (their A fragments are zero)
-template <int TN>
-__device__ __forceinline__ u32x4 gemm_tile(const GemmJob& g, const GemmGeom& q, int lane, int s, int j) {
-  const int ch = min(s / q.nbr, q.nch - 1);
-  const int k = min(q.k0 + (s - ch * q.nbr), q.kw_last);
-  const int tl = min(TN, q.T - ch * TN) - 1;  // last real tile of the chunk
-  const int nt = q.t0 + ch * TN + min(j, tl);
-  return __builtin_nontemporal_load(gbl(g.W) + lane + ((long)nt * g.Kt + k) * 64);
-}
-
-// The weight tiles of a wave's first NS steps, numbered t = step * TN + j: tiles t < kPf
-// travel in the carry registers, the others (TN = 6) in registers of the phase itself.
-// gemm_prefetch requests the carried ones.
-template <int TN>
-__device__ __forceinline__ void gemm_prefetch(const GemmJob& g, int kg, Carry& pf) {
-  constexpr int NS = gemm_ns(TN);
-  constexpr int NPF = NS * TN < kPf ? NS * TN : kPf;
-  const int lane = opaque(threadIdx.x) & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(opaque(threadIdx.x) >> 6);
-  const GemmGeom q = gemm_geom<TN>(g, kg, wave);
-#pragma unroll
-  for (int t = NPF; t < kPf; ++t) pf[t] = u32x4{0u, 0u, 0u, 0u};
-  if (q.total > 0) {
-#pragma unroll
-    for (int t = 0; t < NPF; ++t) {
-      pf[t] = gemm_tile<TN>(g, q, lane, t / TN, t % TN);
-      if (t % TN == TN - 1) __builtin_amdgcn_sched_barrier(0);
-    }
-  } else {
-#pragma unroll
-    for (int t = 0; t < NPF; ++t) pf[t] = u32x4{0u, 0u, 0u, 0u};
-  }
-}
-
-__device__ __forceinline__ void prefetch_gemm(Args a, int kind, int layer, Carry& pf) {
-  const GemmJob g = make_job(a, kind, layer);
-  if (kind == PH_LM) {
-    gemm_prefetch<8>(g, 1, pf);
-    return;
-  }
-  const int kg = a->kg[kind];
-  switch (a->tn[kind]) {
-    case 2: gemm_prefetch<2>(g, kg, pf); break;
-    case 4: gemm_prefetch<4>(g, kg, pf); break;
-    case 6: gemm_prefetch<6>(g, kg, pf); break;
-    default: gemm_prefetch<8>(g, kg, pf); break;
-  }
 }
 
 // One GEMM phase, y = x W^T for the 16 block rows.  The work-groups form R = blocks / kg
@@ -858,9 +808,9 @@ __device__ __forceinline__ void prefetch_gemm(Args a, int kind, int layer, Carry
 // last work-group of the range to arrive adds the kg partials in K order and finishes the
 // range's tiles, so results never depend on timing.  The first NS steps of weights are
 // requested before the grid barrier: they do not depend on the previous phase.
-template <int EPI, int TN, typename Tail>
-__device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int kg, const PhaseCtl& pc,
-                                           bool& failed, u32x4* smem, Carry& pf, bool have_pf, Tail tail) {
+template <int EPI, int TN>
+__device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int kind, int kg, const PhaseCtl& pc,
+                                           bool& failed, u32x4* smem) {
   constexpr int NS = gemm_ns(TN);
   static_assert(TN <= kTNMax && TN <= kWaves, "one tile per wave in the chunk epilogue");
   f32x4* red = reinterpret_cast<f32x4*>(smem);
@@ -874,19 +824,32 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
   const int tid = opaque(threadIdx.x), lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int nblk = gridDim.x, b = blockIdx.x;
-  const GemmGeom geo = gemm_geom<TN>(g, kg, wave);
+  const GemmGeom geo = gemm_geom<TN>(a, kind, kg, wave);
   const int rg = geo.rg, t0 = geo.t0, T = geo.T, nch = geo.nch, k0 = geo.k0, k1 = geo.k1, nbr = geo.nbr,
             total = geo.total;
   const int M = a->B;
 
+  const GLOBAL u32x4* Wg = gbl(g.W) + lane;
   const GLOBAL u32x4* Ah = gbl(g.Ahi) + lane;
   const GLOBAL u32x4* Al = gbl(g.Alo) + lane;
   const GLOBAL u32x4* Zt = gbl(a->zero) + lane;
 
-  auto load_a = [&](u32x4& hv, u32x4& lv, int s) {
-    const int ch = s / nbr;
-    const int k = k0 + (s - ch * nbr);
-    const bool real = k < k1 && s < total;
+  // Load cursor: the NS steps of a block share their chunk (nbr is a multiple of NS), so the
+  // tile offsets wb[j] of a chunk are recomputed only when a block starts a new chunk.
+  long wb[TN];
+  auto chunk_bases = [&](int ch) {
+    const int tl = min(TN, T - ch * TN) - 1;  // last real tile of the chunk
+#pragma unroll
+    for (int j = 0; j < TN; ++j) wb[j] = (long)(t0 + ch * TN + min(j, tl)) * g.Kt * 64;
+  };
+  // the weight tiles and A fragments of step kb + i of the current chunk; padding steps past
+  // the wave's slice re-read its last tile with zero A fragments
+  auto load_step = [&](u32x4* w, u32x4& hv, u32x4& lv, int kb, int i) {
+    const int k = k0 + kb + i;
+    const long ko = (long)min(k, geo.kw_last) * 64;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) w[j] = __builtin_nontemporal_load(Wg + wb[j] + ko);
+    const bool real = k < k1;
     hv = *(real ? Ah + (long)k * 64 : Zt);
     lv = *(real ? Al + (long)k * 64 : Zt);
   };
@@ -894,24 +857,26 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
   float best_v = -INFINITY;  // ARGMAX: running best of the work-group per row (threads < 16)
   int best_i = 0x7FFFFFFF;
 
-  // Weight storage of the NS steps in flight: tile t = step * TN + j in pf[t] (t < kPf) or
-  // in ext.  The first NS steps' carried tiles come from the previous phase's tail, else they
-  // are requested here; the others are requested here.  Both go out before the grid barrier
-  // (they do not depend on the previous phase).
-  constexpr int NALL = NS * TN, NPF = NALL < kPf ? NALL : kPf, NEXT = NALL - NPF;
-  u32x4 ext[NEXT > 0 ? NEXT : 1];
-  auto wt = [&](int t) -> u32x4& { return t < kPf ? pf[t] : ext[t - kPf]; };
-  if (!have_pf) gemm_prefetch<TN>(g, kg, pf);
+  // The first NS steps' weights go out before the grid barrier (they do not depend on the
+  // previous phase), their A fragments after it.
+  u32x4 w[NS][TN], ah[NS], al[NS];
   if (total > 0) {
+    chunk_bases(0);
 #pragma unroll
-    for (int t = NPF; t < NALL; ++t) ext[t - NPF] = gemm_tile<TN>(g, geo, lane, t / TN, t % TN);
+    for (int i = 0; i < NS; ++i) {
+      const long ko = (long)min(k0 + i, geo.kw_last) * 64;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) w[i][j] = __builtin_nontemporal_load(Wg + wb[j] + ko);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
-  u32x4 ah[NS], al[NS];
   phase_begin(a, c, pc, failed);
   if (total > 0) {
 #pragma unroll
     for (int i = 0; i < NS; ++i) {
-      load_a(ah[i], al[i], i);
+      const int k = k0 + i;
+      ah[i] = *(k < k1 ? Ah + (long)k * 64 : Zt);
+      al[i] = *(k < k1 ? Al + (long)k * 64 : Zt);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -989,36 +954,41 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
   // compiler sinks a reload past the other sets' MFMAs, and the wait for the next set then
   // drains every load in flight.  The last NS steps (total is a multiple of NS) request
   // nothing more.
+  int lch = 0, lkb = 0;  // chunk and first step of the block being requested
+  int cch = 0, ckb = 0;  // chunk and first step of the block being consumed
   for (int s0 = 0; s0 + NS < total; s0 += NS) {
+    lkb += NS;
+    if (lkb == nbr) {
+      lkb = 0;
+      ++lch;
+      chunk_bases(lch);
+    }
 #pragma unroll
     for (int i = 0; i < NS; ++i) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        acc[j] = mfma(ah[i], wt(i * TN + j), acc[j]);
-        acc[j] = mfma(al[i], wt(i * TN + j), acc[j]);
+        acc[j] = mfma(ah[i], w[i][j], acc[j]);
+        acc[j] = mfma(al[i], w[i][j], acc[j]);
       }
       __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) wt(i * TN + j) = gemm_tile<TN>(g, geo, lane, s0 + NS + i, j);
-      load_a(ah[i], al[i], s0 + NS + i);
+      load_step(w[i], ah[i], al[i], lkb, i);
       __builtin_amdgcn_sched_barrier(0);
     }
-    const int done = s0 + NS;
-    if (done % nbr == 0) chunk_end(done / nbr - 1);
+    ckb += NS;
+    if (ckb == nbr) {
+      ckb = 0;
+      chunk_end(cch++);
+    }
   }
   if (total > 0) {
 #pragma unroll
     for (int i = 0; i < NS; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        acc[j] = mfma(ah[i], wt(i * TN + j), acc[j]);
-        acc[j] = mfma(al[i], wt(i * TN + j), acc[j]);
+        acc[j] = mfma(ah[i], w[i][j], acc[j]);
+        acc[j] = mfma(al[i], w[i][j], acc[j]);
       }
     trace_mark(c, pc.slot + 1, pc.nslots);
-  }
-  // the next phase's first loads go out now, ahead of this phase's epilogue and stores
-  tail();
-  if (total > 0) {
     chunk_end(nch - 1);
     trace_mark(c, pc.slot + 2, pc.nslots);
   }
@@ -1107,7 +1077,6 @@ struct AttnShape {
   static constexpr int KP = CKM * KC, VP = HD * VC;
   static constexpr int PER = (KP + VP) / kThreads;  // pieces per thread
   static_assert((KP + VP) % kThreads == 0, "pieces must split evenly over the work-group");
-  static_assert(PER <= kPf, "the first item's pieces travel in the carry registers");
 };
 
 // Request the pieces of attention item j (chunk j / n_kv, KV head j % n_kv) of a layer:
@@ -1146,28 +1115,63 @@ __device__ __forceinline__ void attn_issue(Args a, Call dc, int layer, int j, in
   }
 }
 
-// the context pieces of this work-group's first attention item, into the carry registers
+// Stream the context pieces of attention item j of `layer` into the LDS staging area with
+// LDS-direct loads, by waves w0 .. 7: one instruction fills 64 consecutive staging slots
+// (1 KiB), lane l fetching the piece that belongs in slot l, so the swizzled layout comes
+// for free.  Slots whose piece is not a context piece (block keys, lines shared with them,
+// keys past the end) are filled with some cache piece; the attention phase overwrites
+// them.  Issued in a phase that does not touch the staging area, by waves that wait for no
+// memory until the phase ends (their arrival at the grid barrier completes the loads).
 template <int HD>
-__device__ __forceinline__ void attn_prefetch(Args a, Call dc, int layer, Carry& pf) {
-  const int nch = max(1, (dc->L + kChunk - 1) / kChunk);
-#pragma unroll
-  for (int i = 0; i < kPf; ++i) pf[i] = u32x4{0u, 0u, 0u, 0u};
-  if ((int)blockIdx.x < nch * a->n_kv) attn_issue<HD>(a, dc, layer, blockIdx.x, 0, pf);
+__device__ __forceinline__ void attn_dma(Args a, Call dc, int layer, int j, u32x4* smem, int w0) {
+  using A = AttnShape<HD>;
+  static_assert(A::KP % 64 == 0 && A::VP % 64 == 0, "whole 64-slot blocks");
+  constexpr int NB = (A::KP + A::VP) / 64;
+  const int L = dc->L;
+  const int nch = max(1, (L + A::CK - 1) / A::CK);
+  const int wave = __builtin_amdgcn_readfirstlane(opaque(threadIdx.x) >> 6);
+  if (j >= nch * a->n_kv || wave < w0) return;
+  const int c = j / a->n_kv, g = j % a->n_kv;
+  const int kbeg = c * A::CK;
+  const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + A::CK) - kbeg;
+  const uint16_t* kc = a->kc + layer * a->cache_layer;
+  const uint16_t* vt = a->vt + layer * a->cache_layer;
+  const int lane = opaque(threadIdx.x) & 63;
+  LDSP char* stage = (LDSP char*)(char*)smem + kStageOff;
+  for (int bl = wave - w0; bl < NB; bl += kWaves - w0) {
+    const int p = bl * 64 + lane;  // staging slot
+    const uint16_t* src;
+    bool ok;
+    if (bl * 64 < A::KP) {
+      const int r = p / A::KC, col = (p % A::KC) ^ (r & 7);
+      ok = r < nkeys && kbeg + r < L;
+      src = kc + ((long)g * a->Lcap + kbeg + r) * HD + col * 8;
+    } else {
+      const int pv = p - A::KP;
+      const int d = pv / A::VC, col = (pv % A::VC) ^ (d & 3);
+      ok = col * 8 < nkeys && ((kbeg + col * 8) & ~63) + 64 <= L;
+      src = vt + ((long)g * HD + d) * a->Lcap + kbeg + col * 8;
+    }
+    // every lane loads; slots that are not context pieces get the cache's first piece, and
+    // the attention phase overwrites them
+    __builtin_amdgcn_global_load_lds(ok ? src : kc, stage + bl * 1024, 16, 0, 0);
+  }
 }
 
 template <int HD>
 __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed,
-                                           u32x4* smem, Carry& pf, bool have_pf) {
+                                           u32x4* smem, bool have_dma) {
   using A = AttnShape<HD>;
   constexpr int CK = A::CK, CKM = A::CKM, NKB = A::NKB, KC = A::KC, VC = A::VC, KP = A::KP, VP = A::VP,
                 PER = A::PER;
   constexpr int DT = HD / 16;                // 16-dim tiles of an output row
   static_assert(KC >= 8, "K swizzle needs 8 columns");
-  u32x4* sK = smem;                                        // (row r, column c) at r*KC + (c ^ (r & 7))
-  u32x4* sV = smem + KP;                                   // (row d, column c) at d*VC + (c ^ (d & 3))
-  f32x4* sO = reinterpret_cast<f32x4*>(smem + KP + VP);    // merge: [kWaves][DT][64]
+  u32x4* sK = smem + kStageOff / 16;                       // (row r, column c) at r*KC + (c ^ (r & 7))
+  u32x4* sV = sK + KP;                                     // (row d, column c) at d*VC + (c ^ (d & 3))
+  f32x4* sO = reinterpret_cast<f32x4*>(smem);              // merge: [kWaves][DT][64]
   float2* sML = reinterpret_cast<float2*>(sO + kWaves * DT * 64);  // [kWaves][16]
-  static_assert((KP + VP) * 16 + kWaves * DT * 64 * 16 + kWaves * 16 * 8 <= kLdsBytes, "LDS");
+  static_assert(kStageOff + (KP + VP) * 16 <= kLdsBytes, "LDS staging");
+  static_assert(kWaves * DT * 64 * 16 + kWaves * 16 * 8 <= kStageOff, "LDS merge area");
   (void)CKM;
 
   const int tid = opaque(threadIdx.x), lane = tid & 63;
@@ -1183,7 +1187,7 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
   auto issue = [&](int j, int pass, u32x4* pcs) { attn_issue<HD>(a, dc, layer, j, pass, pcs); };
 
   // everything of item j after its context pieces were requested
-  auto finish = [&](int j, u32x4* pcs) {
+  auto finish = [&](int j, u32x4* pcs, bool dma) {
     issue(j, 1, pcs);
     const int c = j / a->n_kv, g = j % a->n_kv;
     const int nkeys = ((c == nch - 1) ? L + a->B : c * CK + CK) - c * CK;
@@ -1217,15 +1221,17 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
     // pieces to LDS (values of keys past the end become zeros)
     int tid2 = threadIdx.x;
     asm volatile("" : "+v"(tid2));
+    const int kbeg = c * CK;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int p = i * kThreads + tid2;
       if (p < KP) {
         const int rr = p / KC, col = p % KC;
-        sK[rr * KC + (col ^ (rr & 7))] = pcs[i];
+        if (!(dma && rr < nkeys && kbeg + rr < L)) sK[rr * KC + (col ^ (rr & 7))] = pcs[i];
       } else {
         const int pv = p - KP;
         const int d = pv / VC, col = pv % VC;
+        if (dma && col * 8 < nkeys && ((kbeg + col * 8) & ~63) + 64 <= L) continue;  // streamed in already
         u32x4 v = pcs[i];
         const int nv = nkeys - col * 8;  // valid keys in this piece
         if (nv < 8) {
@@ -1262,29 +1268,42 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
       const int qq = ln & 15, qd = ln >> 4;
       int k_at[HD / 32];
 #pragma unroll
-      for (int ks = 0; ks < HD / 32; ++ks) k_at[ks] = opaque((qq * KC + ((ks * 4 + qd) ^ (qq & 7))) * 16);
+      for (int ks = 0; ks < HD / 32; ++ks) k_at[ks] = opaque(kStageOff + (qq * KC + ((ks * 4 + qd) ^ (qq & 7))) * 16);
       const int vx = (qd >> 1) ^ (qq & 3);
-      const int vbase = KP * 16 + (qd & 1) * 8;  // sV, half of a 16-byte column
+      const int vbase = kStageOff + KP * 16 + (qd & 1) * 8;  // sV, half of a 16-byte column
       const int v0 = opaque(vbase + (qq * VC + vx) * 16), v1 = opaque(vbase + (qq * VC + (vx ^ 2)) * 16);
-      // scores of the wave's blocks (blocks outside [kb0, kb1) and keys past the end: -inf)
+      // scores of the wave's blocks (blocks outside [kb0, kb1) and keys past the end: -inf).
+      // Per 32-key block, four independent accumulation chains (two key tiles x hi/lo query
+      // parts) keep the matrix cores busy.
       f32x4 sc[2 * NKB];
 #pragma unroll
-      for (int kt = 0; kt < 2 * NKB; ++kt) {
-        f32x4 acc = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-        if (kt / 2 >= kb0 && kt / 2 < kb1) {
-          acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int kk = 0; kk < NKB; ++kk) {
+        f32x4 a0 = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, a1 = a0;
+        if (kk >= kb0 && kk < kb1) {
+          f32x4 h0 = {0.f, 0.f, 0.f, 0.f}, l0 = h0, h1 = h0, l1 = h0;
+          u32x4 k0v[HD / 32], k1v[HD / 32];
 #pragma unroll
           for (int ks = 0; ks < HD / 32; ++ks) {
-            const u32x4 kv = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + kt * 16 * KC * 16);
-            acc = mfma_h(kv, qh[ks], acc);
-            acc = mfma_h(kv, ql[ks], acc);
+            k0v[ks] = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + (2 * kk) * 16 * KC * 16);
+            k1v[ks] = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + (2 * kk + 1) * 16 * KC * 16);
           }
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (kt * 16 + qd * 4 + i >= nkeys) acc[i] = -INFINITY;
+          for (int ks = 0; ks < HD / 32; ++ks) {
+            h0 = mfma_h(k0v[ks], qh[ks], h0);
+            h1 = mfma_h(k1v[ks], qh[ks], h1);
+            l0 = mfma_h(k0v[ks], ql[ks], l0);
+            l1 = mfma_h(k1v[ks], ql[ks], l1);
+          }
+          a0 = h0 + l0;
+          a1 = h1 + l1;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (2 * kk * 16 + qd * 4 + i >= nkeys) a0[i] = -INFINITY;
+            if ((2 * kk + 1) * 16 + qd * 4 + i >= nkeys) a1[i] = -INFINITY;
+          }
         }
-        sc[kt] = acc;
-        __builtin_amdgcn_sched_barrier(0);  // bound how far LDS reads are hoisted (registers)
+        sc[2 * kk] = a0;
+        sc[2 * kk + 1] = a1;
       }
       // softmax statistics per query row (column q), in the log2 domain
 #pragma unroll
@@ -1322,7 +1341,6 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
             o[dt] = mfma_h(vv, pl, o[dt]);
           }
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
     }
     if (j == (int)blockIdx.x && w == 0) trace_mark(dc, pc.slot + 2, pc.nslots);
@@ -1362,33 +1380,44 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
     __syncthreads();  // LDS is refilled by the next item
   };
 
-  // The first item's context pieces come in the carry registers (requested by the QKV
-  // phase's tail) or are requested here, before the barrier.  Later items keep their pieces
-  // in a register array of their own scope, so none stays live across items.
+  // The first item's context pieces were streamed into LDS during an earlier phase
+  // (have_dma), or are requested here, before the barrier.  One call site for the item
+  // body keeps the phase's code small (it runs from a cold instruction cache).
   const int j0 = blockIdx.x;
-  if (!have_pf) attn_prefetch<HD>(a, dc, layer, pf);
-  phase_begin(a, dc, pc, failed);
-  if (j0 < items) finish(j0, pf);
-  for (int j = j0 + gridDim.x; j < items; j += gridDim.x) {
-    u32x4 pcs[PER];
+  u32x4 pcs[PER];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) pcs[i] = u32x4{0u, 0u, 0u, 0u};
-    issue(j, 0, pcs);
-    finish(j, pcs);
+  for (int i = 0; i < PER; ++i) pcs[i] = u32x4{0u, 0u, 0u, 0u};
+  if (!have_dma && j0 < items) issue(j0, 0, pcs);
+  phase_begin(a, dc, pc, failed);
+  for (int j = j0; j < items; j += gridDim.x) {
+    const bool dma = have_dma && j == j0;
+    if (j != j0) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) pcs[i] = u32x4{0u, 0u, 0u, 0u};
+      issue(j, 0, pcs);
+    }
+    finish(j, pcs, dma);
   }
 }
 
-// ---- COMB: merge the chunk partials of query row r of KV head g (one wave per row):
-// O = sum_c 2^(m_c - M) O_c / sum_c 2^(m_c - M) l_c, written as the A fragments of the
-// output projection.  Chunks are added in ascending order.
+// whether the combine phase leaves waves idle (they stage the next layer's attention item)
+__device__ __forceinline__ bool comb_stages(Args a) {
+  const int items = a->n_q * a->B;  // (query head, block row) pairs
+  return (items + (int)gridDim.x - 1) / (int)gridDim.x < kWaves;
+}
+
 template <int HD>
-__device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed) {
+__device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed, u32x4* smem) {
   constexpr int DPL = HD / 64;  // dims per lane
   phase_begin(a, dc, pc, failed);
   const int lane = opaque(threadIdx.x) & 63;
   const int G = a->n_q / a->n_kv, R = G * a->B;
   const int nch = max(1, (dc->L + kChunk - 1) / kChunk);
   const int items = a->n_kv * R;
+  // waves without a row to combine stream the next layer's first attention item into LDS
+  // (HBM is otherwise idle in this phase); with no idle wave, the attention phase loads it
+  if (comb_stages(a) && layer + 1 < a->D)
+    attn_dma<HD>(a, dc, layer + 1, blockIdx.x, smem, (items + (int)gridDim.x - 1) / (int)gridDim.x);
   const int q_Kt = a->n_q * HD / 32;
   uint32_t* ohi = reinterpret_cast<uint32_t*>(a->OA + layer * a->oa_stride);
   uint32_t* olo = reinterpret_cast<uint32_t*>(a->OA + layer * a->oa_stride + (long)(q_Kt + kKtPad) * 64);
@@ -1444,22 +1473,22 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
 }
 
 // GEMM phase with the plan's chunk width (the LM head always uses 8)
-template <int EPI, typename Tail>
+template <int EPI>
 __device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int layer, const PhaseCtl& pc, bool& failed,
-                                              u32x4* smem, Carry& pf, bool have_pf, Tail tail) {
+                                              u32x4* smem) {
   GemmJob g = make_job(a, kind, layer);
   const int kg = kind == PH_LM ? 1 : a->kg[kind];
   const int slot = kind == PH_QKV ? 0 : kind == PH_O ? 1 : kind == PH_GU ? 2 : 3;
   g.cnt = a->kcnt + (long)slot * kMaxBlocks * 32;
   g.target = (c->done_epoch * (unsigned)a->D + (unsigned)layer + 1u) * (unsigned)kg;
   if constexpr (EPI == EPI_ARGMAX) {
-    gemm_phase<EPI, 8>(a, c, g, 1, pc, failed, smem, pf, have_pf, tail);
+    gemm_phase<EPI, 8>(a, c, g, kind, 1, pc, failed, smem);
   } else {
     switch (a->tn[kind]) {
-      case 2: gemm_phase<EPI, 2>(a, c, g, kg, pc, failed, smem, pf, have_pf, tail); break;
-      case 4: gemm_phase<EPI, 4>(a, c, g, kg, pc, failed, smem, pf, have_pf, tail); break;
-      case 6: gemm_phase<EPI, 6>(a, c, g, kg, pc, failed, smem, pf, have_pf, tail); break;
-      default: gemm_phase<EPI, 8>(a, c, g, kg, pc, failed, smem, pf, have_pf, tail); break;
+      case 2: gemm_phase<EPI, 2>(a, c, g, kind, kg, pc, failed, smem); break;
+      case 4: gemm_phase<EPI, 4>(a, c, g, kind, kg, pc, failed, smem); break;
+      case 6: gemm_phase<EPI, 6>(a, c, g, kind, kg, pc, failed, smem); break;
+      default: gemm_phase<EPI, 8>(a, c, g, kind, kg, pc, failed, smem); break;
     }
   }
 }
@@ -1477,7 +1506,6 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
   const int nphase = phase_count(a->D);
   const int nslots = kTraceSlots * nphase;
   bool failed = false;
-  Carry pf;
   for (int p = p0; p < p1; ++p) {
     int kind, layer;
     phase_of(p, a->D, kind, layer);
@@ -1486,39 +1514,37 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
     pc.epoch = c->bar_epoch + (unsigned)(p - p0);
     pc.slot = kTraceSlots * p;
     pc.nslots = nslots;
-    // The QKV phase's tail requests the context pieces of the first attention item (into the
-    // carry registers), ahead of its epilogue, its stores and the grid barrier; the attention
-    // phase uses them when that tail ran in this launch.  Other phases request their first
-    // loads themselves: a tail load ahead of an epilogue that reads memory (the residual
-    // stream, split-K partials, counters) would hold that epilogue up, since a wave's loads
-    // complete in order.
-    const bool prev = p > p0;
+    // The context pieces of a layer's first attention item are streamed into LDS during the
+    // previous layer's combine phase by its idle waves (the embedding phase for layer 0);
+    // the attention phase uses them when that phase ran in this launch.
     switch (kind) {
       case PH_EMBED:
         phase_begin(a, c, pc, failed);
         phase_embed(a, c);
+        attn_dma<HD>(a, c, 0, blockIdx.x, smem, 0);
         break;
       case PH_QKV:
-        gemm_dispatch<EPI_QKV>(a, c, kind, layer, pc, failed, smem, pf, false,
-                               [&]() { attn_prefetch<HD>(a, c, layer, pf); });
+        gemm_dispatch<EPI_QKV>(a, c, kind, layer, pc, failed, smem);
         break;
       case PH_ATTN:
-        phase_attn<HD>(a, c, layer, pc, failed, smem, pf, prev);
+        // staged by the embedding phase (layer 0) or by the previous layer's combine phase
+        phase_attn<HD>(a, c, layer, pc, failed, smem,
+                       layer == 0 ? p - 2 >= p0 : (p - 5 >= p0 && comb_stages(a)));
         break;
       case PH_COMB:
-        phase_comb<HD>(a, c, layer, pc, failed);
+        phase_comb<HD>(a, c, layer, pc, failed, smem);
         break;
       case PH_O:
-        gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem, pf, false, []() {});
+        gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem);
         break;
       case PH_GU:
-        gemm_dispatch<EPI_SWIGLU>(a, c, kind, layer, pc, failed, smem, pf, false, []() {});
+        gemm_dispatch<EPI_SWIGLU>(a, c, kind, layer, pc, failed, smem);
         break;
       case PH_DOWN:
-        gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem, pf, false, []() {});
+        gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem);
         break;
       default:  // PH_LM
-        gemm_dispatch<EPI_ARGMAX>(a, c, kind, layer, pc, failed, smem, pf, false, []() {});
+        gemm_dispatch<EPI_ARGMAX>(a, c, kind, layer, pc, failed, smem);
         break;
     }
     if (p + 1 < p1) grid_arrive(a);

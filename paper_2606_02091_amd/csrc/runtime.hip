@@ -457,9 +457,24 @@ DraftArgs draft_args(const dflare_handle* h) {
   a.nch = h->attn_nch;
   a.eps = c.rms_eps;
   a.qscale = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
+  const int H = c.hidden, Kt_H = H / 32, q = c.n_q_heads * c.head_dim, kv = c.n_kv_heads * c.head_dim;
   for (int k = 0; k < PH_COUNT; ++k) {
     a.tn[k] = h->plan[k].tn;
     a.kg[k] = h->plan[k].kg;
+    int Nt = 0, Kt = 0;
+    switch (k) {
+      case PH_QKV: Nt = (q + 2 * kv) / 16; Kt = Kt_H; break;
+      case PH_O: Nt = H / 16; Kt = q / 32; break;
+      case PH_GU: Nt = 2 * c.ffn / 16; Kt = Kt_H; break;
+      case PH_DOWN: Nt = H / 16; Kt = c.ffn / 32; break;
+      case PH_LM: Nt = (c.vocab + 15) / 16; Kt = Kt_H; break;
+      default: break;
+    }
+    const int R = h->blocks / std::max(a.kg[k], 1);
+    a.nq[k] = Nt / R;
+    a.nr[k] = Nt % R;
+    a.kq[k] = Kt / std::max(a.kg[k], 1);
+    a.kr[k] = Kt % std::max(a.kg[k], 1);
   }
   a.embed = h->embed;
   a.w_qkv = h->w_qkv;
