@@ -67,6 +67,8 @@ typedef struct {
   int32_t max_new;         /* largest n_new accepted by dflare_fuse_append       */
   float rope_base;         /* rotary base, e.g. 1e6                              */
   float rms_eps;           /* RMSNorm epsilon, e.g. 1e-6                         */
+  int32_t max_batch;       /* sequence slots for the batched calls, 1..64
+                              (0 means 1); slot 0 is the batch-1 context         */
 } dflare_config;
 
 /*
@@ -107,7 +109,9 @@ typedef struct dflare_handle dflare_handle;
  *                  computed here in double precision and cached as float.  A row
  *                  with NaN or +inf, or with no finite entry, is INVALID_ARG.
  *   stream         hipStream_t for all work of this handle (NULL = default stream).
- *   out            receives the handle.  The context starts empty (L = 0).
+ *   out            receives the handle.  Every context starts empty (L = 0).
+ * Each of the max_batch sequence slots owns a context cache of max_context rows
+ * per draft layer.
  * Synchronises the stream before returning.
  */
 int dflare_init(const dflare_config* cfg, const dflare_weights* weights,
@@ -154,6 +158,43 @@ int dflare_truncate(dflare_handle* h, int32_t new_len);
 /* dflare_context_len -- current context length L into *out. */
 int dflare_context_len(const dflare_handle* h, int32_t* out);
 
+/*
+ * Batched calls: the draft step of several independent sequences at once (Sec. 3.2
+ * drafting phase and Sec. 4.1-4.2 context update, applied per sequence; the
+ * sequences share the draft weights and nothing else).  Sequence slots are
+ * 0 .. max_batch-1, each with its own context length and cache; the batch-1 calls
+ * above work on slot 0.  In every batched call:
+ *   n_seq          1 <= n_seq <= max_batch
+ *   seq            HOST int32 [n_seq]: distinct slots in [0, max_batch)
+ * Results are those of the batch-1 calls on each slot in turn, up to rounding
+ * order: the batched kernels sum in a different order (same precision).
+ */
+
+/*
+ * dflare_fuse_append_batched -- dflare_fuse_append for sequence seq[i] with
+ * n_new[i] rows, for every i.
+ *   n_new          HOST int32 [n_seq], each >= 1, sum <= max_new, else INVALID_ARG;
+ *                  L_seq[i] + n_new[i] > max_context for any i gives CONTEXT_FULL
+ *                  and changes nothing.
+ *   target_hidden  DEVICE bf16 [S, sum(n_new), H]: for each target layer, the rows
+ *                  of seq[0], then those of seq[1], ...
+ */
+int dflare_fuse_append_batched(dflare_handle* h, int32_t n_seq, const int32_t* seq, const int32_t* n_new,
+                               const void* target_hidden);
+
+/*
+ * dflare_draft_block_batched -- dflare_draft_block for every listed sequence.
+ *   block_ids      DEVICE int32 [n_seq, B]: row i is the block of seq[i].
+ *   draft_tokens   DEVICE int32 [n_seq, B]: greedy tokens, row i for seq[i].
+ * Block row b of seq[i] sits at position L_seq[i] + b.  No cache is modified.
+ */
+int dflare_draft_block_batched(dflare_handle* h, int32_t n_seq, const int32_t* seq, const int32_t* block_ids,
+                               int32_t* draft_tokens);
+
+/* dflare_truncate_seq / dflare_context_len_seq -- as above, for one slot. */
+int dflare_truncate_seq(dflare_handle* h, int32_t seq, int32_t new_len);
+int dflare_context_len_seq(const dflare_handle* h, int32_t seq, int32_t* out);
+
 /* dflare_set_stream -- make later work of the handle go to `stream`. */
 int dflare_set_stream(dflare_handle* h, void* stream);
 
@@ -176,6 +217,8 @@ const char* dflare_last_error(const dflare_handle* h);
  *   what = DFLARE_DBG_HIDDEN  layer i: [B, H]        block rows after layer i
  *   what = DFLARE_DBG_LOGITS  (layer ignored) [B, V] logits of the last draft_block
  *   what = DFLARE_DBG_ALPHA   (layer ignored) [D, S] cached fusion weights
+ *   what = DFLARE_DBG_BLOGITS (layer ignored) [n_seq, B, V] logits of the last
+ *                             dflare_draft_block_batched (n_seq of that call)
  *   what = DFLARE_DBG_TRACE   (layer ignored) [blocks, phases, 4] microseconds, relative to
  *                             the earliest mark, at which each work-group of the last
  *                             draft_block reached four marks of each phase: body start
@@ -185,13 +228,17 @@ const char* dflare_last_error(const dflare_handle* h);
  *                             no such mark.  Needs DFLARE_OPT_TRACE (sizes from
  *                             dflare_kernel_stats)
  * `count` is the number of floats host_out can hold; too small is INVALID_ARG.
- * Debug capture makes draft_block run one launch per phase.
+ * Debug capture makes draft_block run one launch per phase.  FUSED after a
+ * batched append holds all sum(n_new) rows of that call.
+ * dflare_debug_read_seq reads DFLARE_DBG_KCACHE / DFLARE_DBG_VCACHE of slot `seq`
+ * ([L_seq, n_kv, hd]); dflare_debug_read reads those of slot 0.
  */
 enum { DFLARE_DBG_FUSED = 0, DFLARE_DBG_KCACHE = 1, DFLARE_DBG_VCACHE = 2,
        DFLARE_DBG_HIDDEN = 3, DFLARE_DBG_LOGITS = 4, DFLARE_DBG_ALPHA = 5,
-       DFLARE_DBG_TRACE = 6 };
+       DFLARE_DBG_TRACE = 6, DFLARE_DBG_BLOGITS = 7 };
 int dflare_debug_capture(dflare_handle* h, int on);
 int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, int64_t count);
+int dflare_debug_read_seq(dflare_handle* h, int what, int seq, int layer, float* host_out, int64_t count);
 
 /*
  * dflare_kernel_stats -- launch shape, for measurement: writes up to `count`

@@ -25,6 +25,7 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kStatsPad = 32;   // floats per 16-column tile in the sums-of-squares arrays (one 128 B line)
 constexpr int kBarCounters = 16;  // grid-barrier arrival counters, each on its own 128 B line
 constexpr int kMaxBlock = 16;     // draft block rows (one 16-row MFMA tile)
+constexpr int kChunk = 128;       // context keys per attention work item
 // wall-clock marks per phase: body start (after the grid barrier), two inner marks
 // (GEMM: main loop done, chunk epilogues done; attention: keys staged, scores and
 // values done; combine: partials loaded), stores complete

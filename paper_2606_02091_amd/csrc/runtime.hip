@@ -1,9 +1,9 @@
 // Host runtime and C ABI of the DFlare draft step (see include/dflare.h).
 //
 // One handle owns: the re-packed weights, the cached fusion weights alpha, the
-// per-draft-layer context cache (K as [n_kv, Lcap, hd], V transposed as
-// [n_kv, hd, Lcap], each as two bf16 planes hi + lo), a rotary table, and the
-// activation buffers of one draft block.  fuse_append enqueues two kernels (fusion,
+// per-draft-layer context cache of every sequence slot (K as [n_kv, Lcap, hd], V
+// transposed as [n_kv, hd, Lcap], fp16), a rotary table, and the activation buffers of
+// one draft block and of one batched draft step.  fuse_append enqueues two kernels (fusion,
 // context K/V projection); draft_block enqueues one persistent cooperative kernel (or,
 // on request, the same kernel once per phase).  Values that change between calls (L,
 // n_new, positions, the block ids pointer) travel as kernel arguments.
@@ -18,6 +18,7 @@
 #include <unordered_set>
 #include <vector>
 
+#include "batched.h"
 #include "dflare.h"
 #include "dflare_impl.h"
 
@@ -60,7 +61,7 @@ struct dflare_handle {
   dflare_config cfg{};
   hipStream_t stream = nullptr;
   int device = 0;
-  int L = 0;
+  std::vector<int> Ls;  // context length of each sequence slot (slot 0: the batch-1 calls)
   int Lcap = 0;
   int q_dim = 0, kv_dim = 0;
   int Rpad = 0;
@@ -119,6 +120,19 @@ struct dflare_handle {
   int prof_kind = 0;
   std::vector<hipEvent_t> prof_ev;  // pairs
   int prof_n = 0;
+  // batched draft step
+  int cus = 0;
+  long seq_stride = 0;     // cache elements of one sequence slot (all layers)
+  int b_mt = 1;            // m-tiles of the largest batched call
+  long bY_elems = 0;       // capacity of the GEMM K-slice buffer (floats)
+  float *bX = nullptr, *bstats = nullptr, *brstd = nullptr, *bQ = nullptr, *bY = nullptr, *bOP = nullptr;
+  float2* bML = nullptr;
+  u32x4 *bA = nullptr, *bOA = nullptr, *bHA = nullptr;  // A fragments: hi plane, then lo plane
+  long bA_plane = 0, bOA_plane = 0, bHA_plane = 0;
+  float* bpmax = nullptr;
+  int* bpidx = nullptr;
+  float* dbg_blogits = nullptr;
+  int dbg_blogits_rows = 0;
   std::vector<void*> allocs;
   std::string err;
 };
@@ -224,6 +238,8 @@ int validate_config(const dflare_config* c) {
   if (c->hidden > 8192) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "hidden must be <= 8192");
   if ((long)c->max_context + c->block_size > (1L << 30))
     return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "max_context too large");
+  if (c->max_batch < 0 || c->max_batch > kMaxSeq)
+    return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "max_batch must be in [0, 64]");
   return DFLARE_OK;
 }
 
@@ -276,6 +292,30 @@ GemmPlan choose_plan(const char* name, int Nt, int Kt, int blocks, bool allow_sp
   return best;
 }
 
+// K split of a batched GEMM: the smallest estimated time, counted as (work-group
+// rounds over the CUs) x (k-tiles per work-group) plus a fixed 4 k-tiles per extra slice
+// for writing and summing it.  DFLARE_BSPLIT_<NAME>=kg overrides the choice (tuning).
+int bgemm_split(const dflare_handle* h, const char* name, int Nt, int Mt, int Kt) {
+  const long groups = bgemm_groups(Nt, Mt);
+  int best = 1;
+  double best_t = 1e300;
+  for (int kg : {1, 2, 3, 4, 6, 8}) {
+    if (kg > 1 && Kt < 8 * kg) continue;
+    const double t = (double)ceil_div(groups * kg, h->cus) * ceil_div(Kt, kg) + 4.0 * (kg - 1);
+    if (t < best_t - 1e-9) {
+      best_t = t;
+      best = kg;
+    }
+  }
+  char key[64];
+  snprintf(key, sizeof key, "DFLARE_BSPLIT_%s", name);
+  if (const char* env = getenv(key)) {
+    const int v = atoi(env);
+    if (v >= 1 && v <= 8 && v <= Kt) best = v;
+  }
+  return best;
+}
+
 DraftArgs draft_args(const dflare_handle* h);
 
 int build(dflare_handle* h, const dflare_weights* w) {
@@ -299,6 +339,7 @@ int build(dflare_handle* h, const dflare_weights* w) {
   // ---- launch shape of the draft block: one work-group of kThreads per CU
   int cus = 0;
   HIP_OR_FAIL(h, hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device));
+  h->cus = cus;
   int coop = 0;
   HIP_OR_FAIL(h, hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device));
   const int per_cu = draft_blocks_per_cu(hd);
@@ -388,8 +429,10 @@ int build(dflare_handle* h, const dflare_weights* w) {
   // ---- context cache, rotary table
   // per layer: K (or V^T) in fp16
   h->cache_layer_stride = (long)c.n_kv_heads * h->Lcap * hd;
-  TRY(dev_zalloc(h, &h->kc, (size_t)h->cache_layer_stride * D * 2));
-  TRY(dev_zalloc(h, &h->vt, (size_t)h->cache_layer_stride * D * 2));
+  h->seq_stride = h->cache_layer_stride * D;
+  h->Ls.assign(c.max_batch, 0);
+  TRY(dev_zalloc(h, &h->kc, (size_t)h->seq_stride * c.max_batch * 2));
+  TRY(dev_zalloc(h, &h->vt, (size_t)h->seq_stride * c.max_batch * 2));
   {
     const int half = hd / 2;
     std::vector<float2> tab((size_t)h->Lcap * half);
@@ -428,6 +471,40 @@ int build(dflare_handle* h, const dflare_weights* w) {
   TRY(dev_zalloc(h, &h->pidx, (size_t)h->blocks * kStatsPad * 4));
   TRY(dev_zalloc(h, &h->part, (size_t)h->blocks * kTNMax * 1024));
   TRY(dev_zalloc(h, &h->sync, kSyncBytes));
+
+  // ---- batched draft step: activations of max_batch * B rows
+  {
+    h->b_mt = ceil_div((long)c.max_batch * B, 16);
+    const long rows = (long)h->b_mt * 16;
+    TRY(dev_zalloc(h, &h->bX, (size_t)rows * H * 4));
+    TRY(dev_zalloc(h, &h->bstats, (size_t)rows * (H / 16) * 4));
+    TRY(dev_zalloc(h, &h->brstd, (size_t)std::max(rows, (long)mt_max * 16) * 4));
+    TRY(dev_zalloc(h, &h->bQ, (size_t)rows * q * 4));
+    h->bA_plane = (long)h->b_mt * Kt_H * 64;
+    h->bOA_plane = (long)h->b_mt * Kt_q * 64;
+    h->bHA_plane = (long)h->b_mt * Kt_F * 64;
+    TRY(dev_zalloc(h, &h->bA, (size_t)2 * h->bA_plane * 16));
+    TRY(dev_zalloc(h, &h->bOA, (size_t)2 * h->bOA_plane * 16));
+    TRY(dev_zalloc(h, &h->bHA, (size_t)2 * h->bHA_plane * 16));
+    // K slices of the largest GEMM of any call shape
+    long y = 0;
+    for (int mt = 1; mt <= h->b_mt; ++mt) {
+      y = std::max(y, (long)bgemm_split(h, "QKV", Nt_qkv, mt, Kt_H) * mt * 16 * Nt_qkv * 16);
+      y = std::max(y, (long)bgemm_split(h, "O", Nt_o, mt, Kt_q) * mt * 16 * Nt_o * 16);
+      y = std::max(y, (long)bgemm_split(h, "GU", Nt_gu, mt, Kt_H) * mt * 16 * Nt_gu * 16);
+      y = std::max(y, (long)bgemm_split(h, "DOWN", Nt_down, mt, Kt_F) * mt * 16 * Nt_down * 16);
+    }
+    for (int mt = 1; mt <= mt_max; ++mt)
+      y = std::max(y, (long)bgemm_split(h, "KVT", Nt_kvt, mt, Kt_H) * mt * 16 * Nt_kvt * 16);
+    h->bY_elems = y;
+    TRY(dev_alloc(h, &h->bY, (size_t)y * 4));
+    const long items = (long)c.max_batch * h->attn_nch * c.n_kv_heads;
+    TRY(dev_alloc(h, &h->bOP, (size_t)items * h->Rpad * hd * 4));
+    TRY(dev_alloc(h, &h->bML, (size_t)items * h->Rpad * sizeof(float2)));
+    const long ng_lm = ceil_div(Nt_lm, kBN);
+    TRY(dev_alloc(h, &h->bpmax, (size_t)ng_lm * rows * 4));
+    TRY(dev_alloc(h, &h->bpidx, (size_t)ng_lm * rows * 4));
+  }
   HIP_OR_FAIL(h, hipHostMalloc((void**)&h->err_host, 64, hipHostMallocMapped | hipHostMallocCoherent));
   *(volatile int*)h->err_host = 0;
   HIP_OR_FAIL(h, hipHostGetDevicePointer((void**)&h->err_dev, h->err_host, 0));
@@ -520,8 +597,8 @@ DraftArgs draft_args(const dflare_handle* h) {
 DraftCall draft_call(const dflare_handle* h, const int32_t* ids, const int32_t* positions_host, int32_t* out) {
   const dflare_config& c = h->cfg;
   DraftCall d{};
-  d.L = h->L;
-  for (int b = 0; b < kMaxBlock; ++b) d.pos[b] = (b < c.block_size) ? (positions_host ? positions_host[b] : h->L + b) : 0;
+  d.L = h->Ls[0];
+  for (int b = 0; b < kMaxBlock; ++b) d.pos[b] = (b < c.block_size) ? (positions_host ? positions_host[b] : h->Ls[0] + b) : 0;
   d.ids = ids;
   d.tokens = out;
   d.logits = h->debug ? h->dbg_logits : nullptr;
@@ -594,6 +671,186 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   return check_launch(h, "draft_block");
 }
 
+// n_seq distinct slots in range
+int check_seqs(dflare_handle* h, int32_t n_seq, const int32_t* seq) {
+  if (n_seq < 1 || n_seq > h->cfg.max_batch) return fail(h, DFLARE_ERR_INVALID_ARG, "n_seq must be in [1, max_batch]");
+  if (!seq) return fail(h, DFLARE_ERR_INVALID_ARG, "seq is NULL");
+  std::vector<char> seen(h->cfg.max_batch, 0);
+  for (int i = 0; i < n_seq; ++i) {
+    if (seq[i] < 0 || seq[i] >= h->cfg.max_batch)
+      return fail(h, DFLARE_ERR_INVALID_ARG, "a sequence slot is outside [0, max_batch)");
+    if (seen[seq[i]]) return fail(h, DFLARE_ERR_INVALID_ARG, "sequence slots must be distinct");
+    seen[seq[i]] = 1;
+  }
+  return DFLARE_OK;
+}
+
+// Y = A W^T over all rows of a batched call, K split chosen per shape (bounded by the slice buffer)
+int bgemm(dflare_handle* h, const char* name, const u32x4* a_hi, const u32x4* a_lo, int a_kt, const u32x4* w,
+          int Nt, int Kt, int M, BEpiArgs& e) {
+  BGemmArgs g{};
+  g.Ahi = a_hi;
+  g.Alo = a_lo;
+  g.a_kt = a_kt;
+  g.W = w;
+  g.Nt = Nt;
+  g.Kt = Kt;
+  g.zero = h->zero_tile;
+  g.Mt = ceil_div(M, 16);
+  g.M = M;
+  g.kg = bgemm_split(h, name, Nt, g.Mt, Kt);
+  while (g.kg > 1 && (long)g.kg * g.Mt * 16 * Nt * 16 > h->bY_elems) --g.kg;
+  g.Y = h->bY;
+  g.ldy = Nt * 16;
+  launch_bgemm(h->stream, g, false);
+  e.Y = h->bY;
+  e.kg = g.kg;
+  e.Mpad = g.Mt * 16;
+  e.ldy = g.ldy;
+  e.N = Nt * 16;
+  e.M = M;
+  return DFLARE_OK;
+}
+
+BEpiArgs bepi_base(const dflare_handle* h) {
+  const dflare_config& c = h->cfg;
+  BEpiArgs e{};
+  e.H = c.hidden;
+  e.rstd = h->brstd;
+  e.X = h->bX;
+  e.stats = h->bstats;
+  e.Q = h->bQ;
+  e.q_dim = h->q_dim;
+  e.kc = h->kc;
+  e.vt = h->vt;
+  e.seq_stride = h->seq_stride;
+  e.cache_layer = h->cache_layer_stride;
+  e.Lcap = h->Lcap;
+  e.hd = c.head_dim;
+  e.q_tiles = h->q_dim / 16;
+  e.kv_tiles = h->kv_dim / 16;
+  e.rope = h->rope;
+  return e;
+}
+
+int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int32_t* n_new, const void* hidden) {
+  const dflare_config& c = h->cfg;
+  const int H = c.hidden, D = c.n_draft_layers, S = c.n_target_layers, Kt_H = H / 32;
+  hipStream_t s = h->stream;
+  BRows rows{};
+  rows.n_seq = n_seq;
+  for (int i = 0; i < n_seq; ++i) {
+    rows.seq[i] = seq[i];
+    rows.L[i] = h->Ls[seq[i]];
+    rows.off[i + 1] = rows.off[i] + n_new[i];
+  }
+  const int N = rows.off[n_seq];
+  launch_fuse(s, (const uint16_t*)hidden, N, S, H, D, h->alpha, h->g_fuse, h->Ustats, h->ua_hi, h->ua_lo, c.max_new,
+              h->mt_max);
+  const long ua_layer = (long)h->mt_max * Kt_H * 64;
+  for (int l = 0; l < D; ++l) {
+    launch_brstd(s, h->Ustats + (long)l * c.max_new * (H / 16), H / 16, N, 1.0f / H, c.rms_eps, h->brstd);
+    BEpiArgs e = bepi_base(h);
+    TRY(bgemm(h, "KVT", h->ua_hi + l * ua_layer, h->ua_lo + l * ua_layer, Kt_H, h->w_kvt + l * h->s_kvt,
+              2 * h->kv_dim / 16, Kt_H, N, e));
+    e.layer = l;
+    e.q_tiles = 0;
+    launch_bepi(s, BEPI_QKV, e, rows);
+  }
+  if (h->debug) {
+    launch_fused_rows(s, h->ua_hi, h->ua_lo, h->Ustats, N, H, D, c.max_new, h->mt_max, c.rms_eps, h->dbg_fused);
+    h->dbg_fused_n = N;
+  }
+  TRY(check_launch(h, "fuse_append_batched"));
+  for (int i = 0; i < n_seq; ++i) h->Ls[seq[i]] += n_new[i];
+  return DFLARE_OK;
+}
+
+int run_draft_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int32_t* ids, int32_t* out) {
+  const dflare_config& c = h->cfg;
+  const int H = c.hidden, F = c.ffn, V = c.vocab, D = c.n_draft_layers, B = c.block_size, hd = c.head_dim;
+  const int Kt_H = H / 32, Kt_q = h->q_dim / 32, Kt_F = F / 32;
+  const int Nt_qkv = (h->q_dim + 2 * h->kv_dim) / 16, Nt_H = H / 16, Nt_gu = 2 * F / 16, Nt_lm = ceil_div(V, 16);
+  hipStream_t s = h->stream;
+  const int M = n_seq * B, Mt = ceil_div(M, 16);
+  BRows rows{};
+  rows.n_seq = n_seq;
+  for (int i = 0; i < n_seq; ++i) {
+    rows.seq[i] = seq[i];
+    rows.L[i] = h->Ls[seq[i]];
+    rows.off[i + 1] = (i + 1) * B;
+    rows.ipfx[i + 1] = rows.ipfx[i] + std::max(1, ceil_div(rows.L[i], kChunk)) * c.n_kv_heads;
+  }
+  const int items = rows.ipfx[n_seq];
+  BAttnArgs at{};
+  at.Q = h->bQ;
+  at.kc = h->kc;
+  at.vt = h->vt;
+  at.seq_stride = h->seq_stride;
+  at.cache_layer = h->cache_layer_stride;
+  at.Lcap = h->Lcap;
+  at.B = B;
+  at.n_q = c.n_q_heads;
+  at.n_kv = c.n_kv_heads;
+  at.Rpad = h->Rpad;
+  at.qscale = (float)(1.4426950408889634 / sqrt((double)hd));
+  at.OP = h->bOP;
+  at.ML = h->bML;
+  const float inv_H = 1.0f / H;
+
+  launch_bembed(s, h->embed, ids, M, H, V, h->g_attn, h->bX, h->bstats, h->bA, h->bA + h->bA_plane, Kt_H);
+  for (int l = 0; l < D; ++l) {
+    launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
+    BEpiArgs e = bepi_base(h);
+    TRY(bgemm(h, "QKV", h->bA, h->bA + h->bA_plane, Kt_H, h->w_qkv + l * h->s_qkv, Nt_qkv, Kt_H, M, e));
+    e.layer = l;
+    launch_bepi(s, BEPI_QKV, e, rows);
+    at.layer = l;
+    launch_battn(s, hd, at, rows, items);
+    launch_bcomb(s, hd, at, rows, h->bOA, h->bOA + h->bOA_plane, Kt_q);
+    TRY(bgemm(h, "O", h->bOA, h->bOA + h->bOA_plane, Kt_q, h->w_o + l * h->s_o, Nt_H, Kt_q, M, e));
+    e.gain = h->g_mlp + (long)l * H;
+    e.ahi = h->bA;
+    e.alo = h->bA + h->bA_plane;
+    e.a_kt = Kt_H;
+    launch_bepi(s, BEPI_RESID, e, rows);
+    launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
+    TRY(bgemm(h, "GU", h->bA, h->bA + h->bA_plane, Kt_H, h->w_gu + l * h->s_gu, Nt_gu, Kt_H, M, e));
+    e.ahi = h->bHA;
+    e.alo = h->bHA + h->bHA_plane;
+    e.a_kt = Kt_F;
+    launch_bepi(s, BEPI_SWIGLU, e, rows);
+    TRY(bgemm(h, "DOWN", h->bHA, h->bHA + h->bHA_plane, Kt_F, h->w_down + l * h->s_down, Nt_H, Kt_F, M, e));
+    e.gain = (l + 1 < D) ? h->g_attn + (long)(l + 1) * H : h->g_final;
+    e.ahi = h->bA;
+    e.alo = h->bA + h->bA_plane;
+    e.a_kt = Kt_H;
+    launch_bepi(s, BEPI_RESID, e, rows);
+  }
+  launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
+  BGemmArgs g{};
+  g.Ahi = h->bA;
+  g.Alo = h->bA + h->bA_plane;
+  g.a_kt = Kt_H;
+  g.W = h->w_lm;
+  g.Nt = Nt_lm;
+  g.Kt = Kt_H;
+  g.zero = h->zero_tile;
+  g.Mt = Mt;
+  g.M = M;
+  g.kg = 1;
+  g.rstd = h->brstd;
+  g.logits = h->debug ? h->dbg_blogits : nullptr;
+  g.V = V;
+  g.pmax = h->bpmax;
+  g.pidx = h->bpidx;
+  g.pld = h->b_mt * 16;
+  launch_bgemm(s, g, true);
+  launch_bargmax(s, h->bpmax, h->bpidx, ceil_div(Nt_lm, kBN), g.pld, M, out);
+  if (h->debug) h->dbg_blogits_rows = M;
+  return check_launch(h, "draft_block_batched");
+}
+
 }  // namespace
 
 extern "C" {
@@ -626,6 +883,7 @@ int dflare_init(const dflare_config* cfg, const dflare_weights* w, const float* 
   }
   dflare_handle* h = new dflare_handle();
   h->cfg = *cfg;
+  if (h->cfg.max_batch == 0) h->cfg.max_batch = 1;
   h->stream = (hipStream_t)stream;
   h->alpha_host = alpha;
   int rc = build(h, w);
@@ -649,7 +907,7 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   if (!target_hidden) return fail(h, DFLARE_ERR_INVALID_ARG, "target_hidden is NULL");
   if (n_new < 1 || n_new > h->cfg.max_new)
     return fail(h, DFLARE_ERR_INVALID_ARG, "n_new must be in [1, max_new]");
-  if ((long)h->L + n_new > h->cfg.max_context)
+  if ((long)h->Ls[0] + n_new > h->cfg.max_context)
     return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
   const dflare_config& c = h->cfg;
   const int H = c.hidden, D = c.n_draft_layers, S = c.n_target_layers;
@@ -672,7 +930,7 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   a.n_stat = H / 16;
   a.inv_dim = 1.0f / H;
   a.eps = c.rms_eps;
-  a.L = h->L;
+  a.L = h->Ls[0];
   a.n_new = n_new;
   a.kc = h->kc;
   a.vt = h->vt;
@@ -691,7 +949,7 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   }
   int rc = check_launch(h, "fuse_append");
   if (rc != DFLARE_OK) return rc;
-  h->L += n_new;
+  h->Ls[0] += n_new;
   return DFLARE_OK;
 }
 
@@ -712,16 +970,55 @@ int dflare_draft_block_pos(dflare_handle* h, const int32_t* block_ids, const int
   return run_draft_block(h, block_ids, positions, draft_tokens);
 }
 
+int dflare_fuse_append_batched(dflare_handle* h, int32_t n_seq, const int32_t* seq, const int32_t* n_new,
+                               const void* target_hidden) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  TRY(check_seqs(h, n_seq, seq));
+  if (!n_new || !target_hidden) return fail(h, DFLARE_ERR_INVALID_ARG, "n_new / target_hidden is NULL");
+  long total = 0;
+  for (int i = 0; i < n_seq; ++i) {
+    if (n_new[i] < 1) return fail(h, DFLARE_ERR_INVALID_ARG, "every n_new must be >= 1");
+    total += n_new[i];
+  }
+  if (total > h->cfg.max_new) return fail(h, DFLARE_ERR_INVALID_ARG, "sum of n_new must be <= max_new");
+  for (int i = 0; i < n_seq; ++i)
+    if ((long)h->Ls[seq[i]] + n_new[i] > h->cfg.max_context)
+      return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
+  return run_fuse_batched(h, n_seq, seq, n_new, target_hidden);
+}
+
+int dflare_draft_block_batched(dflare_handle* h, int32_t n_seq, const int32_t* seq, const int32_t* block_ids,
+                               int32_t* draft_tokens) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  TRY(check_seqs(h, n_seq, seq));
+  if (!block_ids || !draft_tokens) return fail(h, DFLARE_ERR_INVALID_ARG, "block_ids / draft_tokens is NULL");
+  return run_draft_batched(h, n_seq, seq, block_ids, draft_tokens);
+}
+
+int dflare_truncate_seq(dflare_handle* h, int32_t seq, int32_t new_len) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (seq < 0 || seq >= h->cfg.max_batch) return fail(h, DFLARE_ERR_INVALID_ARG, "seq must be in [0, max_batch)");
+  if (new_len < 0 || new_len > h->Ls[seq]) return fail(h, DFLARE_ERR_INVALID_ARG, "new_len must be in [0, L]");
+  h->Ls[seq] = new_len;
+  return DFLARE_OK;
+}
+
+int dflare_context_len_seq(const dflare_handle* h, int32_t seq, int32_t* out) {
+  if (!live(h) || !out || seq < 0 || seq >= h->cfg.max_batch) return DFLARE_ERR_INVALID_ARG;
+  *out = h->Ls[seq];
+  return DFLARE_OK;
+}
+
 int dflare_truncate(dflare_handle* h, int32_t new_len) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
-  if (new_len < 0 || new_len > h->L) return fail(h, DFLARE_ERR_INVALID_ARG, "new_len must be in [0, L]");
-  h->L = new_len;
+  if (new_len < 0 || new_len > h->Ls[0]) return fail(h, DFLARE_ERR_INVALID_ARG, "new_len must be in [0, L]");
+  h->Ls[0] = new_len;
   return DFLARE_OK;
 }
 
 int dflare_context_len(const dflare_handle* h, int32_t* out) {
   if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
-  *out = h->L;
+  *out = h->Ls[0];
   return DFLARE_OK;
 }
 
@@ -769,21 +1066,30 @@ int dflare_debug_capture(dflare_handle* h, int on) {
     TRY(dev_alloc(h, &h->dbg_hidden, (size_t)c.n_draft_layers * c.block_size * c.hidden * 4));
     TRY(dev_alloc(h, &h->dbg_logits, (size_t)c.block_size * c.vocab * 4));
     TRY(dev_alloc(h, &h->dbg_fused, (size_t)c.n_draft_layers * c.max_new * c.hidden * 4));
+    TRY(dev_alloc(h, &h->dbg_blogits, (size_t)c.max_batch * c.block_size * c.vocab * 4));
   }
   h->debug = on != 0;
   return DFLARE_OK;
 }
 
 int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, int64_t count) {
+  return dflare_debug_read_seq(h, what, 0, layer, host_out, count);
+}
+
+int dflare_debug_read_seq(dflare_handle* h, int what, int seq, int layer, float* host_out, int64_t count) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
   if (!host_out) return fail(h, DFLARE_ERR_INVALID_ARG, "host_out is NULL");
+  if (seq < 0 || seq >= h->cfg.max_batch) return fail(h, DFLARE_ERR_INVALID_ARG, "seq must be in [0, max_batch)");
+  if (seq != 0 && what != DFLARE_DBG_KCACHE && what != DFLARE_DBG_VCACHE)
+    return fail(h, DFLARE_ERR_INVALID_ARG, "only the caches are read per sequence slot");
   const dflare_config& c = h->cfg;
   const int H = c.hidden, B = c.block_size, hd = c.head_dim, nkv = c.n_kv_heads;
   const bool needs_layer = what == DFLARE_DBG_FUSED || what == DFLARE_DBG_KCACHE || what == DFLARE_DBG_VCACHE ||
                            what == DFLARE_DBG_HIDDEN;
   if (needs_layer && (layer < 0 || layer >= c.n_draft_layers))
     return fail(h, DFLARE_ERR_INVALID_ARG, "layer out of range");
-  if ((what == DFLARE_DBG_FUSED || what == DFLARE_DBG_HIDDEN || what == DFLARE_DBG_LOGITS) && !h->dbg_hidden)
+  if ((what == DFLARE_DBG_FUSED || what == DFLARE_DBG_HIDDEN || what == DFLARE_DBG_LOGITS ||
+       what == DFLARE_DBG_BLOGITS) && !h->dbg_hidden)
     return fail(h, DFLARE_ERR_INVALID_ARG, "debug capture was never enabled");
   if (what == DFLARE_DBG_TRACE && !h->trace_buf) return fail(h, DFLARE_ERR_INVALID_ARG, "tracing was never enabled");
   HIP_OR_FAIL(h, hipStreamSynchronize(h->stream));
@@ -813,14 +1119,22 @@ int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, in
       HIP_OR_FAIL(h, hipMemcpy(host_out, h->dbg_logits, n * 4, hipMemcpyDeviceToHost));
       return DFLARE_OK;
     }
+    case DFLARE_DBG_BLOGITS: {
+      const int64_t n = (int64_t)h->dbg_blogits_rows * c.vocab;
+      if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
+      HIP_OR_FAIL(h, hipMemcpy(host_out, h->dbg_blogits, n * 4, hipMemcpyDeviceToHost));
+      return DFLARE_OK;
+    }
     case DFLARE_DBG_KCACHE:
     case DFLARE_DBG_VCACHE: {
-      const int64_t n = (int64_t)h->L * nkv * hd;
+      const int L = h->Ls[seq];
+      const int64_t n = (int64_t)L * nkv * hd;
       if (count < n) return fail(h, DFLARE_ERR_INVALID_ARG, "host buffer too small");
       std::vector<uint16_t> raw((size_t)h->cache_layer_stride);
-      const uint16_t* src = (what == DFLARE_DBG_KCACHE ? h->kc : h->vt) + (long)layer * h->cache_layer_stride;
+      const uint16_t* src = (what == DFLARE_DBG_KCACHE ? h->kc : h->vt) + seq * h->seq_stride +
+                            (long)layer * h->cache_layer_stride;
       HIP_OR_FAIL(h, hipMemcpy(raw.data(), src, raw.size() * 2, hipMemcpyDeviceToHost));
-      for (int p = 0; p < h->L; ++p)
+      for (int p = 0; p < L; ++p)
         for (int g = 0; g < nkv; ++g)
           for (int d = 0; d < hd; ++d) {
             const size_t ix = (what == DFLARE_DBG_KCACHE) ? ((size_t)g * h->Lcap + p) * hd + d

@@ -17,7 +17,7 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "libdflare.so")
 
 OK, ERR_INVALID_ARG, ERR_OUT_OF_MEMORY, ERR_CONTEXT_FULL, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-DBG_FUSED, DBG_KCACHE, DBG_VCACHE, DBG_HIDDEN, DBG_LOGITS, DBG_ALPHA, DBG_TRACE = range(7)
+DBG_FUSED, DBG_KCACHE, DBG_VCACHE, DBG_HIDDEN, DBG_LOGITS, DBG_ALPHA, DBG_TRACE, DBG_BLOGITS = range(8)
 OPT_PERSISTENT, OPT_TRACE = 1, 2
 
 EXPORTED = (
@@ -25,6 +25,8 @@ EXPORTED = (
     "dflare_truncate", "dflare_context_len", "dflare_set_stream", "dflare_destroy",
     "dflare_status_str", "dflare_last_error", "dflare_debug_capture", "dflare_debug_read",
     "dflare_kernel_stats", "dflare_profile_begin", "dflare_profile_end", "dflare_set_option",
+    "dflare_fuse_append_batched", "dflare_draft_block_batched", "dflare_truncate_seq",
+    "dflare_context_len_seq", "dflare_debug_read_seq",
 )
 K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T, K_DRAFT = range(1, 10)
 
@@ -39,7 +41,7 @@ class dflare_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "vocab", "n_draft_layers",
         "n_target_layers", "block_size", "max_context", "max_new")] + [
-        ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float)]
+        ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float), ("max_batch", ctypes.c_int32)]
 
 
 WEIGHT_FIELDS = ("embed", "lm_head", "final_norm", "fuse_norm", "attn_norm", "mlp_norm", "wq", "wk_d",
@@ -81,6 +83,12 @@ def lib() -> ctypes.CDLL:
         "dflare_profile_begin": ([vp, ctypes.c_int], ctypes.c_int),
         "dflare_profile_end": ([vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)], ctypes.c_int),
         "dflare_set_option": ([vp, ctypes.c_int, ctypes.c_int], ctypes.c_int),
+        "dflare_fuse_append_batched": ([vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32), vp], ctypes.c_int),
+        "dflare_draft_block_batched": ([vp, i32, ctypes.POINTER(i32), vp, vp], ctypes.c_int),
+        "dflare_truncate_seq": ([vp, i32, i32], ctypes.c_int),
+        "dflare_context_len_seq": ([vp, i32, ctypes.POINTER(i32)], ctypes.c_int),
+        "dflare_debug_read_seq": ([vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float),
+                                   i64], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -112,11 +120,11 @@ def _stream(stream) -> int:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def make_config(cfg, max_context: int, max_new: int = 16) -> dflare_config:
+def make_config(cfg, max_context: int, max_new: int = 16, max_batch: int = 1) -> dflare_config:
     """dflare_config from any object with the model attributes (hidden, n_q_heads, ...)."""
     return dflare_config(cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn, cfg.vocab,
                          cfg.n_draft_layers, cfg.n_target_layers, cfg.block_size, max_context, max_new,
-                         cfg.rope_base, cfg.rms_eps)
+                         cfg.rope_base, cfg.rms_eps, max_batch)
 
 
 def dflare_init(config: dflare_config, weights: dict, fusion_logits, stream=None) -> int:
@@ -144,6 +152,45 @@ def dflare_draft_block_pos(h: int, block_ids: torch.Tensor, positions, draft_tok
     pos = np.ascontiguousarray(np.asarray(positions, dtype=np.int32))
     _check(lib().dflare_draft_block_pos(h, _ptr(block_ids), pos.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                         _ptr(draft_tokens)), h)
+
+
+def _i32_array(values) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(values, dtype=np.int32).reshape(-1))
+
+
+def _i32p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def dflare_fuse_append_batched(h: int, seq, n_new, target_hidden: torch.Tensor) -> None:
+    """Append n_new[i] rows to slot seq[i]; target_hidden is [S, sum(n_new), H], sequence-major rows."""
+    sq, nn = _i32_array(seq), _i32_array(n_new)
+    if sq.size != nn.size:
+        raise ValueError("seq and n_new differ in length")
+    _check(lib().dflare_fuse_append_batched(h, sq.size, _i32p(sq), _i32p(nn), _ptr(target_hidden)), h)
+
+
+def dflare_draft_block_batched(h: int, seq, block_ids: torch.Tensor, draft_tokens: torch.Tensor) -> None:
+    """block_ids / draft_tokens: device int32 [n_seq, B]; row i belongs to slot seq[i]."""
+    sq = _i32_array(seq)
+    _check(lib().dflare_draft_block_batched(h, sq.size, _i32p(sq), _ptr(block_ids), _ptr(draft_tokens)), h)
+
+
+def dflare_truncate_seq(h: int, seq: int, new_len: int) -> None:
+    _check(lib().dflare_truncate_seq(h, int(seq), int(new_len)), h)
+
+
+def dflare_context_len_seq(h: int, seq: int) -> int:
+    out = ctypes.c_int32()
+    _check(lib().dflare_context_len_seq(h, int(seq), ctypes.byref(out)), h)
+    return out.value
+
+
+def dflare_debug_read_seq(h: int, what: int, seq: int, layer: int, shape) -> np.ndarray:
+    out = np.empty(int(np.prod(shape)), dtype=np.float32)
+    _check(lib().dflare_debug_read_seq(h, what, int(seq), layer,
+                                       out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), out.size), h)
+    return out.reshape(shape)
 
 
 def dflare_truncate(h: int, new_len: int) -> None:
@@ -207,9 +254,9 @@ class DraftModel:
     """Owner of one handle: the three calls of the draft step plus helpers."""
 
     def __init__(self, cfg, weights_bits: dict, fusion_logits, max_context: int, max_new: int = 16,
-                 device="cuda", stream=None):
+                 device="cuda", stream=None, max_batch: int = 1):
         self.cfg = cfg
-        self.config = make_config(cfg, max_context, max_new)
+        self.config = make_config(cfg, max_context, max_new, max_batch)
         dev = {k: (None if weights_bits.get(k) is None else bf16_tensor(weights_bits[k], device))
                for k in WEIGHT_FIELDS}
         self.h = dflare_init(self.config, dev, fusion_logits, stream)
@@ -227,6 +274,15 @@ class DraftModel:
 
     def truncate(self, n: int) -> None:
         dflare_truncate(self.h, n)
+
+    def fuse_append_batched(self, seq, n_new, target_hidden: torch.Tensor) -> None:
+        dflare_fuse_append_batched(self.h, seq, n_new, target_hidden)
+
+    def draft_block_batched(self, seq, block_ids: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+        if out is None:
+            out = torch.empty(block_ids.shape, dtype=torch.int32, device=self.device)
+        dflare_draft_block_batched(self.h, seq, block_ids, out)
+        return out
 
     @property
     def context_len(self) -> int:

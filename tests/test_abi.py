@@ -67,6 +67,8 @@ def _init(cfg, logits=None, weights=True):
     ("hidden", 264, dfl.ERR_UNSUPPORTED),
     ("max_new", 0, dfl.ERR_INVALID_ARG),
     ("rope_base", 0.0, dfl.ERR_INVALID_ARG),
+    ("max_batch", 65, dfl.ERR_UNSUPPORTED),
+    ("max_batch", -1, dfl.ERR_UNSUPPORTED),
 ])
 def test_init_rejects_bad_config(L, field, value, code):
     rc, h = _init(_cfg(**{field: value}))
@@ -97,3 +99,10 @@ def test_calls_on_invalid_handles(L):
     assert L.dflare_truncate(0x1234, 0) == dfl.ERR_INVALID_ARG
     assert L.dflare_fuse_append(0x1234, 0x1000, 1) == dfl.ERR_INVALID_ARG
     assert L.dflare_draft_block(None, 0x1000, 0x1000) == dfl.ERR_INVALID_ARG
+    seq = (ctypes.c_int32 * 1)(0)
+    assert L.dflare_fuse_append_batched(0x1234, 1, seq, seq, 0x1000) == dfl.ERR_INVALID_ARG
+    assert L.dflare_draft_block_batched(None, 1, seq, 0x1000, 0x1000) == dfl.ERR_INVALID_ARG
+    assert L.dflare_truncate_seq(0x1234, 0, 0) == dfl.ERR_INVALID_ARG
+    assert L.dflare_context_len_seq(None, 0, ctypes.byref(out)) == dfl.ERR_INVALID_ARG
+    buf = (ctypes.c_float * 4)()
+    assert L.dflare_debug_read_seq(None, dfl.DBG_KCACHE, 0, 0, buf, 4) == dfl.ERR_INVALID_ARG
