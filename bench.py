@@ -36,7 +36,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="qwen3_8b")
+    ap.add_argument("--config", default="qwen3_8b",
+                    help="qwen3_8b (default), qwen3_4b, gpt_oss_20b, or batched (32 ragged sequences)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-context", type=int, default=256,
                     help="context rows of the oracle's timed sample")
@@ -104,6 +105,10 @@ def main():
         print(json.dumps({"error": "this build runs the draft step on one GPU only; "
                                    "bench.py --gpus N with N > 1 is not supported"}), flush=True)
         sys.exit(2)
+
+    if args.config == "batched":
+        bench_batched(args)
+        return
 
     import numpy as np
     import torch
@@ -224,6 +229,152 @@ def main():
         "per_phase_launches": per_phase,
     }
 
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context)
+    print(json.dumps(result), flush=True)
+    model.close()
+
+
+MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 / fp16
+
+
+def bench_batched(args):
+    """Batched serving workload: 32 Qwen3-8B-shaped sequences with ragged contexts
+    (L ~ U{512..4096}) drafted together.  One step = per sequence, truncate by its n_new and
+    append n_new ~ U{1..16} rows (one batched fuse_append), then one batched draft_block:
+    32 draft blocks per step."""
+    import numpy as np
+    import torch
+
+    from paper_2606_02091_amd import dflare as dfl
+    from paper_2606_02091_amd import synth
+
+    spec = synth.BATCHED
+    cfg = synth.CONFIGS[spec["model"]]
+    n_seq = spec["n_seq"]
+    lengths = [int(x) for x in synth.batched_lengths(n_seq, spec["lo"], spec["hi"])]
+    B, S, H, V = cfg.block_size, cfg.n_target_layers, cfg.hidden, cfg.vocab
+    q, kv, F, D = cfg.q_dim, cfg.kv_dim, cfg.ffn, cfg.n_draft_layers
+    torch.cuda.set_device(0)
+    side = torch.cuda.Stream()
+    torch.cuda.set_stream(side)
+    t0 = time.time()
+    w = synth.make_weights(cfg)
+    fusion_logits = w.pop("fusion_logits")
+    print(f"[bench] weights generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+    model = dfl.DraftModel(cfg, w, fusion_logits, max_context=max(lengths) + 16, max_new=16 * n_seq,
+                           max_batch=n_seq)
+    h = model.h
+    # one shared stream of target rows on the device; sequence i reads rows 16 i + (0 .. L_i)
+    base = [16 * i for i in range(n_seq)]
+    R = max(b + L for b, L in zip(base, lengths))
+    rows_dev = dfl.bf16_tensor(synth.hidden_rows(cfg, 0, R))
+    for i, L in enumerate(lengths):
+        for s0 in range(0, L, 512):
+            n = min(512, L - s0)
+            model.fuse_append_batched([i], [n], rows_dev[:, base[i] + s0:base[i] + s0 + n].contiguous())
+    torch.cuda.synchronize()
+    print(f"[bench] {n_seq} contexts prefilled, mean L {np.mean(lengths):.0f}", file=sys.stderr, flush=True)
+
+    seqs = list(range(n_seq))
+    total = args.warmup + args.steps
+    pool = 8
+    sizes = synth.append_sizes(pool * n_seq).reshape(pool, n_seq)
+    inputs = []
+    for k in range(pool):
+        parts = [rows_dev[:, base[i] + lengths[i] - int(sizes[k, i]):base[i] + lengths[i]] for i in seqs]
+        inputs.append(torch.cat(parts, dim=1).contiguous())
+    ids = torch.from_numpy(np.stack([synth.block_ids(cfg, step=0, seed=200 + i) for i in seqs])).cuda()
+    out = torch.empty((n_seq, B), dtype=torch.int32, device="cuda")
+
+    def step(k):
+        nk = sizes[k % pool]
+        for i in seqs:
+            dfl.dflare_truncate_seq(h, i, lengths[i] - int(nk[i]))
+        dfl.dflare_fuse_append_batched(h, seqs, nk, inputs[k % pool])
+        dfl.dflare_draft_block_batched(h, seqs, ids, out)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for k in range(args.warmup, total):
+        step(k)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    print(f"[bench] timed {args.steps} batched steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # per-kind durations (library hipEvents, one kind per pass)
+    M = n_seq * B
+    n_mean = float(sizes.mean()) * n_seq
+    kv_bytes = sum(2 * L * kv * 2 for L in lengths)          # context K and V of one layer, all sequences
+    work = {  # algorithmic (FLOPs, HBM bytes) per launch
+        "qkv": (2 * M * (q + 2 * kv) * H, (q + 2 * kv) * H * 2),
+        "attn": (sum(4 * q * B * (L + B) for L in lengths), kv_bytes),
+        "o": (2 * M * H * q, H * q * 2),
+        "gate_up": (2 * M * 2 * F * H, 2 * F * H * 2),
+        "down": (2 * M * H * F, H * F * 2),
+        "lm_head": (2 * M * V * H, V * H * 2),
+        "kv_t": (2 * n_mean * 2 * kv * H, 2 * kv * H * 2),
+        "epilogues": (0, 0),
+        "fuse": (0, S * n_mean * H * 2),
+        "draft": (0, 0),
+        "append": (0, 0),
+    }
+    kinds = {"qkv": dfl.K_B_QKV, "attn": dfl.K_B_ATTN, "o": dfl.K_B_O, "gate_up": dfl.K_B_GATE_UP,
+             "down": dfl.K_B_DOWN, "lm_head": dfl.K_B_LM_HEAD, "kv_t": dfl.K_B_KV_T, "epilogues": dfl.K_B_EPI,
+             "fuse": dfl.K_B_FUSE, "draft": dfl.K_B_DRAFT, "append": dfl.K_B_APPEND}
+    kern = {}
+    for name, kind in kinds.items():
+        dfl.dflare_profile_begin(h, kind)
+        for k in range(args.profile_steps):
+            step(k)
+        tot, launches = dfl.dflare_profile_end(h)
+        avg_us = 1000.0 * tot / max(launches, 1)
+        fl, by = work[name]
+        kern[name] = {"avg_us": round(avg_us, 3), "launches_per_step": launches / args.profile_steps,
+                      "us_per_step": round(1000.0 * tot / args.profile_steps, 2)}
+        if fl:
+            kern[name]["TFLOPs"] = round(fl / (avg_us * 1e-6) / 1e12, 1)
+            kern[name]["flops_per_launch"] = int(fl)
+        if by:
+            kern[name]["GBs"] = round(by / (avg_us * 1e-6) / 1e9, 1)
+            kern[name]["bytes_per_launch"] = int(by)
+    gemms = ("qkv", "o", "gate_up", "down", "lm_head")
+    dom = max(gemms, key=lambda k: kern[k]["us_per_step"])
+    d = kern[dom]
+    # whole step: every GEMM and the attention, against both roofs
+    step_flops = sum(work[k][0] * kern[k]["launches_per_step"] for k in ("qkv", "attn", "o", "gate_up", "down",
+                                                                          "lm_head", "kv_t"))
+    step_bytes = cfg.block_bytes(0) - B * H * 2 + D * kv_bytes + M * H * 2 + cfg.append_bytes(n_mean)
+    result = {
+        "metric": "draft blocks/sec (B=16, Qwen3-8B shape, batch 32, ragged contexts)",
+        "value": round(1000.0 * n_seq / ms, 1),
+        "unit": "blocks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-shaped draft step for {n_seq} sequences at once: L ~ U{{"
+                               f"{spec['lo']}..{spec['hi']}}} per sequence (mean {np.mean(lengths):.0f}), "
+                               f"n_new ~ U{{1..16}} per sequence per step, B={B}",
+                   "global_batch": n_seq, "seq_len": int(max(lengths)), "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": d["TFLOPs"], "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(d["TFLOPs"] / MFMA_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+                     "flops_per_launch": d["flops_per_launch"], "avg_us": d["avg_us"]},
+        "step_roofline": {"flops_per_step": int(step_flops), "bytes_per_step": int(step_bytes),
+                          "mfma_frac": round(step_flops / (ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS, 4),
+                          "hbm_frac": round(step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "kernels": kern,
+    }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context)
     print(json.dumps(result), flush=True)

@@ -269,7 +269,19 @@ enum { DFLARE_K_QKV = 1,       /* RMSNorm + Q/K^d/V^d projection + RoPE         
        DFLARE_K_LM_HEAD = 6,   /* final RMSNorm + LM head + argmax                 */
        DFLARE_K_FUSE = 7,      /* layer fusion (Eq. 3)                             */
        DFLARE_K_KV_T = 8,      /* context K/V projection + RoPE + append (Eq. 4)   */
-       DFLARE_K_DRAFT = 9 };   /* a whole draft_block, as configured               */
+       DFLARE_K_DRAFT = 9,     /* a whole draft_block, as configured               */
+       /* batched calls */
+       DFLARE_K_B_QKV = 10,    /* Q/K^d/V^d projection GEMM                        */
+       DFLARE_K_B_ATTN = 11,   /* attention over every sequence + combine          */
+       DFLARE_K_B_O = 12,      /* output projection GEMM                           */
+       DFLARE_K_B_GATE_UP = 13,/* gate/up projection GEMM                          */
+       DFLARE_K_B_DOWN = 14,   /* down projection GEMM                             */
+       DFLARE_K_B_LM_HEAD = 15,/* LM-head GEMM with partial argmax + final argmax  */
+       DFLARE_K_B_KV_T = 16,   /* context K/V projection GEMM of an append         */
+       DFLARE_K_B_EPI = 17,    /* embedding, row norms and GEMM epilogues          */
+       DFLARE_K_B_FUSE = 18,   /* layer fusion of an append                        */
+       DFLARE_K_B_DRAFT = 19,  /* a whole dflare_draft_block_batched               */
+       DFLARE_K_B_APPEND = 20 };/* a whole dflare_fuse_append_batched              */
 int dflare_profile_begin(dflare_handle* h, int kind);
 int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches);
 

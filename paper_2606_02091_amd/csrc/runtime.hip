@@ -686,8 +686,8 @@ int check_seqs(dflare_handle* h, int32_t n_seq, const int32_t* seq) {
 }
 
 // Y = A W^T over all rows of a batched call, K split chosen per shape (bounded by the slice buffer)
-int bgemm(dflare_handle* h, const char* name, const u32x4* a_hi, const u32x4* a_lo, int a_kt, const u32x4* w,
-          int Nt, int Kt, int M, BEpiArgs& e) {
+int bgemm(dflare_handle* h, int kind, const char* name, const u32x4* a_hi, const u32x4* a_lo, int a_kt,
+          const u32x4* w, int Nt, int Kt, int M, BEpiArgs& e) {
   BGemmArgs g{};
   g.Ahi = a_hi;
   g.Alo = a_lo;
@@ -702,7 +702,9 @@ int bgemm(dflare_handle* h, const char* name, const u32x4* a_hi, const u32x4* a_
   while (g.kg > 1 && (long)g.kg * g.Mt * 16 * Nt * 16 > h->bY_elems) --g.kg;
   g.Y = h->bY;
   g.ldy = Nt * 16;
+  prof_mark(h, kind, true);
   launch_bgemm(h->stream, g, false);
+  prof_mark(h, kind, false);
   e.Y = h->bY;
   e.kg = g.kg;
   e.Mpad = g.Mt * 16;
@@ -745,17 +747,23 @@ int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int3
     rows.off[i + 1] = rows.off[i] + n_new[i];
   }
   const int N = rows.off[n_seq];
+  prof_mark(h, DFLARE_K_B_FUSE, true);
   launch_fuse(s, (const uint16_t*)hidden, N, S, H, D, h->alpha, h->g_fuse, h->Ustats, h->ua_hi, h->ua_lo, c.max_new,
               h->mt_max);
+  prof_mark(h, DFLARE_K_B_FUSE, false);
   const long ua_layer = (long)h->mt_max * Kt_H * 64;
   for (int l = 0; l < D; ++l) {
+    prof_mark(h, DFLARE_K_B_EPI, true);
     launch_brstd(s, h->Ustats + (long)l * c.max_new * (H / 16), H / 16, N, 1.0f / H, c.rms_eps, h->brstd);
+    prof_mark(h, DFLARE_K_B_EPI, false);
     BEpiArgs e = bepi_base(h);
-    TRY(bgemm(h, "KVT", h->ua_hi + l * ua_layer, h->ua_lo + l * ua_layer, Kt_H, h->w_kvt + l * h->s_kvt,
+    TRY(bgemm(h, DFLARE_K_B_KV_T, "KVT", h->ua_hi + l * ua_layer, h->ua_lo + l * ua_layer, Kt_H, h->w_kvt + l * h->s_kvt,
               2 * h->kv_dim / 16, Kt_H, N, e));
     e.layer = l;
     e.q_tiles = 0;
+    prof_mark(h, DFLARE_K_B_EPI, true);
     launch_bepi(s, BEPI_QKV, e, rows);
+    prof_mark(h, DFLARE_K_B_EPI, false);
   }
   if (h->debug) {
     launch_fused_rows(s, h->ua_hi, h->ua_lo, h->Ustats, N, H, D, c.max_new, h->mt_max, c.rms_eps, h->dbg_fused);
@@ -798,36 +806,52 @@ int run_draft_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int
   at.ML = h->bML;
   const float inv_H = 1.0f / H;
 
+  prof_mark(h, DFLARE_K_B_EPI, true);
   launch_bembed(s, h->embed, ids, M, H, V, h->g_attn, h->bX, h->bstats, h->bA, h->bA + h->bA_plane, Kt_H);
+  prof_mark(h, DFLARE_K_B_EPI, false);
   for (int l = 0; l < D; ++l) {
+    prof_mark(h, DFLARE_K_B_EPI, true);
     launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
+    prof_mark(h, DFLARE_K_B_EPI, false);
     BEpiArgs e = bepi_base(h);
-    TRY(bgemm(h, "QKV", h->bA, h->bA + h->bA_plane, Kt_H, h->w_qkv + l * h->s_qkv, Nt_qkv, Kt_H, M, e));
+    TRY(bgemm(h, DFLARE_K_B_QKV, "QKV", h->bA, h->bA + h->bA_plane, Kt_H, h->w_qkv + l * h->s_qkv, Nt_qkv, Kt_H, M, e));
     e.layer = l;
+    prof_mark(h, DFLARE_K_B_EPI, true);
     launch_bepi(s, BEPI_QKV, e, rows);
+    prof_mark(h, DFLARE_K_B_EPI, false);
     at.layer = l;
+    prof_mark(h, DFLARE_K_B_ATTN, true);
     launch_battn(s, hd, at, rows, items);
     launch_bcomb(s, hd, at, rows, h->bOA, h->bOA + h->bOA_plane, Kt_q);
-    TRY(bgemm(h, "O", h->bOA, h->bOA + h->bOA_plane, Kt_q, h->w_o + l * h->s_o, Nt_H, Kt_q, M, e));
+    prof_mark(h, DFLARE_K_B_ATTN, false);
+    TRY(bgemm(h, DFLARE_K_B_O, "O", h->bOA, h->bOA + h->bOA_plane, Kt_q, h->w_o + l * h->s_o, Nt_H, Kt_q, M, e));
     e.gain = h->g_mlp + (long)l * H;
     e.ahi = h->bA;
     e.alo = h->bA + h->bA_plane;
     e.a_kt = Kt_H;
+    prof_mark(h, DFLARE_K_B_EPI, true);
     launch_bepi(s, BEPI_RESID, e, rows);
     launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
-    TRY(bgemm(h, "GU", h->bA, h->bA + h->bA_plane, Kt_H, h->w_gu + l * h->s_gu, Nt_gu, Kt_H, M, e));
+    prof_mark(h, DFLARE_K_B_EPI, false);
+    TRY(bgemm(h, DFLARE_K_B_GATE_UP, "GU", h->bA, h->bA + h->bA_plane, Kt_H, h->w_gu + l * h->s_gu, Nt_gu, Kt_H, M, e));
     e.ahi = h->bHA;
     e.alo = h->bHA + h->bHA_plane;
     e.a_kt = Kt_F;
+    prof_mark(h, DFLARE_K_B_EPI, true);
     launch_bepi(s, BEPI_SWIGLU, e, rows);
-    TRY(bgemm(h, "DOWN", h->bHA, h->bHA + h->bHA_plane, Kt_F, h->w_down + l * h->s_down, Nt_H, Kt_F, M, e));
+    prof_mark(h, DFLARE_K_B_EPI, false);
+    TRY(bgemm(h, DFLARE_K_B_DOWN, "DOWN", h->bHA, h->bHA + h->bHA_plane, Kt_F, h->w_down + l * h->s_down, Nt_H, Kt_F, M, e));
     e.gain = (l + 1 < D) ? h->g_attn + (long)(l + 1) * H : h->g_final;
     e.ahi = h->bA;
     e.alo = h->bA + h->bA_plane;
     e.a_kt = Kt_H;
+    prof_mark(h, DFLARE_K_B_EPI, true);
     launch_bepi(s, BEPI_RESID, e, rows);
+    prof_mark(h, DFLARE_K_B_EPI, false);
   }
+  prof_mark(h, DFLARE_K_B_EPI, true);
   launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
+  prof_mark(h, DFLARE_K_B_EPI, false);
   BGemmArgs g{};
   g.Ahi = h->bA;
   g.Alo = h->bA + h->bA_plane;
@@ -845,8 +869,10 @@ int run_draft_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int
   g.pmax = h->bpmax;
   g.pidx = h->bpidx;
   g.pld = h->b_mt * 16;
+  prof_mark(h, DFLARE_K_B_LM_HEAD, true);
   launch_bgemm(s, g, true);
   launch_bargmax(s, h->bpmax, h->bpidx, ceil_div(Nt_lm, kBN), g.pld, M, out);
+  prof_mark(h, DFLARE_K_B_LM_HEAD, false);
   if (h->debug) h->dbg_blogits_rows = M;
   return check_launch(h, "draft_block_batched");
 }
@@ -984,7 +1010,10 @@ int dflare_fuse_append_batched(dflare_handle* h, int32_t n_seq, const int32_t* s
   for (int i = 0; i < n_seq; ++i)
     if ((long)h->Ls[seq[i]] + n_new[i] > h->cfg.max_context)
       return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
-  return run_fuse_batched(h, n_seq, seq, n_new, target_hidden);
+  prof_mark(h, DFLARE_K_B_APPEND, true);
+  const int rc = run_fuse_batched(h, n_seq, seq, n_new, target_hidden);
+  prof_mark(h, DFLARE_K_B_APPEND, false);
+  return rc;
 }
 
 int dflare_draft_block_batched(dflare_handle* h, int32_t n_seq, const int32_t* seq, const int32_t* block_ids,
@@ -992,7 +1021,10 @@ int dflare_draft_block_batched(dflare_handle* h, int32_t n_seq, const int32_t* s
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
   TRY(check_seqs(h, n_seq, seq));
   if (!block_ids || !draft_tokens) return fail(h, DFLARE_ERR_INVALID_ARG, "block_ids / draft_tokens is NULL");
-  return run_draft_batched(h, n_seq, seq, block_ids, draft_tokens);
+  prof_mark(h, DFLARE_K_B_DRAFT, true);
+  const int rc = run_draft_batched(h, n_seq, seq, block_ids, draft_tokens);
+  prof_mark(h, DFLARE_K_B_DRAFT, false);
+  return rc;
 }
 
 int dflare_truncate_seq(dflare_handle* h, int32_t seq, int32_t new_len) {
@@ -1161,7 +1193,7 @@ int dflare_debug_read_seq(dflare_handle* h, int what, int seq, int layer, float*
 
 int dflare_profile_begin(dflare_handle* h, int kind) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
-  if (kind < 0 || kind > DFLARE_K_DRAFT) return fail(h, DFLARE_ERR_INVALID_ARG, "unknown kernel kind");
+  if (kind < 0 || kind > DFLARE_K_B_APPEND) return fail(h, DFLARE_ERR_INVALID_ARG, "unknown kernel kind");
   h->prof_kind = kind;
   h->prof_n = 0;
   return DFLARE_OK;

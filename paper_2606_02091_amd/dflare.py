@@ -29,6 +29,8 @@ EXPORTED = (
     "dflare_context_len_seq", "dflare_debug_read_seq",
 )
 K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T, K_DRAFT = range(1, 10)
+(K_B_QKV, K_B_ATTN, K_B_O, K_B_GATE_UP, K_B_DOWN, K_B_LM_HEAD, K_B_KV_T, K_B_EPI, K_B_FUSE, K_B_DRAFT,
+ K_B_APPEND) = range(10, 21)
 
 
 class DFlareError(RuntimeError):

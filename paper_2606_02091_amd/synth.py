@@ -29,7 +29,7 @@ import numpy as np
 
 __all__ = [
     "ModelConfig", "CONFIGS", "round_bf16", "bf16_to_f32", "make_weights",
-    "hidden_rows", "append_sizes", "block_ids", "WEIGHT_KINDS",
+    "hidden_rows", "append_sizes", "block_ids", "WEIGHT_KINDS", "BATCHED", "batched_lengths",
 ]
 
 
@@ -220,3 +220,14 @@ def block_ids(cfg: ModelConfig, step: int = 0, seed: int = 3) -> np.ndarray:
     ids = np.full(cfg.block_size, cfg.vocab - 1, np.int32)
     ids[0] = rng.integers(0, cfg.vocab - 1)
     return ids
+
+
+# Batched serving workload: n_seq sequences of the Qwen3-8B-shaped draft drafted together,
+# ragged context lengths, each sequence appending U{1..16} accepted rows per step.
+BATCHED = {"model": "qwen3_8b", "n_seq": 32, "lo": 512, "hi": 4096}
+
+
+def batched_lengths(n_seq: int = 32, lo: int = 512, hi: int = 4096, seed: int = 4) -> np.ndarray:
+    """Context length of each sequence of the batched workload, uniform on {lo..hi}."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.integers(lo, hi + 1, size=n_seq).astype(np.int32)

@@ -84,3 +84,61 @@ def test_fullsize_parity(name):
             ids = synth.block_ids(cfg, step=step + 1)
             ids_t = torch.from_numpy(ids).cuda()
         model.close()
+
+
+@pytest.mark.timeout(900)
+def test_fullsize_batched():
+    """The batched workload at full size: 32 Qwen3-8B-shaped sequences with ragged contexts
+    (L ~ U{512..4096}), prefilled and drafted as bench.py --config batched does.  The oracle
+    checks the shortest sequence (its whole cache, logits and tokens); every sequence is
+    checked against drafting it alone (n_seq = 1), to the batch-1 agreement bound of the
+    batched parity tests; debug capture must not change any token."""
+    spec = synth.BATCHED
+    cfg = synth.CONFIGS[spec["model"]]
+    n_seq = spec["n_seq"]
+    lengths = [int(x) for x in synth.batched_lengths(n_seq, spec["lo"], spec["hi"])]
+    B, V = cfg.block_size, cfg.vocab
+    print(f"[fullsize] batched: generating weights", flush=True)
+    w, lg = P.weights_for(cfg)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        model = dfl.DraftModel(cfg, w, lg, max_context=max(lengths) + 16, max_new=16 * n_seq, max_batch=n_seq)
+        base = [16 * i for i in range(n_seq)]
+        rows_dev = dfl.bf16_tensor(synth.hidden_rows(cfg, 0, max(b + L for b, L in zip(base, lengths))))
+        for i, L in enumerate(lengths):
+            for s0 in range(0, L, 512):
+                n = min(512, L - s0)
+                model.fuse_append_batched([i], [n], rows_dev[:, base[i] + s0:base[i] + s0 + n].contiguous())
+        side.synchronize()
+        print(f"[fullsize] batched: {n_seq} contexts appended", flush=True)
+        seqs = list(range(n_seq))
+        ids = np.stack([synth.block_ids(cfg, step=0, seed=200 + i) for i in seqs])
+        ids_t = torch.from_numpy(ids).cuda()
+        out = model.draft_block_batched(seqs, ids_t)
+        side.synchronize()
+        plain = out.cpu().numpy().copy()
+        dfl.dflare_debug_capture(model.h, True)
+        dbg = model.draft_block_batched(seqs, ids_t).cpu().numpy()
+        side.synchronize()
+        assert np.array_equal(plain, dbg)
+        logits = dfl.dflare_debug_read(model.h, dfl.DBG_BLOGITS, 0, (n_seq, B, V))
+        for i in seqs:
+            one = model.draft_block_batched([i], ids_t[i:i + 1]).cpu().numpy()[0]
+            z = dfl.dflare_debug_read(model.h, dfl.DBG_BLOGITS, 0, (1, B, V))[0]
+            assert P.relinf(z, logits[i]) <= 2e-3, i
+            P.check_tokens(one, logits[i])
+        print(f"[fullsize] batched: every sequence agrees with drafting it alone", flush=True)
+        j = int(np.argmin(lengths))
+        orc = P.oracle_for(cfg, w, lg, lengths[j] + 64)
+        orc.append(synth.hidden_rows(cfg, base[j], lengths[j]))
+        for i in range(cfg.n_draft_layers):
+            for what, ref in ((dfl.DBG_KCACHE, orc.k_cache[i]), (dfl.DBG_VCACHE, orc.v_cache[i])):
+                got = dfl.dflare_debug_read_seq(model.h, what, j, i, (lengths[j], cfg.n_kv_heads, cfg.head_dim))
+                assert P.relinf(got, ref) <= P.REL_TOL, (i, what)
+        ref = orc.draft_block(ids[j])
+        e = P.relinf(logits[j], ref["logits"])
+        assert e <= P.REL_TOL, e
+        stats = P.check_tokens(dbg[j], ref["logits"])
+        print(f"[fullsize] batched: sequence {j} (L {lengths[j]}) logits rel err {e:.2e} tokens {stats}",
+              flush=True)
+        model.close()
