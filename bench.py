@@ -318,7 +318,7 @@ def bench_batched(args):
         "gate_up": (2 * M * 2 * F * H, 2 * F * H * 2),
         "down": (2 * M * H * F, H * F * 2),
         "lm_head": (2 * M * V * H, V * H * 2),
-        "kv_t": (2 * n_mean * 2 * kv * H, 2 * kv * H * 2),
+        "kv_t": (D * 2 * n_mean * 2 * kv * H, D * 2 * kv * H * 2),  # one launch for every layer
         "epilogues": (0, 0),
         "fuse": (0, S * n_mean * H * 2),
         "draft": (0, 0),

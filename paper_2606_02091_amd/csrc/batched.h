@@ -7,11 +7,18 @@
 
 namespace dflare {
 
-constexpr int kBM = 8;        // 16-row m-tiles per GEMM work-group (128 rows)
-constexpr int kBN = 8;        // 16-column n-tiles per GEMM work-group (128 columns)
-constexpr int kMaxSeq = 64;   // sequences in one batched call
+constexpr int kBWaves = 4;               // GEMM work-group: 4 waves
+constexpr int kBWavesPerSimd = 2;        // GEMM work-groups resident per CU (waves per SIMD)
+constexpr int kBPrefetch = 3;            // k-tiles of GEMM operand loads in flight per wave
+constexpr int kBM = 8;                   // m-tiles per work-group (128 rows); every wave covers all of them
+constexpr int kBNW = 4;                  // n-tiles per wave (64 columns)
+constexpr int kBN = kBWaves * kBNW;      // n-tiles per work-group (256 columns)
+constexpr int kMaxSeq = 64;              // sequences in one batched call
+constexpr int kBSplitMax = 8;            // K parts of one batched GEMM output tile
+constexpr long kBPartFloats = (long)kBWaves * kBM * kBNW * 256;  // one work-group's partial tile
+constexpr int kBCounters = 4096;         // split-K arrival counters (output tiles of one launch)
 
-enum BEpi { BEPI_QKV = 0, BEPI_RESID = 1, BEPI_SWIGLU = 2 };
+enum BEpi { BEPI_QKV = 0, BEPI_RESID = 1, BEPI_SWIGLU = 2, BEPI_ARGMAX = 3 };
 
 // Rows of one batched call, passed by value: call sequence i (cache slot seq[i], context
 // length L[i]) owns rows off[i] .. off[i+1]-1 of the call's activations; its attention work
@@ -24,50 +31,41 @@ struct BRows {
   int ipfx[kMaxSeq + 1];
 };
 
-// Y = A W^T.  A: hi/lo bf16 A fragments [Mt][a_kt][64]; W: packed tiles [Nt][Kt][64].
-// Grid: n-groups of kBN tiles x m-groups of kBM tiles x kg K parts, as one dimension.
+// Y = A W^T with a fused epilogue.  A: fp16 A fragments [layers][Mt][Kt][64 lanes x 16 B]
+// (the MFMA A-operand layout of the activations, one plane); W: packed weight tiles in
+// fp16 [layers][Nt][Kt][64].  Work-group = (layer, K part,
+// 256-column n-group, 128-row m-group); with kg > 1 the K parts of a tile leave fp32
+// partial tiles and the last to arrive sums them in K order and runs the epilogue.
 struct BGemmArgs {
-  const u32x4* Ahi;
-  const u32x4* Alo;
-  int a_kt;
+  const u32x4* A;
+  long a_layer;   // u32x4 units between layers
   const u32x4* W;
-  int Nt, Kt;
-  const u32x4* zero;  // one zero fragment (64 lanes x 16 bytes)
-  int Mt, M, kg;
-  // plain output: fp32 slices Y[kg][Mt * 16][ldy]
-  float* Y;
-  int ldy;
-  // LM head: row scale, optional logits [M, V], best (logit, id) per (n-group, row)
-  const float* rstd;
-  float* logits;
-  int V;
-  float* pmax;
-  int* pidx;
-  int pld;
-};
-
-// Epilogue of a GEMM: sums the kg slices in order, then per operator (see BEpi).
-struct BEpiArgs {
-  const float* Y;
-  int kg, Mpad, ldy;
-  int M, N, H;
-  const float* rstd;  // row scale (QKV, SWIGLU)
-  // RESID: residual stream [M, H] += Y; sums of squares [M][H/16] of the new rows
-  float* X;
-  float* stats;
-  const float* gain;  // gain of the next RMSNorm (RESID)
-  // A fragments written (RESID: x * gain, SWIGLU: the MLP hidden rows)
-  u32x4* ahi;
-  u32x4* alo;
-  int a_kt;
-  // QKV: rotated queries [M, q_dim]; keys and values to the rows' caches
+  long w_layer;
+  int Nt, Kt, Mt, M, kg, layers;
+  const u32x4* zero;   // one zero fragment
+  float* part;         // partial tiles [tiles][kg][kBPartFloats]
+  unsigned* cnt;       // arrival counters [tiles], 32 words apart, zero between launches
+  // QKV (block rows) and KVT (appended context rows): queries [M, q_dim] fp32; keys and
+  // values (fp16) to the rows' sequence caches at their slots; RoPE at the slot position
   float* Q;
   int q_dim;
   uint16_t* kc;
   uint16_t* vt;
   long seq_stride, cache_layer;
-  int layer, Lcap, hd, q_tiles, kv_tiles;
+  int layer0, Lcap, hd, q_tiles, kv_tiles;
   const float2* rope;
+  // RESID: residual stream X [M, H] += Y
+  float* X;
+  int H;
+  // SWIGLU: fp16 A fragments of the MLP hidden rows [Mt][out_kt][64]
+  u32x4* out16;
+  int out_kt;
+  // ARGMAX: optional logits [M, V]; best (logit, id) per (n-group, row)
+  float* logits;
+  int V;
+  float* pmax;
+  int* pidx;
+  int pld;
 };
 
 struct BAttnArgs {
@@ -81,14 +79,21 @@ struct BAttnArgs {
   float2* ML;   // [items][Rpad] (max, sum), log2 domain
 };
 
-void launch_bgemm(hipStream_t s, const BGemmArgs& g, bool argmax);
-int bgemm_groups(int Nt, int Mt);  // work-groups of one K part
+int bgemm_groups(int Nt, int Mt);  // output tiles of one layer
+// n 16-byte slots of packed bf16 weight tiles -> fp16 (same layout)
+void launch_tiles_to_f16(hipStream_t s, u32x4* dst, const u32x4* src, long n);
+void launch_bgemm(hipStream_t s, int epi, const BGemmArgs& g, const BRows& rows);
 void launch_bargmax(hipStream_t s, const float* pmax, const int* pidx, int ngroups, int pld, int M, int* tokens);
-void launch_brstd(hipStream_t s, const float* stats, int n_st, int M, float inv_dim, float eps, float* rstd);
-void launch_bembed(hipStream_t s, const uint16_t* embed, const int32_t* ids, int M, int H, int V,
-                   const float* gain, float* X, float* stats, u32x4* ahi, u32x4* alo, int a_kt);
-void launch_bepi(hipStream_t s, int kind, const BEpiArgs& e, const BRows& rows);
+// RMSNorm of rows of X (or of embedding rows) into fp16 A fragments
+void launch_bnorm(hipStream_t s, const float* X, int M, int H, const float* gain, float eps, u32x4* A, int a_kt);
+void launch_bembed_norm(hipStream_t s, const uint16_t* embed, const int32_t* ids, int M, int H, int V,
+                        const float* gain, float eps, float* X, u32x4* A, int a_kt);
+// layer fusion (Eq. 3) of N appended rows for every draft layer, normalised, into fp16 A
+// fragments [D][mt_max][H/32][64]
+void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int S, int H, int D, const float* alpha,
+                  const float* gain, float eps, u32x4* A, int mt_max);
+void launch_bfrag_rows(hipStream_t s, const u32x4* A, int n, int H, int D, int mt_max, float* out);
 void launch_battn(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, int items);
-void launch_bcomb(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, u32x4* ohi, u32x4* olo, int a_kt);
+void launch_bcomb(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, u32x4* out16, int a_kt);
 
 }  // namespace dflare

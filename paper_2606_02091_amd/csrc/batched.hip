@@ -1,11 +1,18 @@
 // Batched draft step: many sequences share the draft weights, each with its own context
 // cache (Sec. 3.2 drafting pass, Eq. 3 and Eq. 4, applied to every sequence).  The
 // M = n_seq * B block rows of a call go through the draft layers together, so the
-// projections are real GEMMs: tiles of 128 x 128 outputs staged through LDS on the matrix
-// cores, optionally split over K into fp32 slices, followed by an epilogue kernel per
-// operator (RoPE and cache store, residual and norm statistics, SwiGLU, argmax).  Numerics
-// match the batch-1 path: bf16 weights against hi/lo bf16 activations, fp32 accumulation,
-// fp16 KV cache, fp16 hi/lo queries and probabilities in attention.
+// projections are GEMMs with M up to 1024 rows, bound by the matrix cores rather than by
+// the weight stream.
+//
+// Precision.  GEMM operands are fp16 on the fp16 matrix cores with fp32 accumulation: the
+// activations enter as normalised fp16 rows (RMSNorm applied before the GEMM, saturated
+// to +-65504), the weights as an fp16 copy of the packed bf16 tiles made once (exact for
+// every weight of magnitude in [2^-14, 65504]; smaller ones keep an absolute error below
+// 2^-25).  The KV cache is fp16 and attention computes as on the batch-1 path (fp16
+// hi/lo queries and probabilities).  One fp16 operand plane does half the matrix-core
+// work of the batch-1 path's bf16 hi/lo pair, which matters here because these GEMMs are
+// compute bound; its rounding (2^-11 relative) keeps the logits within about 1e-3 of
+// the exact values.
 #include <math.h>
 
 #include "batched.h"
@@ -13,175 +20,326 @@
 
 namespace dflare {
 
-constexpr int kBT = 512;  // GEMM work-group: 8 waves
-constexpr int kBK = 2;    // k-tiles per LDS stage
-constexpr int kBF = 2 * kBM * kBK + kBN * kBK;  // fragments per stage: A hi/lo, then W
-static_assert(kBF % 8 == 0, "fragments split evenly over the waves");
+constexpr int kBT = kBWaves * 64;
+
+// fp16 bits of x, round to nearest even, no saturation (weights)
+__device__ __forceinline__ uint32_t f2h_raw(float x) { return __builtin_bit_cast(uint16_t, (_Float16)x); }
+
+// two floats -> packed fp16 pair (saturated), element order low then high
+__device__ __forceinline__ uint32_t pack_h2(float a, float b) { return (uint32_t)f2h(a) | ((uint32_t)f2h(b) << 16); }
+
+// 8 bf16 values (one B-operand lane slot) -> 8 fp16 values
+__device__ __forceinline__ u32x4 bf16x8_to_f16x8(u32x4 v) {
+  u32x4 r;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float lo = __uint_as_float(v[e] << 16), hi = __uint_as_float(v[e] & 0xFFFF0000u);
+    r[e] = f2h_raw(lo) | (f2h_raw(hi) << 16);
+  }
+  return r;
+}
+
+// packed bf16 weight tiles -> the same tiles in fp16 (one 16-byte lane slot per thread)
+__global__ void k_tiles_to_f16(u32x4* dst, const u32x4* src, long n) {
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
+    dst[i] = bf16x8_to_f16x8(src[i]);
+}
+
+// 8 floats -> one 16-byte fp16 A-fragment slot (saturated)
+__device__ __forceinline__ u32x4 pack_h8(const float* v) {
+  return u32x4{pack_h2(v[0], v[1]), pack_h2(v[2], v[3]), pack_h2(v[4], v[5]), pack_h2(v[6], v[7])};
+}
+
+// deterministic sum over a work-group of 256 threads (fixed shuffle and wave order)
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) v += __shfl_xor(v, off);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
 
 // ------------------------------------------------------------------------------------------
-// GEMM: Y = A W^T for A given as hi/lo bf16 fragments [mt][a_kt][64] and W packed
-// [nt][Kt][64].  Work-group (n-group ng, m-group mg, K part kz): 8 m-tiles x 8 n-tiles of
-// output over k-tiles [kb, ke).  Wave w computes m-tiles 2 (w & 3) + {0, 1} against n-tiles
-// 4 (w >> 2) + {0 .. 3}.  Stages of kBK k-tiles are copied global -> registers -> LDS
-// (double buffered, one barrier per stage); every fragment is a contiguous 1 KiB block read
-// back by lane l at l * 16 bytes, so LDS accesses are conflict-free.  A fragments of
-// m-tiles >= Mt or k-tiles >= ke read a zero fragment; W tiles past the matrix are clamped
-// (their outputs are dropped).
+// GEMM.  Work-group: 4 waves; output tile 128 rows x 256 columns, wave w owning columns
+// 64 w .. 64 w + 63 for all 128 rows (8 x 4 MFMA tiles, 128 accumulators per lane); two
+// work-groups share a CU (two waves per SIMD), so one wave's MFMAs run while the other
+// waits for LDS or the barrier.  Per k-tile (32 deep) a wave reads its 4 weight
+// fragments straight from memory (each a coalesced 1 KiB load of its own columns, used
+// directly as MFMA operands; the work-groups of the other m-groups of the same columns
+// run on the same XCD and meet in its L2) and loads 2 of the 8 A fragments, which go
+// through a 2-slot LDS ring so that every wave reads all 8 with one barrier per k-tile.
+// The loads of k-tile t + P are issued after the MFMAs of k-tile t; they are never
+// skipped (past the last k-tile they repeat it), so the compiler can wait for exactly the
+// loads a step needs.
 // ------------------------------------------------------------------------------------------
-template <bool ARGMAX>
-__global__ __launch_bounds__(kBT) void k_bgemm(BGemmArgs g) {
-  __shared__ u32x4 st[2][kBF * 64];
+template <int EPI>
+__global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerSimd, kBWavesPerSimd))) void k_bgemm(
+    BGemmArgs g, BRows rows) {
+  constexpr int P = kBPrefetch;
+  __shared__ u32x4 sa[2][kBM * 64];
+  __shared__ int s_slot[kBM * 16];
+  __shared__ long s_cache[kBM * 16];
+  __shared__ float s_bv[kBWaves][kBM * 16];
+  __shared__ int s_bi[kBWaves][kBM * 16];
+  __shared__ int s_last;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wm = w & 3, wn = w >> 2;
-  // Work-groups are dispatched to the 8 XCDs in turn (id % 8).  The m-groups of one
-  // (n-group, K part) read the same weight tiles, so they are given consecutive ids
-  // on one XCD and meet in its L2.
+  const int quad = lane >> 4, col = lane & 15;
+
+  // work-group -> (layer, K part, n-group, m-group).  Work-groups go to the 8 XCDs in
+  // turn (id % 8); the m-groups of one (layer, K part, n-group) read the same weight
+  // tiles, so they get consecutive ids on one XCD.
   const int Ng = (g.Nt + kBN - 1) / kBN, Mg = (g.Mt + kBM - 1) / kBM;
-  const int nb = Ng * Mg * g.kg;
+  const int nb = Ng * Mg * g.kg * g.layers;
   const int bid = blockIdx.x;
   const int t = (nb % 8 == 0) ? (bid % 8) * (nb / 8) + bid / 8 : bid;
-  const int mg = t % Mg, ng = (t / Mg) % Ng, kz = t / (Mg * Ng);
+  const int mg = t % Mg, ng = (t / Mg) % Ng, kz = (t / (Mg * Ng)) % g.kg, layer = t / (Mg * Ng * g.kg);
+  const int tile = (layer * Ng + ng) * Mg + mg;
   const int kb = (int)((long)kz * g.Kt / g.kg), ke = (int)((long)(kz + 1) * g.Kt / g.kg);
-  const int nst = (ke - kb + kBK - 1) / kBK;
+  const int nk = ke - kb;
 
-  // fragment f of a stage: f < 2*kBM*kBK: A (k = f / (2 kBM), m = (f / 2) % kBM, plane f % 2);
-  // else W (k = (f - A) / kBN, n = (f - A) % kBN).  Wave w copies fragments w, w + 8, ...
-  constexpr int FA = 2 * kBM * kBK, PERW = kBF / 8;
-  auto src = [&](int f, int s) -> const u32x4* {
-    if (f < FA) {
-      const int k = f / (2 * kBM), m = (f / 2) % kBM, pl = f & 1;
-      const int mt = mg * kBM + m, kt = kb + s * kBK + k;
-      if (mt >= g.Mt || kt >= ke) return g.zero + lane;
-      return (pl ? g.Alo : g.Ahi) + ((long)mt * g.a_kt + kt) * 64 + lane;
-    }
-    const int f2 = f - FA, k = f2 / kBN, n = f2 % kBN;
-    const int nt = min(ng * kBN + n, g.Nt - 1), kt = min(kb + s * kBK + k, g.Kt - 1);
-    return g.W + ((long)nt * g.Kt + kt) * 64 + lane;
-  };
-  u32x4 ld[PERW];
-  auto fetch = [&](int s) {
+  const u32x4* A = g.A + layer * g.a_layer;
+  const u32x4* W = g.W + layer * g.w_layer;
+  const int nt0 = ng * kBN + w * kBNW;
+  const u32x4* wp[kBNW];
 #pragma unroll
-    for (int i = 0; i < PERW; ++i) ld[i] = *src(w + 8 * i, s);
-  };
-  auto stash = [&](int buf) {
+  for (int n = 0; n < kBNW; ++n) wp[n] = W + ((long)min(nt0 + n, g.Nt - 1) * g.Kt + kb) * 64 + lane;
+  const u32x4* ap[2];
+  int astep[2];
 #pragma unroll
-    for (int i = 0; i < PERW; ++i) st[buf][(w + 8 * i) * 64 + lane] = ld[i];
-  };
-
-  f32x4 acc[2][4];
-#pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  if (nst > 0) {
-    fetch(0);
-    stash(0);
-    __syncthreads();
-    if (nst > 1) fetch(1);
+  for (int j = 0; j < 2; ++j) {
+    const int mt = mg * kBM + 2 * w + j;
+    const bool ok = mt < g.Mt;
+    ap[j] = ok ? A + ((long)mt * g.Kt + kb) * 64 + lane : g.zero + lane;
+    astep[j] = ok ? 64 : 0;
   }
-  for (int s = 0; s < nst; ++s) {
-    const u32x4* sb = st[s & 1];
+  const int klast = max(nk - 1, 0);
+
+  f32x4 acc[kBM][kBNW];
 #pragma unroll
-    for (int k = 0; k < kBK; ++k) {
-      u32x4 ah[2], al[2], wv[4];
+  for (int m = 0; m < kBM; ++m)
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi) {
-        const int m = 2 * wm + mi;
-        ah[mi] = sb[(k * 2 * kBM + 2 * m) * 64 + lane];
-        al[mi] = sb[(k * 2 * kBM + 2 * m + 1) * 64 + lane];
+    for (int n = 0; n < kBNW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto kidx = [&](int i) -> long { return min(i, klast); };
+  if (nk > 0) {
+    u32x4 wr[P][kBNW], ar[P][2];
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+      const long kt = kidx(j);
+#pragma unroll
+      for (int n = 0; n < kBNW; ++n) wr[j][n] = wp[n][kt * 64];
+      ar[j][0] = ap[0][kt * astep[0]];
+      ar[j][1] = ap[1][kt * astep[1]];
+    }
+    for (int t0 = 0; t0 < nk; t0 += P) {
+#pragma unroll
+      for (int j = 0; j < P; ++j) {
+        const int tk = t0 + j;
+        // slot tk % 2 was last read at k-tile tk - 2, before the barrier of k-tile tk - 1
+        u32x4* slot = sa[tk & 1];
+        slot[(2 * w) * 64 + lane] = ar[j][0];
+        slot[(2 * w + 1) * 64 + lane] = ar[j][1];
+        __syncthreads();
+        if (tk < nk) {
+#pragma unroll
+          for (int m = 0; m < kBM; ++m) {
+            const u32x4 a = slot[m * 64 + lane];
+#pragma unroll
+            for (int n = 0; n < kBNW; ++n) acc[m][n] = mfma_h(a, wr[j][n], acc[m][n]);
+          }
+        }
+        const long kt = kidx(tk + P);
+#pragma unroll
+        for (int n = 0; n < kBNW; ++n) wr[j][n] = wp[n][kt * 64];
+        ar[j][0] = ap[0][kt * astep[0]];
+        ar[j][1] = ap[1][kt * astep[1]];
       }
+    }
+  }
+
+  if (g.kg > 1) {
+    // split K: leave this part's tile, then the last part to arrive sums all parts in K order
+    // (each 1 KiB block: elements 0-1 of the 64 lanes, then elements 2-3, so that every
+    // 8-byte store or load instruction covers 512 contiguous bytes)
+    float* mine = g.part + (((long)tile * g.kg + kz) * kBWaves + w) * (kBM * kBNW * 256);
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) wv[ni] = sb[(FA + k * kBN + 4 * wn + ni) * 64 + lane];
+    for (int m = 0; m < kBM; ++m)
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
+      for (int n = 0; n < kBNW; ++n) {
+        float* blk = mine + (m * kBNW + n) * 256;
+        const u32x4 v = __builtin_bit_cast(u32x4, acc[m][n]);
+        st_wt8(blk + lane * 2, (uint64_t)v[0] | ((uint64_t)v[1] << 32));
+        st_wt8(blk + 128 + lane * 2, (uint64_t)v[2] | ((uint64_t)v[3] << 32));
+      }
+    wait_vm();
+    __syncthreads();
+    if (tid == 0) {
+      const unsigned old = __hip_atomic_fetch_add(g.cnt + tile * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_last = old == (unsigned)(g.kg - 1);
+    }
+    __syncthreads();
+    if (!s_last) return;
+    if (tid == 0) st_wt(g.cnt + tile * 32, 0u);
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
-          acc[mi][ni] = mfma(ah[mi], wv[ni], acc[mi][ni]);
-          acc[mi][ni] = mfma(al[mi], wv[ni], acc[mi][ni]);
+    for (int m = 0; m < kBM; ++m)
+#pragma unroll
+      for (int n = 0; n < kBNW; ++n) {
+        f32x4 s = {0.f, 0.f, 0.f, 0.f};
+        for (int z = 0; z < g.kg; ++z) {
+          const float* blk = g.part + (((long)tile * g.kg + z) * kBWaves + w) * (kBM * kBNW * 256) +
+                             (m * kBNW + n) * 256;
+          if (z == kz) {
+            s += acc[m][n];
+          } else {
+            const float2 lo = ld_coh2(blk + lane * 2), hi = ld_coh2(blk + 128 + lane * 2);
+            s += f32x4{lo.x, lo.y, hi.x, hi.y};
+          }
+        }
+        acc[m][n] = s;
+      }
+  }
+
+  const int row0 = mg * kBM * 16;
+  if constexpr (EPI == BEPI_QKV) {
+    // rows -> cache slot and cache base of their sequence
+    if (tid < kBM * 16) {
+      const int row = min(row0 + tid, g.M - 1);
+      int i = 0;
+      while (i + 1 < rows.n_seq && row >= rows.off[i + 1]) ++i;
+      s_slot[tid] = rows.L[i] + (row - rows.off[i]);
+      s_cache[tid] = (long)rows.seq[i] * g.seq_stride + (long)(g.layer0 + layer) * g.cache_layer;
+    }
+    __syncthreads();
+    const int tph = g.hd / 16, half = g.hd / 2;
+#pragma unroll
+    for (int n = 0; n < kBNW; ++n) {
+      const int nt = nt0 + n;
+      if (nt >= g.Nt) continue;
+      int region, tt;  // 0 = Q, 1 = K, 2 = V
+      if (nt < g.q_tiles) {
+        region = 0;
+        tt = nt;
+      } else if (nt < g.q_tiles + g.kv_tiles) {
+        region = 1;
+        tt = nt - g.q_tiles;
+      } else {
+        region = 2;
+        tt = nt - g.q_tiles - g.kv_tiles;
+      }
+      const int head = tt / tph, jj = tt % tph;
+#pragma unroll
+      for (int m = 0; m < kBM; ++m)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = m * 16 + quad * 4 + e, row = row0 + r;
+          const float x = acc[m][n][e];
+          const float partner = __shfl_xor(x, 8);
+          if (row >= g.M) continue;
+          const int slot = s_slot[r];
+          if (region < 2) {
+            const int mm = 8 * jj + (col & 7);
+            const int dim = (col < 8) ? mm : half + mm;
+            const float2 cs = g.rope[(long)slot * half + mm];
+            const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
+            if (region == 0) g.Q[(long)row * g.q_dim + head * g.hd + dim] = y;
+            else g.kc[s_cache[r] + ((long)head * g.Lcap + slot) * g.hd + dim] = f2h(y);
+          } else {
+            g.vt[s_cache[r] + ((long)head * g.hd + jj * 16 + col) * g.Lcap + slot] = f2h(x);
+          }
         }
     }
-    if (s + 1 < nst) {
-      stash((s + 1) & 1);  // this buffer was last read in stage s - 1, before the barrier below
-      __syncthreads();
-      if (s + 2 < nst) fetch(s + 2);
+  } else if constexpr (EPI == BEPI_RESID) {
+#pragma unroll
+    for (int n = 0; n < kBNW; ++n) {
+      const int nt = nt0 + n;
+      if (nt >= g.Nt) continue;
+#pragma unroll
+      for (int m = 0; m < kBM; ++m)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int row = row0 + m * 16 + quad * 4 + e;
+          if (row < g.M) g.X[(long)row * g.H + nt * 16 + col] += acc[m][n][e];
+        }
     }
-  }
-
-  const int quad = lane >> 4, col = lane & 15;
-  if constexpr (!ARGMAX) {
-    float* Y = g.Y + (long)kz * g.Mt * 16 * g.ldy;
+  } else if constexpr (EPI == BEPI_SWIGLU) {
+    uint32_t* out = reinterpret_cast<uint32_t*>(g.out16);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int n = 0; n < kBNW; ++n) {
+      const int nt = nt0 + n;
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const int mt = mg * kBM + 2 * wm + mi, nt = ng * kBN + 4 * wn + ni;
-        if (mt < g.Mt && nt < g.Nt)
+      for (int m = 0; m < kBM; ++m)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) Y[(long)(mt * 16 + quad * 4 + i) * g.ldy + nt * 16 + col] = acc[mi][ni][i];
-      }
-  } else {
-    // LM head: logits scaled by the final RMSNorm's 1/rms; best (logit, id) per row of this
-    // n-group, ties to the lowest id (tiles visited in id order)
-    __syncthreads();  // the stage buffers are reused below
-    float* sv = reinterpret_cast<float*>(&st[0][0]);   // [2 wn][kBM * 16 rows]
-    int* si = reinterpret_cast<int*>(sv + 2 * kBM * 16);
+        for (int e = 0; e < 4; ++e) {
+          const int row = row0 + m * 16 + quad * 4 + e;
+          const float gt = acc[m][n][e];
+          const float up = __shfl_xor(gt, 8);
+          const float hv = (col < 8) ? gt / (1.0f + expf(-gt)) * up : 0.f;
+          const float h1 = __shfl_xor(hv, 1);
+          if (nt < g.Nt && row < g.M && col < 8 && (col & 1) == 0)
+            out[frag_off(row, nt * 8 + col, g.out_kt) >> 1] = pack_h2(hv, h1);
+        }
+    }
+  } else if constexpr (EPI == BEPI_ARGMAX) {
+    // best (logit, id) of each row over this wave's 64 columns, then over the 4 waves;
+    // ties go to the lowest id (ids grow with n and col)
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi) {
-      const int mt = mg * kBM + 2 * wm + mi;
+    for (int m = 0; m < kBM; ++m) {
       float bv[4];
       int bi[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        bv[i] = -INFINITY;
-        bi[i] = 0x7FFFFFFF;
+      for (int e = 0; e < 4; ++e) {
+        bv[e] = -INFINITY;
+        bi[e] = 0x7FFFFFFF;
       }
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const int nt = ng * kBN + 4 * wn + ni;
-        const int vc = nt * 16 + col;
-        const bool ok = nt < g.Nt && vc < g.V;
+      for (int n = 0; n < kBNW; ++n) {
+        const int vc = (nt0 + n) * 16 + col;
+        const bool ok = vc < g.V;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = mt * 16 + quad * 4 + i;
-          const float v = acc[mi][ni][i] * (mt < g.Mt ? g.rstd[row] : 0.f);
+        for (int e = 0; e < 4; ++e) {
+          const int row = row0 + m * 16 + quad * 4 + e;
+          const float v = acc[m][n][e];
           if (ok && row < g.M && g.logits) g.logits[(long)row * g.V + vc] = v;
-          if (ok && (v > bv[i] || (v == bv[i] && vc < bi[i]))) {
-            bv[i] = v;
-            bi[i] = vc;
+          if (ok && (v > bv[e] || (v == bv[e] && vc < bi[e]))) {
+            bv[e] = v;
+            bi[e] = vc;
           }
         }
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int e = 0; e < 4; ++e)
 #pragma unroll
         for (int off = 1; off < 16; off <<= 1) {
-          const float ov = __shfl_xor(bv[i], off);
-          const int oi = __shfl_xor(bi[i], off);
-          if (ov > bv[i] || (ov == bv[i] && oi < bi[i])) {
-            bv[i] = ov;
-            bi[i] = oi;
+          const float ov = __shfl_xor(bv[e], off);
+          const int oi = __shfl_xor(bi[e], off);
+          if (ov > bv[e] || (ov == bv[e] && oi < bi[e])) {
+            bv[e] = ov;
+            bi[e] = oi;
           }
         }
       if (col == 0)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = (2 * wm + mi) * 16 + quad * 4 + i;
-          sv[wn * kBM * 16 + r] = bv[i];
-          si[wn * kBM * 16 + r] = bi[i];
+        for (int e = 0; e < 4; ++e) {
+          s_bv[w][m * 16 + quad * 4 + e] = bv[e];
+          s_bi[w][m * 16 + quad * 4 + e] = bi[e];
         }
     }
     __syncthreads();
     if (tid < kBM * 16) {
-      const int row = mg * kBM * 16 + tid;
-      float v = sv[tid];
-      int ix = si[tid];
-      const float v1 = sv[kBM * 16 + tid];
-      const int i1 = si[kBM * 16 + tid];
-      if (v1 > v || (v1 == v && i1 < ix)) {
-        v = v1;
-        ix = i1;
+      float v = s_bv[0][tid];
+      int ix = s_bi[0][tid];
+#pragma unroll
+      for (int q = 1; q < kBWaves; ++q) {
+        const float ov = s_bv[q][tid];
+        const int oi = s_bi[q][tid];
+        if (ov > v || (ov == v && oi < ix)) {
+          v = ov;
+          ix = oi;
+        }
       }
+      const int row = row0 + tid;
       if (row < g.Mt * 16) {
         g.pmax[(long)ng * g.pld + row] = v;
         g.pidx[(long)ng * g.pld + row] = ix;
@@ -217,177 +375,112 @@ __global__ __launch_bounds__(64) void k_bargmax(const float* pmax, const int* pi
   if (lane == 0) tokens[row] = (ix == 0x7FFFFFFF) ? 0 : ix;
 }
 
-// 1/rms of each row from its per-16-column sums of squares [rows][n_st] (one wave per row)
-__global__ __launch_bounds__(64) void k_brstd(const float* stats, int n_st, int M, float inv_dim, float eps,
-                                              float* rstd) {
-  const int row = blockIdx.x, lane = threadIdx.x;
-  if (row >= M) return;
-  float s = 0.f;
-  for (int t = lane; t < n_st; t += 64) s += stats[(long)row * n_st + t];
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) s += __shfl_xor(s, off);
-  if (lane == 0) rstd[row] = rsqrtf(s * inv_dim + eps);
-}
 
-// the 16 outputs of (row, columns c0 .. c0+15): sum of the K slices, in slice order
-__device__ __forceinline__ void bsum16(const BEpiArgs& e, int row, int c0, float* v) {
+// RMSNorm of row blockIdx.x of X [M, H] (fp32) with gain g into fp16 A fragments.  One
+// work-group of 256 threads per row, 8 consecutive columns per thread and step.
+__global__ __launch_bounds__(256) void k_bnorm(const float* X, int H, const float* gain, float eps, u32x4* A,
+                                               int a_kt) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  const float* x = X + (long)row * H;
+  float sq = 0.f;
+  for (int k0 = threadIdx.x * 8; k0 < H; k0 += 2048) {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(x + k0), b = *reinterpret_cast<const f32x4*>(x + k0 + 4);
 #pragma unroll
-  for (int c = 0; c < 16; ++c) v[c] = 0.f;
-  for (int z = 0; z < e.kg; ++z) {
-    const f32x4* p = reinterpret_cast<const f32x4*>(e.Y + ((long)z * e.Mpad + row) * e.ldy + c0);
+    for (int e = 0; e < 4; ++e) sq += a[e] * a[e] + b[e] * b[e];
+  }
+  const float rstd = rsqrtf(block_sum256(sq, red) / H + eps);
+  for (int k0 = threadIdx.x * 8; k0 < H; k0 += 2048) {
+    float v[8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const f32x4 x = p[j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) v[4 * j + i] += x[i];
-    }
+    for (int e = 0; e < 8; ++e) v[e] = x[k0 + e] * rstd * gain[k0 + e];
+    A[frag_off(row, k0, a_kt) >> 3] = pack_h8(v);
   }
 }
 
-// A fragments of 8 consecutive columns k0 .. k0+7 of `row` (k0 a multiple of 8)
-__device__ __forceinline__ void store_frag8(u32x4* hi, u32x4* lo, int row, int k0, int a_kt, const float* v) {
-  u32x4 h, l;
-  split_pack8(v, h, l);
-  const long o = frag_off(row, k0, a_kt) >> 3;
-  hi[o] = h;
-  lo[o] = l;
-}
-
-// ---- epilogues: one thread per (row, 16-column output tile) ----
-// EMBED: X = E[ids]; stats; A fragments of x * g
-__global__ void k_bembed(const uint16_t* embed, const int32_t* ids, int M, int H, int V, const float* gain,
-                         float* X, float* stats, u32x4* ahi, u32x4* alo, int a_kt) {
-  const int n_st = H / 16;
-  const long item = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (item >= (long)M * n_st) return;
-  const int row = (int)(item / n_st), t = (int)(item % n_st);
+// embedding rows X = E[ids] (ids clamped into [0, V)), then as k_bnorm
+__global__ __launch_bounds__(256) void k_bembed_norm(const uint16_t* embed, const int32_t* ids, int H, int V,
+                                                     const float* gain, float eps, float* X, u32x4* A, int a_kt) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
   int id = ids[row];
   id = id < 0 ? 0 : (id >= V ? V - 1 : id);
-  float x[16], sq = 0.f;
-  const u32x4* e = reinterpret_cast<const u32x4*>(embed + (long)id * H + t * 16);
+  const uint16_t* er = embed + (long)id * H;
+  float* x = X + (long)row * H;
+  float sq = 0.f;
+  for (int k0 = threadIdx.x * 8; k0 < H; k0 += 2048) {
+    const u32x4 u = *reinterpret_cast<const u32x4*>(er + k0);
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const u32x4 v = e[h];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      x[h * 8 + 2 * j] = bf2f(v[j] & 0xFFFFu);
-      x[h * 8 + 2 * j + 1] = bf2f(v[j] >> 16);
+    for (int e = 0; e < 4; ++e) {
+      const float a = bf2f(u[e] & 0xFFFFu), b = bf2f(u[e] >> 16);
+      x[k0 + 2 * e] = a;
+      x[k0 + 2 * e + 1] = b;
+      sq += a * a + b * b;
     }
   }
-  float y[16];
+  const float rstd = rsqrtf(block_sum256(sq, red) / H + eps);
+  for (int k0 = threadIdx.x * 8; k0 < H; k0 += 2048) {
+    const u32x4 u = *reinterpret_cast<const u32x4*>(er + k0);
+    float v[8];
 #pragma unroll
-  for (int c = 0; c < 16; ++c) {
-    X[(long)row * H + t * 16 + c] = x[c];
-    sq += x[c] * x[c];
-    y[c] = x[c] * gain[t * 16 + c];
-  }
-  stats[(long)row * n_st + t] = sq;
-  store_frag8(ahi, alo, row, t * 16, a_kt, y);
-  store_frag8(ahi, alo, row, t * 16 + 8, a_kt, y + 8);
-}
-
-// RESID: X += y (slices summed); stats of the new rows; A fragments of x * g_next
-__global__ void k_bresid(BEpiArgs e) {
-  const int n_st = e.H / 16;
-  const long item = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (item >= (long)e.M * n_st) return;
-  const int row = (int)(item / n_st), t = (int)(item % n_st);
-  float x[16], y[16], sq = 0.f;
-  bsum16(e, row, t * 16, x);
-  f32x4* px = reinterpret_cast<f32x4*>(e.X + (long)row * e.H + t * 16);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    f32x4 v = px[j];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[i] += x[4 * j + i];
-      x[4 * j + i] = v[i];
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] = bf2f(u[e] & 0xFFFFu) * rstd * gain[k0 + 2 * e];
+      v[2 * e + 1] = bf2f(u[e] >> 16) * rstd * gain[k0 + 2 * e + 1];
     }
-    px[j] = v;
+    A[frag_off(row, k0, a_kt) >> 3] = pack_h8(v);
   }
-#pragma unroll
-  for (int c = 0; c < 16; ++c) {
-    sq += x[c] * x[c];
-    y[c] = x[c] * e.gain[t * 16 + c];
-  }
-  e.stats[(long)row * n_st + t] = sq;
-  store_frag8(e.ahi, e.alo, row, t * 16, e.a_kt, y);
-  store_frag8(e.ahi, e.alo, row, t * 16 + 8, e.a_kt, y + 8);
 }
 
-// SWIGLU: packed tile t holds gate rows 8t .. 8t+7 then the matching up rows
-__global__ void k_bswiglu(BEpiArgs e) {
-  const int nt = e.N / 16;
-  const long item = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (item >= (long)e.M * nt) return;
-  const int row = (int)(item / nt), t = (int)(item % nt);
-  const float r = e.rstd[row];
-  float v[16], h[8];
-  bsum16(e, row, t * 16, v);
+// layer fusion (Eq. 3) of appended row r for draft layer i: u = sum_j alpha[i, j] h^(j)[r]
+// in j order, then f = RMSNorm(u; g_fuse^(i)) into the fp16 A fragments of layer i.  One
+// work-group per (row, layer); the S target rows of r are read from HBM once and found in
+// L2 by the work-groups of the other layers.
+__global__ __launch_bounds__(256) void k_bfuse(const uint16_t* hidden, int N, int S, int H, const float* alpha,
+                                               const float* gain, float eps, u32x4* A, int mt_max) {
+  constexpr int kMaxChunks = 4;  // H <= 8192
+  __shared__ float red[4];
+  const int r = blockIdx.x, i = blockIdx.y;
+  const int Kt = H / 32;
+  float u[kMaxChunks][8];
+  float sq = 0.f;
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    const float gt = v[c] * r, up = v[c + 8] * r;
-    h[c] = gt / (1.0f + expf(-gt)) * up;
-  }
-  store_frag8(e.ahi, e.alo, row, t * 8, e.a_kt, h);
-}
-
-// QKV (block rows) and KVT (appended context rows): packed Q/K tiles hold 8 rotary pairs
-// (m, m + hd/2) of one head; RoPE at the row's position; Q rows fp32, K and V to the
-// row's sequence cache (fp16) at the row's slot.
-__global__ void k_bqkv(BEpiArgs e, BRows rows) {
-  const int nt_all = e.N / 16;
-  const long item = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (item >= (long)e.M * nt_all) return;
-  const int row = (int)(item / nt_all), t = (int)(item % nt_all);
-  const int hd = e.hd, tph = hd / 16, half = hd / 2;
-  const int q_tiles = e.q_tiles, kv_tiles = e.kv_tiles;
-  int region, tt;  // 0 = Q, 1 = K, 2 = V
-  if (t < q_tiles) {
-    region = 0;
-    tt = t;
-  } else if (t < q_tiles + kv_tiles) {
-    region = 1;
-    tt = t - q_tiles;
-  } else {
-    region = 2;
-    tt = t - q_tiles - kv_tiles;
-  }
-  const int head = tt / tph, jj = tt % tph;
-  // the row's sequence, position and cache slot
-  int i = 0;
-  while (i + 1 < rows.n_seq && row >= rows.off[i + 1]) ++i;
-  const int slot = rows.L[i] + (row - rows.off[i]);
-  const long cache = (long)rows.seq[i] * e.seq_stride + (long)e.layer * e.cache_layer;
-  const float r = e.rstd[row];
-  float v[16];
-  bsum16(e, row, t * 16, v);
+  for (int c = 0; c < kMaxChunks; ++c) {
+    const int k0 = threadIdx.x * 8 + c * 2048;
 #pragma unroll
-  for (int c = 0; c < 16; ++c) v[c] *= r;
-  if (region < 2) {
-    const float2* cs = e.rope + (long)slot * half;
+    for (int e = 0; e < 8; ++e) u[c][e] = 0.f;
+    if (k0 < H) {
+      for (int j = 0; j < S; ++j) {
+        const float a = alpha[i * S + j];
+        const u32x4 v = *reinterpret_cast<const u32x4*>(hidden + ((long)j * N + r) * H + k0);
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const int m = 8 * jj + c;
-      const float2 w = cs[m];
-      const float a = v[c], b = v[c + 8];
-      const float ya = a * w.x - b * w.y, yb = b * w.x + a * w.y;
-      if (region == 0) {
-        e.Q[(long)row * e.q_dim + head * hd + m] = ya;
-        e.Q[(long)row * e.q_dim + head * hd + half + m] = yb;
-      } else {
-        uint16_t* k = e.kc + cache + ((long)head * e.Lcap + slot) * hd;
-        k[m] = f2h(ya);
-        k[half + m] = f2h(yb);
+        for (int e = 0; e < 4; ++e) {
+          u[c][2 * e] = fmaf(a, bf2f(v[e] & 0xFFFFu), u[c][2 * e]);
+          u[c][2 * e + 1] = fmaf(a, bf2f(v[e] >> 16), u[c][2 * e + 1]);
+        }
       }
-    }
-  } else {
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const int dim = jj * 16 + c;
-      e.vt[cache + ((long)head * hd + dim) * e.Lcap + slot] = f2h(v[c]);
+      for (int e = 0; e < 8; ++e) sq += u[c][e] * u[c][e];
     }
   }
+  const float rstd = rsqrtf(block_sum256(sq, red) / H + eps);
+  u32x4* Ai = A + (long)i * mt_max * Kt * 64;
+#pragma unroll
+  for (int c = 0; c < kMaxChunks; ++c) {
+    const int k0 = threadIdx.x * 8 + c * 2048;
+    if (k0 < H) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = u[c][e] * rstd * gain[(long)i * H + k0 + e];
+      Ai[frag_off(r, k0, Kt) >> 3] = pack_h8(v);
+    }
+  }
+}
+
+// debug: fp16 A fragments of D layers -> rows [D, n, H] fp32
+__global__ void k_bfrag_rows(const u32x4* A, int n, int H, int mt_max, float* out) {
+  const int r = blockIdx.x, i = blockIdx.y, Kt = H / 32;
+  const uint16_t* a = reinterpret_cast<const uint16_t*>(A + (long)i * mt_max * Kt * 64);
+  for (int k = threadIdx.x; k < H; k += blockDim.x) out[((long)i * n + r) * H + k] = h2f(a[frag_off(r, k, Kt)]);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -559,9 +652,9 @@ __global__ __launch_bounds__(256, 2) void k_battn(BAttnArgs a, BRows rows) {
 }
 
 // merge the chunk partials of query row r of head g of sequence i (one wave per row) and
-// write the A fragments of the output projection at row off[i] + r % B
+// write the fp16 A fragments of the output projection at row off[i] + r % B
 template <int HD>
-__global__ __launch_bounds__(64) void k_bcomb(BAttnArgs a, BRows rows, u32x4* ohi, u32x4* olo, int a_kt) {
+__global__ __launch_bounds__(64) void k_bcomb(BAttnArgs a, BRows rows, u32x4* out16, int a_kt) {
   constexpr int DPL = HD / 64;
   const int lane = threadIdx.x;
   const int G = a.n_q / a.n_kv, R = G * a.B;
@@ -587,55 +680,55 @@ __global__ __launch_bounds__(64) void k_bcomb(BAttnArgs a, BRows rows, u32x4* oh
   }
   const float inv = 1.0f / den;
   const int row = rows.off[i] + r % a.B, h = g * G + r / a.B;
-  uint32_t* hi = reinterpret_cast<uint32_t*>(ohi);
-  uint32_t* lo = reinterpret_cast<uint32_t*>(olo);
+  uint32_t* o = reinterpret_cast<uint32_t*>(out16);
   if constexpr (DPL == 2) {
-    store_frag_pair(hi, lo, row, h * HD + 2 * lane, a_kt, num[0] * inv, num[1] * inv);
+    o[frag_off(row, h * HD + 2 * lane, a_kt) >> 1] = pack_h2(num[0] * inv, num[1] * inv);
   } else {
     const float y = num[0] * inv, y1 = __shfl_xor(y, 1);
-    if ((lane & 1) == 0) store_frag_pair(hi, lo, row, h * HD + lane, a_kt, y, y1);
+    if ((lane & 1) == 0) o[frag_off(row, h * HD + lane, a_kt) >> 1] = pack_h2(y, y1);
   }
 }
+
 
 // ------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------
 int bgemm_groups(int Nt, int Mt) { return ((Nt + kBN - 1) / kBN) * ((Mt + kBM - 1) / kBM); }
 
-void launch_bgemm(hipStream_t s, const BGemmArgs& g, bool argmax) {
-  const dim3 grid(bgemm_groups(g.Nt, g.Mt) * g.kg);
-  if (argmax) hipLaunchKernelGGL(k_bgemm<true>, grid, dim3(kBT), 0, s, g);
-  else hipLaunchKernelGGL(k_bgemm<false>, grid, dim3(kBT), 0, s, g);
+void launch_tiles_to_f16(hipStream_t s, u32x4* dst, const u32x4* src, long n) {
+  hipLaunchKernelGGL(k_tiles_to_f16, dim3(2048), dim3(256), 0, s, dst, src, n);
+}
+
+void launch_bgemm(hipStream_t s, int epi, const BGemmArgs& g, const BRows& rows) {
+  const dim3 grid(bgemm_groups(g.Nt, g.Mt) * g.kg * g.layers);
+  switch (epi) {
+    case BEPI_QKV: hipLaunchKernelGGL(k_bgemm<BEPI_QKV>, grid, dim3(kBT), 0, s, g, rows); break;
+    case BEPI_RESID: hipLaunchKernelGGL(k_bgemm<BEPI_RESID>, grid, dim3(kBT), 0, s, g, rows); break;
+    case BEPI_SWIGLU: hipLaunchKernelGGL(k_bgemm<BEPI_SWIGLU>, grid, dim3(kBT), 0, s, g, rows); break;
+    default: hipLaunchKernelGGL(k_bgemm<BEPI_ARGMAX>, grid, dim3(kBT), 0, s, g, rows); break;
+  }
 }
 
 void launch_bargmax(hipStream_t s, const float* pmax, const int* pidx, int ngroups, int pld, int M, int* tokens) {
   hipLaunchKernelGGL(k_bargmax, dim3(M), dim3(64), 0, s, pmax, pidx, ngroups, pld, M, tokens);
 }
 
-void launch_brstd(hipStream_t s, const float* stats, int n_st, int M, float inv_dim, float eps, float* rstd) {
-  hipLaunchKernelGGL(k_brstd, dim3(M), dim3(64), 0, s, stats, n_st, M, inv_dim, eps, rstd);
+void launch_bnorm(hipStream_t s, const float* X, int M, int H, const float* gain, float eps, u32x4* A, int a_kt) {
+  hipLaunchKernelGGL(k_bnorm, dim3(M), dim3(256), 0, s, X, H, gain, eps, A, a_kt);
 }
 
-static int blocks_for(long items) { return (int)((items + 255) / 256); }
-
-void launch_bembed(hipStream_t s, const uint16_t* embed, const int32_t* ids, int M, int H, int V,
-                   const float* gain, float* X, float* stats, u32x4* ahi, u32x4* alo, int a_kt) {
-  hipLaunchKernelGGL(k_bembed, dim3(blocks_for((long)M * (H / 16))), dim3(256), 0, s, embed, ids, M, H, V, gain, X,
-                     stats, ahi, alo, a_kt);
+void launch_bembed_norm(hipStream_t s, const uint16_t* embed, const int32_t* ids, int M, int H, int V,
+                        const float* gain, float eps, float* X, u32x4* A, int a_kt) {
+  hipLaunchKernelGGL(k_bembed_norm, dim3(M), dim3(256), 0, s, embed, ids, H, V, gain, eps, X, A, a_kt);
 }
 
-void launch_bepi(hipStream_t s, int kind, const BEpiArgs& e, const BRows& rows) {
-  switch (kind) {
-    case BEPI_RESID:
-      hipLaunchKernelGGL(k_bresid, dim3(blocks_for((long)e.M * (e.H / 16))), dim3(256), 0, s, e);
-      break;
-    case BEPI_SWIGLU:
-      hipLaunchKernelGGL(k_bswiglu, dim3(blocks_for((long)e.M * (e.N / 16))), dim3(256), 0, s, e);
-      break;
-    default:
-      hipLaunchKernelGGL(k_bqkv, dim3(blocks_for((long)e.M * (e.N / 16))), dim3(256), 0, s, e, rows);
-      break;
-  }
+void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int S, int H, int D, const float* alpha,
+                  const float* gain, float eps, u32x4* A, int mt_max) {
+  hipLaunchKernelGGL(k_bfuse, dim3(N, D), dim3(256), 0, s, hidden, N, S, H, alpha, gain, eps, A, mt_max);
+}
+
+void launch_bfrag_rows(hipStream_t s, const u32x4* A, int n, int H, int D, int mt_max, float* out) {
+  hipLaunchKernelGGL(k_bfrag_rows, dim3(n, D), dim3(256), 0, s, A, n, H, mt_max, out);
 }
 
 void launch_battn(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, int items) {
@@ -643,11 +736,11 @@ void launch_battn(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, 
   else hipLaunchKernelGGL(k_battn<128>, dim3(items), dim3(256), 0, s, a, rows);
 }
 
-void launch_bcomb(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, u32x4* ohi, u32x4* olo, int a_kt) {
+void launch_bcomb(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, u32x4* out16, int a_kt) {
   const int R = (a.n_q / a.n_kv) * a.B;
   const dim3 grid(rows.n_seq * a.n_kv * R);
-  if (hd == 64) hipLaunchKernelGGL(k_bcomb<64>, grid, dim3(64), 0, s, a, rows, ohi, olo, a_kt);
-  else hipLaunchKernelGGL(k_bcomb<128>, grid, dim3(64), 0, s, a, rows, ohi, olo, a_kt);
+  if (hd == 64) hipLaunchKernelGGL(k_bcomb<64>, grid, dim3(64), 0, s, a, rows, out16, a_kt);
+  else hipLaunchKernelGGL(k_bcomb<128>, grid, dim3(64), 0, s, a, rows, out16, a_kt);
 }
 
 }  // namespace dflare

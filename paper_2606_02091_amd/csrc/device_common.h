@@ -107,6 +107,11 @@ __device__ __forceinline__ float2 ld_coh2(const void* p) {
                                        __HIP_MEMORY_SCOPE_AGENT);
   return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
 }
+// 16-byte coherent load (two 8-byte agent-scope loads)
+__device__ __forceinline__ f32x4 ld_coh16(const f32x4* p) {
+  const float2 x = ld_coh2(p), y = ld_coh2(reinterpret_cast<const float*>(p) + 2);
+  return f32x4{x.x, x.y, y.x, y.y};
+}
 // an integer the compiler cannot see through (keeps address arithmetic where it is written)
 __device__ __forceinline__ int opaque(int x) {
   asm volatile("" : "+v"(x));

@@ -430,11 +430,6 @@ constexpr int kLdsRedBytes = kWaves * kTNMax * 1024;
 constexpr int kStageOff = 80 * 1024;
 static_assert(kLdsRedBytes + 2048 <= kStageOff, "GEMM scratch stays below the attention staging area");
 
-// 16-byte coherent load (two 8-byte agent-scope loads)
-__device__ __forceinline__ f32x4 ld_coh16(const f32x4* p) {
-  const float2 x = ld_coh2(p), y = ld_coh2(reinterpret_cast<const float*>(p) + 2);
-  return f32x4{x.x, x.y, y.x, y.y};
-}
 
 // Epilogue of one finished 16 x 16 output tile nt (lane holds rows quad*4 .. +3 of column
 // col); v already carries the RMSNorm row scale.  ARGMAX leaves the tile's best (logit,

@@ -124,11 +124,15 @@ struct dflare_handle {
   int cus = 0;
   long seq_stride = 0;     // cache elements of one sequence slot (all layers)
   int b_mt = 1;            // m-tiles of the largest batched call
-  long bY_elems = 0;       // capacity of the GEMM K-slice buffer (floats)
-  float *bX = nullptr, *bstats = nullptr, *brstd = nullptr, *bQ = nullptr, *bY = nullptr, *bOP = nullptr;
+  float *bX = nullptr, *bQ = nullptr, *bOP = nullptr;
   float2* bML = nullptr;
-  u32x4 *bA = nullptr, *bOA = nullptr, *bHA = nullptr;  // A fragments: hi plane, then lo plane
-  long bA_plane = 0, bOA_plane = 0, bHA_plane = 0;
+  u32x4 *bA = nullptr, *bOA = nullptr, *bHA = nullptr;  // fp16 A fragments of the GEMM inputs
+  u32x4* bU = nullptr;     // fp16 A fragments of the fused rows of a batched append, per layer
+  // fp16 copies of the packed weight tiles, made on first use of the batched path
+  u32x4 *h_qkv = nullptr, *h_o = nullptr, *h_gu = nullptr, *h_down = nullptr, *h_kvt = nullptr, *h_lm = nullptr;
+  float* bpart = nullptr;  // split-K partial tiles
+  long bpart_floats = 0;
+  unsigned* bcnt = nullptr;
   float* bpmax = nullptr;
   int* bpidx = nullptr;
   float* dbg_blogits = nullptr;
@@ -292,16 +296,21 @@ GemmPlan choose_plan(const char* name, int Nt, int Kt, int blocks, bool allow_sp
   return best;
 }
 
-// K split of a batched GEMM: the smallest estimated time, counted as (work-group
-// rounds over the CUs) x (k-tiles per work-group) plus a fixed 4 k-tiles per extra slice
-// for writing and summing it.  DFLARE_BSPLIT_<NAME>=kg overrides the choice (tuning).
-int bgemm_split(const dflare_handle* h, const char* name, int Nt, int Mt, int Kt) {
-  const long groups = bgemm_groups(Nt, Mt);
+// K split of a batched GEMM (1 where the epilogue needs whole sums before it can start
+// or the tiles outnumber the arrival counters): the smallest estimated time, counted in
+// k-tiles per work-group as (rounds of work-groups over the resident slots, two per CU)
+// x (k-tiles per part), plus 20 k-tiles per extra part for writing and reading back its
+// partial tile (a measured fit).
+// DFLARE_BSPLIT_<NAME>=kg overrides the choice (tuning).
+int bgemm_split(int cus, const char* name, int Nt, int Mt, int Kt, int layers, bool allow) {
+  const long tiles = (long)bgemm_groups(Nt, Mt) * layers;
+  if (!allow || tiles > kBCounters) return 1;
   int best = 1;
   double best_t = 1e300;
   for (int kg : {1, 2, 3, 4, 6, 8}) {
     if (kg > 1 && Kt < 8 * kg) continue;
-    const double t = (double)ceil_div(groups * kg, h->cus) * ceil_div(Kt, kg) + 4.0 * (kg - 1);
+    const double t = (double)ceil_div(tiles * kg, (long)cus * kBWavesPerSimd) * ceil_div(Kt, kg) +
+                     (kg > 1 ? 4.0 + 20.0 * (kg - 1) : 0.0);
     if (t < best_t - 1e-9) {
       best_t = t;
       best = kg;
@@ -311,12 +320,13 @@ int bgemm_split(const dflare_handle* h, const char* name, int Nt, int Mt, int Kt
   snprintf(key, sizeof key, "DFLARE_BSPLIT_%s", name);
   if (const char* env = getenv(key)) {
     const int v = atoi(env);
-    if (v >= 1 && v <= 8 && v <= Kt) best = v;
+    if (v >= 1 && v <= kBSplitMax && v <= Kt) best = v;
   }
   return best;
 }
 
 DraftArgs draft_args(const dflare_handle* h);
+int ensure_f16_weights(dflare_handle* h);
 
 int build(dflare_handle* h, const dflare_weights* w) {
   const dflare_config& c = h->cfg;
@@ -477,27 +487,27 @@ int build(dflare_handle* h, const dflare_weights* w) {
     h->b_mt = ceil_div((long)c.max_batch * B, 16);
     const long rows = (long)h->b_mt * 16;
     TRY(dev_zalloc(h, &h->bX, (size_t)rows * H * 4));
-    TRY(dev_zalloc(h, &h->bstats, (size_t)rows * (H / 16) * 4));
-    TRY(dev_zalloc(h, &h->brstd, (size_t)std::max(rows, (long)mt_max * 16) * 4));
     TRY(dev_zalloc(h, &h->bQ, (size_t)rows * q * 4));
-    h->bA_plane = (long)h->b_mt * Kt_H * 64;
-    h->bOA_plane = (long)h->b_mt * Kt_q * 64;
-    h->bHA_plane = (long)h->b_mt * Kt_F * 64;
-    TRY(dev_zalloc(h, &h->bA, (size_t)2 * h->bA_plane * 16));
-    TRY(dev_zalloc(h, &h->bOA, (size_t)2 * h->bOA_plane * 16));
-    TRY(dev_zalloc(h, &h->bHA, (size_t)2 * h->bHA_plane * 16));
-    // K slices of the largest GEMM of any call shape
-    long y = 0;
+    TRY(dev_zalloc(h, &h->bA, (size_t)h->b_mt * Kt_H * 1024));
+    TRY(dev_zalloc(h, &h->bOA, (size_t)h->b_mt * Kt_q * 1024));
+    TRY(dev_zalloc(h, &h->bHA, (size_t)h->b_mt * Kt_F * 1024));
+    TRY(dev_zalloc(h, &h->bU, (size_t)D * mt_max * Kt_H * 1024));
+    // partial tiles of the largest split of any call shape
+    long part = 0;
+    auto need = [&](const char* name, int Nt, int mt, int Kt, int layers) {
+      const int kg = bgemm_split(h->cus, name, Nt, mt, Kt, layers, true);
+      if (kg > 1) part = std::max(part, (long)bgemm_groups(Nt, mt) * layers * kg * kBPartFloats);
+    };
     for (int mt = 1; mt <= h->b_mt; ++mt) {
-      y = std::max(y, (long)bgemm_split(h, "QKV", Nt_qkv, mt, Kt_H) * mt * 16 * Nt_qkv * 16);
-      y = std::max(y, (long)bgemm_split(h, "O", Nt_o, mt, Kt_q) * mt * 16 * Nt_o * 16);
-      y = std::max(y, (long)bgemm_split(h, "GU", Nt_gu, mt, Kt_H) * mt * 16 * Nt_gu * 16);
-      y = std::max(y, (long)bgemm_split(h, "DOWN", Nt_down, mt, Kt_F) * mt * 16 * Nt_down * 16);
+      need("QKV", Nt_qkv, mt, Kt_H, 1);
+      need("O", Nt_o, mt, Kt_q, 1);
+      need("GU", Nt_gu, mt, Kt_H, 1);
+      need("DOWN", Nt_down, mt, Kt_F, 1);
     }
-    for (int mt = 1; mt <= mt_max; ++mt)
-      y = std::max(y, (long)bgemm_split(h, "KVT", Nt_kvt, mt, Kt_H) * mt * 16 * Nt_kvt * 16);
-    h->bY_elems = y;
-    TRY(dev_alloc(h, &h->bY, (size_t)y * 4));
+    for (int mt = 1; mt <= mt_max; ++mt) need("KVT", Nt_kvt, mt, Kt_H, D);
+    h->bpart_floats = part;
+    TRY(dev_alloc(h, &h->bpart, (size_t)std::max(part, 64L) * 4));
+    TRY(dev_zalloc(h, &h->bcnt, (size_t)kBCounters * 128));
     const long items = (long)c.max_batch * h->attn_nch * c.n_kv_heads;
     TRY(dev_alloc(h, &h->bOP, (size_t)items * h->Rpad * hd * 4));
     TRY(dev_alloc(h, &h->bML, (size_t)items * h->Rpad * sizeof(float2)));
@@ -505,6 +515,7 @@ int build(dflare_handle* h, const dflare_weights* w) {
     TRY(dev_alloc(h, &h->bpmax, (size_t)ng_lm * rows * 4));
     TRY(dev_alloc(h, &h->bpidx, (size_t)ng_lm * rows * 4));
   }
+  if (c.max_batch > 1) TRY(ensure_f16_weights(h));
   HIP_OR_FAIL(h, hipHostMalloc((void**)&h->err_host, 64, hipHostMallocMapped | hipHostMallocCoherent));
   *(volatile int*)h->err_host = 0;
   HIP_OR_FAIL(h, hipHostGetDevicePointer((void**)&h->err_dev, h->err_host, 0));
@@ -685,54 +696,64 @@ int check_seqs(dflare_handle* h, int32_t n_seq, const int32_t* seq) {
   return DFLARE_OK;
 }
 
-// Y = A W^T over all rows of a batched call, K split chosen per shape (bounded by the slice buffer)
-int bgemm(dflare_handle* h, int kind, const char* name, const u32x4* a_hi, const u32x4* a_lo, int a_kt,
-          const u32x4* w, int Nt, int Kt, int M, BEpiArgs& e) {
-  BGemmArgs g{};
-  g.Ahi = a_hi;
-  g.Alo = a_lo;
-  g.a_kt = a_kt;
-  g.W = w;
-  g.Nt = Nt;
-  g.Kt = Kt;
-  g.zero = h->zero_tile;
-  g.Mt = ceil_div(M, 16);
-  g.M = M;
-  g.kg = bgemm_split(h, name, Nt, g.Mt, Kt);
-  while (g.kg > 1 && (long)g.kg * g.Mt * 16 * Nt * 16 > h->bY_elems) --g.kg;
-  g.Y = h->bY;
-  g.ldy = Nt * 16;
-  prof_mark(h, kind, true);
-  launch_bgemm(h->stream, g, false);
-  prof_mark(h, kind, false);
-  e.Y = h->bY;
-  e.kg = g.kg;
-  e.Mpad = g.Mt * 16;
-  e.ldy = g.ldy;
-  e.N = Nt * 16;
-  e.M = M;
-  return DFLARE_OK;
+// fp16 copies of the packed weights for the batched GEMMs (allocated and converted once)
+int ensure_f16_weights(dflare_handle* h) {
+  if (h->h_lm) return DFLARE_OK;
+  const dflare_config& c = h->cfg;
+  const long D = c.n_draft_layers;
+  const long lm = (long)ceil_div(c.vocab, 16) * (c.hidden / 32) * 64;
+  struct Item {
+    u32x4** dst;
+    const u32x4* src;
+    long n;
+  } items[] = {{&h->h_qkv, h->w_qkv, h->s_qkv * D}, {&h->h_o, h->w_o, h->s_o * D},
+               {&h->h_gu, h->w_gu, h->s_gu * D},    {&h->h_down, h->w_down, h->s_down * D},
+               {&h->h_kvt, h->w_kvt, h->s_kvt * D}, {&h->h_lm, h->w_lm, lm}};
+  for (const Item& it : items) {
+    u32x4* p = nullptr;
+    TRY(dev_alloc(h, &p, (size_t)it.n * 16));
+    launch_tiles_to_f16(h->stream, p, it.src, it.n);
+    *it.dst = p;
+  }
+  return check_launch(h, "weight conversion");
 }
 
-BEpiArgs bepi_base(const dflare_handle* h) {
+// one batched GEMM with its fused epilogue; the K split is chosen per shape
+void bgemm(dflare_handle* h, int kind, const char* name, int epi, BGemmArgs g, const BRows& rows) {
+  g.kg = bgemm_split(h->cus, name, g.Nt, g.Mt, g.Kt, g.layers, epi != BEPI_ARGMAX);
+  g.zero = h->zero_tile;
+  g.part = h->bpart;
+  g.cnt = h->bcnt;
+  prof_mark(h, kind, true);
+  launch_bgemm(h->stream, epi, g, rows);
+  prof_mark(h, kind, false);
+}
+
+// epilogue fields shared by every batched GEMM of a handle
+BGemmArgs bgemm_base(const dflare_handle* h) {
   const dflare_config& c = h->cfg;
-  BEpiArgs e{};
-  e.H = c.hidden;
-  e.rstd = h->brstd;
-  e.X = h->bX;
-  e.stats = h->bstats;
-  e.Q = h->bQ;
-  e.q_dim = h->q_dim;
-  e.kc = h->kc;
-  e.vt = h->vt;
-  e.seq_stride = h->seq_stride;
-  e.cache_layer = h->cache_layer_stride;
-  e.Lcap = h->Lcap;
-  e.hd = c.head_dim;
-  e.q_tiles = h->q_dim / 16;
-  e.kv_tiles = h->kv_dim / 16;
-  e.rope = h->rope;
-  return e;
+  BGemmArgs g{};
+  g.layers = 1;
+  g.Q = h->bQ;
+  g.q_dim = h->q_dim;
+  g.kc = h->kc;
+  g.vt = h->vt;
+  g.seq_stride = h->seq_stride;
+  g.cache_layer = h->cache_layer_stride;
+  g.Lcap = h->Lcap;
+  g.hd = c.head_dim;
+  g.q_tiles = h->q_dim / 16;
+  g.kv_tiles = h->kv_dim / 16;
+  g.rope = h->rope;
+  g.X = h->bX;
+  g.H = c.hidden;
+  g.out16 = h->bHA;
+  g.out_kt = c.ffn / 32;
+  g.V = c.vocab;
+  g.pmax = h->bpmax;
+  g.pidx = h->bpidx;
+  g.pld = h->b_mt * 16;
+  return g;
 }
 
 int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int32_t* n_new, const void* hidden) {
@@ -748,25 +769,23 @@ int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int3
   }
   const int N = rows.off[n_seq];
   prof_mark(h, DFLARE_K_B_FUSE, true);
-  launch_fuse(s, (const uint16_t*)hidden, N, S, H, D, h->alpha, h->g_fuse, h->Ustats, h->ua_hi, h->ua_lo, c.max_new,
-              h->mt_max);
+  launch_bfuse(s, (const uint16_t*)hidden, N, S, H, D, h->alpha, h->g_fuse, c.rms_eps, h->bU, h->mt_max);
   prof_mark(h, DFLARE_K_B_FUSE, false);
-  const long ua_layer = (long)h->mt_max * Kt_H * 64;
-  for (int l = 0; l < D; ++l) {
-    prof_mark(h, DFLARE_K_B_EPI, true);
-    launch_brstd(s, h->Ustats + (long)l * c.max_new * (H / 16), H / 16, N, 1.0f / H, c.rms_eps, h->brstd);
-    prof_mark(h, DFLARE_K_B_EPI, false);
-    BEpiArgs e = bepi_base(h);
-    TRY(bgemm(h, DFLARE_K_B_KV_T, "KVT", h->ua_hi + l * ua_layer, h->ua_lo + l * ua_layer, Kt_H, h->w_kvt + l * h->s_kvt,
-              2 * h->kv_dim / 16, Kt_H, N, e));
-    e.layer = l;
-    e.q_tiles = 0;
-    prof_mark(h, DFLARE_K_B_EPI, true);
-    launch_bepi(s, BEPI_QKV, e, rows);
-    prof_mark(h, DFLARE_K_B_EPI, false);
-  }
+  BGemmArgs g = bgemm_base(h);
+  g.A = h->bU;
+  g.a_layer = (long)h->mt_max * Kt_H * 64;
+  g.W = h->h_kvt;
+  g.w_layer = h->s_kvt;
+  g.Nt = 2 * h->kv_dim / 16;
+  g.Kt = Kt_H;
+  g.Mt = ceil_div(N, 16);
+  g.M = N;
+  g.layers = D;
+  g.layer0 = 0;
+  g.q_tiles = 0;
+  bgemm(h, DFLARE_K_B_KV_T, "KVT", BEPI_QKV, g, rows);
   if (h->debug) {
-    launch_fused_rows(s, h->ua_hi, h->ua_lo, h->Ustats, N, H, D, c.max_new, h->mt_max, c.rms_eps, h->dbg_fused);
+    launch_bfrag_rows(s, h->bU, N, H, D, h->mt_max, h->dbg_fused);
     h->dbg_fused_n = N;
   }
   TRY(check_launch(h, "fuse_append_batched"));
@@ -804,73 +823,54 @@ int run_draft_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int
   at.qscale = (float)(1.4426950408889634 / sqrt((double)hd));
   at.OP = h->bOP;
   at.ML = h->bML;
-  const float inv_H = 1.0f / H;
+  BGemmArgs g = bgemm_base(h);
+  g.Mt = Mt;
+  g.M = M;
 
   prof_mark(h, DFLARE_K_B_EPI, true);
-  launch_bembed(s, h->embed, ids, M, H, V, h->g_attn, h->bX, h->bstats, h->bA, h->bA + h->bA_plane, Kt_H);
+  launch_bembed_norm(s, h->embed, ids, M, H, V, h->g_attn, c.rms_eps, h->bX, h->bA, Kt_H);
   prof_mark(h, DFLARE_K_B_EPI, false);
   for (int l = 0; l < D; ++l) {
-    prof_mark(h, DFLARE_K_B_EPI, true);
-    launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
-    prof_mark(h, DFLARE_K_B_EPI, false);
-    BEpiArgs e = bepi_base(h);
-    TRY(bgemm(h, DFLARE_K_B_QKV, "QKV", h->bA, h->bA + h->bA_plane, Kt_H, h->w_qkv + l * h->s_qkv, Nt_qkv, Kt_H, M, e));
-    e.layer = l;
-    prof_mark(h, DFLARE_K_B_EPI, true);
-    launch_bepi(s, BEPI_QKV, e, rows);
-    prof_mark(h, DFLARE_K_B_EPI, false);
+    g.layer0 = l;
+    g.A = h->bA;
+    g.W = h->h_qkv + l * h->s_qkv;
+    g.Nt = Nt_qkv;
+    g.Kt = Kt_H;
+    bgemm(h, DFLARE_K_B_QKV, "QKV", BEPI_QKV, g, rows);
     at.layer = l;
     prof_mark(h, DFLARE_K_B_ATTN, true);
     launch_battn(s, hd, at, rows, items);
-    launch_bcomb(s, hd, at, rows, h->bOA, h->bOA + h->bOA_plane, Kt_q);
+    launch_bcomb(s, hd, at, rows, h->bOA, Kt_q);
     prof_mark(h, DFLARE_K_B_ATTN, false);
-    TRY(bgemm(h, DFLARE_K_B_O, "O", h->bOA, h->bOA + h->bOA_plane, Kt_q, h->w_o + l * h->s_o, Nt_H, Kt_q, M, e));
-    e.gain = h->g_mlp + (long)l * H;
-    e.ahi = h->bA;
-    e.alo = h->bA + h->bA_plane;
-    e.a_kt = Kt_H;
+    g.A = h->bOA;
+    g.W = h->h_o + l * h->s_o;
+    g.Nt = Nt_H;
+    g.Kt = Kt_q;
+    bgemm(h, DFLARE_K_B_O, "O", BEPI_RESID, g, rows);
     prof_mark(h, DFLARE_K_B_EPI, true);
-    launch_bepi(s, BEPI_RESID, e, rows);
-    launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
+    launch_bnorm(s, h->bX, M, H, h->g_mlp + (long)l * H, c.rms_eps, h->bA, Kt_H);
     prof_mark(h, DFLARE_K_B_EPI, false);
-    TRY(bgemm(h, DFLARE_K_B_GATE_UP, "GU", h->bA, h->bA + h->bA_plane, Kt_H, h->w_gu + l * h->s_gu, Nt_gu, Kt_H, M, e));
-    e.ahi = h->bHA;
-    e.alo = h->bHA + h->bHA_plane;
-    e.a_kt = Kt_F;
+    g.A = h->bA;
+    g.W = h->h_gu + l * h->s_gu;
+    g.Nt = Nt_gu;
+    g.Kt = Kt_H;
+    bgemm(h, DFLARE_K_B_GATE_UP, "GU", BEPI_SWIGLU, g, rows);
+    g.A = h->bHA;
+    g.W = h->h_down + l * h->s_down;
+    g.Nt = Nt_H;
+    g.Kt = Kt_F;
+    bgemm(h, DFLARE_K_B_DOWN, "DOWN", BEPI_RESID, g, rows);
     prof_mark(h, DFLARE_K_B_EPI, true);
-    launch_bepi(s, BEPI_SWIGLU, e, rows);
-    prof_mark(h, DFLARE_K_B_EPI, false);
-    TRY(bgemm(h, DFLARE_K_B_DOWN, "DOWN", h->bHA, h->bHA + h->bHA_plane, Kt_F, h->w_down + l * h->s_down, Nt_H, Kt_F, M, e));
-    e.gain = (l + 1 < D) ? h->g_attn + (long)(l + 1) * H : h->g_final;
-    e.ahi = h->bA;
-    e.alo = h->bA + h->bA_plane;
-    e.a_kt = Kt_H;
-    prof_mark(h, DFLARE_K_B_EPI, true);
-    launch_bepi(s, BEPI_RESID, e, rows);
+    launch_bnorm(s, h->bX, M, H, (l + 1 < D) ? h->g_attn + (long)(l + 1) * H : h->g_final, c.rms_eps, h->bA, Kt_H);
     prof_mark(h, DFLARE_K_B_EPI, false);
   }
-  prof_mark(h, DFLARE_K_B_EPI, true);
-  launch_brstd(s, h->bstats, H / 16, M, inv_H, c.rms_eps, h->brstd);
-  prof_mark(h, DFLARE_K_B_EPI, false);
-  BGemmArgs g{};
-  g.Ahi = h->bA;
-  g.Alo = h->bA + h->bA_plane;
-  g.a_kt = Kt_H;
-  g.W = h->w_lm;
+  g.A = h->bA;
+  g.W = h->h_lm;
   g.Nt = Nt_lm;
   g.Kt = Kt_H;
-  g.zero = h->zero_tile;
-  g.Mt = Mt;
-  g.M = M;
-  g.kg = 1;
-  g.rstd = h->brstd;
   g.logits = h->debug ? h->dbg_blogits : nullptr;
-  g.V = V;
-  g.pmax = h->bpmax;
-  g.pidx = h->bpidx;
-  g.pld = h->b_mt * 16;
   prof_mark(h, DFLARE_K_B_LM_HEAD, true);
-  launch_bgemm(s, g, true);
+  bgemm(h, -1, "LM", BEPI_ARGMAX, g, rows);  // timed with the final argmax below
   launch_bargmax(s, h->bpmax, h->bpidx, ceil_div(Nt_lm, kBN), g.pld, M, out);
   prof_mark(h, DFLARE_K_B_LM_HEAD, false);
   if (h->debug) h->dbg_blogits_rows = M;
@@ -1010,6 +1010,7 @@ int dflare_fuse_append_batched(dflare_handle* h, int32_t n_seq, const int32_t* s
   for (int i = 0; i < n_seq; ++i)
     if ((long)h->Ls[seq[i]] + n_new[i] > h->cfg.max_context)
       return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
+  TRY(ensure_f16_weights(h));
   prof_mark(h, DFLARE_K_B_APPEND, true);
   const int rc = run_fuse_batched(h, n_seq, seq, n_new, target_hidden);
   prof_mark(h, DFLARE_K_B_APPEND, false);
@@ -1021,6 +1022,7 @@ int dflare_draft_block_batched(dflare_handle* h, int32_t n_seq, const int32_t* s
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
   TRY(check_seqs(h, n_seq, seq));
   if (!block_ids || !draft_tokens) return fail(h, DFLARE_ERR_INVALID_ARG, "block_ids / draft_tokens is NULL");
+  TRY(ensure_f16_weights(h));
   prof_mark(h, DFLARE_K_B_DRAFT, true);
   const int rc = run_draft_batched(h, n_seq, seq, block_ids, draft_tokens);
   prof_mark(h, DFLARE_K_B_DRAFT, false);

@@ -8,10 +8,14 @@ row counts (B = 5 gives sequences that straddle 16-row tiles), empty and one-row
 contexts, contexts on and off the 128-key chunk grid, vocabularies that are not a
 multiple of 16, slots listed out of order and calls on subsets of the slots.
 
-The batched kernels compute in the same precisions as the batch-1 path and differ
-from it only in the order of fp32 sums, so one sequence drafted both ways must agree
-to far better than the oracle bar: within BATCH1_TOL, which allows a few fp16 cache
-roundings (2^-11 relative each) to fall the other way.
+Besides the oracle bar, two batched results are compared directly: the same sequence
+drafted by batched calls of other shapes (other rows, other K splits), and by the
+batch-1 path.  The batched GEMMs take fp16 operands, rounded to 2^-11 relative; which
+way each rounding falls depends on the order of the fp32 sums before it (the K split),
+and the draft layers carry such differences forward, so a batched result sits about
+2.5e-3 of the logit range from the exact one at full size (1e-3 on the small cases
+here) and any two of them, or one and the batch-1 path's, agree within AGREE_TOL =
+5e-3, a quarter of the oracle bar.
 """
 import numpy as np
 import pytest
@@ -26,7 +30,7 @@ pytestmark = pytest.mark.gpu
 if not torch.cuda.is_available():  # pragma: no cover - CPU container
     pytest.skip("needs a GPU", allow_module_level=True)
 
-BATCH1_TOL = 2e-3
+AGREE_TOL = 5e-3
 
 CASES = {
     # name: (config, context length per listed slot, slots, max_batch)
@@ -131,7 +135,7 @@ def test_batched_matches_oracles(name):
     t2, l2, _ = compare_draft(model, orcs, cfg, sub)
     for j, s in enumerate(sub):
         i = slots.index(s)
-        assert P.relinf(l2[j], logits[i]) <= BATCH1_TOL
+        assert P.relinf(l2[j], logits[i]) <= AGREE_TOL
     model.close()
 
 
@@ -159,7 +163,7 @@ def test_batched_single_equals_batch1():
         for what in (dfl.DBG_KCACHE, dfl.DBG_VCACHE):
             a = dfl.dflare_debug_read_seq(model.h, what, 0, i, (L, cfg.n_kv_heads, cfg.head_dim))
             b = dfl.dflare_debug_read_seq(model.h, what, 1, i, (L, cfg.n_kv_heads, cfg.head_dim))
-            assert P.relinf(b, a) <= BATCH1_TOL, (i, what)
+            assert P.relinf(b, a) <= AGREE_TOL, (i, what)
     for step in range(2):
         ids = slot_ids(cfg, 0, step)
         t1 = model.draft_block(ids_tensor(ids)).cpu().numpy()
@@ -168,13 +172,14 @@ def test_batched_single_equals_batch1():
         zb = dfl.dflare_debug_read(model.h, dfl.DBG_BLOGITS, 0, (1, cfg.block_size, cfg.vocab))[0]
         ref = orc.draft_block(ids)
         assert P.relinf(zb, ref["logits"]) <= P.REL_TOL
-        assert P.relinf(zb, z1) <= BATCH1_TOL
+        assert P.relinf(zb, z1) <= AGREE_TOL
         P.check_tokens(t1, ref["logits"])
         P.check_tokens(tb, ref["logits"])
         # the batched call on slot 0 reads the batch-1 context
         t0 = model.draft_block_batched([0], ids_tensor(ids[None])).cpu().numpy()[0]
         z0 = dfl.dflare_debug_read(model.h, dfl.DBG_BLOGITS, 0, (1, cfg.block_size, cfg.vocab))[0]
-        assert P.relinf(z0, z1) <= BATCH1_TOL
+        assert P.relinf(z0, z1) <= AGREE_TOL
+        assert P.relinf(z0, zb) <= AGREE_TOL
         P.check_tokens(t0, ref["logits"])
     model.close()
 
