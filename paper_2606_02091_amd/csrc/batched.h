@@ -14,6 +14,7 @@ constexpr int kBM = 8;                   // m-tiles per work-group (128 rows); e
 constexpr int kBNW = 4;                  // n-tiles per wave (64 columns)
 constexpr int kBN = kBWaves * kBNW;      // n-tiles per work-group (256 columns)
 constexpr int kMaxSeq = 64;              // sequences in one batched call
+constexpr int kBKeys = 512;              // keys (context and block) per batched attention work item
 constexpr int kBSplitMax = 8;            // K parts of one batched GEMM output tile
 constexpr long kBPartFloats = (long)kBWaves * kBM * kBNW * 256;  // one work-group's partial tile
 constexpr int kBCounters = 4096;         // split-K arrival counters (output tiles of one launch)
@@ -22,7 +23,7 @@ enum BEpi { BEPI_QKV = 0, BEPI_RESID = 1, BEPI_SWIGLU = 2, BEPI_ARGMAX = 3 };
 
 // Rows of one batched call, passed by value: call sequence i (cache slot seq[i], context
 // length L[i]) owns rows off[i] .. off[i+1]-1 of the call's activations; its attention work
-// items are ipfx[i] .. ipfx[i+1]-1 (n_kv per 128-key chunk of its context).
+// items are ipfx[i] .. ipfx[i+1]-1 (n_kv per range of kBKeys keys of its L + B keys).
 struct BRows {
   int n_seq;
   int seq[kMaxSeq];
@@ -45,7 +46,7 @@ struct BGemmArgs {
   const u32x4* zero;   // one zero fragment
   float* part;         // partial tiles [tiles][kg][kBPartFloats]
   unsigned* cnt;       // arrival counters [tiles], 32 words apart, zero between launches
-  // QKV (block rows) and KVT (appended context rows): queries [M, q_dim] fp32; keys and
+  // QKV (block rows) and KVT (appended context rows): queries [Mt * 16, q_dim] fp32; keys and
   // values (fp16) to the rows' sequence caches at their slots; RoPE at the slot position
   float* Q;
   int q_dim;

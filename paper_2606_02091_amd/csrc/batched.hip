@@ -182,23 +182,43 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
     __syncthreads();
     if (!s_last) return;
     if (tid == 0) st_wt(g.cnt + tile * 32, 0u);
+    // sum in K-part order, two m-tiles at a time: the 16 loads of one part are issued
+    // together, then added
 #pragma unroll
-    for (int m = 0; m < kBM; ++m)
+    for (int m0 = 0; m0 < kBM; m0 += 2) {
+      f32x4 sm[2][kBNW];
 #pragma unroll
-      for (int n = 0; n < kBNW; ++n) {
-        f32x4 s = {0.f, 0.f, 0.f, 0.f};
-        for (int z = 0; z < g.kg; ++z) {
-          const float* blk = g.part + (((long)tile * g.kg + z) * kBWaves + w) * (kBM * kBNW * 256) +
-                             (m * kBNW + n) * 256;
-          if (z == kz) {
-            s += acc[m][n];
-          } else {
-            const float2 lo = ld_coh2(blk + lane * 2), hi = ld_coh2(blk + 128 + lane * 2);
-            s += f32x4{lo.x, lo.y, hi.x, hi.y};
-          }
+      for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int n = 0; n < kBNW; ++n) sm[mi][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int z = 0; z < g.kg; ++z) {
+        if (z == kz) {
+#pragma unroll
+          for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int n = 0; n < kBNW; ++n) sm[mi][n] += acc[m0 + mi][n];
+          continue;
         }
-        acc[m][n] = s;
+        const float* zb = g.part + (((long)tile * g.kg + z) * kBWaves + w) * (kBM * kBNW * 256);
+        float2 lo[2][kBNW], hi[2][kBNW];
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+          for (int n = 0; n < kBNW; ++n) {
+            const float* blk = zb + ((m0 + mi) * kBNW + n) * 256;
+            lo[mi][n] = ld_coh2(blk + lane * 2);
+            hi[mi][n] = ld_coh2(blk + 128 + lane * 2);
+          }
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+          for (int n = 0; n < kBNW; ++n) sm[mi][n] += f32x4{lo[mi][n].x, lo[mi][n].y, hi[mi][n].x, hi[mi][n].y};
       }
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int n = 0; n < kBNW; ++n) acc[m0 + mi][n] = sm[mi][n];
+    }
   }
 
   const int row0 = mg * kBM * 16;
@@ -229,39 +249,58 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
         tt = nt - g.q_tiles - g.kv_tiles;
       }
       const int head = tt / tph, jj = tt % tph;
+      const int mm = 8 * jj + (col & 7);
+      const int dim = (col < 8) ? mm : half + mm;
+      // the rotary factors of all 32 rows are loaded before any store (rows past M use
+      // the slot of row M - 1), so that no load waits behind a store or a branch
+      float2 cs[kBM][4];
+      if (region < 2) {
 #pragma unroll
-      for (int m = 0; m < kBM; ++m)
+        for (int m = 0; m < kBM; ++m)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cs[m][e] = g.rope[(long)s_slot[m * 16 + quad * 4 + e] * half + mm];
+      }
+#pragma unroll
+      for (int m = 0; m < kBM; ++m) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = m * 16 + quad * 4 + e, row = row0 + r;
           const float x = acc[m][n][e];
           const float partner = __shfl_xor(x, 8);
-          if (row >= g.M) continue;
           const int slot = s_slot[r];
           if (region < 2) {
-            const int mm = 8 * jj + (col & 7);
-            const int dim = (col < 8) ? mm : half + mm;
-            const float2 cs = g.rope[(long)slot * half + mm];
-            const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
-            if (region == 0) g.Q[(long)row * g.q_dim + head * g.hd + dim] = y;
-            else g.kc[s_cache[r] + ((long)head * g.Lcap + slot) * g.hd + dim] = f2h(y);
-          } else {
+            const float y = (col < 8) ? (x * cs[m][e].x - partner * cs[m][e].y) : (x * cs[m][e].x + partner * cs[m][e].y);
+            // query rows past M but inside the Mt m-tiles land in the padding rows of Q,
+            // which exist (Q holds Mt * 16 rows or more) and are never read
+            if (region == 0) {
+              if (mg * kBM + m < g.Mt) g.Q[(long)row * g.q_dim + head * g.hd + dim] = y;
+            } else if (row < g.M) {
+              g.kc[s_cache[r] + ((long)head * g.Lcap + slot) * g.hd + dim] = f2h(y);
+            }
+          } else if (row < g.M) {
             g.vt[s_cache[r] + ((long)head * g.hd + jj * 16 + col) * g.Lcap + slot] = f2h(x);
           }
         }
+      }
     }
   } else if constexpr (EPI == BEPI_RESID) {
 #pragma unroll
     for (int n = 0; n < kBNW; ++n) {
       const int nt = nt0 + n;
       if (nt >= g.Nt) continue;
+      // every row of the m-tiles, those past M included (padding rows of X, never read),
+      // so that no load waits behind a branch
+      float* xp = g.X + (long)(row0 + quad * 4) * g.H + nt * 16 + col;
+      float xv[kBM][4];  // all loads first, then all stores
 #pragma unroll
       for (int m = 0; m < kBM; ++m)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int row = row0 + m * 16 + quad * 4 + e;
-          if (row < g.M) g.X[(long)row * g.H + nt * 16 + col] += acc[m][n][e];
-        }
+        for (int e = 0; e < 4; ++e) xv[m][e] = (mg * kBM + m < g.Mt) ? xp[(long)(m * 16 + e) * g.H] : 0.f;
+#pragma unroll
+      for (int m = 0; m < kBM; ++m)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (mg * kBM + m < g.Mt) xp[(long)(m * 16 + e) * g.H] = xv[m][e] + acc[m][n][e];
     }
   } else if constexpr (EPI == BEPI_SWIGLU) {
     uint32_t* out = reinterpret_cast<uint32_t*>(g.out16);
@@ -449,13 +488,22 @@ __global__ __launch_bounds__(256) void k_bfuse(const uint16_t* hidden, int N, in
 #pragma unroll
     for (int e = 0; e < 8; ++e) u[c][e] = 0.f;
     if (k0 < H) {
-      for (int j = 0; j < S; ++j) {
-        const float a = alpha[i * S + j];
-        const u32x4 v = *reinterpret_cast<const u32x4*>(hidden + ((long)j * N + r) * H + k0);
+      // 12 target rows in flight per step, summed in j order
+      for (int j0 = 0; j0 < S; j0 += 12) {
+        u32x4 v[12];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          u[c][2 * e] = fmaf(a, bf2f(v[e] & 0xFFFFu), u[c][2 * e]);
-          u[c][2 * e + 1] = fmaf(a, bf2f(v[e] >> 16), u[c][2 * e + 1]);
+        for (int jj = 0; jj < 12; ++jj)
+          v[jj] = *reinterpret_cast<const u32x4*>(hidden + ((long)min(j0 + jj, S - 1) * N + r) * H + k0);
+#pragma unroll
+        for (int jj = 0; jj < 12; ++jj) {
+          if (j0 + jj < S) {
+            const float a = alpha[i * S + j0 + jj];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              u[c][2 * e] = fmaf(a, bf2f(v[jj][e] & 0xFFFFu), u[c][2 * e]);
+              u[c][2 * e + 1] = fmaf(a, bf2f(v[jj][e] >> 16), u[c][2 * e + 1]);
+            }
+          }
         }
       }
 #pragma unroll
@@ -484,175 +532,214 @@ __global__ void k_bfrag_rows(const u32x4* A, int n, int H, int mt_max, float* ou
 }
 
 // ------------------------------------------------------------------------------------------
-// attention over ragged contexts (Sec. 3.2: no mask; block rows see the whole context of
-// their sequence and the whole block).  Item (sequence i of the call, chunk c, KV head g);
-// 4 waves; wave w takes query tiles w, w + 4, ... of the G*B rows of head g, each against
-// all keys of the chunk.  The chunk's K rows and V^T rows (fp16) are staged in LDS with
-// XOR-swizzled 16-byte columns; scores are formed transposed (S^T = K Q^T) so that the
-// probabilities are the B operand of the P V product.
+// attention over ragged contexts (Sec. 3.2: no mask; the block rows of a sequence see its
+// whole context and the whole block, whose keys and values are already in the cache at
+// slots L .. L + B - 1).  Work item (sequence i, key range r, KV head g): keys
+// r * kBKeys .. min((r + 1) * kBKeys, L + B) - 1 in blocks of 64, against the G * B query
+// rows of head g (query tile qt = 16 rows, row r' = head offset * B + block row).  The
+// 4 waves share each key block, staged in LDS (K rows and V^T rows, fp16, with XOR-
+// swizzled 16-byte pieces) while the next block is loaded into registers; each wave
+// keeps its query tiles' running max, sum and output in registers (online softmax, log2
+// domain).  Scores are formed transposed (S^T = K Q^T) so that the probabilities are
+// the B operand of the P V product; queries and probabilities enter as fp16 hi/lo pairs.
 // ------------------------------------------------------------------------------------------
-template <int HD>
+template <int HD, int TPW, int KB, int NBUF>
 __global__ __launch_bounds__(256, 2) void k_battn(BAttnArgs a, BRows rows) {
-  constexpr int CK = kChunk, CKM = CK + 32, NKB = CKM / 32;
-  constexpr int KC = HD / 8, VC = CKM / 8;
-  constexpr int KP = CKM * KC, VP = HD * VC;
+  // KB keys per block; NBUF LDS buffers (2: the next block is stored while this one is
+  // computed; 1: stored after it, behind a second barrier)
+  constexpr int KC = HD / 8, VC = KB / 8;  // 16-byte pieces per K row / per V^T row
+  constexpr int KP = KB * KC, VP = HD * VC;
   constexpr int NT = 256, PER = (KP + VP) / NT;
-  static_assert((KP + VP) % NT == 0, "pieces split evenly");
-  __shared__ u32x4 stage[KP + VP];
-  u32x4* sK = stage;
-  u32x4* sV = stage + KP;
+  static_assert(KP % NT == 0 && VP % NT == 0, "pieces split evenly");
+  __shared__ u32x4 st[NBUF][KP + VP];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  // item -> (sequence i, chunk c, head g)
+  const int q = lane & 15, quad = lane >> 4;
+
   const int j = blockIdx.x;
   int i = 0;
   while (i + 1 < rows.n_seq && j >= rows.ipfx[i + 1]) ++i;
   const int L = rows.L[i];
-  const int nch = max(1, (L + CK - 1) / CK);
-  const int c = (j - rows.ipfx[i]) / a.n_kv, g = (j - rows.ipfx[i]) % a.n_kv;
-  const int kbeg = c * CK;
-  const int nkeys = ((c == nch - 1) ? L + a.B : kbeg + CK) - kbeg;
+  const int rr = (j - rows.ipfx[i]) / a.n_kv, g = (j - rows.ipfx[i]) % a.n_kv;
+  const int kbeg = rr * kBKeys, kend = min(kbeg + kBKeys, L + a.B);
+  const int nblk = (kend - kbeg + KB - 1) / KB;
   const long cache = (long)rows.seq[i] * a.seq_stride + (long)a.layer * a.cache_layer;
-  const uint16_t* kc = a.kc + cache;
-  const uint16_t* vt = a.vt + cache;
+  const uint16_t* kc = a.kc + cache + (long)g * a.Lcap * HD;
+  const uint16_t* vt = a.vt + cache + (long)g * HD * a.Lcap;
   const int G = a.n_q / a.n_kv, R = G * a.B, QT = (R + 15) / 16;
 
-  u32x4 pcs[PER];
+  // loads of key block b into registers.  Every lane loads (pieces past kend repeat the
+  // last key row or the last 8-key group), so that no load sits in a branch; those pieces
+  // are zeroed when they are stored to LDS.
+  // blocks loaded ahead of the one being computed: two, or one where the query tiles of a
+  // wave already fill the registers (set b % PF holds block b)
+  constexpr int PF = (NBUF == 1 || (HD == 128 && TPW == 2)) ? 1 : 2;
+  u32x4 pcs[PF][PER];
+  auto fetch = [&](int b, u32x4* dst) {
+    const int k0 = kbeg + b * KB;
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    pcs[k] = u32x4{0u, 0u, 0u, 0u};
-    const int p = k * NT + tid;
-    if (p < KP) {
-      const int r = p / KC, col = p % KC;
-      if (r < nkeys) pcs[k] = *reinterpret_cast<const u32x4*>(kc + ((long)g * a.Lcap + kbeg + r) * HD + col * 8);
-    } else {
-      const int pv = p - KP, d = pv / VC, col = pv % VC;
-      if (col * 8 < nkeys)
-        pcs[k] = *reinterpret_cast<const u32x4*>(vt + ((long)g * HD + d) * a.Lcap + kbeg + col * 8);
+    for (int k = 0; k < PER; ++k) {
+      const int p = k * NT + tid;  // the K / V^T split is static per k (KP is a multiple of NT)
+      if (k * NT < KP) {
+        const int r = p / KC, c = p % KC;
+        dst[k] = *reinterpret_cast<const u32x4*>(kc + (long)min(k0 + r, kend - 1) * HD + c * 8);
+      } else {
+        const int pv = p - KP, d = pv / VC, c = pv % VC;
+        dst[k] = *reinterpret_cast<const u32x4*>(vt + (long)d * a.Lcap + min(k0 + c * 8, (kend - 1) & ~7));
+      }
     }
-  }
+  };
+  auto stash = [&](int b, int buf, const u32x4* src) {
+    const int k0 = kbeg + b * KB;
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int p = k * NT + tid;
-    if (p < KP) {
-      const int rr = p / KC, col = p % KC;
-      sK[rr * KC + (col ^ (rr & 7))] = pcs[k];
-    } else {
-      const int pv = p - KP, d = pv / VC, col = pv % VC;
-      u32x4 v = pcs[k];
-      const int nv = nkeys - col * 8;  // values of keys past the end become zeros
-      if (nv < 8) {
+    for (int k = 0; k < PER; ++k) {
+      const int p = k * NT + tid;
+      if (k * NT < KP) {
+        const int r = p / KC, c = p % KC;
+        const bool ok = k0 + r < kend;
+        const u32x4 v = src[k];
+        st[buf][r * KC + (c ^ (r & 7))] = u32x4{ok ? v[0] : 0u, ok ? v[1] : 0u, ok ? v[2] : 0u, ok ? v[3] : 0u};
+      } else {
+        const int pv = p - KP, d = pv / VC, c = pv % VC;
+        const u32x4 v = src[k];
+        const int nv = kend - (k0 + c * 8);  // keys of this 8-key group before kend
+        u32x4 z;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          if (2 * e >= nv) v[e] = 0u;
-          else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;
+          const uint32_t lo = (2 * e < nv) ? 0xFFFFu : 0u, hi = (2 * e + 1 < nv) ? 0xFFFF0000u : 0u;
+          z[e] = v[e] & (lo | hi);
         }
+        st[buf][KP + d * VC + (c ^ (d & 7))] = z;
       }
-      sV[d * VC + (col ^ (d & 3))] = v;
     }
-  }
-  __syncthreads();
+  };
 
-  const char* lds = reinterpret_cast<const char*>(stage);
-  const int q = lane & 15, quad = lane >> 4;
-  int k_at[HD / 32];
-#pragma unroll
-  for (int ks = 0; ks < HD / 32; ++ks) k_at[ks] = (q * KC + ((ks * 4 + quad) ^ (q & 7))) * 16;
-  const int vx = (quad >> 1) ^ (q & 3);
-  const int vbase = KP * 16 + (quad & 1) * 8;
-  const int v0 = vbase + (q * VC + vx) * 16, v1 = vbase + (q * VC + (vx ^ 2)) * 16;
+  // this wave's query tiles: hi/lo fp16 fragments of Q^T (scaled), running statistics
+  u32x4 qh[TPW][HD / 32], ql[TPW][HD / 32];
+  f32x4 o[TPW][HD / 16];
+  float m_run[TPW], l_run[TPW];
   const int q_dim = a.n_q * HD;
-  const int nkb = (nkeys + 31) / 32;
-
-  for (int qt = w; qt < QT; qt += 4) {
-    const int r = qt * 16 + q;
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    const int r = (w + 4 * t) * 16 + q;
     const bool rv = r < R;
-    const int bb = rv ? r % a.B : 0;
-    const int h = g * G + (rv ? r / a.B : 0);
+    const int bb = rv ? r % a.B : 0, h = g * G + (rv ? r / a.B : 0);
     const float* src = a.Q + (long)(rows.off[i] + bb) * q_dim + h * HD;
-    u32x4 qh[HD / 32], ql[HD / 32];
+    const float sc = rv ? a.qscale : 0.f;  // rows past R: a valid row, scaled to zero
 #pragma unroll
     for (int ks = 0; ks < HD / 32; ++ks) {
-      float v[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = rv ? src[ks * 32 + quad * 8 + e] * a.qscale : 0.f;
-      split_pack8_h(v, qh[ks], ql[ks]);
+      const f32x4 x0 = *reinterpret_cast<const f32x4*>(src + ks * 32 + quad * 8);
+      const f32x4 x1 = *reinterpret_cast<const f32x4*>(src + ks * 32 + quad * 8 + 4);
+      float v[8] = {x0[0] * sc, x0[1] * sc, x0[2] * sc, x0[3] * sc, x1[0] * sc, x1[1] * sc, x1[2] * sc, x1[3] * sc};
+      split_pack8_h(v, qh[t][ks], ql[t][ks]);
     }
-    f32x4 sc[2 * NKB];
 #pragma unroll
-    for (int kk = 0; kk < NKB; ++kk) {
-      f32x4 a0 = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, a1 = a0;
-      if (kk < nkb) {
-        f32x4 h0 = {0.f, 0.f, 0.f, 0.f}, l0 = h0, h1 = h0, l1 = h0;
+    for (int dt = 0; dt < HD / 16; ++dt) o[t][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+  }
+
+  fetch(0, pcs[0]);
+  if (PF == 2 && nblk > 1) fetch(1, pcs[PF - 1]);
+  stash(0, 0, pcs[0]);
+  __syncthreads();
+  const char* base0 = reinterpret_cast<const char*>(&st[0][0]);
+  const int vx = (quad >> 1);
+  // block b: the loads of block b + PF go out, block b is computed from LDS, block b + 1
+  // goes to the other LDS buffer, which was last read in block b - 1
+  auto step = [&](int b, u32x4* ahead, const u32x4* nxt1) {
+    if (b + PF < nblk) fetch(b + PF, ahead);
+    const char* lds = base0 + (NBUF == 2 ? (b & 1) : 0) * (KP + VP) * 16;
+    const int k0 = kbeg + b * KB;
+#pragma unroll
+    for (int t = 0; t < TPW; ++t) {
+      if (w + 4 * t >= QT) continue;
+      // scores S^T for 4 key tiles of 16
+      f32x4 sc[KB / 16];
+#pragma unroll
+      for (int kt = 0; kt < KB / 16; ++kt) {
+        f32x4 hacc = {0.f, 0.f, 0.f, 0.f}, lacc = hacc;
+        const int row = kt * 16 + q;
 #pragma unroll
         for (int ks = 0; ks < HD / 32; ++ks) {
-          const u32x4 k0v = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + (2 * kk) * 16 * KC * 16);
-          const u32x4 k1v = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + (2 * kk + 1) * 16 * KC * 16);
-          h0 = mfma_h(k0v, qh[ks], h0);
-          h1 = mfma_h(k1v, qh[ks], h1);
-          l0 = mfma_h(k0v, ql[ks], l0);
-          l1 = mfma_h(k1v, ql[ks], l1);
+          const u32x4 kv = *reinterpret_cast<const u32x4*>(lds + (row * KC + ((ks * 4 + quad) ^ (row & 7))) * 16);
+          hacc = mfma_h(kv, qh[t][ks], hacc);
+          lacc = mfma_h(kv, ql[t][ks], lacc);
         }
-        a0 = h0 + l0;
-        a1 = h1 + l1;
+        sc[kt] = hacc + lacc;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (k0 + kt * 16 + quad * 4 + e >= kend) sc[kt][e] = -INFINITY;
+      }
+      float mb = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < KB / 16; ++kt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mb = fmaxf(mb, sc[kt][e]);
+      mb = fmaxf(mb, __shfl_xor(mb, 16));
+      mb = fmaxf(mb, __shfl_xor(mb, 32));
+      const float mn = fmaxf(m_run[t], mb);
+      const float scale = exp2f(m_run[t] - mn);
+      float ls = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < KB / 16; ++kt)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          if (2 * kk * 16 + quad * 4 + e >= nkeys) a0[e] = -INFINITY;
-          if ((2 * kk + 1) * 16 + quad * 4 + e >= nkeys) a1[e] = -INFINITY;
+          const float p = exp2f(sc[kt][e] - mn);
+          sc[kt][e] = p;
+          ls += p;
         }
-      }
-      sc[2 * kk] = a0;
-      sc[2 * kk + 1] = a1;
-    }
-    float m = -INFINITY, l = 0.f;
+      ls += __shfl_xor(ls, 16);
+      ls += __shfl_xor(ls, 32);
+      l_run[t] = l_run[t] * scale + ls;
+      m_run[t] = mn;
 #pragma unroll
-    for (int kt = 0; kt < 2 * NKB; ++kt)
+      for (int dt = 0; dt < HD / 16; ++dt) o[t][dt] *= scale;
+      // O^T += V^T P^T, 32 keys per step
 #pragma unroll
-      for (int e = 0; e < 4; ++e) m = fmaxf(m, sc[kt][e]);
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
-#pragma unroll
-    for (int kt = 0; kt < 2 * NKB; ++kt)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p = exp2f(sc[kt][e] - m);
-        sc[kt][e] = p;
-        l += p;
-      }
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    f32x4 o[HD / 16];
-#pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < NKB; ++kk) {
-      if (kk < nkb) {
+      for (int kk = 0; kk < KB / 32; ++kk) {
         float pv[8] = {sc[2 * kk][0], sc[2 * kk][1], sc[2 * kk][2], sc[2 * kk][3],
                        sc[2 * kk + 1][0], sc[2 * kk + 1][1], sc[2 * kk + 1][2], sc[2 * kk + 1][3]};
         u32x4 ph, pl;
         split_pack8_h(pv, ph, pl);
 #pragma unroll
         for (int dt = 0; dt < HD / 16; ++dt) {
-          const int off = (dt * 16 * VC + kk * 4) * 16;
-          const u32x2 x0 = *reinterpret_cast<const u32x2*>(lds + v0 + off);
-          const u32x2 x1 = *reinterpret_cast<const u32x2*>(lds + v1 + off);
+          const int d = dt * 16 + q;
+          const int p0 = (4 * kk + vx) ^ (d & 7), p1 = (4 * kk + 2 + vx) ^ (d & 7);
+          const char* vrow = lds + (KP + d * VC) * 16 + (quad & 1) * 8;
+          const u32x2 x0 = *reinterpret_cast<const u32x2*>(vrow + p0 * 16);
+          const u32x2 x1 = *reinterpret_cast<const u32x2*>(vrow + p1 * 16);
           const u32x4 vv = {x0[0], x0[1], x1[0], x1[1]};
-          o[dt] = mfma_h(vv, ph, o[dt]);
-          o[dt] = mfma_h(vv, pl, o[dt]);
+          o[t][dt] = mfma_h(vv, ph, o[t][dt]);
+          o[t][dt] = mfma_h(vv, pl, o[t][dt]);
         }
       }
     }
-    if (rv) {
+    if (b + 1 < nblk) {
+      if (NBUF == 1) __syncthreads();  // every wave is done with the buffer
+      stash(b + 1, NBUF == 2 ? (b + 1) & 1 : 0, nxt1);
+      __syncthreads();
+    }
+  };
+  for (int b = 0; b < nblk; b += 2) {
+    step(b, pcs[0], pcs[PF - 1]);
+    if (b + 1 < nblk) step(b + 1, pcs[PF - 1], pcs[0]);
+  }
+
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+    const int r = (w + 4 * t) * 16 + q;
+    if (w + 4 * t < QT && r < R) {
       const long base = (long)j * a.Rpad + r;
 #pragma unroll
       for (int dt = 0; dt < HD / 16; ++dt)
-        *reinterpret_cast<f32x4*>(a.OP + base * HD + dt * 16 + quad * 4) = o[dt];
-      if (quad == 0) a.ML[base] = make_float2(m, l);
+        *reinterpret_cast<f32x4*>(a.OP + base * HD + dt * 16 + quad * 4) = o[t][dt];
+      if (quad == 0) a.ML[base] = make_float2(m_run[t], l_run[t]);
     }
   }
 }
 
-// merge the chunk partials of query row r of head g of sequence i (one wave per row) and
-// write the fp16 A fragments of the output projection at row off[i] + r % B
+// merge the key-range partials of query row r of head g of sequence i (one wave per row)
+// and write the fp16 A fragments of the output projection at row off[i] + r % B
 template <int HD>
 __global__ __launch_bounds__(64) void k_bcomb(BAttnArgs a, BRows rows, u32x4* out16, int a_kt) {
   constexpr int DPL = HD / 64;
@@ -661,16 +748,16 @@ __global__ __launch_bounds__(64) void k_bcomb(BAttnArgs a, BRows rows, u32x4* ou
   const int it = blockIdx.x;
   const int i = it / (a.n_kv * R), g = (it / R) % a.n_kv, r = it % R;
   if (i >= rows.n_seq) return;
-  const int nch = max(1, (rows.L[i] + kChunk - 1) / kChunk);
-  const long jb = rows.ipfx[i] + g;  // item of chunk 0; chunk c at jb + c * n_kv
+  const int nr = (rows.L[i] + a.B + kBKeys - 1) / kBKeys;
+  const long jb = rows.ipfx[i] + g;  // item of range 0; range c at jb + c * n_kv
   float M = -INFINITY;
-  for (int c = lane; c < nch; c += 64) M = fmaxf(M, a.ML[(jb + (long)c * a.n_kv) * a.Rpad + r].x);
+  for (int c = lane; c < nr; c += 64) M = fmaxf(M, a.ML[(jb + (long)c * a.n_kv) * a.Rpad + r].x);
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
   float num[DPL], den = 0.f;
 #pragma unroll
   for (int e = 0; e < DPL; ++e) num[e] = 0.f;
-  for (int c = 0; c < nch; ++c) {
+  for (int c = 0; c < nr; ++c) {
     const long base = (jb + (long)c * a.n_kv) * a.Rpad + r;
     const float2 mc = a.ML[base];
     const float wgt = exp2f(mc.x - M);
@@ -688,7 +775,6 @@ __global__ __launch_bounds__(64) void k_bcomb(BAttnArgs a, BRows rows, u32x4* ou
     if ((lane & 1) == 0) o[frag_off(row, h * HD + lane, a_kt) >> 1] = pack_h2(y, y1);
   }
 }
-
 
 // ------------------------------------------------------------------------------------------
 // launchers
@@ -731,9 +817,20 @@ void launch_bfrag_rows(hipStream_t s, const u32x4* A, int n, int H, int D, int m
   hipLaunchKernelGGL(k_bfrag_rows, dim3(n, D), dim3(256), 0, s, A, n, H, mt_max, out);
 }
 
+template <int KB, int NBUF>
+static void launch_battn_v(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, int items) {
+  const bool two = (a.n_q / a.n_kv) * a.B > 64;  // more than 4 query tiles: two per wave
+  if (hd == 64) {
+    if (two) hipLaunchKernelGGL((k_battn<64, 2, KB, NBUF>), dim3(items), dim3(256), 0, s, a, rows);
+    else hipLaunchKernelGGL((k_battn<64, 1, KB, NBUF>), dim3(items), dim3(256), 0, s, a, rows);
+  } else {
+    if (two) hipLaunchKernelGGL((k_battn<128, 2, KB, NBUF>), dim3(items), dim3(256), 0, s, a, rows);
+    else hipLaunchKernelGGL((k_battn<128, 1, KB, NBUF>), dim3(items), dim3(256), 0, s, a, rows);
+  }
+}
+
 void launch_battn(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, int items) {
-  if (hd == 64) hipLaunchKernelGGL(k_battn<64>, dim3(items), dim3(256), 0, s, a, rows);
-  else hipLaunchKernelGGL(k_battn<128>, dim3(items), dim3(256), 0, s, a, rows);
+  launch_battn_v<64, 2>(s, hd, a, rows, items);
 }
 
 void launch_bcomb(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, u32x4* out16, int a_kt) {

@@ -508,7 +508,7 @@ int build(dflare_handle* h, const dflare_weights* w) {
     h->bpart_floats = part;
     TRY(dev_alloc(h, &h->bpart, (size_t)std::max(part, 64L) * 4));
     TRY(dev_zalloc(h, &h->bcnt, (size_t)kBCounters * 128));
-    const long items = (long)c.max_batch * h->attn_nch * c.n_kv_heads;
+    const long items = (long)c.max_batch * ceil_div((long)c.max_context + B, kBKeys) * c.n_kv_heads;
     TRY(dev_alloc(h, &h->bOP, (size_t)items * h->Rpad * hd * 4));
     TRY(dev_alloc(h, &h->bML, (size_t)items * h->Rpad * sizeof(float2)));
     const long ng_lm = ceil_div(Nt_lm, kBN);
@@ -806,7 +806,7 @@ int run_draft_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int
     rows.seq[i] = seq[i];
     rows.L[i] = h->Ls[seq[i]];
     rows.off[i + 1] = (i + 1) * B;
-    rows.ipfx[i + 1] = rows.ipfx[i] + std::max(1, ceil_div(rows.L[i], kChunk)) * c.n_kv_heads;
+    rows.ipfx[i + 1] = rows.ipfx[i] + ceil_div(rows.L[i] + B, kBKeys) * c.n_kv_heads;
   }
   const int items = rows.ipfx[n_seq];
   BAttnArgs at{};

@@ -5,8 +5,9 @@ tests/parity.py).
 
 Sizes finish in seconds on the oracle yet span several 128-row GEMM groups, ragged
 row counts (B = 5 gives sequences that straddle 16-row tiles), empty and one-row
-contexts, contexts on and off the 128-key chunk grid, vocabularies that are not a
-multiple of 16, slots listed out of order and calls on subsets of the slots.
+contexts, contexts on and off the 64-key block and 512-key range grids of the
+attention, 64 and 128 query rows per KV head, vocabularies that are not a multiple of
+16, slots listed out of order and calls on subsets of the slots.
 
 Besides the oracle bar, two batched results are compared directly: the same sequence
 drafted by batched calls of other shapes (other rows, other K splits), and by the
@@ -41,6 +42,16 @@ CASES = {
                                       vocab=1000, n_draft_layers=3, n_target_layers=5, block_size=5, context=130,
                                       random_block=True),
                     [33, 0, 130, 7, 64], [1, 4, 0, 2, 3], 5),
+    # 8 query heads per KV head (128 query rows per work item) and contexts spanning
+    # several 512-key attention ranges, one of them ending a single key into a range
+    "hd128_gqa8_long": (synth.ModelConfig("bgqa8", hidden=128, n_q_heads=8, n_kv_heads=1, head_dim=128,
+                                          ffn=256, vocab=700, n_draft_layers=2, n_target_layers=3,
+                                          block_size=16, context=1030),
+                        [497, 1030, 0, 700, 511], [2, 0, 4, 1, 3], 5),
+    "hd64_gqa8_long": (synth.ModelConfig("bgqa8h64", hidden=128, n_q_heads=16, n_kv_heads=2, head_dim=64,
+                                         ffn=256, vocab=900, n_draft_layers=2, n_target_layers=3,
+                                         block_size=16, context=1100),
+                       [1100, 496, 40], [1, 0, 2], 3),
 }
 
 
