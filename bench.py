@@ -78,19 +78,29 @@ def kernel_bytes(cfg, L, n_mean):
     }
 
 
-def counter_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` measured with rocprofv3 byte counters, if the
-    recorded measurement belongs to the kernel source of this build; else None."""
+KERNEL_SOURCES = ("kernels.hip", "batched.hip", "device_common.h", "dflare_impl.h", "batched.h")
+
+
+def source_sha() -> str:
+    """sha256 prefix of the device sources the recorded counter values belong to."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "hbm_counters_qwen3_8b.json")
-    src = os.path.join(ROOT, "paper_2606_02091_amd", "csrc", "kernels.hip")
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_02091_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(kernel: str, record: str = "hbm_counters_qwen3_8b.json"):
+    """HBM bytes per launch of `kernel` measured with rocprofv3 byte counters, if the
+    recorded measurement belongs to the device sources of this build; else None."""
     try:
-        rec = json.load(open(path))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        rec = json.load(open(os.path.join(ROOT, "profiles", record)))
+        sha = source_sha()
     except (OSError, ValueError):
         return None
     k = rec.get("kernels", {}).get(kernel)
-    if rec.get("kernels_hip_sha256_16") != sha or k is None:
+    if rec.get("sources_sha256_16") != sha or k is None:
         return None
     return int(k["fetch_kib"] * 1024 * rec["fetch_scale"] + k["write_kib"] * 1024 * rec["write_scale"])
 
@@ -368,7 +378,8 @@ def bench_batched(args):
                                f"n_new ~ U{{1..16}} per sequence per step, B={B}",
                    "global_batch": n_seq, "seq_len": int(max(lengths)), "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": d["TFLOPs"], "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(d["TFLOPs"] / MFMA_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+                     "frac": round(d["TFLOPs"] / MFMA_PEAK_TFLOPS, 4),
+                     "traffic": counter_traffic(dom, "hbm_counters_batched.json"), "kernel": dom,
                      "flops_per_launch": d["flops_per_launch"], "avg_us": d["avg_us"]},
         "step_roofline": {"flops_per_step": int(step_flops), "bytes_per_step": int(step_bytes),
                           "mfma_frac": round(step_flops / (ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS, 4),
