@@ -29,6 +29,9 @@ Readings where the paper is silent:
 Weights use the [out, in] row-major convention: y = x @ W.T (the paper writes x W
 with W in R^{d x d_kv}; it is the same map).
 
+Temperature sampling (Sec. 5, Table 1 lower half): Gumbel-max draws with uniforms from
+Philox4x64-10; see sample_tokens.
+
 Parity pins: see tests/test_oracle_pins.py (closed forms, invariants, brute force,
 library routines).  Parity unpinned: the readings above that the paper leaves
 open (layer internals, rotary convention, positions) -- any consistent reading
@@ -43,7 +46,7 @@ import numpy as np
 __all__ = [
     "bf16_to_f64", "fusion_weights", "rms_norm", "rope", "silu", "fuse_rows",
     "context_kv", "block_attention", "draft_layer", "lm_head_logits", "argmax_lowest",
-    "DraftOracle",
+    "philox4x64_10", "sampling_uniforms", "sample_tokens", "DraftOracle",
 ]
 
 
@@ -192,6 +195,68 @@ def argmax_lowest(z: np.ndarray) -> np.ndarray:
     return np.argmax(z, axis=-1).astype(np.int32)
 
 
+# ---- temperature sampling (the paper's temperature-1 decoding, Sec. 5, Table 1 lower half) ----
+# A candidate is drawn from softmax(z / T) by the Gumbel-max rule: argmax_v (z_v / T + G_v) with
+# G_v = -log(-log(U_v)) and U_v independent uniforms on (0, 1).  The uniforms come from the
+# counter-based generator Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
+# easy as 1, 2, 3", SC 2011) keyed by (seed, 0) at counter (v, b, draw, slot): vocabulary id v, block
+# position b, draw index, sequence slot; U = (top 24 bits of output word 0 + 1/2) / 2^24.  These
+# generator details are this library's convention (the paper fixes none of them).
+
+_PHILOX_M0 = np.uint64(0xD2E7470EE14C6C93)
+_PHILOX_M1 = np.uint64(0xCA5A826395121157)
+_PHILOX_W0 = np.uint64(0x9E3779B97F4A7C15)
+_PHILOX_W1 = np.uint64(0xBB67AE8584CAA73B)
+
+
+def _mulhilo64(a: np.ndarray, m: np.uint64):
+    """(high, low) 64-bit halves of the 128-bit products a * m, from 32-bit partial products."""
+    m32 = np.uint64(0xFFFFFFFF)
+    s32 = np.uint64(32)
+    a_lo, a_hi = a & m32, a >> s32
+    m_lo, m_hi = m & m32, m >> s32
+    ll, lh, hl, hh = a_lo * m_lo, a_lo * m_hi, a_hi * m_lo, a_hi * m_hi
+    mid = (ll >> s32) + (lh & m32) + (hl & m32)
+    lo = (ll & m32) | ((mid & m32) << s32)
+    hi = hh + (lh >> s32) + (hl >> s32) + (mid >> s32)
+    return hi, lo
+
+
+def philox4x64_10(counter, key):
+    """Philox4x64 with 10 rounds (Salmon et al. 2011): counter = 4 uint64 arrays (broadcast),
+    key = 2 uint64 values.  Each round multiplies words 0 and 2 by the two round constants,
+    mixes the high halves with words 1, 3 and the key, and bumps the key by the Weyl constants."""
+    c0, c1, c2, c3 = (np.asarray(x, dtype=np.uint64) for x in counter)
+    c0, c1, c2, c3 = np.broadcast_arrays(c0, c1, c2, c3)
+    k0, k1 = np.uint64(key[0]), np.uint64(key[1])
+    with np.errstate(over="ignore"):
+        for _ in range(10):
+            hi0, lo0 = _mulhilo64(c0, _PHILOX_M0)
+            hi1, lo1 = _mulhilo64(c2, _PHILOX_M1)
+            c0, c1, c2, c3 = hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0
+            k0 = np.uint64((int(k0) + int(_PHILOX_W0)) & 0xFFFFFFFFFFFFFFFF)
+            k1 = np.uint64((int(k1) + int(_PHILOX_W1)) & 0xFFFFFFFFFFFFFFFF)
+    return c0, c1, c2, c3
+
+
+def sampling_uniforms(seed: int, draw: int, slot: int, n_pos: int, vocab: int) -> np.ndarray:
+    """U[b, v] in (0, 1) for block positions b < n_pos and vocabulary ids v < vocab."""
+    v = np.arange(vocab, dtype=np.uint64)[None, :]
+    b = np.arange(n_pos, dtype=np.uint64)[:, None]
+    w0 = philox4x64_10((v, b, np.uint64(draw), np.uint64(slot)), (np.uint64(seed), np.uint64(0)))[0]
+    return ((w0 >> np.uint64(40)).astype(np.float64) + 0.5) / float(1 << 24)
+
+
+def sample_tokens(z: np.ndarray, temperature: float, seed: int, draw: int, slot: int = 0):
+    """Candidates from logits z [B, V]: greedy argmax for temperature <= 0, else the
+    Gumbel-max draw from softmax(z / temperature).  Returns (tokens, perturbed scores)."""
+    if temperature <= 0:
+        return argmax_lowest(z), z
+    u = sampling_uniforms(seed, draw, slot, z.shape[0], z.shape[1])
+    y = z / temperature - np.log(-np.log(u))
+    return argmax_lowest(y), y
+
+
 _LAYER_KINDS = ("attn_norm", "mlp_norm", "wq", "wk_d", "wv_d", "wo", "w_gate", "w_up", "w_down")
 
 
@@ -293,11 +358,14 @@ class DraftOracle:
         self.L = new_len
 
     # -- block pass ----------------------------------------------------------
-    def draft_block(self, ids, positions=None, keep_logits: bool = True) -> dict:
+    def draft_block(self, ids, positions=None, keep_logits: bool = True, temperature: float = 0.0,
+                    seed: int = 0, draw: int = 0, slot: int = 0) -> dict:
         """One drafting forward pass over the block ids [B]  (Sec. 3.2).
 
         Returns dict(tokens [B] int32, logits [B, V] (if keep_logits),
-        hidden [D, B, H] = block rows after each layer).
+        hidden [D, B, H] = block rows after each layer).  With temperature > 0 the
+        tokens are Gumbel-max draws (see sample_tokens) and "scores" holds the
+        perturbed scores z / T + G they maximise.
         """
         cfg = self.cfg
         ids = np.asarray(ids, dtype=np.int64)
@@ -309,7 +377,9 @@ class DraftOracle:
             X = draft_layer(X, self.layer_weights(i), self._k[i][:self.L], self._v[i][:self.L], pos, cfg)
             hs.append(X)
         z = lm_head_logits(X, self._gain("final_norm"), self.w["lm_head"], cfg.rms_eps)
-        out = {"tokens": argmax_lowest(z), "hidden": np.stack(hs)}
+        tokens, scores = sample_tokens(z, temperature, seed, draw, slot)
+        out = {"tokens": tokens, "hidden": np.stack(hs)}
         if keep_logits:
             out["logits"] = z
+            out["scores"] = scores
         return out

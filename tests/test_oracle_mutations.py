@@ -150,6 +150,44 @@ def _argmax_highest(z):
     return (z.shape[-1] - 1 - np.argmax(z[..., ::-1], axis=-1)).astype(np.int32)
 
 
+def _sample_exponential_noise(z, temperature, seed, draw, slot=0):
+    if temperature <= 0:
+        return orc.argmax_lowest(z), z
+    u = orc.sampling_uniforms(seed, draw, slot, z.shape[0], z.shape[1])
+    y = z / temperature - np.log(u)  # exponential, not Gumbel, noise
+    return orc.argmax_lowest(y), y
+
+
+def _sample_temperature_multiplies(z, temperature, seed, draw, slot=0):
+    if temperature <= 0:
+        return orc.argmax_lowest(z), z
+    u = orc.sampling_uniforms(seed, draw, slot, z.shape[0], z.shape[1])
+    y = z * temperature - np.log(-np.log(u))
+    return orc.argmax_lowest(y), y
+
+
+def _philox_no_key_schedule(counter, key):
+    c0, c1, c2, c3 = np.broadcast_arrays(*(np.asarray(x, dtype=np.uint64) for x in counter))
+    k0, k1 = np.uint64(key[0]), np.uint64(key[1])
+    for _ in range(10):
+        hi0, lo0 = orc._mulhilo64(c0, orc._PHILOX_M0)
+        hi1, lo1 = orc._mulhilo64(c2, orc._PHILOX_M1)
+        c0, c1, c2, c3 = hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0
+    return c0, c1, c2, c3
+
+
+def _philox_swapped_multipliers(counter, key):
+    c0, c1, c2, c3 = np.broadcast_arrays(*(np.asarray(x, dtype=np.uint64) for x in counter))
+    k0, k1 = int(key[0]), int(key[1])
+    for _ in range(10):
+        hi0, lo0 = orc._mulhilo64(c0, orc._PHILOX_M1)
+        hi1, lo1 = orc._mulhilo64(c2, orc._PHILOX_M0)
+        c0, c1, c2, c3 = hi1 ^ c1 ^ np.uint64(k0), lo1, hi0 ^ c3 ^ np.uint64(k1), lo0
+        k0 = (k0 + int(orc._PHILOX_W0)) & 0xFFFFFFFFFFFFFFFF
+        k1 = (k1 + int(orc._PHILOX_W1)) & 0xFFFFFFFFFFFFFFFF
+    return c0, c1, c2, c3
+
+
 _ORIG = {k: getattr(orc, k) for k in ("fuse_rows", "rope", "context_kv")}
 
 MUTANTS = {
@@ -179,6 +217,10 @@ MUTANTS = {
     "layer_no_mlp_norm": ("draft_layer", _layer_variant(no_mlp_norm=True)),
     "lm_head_without_final_norm": ("lm_head_logits", _lm_no_norm),
     "argmax_ties_to_highest": ("argmax_lowest", _argmax_highest),
+    "sampling_exponential_noise": ("sample_tokens", _sample_exponential_noise),
+    "sampling_temperature_multiplies": ("sample_tokens", _sample_temperature_multiplies),
+    "philox_without_key_schedule": ("philox4x64_10", _philox_no_key_schedule),
+    "philox_multipliers_swapped": ("philox4x64_10", _philox_swapped_multipliers),
 }
 
 

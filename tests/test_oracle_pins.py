@@ -571,4 +571,81 @@ def test_truncate_and_context_full():
         o.truncate(5)
 
 
+# ---- temperature sampling: Philox4x64-10 uniforms and Gumbel-max draws ----
+
+def check_philox_matches_numpy():
+    # numpy's Philox bit generator is the same Philox4x64-10; it advances its 256-bit counter
+    # before each block, so its block after counter c - 1 is the function's block at c
+    cases = [((1, 0, 0, 0), (0, 0)), ((0x243F6A8885A308D3, 0x13198A2E03707344, 7, 0xFFFFFFFFFFFFFFFF),
+                                     (0xA4093822299F31D0, 0x082EFA98EC4E6C89)),
+             ((123456789, 42, 3, 1), (2026, 0))]
+    for ctr, key in cases:
+        bg = np.random.Philox(key=np.array(key, dtype=np.uint64),
+                              counter=np.array((ctr[0] - 1,) + ctr[1:], dtype=np.uint64))
+        ref = [int(x) for x in bg.random_raw(4)]
+        got = [int(x) for x in orc.philox4x64_10(tuple(np.uint64(c) for c in ctr), key)]
+        assert got == ref, (ctr, key, [hex(x) for x in got], [hex(x) for x in ref])
+
+
+def check_sampling_uniforms():
+    u = orc.sampling_uniforms(seed=5, draw=0, slot=0, n_pos=64, vocab=2048)
+    assert u.shape == (64, 2048) and u.min() > 0.0 and u.max() < 1.0
+    assert abs(u.mean() - 0.5) < 5e-3 and abs(u.var() - 1.0 / 12.0) < 2e-3
+    # every counter word matters: another draw, slot or seed gives other numbers
+    for kw in ({"draw": 1}, {"slot": 1}, {"seed": 6}):
+        args = {"seed": 5, "draw": 0, "slot": 0}
+        args.update(kw)
+        v = orc.sampling_uniforms(n_pos=64, vocab=2048, **args)
+        assert np.mean(v == u) < 1e-3
+
+
+def _chi2(counts, probs):
+    n = counts.sum()
+    return float(np.sum((counts - n * probs) ** 2 / (n * probs)))
+
+
+def check_gumbel_max_draws_follow_softmax():
+    # 20000 independent draws (one per block position) from a 6-token distribution; chi-square
+    # against softmax(z / T) with 5 degrees of freedom: 25.7 is its 1e-4 upper quantile
+    z = np.array([0.3, -1.0, 1.2, 0.0, 2.0, -0.5])
+    n = 20000
+    for temperature in (1.0, 2.0, 0.5):
+        tok, _ = orc.sample_tokens(np.tile(z, (n, 1)), temperature, seed=11, draw=3, slot=2)
+        counts = np.bincount(tok, minlength=z.size).astype(np.float64)
+        p = np.exp(z / temperature - (z / temperature).max())
+        p /= p.sum()
+        assert _chi2(counts, p) < 25.7, (temperature, counts, n * p)
+
+
+def check_sampling_limits_and_replay():
+    rng = np.random.default_rng(9)
+    z = rng.standard_normal((8, 300))
+    assert np.array_equal(orc.sample_tokens(z, 0.0, 1, 0)[0], orc.argmax_lowest(z))
+    # vanishing temperature: the noise is negligible against z / T
+    assert np.array_equal(orc.sample_tokens(z, 1e-9, 1, 0)[0], orc.argmax_lowest(z))
+    a = orc.sample_tokens(z, 1.0, seed=3, draw=4, slot=1)[0]
+    assert np.array_equal(a, orc.sample_tokens(z, 1.0, seed=3, draw=4, slot=1)[0])
+    # a flat distribution: other draws give other tokens at almost every position
+    flat = np.zeros((64, 1000))
+    t0 = orc.sample_tokens(flat, 1.0, seed=3, draw=0)[0]
+    t1 = orc.sample_tokens(flat, 1.0, seed=3, draw=1)[0]
+    assert np.mean(t0 == t1) < 0.05
+
+
+def test_philox_matches_numpy():
+    check_philox_matches_numpy()
+
+
+def test_sampling_uniforms():
+    check_sampling_uniforms()
+
+
+def test_gumbel_max_draws_follow_softmax():
+    check_gumbel_max_draws_follow_softmax()
+
+
+def test_sampling_limits_and_replay():
+    check_sampling_limits_and_replay()
+
+
 ALL_CHECKS = [v for k, v in sorted(globals().items()) if k.startswith("check_")]
