@@ -199,9 +199,12 @@ def argmax_lowest(z: np.ndarray) -> np.ndarray:
 # A candidate is drawn from softmax(z / T) by the Gumbel-max rule: argmax_v (z_v / T + G_v) with
 # G_v = -log(-log(U_v)) and U_v independent uniforms on (0, 1).  The uniforms come from the
 # counter-based generator Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
-# easy as 1, 2, 3", SC 2011) keyed by (seed, 0) at counter (v, b, draw, slot): vocabulary id v, block
-# position b, draw index, sequence slot; U = (top 24 bits of output word 0 + 1/2) / 2^24.  These
-# generator details are this library's convention (the paper fixes none of them).
+# easy as 1, 2, 3", SC 2011) keyed by (seed, 0): U of vocabulary id v at block position b in draw
+# `draw` of sequence slot `slot` is made from output word b mod 4 at counter (v, b div 4, draw,
+# slot), so one generator call serves four consecutive positions; U = (top 23 bits of the word +
+# 1/2) / 2^23, a value that single precision holds exactly and that stays below 1 there too, so a
+# kernel computing the noise in fp32 never meets log(1).  These generator details are this
+# library's convention (the paper fixes none of them).
 
 _PHILOX_M0 = np.uint64(0xD2E7470EE14C6C93)
 _PHILOX_M1 = np.uint64(0xCA5A826395121157)
@@ -243,8 +246,10 @@ def sampling_uniforms(seed: int, draw: int, slot: int, n_pos: int, vocab: int) -
     """U[b, v] in (0, 1) for block positions b < n_pos and vocabulary ids v < vocab."""
     v = np.arange(vocab, dtype=np.uint64)[None, :]
     b = np.arange(n_pos, dtype=np.uint64)[:, None]
-    w0 = philox4x64_10((v, b, np.uint64(draw), np.uint64(slot)), (np.uint64(seed), np.uint64(0)))[0]
-    return ((w0 >> np.uint64(40)).astype(np.float64) + 0.5) / float(1 << 24)
+    words = np.stack(philox4x64_10((v, b >> np.uint64(2), np.uint64(draw), np.uint64(slot)),
+                                   (np.uint64(seed), np.uint64(0))))  # [4, n_pos, vocab]
+    w = words[(np.arange(n_pos) % 4)[:, None], np.arange(n_pos)[:, None], np.arange(vocab)[None, :]]
+    return ((w >> np.uint64(41)).astype(np.float64) + 0.5) / float(1 << 23)
 
 
 def sample_tokens(z: np.ndarray, temperature: float, seed: int, draw: int, slot: int = 0):

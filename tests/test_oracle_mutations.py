@@ -188,6 +188,27 @@ def _philox_swapped_multipliers(counter, key):
     return c0, c1, c2, c3
 
 
+def _uniform_words(seed, draw, slot, n_pos, vocab):
+    v = np.arange(vocab, dtype=np.uint64)[None, :]
+    b = np.arange(n_pos, dtype=np.uint64)[:, None]
+    words = np.stack(orc.philox4x64_10((v, b >> np.uint64(2), np.uint64(draw), np.uint64(slot)),
+                                       (np.uint64(seed), np.uint64(0))))
+    return words[(np.arange(n_pos) % 4)[:, None], np.arange(n_pos)[:, None], np.arange(vocab)[None, :]]
+
+
+def _uniforms_24_bits(seed, draw, slot, n_pos, vocab):
+    w = _uniform_words(seed, draw, slot, n_pos, vocab)
+    return ((w >> np.uint64(40)).astype(np.float64) + 0.5) / float(1 << 24)  # not exact in fp32
+
+
+def _uniforms_word0_only(seed, draw, slot, n_pos, vocab):
+    v = np.arange(vocab, dtype=np.uint64)[None, :]
+    b = np.arange(n_pos, dtype=np.uint64)[:, None]
+    w = orc.philox4x64_10((v, b >> np.uint64(2), np.uint64(draw), np.uint64(slot)),
+                          (np.uint64(seed), np.uint64(0)))[0]  # four positions share one number
+    return ((w >> np.uint64(41)).astype(np.float64) + 0.5) / float(1 << 23)
+
+
 _ORIG = {k: getattr(orc, k) for k in ("fuse_rows", "rope", "context_kv")}
 
 MUTANTS = {
@@ -221,6 +242,8 @@ MUTANTS = {
     "sampling_temperature_multiplies": ("sample_tokens", _sample_temperature_multiplies),
     "philox_without_key_schedule": ("philox4x64_10", _philox_no_key_schedule),
     "philox_multipliers_swapped": ("philox4x64_10", _philox_swapped_multipliers),
+    "uniforms_not_exact_in_fp32": ("sampling_uniforms", _uniforms_24_bits),
+    "uniforms_same_word_for_four_positions": ("sampling_uniforms", _uniforms_word0_only),
 }
 
 

@@ -591,6 +591,21 @@ def check_sampling_uniforms():
     u = orc.sampling_uniforms(seed=5, draw=0, slot=0, n_pos=64, vocab=2048)
     assert u.shape == (64, 2048) and u.min() > 0.0 and u.max() < 1.0
     assert abs(u.mean() - 0.5) < 5e-3 and abs(u.var() - 1.0 / 12.0) < 2e-3
+    # single precision holds every uniform exactly, the extremes included: the largest is
+    # 1 - 2^-24, below 1 in fp32 as well, so fp32 noise -log(-log U) stays finite
+    assert np.array_equal(u.astype(np.float32).astype(np.float64), u)
+    for k in (0, (1 << 23) - 1):
+        top = (float(k) + 0.5) / float(1 << 23)
+        assert np.float32(top) == top and np.float32(top) < np.float32(1.0)
+        assert np.isfinite(np.float32(-np.log(-np.log(np.float32(top)))))
+    # the four positions served by one generator call take different output words
+    for b in range(1, 4):
+        assert np.mean(u[0] == u[b]) < 1e-3 and np.mean(u[4 + b] == u[4]) < 1e-3
+    # one generator call per four positions: positions 4 q + j, word j of counter (v, q, ...)
+    c = orc.philox4x64_10((np.arange(2048, dtype=np.uint64), np.uint64(3), np.uint64(0), np.uint64(0)),
+                          (np.uint64(5), np.uint64(0)))
+    for j in range(4):
+        assert np.array_equal(u[12 + j], ((c[j] >> np.uint64(41)).astype(np.float64) + 0.5) / 2.0 ** 23)
     # every counter word matters: another draw, slot or seed gives other numbers
     for kw in ({"draw": 1}, {"slot": 1}, {"seed": 6}):
         args = {"seed": 5, "draw": 0, "slot": 0}
