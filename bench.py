@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="qwen3_8b",
                     help="qwen3_8b (default), qwen3_4b, gpt_oss_20b, or batched (32 ragged sequences)")
+    ap.add_argument("--temperature", type=float, default=0.0,
+                    help="0 (default): greedy drafts; > 0: Gumbel-max draws from softmax(z / T)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-context", type=int, default=256,
                     help="context rows of the oracle's timed sample")
@@ -138,6 +140,7 @@ def main():
     print(f"[bench] weights generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
     model = dfl.DraftModel(cfg, w, fusion_logits, max_context=L + 16, max_new=512)
     h = model.h
+    dfl.dflare_set_sampling(h, args.temperature, 1)
     chunk = 512
     for s in range(0, L, chunk):
         n = min(chunk, L - s)
@@ -225,7 +228,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}-shaped draft step: H={H}, {cfg.n_q_heads}q/{cfg.n_kv_heads}kv x "
                                f"{cfg.head_dim}, F={cfg.ffn}, V={cfg.vocab}, D={cfg.n_draft_layers}, S={S}, "
-                               f"L={L}, B={B}, batch 1, n_new~U{{1..16}}",
+                               f"L={L}, B={B}, batch 1, n_new~U{{1..16}}"
+                               + (f", sampled at T={args.temperature}" if args.temperature > 0 else ", greedy"),
                    "global_batch": 1, "seq_len": L, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(d["achieved_GBs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(d["achieved_GBs"] / HBM_PEAK_GBS, 4),
@@ -275,6 +279,7 @@ def bench_batched(args):
     model = dfl.DraftModel(cfg, w, fusion_logits, max_context=max(lengths) + 16, max_new=16 * n_seq,
                            max_batch=n_seq)
     h = model.h
+    dfl.dflare_set_sampling(h, args.temperature, 1)
     # one shared stream of target rows on the device; sequence i reads rows 16 i + (0 .. L_i)
     base = [16 * i for i in range(n_seq)]
     R = max(b + L for b, L in zip(base, lengths))
@@ -375,7 +380,8 @@ def bench_batched(args):
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}-shaped draft step for {n_seq} sequences at once: L ~ U{{"
                                f"{spec['lo']}..{spec['hi']}}} per sequence (mean {np.mean(lengths):.0f}), "
-                               f"n_new ~ U{{1..16}} per sequence per step, B={B}",
+                               f"n_new ~ U{{1..16}} per sequence per step, B={B}"
+                               + (f", sampled at T={args.temperature}" if args.temperature > 0 else ", greedy"),
                    "global_batch": n_seq, "seq_len": int(max(lengths)), "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": d["TFLOPs"], "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(d["TFLOPs"] / MFMA_PEAK_TFLOPS, 4),

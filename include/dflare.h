@@ -19,7 +19,7 @@
  * rotate-half convention (context keys rotated at their own positions when
  * appended), context row r at position r and block row b at position L + b,
  * scale 1/sqrt(head_dim), query head h uses KV head h / (n_q / n_kv), greedy
- * argmax with ties to the lowest id.
+ * argmax with ties to the lowest id unless dflare_set_sampling sets a temperature.
  *
  * Conventions for every entry point:
  *   - Return value: DFLARE_OK (0) or a negative dflare_status.  Nothing throws.
@@ -132,8 +132,9 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
  * dflare_draft_block -- one drafting forward pass (Sec. 3.2, drafting phase).
  *   block_ids      DEVICE int32 [B]: x_t at index 0, the mask id at 1..B-1 (the
  *                  library treats all ids alike; ids outside [0, V) are clamped).
- *   draft_tokens   DEVICE int32 [B]: greedy token at every block position; index 0
- *                  is not a candidate (the B-1 candidates are 1..B-1).
+ *   draft_tokens   DEVICE int32 [B]: token at every block position (greedy, or sampled
+ *                  as dflare_set_sampling sets, in sequence slot 0); index 0 is not a
+ *                  candidate (the B-1 candidates are 1..B-1).
  * Block row b sits at position L + b.  The context cache is not modified, so the
  * call can be repeated.  An empty context (L = 0) is allowed.
  * By default the whole pass is one cooperative launch of one work-group per CU
@@ -185,11 +186,28 @@ int dflare_fuse_append_batched(dflare_handle* h, int32_t n_seq, const int32_t* s
 /*
  * dflare_draft_block_batched -- dflare_draft_block for every listed sequence.
  *   block_ids      DEVICE int32 [n_seq, B]: row i is the block of seq[i].
- *   draft_tokens   DEVICE int32 [n_seq, B]: greedy tokens, row i for seq[i].
+ *   draft_tokens   DEVICE int32 [n_seq, B]: tokens (greedy, or sampled as dflare_set_sampling
+ *                  sets), row i for seq[i].
  * Block row b of seq[i] sits at position L_seq[i] + b.  No cache is modified.
  */
 int dflare_draft_block_batched(dflare_handle* h, int32_t n_seq, const int32_t* seq, const int32_t* block_ids,
                                int32_t* draft_tokens);
+
+/*
+ * dflare_set_sampling -- how draft tokens are chosen from the logits z (Sec. 3.2 samples the
+ * candidates; the paper reports greedy and temperature-1 decoding, Sec. 5, Table 1).
+ *   temperature    0 (the default): greedy argmax, ties to the lowest id.  > 0: each position's
+ *                  token is argmax_v (z_v / temperature + G_v) with Gumbel noise
+ *                  G_v = -log(-log(U_v)), a draw from softmax(z / temperature).  Negative,
+ *                  NaN, infinite, or so small that 1 / temperature overflows fp32: INVALID_ARG.
+ *   seed           key of the noise.  U_v at block position b = (top 23 bits of word b mod 4 of
+ *                  Philox4x64-10 (Salmon et al., SC 2011) at counter (v, b div 4, draw, sequence
+ *                  slot) under key (seed, 0) + 1/2) / 2^23, exact in fp32; draw counts the draft
+ *                  calls (batch-1 or batched) made since this call, from 0.  The batch-1 calls use
+ *                  slot 0.
+ * Debug logits stay the unperturbed z.  Takes effect for later draft calls.
+ */
+int dflare_set_sampling(dflare_handle* h, float temperature, uint64_t seed);
 
 /* dflare_truncate_seq / dflare_context_len_seq -- as above, for one slot. */
 int dflare_truncate_seq(dflare_handle* h, int32_t seq, int32_t new_len);

@@ -61,12 +61,17 @@ struct BGemmArgs {
   // SWIGLU: fp16 A fragments of the MLP hidden rows [Mt][out_kt][64]
   u32x4* out16;
   int out_kt;
-  // ARGMAX: optional logits [M, V]; best (logit, id) per (n-group, row)
+  // ARGMAX: optional logits [M, V]; best (score, id) per (n-group, row); the score is the
+  // logit, or with inv_temp > 0 the logit * inv_temp plus the Gumbel noise of draw `draw`
+  // under `seed` at the row's (sequence slot, block position)
   float* logits;
   int V;
   float* pmax;
   int* pidx;
   int pld;
+  float inv_temp;
+  unsigned draw;
+  unsigned long long seed;
 };
 
 struct BAttnArgs {

@@ -15,6 +15,8 @@
 // the exact values.
 #include <math.h>
 
+#include <type_traits>
+
 #include "batched.h"
 #include "device_common.h"
 
@@ -61,6 +63,37 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
+// f(integral_constant<int, I>) for I = B .. E-1, as straight-line code
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// best (score, id) of 4 rows over the 16 lanes of a quad (ties to the lowest id); lane col 0
+// writes them to bv_out[0..3], bi_out[0..3]
+__device__ __forceinline__ void row_best_to_lds(float bv[4], int bi[4], int col, float* bv_out, int* bi_out) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const float ov = __shfl_xor(bv[e], off);
+      const int oi = __shfl_xor(bi[e], off);
+      if (ov > bv[e] || (ov == bv[e] && oi < bi[e])) {
+        bv[e] = ov;
+        bi[e] = oi;
+      }
+    }
+  if (col == 0)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      bv_out[e] = bv[e];
+      bi_out[e] = bi[e];
+    }
+}
+
 // ------------------------------------------------------------------------------------------
 // GEMM.  Work-group: 4 waves; output tile 128 rows x 256 columns, wave w owning columns
 // 64 w .. 64 w + 63 for all 128 rows (8 x 4 MFMA tiles, 128 accumulators per lane); two
@@ -80,6 +113,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
   constexpr int P = kBPrefetch;
   __shared__ u32x4 sa[2][kBM * 64];
   __shared__ int s_slot[kBM * 16];
+  __shared__ int s_pos[kBM * 16];
   __shared__ long s_cache[kBM * 16];
   __shared__ float s_bv[kBWaves][kBM * 16];
   __shared__ int s_bi[kBWaves][kBM * 16];
@@ -321,49 +355,100 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
         }
     }
   } else if constexpr (EPI == BEPI_ARGMAX) {
-    // best (logit, id) of each row over this wave's 64 columns, then over the 4 waves;
+    // best (score, id) of each row over this wave's 64 columns, then over the 4 waves;
     // ties go to the lowest id (ids grow with n and col)
+    if (!(g.inv_temp > 0.f)) {
 #pragma unroll
-    for (int m = 0; m < kBM; ++m) {
-      float bv[4];
-      int bi[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        bv[e] = -INFINITY;
-        bi[e] = 0x7FFFFFFF;
-      }
-#pragma unroll
-      for (int n = 0; n < kBNW; ++n) {
-        const int vc = (nt0 + n) * 16 + col;
-        const bool ok = vc < g.V;
+      for (int m = 0; m < kBM; ++m) {
+        float bv[4];
+        int bi[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int row = row0 + m * 16 + quad * 4 + e;
-          const float v = acc[m][n][e];
-          if (ok && row < g.M && g.logits) g.logits[(long)row * g.V + vc] = v;
-          if (ok && (v > bv[e] || (v == bv[e] && vc < bi[e]))) {
-            bv[e] = v;
-            bi[e] = vc;
+          bv[e] = -INFINITY;
+          bi[e] = 0x7FFFFFFF;
+        }
+#pragma unroll
+        for (int n = 0; n < kBNW; ++n) {
+          const int vc = (nt0 + n) * 16 + col;
+          const bool ok = vc < g.V;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int row = row0 + m * 16 + quad * 4 + e;
+            const float z = acc[m][n][e];
+            if (ok && row < g.M && g.logits) g.logits[(long)row * g.V + vc] = z;
+            if (ok && (z > bv[e] || (z == bv[e] && vc < bi[e]))) {
+              bv[e] = z;
+              bi[e] = vc;
+            }
           }
         }
+        row_best_to_lds(bv, bi, col, s_bv[w] + m * 16 + quad * 4, s_bi[w] + m * 16 + quad * 4);
       }
+    } else {
+      // sampling: score z / T + Gumbel noise of the row's (sequence slot, block position).
+      // The noise costs a Philox call per four positions, so this part runs as rolled loops
+      // (one copy of the generator in the code): per m-tile the thread's 16 scaled logits go
+      // to its own LDS slots (the A ring, idle after the k loop), the noise is added there,
+      // and the best is taken from there.
+      if (tid < kBM * 16) {
+        const int row = min(row0 + tid, g.M - 1);
+        int i = 0;
+        while (i + 1 < rows.n_seq && row >= rows.off[i + 1]) ++i;
+        s_slot[tid] = rows.seq[i];
+        s_pos[tid] = row - rows.off[i];
+      }
+      __syncthreads();  // also: every wave is past its last read of the A ring
+      uint64_t words[4];
+      float* zs = reinterpret_cast<float*>(&sa[0][0]) + tid;  // [16][kBT], this thread's column
+      // m is unrolled at compile time (the accumulators are indexed by constants) while the
+      // noise loop inside stays rolled
+      static_for<0, kBM>([&](auto mc) {
+        constexpr int m = decltype(mc)::value;
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
+        for (int n = 0; n < kBNW; ++n) {
+          const int vc = (nt0 + n) * 16 + col;
 #pragma unroll
-        for (int off = 1; off < 16; off <<= 1) {
-          const float ov = __shfl_xor(bv[e], off);
-          const int oi = __shfl_xor(bi[e], off);
-          if (ov > bv[e] || (ov == bv[e] && oi < bi[e])) {
-            bv[e] = ov;
-            bi[e] = oi;
+          for (int e = 0; e < 4; ++e) {
+            const int row = row0 + m * 16 + quad * 4 + e;
+            const float z = acc[m][n][e];
+            if (vc < g.V && row < g.M && g.logits) g.logits[(long)row * g.V + vc] = z;
+            zs[(n * 4 + e) * kBT] = z * g.inv_temp;
           }
         }
-      if (col == 0)
+        const int r0 = m * 16 + quad * 4;
+        // rows 4 q .. 4 q + 3 of one sequence share one Philox call, else one call per row
+        const bool grouped = (s_pos[r0] & 3) == 0 && s_pos[r0 + 3] == s_pos[r0] + 3 && s_slot[r0 + 3] == s_slot[r0];
+#pragma unroll 1
+        for (int j = 0; j < kBNW * 4; ++j) {
+          const int n = j >> 2, e = j & 3;
+          if (e == 0 || !grouped) {
+            const int pos = s_pos[r0 + e], slot = s_slot[r0 + e];
+            gumbel_words(g.seed, (nt0 + n) * 16 + col, pos >> 2, g.draw, slot, words);
+          }
+          const int k = grouped ? e : (s_pos[r0 + e] & 3);
+          zs[j * kBT] += gumbel_of_word(k == 0 ? words[0] : k == 1 ? words[1] : k == 2 ? words[2] : words[3]);
+        }
+        float bv[4];
+        int bi[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          s_bv[w][m * 16 + quad * 4 + e] = bv[e];
-          s_bi[w][m * 16 + quad * 4 + e] = bi[e];
+          bv[e] = -INFINITY;
+          bi[e] = 0x7FFFFFFF;
         }
+#pragma unroll
+        for (int n = 0; n < kBNW; ++n) {
+          const int vc = (nt0 + n) * 16 + col;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float v = zs[(n * 4 + e) * kBT];
+            if (vc < g.V && (v > bv[e] || (v == bv[e] && vc < bi[e]))) {
+              bv[e] = v;
+              bi[e] = vc;
+            }
+          }
+        }
+        row_best_to_lds(bv, bi, col, s_bv[w] + r0, s_bi[w] + r0);
+      });
     }
     __syncthreads();
     if (tid < kBM * 16) {

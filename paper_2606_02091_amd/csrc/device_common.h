@@ -121,6 +121,65 @@ __device__ __forceinline__ int opaque(int x) {
 // wait until this wave's memory operations (stores included) have completed
 __device__ __forceinline__ void wait_vm() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// ---- temperature sampling: Gumbel-max draws ----
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3",
+// SC 2011) of the counter (c0, c1, c2, c3) under the key (k0, k1); the four output words
+// replace the counter.
+__device__ __forceinline__ void philox4x64_10(uint64_t& c0, uint64_t& c1, uint64_t& c2, uint64_t& c3, uint64_t k0,
+                                              uint64_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t hi0 = __umul64hi(c0, 0xD2E7470EE14C6C93ull), lo0 = c0 * 0xD2E7470EE14C6C93ull;
+    const uint64_t hi1 = __umul64hi(c2, 0xCA5A826395121157ull), lo1 = c2 * 0xCA5A826395121157ull;
+    c0 = hi1 ^ c1 ^ k0;
+    c1 = lo1;
+    c2 = hi0 ^ c3 ^ k1;
+    c3 = lo0;
+    k0 += 0x9E3779B97F4A7C15ull;
+    k1 += 0xBB67AE8584CAA73Bull;
+  }
+}
+
+// Temperature sampling draws token argmax_v (z_v / T + G_v), a draw from softmax(z / T), with
+// Gumbel noise G = -log(-log U).  U of vocabulary id v at block position b, in draft call
+// `draw` of sequence slot `slot`, comes from output word b % 4 of Philox4x64-10 at counter
+// (v, b / 4, draw, slot) under key (seed, 0): one call serves four consecutive positions.
+// gumbel_of_word: U = (top 23 bits of the word + 1/2) / 2^23, exact in fp32 and at most
+// 1 - 2^-24, so the noise is finite.
+__device__ __forceinline__ float gumbel_of_word(uint64_t x) {
+  const float u = ((float)(uint32_t)(x >> 41) + 0.5f) * 1.1920928955078125e-7f;  // 2^-23
+  return -logf(-logf(u));
+}
+
+// the four Philox words of counter (v, q, draw, slot): the noise words of positions 4 q .. 4 q + 3
+__device__ __forceinline__ void gumbel_words(unsigned long long seed, int v, int q, unsigned draw, int slot,
+                                             uint64_t w[4]) {
+  w[0] = (uint64_t)v;
+  w[1] = (uint64_t)q;
+  w[2] = (uint64_t)draw;
+  w[3] = (uint64_t)slot;
+  philox4x64_10(w[0], w[1], w[2], w[3], seed, 0ull);
+}
+
+// the noise of positions 4 q .. 4 q + 3 (one Philox call)
+__device__ __forceinline__ void gumbel_noise4(unsigned long long seed, int v, int q, unsigned draw, int slot,
+                                              float out[4]) {
+  uint64_t c0 = (uint64_t)v, c1 = (uint64_t)q, c2 = (uint64_t)draw, c3 = (uint64_t)slot;
+  philox4x64_10(c0, c1, c2, c3, seed, 0ull);
+  out[0] = gumbel_of_word(c0);
+  out[1] = gumbel_of_word(c1);
+  out[2] = gumbel_of_word(c2);
+  out[3] = gumbel_of_word(c3);
+}
+
+// the noise of one position b
+__device__ __forceinline__ float gumbel_noise1(unsigned long long seed, int v, int b, unsigned draw, int slot) {
+  uint64_t c0 = (uint64_t)v, c1 = (uint64_t)(b >> 2), c2 = (uint64_t)draw, c3 = (uint64_t)slot;
+  philox4x64_10(c0, c1, c2, c3, seed, 0ull);
+  const int k = b & 3;
+  return gumbel_of_word(k == 0 ? c0 : k == 1 ? c1 : k == 2 ? c2 : c3);
+}
+
 // Activations handed from one GEMM to the next are stored directly in the A-operand
 // layout of v_mfma_f32_16x16x32_bf16, as two bf16 planes hi and lo (x ~= hi + lo):
 //   element (row, k) of a [rows, K] matrix sits in 16-row tile row/16, k-tile k/32,

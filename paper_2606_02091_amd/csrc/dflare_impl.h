@@ -71,6 +71,11 @@ struct DraftCall {
   unsigned bar_epoch;   // grid barriers completed by earlier launches
   unsigned done_epoch;  // launches that ran the LM phase before this one
   unsigned long long* trace;  // optional [blocks][phases][kTraceSlots] wall clock at marks of each phase
+  // candidate selection: inv_temp = 0 greedy argmax; otherwise argmax of z * inv_temp plus
+  // Gumbel noise of draw `draw` under `seed` (sequence slot 0)
+  float inv_temp;
+  unsigned draw;
+  unsigned long long seed;
 };
 
 // Everything else the draft-block kernel needs; written to device memory once at init and

@@ -526,11 +526,17 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
     const bool ok = vc < a->V;
     float bv[4];
     int bix[4];
+    // sampling: the Gumbel-max score z / T + noise; the lane's rows 4 quad .. 4 quad + 3 are
+    // block positions of one Philox call (sequence slot 0).  The logits stay unperturbed.
+    const float inv_temp = c->inv_temp;
+    float noise[4] = {0.f, 0.f, 0.f, 0.f};
+    if (inv_temp > 0.f) gumbel_noise4(c->seed, vc, quad, c->draw, 0, noise);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = quad * 4 + i;
       if (ok && c->logits && row < M) c->logits[(long)row * a->V + vc] = v[i];
-      bv[i] = ok ? v[i] : -INFINITY;
+      const float y = (inv_temp > 0.f) ? v[i] * inv_temp + noise[i] : v[i];
+      bv[i] = ok ? y : -INFINITY;
       bix[i] = ok ? vc : 0x7FFFFFFF;
     }
 #pragma unroll

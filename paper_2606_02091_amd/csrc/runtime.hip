@@ -120,6 +120,10 @@ struct dflare_handle {
   int prof_kind = 0;
   std::vector<hipEvent_t> prof_ev;  // pairs
   int prof_n = 0;
+  // candidate selection: temperature 0 greedy, else Gumbel-max draws (draw counts draft calls)
+  float temperature = 0.f;
+  unsigned long long seed = 0;
+  unsigned draw = 0;
   // batched draft step
   int cus = 0;
   long seq_stride = 0;     // cache elements of one sequence slot (all layers)
@@ -616,6 +620,9 @@ DraftCall draft_call(const dflare_handle* h, const int32_t* ids, const int32_t* 
   d.bar_epoch = h->bar_epoch;
   d.done_epoch = h->done_epoch;
   d.trace = h->trace ? h->trace_buf : nullptr;
+  d.inv_temp = h->temperature > 0.f ? 1.0f / h->temperature : 0.f;
+  d.draw = h->draw;
+  d.seed = h->seed;
   return d;
 }
 
@@ -678,6 +685,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
     }
   }
   h->done_epoch += 1;
+  if (h->temperature > 0.f) ++h->draw;
   prof_mark(h, DFLARE_K_DRAFT, false);
   return check_launch(h, "draft_block");
 }
@@ -869,6 +877,10 @@ int run_draft_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int
   g.Nt = Nt_lm;
   g.Kt = Kt_H;
   g.logits = h->debug ? h->dbg_blogits : nullptr;
+  g.inv_temp = h->temperature > 0.f ? 1.0f / h->temperature : 0.f;
+  g.draw = h->draw;
+  g.seed = h->seed;
+  if (h->temperature > 0.f) ++h->draw;
   prof_mark(h, DFLARE_K_B_LM_HEAD, true);
   bgemm(h, -1, "LM", BEPI_ARGMAX, g, rows);  // timed with the final argmax below
   launch_bargmax(s, h->bpmax, h->bpidx, ceil_div(Nt_lm, kBN), g.pld, M, out);
@@ -1027,6 +1039,16 @@ int dflare_draft_block_batched(dflare_handle* h, int32_t n_seq, const int32_t* s
   const int rc = run_draft_batched(h, n_seq, seq, block_ids, draft_tokens);
   prof_mark(h, DFLARE_K_B_DRAFT, false);
   return rc;
+}
+
+int dflare_set_sampling(dflare_handle* h, float temperature, uint64_t seed) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!(temperature >= 0.f) || !isfinite(temperature) || (temperature > 0.f && !isfinite(1.f / temperature)))
+    return fail(h, DFLARE_ERR_INVALID_ARG, "temperature must be 0 or finite with a finite reciprocal");
+  h->temperature = temperature;
+  h->seed = seed;
+  h->draw = 0;
+  return DFLARE_OK;
 }
 
 int dflare_truncate_seq(dflare_handle* h, int32_t seq, int32_t new_len) {

@@ -26,7 +26,7 @@ EXPORTED = (
     "dflare_status_str", "dflare_last_error", "dflare_debug_capture", "dflare_debug_read",
     "dflare_kernel_stats", "dflare_profile_begin", "dflare_profile_end", "dflare_set_option",
     "dflare_fuse_append_batched", "dflare_draft_block_batched", "dflare_truncate_seq",
-    "dflare_context_len_seq", "dflare_debug_read_seq",
+    "dflare_context_len_seq", "dflare_debug_read_seq", "dflare_set_sampling",
 )
 K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T, K_DRAFT = range(1, 10)
 (K_B_QKV, K_B_ATTN, K_B_O, K_B_GATE_UP, K_B_DOWN, K_B_LM_HEAD, K_B_KV_T, K_B_EPI, K_B_FUSE, K_B_DRAFT,
@@ -88,6 +88,7 @@ def lib() -> ctypes.CDLL:
         "dflare_fuse_append_batched": ([vp, i32, ctypes.POINTER(i32), ctypes.POINTER(i32), vp], ctypes.c_int),
         "dflare_draft_block_batched": ([vp, i32, ctypes.POINTER(i32), vp, vp], ctypes.c_int),
         "dflare_truncate_seq": ([vp, i32, i32], ctypes.c_int),
+        "dflare_set_sampling": ([vp, ctypes.c_float, ctypes.c_uint64], ctypes.c_int),
         "dflare_context_len_seq": ([vp, i32, ctypes.POINTER(i32)], ctypes.c_int),
         "dflare_debug_read_seq": ([vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float),
                                    i64], ctypes.c_int),
@@ -176,6 +177,11 @@ def dflare_draft_block_batched(h: int, seq, block_ids: torch.Tensor, draft_token
     """block_ids / draft_tokens: device int32 [n_seq, B]; row i belongs to slot seq[i]."""
     sq = _i32_array(seq)
     _check(lib().dflare_draft_block_batched(h, sq.size, _i32p(sq), _ptr(block_ids), _ptr(draft_tokens)), h)
+
+
+def dflare_set_sampling(h: int, temperature: float, seed: int = 0) -> None:
+    """temperature 0: greedy argmax; > 0: Gumbel-max draws from softmax(z / temperature)."""
+    _check(lib().dflare_set_sampling(h, float(temperature), int(seed) & 0xFFFFFFFFFFFFFFFF), h)
 
 
 def dflare_truncate_seq(h: int, seq: int, new_len: int) -> None:
