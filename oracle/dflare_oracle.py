@@ -32,6 +32,16 @@ with W in R^{d x d_kv}; it is the same map).
 Temperature sampling (Sec. 5, Table 1 lower half): Gumbel-max draws with uniforms from
 Philox4x64-10; see sample_tokens.
 
+Variants (DraftOracle's `variant` bit field; 0 is the method as described):
+* VARIANT_NO_SOFTMAX  -Softmax of Sec. 6.3 (Table 2): alpha = W^fuse as given
+* VARIANT_SHARED_KV   -KVProj of Sec. 6.3: the context goes through the draft layer's own
+                      W_K^d, W_V^d (as in Eq. 2) instead of W_K^t, W_V^t
+* VARIANT_POST_FC     +FC of Sec. 6.3: f' = f W_pfc^T + b_pfc per draft layer, between the
+                      fusion (Eq. 3) and the context projection (Eq. 4)
+* VARIANT_DFLASH      the DFlash baseline of Sec. 3.1-3.2: c_t = W_fc [h^(1); ...; h^(S)] + b_fc
+                      (Eq. 1), one context shared by every draft layer, projected by each
+                      layer's W_K^d, W_V^d (Eq. 2); no fusion weights, no fusion norm
+
 Parity pins: see tests/test_oracle_pins.py (closed forms, invariants, brute force,
 library routines).  Parity unpinned: the readings above that the paper leaves
 open (layer internals, rotary convention, positions) -- any consistent reading
@@ -46,8 +56,11 @@ import numpy as np
 __all__ = [
     "bf16_to_f64", "fusion_weights", "rms_norm", "rope", "silu", "fuse_rows",
     "context_kv", "block_attention", "draft_layer", "lm_head_logits", "argmax_lowest",
-    "philox4x64_10", "sampling_uniforms", "sample_tokens", "DraftOracle",
+    "philox4x64_10", "sampling_uniforms", "sample_tokens", "post_fc", "dflash_context", "DraftOracle",
+    "VARIANT_NO_SOFTMAX", "VARIANT_SHARED_KV", "VARIANT_POST_FC", "VARIANT_DFLASH",
 ]
+
+VARIANT_NO_SOFTMAX, VARIANT_SHARED_KV, VARIANT_POST_FC, VARIANT_DFLASH = 1, 2, 4, 8
 
 
 def bf16_to_f64(u16) -> np.ndarray:
@@ -56,17 +69,22 @@ def bf16_to_f64(u16) -> np.ndarray:
     return (u.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def fusion_weights(fusion_logits) -> np.ndarray:
+def fusion_weights(fusion_logits, normalize: bool = True) -> np.ndarray:
     """alpha^(i) = softmax over target layers of row i of W^fuse  (Sec. 4.1, Eq. 3).
 
     fusion_logits: [D, S] real.  Returns [D, S] fp64 with rows summing to 1.
     The maximum of each row is subtracted first so that large logits do not
     overflow; this does not change the softmax.  Raises ValueError for a row with
-    a NaN, +inf, or no finite entry.
+    a NaN, +inf, or no finite entry.  normalize=False is the -Softmax ablation
+    (Sec. 6.3): W^fuse itself, every entry finite.
     """
     lg = np.asarray(fusion_logits, dtype=np.float64)
     if lg.ndim != 2:
         raise ValueError("fusion logits must be [D, S]")
+    if not normalize:
+        if not np.isfinite(lg).all():
+            raise ValueError("unnormalised fusion weights must be finite")
+        return lg.copy()
     if np.isnan(lg).any() or np.isposinf(lg).any():
         raise ValueError("fusion logits must not contain NaN or +inf")
     if not np.isfinite(lg).any(axis=1).all():
@@ -132,6 +150,27 @@ def context_kv(f_i: np.ndarray, wk_t: np.ndarray, wv_t: np.ndarray, positions,
     k = (f_i @ wk_t.T).reshape(n, n_kv, hd)
     v = (f_i @ wv_t.T).reshape(n, n_kv, hd)
     return rope(k, positions, base), v
+
+
+def post_fc(f_i: np.ndarray, w: np.ndarray, b) -> np.ndarray:
+    """+FC ablation (Sec. 6.3): one more fully connected layer on a draft layer's fused
+    rows before they are projected into its cache, f' = f W^T + b.  f_i: [n, H];
+    w: [H, H] ([out, in]); b: [H] or None."""
+    out = f_i @ w.T
+    return out if b is None else out + b
+
+
+def dflash_context(hidden: np.ndarray, w_fc: np.ndarray, b_fc) -> np.ndarray:
+    """DFlash context features (Sec. 3.1, Eq. 1): c_t = W_fc [h_t^(1); ...; h_t^(S)] + b_fc.
+
+    hidden: [S, n, H] (target layer major); w_fc: [H, S*H] ([out, in], the input being
+    the S rows of a position concatenated in layer order); b_fc: [H] or None.
+    Returns C: [n, H], one row per position, shared by every draft layer.
+    """
+    S, n, H = hidden.shape
+    concat = np.transpose(hidden, (1, 0, 2)).reshape(n, S * H)
+    out = concat @ w_fc.T
+    return out if b_fc is None else out + b_fc
 
 
 def block_attention(q, k_ctx, v_ctx, k_blk, v_blk) -> np.ndarray:
@@ -277,13 +316,19 @@ class DraftOracle:
     """
 
     def __init__(self, cfg, weights: dict, fusion_logits, max_context: int = 1 << 16,
-                 cache_weights: bool = False):
+                 cache_weights: bool = False, variant: int = 0):
         self.cfg = cfg
         self.w = weights
-        self.alpha = fusion_weights(fusion_logits)
+        self.variant = variant
         D = cfg.n_draft_layers
-        if self.alpha.shape != (D, cfg.n_target_layers):
-            raise ValueError("fusion logits must be [D, S]")
+        if variant & ~15 or (variant & VARIANT_DFLASH and variant != VARIANT_DFLASH):
+            raise ValueError("unknown variant, or DFlash combined with another variant")
+        if variant & VARIANT_DFLASH:
+            self.alpha = None
+        else:
+            self.alpha = fusion_weights(fusion_logits, normalize=not variant & VARIANT_NO_SOFTMAX)
+            if self.alpha.shape != (D, cfg.n_target_layers):
+                raise ValueError("fusion logits must be [D, S]")
         self.max_context = max_context
         self.L = 0
         # context keys/values per draft layer, grown by doubling; rows [0, L) are live
@@ -334,7 +379,8 @@ class DraftOracle:
     def append(self, hidden_bf16, positions=None) -> np.ndarray:
         """Fuse n new target rows [S, n, H] and append their K/V to every layer.
 
-        Returns the fused rows [D, n, H] (Eq. 3).  Positions default to L..L+n-1.
+        Returns the fused rows [D, n, H] (Eq. 3; with +FC after the extra layer; with DFlash
+        the shared context C of Eq. 1 for every layer).  Positions default to L..L+n-1.
         """
         cfg = self.cfg
         h = bf16_to_f64(hidden_bf16)
@@ -344,12 +390,24 @@ class DraftOracle:
         if self.L + n > self.max_context:
             raise ValueError("context full")
         pos = np.arange(self.L, self.L + n) if positions is None else np.asarray(positions)
-        fuse_g = self.w.get("fuse_norm")
-        gains = None if fuse_g is None else bf16_to_f64(fuse_g)
-        f = fuse_rows(self.alpha, h, gains, cfg.rms_eps)
+        D = cfg.n_draft_layers
+        if self.variant & VARIANT_DFLASH:
+            b = self.w.get("fc_bias")
+            c = dflash_context(h, bf16_to_f64(self.w["fc"]), None if b is None else bf16_to_f64(b))
+            f = np.broadcast_to(c, (D,) + c.shape)
+        else:
+            fuse_g = self.w.get("fuse_norm")
+            gains = None if fuse_g is None else bf16_to_f64(fuse_g)
+            f = fuse_rows(self.alpha, h, gains, cfg.rms_eps)
+            if self.variant & VARIANT_POST_FC:
+                bias = self.w.get("post_fc_bias")
+                f = np.stack([post_fc(f[i], bf16_to_f64(self.w["post_fc"][i]),
+                                      None if bias is None else bf16_to_f64(bias[i])) for i in range(D)])
+        shared = self.variant & (VARIANT_SHARED_KV | VARIANT_DFLASH)
+        wk, wv = ("wk_d", "wv_d") if shared else ("wk_t", "wv_t")
         self._reserve(self.L + n)
-        for i in range(cfg.n_draft_layers):
-            k, v = context_kv(f[i], bf16_to_f64(self.w["wk_t"][i]), bf16_to_f64(self.w["wv_t"][i]),
+        for i in range(D):
+            k, v = context_kv(f[i], bf16_to_f64(self.w[wk][i]), bf16_to_f64(self.w[wv][i]),
                               pos, cfg.n_kv_heads, cfg.head_dim, cfg.rope_base)
             self._k[i][self.L:self.L + n] = k
             self._v[i][self.L:self.L + n] = v

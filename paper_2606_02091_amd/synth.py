@@ -88,11 +88,15 @@ CONFIGS: dict[str, ModelConfig] = {
 
 # Order in which weight tensors are drawn; each gets its own child seed so that
 # they can be drawn in parallel and a single tensor can be regenerated alone.
-WEIGHT_KINDS = (
+BASE_KINDS = (
     "embed", "lm_head", "final_norm", "fusion_logits",
     "fuse_norm", "attn_norm", "mlp_norm",
     "wq", "wk_d", "wv_d", "wk_t", "wv_t", "wo", "w_gate", "w_up", "w_down",
 )
+# weights of the model variants only: the +FC layer after the fusion and the DFlash FC
+# fusion (Eq. 1); drawn only when asked for
+VARIANT_KINDS = ("post_fc", "post_fc_bias", "fc", "fc_bias")
+WEIGHT_KINDS = BASE_KINDS + VARIANT_KINDS
 
 
 def round_bf16(x: np.ndarray, out: np.ndarray | None = None) -> np.ndarray:
@@ -129,6 +133,7 @@ def _shape(cfg: ModelConfig, kind: str) -> tuple[int, ...]:
         "wq": (D, q, H), "wk_d": (D, kv, H), "wv_d": (D, kv, H),
         "wk_t": (D, kv, H), "wv_t": (D, kv, H), "wo": (D, H, q),
         "w_gate": (D, F, H), "w_up": (D, F, H), "w_down": (D, H, F),
+        "post_fc": (D, H, H), "post_fc_bias": (D, H), "fc": (H, S * H), "fc_bias": (H,),
     }[kind]
 
 
@@ -145,7 +150,7 @@ def _draw_chunk(kind: str, idx: int, seed: int, c: int, flat_out: np.ndarray) ->
     round_bf16(z, out=flat_out)
 
 
-def make_weights(cfg: ModelConfig, seed: int = 0, kinds=WEIGHT_KINDS,
+def make_weights(cfg: ModelConfig, seed: int = 0, kinds=BASE_KINDS,
                  threads: int = 8) -> dict[str, np.ndarray]:
     """All draft weights as bf16 bit arrays (uint16); fusion logits as float32.
 

@@ -15,13 +15,13 @@ from oracle import dflare_oracle as orc
 import test_oracle_pins as pins
 
 
-def _softmax_wrong_axis(lg):
+def _softmax_wrong_axis(lg, normalize=True):
     lg = np.asarray(lg, np.float64)
     e = np.exp(lg - lg.max(axis=0, keepdims=True))
     return e / e.sum(axis=0, keepdims=True)
 
 
-def _softmax_unnormalised(lg):
+def _softmax_unnormalised(lg, normalize=True):
     return np.exp(np.asarray(lg, np.float64))
 
 
@@ -209,7 +209,31 @@ def _uniforms_word0_only(seed, draw, slot, n_pos, vocab):
     return ((w >> np.uint64(41)).astype(np.float64) + 0.5) / float(1 << 23)
 
 
-_ORIG = {k: getattr(orc, k) for k in ("fuse_rows", "rope", "context_kv")}
+def _no_softmax_still_normalises(lg, normalize=True):
+    return _ORIG["fusion_weights"](lg)
+
+
+def _post_fc_transposed(f_i, w, b):
+    out = f_i @ w
+    return out if b is None else out + b
+
+
+def _post_fc_drops_bias(f_i, w, b):
+    return f_i @ w.T
+
+
+def _dflash_concat_wrong_order(hidden, w_fc, b_fc):
+    S, n, H = hidden.shape
+    concat = hidden.reshape(S * H, n).T  # not the S rows of one position side by side
+    out = concat @ w_fc.T
+    return out if b_fc is None else out + b_fc
+
+
+def _dflash_drops_bias(hidden, w_fc, b_fc):
+    return _ORIG["dflash_context"](hidden, w_fc, None)
+
+
+_ORIG = {k: getattr(orc, k) for k in ("fuse_rows", "rope", "context_kv", "fusion_weights", "dflash_context")}
 
 MUTANTS = {
     "softmax_wrong_axis": ("fusion_weights", _softmax_wrong_axis),
@@ -244,6 +268,11 @@ MUTANTS = {
     "philox_multipliers_swapped": ("philox4x64_10", _philox_swapped_multipliers),
     "uniforms_not_exact_in_fp32": ("sampling_uniforms", _uniforms_24_bits),
     "uniforms_same_word_for_four_positions": ("sampling_uniforms", _uniforms_word0_only),
+    "no_softmax_still_normalises": ("fusion_weights", _no_softmax_still_normalises),
+    "post_fc_transposed": ("post_fc", _post_fc_transposed),
+    "post_fc_drops_bias": ("post_fc", _post_fc_drops_bias),
+    "dflash_concat_wrong_order": ("dflash_context", _dflash_concat_wrong_order),
+    "dflash_drops_bias": ("dflash_context", _dflash_drops_bias),
 }
 
 

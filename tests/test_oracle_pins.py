@@ -663,4 +663,168 @@ def test_sampling_limits_and_replay():
     check_sampling_limits_and_replay()
 
 
+# --------------------------------------------------------------------------------------
+# model variants: the ablations of Sec. 6.3 (Table 2) and the DFlash baseline (Eq. 1-2)
+# --------------------------------------------------------------------------------------
+
+VAR = orc.VARIANT_NO_SOFTMAX, orc.VARIANT_SHARED_KV, orc.VARIANT_POST_FC, orc.VARIANT_DFLASH
+
+
+def variant_weights(cfg=MICRO, seed=0):
+    w = synth.make_weights(cfg, seed=seed, threads=1, kinds=synth.WEIGHT_KINDS)
+    logits = w.pop("fusion_logits")
+    return w, logits
+
+
+def loops_kv(f_rows, wk, wv, positions, cfg):
+    """K (rotated) and V of fused rows by explicit loops, as in check_context_kv_bruteforce."""
+    H, nkv, hd = cfg.hidden, cfg.n_kv_heads, cfg.head_dim
+    K, V = [], []
+    for r, p in zip(range(len(f_rows)), positions):
+        kr_all, vr_all = [], []
+        for g in range(nkv):
+            kr = [sum(f_rows[r][k] * wk[g * hd + d, k] for k in range(H)) for d in range(hd)]
+            vr = [sum(f_rows[r][k] * wv[g * hd + d, k] for k in range(H)) for d in range(hd)]
+            rot = []
+            for d in range(hd):
+                m = d % (hd // 2)
+                th = p / (cfg.rope_base ** (2.0 * m / hd))
+                if d < hd // 2:
+                    rot.append(kr[d] * math.cos(th) - kr[d + hd // 2] * math.sin(th))
+                else:
+                    rot.append(kr[d] * math.cos(th) + kr[d - hd // 2] * math.sin(th))
+            kr_all.append(rot)
+            vr_all.append(vr)
+        K.append(kr_all)
+        V.append(vr_all)
+    return np.array(K), np.array(V)
+
+
+def check_no_softmax_scale_invariance():
+    """-Softmax: alpha is W^fuse as given.  RMSNorm ignores a common positive scale of the
+    fused sum (up to eps), so raw weights c * softmax(x) reproduce the model with logits x;
+    a softmax left in place would turn c * softmax(x) into other weights."""
+    cfg = MICRO
+    w, lg = micro_weights(cfg)
+    hid = synth.hidden_rows(cfg, 0, 5)
+    ref = orc.DraftOracle(cfg, w, lg)
+    ref.append(hid)
+    a = orc.fusion_weights(lg)
+    for c in (0.37, 5.0):
+        raw = c * a
+        assert np.array_equal(orc.fusion_weights(raw, normalize=False), raw)
+        o = orc.DraftOracle(cfg, w, raw, variant=orc.VARIANT_NO_SOFTMAX)
+        o.append(hid)
+        # the eps term: RMSNorm(c u) / RMSNorm(u) = sqrt((m + eps) / (m + eps / c^2)), within
+        # eps (1 / c^2 - 1) / (2 m) ~ 2e-5 of 1 for rows with mean square m ~ 0.4
+        for i in range(cfg.n_draft_layers):
+            assert rel(o.k_cache[i], ref.k_cache[i]) < 1e-4 and rel(o.v_cache[i], ref.v_cache[i]) < 1e-4
+    # a raw weight vector that is not a scaled softmax gives another model
+    skew = a.copy()
+    skew[:, 0] *= 3.0
+    o = orc.DraftOracle(cfg, w, skew, variant=orc.VARIANT_NO_SOFTMAX)
+    o.append(hid)
+    assert rel(o.k_cache[0], ref.k_cache[0]) > 1e-3
+    for bad in (np.nan, np.inf, -np.inf):
+        x = a.copy()
+        x[0, 1] = bad
+        with pytest.raises(ValueError):
+            orc.fusion_weights(x, normalize=False)
+
+
+def check_shared_kv_bruteforce():
+    """-KVProj: the context K/V of layer i come from its own W_K^d, W_V^d (loops)."""
+    cfg = MICRO
+    w, lg = micro_weights(cfg)
+    hid = synth.hidden_rows(cfg, 0, 2)
+    o = orc.DraftOracle(cfg, w, lg, variant=orc.VARIANT_SHARED_KV)
+    f = o.append(hid)
+    for i in range(cfg.n_draft_layers):
+        K, V = loops_kv(f[i], f64(w["wk_d"][i]), f64(w["wv_d"][i]), [0, 1], cfg)
+        assert np.allclose(o.k_cache[i], K, rtol=1e-12, atol=1e-13)
+        assert np.allclose(o.v_cache[i], V, rtol=1e-12, atol=1e-13)
+
+
+def check_post_fc():
+    """+FC: f' = f W^T + b on the fused rows.  Identity layer without bias: the plain model,
+    bit for bit.  Zero weights: every row becomes b, so V = W_V^t b for all rows.  A random
+    layer against loops."""
+    cfg = MICRO
+    H, D = cfg.hidden, cfg.n_draft_layers
+    w, lg = variant_weights(cfg)
+    hid = synth.hidden_rows(cfg, 0, 3)
+    plain = orc.DraftOracle(cfg, w, lg)
+    plain.append(hid)
+    eye = dict(w, post_fc=np.broadcast_to(bf16(np.eye(H)), (D, H, H)).copy(), post_fc_bias=None)
+    o = orc.DraftOracle(cfg, eye, lg, variant=orc.VARIANT_POST_FC)
+    o.append(hid)
+    for i in range(D):
+        assert np.array_equal(o.k_cache[i], plain.k_cache[i]) and np.array_equal(o.v_cache[i], plain.v_cache[i])
+    zero = dict(w, post_fc=np.zeros((D, H, H), np.uint16))
+    o = orc.DraftOracle(cfg, zero, lg, variant=orc.VARIANT_POST_FC)
+    o.append(hid)
+    for i in range(D):
+        b = f64(w["post_fc_bias"][i])
+        wv = f64(w["wv_t"][i])
+        vb = [[sum(wv[g * cfg.head_dim + d, k] * b[k] for k in range(H)) for d in range(cfg.head_dim)]
+              for g in range(cfg.n_kv_heads)]
+        for r in range(3):
+            assert np.allclose(o.v_cache[i][r], vb, rtol=1e-12, atol=1e-13)
+    o = orc.DraftOracle(cfg, w, lg, variant=orc.VARIANT_POST_FC)
+    fp = o.append(hid)
+    f = orc.fuse_rows(orc.fusion_weights(lg), f64(hid), f64(w["fuse_norm"]), cfg.rms_eps)
+    for i in range(D):
+        W, b = f64(w["post_fc"][i]), f64(w["post_fc_bias"][i])
+        for r in range(3):
+            want = [sum(W[oo, k] * f[i, r, k] for k in range(H)) + b[oo] for oo in range(H)]
+            assert np.allclose(fp[i, r], want, rtol=1e-12, atol=1e-13)
+        K, V = loops_kv(fp[i], f64(w["wk_t"][i]), f64(w["wv_t"][i]), [0, 1, 2], cfg)
+        assert np.allclose(o.k_cache[i], K, rtol=1e-12, atol=1e-13)
+        assert np.allclose(o.v_cache[i], V, rtol=1e-12, atol=1e-13)
+
+
+def check_dflash_context():
+    """DFlash (Eq. 1-2): c_t = W_fc [h^(1); ...; h^(S)] + b_fc by loops, the same context for
+    every layer, projected by each layer's W_K^d, W_V^d; a W_fc that selects target layer j
+    (identity in block j, no bias) makes C the rows of layer j."""
+    cfg = MICRO
+    H, S, D = cfg.hidden, cfg.n_target_layers, cfg.n_draft_layers
+    w, _ = variant_weights(cfg)
+    hid = synth.hidden_rows(cfg, 0, 2)
+    h = f64(hid)
+    o = orc.DraftOracle(cfg, w, None, variant=orc.VARIANT_DFLASH)
+    c = o.append(hid)
+    W, b = f64(w["fc"]), f64(w["fc_bias"])
+    for t in range(2):
+        want = [sum(W[oo, j * H + k] * h[j, t, k] for j in range(S) for k in range(H)) + b[oo] for oo in range(H)]
+        assert np.allclose(c[0, t], want, rtol=1e-12, atol=1e-13)
+    for i in range(D):
+        assert np.array_equal(c[i], c[0])
+        K, V = loops_kv(c[i], f64(w["wk_d"][i]), f64(w["wv_d"][i]), [0, 1], cfg)
+        assert np.allclose(o.k_cache[i], K, rtol=1e-12, atol=1e-13)
+        assert np.allclose(o.v_cache[i], V, rtol=1e-12, atol=1e-13)
+    sel = np.zeros((H, S * H), np.float32)
+    sel[:, H:2 * H] = np.eye(H)
+    o = orc.DraftOracle(cfg, dict(w, fc=bf16(sel), fc_bias=None), None, variant=orc.VARIANT_DFLASH)
+    assert np.array_equal(o.append(hid)[0], h[1])
+    with pytest.raises(ValueError):
+        orc.DraftOracle(cfg, w, None, variant=orc.VARIANT_DFLASH | orc.VARIANT_POST_FC)
+
+
+def test_no_softmax_scale_invariance():
+    check_no_softmax_scale_invariance()
+
+
+def test_shared_kv_bruteforce():
+    check_shared_kv_bruteforce()
+
+
+def test_post_fc():
+    check_post_fc()
+
+
+def test_dflash_context():
+    check_dflash_context()
+
+
 ALL_CHECKS = [v for k, v in sorted(globals().items()) if k.startswith("check_")]
