@@ -31,6 +31,16 @@ METRIC = "draft blocks/sec (B=16, Qwen3-8B shape, batch 1) + % HBM roofline"
 HBM_PEAK_GBS = 8000.0
 
 
+# --variant -> (library flags, extra weight kinds)
+VARIANTS = {
+    "dflare": (0, ()),
+    "no_softmax": (1, ()),
+    "shared_kv": (2, ()),
+    "post_fc": (4, ("post_fc", "post_fc_bias")),
+    "dflash": (8, ("fc", "fc_bias")),
+}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -38,6 +48,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="qwen3_8b",
                     help="qwen3_8b (default), qwen3_4b, gpt_oss_20b, or batched (32 ragged sequences)")
+    ap.add_argument("--variant", default="dflare", choices=sorted(VARIANTS),
+                    help="model variant: the method (dflare), the Sec. 6.3 ablations (no_softmax, "
+                         "shared_kv, post_fc) or the DFlash FC fusion baseline (dflash)")
+    ap.add_argument("--target-layers", type=int, default=0,
+                    help="number S of fused target layers (default: the model's)")
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="0 (default): greedy drafts; > 0: Gumbel-max draws from softmax(z / T)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -63,10 +78,13 @@ def calibrate_copy():
     print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "launches": 3}), flush=True)
 
 
-def kernel_bytes(cfg, L, n_mean):
-    """Algorithmic HBM bytes per launch of each kernel kind (bf16 storage)."""
+def kernel_bytes(cfg, L, n_mean, variant="dflare"):
+    """Algorithmic HBM bytes per launch of each kernel kind (bf16 storage; the DFlash
+    append's "fuse" is the concatenation and the FC layer of Eq. 1, whose fp16 W_fc is read
+    once per append)."""
     H, F, V, D, S = cfg.hidden, cfg.ffn, cfg.vocab, cfg.n_draft_layers, cfg.n_target_layers
     q, kv = cfg.q_dim, cfg.kv_dim
+    fc = H * S * H * 2 if variant == "dflash" else 0
     return {
         "draft_block": cfg.block_bytes(L),    # every draft-layer weight, LM head, context K/V
         "qkv": (q + 2 * kv) * H * 2,          # W_Q, W_K^d, W_V^d of one layer
@@ -75,7 +93,7 @@ def kernel_bytes(cfg, L, n_mean):
         "gate_up": 2 * F * H * 2,
         "down": H * F * 2,
         "lm_head": V * H * 2,
-        "fuse": S * n_mean * H * 2,           # the target rows, read once
+        "fuse": S * n_mean * H * 2 + fc,      # the target rows, read once (+ W_fc)
         "kv_t": D * 2 * kv * H * 2,           # W_K^t, W_V^t of all layers (one launch)
     }
 
@@ -129,16 +147,21 @@ def main():
     from paper_2606_02091_amd import synth
 
     cfg = synth.CONFIGS[args.config]
+    if args.target_layers:
+        cfg = cfg.replace(n_target_layers=args.target_layers)
     L, B, S, H = cfg.context, cfg.block_size, cfg.n_target_layers, cfg.hidden
+    variant, extra = VARIANTS[args.variant]
+    dflash = args.variant == "dflash"
     torch.cuda.set_device(0)
     # a non-default stream of default priority, as a serving loop would use
     side = torch.cuda.Stream()
     torch.cuda.set_stream(side)
     t0 = time.time()
-    w = synth.make_weights(cfg)
+    w = synth.make_weights(cfg, kinds=synth.BASE_KINDS + extra)
     fusion_logits = w.pop("fusion_logits")
     print(f"[bench] weights generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
-    model = dfl.DraftModel(cfg, w, fusion_logits, max_context=L + 16, max_new=512)
+    model = dfl.DraftModel(cfg, w, None if dflash else fusion_logits, max_context=L + 16, max_new=512,
+                           variant=variant)
     h = model.h
     dfl.dflare_set_sampling(h, args.temperature, 1)
     chunk = 512
@@ -186,7 +209,7 @@ def main():
 
     # per-kernel durations (hipEvents in the library, one kind per pass).  The kernels of a
     # step: the persistent draft-block kernel, fusion and context K/V projection.
-    kb = kernel_bytes(cfg, L, n_mean)
+    kb = kernel_bytes(cfg, L, n_mean, args.variant)
 
     def profile(kinds):
         res = {}
@@ -203,7 +226,9 @@ def main():
                          "achieved_GBs": round(gbs, 1)}
         return res
 
-    kern = profile({"draft_block": dfl.K_DRAFT, "fuse": dfl.K_FUSE, "kv_t": dfl.K_KV_T})
+    # the DFlash append runs on the batched GEMM kernels (slot 0)
+    kern = profile({"draft_block": dfl.K_DRAFT, "fuse": dfl.K_B_FUSE if dflash else dfl.K_FUSE,
+                    "kv_t": dfl.K_B_KV_T if dflash else dfl.K_KV_T})
     dom = max(kern, key=lambda k: kern[k]["us_per_step"])
     d = kern[dom]
     # the same phases launched one kernel each (what the persistent launch saves)
@@ -211,7 +236,7 @@ def main():
                          "down": dfl.K_DOWN, "lm_head": dfl.K_LM_HEAD})
     phases = phase_trace(dfl, h, step, cfg, kb, args.profile_steps)
 
-    step_bytes = cfg.block_bytes(L) + cfg.append_bytes(n_mean)
+    step_bytes = cfg.block_bytes(L) + cfg.append_bytes(n_mean) + (H * S * H * 2 if dflash else 0)
     step_gbs = step_bytes / (ms * 1e-3) / 1e9
     result = {
         "metric": METRIC,
@@ -229,7 +254,8 @@ def main():
         "config": {"workload": f"{cfg.name}-shaped draft step: H={H}, {cfg.n_q_heads}q/{cfg.n_kv_heads}kv x "
                                f"{cfg.head_dim}, F={cfg.ffn}, V={cfg.vocab}, D={cfg.n_draft_layers}, S={S}, "
                                f"L={L}, B={B}, batch 1, n_new~U{{1..16}}"
-                               + (f", sampled at T={args.temperature}" if args.temperature > 0 else ", greedy"),
+                               + (f", sampled at T={args.temperature}" if args.temperature > 0 else ", greedy")
+                               + (f", variant {args.variant}" if args.variant != "dflare" else ""),
                    "global_batch": 1, "seq_len": L, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(d["achieved_GBs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(d["achieved_GBs"] / HBM_PEAK_GBS, 4),
@@ -244,7 +270,7 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context)
+        result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context, variant)
     print(json.dumps(result), flush=True)
     model.close()
 
@@ -445,7 +471,7 @@ def phase_trace(dfl, h, step, cfg, kb, steps):
     return out
 
 
-def cpu_baseline(cfg, w, fusion_logits, ctx):
+def cpu_baseline(cfg, w, fusion_logits, ctx, variant=0):
     """The fp64 oracle, as it stands, timed on this host for one draft step."""
     import numpy as np
     from threadpoolctl import threadpool_info
@@ -453,7 +479,7 @@ def cpu_baseline(cfg, w, fusion_logits, ctx):
     from oracle import dflare_oracle as orc
     from paper_2606_02091_amd import synth
 
-    o = orc.DraftOracle(cfg, w, fusion_logits, max_context=ctx + 64)
+    o = orc.DraftOracle(cfg, w, None if variant & 8 else fusion_logits, max_context=ctx + 64, variant=variant)
     o.append(synth.hidden_rows(cfg, 0, ctx))
     rows = synth.hidden_rows(cfg, ctx, 8)
     ids = synth.block_ids(cfg)

@@ -69,7 +69,33 @@ typedef struct {
   float rms_eps;           /* RMSNorm epsilon, e.g. 1e-6                         */
   int32_t max_batch;       /* sequence slots for the batched calls, 1..64
                               (0 means 1); slot 0 is the batch-1 context         */
+  int32_t variant;         /* 0, or DFLARE_VARIANT_* flags (below)               */
 } dflare_config;
+
+/*
+ * Model variants (dflare_config.variant; 0 is the method as described).  They change
+ * only how appended target rows become context K/V (dflare_fuse_append and its
+ * batched form); the draft block is the same for all of them.
+ *   NO_SOFTMAX  the -Softmax ablation (Sec. 6.3, Table 2): alpha = W^fuse as given,
+ *               every entry finite.
+ *   SHARED_KV   the -KVProj ablation (Sec. 6.3): the fused context goes through each
+ *               layer's own W_K^d, W_V^d; wk_t and wv_t are not read (may be NULL).
+ *   POST_FC     the +FC ablation (Sec. 6.3): f' = f W_pfc^T + b_pfc on each layer's
+ *               fused rows before its context projection (weights post_fc,
+ *               post_fc_bias).  The library folds the layer into the projection at
+ *               init: W' = W_K W_pfc and b' = W_K b_pfc (likewise for V) in double
+ *               precision, W' rounded to bf16, b' kept in fp32.
+ *   DFLASH      the DFlash baseline (Sec. 3.1-3.2, Eq. 1-2): one context row
+ *               c_t = W_fc [h_t^(1); ...; h_t^(S)] + b_fc (weights fc, fc_bias) for
+ *               every draft layer, projected by the layer's W_K^d, W_V^d; no fusion
+ *               weights (fusion_logits may be NULL) and no fusion norm.  The append
+ *               runs on fp16 matrix-core operands (target rows saturated to +-65504).
+ *               Not combinable with the other flags.
+ */
+#define DFLARE_VARIANT_NO_SOFTMAX 1
+#define DFLARE_VARIANT_SHARED_KV 2
+#define DFLARE_VARIANT_POST_FC 4
+#define DFLARE_VARIANT_DFLASH 8
 
 /*
  * Draft weights: device pointers to bf16 tensors, row-major, linear weights in the
@@ -94,6 +120,12 @@ typedef struct {
   const void* w_gate;     /* [D, F, H]  SwiGLU gate                             */
   const void* w_up;       /* [D, F, H]  SwiGLU up                               */
   const void* w_down;     /* [D, H, F]  SwiGLU down                             */
+  /* variant weights, read only by the variants that use them (NULL otherwise)    */
+  const void* post_fc;      /* [D, H, H]   POST_FC: W_pfc per draft layer        */
+  const void* post_fc_bias; /* [D, H]      POST_FC: b_pfc, or NULL for zeros      */
+  const void* fc;           /* [H, S*H]    DFLASH: W_fc (Eq. 1), input = the S
+                                           rows of a position in layer order      */
+  const void* fc_bias;      /* [H]         DFLASH: b_fc, or NULL for zeros        */
 } dflare_weights;
 
 typedef struct dflare_handle dflare_handle;
@@ -108,6 +140,10 @@ typedef struct dflare_handle dflare_handle;
  *   fusion_logits  HOST float [D, S] = W^fuse.  alpha = softmax of each row is
  *                  computed here in double precision and cached as float.  A row
  *                  with NaN or +inf, or with no finite entry, is INVALID_ARG.
+ *                  Unused (may be NULL) with DFLARE_VARIANT_DFLASH; taken as alpha
+ *                  itself with DFLARE_VARIANT_NO_SOFTMAX.
+ *   A variant value with unknown bits, DFLASH combined with another flag, or a
+ *   missing weight that the variant reads is INVALID_ARG.
  *   stream         hipStream_t for all work of this handle (NULL = default stream).
  *   out            receives the handle.  Every context starts empty (L = 0).
  * Each of the max_batch sequence slots owns a context cache of max_context rows

@@ -19,7 +19,7 @@ constexpr int kBSplitMax = 8;            // K parts of one batched GEMM output t
 constexpr long kBPartFloats = (long)kBWaves * kBM * kBNW * 256;  // one work-group's partial tile
 constexpr int kBCounters = 4096;         // split-K arrival counters (output tiles of one launch)
 
-enum BEpi { BEPI_QKV = 0, BEPI_RESID = 1, BEPI_SWIGLU = 2, BEPI_ARGMAX = 3 };
+enum BEpi { BEPI_QKV = 0, BEPI_RESID = 1, BEPI_SWIGLU = 2, BEPI_ARGMAX = 3, BEPI_BIAS16 = 4 };
 
 // Rows of one batched call, passed by value: call sequence i (cache slot seq[i], context
 // length L[i]) owns rows off[i] .. off[i+1]-1 of the call's activations; its attention work
@@ -55,10 +55,14 @@ struct BGemmArgs {
   long seq_stride, cache_layer;
   int layer0, Lcap, hd, q_tiles, kv_tiles;
   const float2* rope;
+  // QKV with q_tiles = 0 (context K/V): optional fp32 bias [layers][K kv | V kv], added
+  // before the rotation.  BIAS16: optional fp32 bias per output column.
+  const float* bias;
   // RESID: residual stream X [M, H] += Y
   float* X;
   int H;
-  // SWIGLU: fp16 A fragments of the MLP hidden rows [Mt][out_kt][64]
+  // SWIGLU: fp16 A fragments of the MLP hidden rows [Mt][out_kt][64]; BIAS16: fp16 A
+  // fragments of Y + bias in the same layout
   u32x4* out16;
   int out_kt;
   // ARGMAX: optional logits [M, V]; best (score, id) per (n-group, row); the score is the
@@ -99,6 +103,9 @@ void launch_bembed_norm(hipStream_t s, const uint16_t* embed, const int32_t* ids
 void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int S, int H, int D, const float* alpha,
                   const float* gain, float eps, u32x4* A, int mt_max);
 void launch_bfrag_rows(hipStream_t s, const u32x4* A, int n, int H, int D, int mt_max, float* out);
+// target rows [S, N, H] (bf16) -> fp16 A fragments of the rows [h^(1); ...; h^(S)] of each
+// position, [mt][S*H/32][64] (the input of the DFlash FC layer, Eq. 1)
+void launch_bfrag_cat(hipStream_t s, const uint16_t* hidden, int N, int S, int H, u32x4* A);
 void launch_battn(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, int items);
 void launch_bcomb(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, u32x4* out16, int a_kt);
 

@@ -267,6 +267,8 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
     }
     __syncthreads();
     const int tph = g.hd / 16, half = g.hd / 2;
+    const int kvd = g.kv_tiles * 16;
+    const float* kvb = g.bias ? g.bias + (long)(g.layer0 + layer) * 2 * kvd : nullptr;
 #pragma unroll
     for (int n = 0; n < kBNW; ++n) {
       const int nt = nt0 + n;
@@ -285,6 +287,8 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
       const int head = tt / tph, jj = tt % tph;
       const int mm = 8 * jj + (col & 7);
       const int dim = (col < 8) ? mm : half + mm;
+      // bias of this lane's column (context K/V only; region 0 has none)
+      const float bcol = (kvb && region > 0) ? kvb[(region == 1 ? 0 : kvd) + head * g.hd + (region == 1 ? dim : jj * 16 + col)] : 0.f;
       // the rotary factors of all 32 rows are loaded before any store (rows past M use
       // the slot of row M - 1), so that no load waits behind a store or a branch
       float2 cs[kBM][4];
@@ -299,7 +303,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = m * 16 + quad * 4 + e, row = row0 + r;
-          const float x = acc[m][n][e];
+          const float x = acc[m][n][e] + bcol;
           const float partner = __shfl_xor(x, 8);
           const int slot = s_slot[r];
           if (region < 2) {
@@ -352,6 +356,22 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
           const float h1 = __shfl_xor(hv, 1);
           if (nt < g.Nt && row < g.M && col < 8 && (col & 1) == 0)
             out[frag_off(row, nt * 8 + col, g.out_kt) >> 1] = pack_h2(hv, h1);
+        }
+    }
+  } else if constexpr (EPI == BEPI_BIAS16) {
+    uint32_t* out = reinterpret_cast<uint32_t*>(g.out16);
+#pragma unroll
+    for (int n = 0; n < kBNW; ++n) {
+      const int nt = nt0 + n;
+      const float bcol = (g.bias && nt < g.Nt) ? g.bias[nt * 16 + col] : 0.f;
+#pragma unroll
+      for (int m = 0; m < kBM; ++m)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int row = row0 + m * 16 + quad * 4 + e;
+          const float y = acc[m][n][e] + bcol;
+          const float y1 = __shfl_xor(y, 1);
+          if (nt < g.Nt && row < g.M && (col & 1) == 0) out[frag_off(row, nt * 16 + col, g.out_kt) >> 1] = pack_h2(y, y1);
         }
     }
   } else if constexpr (EPI == BEPI_ARGMAX) {
@@ -616,6 +636,23 @@ __global__ void k_bfrag_rows(const u32x4* A, int n, int H, int mt_max, float* ou
   for (int k = threadIdx.x; k < H; k += blockDim.x) out[((long)i * n + r) * H + k] = h2f(a[frag_off(r, k, Kt)]);
 }
 
+// DFlash FC input (Eq. 1): row r of the call, the S target rows of its position side by
+// side in layer order, as fp16 A fragments [mt][S*H/32][64]; block (row r, target layer j),
+// a thread converts 8 consecutive values (one 16-byte fragment slot).
+__global__ __launch_bounds__(256) void k_bfrag_cat(const uint16_t* hidden, int N, int S, int H, u32x4* A) {
+  const int r = blockIdx.x, j = blockIdx.y, Kt = S * H / 32;
+  for (int k0 = threadIdx.x * 8; k0 < H; k0 += 256 * 8) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(hidden + ((long)j * N + r) * H + k0);
+    float f[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      f[2 * e] = bf2f(v[e] & 0xFFFFu);
+      f[2 * e + 1] = bf2f(v[e] >> 16);
+    }
+    A[frag_off(r, j * H + k0, Kt) >> 3] = pack_h8(f);
+  }
+}
+
 // ------------------------------------------------------------------------------------------
 // attention over ragged contexts (Sec. 3.2: no mask; the block rows of a sequence see its
 // whole context and the whole block, whose keys and values are already in the cache at
@@ -876,6 +913,7 @@ void launch_bgemm(hipStream_t s, int epi, const BGemmArgs& g, const BRows& rows)
     case BEPI_QKV: hipLaunchKernelGGL(k_bgemm<BEPI_QKV>, grid, dim3(kBT), 0, s, g, rows); break;
     case BEPI_RESID: hipLaunchKernelGGL(k_bgemm<BEPI_RESID>, grid, dim3(kBT), 0, s, g, rows); break;
     case BEPI_SWIGLU: hipLaunchKernelGGL(k_bgemm<BEPI_SWIGLU>, grid, dim3(kBT), 0, s, g, rows); break;
+    case BEPI_BIAS16: hipLaunchKernelGGL(k_bgemm<BEPI_BIAS16>, grid, dim3(kBT), 0, s, g, rows); break;
     default: hipLaunchKernelGGL(k_bgemm<BEPI_ARGMAX>, grid, dim3(kBT), 0, s, g, rows); break;
   }
 }
@@ -896,6 +934,10 @@ void launch_bembed_norm(hipStream_t s, const uint16_t* embed, const int32_t* ids
 void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int S, int H, int D, const float* alpha,
                   const float* gain, float eps, u32x4* A, int mt_max) {
   hipLaunchKernelGGL(k_bfuse, dim3(N, D), dim3(256), 0, s, hidden, N, S, H, alpha, gain, eps, A, mt_max);
+}
+
+void launch_bfrag_cat(hipStream_t s, const uint16_t* hidden, int N, int S, int H, u32x4* A) {
+  hipLaunchKernelGGL(k_bfrag_cat, dim3(N, S), dim3(256), 0, s, hidden, N, S, H, A);
 }
 
 void launch_bfrag_rows(hipStream_t s, const u32x4* A, int n, int H, int D, int mt_max, float* out) {

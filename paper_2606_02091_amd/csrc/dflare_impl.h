@@ -156,12 +156,18 @@ struct KvtArgs {
   long cache_layer_stride;
   int Lcap, hd, kv_tiles;
   const float2* rope;
+  const float* bias;       // optional fp32 [D][K kv | V kv], added before the rotation
 };
 
 // ---- launchers (kernels.hip) ----
 void launch_pack(hipStream_t s, u32x4* dst, const uint16_t* src0, const uint16_t* src1,
                  int n_src_rows, int K, int nt_begin, int nt_count, int Kt_total, int mode, int hd);
 void launch_bf16_to_f32(hipStream_t s, float* dst, const uint16_t* src, long n);
+// init: out[R, K] (bf16, round to nearest even) = A[R, O] B[O, K] with bf16 row-major
+// inputs, accumulated in double precision
+void launch_compose(hipStream_t s, uint16_t* out, const uint16_t* A, const uint16_t* B, int R, int O, int K);
+// init: y[R] (fp32) = A[R, O] b[O] in double precision (b bf16; NULL gives zeros)
+void launch_matvec(hipStream_t s, float* y, const uint16_t* A, const uint16_t* b, int R, int O);
 void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
                  const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max);
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n,

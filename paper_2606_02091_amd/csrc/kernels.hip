@@ -274,12 +274,17 @@ __global__ __launch_bounds__(64 * WAVES) void k_kvt(KvtArgs a) {
     const bool is_k = nt < a.kv_tiles;
     const int t = is_k ? nt : nt - a.kv_tiles;
     const int head = t / tph, jj = t % tph;
+    // bias of this lane's column (K columns are packed in rotary pair order)
+    const int kvd = a.kv_tiles * 16;
+    const int kdim = (col < 8) ? 8 * jj + (col & 7) : half + 8 * jj + (col & 7);
+    const float bcol =
+        a.bias ? a.bias[(long)layer * 2 * kvd + (is_k ? head * a.hd + kdim : kvd + head * a.hd + jj * 16 + col)] : 0.f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = mt * 16 + quad * 4 + i;
       const bool valid = row < M;
       const int slot = a.L + row;
-      const float x = v[i];
+      const float x = v[i] + bcol;
       const float partner = __shfl_xor(x, 8);
       if (is_k) {
         const int m = 8 * jj + (col & 7);
@@ -293,6 +298,58 @@ __global__ __launch_bounds__(64 * WAVES) void k_kvt(KvtArgs a) {
       }
     }
   }
+}
+
+// ---- init: folding a linear layer into the next one (the +FC variant) ----
+// out = A B for bf16 row-major A [R, O] and B [O, K], in double precision.  Work-group:
+// a 64 x 64 tile of out, 256 threads with 4 x 4 outputs each; 16-deep slices of A and B
+// staged in LDS as doubles.
+__global__ __launch_bounds__(256) void k_compose(uint16_t* out, const uint16_t* A, const uint16_t* B, int R, int O,
+                                                 int K) {
+  __shared__ double sa[16][65];
+  __shared__ double sb[16][65];
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  double acc[4][4] = {};
+  for (int o0 = 0; o0 < O; o0 += 16) {
+    for (int i = threadIdx.x; i < 16 * 64; i += 256) {
+      const int oo = i & 15, rr = i >> 4;  // A: row r0 + rr, column o0 + oo
+      sa[oo][rr] = (r0 + rr < R && o0 + oo < O) ? (double)bf2f(A[(long)(r0 + rr) * O + o0 + oo]) : 0.0;
+      const int cc = i & 63, ob = i >> 6;  // B: row o0 + ob, column c0 + cc
+      sb[ob][cc] = (o0 + ob < O && c0 + cc < K) ? (double)bf2f(B[(long)(o0 + ob) * K + c0 + cc]) : 0.0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int oo = 0; oo < 16; ++oo)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] += sa[oo][ty * 4 + i] * sb[oo][tx * 4 + j];
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = r0 + ty * 4 + i, c = c0 + tx * 4 + j;
+      if (r < R && c < K) out[(long)r * K + c] = f2bf((float)acc[i][j]);
+    }
+}
+
+// y = A b in double precision: one work-group of 256 per output row
+__global__ __launch_bounds__(256) void k_matvec(float* y, const uint16_t* A, const uint16_t* b, int O) {
+  __shared__ double red[256];
+  const int r = blockIdx.x;
+  double s = 0.0;
+  if (b)
+    for (int o = threadIdx.x; o < O; o += 256) s += (double)bf2f(A[(long)r * O + o]) * (double)bf2f(b[o]);
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) y[r] = (float)red[0];
 }
 
 // ==========================================================================================
@@ -1424,6 +1481,14 @@ void launch_pack(hipStream_t s, u32x4* dst, const uint16_t* src0, const uint16_t
   if (blocks > 65536) blocks = 65536;
   hipLaunchKernelGGL(k_pack, dim3(blocks), dim3(256), 0, s, dst, src0, src1, n_src_rows, K, nt_begin, nt_count,
                      Kt_total, mode, hd);
+}
+
+void launch_compose(hipStream_t s, uint16_t* out, const uint16_t* A, const uint16_t* B, int R, int O, int K) {
+  hipLaunchKernelGGL(k_compose, dim3((K + 63) / 64, (R + 63) / 64), dim3(256), 0, s, out, A, B, R, O, K);
+}
+
+void launch_matvec(hipStream_t s, float* y, const uint16_t* A, const uint16_t* b, int R, int O) {
+  hipLaunchKernelGGL(k_matvec, dim3(R), dim3(256), 0, s, y, A, b, O);
 }
 
 void launch_bf16_to_f32(hipStream_t s, float* dst, const uint16_t* src, long n) {

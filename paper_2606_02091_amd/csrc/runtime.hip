@@ -132,6 +132,12 @@ struct dflare_handle {
   float2* bML = nullptr;
   u32x4 *bA = nullptr, *bOA = nullptr, *bHA = nullptr;  // fp16 A fragments of the GEMM inputs
   u32x4* bU = nullptr;     // fp16 A fragments of the fused rows of a batched append, per layer
+  // variants: K/V bias of the folded +FC layer [D][2 kv]; DFlash FC weights (bf16 tiles and
+  // their fp16 copy), bias, and the fragments of its input rows and of the context rows
+  float* kv_bias = nullptr;
+  u32x4 *w_fc = nullptr, *h_fc = nullptr;
+  float* fc_bias = nullptr;
+  u32x4 *bCat = nullptr, *bC = nullptr;
   // fp16 copies of the packed weight tiles, made on first use of the batched path
   u32x4 *h_qkv = nullptr, *h_o = nullptr, *h_gu = nullptr, *h_down = nullptr, *h_kvt = nullptr, *h_lm = nullptr;
   float* bpart = nullptr;  // split-K partial tiles
@@ -248,6 +254,9 @@ int validate_config(const dflare_config* c) {
     return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "max_context too large");
   if (c->max_batch < 0 || c->max_batch > kMaxSeq)
     return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "max_batch must be in [0, 64]");
+  if (c->variant & ~15) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "unknown variant flags");
+  if ((c->variant & DFLARE_VARIANT_DFLASH) && (c->variant & ~DFLARE_VARIANT_DFLASH))
+    return fail(nullptr, DFLARE_ERR_INVALID_ARG, "DFLASH does not combine with other variant flags");
   return DFLARE_OK;
 }
 
@@ -403,8 +412,17 @@ int build(dflare_handle* h, const dflare_weights* w) {
   const uint16_t* wq = (const uint16_t*)w->wq;
   const uint16_t* wkd = (const uint16_t*)w->wk_d;
   const uint16_t* wvd = (const uint16_t*)w->wv_d;
-  const uint16_t* wkt = (const uint16_t*)w->wk_t;
-  const uint16_t* wvt = (const uint16_t*)w->wv_t;
+  // context projections: W^t (Eq. 4), or the draft layer's own W^d (-KVProj, DFlash)
+  const bool shared_kv = c.variant & (DFLARE_VARIANT_SHARED_KV | DFLARE_VARIANT_DFLASH);
+  const uint16_t* wkt = (const uint16_t*)(shared_kv ? w->wk_d : w->wk_t);
+  const uint16_t* wvt = (const uint16_t*)(shared_kv ? w->wv_d : w->wv_t);
+  // +FC: W' = W W_pfc per layer (double precision, rounded to bf16), b' = W b_pfc in fp32
+  uint16_t *fold_k = nullptr, *fold_v = nullptr;
+  if (c.variant & DFLARE_VARIANT_POST_FC) {
+    TRY(dev_alloc(h, &fold_k, (size_t)kv * H * 2));
+    TRY(dev_alloc(h, &fold_v, (size_t)kv * H * 2));
+    TRY(dev_alloc(h, &h->kv_bias, (size_t)D * 2 * kv * 4));
+  }
   const uint16_t* wo = (const uint16_t*)w->wo;
   const uint16_t* wg = (const uint16_t*)w->w_gate;
   const uint16_t* wu = (const uint16_t*)w->w_up;
@@ -415,8 +433,20 @@ int build(dflare_handle* h, const dflare_weights* w) {
     launch_pack(s, dq, wkd + (long)i * kv * H, nullptr, kv, H, q / 16, kv / 16, Kt_H, PACK_ROPE, hd);
     launch_pack(s, dq, wvd + (long)i * kv * H, nullptr, kv, H, (q + kv) / 16, kv / 16, Kt_H, PACK_IDENTITY, hd);
     u32x4* dk = h->w_kvt + i * h->s_kvt;
-    launch_pack(s, dk, wkt + (long)i * kv * H, nullptr, kv, H, 0, kv / 16, Kt_H, PACK_ROPE, hd);
-    launch_pack(s, dk, wvt + (long)i * kv * H, nullptr, kv, H, kv / 16, kv / 16, Kt_H, PACK_IDENTITY, hd);
+    const uint16_t* src_k = wkt + (long)i * kv * H;
+    const uint16_t* src_v = wvt + (long)i * kv * H;
+    if (c.variant & DFLARE_VARIANT_POST_FC) {
+      const uint16_t* pfc = (const uint16_t*)w->post_fc + (long)i * H * H;
+      const uint16_t* pb = w->post_fc_bias ? (const uint16_t*)w->post_fc_bias + (long)i * H : nullptr;
+      launch_compose(s, fold_k, src_k, pfc, kv, H, H);
+      launch_compose(s, fold_v, src_v, pfc, kv, H, H);
+      launch_matvec(s, h->kv_bias + (long)i * 2 * kv, src_k, pb, kv, H);
+      launch_matvec(s, h->kv_bias + (long)i * 2 * kv + kv, src_v, pb, kv, H);
+      src_k = fold_k;
+      src_v = fold_v;
+    }
+    launch_pack(s, dk, src_k, nullptr, kv, H, 0, kv / 16, Kt_H, PACK_ROPE, hd);
+    launch_pack(s, dk, src_v, nullptr, kv, H, kv / 16, kv / 16, Kt_H, PACK_IDENTITY, hd);
     launch_pack(s, h->w_o + i * h->s_o, wo + (long)i * H * q, nullptr, H, q, 0, Nt_o, Kt_q, PACK_IDENTITY, hd);
     launch_pack(s, h->w_gu + i * h->s_gu, wg + (long)i * F * H, wu + (long)i * F * H, F, H, 0, Nt_gu, Kt_H,
                 PACK_SWIGLU, hd);
@@ -424,6 +454,12 @@ int build(dflare_handle* h, const dflare_weights* w) {
                 PACK_IDENTITY, hd);
   }
   launch_pack(s, h->w_lm, (const uint16_t*)w->lm_head, nullptr, V, H, 0, Nt_lm, Kt_H, PACK_IDENTITY, hd);
+  if (c.variant & DFLARE_VARIANT_DFLASH) {  // W_fc [H, S*H] as tiles of H/16 outputs x S*H/32 k
+    TRY(dev_alloc(h, &h->w_fc, (size_t)(H / 16) * (S * H / 32) * 64 * 16));
+    launch_pack(s, h->w_fc, (const uint16_t*)w->fc, nullptr, H, S * H, 0, H / 16, S * H / 32, PACK_IDENTITY, hd);
+    TRY(dev_zalloc(h, &h->fc_bias, (size_t)H * 4));
+    if (w->fc_bias) launch_bf16_to_f32(s, h->fc_bias, (const uint16_t*)w->fc_bias, (long)H);
+  }
   TRY(check_launch(h, "weight packing"));
   HIP_OR_FAIL(h, hipMemcpyAsync(h->embed, w->embed, (size_t)V * H * 2, hipMemcpyDeviceToDevice, s));
 
@@ -496,6 +532,10 @@ int build(dflare_handle* h, const dflare_weights* w) {
     TRY(dev_zalloc(h, &h->bOA, (size_t)h->b_mt * Kt_q * 1024));
     TRY(dev_zalloc(h, &h->bHA, (size_t)h->b_mt * Kt_F * 1024));
     TRY(dev_zalloc(h, &h->bU, (size_t)D * mt_max * Kt_H * 1024));
+    if (c.variant & DFLARE_VARIANT_DFLASH) {
+      TRY(dev_zalloc(h, &h->bCat, (size_t)mt_max * (S * H / 32) * 1024));
+      TRY(dev_zalloc(h, &h->bC, (size_t)mt_max * Kt_H * 1024));
+    }
     // partial tiles of the largest split of any call shape
     long part = 0;
     auto need = [&](const char* name, int Nt, int mt, int Kt, int layers) {
@@ -508,7 +548,10 @@ int build(dflare_handle* h, const dflare_weights* w) {
       need("GU", Nt_gu, mt, Kt_H, 1);
       need("DOWN", Nt_down, mt, Kt_F, 1);
     }
-    for (int mt = 1; mt <= mt_max; ++mt) need("KVT", Nt_kvt, mt, Kt_H, D);
+    for (int mt = 1; mt <= mt_max; ++mt) {
+      need("KVT", Nt_kvt, mt, Kt_H, D);
+      if (c.variant & DFLARE_VARIANT_DFLASH) need("FC", H / 16, mt, S * H / 32, 1);
+    }
     h->bpart_floats = part;
     TRY(dev_alloc(h, &h->bpart, (size_t)std::max(part, 64L) * 4));
     TRY(dev_zalloc(h, &h->bcnt, (size_t)kBCounters * 128));
@@ -519,7 +562,7 @@ int build(dflare_handle* h, const dflare_weights* w) {
     TRY(dev_alloc(h, &h->bpmax, (size_t)ng_lm * rows * 4));
     TRY(dev_alloc(h, &h->bpidx, (size_t)ng_lm * rows * 4));
   }
-  if (c.max_batch > 1) TRY(ensure_f16_weights(h));
+  if (c.max_batch > 1 || (c.variant & DFLARE_VARIANT_DFLASH)) TRY(ensure_f16_weights(h));
   HIP_OR_FAIL(h, hipHostMalloc((void**)&h->err_host, 64, hipHostMallocMapped | hipHostMallocCoherent));
   *(volatile int*)h->err_host = 0;
   HIP_OR_FAIL(h, hipHostGetDevicePointer((void**)&h->err_dev, h->err_host, 0));
@@ -723,6 +766,11 @@ int ensure_f16_weights(dflare_handle* h) {
     launch_tiles_to_f16(h->stream, p, it.src, it.n);
     *it.dst = p;
   }
+  if (h->w_fc) {
+    const long n = (long)(c.hidden / 16) * (c.n_target_layers * c.hidden / 32) * 64;
+    TRY(dev_alloc(h, &h->h_fc, (size_t)n * 16));
+    launch_tiles_to_f16(h->stream, h->h_fc, h->w_fc, n);
+  }
   return check_launch(h, "weight conversion");
 }
 
@@ -776,12 +824,36 @@ int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int3
     rows.off[i + 1] = rows.off[i] + n_new[i];
   }
   const int N = rows.off[n_seq];
-  prof_mark(h, DFLARE_K_B_FUSE, true);
-  launch_bfuse(s, (const uint16_t*)hidden, N, S, H, D, h->alpha, h->g_fuse, c.rms_eps, h->bU, h->mt_max);
-  prof_mark(h, DFLARE_K_B_FUSE, false);
+  const bool dflash = c.variant & DFLARE_VARIANT_DFLASH;
   BGemmArgs g = bgemm_base(h);
-  g.A = h->bU;
-  g.a_layer = (long)h->mt_max * Kt_H * 64;
+  if (dflash) {
+    // Eq. 1: C = [h^(1); ...; h^(S)] W_fc^T + b_fc for all N rows, as fp16 fragments
+    prof_mark(h, DFLARE_K_B_FUSE, true);
+    launch_bfrag_cat(s, (const uint16_t*)hidden, N, S, H, h->bCat);
+    g.A = h->bCat;
+    g.a_layer = 0;
+    g.W = h->h_fc;
+    g.w_layer = 0;
+    g.Nt = H / 16;
+    g.Kt = S * H / 32;
+    g.Mt = ceil_div(N, 16);
+    g.M = N;
+    g.out16 = h->bC;
+    g.out_kt = Kt_H;
+    g.bias = h->fc_bias;
+    bgemm(h, -1, "FC", BEPI_BIAS16, g, rows);
+    prof_mark(h, DFLARE_K_B_FUSE, false);
+    g = bgemm_base(h);
+    g.A = h->bC;  // the same context rows for every layer (Eq. 2)
+    g.a_layer = 0;
+  } else {
+    prof_mark(h, DFLARE_K_B_FUSE, true);
+    launch_bfuse(s, (const uint16_t*)hidden, N, S, H, D, h->alpha, h->g_fuse, c.rms_eps, h->bU, h->mt_max);
+    prof_mark(h, DFLARE_K_B_FUSE, false);
+    g.A = h->bU;
+    g.a_layer = (long)h->mt_max * Kt_H * 64;
+    g.bias = h->kv_bias;
+  }
   g.W = h->h_kvt;
   g.w_layer = h->s_kvt;
   g.Nt = 2 * h->kv_dim / 16;
@@ -792,8 +864,8 @@ int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int3
   g.layer0 = 0;
   g.q_tiles = 0;
   bgemm(h, DFLARE_K_B_KV_T, "KVT", BEPI_QKV, g, rows);
-  if (h->debug) {
-    launch_bfrag_rows(s, h->bU, N, H, D, h->mt_max, h->dbg_fused);
+  if (h->debug) {  // DFlash: the shared context rows, as layer 0
+    launch_bfrag_rows(s, dflash ? h->bC : h->bU, N, H, dflash ? 1 : D, h->mt_max, h->dbg_fused);
     h->dbg_fused_n = N;
   }
   TRY(check_launch(h, "fuse_append_batched"));
@@ -899,14 +971,29 @@ int dflare_init(const dflare_config* cfg, const dflare_weights* w, const float* 
   if (!out) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   TRY(validate_config(cfg));
-  if (!w || !w->embed || !w->lm_head || !w->wq || !w->wk_d || !w->wv_d || !w->wk_t || !w->wv_t || !w->wo ||
-      !w->w_gate || !w->w_up || !w->w_down)
+  const int var = cfg->variant;
+  const bool dflash = var & DFLARE_VARIANT_DFLASH;
+  const bool need_t = !(var & (DFLARE_VARIANT_SHARED_KV | DFLARE_VARIANT_DFLASH));
+  if (!w || !w->embed || !w->lm_head || !w->wq || !w->wk_d || !w->wv_d || (need_t && (!w->wk_t || !w->wv_t)) ||
+      !w->wo || !w->w_gate || !w->w_up || !w->w_down)
     return fail(nullptr, DFLARE_ERR_INVALID_ARG, "a required weight pointer is NULL");
-  if (!fusion_logits) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "fusion_logits is NULL");
+  if ((var & DFLARE_VARIANT_POST_FC) && !w->post_fc)
+    return fail(nullptr, DFLARE_ERR_INVALID_ARG, "POST_FC needs post_fc");
+  if (dflash && !w->fc) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "DFLASH needs fc");
+  if (!fusion_logits && !dflash) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "fusion_logits is NULL");
   const int D = cfg->n_draft_layers, S = cfg->n_target_layers;
-  // alpha^(i) = softmax(W^fuse_{i,:}) in double precision, cached as float (Sec. 4.1)
-  std::vector<float> alpha((size_t)D * S);
-  for (int i = 0; i < D; ++i) {
+  // alpha^(i) = softmax(W^fuse_{i,:}) in double precision, cached as float (Sec. 4.1);
+  // -Softmax (Sec. 6.3) keeps W^fuse itself; DFlash has no fusion weights
+  std::vector<float> alpha((size_t)D * S, 0.f);
+  for (int i = 0; i < D && !dflash; ++i) {
+    if (var & DFLARE_VARIANT_NO_SOFTMAX) {
+      for (int j = 0; j < S; ++j) {
+        const float x = fusion_logits[(size_t)i * S + j];
+        if (!isfinite(x)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "unnormalised fusion weights must be finite");
+        alpha[(size_t)i * S + j] = x;
+      }
+      continue;
+    }
     const float* row = fusion_logits + (size_t)i * S;
     double mx = -INFINITY;
     for (int j = 0; j < S; ++j) {
@@ -948,6 +1035,11 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   if ((long)h->Ls[0] + n_new > h->cfg.max_context)
     return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
   const dflare_config& c = h->cfg;
+  if (c.variant & DFLARE_VARIANT_DFLASH) {  // the FC fusion runs on the batched GEMM, slot 0
+    const int32_t seq0 = 0;
+    const int rc = run_fuse_batched(h, 1, &seq0, &n_new, target_hidden);
+    return rc;
+  }
   const int H = c.hidden, D = c.n_draft_layers, S = c.n_target_layers;
   hipStream_t s = h->stream;
   prof_mark(h, DFLARE_K_FUSE, true);
@@ -977,6 +1069,7 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   a.hd = c.head_dim;
   a.kv_tiles = h->kv_dim / 16;
   a.rope = h->rope;
+  a.bias = h->kv_bias;
   prof_mark(h, DFLARE_K_KV_T, true);
   launch_kvt(s, h->kvt_nt, h->kvt_waves, a, D, ceil_div(n_new, 16));
   prof_mark(h, DFLARE_K_KV_T, false);

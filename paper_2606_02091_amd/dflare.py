@@ -43,11 +43,17 @@ class dflare_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "hidden", "n_q_heads", "n_kv_heads", "head_dim", "ffn", "vocab", "n_draft_layers",
         "n_target_layers", "block_size", "max_context", "max_new")] + [
-        ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float), ("max_batch", ctypes.c_int32)]
+        ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float), ("max_batch", ctypes.c_int32),
+        ("variant", ctypes.c_int32)]
+
+
+# model variants (dflare_config.variant), as in include/dflare.h
+VARIANT_NO_SOFTMAX, VARIANT_SHARED_KV, VARIANT_POST_FC, VARIANT_DFLASH = 1, 2, 4, 8
 
 
 WEIGHT_FIELDS = ("embed", "lm_head", "final_norm", "fuse_norm", "attn_norm", "mlp_norm", "wq", "wk_d",
-                 "wv_d", "wk_t", "wv_t", "wo", "w_gate", "w_up", "w_down")
+                 "wv_d", "wk_t", "wv_t", "wo", "w_gate", "w_up", "w_down", "post_fc", "post_fc_bias", "fc",
+                 "fc_bias")
 
 
 class dflare_weights(ctypes.Structure):
@@ -123,20 +129,22 @@ def _stream(stream) -> int:
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
 
-def make_config(cfg, max_context: int, max_new: int = 16, max_batch: int = 1) -> dflare_config:
+def make_config(cfg, max_context: int, max_new: int = 16, max_batch: int = 1, variant: int = 0) -> dflare_config:
     """dflare_config from any object with the model attributes (hidden, n_q_heads, ...)."""
     return dflare_config(cfg.hidden, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn, cfg.vocab,
                          cfg.n_draft_layers, cfg.n_target_layers, cfg.block_size, max_context, max_new,
-                         cfg.rope_base, cfg.rms_eps, max_batch)
+                         cfg.rope_base, cfg.rms_eps, max_batch, variant)
 
 
 def dflare_init(config: dflare_config, weights: dict, fusion_logits, stream=None) -> int:
     """Create a handle; weights maps field name -> device tensor (None for unit norm gains)."""
     w = dflare_weights(**{k: _ptr(weights.get(k)) for k in WEIGHT_FIELDS})
-    lg = np.ascontiguousarray(np.asarray(fusion_logits, dtype=np.float32))
+    lg_ptr = None
+    if fusion_logits is not None:  # may be None for the DFlash variant
+        lg = np.ascontiguousarray(np.asarray(fusion_logits, dtype=np.float32))
+        lg_ptr = lg.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
     h = ctypes.c_void_p()
-    rc = lib().dflare_init(ctypes.byref(config), ctypes.byref(w),
-                           lg.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), _stream(stream), ctypes.byref(h))
+    rc = lib().dflare_init(ctypes.byref(config), ctypes.byref(w), lg_ptr, _stream(stream), ctypes.byref(h))
     _check(rc, None)
     return h.value
 
@@ -262,9 +270,9 @@ class DraftModel:
     """Owner of one handle: the three calls of the draft step plus helpers."""
 
     def __init__(self, cfg, weights_bits: dict, fusion_logits, max_context: int, max_new: int = 16,
-                 device="cuda", stream=None, max_batch: int = 1):
+                 device="cuda", stream=None, max_batch: int = 1, variant: int = 0):
         self.cfg = cfg
-        self.config = make_config(cfg, max_context, max_new, max_batch)
+        self.config = make_config(cfg, max_context, max_new, max_batch, variant)
         dev = {k: (None if weights_bits.get(k) is None else bf16_tensor(weights_bits[k], device))
                for k in WEIGHT_FIELDS}
         self.h = dflare_init(self.config, dev, fusion_logits, stream)

@@ -49,8 +49,8 @@ def _cfg(**kw):
     return c
 
 
-def _init(cfg, logits=None, weights=True):
-    w = dfl.dflare_weights(**{k: (0x1000 if weights else None) for k in dfl.WEIGHT_FIELDS})
+def _init(cfg, logits=None, weights=True, drop=()):
+    w = dfl.dflare_weights(**{k: (0x1000 if weights and k not in drop else None) for k in dfl.WEIGHT_FIELDS})
     lg = np.zeros((cfg.n_draft_layers, cfg.n_target_layers), np.float32) if logits is None else logits
     lg = np.ascontiguousarray(lg, np.float32)
     h = ctypes.c_void_p()
@@ -85,6 +85,28 @@ def test_init_rejects_bad_fusion_logits(L):
         assert rc == dfl.ERR_INVALID_ARG and not h
     lg = np.full((cfg.n_draft_layers, cfg.n_target_layers), -np.inf, np.float32)
     assert _init(cfg, lg)[0] == dfl.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("variant", [16, dfl.VARIANT_DFLASH | dfl.VARIANT_NO_SOFTMAX,
+                                     dfl.VARIANT_DFLASH | dfl.VARIANT_SHARED_KV, -1])
+def test_init_rejects_bad_variant(L, variant):
+    rc, h = _init(_cfg(variant=variant))
+    assert rc == dfl.ERR_INVALID_ARG and not h
+
+
+def test_init_rejects_variants_without_their_weights(L):
+    # +FC needs post_fc, DFlash needs fc (checked before any device work)
+    for variant, field in ((dfl.VARIANT_POST_FC, "post_fc"), (dfl.VARIANT_DFLASH, "fc")):
+        rc, h = _init(_cfg(variant=variant), drop=(field,))
+        assert rc == dfl.ERR_INVALID_ARG and not h
+        assert b"needs" in L.dflare_last_error(None)
+    # -Softmax takes W^fuse as the weights: every entry must be finite
+    cfg = _cfg(variant=dfl.VARIANT_NO_SOFTMAX)
+    for bad in (np.nan, np.inf, -np.inf):
+        lg = np.zeros((cfg.n_draft_layers, cfg.n_target_layers), np.float32)
+        lg[0, 1] = bad
+        rc, h = _init(cfg, lg)
+        assert rc == dfl.ERR_INVALID_ARG and not h
 
 
 def test_init_rejects_missing_weights(L):
