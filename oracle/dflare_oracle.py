@@ -32,6 +32,10 @@ with W in R^{d x d_kv}; it is the same map).
 Temperature sampling (Sec. 5, Table 1 lower half): Gumbel-max draws with uniforms from
 Philox4x64-10; see sample_tokens.
 
+Verification (Sec. 3.2, verification phase), given the target's outputs: accept_block takes
+the longest prefix of candidates that the target agrees with and the bonus token;
+DraftOracle.accept appends the target rows of the verified positions.
+
 Variants (DraftOracle's `variant` bit field; 0 is the method as described):
 * VARIANT_NO_SOFTMAX  -Softmax of Sec. 6.3 (Table 2): alpha = W^fuse as given
 * VARIANT_SHARED_KV   -KVProj of Sec. 6.3: the context goes through the draft layer's own
@@ -56,7 +60,8 @@ import numpy as np
 __all__ = [
     "bf16_to_f64", "fusion_weights", "rms_norm", "rope", "silu", "fuse_rows",
     "context_kv", "block_attention", "draft_layer", "lm_head_logits", "argmax_lowest",
-    "philox4x64_10", "sampling_uniforms", "sample_tokens", "post_fc", "dflash_context", "DraftOracle",
+    "philox4x64_10", "sampling_uniforms", "sample_tokens", "post_fc", "dflash_context", "accept_block",
+    "DraftOracle",
     "VARIANT_NO_SOFTMAX", "VARIANT_SHARED_KV", "VARIANT_POST_FC", "VARIANT_DFLASH",
 ]
 
@@ -301,6 +306,22 @@ def sample_tokens(z: np.ndarray, temperature: float, seed: int, draw: int, slot:
     return argmax_lowest(y), y
 
 
+def accept_block(draft_tokens, target_tokens):
+    """One verification (Sec. 3.2, verification phase).  The block is x_t followed by the
+    candidates draft_tokens[1..B-1]; target_tokens[b] is the target's own next token after
+    block position b.  The longest prefix of candidates equal to the target's predictions is
+    accepted (k of them, 0 <= k <= B-1), and the target's prediction after the last accepted
+    position is the bonus token.  Returns (k, bonus, emitted) with emitted = the k accepted
+    candidates followed by the bonus token (k + 1 tokens)."""
+    d = [int(x) for x in draft_tokens]
+    t = [int(x) for x in target_tokens]
+    B = len(d)
+    k = 0
+    while k + 1 < B and d[k + 1] == t[k]:
+        k += 1
+    return k, t[k], d[1:k + 1] + [t[k]]
+
+
 _LAYER_KINDS = ("attn_norm", "mlp_norm", "wq", "wk_d", "wv_d", "wo", "w_gate", "w_up", "w_down")
 
 
@@ -414,6 +435,16 @@ class DraftOracle:
         self.L += n
         self.last_fused = f
         return f
+
+    def accept(self, draft_tokens, target_tokens, target_hidden_bf16):
+        """Verify a drafted block against the target's outputs and append the target rows of
+        the verified positions: target_hidden [S, B, H] holds the target's hidden rows at the
+        B block positions; rows 0..k (x_t and the k accepted candidates) become context rows
+        L .. L + k.  Returns (k, bonus, emitted) as accept_block; the bonus token is the x_t of
+        the next block."""
+        k, bonus, emitted = accept_block(draft_tokens, target_tokens)
+        self.append(np.asarray(target_hidden_bf16)[:, :k + 1])
+        return k, bonus, emitted
 
     def truncate(self, new_len: int) -> None:
         if not 0 <= new_len <= self.L:

@@ -233,6 +233,23 @@ def _dflash_drops_bias(hidden, w_fc, b_fc):
     return _ORIG["dflash_context"](hidden, w_fc, None)
 
 
+def _accept_bonus_off_by_one(draft_tokens, target_tokens):
+    d, t = list(draft_tokens), list(target_tokens)
+    k = 0
+    while k + 1 < len(d) and d[k + 1] == t[k]:
+        k += 1
+    b = t[min(k + 1, len(t) - 1)]
+    return k, b, d[1:k + 1] + [b]
+
+
+def _accept_compares_same_position(draft_tokens, target_tokens):
+    d, t = list(draft_tokens), list(target_tokens)
+    k = 0
+    while k + 1 < len(d) and d[k + 1] == t[k + 1]:
+        k += 1
+    return k, t[k], d[1:k + 1] + [t[k]]
+
+
 _ORIG = {k: getattr(orc, k) for k in ("fuse_rows", "rope", "context_kv", "fusion_weights", "dflash_context")}
 
 MUTANTS = {
@@ -273,6 +290,8 @@ MUTANTS = {
     "post_fc_drops_bias": ("post_fc", _post_fc_drops_bias),
     "dflash_concat_wrong_order": ("dflash_context", _dflash_concat_wrong_order),
     "dflash_drops_bias": ("dflash_context", _dflash_drops_bias),
+    "accept_bonus_off_by_one": ("accept_block", _accept_bonus_off_by_one),
+    "accept_compares_same_position": ("accept_block", _accept_compares_same_position),
 }
 
 

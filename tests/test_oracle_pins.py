@@ -827,4 +827,61 @@ def test_dflash_context():
     check_dflash_context()
 
 
+# --------------------------------------------------------------------------------------
+# verification (Sec. 3.2, verification phase)
+# --------------------------------------------------------------------------------------
+
+def check_accept_block_exhaustive():
+    """Every (candidates, target predictions) over a 3-token alphabet with B = 4: k is the
+    number of leading positions where candidate j equals the target's prediction after
+    position j - 1; the emitted tokens are exactly the target's own predictions 0..k (the
+    loop emits what the target alone would have emitted greedily); the bonus is the last."""
+    import itertools
+    B = 4
+    for d_tail in itertools.product(range(3), repeat=B - 1):
+        d = (7,) + d_tail
+        for t in itertools.product(range(3), repeat=B):
+            k, bonus, emitted = orc.accept_block(d, t)
+            lead = 0
+            for j in range(1, B):
+                if d[j] != t[j - 1]:
+                    break
+                lead += 1
+            assert k == lead
+            assert emitted == list(t[:k + 1]) and bonus == t[k]
+    assert orc.accept_block([3], [5]) == (0, 5, [5])
+
+
+def check_accept_appends_verified_rows():
+    """accept appends the target rows of positions 0..k only: L grows by k + 1 and the
+    cache equals that of appending those rows directly."""
+    cfg = MICRO
+    w, lg = micro_weights(cfg)
+    B = cfg.block_size
+    hid = synth.hidden_rows(cfg, 0, 4)
+    blk = synth.hidden_rows(cfg, 4, B, seed=3)
+    for k_want in range(B):
+        d = [9] + list(range(1, B))
+        t = list(range(1, B)) + [0]
+        if k_want < B - 1:
+            t[k_want] = 63  # first disagreement after k_want accepted candidates
+        a = build(cfg, w, lg, 0)
+        a.append(hid)
+        k, bonus, _ = a.accept(d, t, blk)
+        assert k == k_want and a.L == 4 + k + 1 and bonus == t[k]
+        b = build(cfg, w, lg, 0)
+        b.append(hid)
+        b.append(blk[:, :k + 1])
+        for i in range(cfg.n_draft_layers):
+            assert np.array_equal(a.k_cache[i], b.k_cache[i])
+
+
+def test_accept_block_exhaustive():
+    check_accept_block_exhaustive()
+
+
+def test_accept_appends_verified_rows():
+    check_accept_appends_verified_rows()
+
+
 ALL_CHECKS = [v for k, v in sorted(globals().items()) if k.startswith("check_")]
