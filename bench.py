@@ -55,6 +55,8 @@ def parse():
                     help="number S of fused target layers (default: the model's)")
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="0 (default): greedy drafts; > 0: Gumbel-max draws from softmax(z / T)")
+    ap.add_argument("--loop", action="store_true",
+                    help="time the draft-then-verify loop (draft_block, a synthetic target, accept) instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-context", type=int, default=256,
                     help="context rows of the oracle's timed sample")
@@ -138,6 +140,9 @@ def main():
 
     if args.config == "batched":
         bench_batched(args)
+        return
+    if args.loop:
+        bench_loop(args)
         return
 
     import numpy as np
@@ -273,6 +278,75 @@ def main():
         result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context, variant)
     print(json.dumps(result), flush=True)
     model.close()
+
+
+def bench_loop(args):
+    """The draft-then-verify loop at batch 1: per iteration draft_block, a synthetic target
+    (its predictions agree with the first k candidates, k drawn ~ U{0..B-1} from a seeded
+    generator and applied on the device; its hidden rows are a fixed seeded block), then
+    dflare_accept, which appends the k + 1 verified rows and waits once for k.  The target
+    model's own forward pass is not part of the loop (no target weights exist here)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_02091_amd import dflare as dfl
+    from paper_2606_02091_amd import synth
+
+    cfg = synth.CONFIGS[args.config]
+    L, B, V = cfg.context, cfg.block_size, cfg.vocab
+    torch.cuda.set_device(0)
+    side = torch.cuda.Stream()
+    torch.cuda.set_stream(side)
+    w = synth.make_weights(cfg)
+    lg = w.pop("fusion_logits")
+    total = args.warmup + args.steps
+    model = dfl.DraftModel(cfg, w, lg, max_context=L + (total + 1) * B, max_new=512)
+    h = model.h
+    for s0 in range(0, L, 512):
+        model.fuse_append(dfl.bf16_tensor(synth.hidden_rows(cfg, s0, min(512, L - s0))))
+    hid = dfl.bf16_tensor(synth.hidden_rows(cfg, L, B, seed=11))
+    ks = torch.from_numpy(np.random.default_rng(5).integers(0, B, size=total).astype(np.int64)).cuda()
+    pos = torch.arange(B, device="cuda")
+    ids = torch.from_numpy(synth.block_ids(cfg)).cuda()
+    draft = torch.empty(B, dtype=torch.int32, device="cuda")
+    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    em = torch.empty(B, dtype=torch.int32, device="cuda")
+    accepted = []
+
+    def it(i):
+        dfl.dflare_draft_block(h, ids, draft)
+        # synthetic target: agrees with candidates 1..k, then predicts another token
+        shifted = torch.roll(draft, -1)
+        tgt = torch.where(pos < ks[i], shifted, (shifted + 1) % V).to(torch.int32)
+        k = dfl.dflare_accept(h, ids, draft, tgt, hid, nxt, em)
+        ids.copy_(nxt)
+        accepted.append(k)
+
+    for i in range(args.warmup):
+        it(i)
+    torch.cuda.synchronize()
+    accepted.clear()
+    t0 = time.perf_counter()
+    for i in range(args.warmup, total):
+        it(i)
+    torch.cuda.synchronize()
+    sec = time.perf_counter() - t0
+    ms = 1000.0 * sec / args.steps
+    tokens = sum(k + 1 for k in accepted)
+    print(f"[bench] loop: {args.steps} iterations, {ms:.4f} ms each, {tokens / sec:.0f} tokens/s",
+          file=sys.stderr, flush=True)
+    print(json.dumps({
+        "metric": "draft-then-verify iterations/sec (draft side; B=16, Qwen3-8B shape, batch 1)",
+        "value": round(1000.0 / ms, 2), "unit": "iterations/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-shaped draft-then-verify loop from context {L}: draft_block, "
+                               f"a synthetic target accepting k ~ U{{0..{B - 1}}} candidates, dflare_accept "
+                               f"(k + 1 rows appended, one host wait per iteration)",
+                   "global_batch": 1, "seq_len": L, "parallelism": "single GPU"},
+        "tokens_per_s": round(tokens / sec, 1), "mean_accepted": round(float(np.mean(accepted)), 3),
+        "timing": "host wall clock (the loop waits for k every iteration)",
+    }), flush=True)
 
 
 MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 / fp16

@@ -165,6 +165,32 @@ int dflare_init(const dflare_config* cfg, const dflare_weights* weights,
 int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_new);
 
 /*
+ * dflare_accept -- the verification step of the draft-then-verify loop (Sec. 3.2,
+ * verification phase) on slot 0, with the target's outputs computed by the caller.
+ *   block_ids      DEVICE int32 [B]: the drafted block (x_t at 0, mask ids at 1..B-1).
+ *   draft_tokens   DEVICE int32 [B]: dflare_draft_block's output for it (candidates
+ *                  at 1..B-1).
+ *   target_tokens  DEVICE int32 [B]: the target's own next token after each block
+ *                  position b (given x_t and candidates 1..b).
+ *   target_hidden  DEVICE bf16 [S, B, H]: the target's hidden rows at the B positions.
+ *   next_ids       DEVICE int32 [B], out: the next block -- the bonus token, then
+ *                  block_ids[1..B-1].
+ *   emitted        DEVICE int32 [B], out: the k accepted candidates, the bonus token,
+ *                  then -1 (k + 1 tokens: what the target alone would emit greedily).
+ *   accepted       HOST int32 out, or NULL: k.
+ * k is the number of leading candidates j = 1.. equal to the target's token after
+ * position j - 1 (0 <= k <= B-1); the bonus token is the target's token after
+ * position k.  The target rows of positions 0..k (x_t and the accepted candidates) are
+ * appended to the context as dflare_fuse_append would (L grows by k + 1), selected and
+ * fused on the device.  The call waits for the stream once, after the selection, so
+ * that the host knows k and the new L.  max_new < B: INVALID_ARG; L + B > max_context:
+ * CONTEXT_FULL, and nothing changes.
+ */
+int dflare_accept(dflare_handle* h, const int32_t* block_ids, const int32_t* draft_tokens,
+                  const int32_t* target_tokens, const void* target_hidden, int32_t* next_ids,
+                  int32_t* emitted, int32_t* accepted);
+
+/*
  * dflare_draft_block -- one drafting forward pass (Sec. 3.2, drafting phase).
  *   block_ids      DEVICE int32 [B]: x_t at index 0, the mask id at 1..B-1 (the
  *                  library treats all ids alike; ids outside [0, V) are clamped).

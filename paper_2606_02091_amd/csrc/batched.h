@@ -100,12 +100,13 @@ void launch_bembed_norm(hipStream_t s, const uint16_t* embed, const int32_t* ids
                         const float* gain, float eps, float* X, u32x4* A, int a_kt);
 // layer fusion (Eq. 3) of N appended rows for every draft layer, normalised, into fp16 A
 // fragments [D][mt_max][H/32][64]
-void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int S, int H, int D, const float* alpha,
+// (hidden: [S, ld, H], rows 0 .. N-1 of each target layer used)
+void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int ld, int S, int H, int D, const float* alpha,
                   const float* gain, float eps, u32x4* A, int mt_max);
 void launch_bfrag_rows(hipStream_t s, const u32x4* A, int n, int H, int D, int mt_max, float* out);
-// target rows [S, N, H] (bf16) -> fp16 A fragments of the rows [h^(1); ...; h^(S)] of each
+// target rows [S, ld, H] (bf16), rows 0 .. N-1 -> fp16 A fragments of the rows [h^(1); ...; h^(S)] of each
 // position, [mt][S*H/32][64] (the input of the DFlash FC layer, Eq. 1)
-void launch_bfrag_cat(hipStream_t s, const uint16_t* hidden, int N, int S, int H, u32x4* A);
+void launch_bfrag_cat(hipStream_t s, const uint16_t* hidden, int N, int ld, int S, int H, u32x4* A);
 void launch_battn(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, int items);
 void launch_bcomb(hipStream_t s, int hd, const BAttnArgs& a, const BRows& rows, u32x4* out16, int a_kt);
 

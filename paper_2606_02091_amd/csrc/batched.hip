@@ -579,7 +579,7 @@ __global__ __launch_bounds__(256) void k_bembed_norm(const uint16_t* embed, cons
 // in j order, then f = RMSNorm(u; g_fuse^(i)) into the fp16 A fragments of layer i.  One
 // work-group per (row, layer); the S target rows of r are read from HBM once and found in
 // L2 by the work-groups of the other layers.
-__global__ __launch_bounds__(256) void k_bfuse(const uint16_t* hidden, int N, int S, int H, const float* alpha,
+__global__ __launch_bounds__(256) void k_bfuse(const uint16_t* hidden, int ld, int S, int H, const float* alpha,
                                                const float* gain, float eps, u32x4* A, int mt_max) {
   constexpr int kMaxChunks = 4;  // H <= 8192
   __shared__ float red[4];
@@ -598,7 +598,7 @@ __global__ __launch_bounds__(256) void k_bfuse(const uint16_t* hidden, int N, in
         u32x4 v[12];
 #pragma unroll
         for (int jj = 0; jj < 12; ++jj)
-          v[jj] = *reinterpret_cast<const u32x4*>(hidden + ((long)min(j0 + jj, S - 1) * N + r) * H + k0);
+          v[jj] = *reinterpret_cast<const u32x4*>(hidden + ((long)min(j0 + jj, S - 1) * ld + r) * H + k0);
 #pragma unroll
         for (int jj = 0; jj < 12; ++jj) {
           if (j0 + jj < S) {
@@ -639,10 +639,10 @@ __global__ void k_bfrag_rows(const u32x4* A, int n, int H, int mt_max, float* ou
 // DFlash FC input (Eq. 1): row r of the call, the S target rows of its position side by
 // side in layer order, as fp16 A fragments [mt][S*H/32][64]; block (row r, target layer j),
 // a thread converts 8 consecutive values (one 16-byte fragment slot).
-__global__ __launch_bounds__(256) void k_bfrag_cat(const uint16_t* hidden, int N, int S, int H, u32x4* A) {
+__global__ __launch_bounds__(256) void k_bfrag_cat(const uint16_t* hidden, int ld, int S, int H, u32x4* A) {
   const int r = blockIdx.x, j = blockIdx.y, Kt = S * H / 32;
   for (int k0 = threadIdx.x * 8; k0 < H; k0 += 256 * 8) {
-    const u32x4 v = *reinterpret_cast<const u32x4*>(hidden + ((long)j * N + r) * H + k0);
+    const u32x4 v = *reinterpret_cast<const u32x4*>(hidden + ((long)j * ld + r) * H + k0);
     float f[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -931,13 +931,13 @@ void launch_bembed_norm(hipStream_t s, const uint16_t* embed, const int32_t* ids
   hipLaunchKernelGGL(k_bembed_norm, dim3(M), dim3(256), 0, s, embed, ids, H, V, gain, eps, X, A, a_kt);
 }
 
-void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int S, int H, int D, const float* alpha,
+void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int ld, int S, int H, int D, const float* alpha,
                   const float* gain, float eps, u32x4* A, int mt_max) {
-  hipLaunchKernelGGL(k_bfuse, dim3(N, D), dim3(256), 0, s, hidden, N, S, H, alpha, gain, eps, A, mt_max);
+  hipLaunchKernelGGL(k_bfuse, dim3(N, D), dim3(256), 0, s, hidden, ld, S, H, alpha, gain, eps, A, mt_max);
 }
 
-void launch_bfrag_cat(hipStream_t s, const uint16_t* hidden, int N, int S, int H, u32x4* A) {
-  hipLaunchKernelGGL(k_bfrag_cat, dim3(N, S), dim3(256), 0, s, hidden, N, S, H, A);
+void launch_bfrag_cat(hipStream_t s, const uint16_t* hidden, int N, int ld, int S, int H, u32x4* A) {
+  hipLaunchKernelGGL(k_bfrag_cat, dim3(N, S), dim3(256), 0, s, hidden, ld, S, H, A);
 }
 
 void launch_bfrag_rows(hipStream_t s, const u32x4* A, int n, int H, int D, int mt_max, float* out) {

@@ -168,8 +168,11 @@ void launch_bf16_to_f32(hipStream_t s, float* dst, const uint16_t* src, long n);
 void launch_compose(hipStream_t s, uint16_t* out, const uint16_t* A, const uint16_t* B, int R, int O, int K);
 // init: y[R] (fp32) = A[R, O] b[O] in double precision (b bf16; NULL gives zeros)
 void launch_matvec(hipStream_t s, float* y, const uint16_t* A, const uint16_t* b, int R, int O);
-void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
+void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int ld, int S, int H, int D, const float* alpha,
                  const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max);
+// verification (Sec. 3.2): accepted count k (to host-visible memory), next block, emitted tokens
+void launch_accept(hipStream_t s, const int32_t* block_ids, const int32_t* draft, const int32_t* target, int B,
+                   int32_t* next_ids, int32_t* emitted, int32_t* k_out);
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n,
                        int H, int D, int n_max, int mt_max, float eps, float* out);
 bool kvt_shape_supported(int nt_per_block, int waves);

@@ -78,7 +78,7 @@ __global__ void k_bf16_to_f32(float* dst, const uint16_t* src, long n) {
 // squares of u^(i); the 1/rms of Eq. 3 is applied in the K/V projection.  The S target rows
 // are read from HBM once; the blocks of the other draft layers find them in L2.
 // ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int n, int S, int H,
+__global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int ld, int S, int H,
                                              const float* __restrict__ alpha, const float* __restrict__ gain,
                                              float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
   const int lane = threadIdx.x;
@@ -92,7 +92,7 @@ __global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden
 #pragma unroll
     for (int qq = 0; qq < 12; ++qq) {
       v[qq] = u32x4{0u, 0u, 0u, 0u};
-      if (ok && j0 + qq < S) v[qq] = *reinterpret_cast<const u32x4*>(hidden + ((long)(j0 + qq) * n + r) * H + k0);
+      if (ok && j0 + qq < S) v[qq] = *reinterpret_cast<const u32x4*>(hidden + ((long)(j0 + qq) * ld + r) * H + k0);
     }
 #pragma unroll
     for (int qq = 0; qq < 12; ++qq) {
@@ -1497,10 +1497,36 @@ void launch_bf16_to_f32(hipStream_t s, float* dst, const uint16_t* src, long n) 
   hipLaunchKernelGGL(k_bf16_to_f32, dim3(blocks), dim3(256), 0, s, dst, src, n);
 }
 
-void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int S, int H, int D, const float* alpha,
+void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int ld, int S, int H, int D, const float* alpha,
                  const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
-  hipLaunchKernelGGL(k_fuse, dim3((H + 511) / 512, n, D), dim3(64), 0, s, hidden, n, S, H, alpha, gain, ustats,
+  hipLaunchKernelGGL(k_fuse, dim3((H + 511) / 512, n, D), dim3(64), 0, s, hidden, ld, S, H, alpha, gain, ustats,
                      ua_hi, ua_lo, n_max, mt_max);
+}
+
+// Verification (Sec. 3.2): one wave.  k = the number of leading candidates j = 1.. that
+// equal the target's prediction after position j - 1; the bonus is the target's
+// prediction after position k.  Writes the next block (bonus, then the mask ids), the
+// emitted tokens (k candidates, bonus, then -1) and k to host-visible memory.
+__global__ __launch_bounds__(64) void k_accept(const int32_t* block_ids, const int32_t* draft, const int32_t* target,
+                                               int B, int32_t* next_ids, int32_t* emitted, int32_t* k_out) {
+  const int b = threadIdx.x;
+  const bool in = b < B;
+  const int d = in ? draft[b] : 0;
+  const int tp = (b >= 1 && b < B) ? target[b - 1] : 0;
+  const unsigned long long miss = __ballot(b >= 1 && b < B && d != tp);
+  const int k = miss ? __ffsll((long long)miss) - 2 : B - 1;
+  const int bonus = target[k];
+  const int dn = __shfl_down(d, 1);  // candidate b + 1
+  if (in) {
+    next_ids[b] = b == 0 ? bonus : block_ids[b];
+    emitted[b] = b < k ? dn : (b == k ? bonus : -1);
+  }
+  if (b == 0) __hip_atomic_store(k_out, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+void launch_accept(hipStream_t s, const int32_t* block_ids, const int32_t* draft, const int32_t* target, int B,
+                   int32_t* next_ids, int32_t* emitted, int32_t* k_out) {
+  hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, block_ids, draft, target, B, next_ids, emitted, k_out);
 }
 
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n, int H,

@@ -812,7 +812,9 @@ BGemmArgs bgemm_base(const dflare_handle* h) {
   return g;
 }
 
-int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int32_t* n_new, const void* hidden) {
+// hidden: [S, ld, H]; the call's rows are rows 0 .. sum(n_new) - 1 of each target layer
+int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int32_t* n_new, const void* hidden,
+                     int ld) {
   const dflare_config& c = h->cfg;
   const int H = c.hidden, D = c.n_draft_layers, S = c.n_target_layers, Kt_H = H / 32;
   hipStream_t s = h->stream;
@@ -829,7 +831,7 @@ int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int3
   if (dflash) {
     // Eq. 1: C = [h^(1); ...; h^(S)] W_fc^T + b_fc for all N rows, as fp16 fragments
     prof_mark(h, DFLARE_K_B_FUSE, true);
-    launch_bfrag_cat(s, (const uint16_t*)hidden, N, S, H, h->bCat);
+    launch_bfrag_cat(s, (const uint16_t*)hidden, N, ld, S, H, h->bCat);
     g.A = h->bCat;
     g.a_layer = 0;
     g.W = h->h_fc;
@@ -848,7 +850,7 @@ int run_fuse_batched(dflare_handle* h, int n_seq, const int32_t* seq, const int3
     g.a_layer = 0;
   } else {
     prof_mark(h, DFLARE_K_B_FUSE, true);
-    launch_bfuse(s, (const uint16_t*)hidden, N, S, H, D, h->alpha, h->g_fuse, c.rms_eps, h->bU, h->mt_max);
+    launch_bfuse(s, (const uint16_t*)hidden, N, ld, S, H, D, h->alpha, h->g_fuse, c.rms_eps, h->bU, h->mt_max);
     prof_mark(h, DFLARE_K_B_FUSE, false);
     g.A = h->bU;
     g.a_layer = (long)h->mt_max * Kt_H * 64;
@@ -1027,23 +1029,17 @@ int dflare_init(const dflare_config* cfg, const dflare_weights* w, const float* 
   return DFLARE_OK;
 }
 
-int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_new) {
-  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
-  if (!target_hidden) return fail(h, DFLARE_ERR_INVALID_ARG, "target_hidden is NULL");
-  if (n_new < 1 || n_new > h->cfg.max_new)
-    return fail(h, DFLARE_ERR_INVALID_ARG, "n_new must be in [1, max_new]");
-  if ((long)h->Ls[0] + n_new > h->cfg.max_context)
-    return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
+// Append rows 0 .. n_new-1 of target_hidden [S, ld, H] to slot 0 (arguments validated)
+int append_rows(dflare_handle* h, const void* target_hidden, int32_t n_new, int ld) {
   const dflare_config& c = h->cfg;
   if (c.variant & DFLARE_VARIANT_DFLASH) {  // the FC fusion runs on the batched GEMM, slot 0
     const int32_t seq0 = 0;
-    const int rc = run_fuse_batched(h, 1, &seq0, &n_new, target_hidden);
-    return rc;
+    return run_fuse_batched(h, 1, &seq0, &n_new, target_hidden, ld);
   }
   const int H = c.hidden, D = c.n_draft_layers, S = c.n_target_layers;
   hipStream_t s = h->stream;
   prof_mark(h, DFLARE_K_FUSE, true);
-  launch_fuse(s, (const uint16_t*)target_hidden, n_new, S, H, D, h->alpha, h->g_fuse, h->Ustats, h->ua_hi,
+  launch_fuse(s, (const uint16_t*)target_hidden, n_new, ld, S, H, D, h->alpha, h->g_fuse, h->Ustats, h->ua_hi,
               h->ua_lo, c.max_new, h->mt_max);
   prof_mark(h, DFLARE_K_FUSE, false);
   KvtArgs a{};
@@ -1084,6 +1080,39 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
   return DFLARE_OK;
 }
 
+int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_new) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!target_hidden) return fail(h, DFLARE_ERR_INVALID_ARG, "target_hidden is NULL");
+  if (n_new < 1 || n_new > h->cfg.max_new)
+    return fail(h, DFLARE_ERR_INVALID_ARG, "n_new must be in [1, max_new]");
+  if ((long)h->Ls[0] + n_new > h->cfg.max_context)
+    return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
+  return append_rows(h, target_hidden, n_new, n_new);
+}
+
+int dflare_accept(dflare_handle* h, const int32_t* block_ids, const int32_t* draft_tokens, const int32_t* target_tokens,
+                  const void* target_hidden, int32_t* next_ids, int32_t* emitted, int32_t* accepted) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!block_ids || !draft_tokens || !target_tokens || !target_hidden || !next_ids || !emitted)
+    return fail(h, DFLARE_ERR_INVALID_ARG, "a device pointer is NULL");
+  const dflare_config& c = h->cfg;
+  const int B = c.block_size;
+  if (c.max_new < B) return fail(h, DFLARE_ERR_INVALID_ARG, "dflare_accept needs max_new >= block_size");
+  if ((long)h->Ls[0] + B > c.max_context)
+    return fail(h, DFLARE_ERR_CONTEXT_FULL, "a verified block could exceed max_context");
+  int32_t* k_host = h->err_host + 8;  // host-mapped word next to the barrier flag
+  int32_t* k_dev = h->err_dev + 8;
+  *(volatile int32_t*)k_host = -1;
+  launch_accept(h->stream, block_ids, draft_tokens, target_tokens, B, next_ids, emitted, k_dev);
+  TRY(check_launch(h, "accept"));
+  HIP_OR_FAIL(h, hipStreamSynchronize(h->stream));
+  const int k = *(volatile int32_t*)k_host;
+  if (k < 0 || k >= B) return fail(h, DFLARE_ERR_HIP, "verification result not received");
+  TRY(append_rows(h, target_hidden, k + 1, B));
+  if (accepted) *accepted = k;
+  return DFLARE_OK;
+}
+
 int dflare_draft_block(dflare_handle* h, const int32_t* block_ids, int32_t* draft_tokens) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
   if (!block_ids || !draft_tokens) return fail(h, DFLARE_ERR_INVALID_ARG, "block_ids / draft_tokens is NULL");
@@ -1117,7 +1146,7 @@ int dflare_fuse_append_batched(dflare_handle* h, int32_t n_seq, const int32_t* s
       return fail(h, DFLARE_ERR_CONTEXT_FULL, "append would exceed max_context");
   TRY(ensure_f16_weights(h));
   prof_mark(h, DFLARE_K_B_APPEND, true);
-  const int rc = run_fuse_batched(h, n_seq, seq, n_new, target_hidden);
+  const int rc = run_fuse_batched(h, n_seq, seq, n_new, target_hidden, (int)total);
   prof_mark(h, DFLARE_K_B_APPEND, false);
   return rc;
 }

@@ -26,7 +26,7 @@ EXPORTED = (
     "dflare_status_str", "dflare_last_error", "dflare_debug_capture", "dflare_debug_read",
     "dflare_kernel_stats", "dflare_profile_begin", "dflare_profile_end", "dflare_set_option",
     "dflare_fuse_append_batched", "dflare_draft_block_batched", "dflare_truncate_seq",
-    "dflare_context_len_seq", "dflare_debug_read_seq", "dflare_set_sampling",
+    "dflare_context_len_seq", "dflare_debug_read_seq", "dflare_set_sampling", "dflare_accept",
 )
 K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T, K_DRAFT = range(1, 10)
 (K_B_QKV, K_B_ATTN, K_B_O, K_B_GATE_UP, K_B_DOWN, K_B_LM_HEAD, K_B_KV_T, K_B_EPI, K_B_FUSE, K_B_DRAFT,
@@ -95,6 +95,7 @@ def lib() -> ctypes.CDLL:
         "dflare_draft_block_batched": ([vp, i32, ctypes.POINTER(i32), vp, vp], ctypes.c_int),
         "dflare_truncate_seq": ([vp, i32, i32], ctypes.c_int),
         "dflare_set_sampling": ([vp, ctypes.c_float, ctypes.c_uint64], ctypes.c_int),
+        "dflare_accept": ([vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
         "dflare_context_len_seq": ([vp, i32, ctypes.POINTER(i32)], ctypes.c_int),
         "dflare_debug_read_seq": ([vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float),
                                    i64], ctypes.c_int),
@@ -185,6 +186,15 @@ def dflare_draft_block_batched(h: int, seq, block_ids: torch.Tensor, draft_token
     """block_ids / draft_tokens: device int32 [n_seq, B]; row i belongs to slot seq[i]."""
     sq = _i32_array(seq)
     _check(lib().dflare_draft_block_batched(h, sq.size, _i32p(sq), _ptr(block_ids), _ptr(draft_tokens)), h)
+
+
+def dflare_accept(h: int, block_ids: torch.Tensor, draft_tokens: torch.Tensor, target_tokens: torch.Tensor,
+                  target_hidden: torch.Tensor, next_ids: torch.Tensor, emitted: torch.Tensor) -> int:
+    """Verify a drafted block against the target's outputs; returns k (see include/dflare.h)."""
+    k = ctypes.c_int32(-1)
+    _check(lib().dflare_accept(h, _ptr(block_ids), _ptr(draft_tokens), _ptr(target_tokens), _ptr(target_hidden),
+                               _ptr(next_ids), _ptr(emitted), ctypes.byref(k)), h)
+    return k.value
 
 
 def dflare_set_sampling(h: int, temperature: float, seed: int = 0) -> None:

@@ -125,6 +125,7 @@ def test_calls_on_invalid_handles(L):
     assert L.dflare_fuse_append_batched(0x1234, 1, seq, seq, 0x1000) == dfl.ERR_INVALID_ARG
     assert L.dflare_draft_block_batched(None, 1, seq, 0x1000, 0x1000) == dfl.ERR_INVALID_ARG
     assert L.dflare_truncate_seq(0x1234, 0, 0) == dfl.ERR_INVALID_ARG
+    assert L.dflare_accept(None, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, None) == dfl.ERR_INVALID_ARG
     assert L.dflare_context_len_seq(None, 0, ctypes.byref(out)) == dfl.ERR_INVALID_ARG
     buf = (ctypes.c_float * 4)()
     assert L.dflare_debug_read_seq(None, dfl.DBG_KCACHE, 0, 0, buf, 4) == dfl.ERR_INVALID_ARG

@@ -1,0 +1,97 @@
+"""GPU parity of the verification step of the draft-then-verify loop (Sec. 3.2, verification
+phase): dflare_accept against the oracle's accept on the same draft tokens, target
+predictions and target rows.  A synthetic target agrees with the draft up to a chosen
+position, so every acceptance length 0 .. B-1 occurs; k, the bonus token, the next block and
+the emitted tokens must match exactly, the caches to the bar of tests/parity.py, and the
+loop (draft -> verify -> draft on the next block) must keep matching the oracle."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import dflare_oracle as orc
+from paper_2606_02091_amd import dflare as dfl
+from paper_2606_02091_amd import synth
+import parity as P
+import test_gpu_parity as TP
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU container
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+
+def synthetic_target(draft, k_want, vocab, rng):
+    """target predictions that agree with the first k_want candidates, then differ"""
+    B = len(draft)
+    t = rng.integers(0, vocab, size=B).astype(np.int32)
+    t[:k_want] = draft[1:k_want + 1]
+    if k_want < B - 1 and t[k_want] == draft[k_want + 1]:
+        t[k_want] = (draft[k_want + 1] + 1) % vocab
+    return t
+
+
+@pytest.mark.parametrize("case,variant", [("hd128", 0), ("ragged", 0), ("gqa8_hd64", dfl.VARIANT_DFLASH)])
+def test_accept_loop_matches_oracle(case, variant):
+    cfg, L, mode = TP.CASES[case]
+    B, V, S, H = cfg.block_size, cfg.vocab, cfg.n_target_layers, cfg.hidden
+    print(f"[accept] {case} variant {variant}", flush=True)
+    kinds = synth.BASE_KINDS + (("fc", "fc_bias") if variant else ())
+    w = synth.make_weights(cfg, kinds=kinds)
+    lg = w.pop("fusion_logits")
+    dl = None if variant else lg
+    model = dfl.DraftModel(cfg, w, dl, max_context=L + 16 * B, max_new=16, variant=variant)
+    dfl.dflare_debug_capture(model.h, True)
+    o = orc.DraftOracle(cfg, w, dl, max_context=L + 16 * B, variant=variant)
+    s = 0
+    for n in TP.append_plan(cfg, L, mode):
+        rows = synth.hidden_rows(cfg, s, n)
+        model.fuse_append(dfl.bf16_tensor(rows))
+        o.append(rows)
+        s += n
+    rng = np.random.default_rng(7)
+    ids = synth.block_ids(cfg, step=0)
+    next_ids = torch.empty(B, dtype=torch.int32, device="cuda")
+    emitted = torch.empty(B, dtype=torch.int32, device="cuda")
+    for it, k_want in enumerate([B - 1, 0] + [int(x) for x in rng.integers(0, B, size=4)]):
+        draft = model.draft_block(TP.ids_tensor(ids)).cpu().numpy()
+        ref = o.draft_block(ids)
+        P.check_tokens(draft, ref["logits"])
+        t = synthetic_target(draft, k_want, V, rng)
+        hid = synth.hidden_rows(cfg, 1000 + it * B, B, seed=11)
+        k = dfl.dflare_accept(model.h, TP.ids_tensor(ids), TP.ids_tensor(draft), TP.ids_tensor(t),
+                              dfl.bf16_tensor(hid), next_ids, emitted)
+        k_ref, bonus, em_ref = o.accept(draft, t, hid)
+        assert k == k_ref == k_want, (it, k, k_ref, k_want)
+        em = emitted.cpu().numpy()
+        assert list(em[:k + 1]) == em_ref and (em[k + 1:] == -1).all()
+        nid = next_ids.cpu().numpy()
+        assert nid[0] == bonus and (nid[1:] == ids[1:]).all()
+        assert model.context_len == o.L
+        for i in range(cfg.n_draft_layers):
+            for what, r in ((dfl.DBG_KCACHE, o.k_cache[i]), (dfl.DBG_VCACHE, o.v_cache[i])):
+                got = dfl.dflare_debug_read(model.h, what, i, (o.L, cfg.n_kv_heads, cfg.head_dim))
+                assert P.relinf(got, r) <= P.REL_TOL, (it, i, what)
+        ids = nid
+    model.close()
+
+
+def test_accept_limits():
+    cfg, L, mode = TP.CASES["tiny"]
+    B = cfg.block_size
+    w, lg = P.weights_for(cfg)
+    small = dfl.DraftModel(cfg, w, lg, max_context=64, max_new=B - 1)
+    z = torch.zeros(B, dtype=torch.int32, device="cuda")
+    hid = dfl.bf16_tensor(synth.hidden_rows(cfg, 0, B))
+    with pytest.raises(dfl.DFlareError) as e:
+        dfl.dflare_accept(small.h, z, z, z, hid, z.clone(), z.clone())
+    assert e.value.status == dfl.ERR_INVALID_ARG
+    small.close()
+    model = dfl.DraftModel(cfg, w, lg, max_context=B + 3, max_new=16)
+    model.fuse_append(dfl.bf16_tensor(synth.hidden_rows(cfg, 0, 4)))
+    with pytest.raises(dfl.DFlareError) as e:  # L + B > max_context: nothing changes
+        dfl.dflare_accept(model.h, z, z, z, hid, z.clone(), z.clone())
+    assert e.value.status == dfl.ERR_CONTEXT_FULL and model.context_len == 4
+    model.truncate(3)
+    k = dfl.dflare_accept(model.h, z, z, z, hid, z.clone(), z.clone())  # all candidates 0 == target 0
+    assert k == B - 1 and model.context_len == 3 + B
+    model.close()
