@@ -57,6 +57,8 @@ def parse():
                     help="0 (default): greedy drafts; > 0: Gumbel-max draws from softmax(z / T)")
     ap.add_argument("--loop", action="store_true",
                     help="time the draft-then-verify loop (draft_block, a synthetic target, accept) instead")
+    ap.add_argument("--training", action="store_true",
+                    help="time the training-side kernels (anchor attention fwd/bwd, weighted CE) instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-context", type=int, default=256,
                     help="context rows of the oracle's timed sample")
@@ -143,6 +145,9 @@ def main():
         return
     if args.loop:
         bench_loop(args)
+        return
+    if args.training:
+        bench_training(args)
         return
 
     import numpy as np
@@ -346,6 +351,84 @@ def bench_loop(args):
                    "global_batch": 1, "seq_len": L, "parallelism": "single GPU"},
         "tokens_per_s": round(tokens / sec, 1), "mean_accepted": round(float(np.mean(accepted)), 3),
         "timing": "host wall clock (the loop waits for k every iteration)",
+    }), flush=True)
+
+
+def bench_training(args):
+    """Training-side kernels at the paper's training shape (a 3,072-token sequence, 512
+    anchors of 16-position blocks, Qwen3-8B heads: 32 query / 8 KV heads of 128): one draft
+    layer's anchor attention forward and backward, and the position-weighted cross-entropy
+    over the 151,936-token vocabulary (logits of the 8,192 block positions).  Inputs are seeded
+    synthetic tensors; anchors ~ U{0..T-B}."""
+    import numpy as np
+    import torch
+
+    from paper_2606_02091_amd import dflare as dfl
+
+    T, n, B, nq, nkv, hd, V = 3072, 512, 16, 32, 8, 128, 151936
+    torch.cuda.set_device(0)
+    side = torch.cuda.Stream()
+    torch.cuda.set_stream(side)
+    g = torch.Generator(device="cuda").manual_seed(0)
+
+    def bf(*shape):
+        return torch.randn(*shape, device="cuda", generator=g).to(torch.bfloat16).view(torch.int16)
+
+    q, kc, vc = bf(n * B, nq, hd), bf(T, nkv, hd), bf(T, nkv, hd)
+    kb, vb = bf(n * B, nkv, hd), bf(n * B, nkv, hd)
+    anchors_np = np.random.default_rng(1).integers(0, T - B + 1, size=n).astype(np.int32)
+    anchors = torch.from_numpy(anchors_np).cuda()
+    dout = torch.randn(n * B, nq, hd, device="cuda", generator=g)
+    logits = 3.0 * torch.randn(n * B, V, device="cuda", generator=g)
+    labels = torch.randint(0, V, (n * B,), device="cuda", generator=g, dtype=torch.int32)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, reps):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    out, lse = dfl.anchor_attention_fwd(q, kc, vc, kb, vb, anchors, B)
+    reps = max(args.steps // 20, 3)
+    fwd_ms = timed(lambda: dfl.anchor_attention_fwd(q, kc, vc, kb, vb, anchors, B), reps)
+    bwd_ms = timed(lambda: dfl.anchor_attention_bwd(q, kc, vc, kb, vb, anchors, B, out, lse, dout), reps)
+    ce_ms = timed(lambda: dfl.weighted_ce(logits, labels, B, 4.5), reps)
+    # algorithmic work: per (block, query head) the two products over its a_i + B keys; the
+    # backward counts the usual five (scores recomputed, dP, dV, dQ, dK)
+    keys = (anchors_np.astype(np.float64) + B).sum()
+    fwd_flop = 4.0 * B * hd * nq * keys
+    bwd_flop = 2.5 * fwd_flop
+    ce_bytes = 2.0 * n * B * V * 4  # logits read once, their gradient written once
+    total_ms = fwd_ms + bwd_ms + ce_ms
+    print(json.dumps({
+        "metric": "training-side kernels (anchor attention fwd+bwd, weighted CE), one draft layer",
+        "value": round((fwd_flop + bwd_flop) / ((fwd_ms + bwd_ms) * 1e-3) / 1e12, 2), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": reps, "warmup": 2, "ms_per_step": round(total_ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"anchor attention of one draft layer: T={T}, {n} anchors ~ U{{0..{T - B}}}, "
+                               f"B={B}, {nq}q/{nkv}kv x {hd}; weighted CE over V={V} for {n * B} rows",
+                   "global_batch": n, "seq_len": T, "parallelism": "single GPU"},
+        "kernels": {
+            "attn_fwd": {"ms": round(fwd_ms, 4), "TFLOPs": round(fwd_flop / (fwd_ms * 1e-3) / 1e12, 1),
+                         "flop": fwd_flop},
+            "attn_bwd": {"ms": round(bwd_ms, 4), "TFLOPs": round(bwd_flop / (bwd_ms * 1e-3) / 1e12, 1),
+                         "flop": bwd_flop},
+            "weighted_ce": {"ms": round(ce_ms, 4), "GBs": round(ce_bytes / (ce_ms * 1e-3) / 1e9, 1),
+                            "bytes": ce_bytes},
+        },
+        "roofline": {"bound": "mfma", "achieved": round((fwd_flop + bwd_flop) / ((fwd_ms + bwd_ms) * 1e-3) / 1e12, 1),
+                     "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round((fwd_flop + bwd_flop) / ((fwd_ms + bwd_ms) * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS, 4),
+                     "traffic": None, "kernel": "anchor attention fwd+bwd"},
+        "ce_roofline": {"bound": "hbm", "achieved": round(ce_bytes / (ce_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(ce_bytes / (ce_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
     }), flush=True)
 
 

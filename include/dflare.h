@@ -376,6 +376,61 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches);
 enum { DFLARE_OPT_PERSISTENT = 1, DFLARE_OPT_TRACE = 2 };
 int dflare_set_option(dflare_handle* h, int option, int value);
 
+/*
+ * ---- Training-side kernels (no handle) ----
+ * Anchor attention of one draft layer (Sec. 3.3): the n_blocks sampled blocks of one
+ * training sequence are processed together; the rows of block i, anchored at sequence
+ * position anchors[i] (0 <= anchors[i] <= T), attend to the target context features of the
+ * positions before the anchor (context keys 0 .. anchors[i]-1) and bidirectionally to the B
+ * positions of their own block; never to another block.  Scale 1/sqrt(hd); query head h
+ * reads KV head h / (n_q / n_kv).  Rotary embedding, if any, is already applied.
+ *   q              DEVICE bf16 [n_blocks*B, n_q, hd]   (row i*B + b: block i, position b)
+ *   k_ctx, v_ctx   DEVICE bf16 [T, n_kv, hd]           (may be NULL when T = 0)
+ *   k_blk, v_blk   DEVICE bf16 [n_blocks*B, n_kv, hd]
+ *   anchors        DEVICE int32 [n_blocks]
+ *   out            DEVICE fp32 [n_blocks*B, n_q, hd];  lse  DEVICE fp32 [n_blocks*B, n_q]
+ *                  (natural log-sum-exp of each row's scaled scores, for the backward pass)
+ *   workspace      DEVICE scratch of at least dflare_anchor_attention_workspace(...) bytes
+ *                  (transposed copies and partial sums; contents need not be kept)
+ * Supported: 1 <= B <= 16, hd 64 or 128, (n_q / n_kv) * B <= 128; else UNSUPPORTED.  The
+ * products run on bf16 matrix cores (probabilities and gradients rounded to bf16 as operands,
+ * fp32 accumulation).  Asynchronous on `stream` (hipStream_t, NULL = default).  Gradients are
+ * deterministic: context-key gradients are summed over chunks of 64 blocks in a fixed order.
+ */
+size_t dflare_anchor_attention_workspace(int32_t n_blocks, int32_t B, int32_t T, int32_t n_q, int32_t n_kv,
+                                         int32_t hd);
+int dflare_anchor_attention_fwd(const void* q, const void* k_ctx, const void* v_ctx, const void* k_blk,
+                                const void* v_blk, const int32_t* anchors, int32_t n_blocks, int32_t B, int32_t T,
+                                int32_t n_q, int32_t n_kv, int32_t hd, float* out, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream);
+/*
+ * Backward of the above for the output gradient dout (DEVICE fp32 [n_blocks*B, n_q, hd]),
+ * given the forward's out and lse: dq [n_blocks*B, n_q, hd], dk_ctx / dv_ctx [T, n_kv, hd],
+ * dk_blk / dv_blk [n_blocks*B, n_kv, hd], all DEVICE fp32, overwritten.
+ */
+int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_ctx, const void* k_blk,
+                                const void* v_blk, const int32_t* anchors, int32_t n_blocks, int32_t B, int32_t T,
+                                int32_t n_q, int32_t n_kv, int32_t hd, const float* out, const float* lse,
+                                const float* dout, float* dq, float* dk_ctx, float* dv_ctx, float* dk_blk,
+                                float* dv_blk, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Progressive position-weighted cross-entropy (Sec. 4.3, Eq. 5) over rows = n_blocks * B
+ * block positions: row r is position b = r % B of its block; the anchor position (b = 0)
+ * and rows with label < 0 (or >= V) carry no loss; position b >= 1 has weight
+ * w = exp(-(b - 1) / gamma), gamma = gamma(s) of the schedule (the caller's).  The loss is
+ * sum w CE / sum w.
+ *   logits   DEVICE fp32 [rows, V];  labels  DEVICE int32 [rows]
+ *   loss     DEVICE fp32 [1] out;  row_ce  DEVICE fp32 [rows] out (CE per row, 0 where no loss)
+ *   dlogits  DEVICE fp32 [rows, V] out: d loss / d logits
+ *   workspace DEVICE scratch of at least dflare_weighted_ce_workspace(rows) bytes
+ * rows not a multiple of B, gamma <= 0 or not finite: INVALID_ARG.  Deterministic.
+ */
+size_t dflare_weighted_ce_workspace(int32_t rows);
+int dflare_weighted_ce(const float* logits, const int32_t* labels, int32_t rows, int32_t V, int32_t B, float gamma,
+                       float* loss, float* row_ce, float* dlogits, void* workspace, size_t workspace_bytes,
+                       void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libdflare.so")
-SOURCES = ["kernels.hip", "batched.hip", "runtime.hip"]
+SOURCES = ["kernels.hip", "batched.hip", "runtime.hip", "training.hip"]
 ARCH = os.environ.get("DFLARE_OFFLOAD_ARCH", "gfx950")
 
 

@@ -1,0 +1,688 @@
+// Training-side kernels of the block diffusion draft model and their C-ABI entry points:
+//   * anchor attention (Sec. 3.3): the sampled blocks of a sequence are processed together;
+//     the rows of block i (anchored at position a_i) attend to the context features of the
+//     positions before a_i and to the B positions of their own block, never to another
+//     block.  Forward (outputs, log-sum-exp) and backward (dQ, context dK/dV, block dK/dV).
+//   * progressive position-weighted cross-entropy (Sec. 4.3, Eq. 5): weights
+//     w_k = exp(-(k - 1) / gamma) on the k-th masked position of each block, the loss is
+//     their weighted mean; forward and the gradient of the logits.
+//
+// Matrix products run on v_mfma_f32_16x16x32_bf16 with every operand read straight from
+// memory in its operand layout: scores are formed transposed (S^T = K Q^T) where the
+// probabilities feed a product over keys (P V, dS K), and untransposed (S = Q K^T) where they
+// feed a product over query rows (P^T dO, dS^T Q).  The operands that need the other
+// orientation (V^T, K^T, Q^T, dO^T) are written once per call into the workspace by
+// transposing kernels; two 16-key (or 16-row) result tiles of a lane hold keys 4q..4q+3 and
+// 16+4q..16+4q+3, so the matching operand is read as two 8-byte pieces.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include <algorithm>
+#include <type_traits>
+
+#include "device_common.h"
+#include "dflare.h"
+
+namespace dflare {
+
+namespace {
+
+constexpr int kTrT = 256;  // threads per work-group (4 waves)
+constexpr int kChunkBlocks = 64;  // blocks per partial of the context-key gradients
+
+struct AttnShapeT {
+  int n_blocks, B, T, n_q, n_kv, hd;
+  int G, R, Rp, Tp, Mp;  // heads per group, rows per (block, group), padded rows / keys
+};
+
+struct AttnT {
+  AttnShapeT s;
+  const uint16_t *q, *kc, *vc, *kb, *vb;  // bf16 inputs
+  const int32_t* anchors;
+  // workspace (bf16 transposed copies, fp32 partials)
+  uint16_t *kct, *vct, *kbt, *vbt;  // [n_kv][hd][Tp] / [n_kv][hd][Mp]
+  uint16_t *qt, *dot, *dob;         // [n_kv][n_blocks][hd][Rp] x2, [M][n_q][hd]
+  float* dsum;                      // [M][n_q] rowsum(dO * O)
+  float* part;                      // [nch][T][n_kv][hd] x2 (dK, dV)
+  int nch;
+  // outputs
+  float *out, *lse;
+  const float* dout;
+  float *dq, *dkc, *dvc, *dkb, *dvb;
+  float scale;
+};
+
+__device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+// keys (or rows) 4q..4q+3 and 16+4q..16+4q+3 of a 32-wide range starting at p
+__device__ __forceinline__ u32x4 ld_pair(const uint16_t* p) {
+  const u32x2 a = *reinterpret_cast<const u32x2*>(p);
+  const u32x2 b = *reinterpret_cast<const u32x2*>(p + 16);
+  return u32x4{a[0], a[1], b[0], b[1]};
+}
+// two result tiles of a lane (4 + 4 values) as one bf16 operand (k order 0..3, then 16..19)
+__device__ __forceinline__ u32x4 pack_bf8(f32x4 x, f32x4 y) {
+  return u32x4{f2bf(x[0]) | (f2bf(x[1]) << 16), f2bf(x[2]) | (f2bf(x[3]) << 16), f2bf(y[0]) | (f2bf(y[1]) << 16),
+               f2bf(y[2]) | (f2bf(y[3]) << 16)};
+}
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+// ---- layout helpers ------------------------------------------------------------------
+// src [rows][n_kv][hd] (bf16) -> dst [n_kv][hd][ld], zeros for rows >= nrows; block
+// (32-row tile, 32-column tile of n_kv*hd) through a padded LDS tile.
+__global__ __launch_bounds__(256) void k_tr_kv_t(const uint16_t* src, int nrows, int cols, int ld, uint16_t* dst) {
+  __shared__ uint16_t tile[32][34];
+  const int r0 = blockIdx.x * 32, c0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  for (int y = ty; y < 32; y += 8) {
+    const int r = r0 + y, c = c0 + tx;
+    tile[y][tx] = (r < nrows && c < cols) ? src[(long)r * cols + c] : (uint16_t)0;
+  }
+  __syncthreads();
+  for (int y = ty; y < 32; y += 8) {
+    const int c = c0 + y, r = r0 + tx;
+    if (c < cols && r < ld) dst[(long)c * ld + r] = tile[tx][y];
+  }
+}
+
+// x [M][n_q][hd] (bf16 bits, or fp32 with F32) -> dst[g][i][d][Rp]: row r of (block i, group g)
+// is block position r % B of query head g*G + r / B; zeros for r >= R
+template <bool F32>
+__global__ __launch_bounds__(256) void k_tr_group_t(const void* x, AttnShapeT s, uint16_t* dst) {
+  const int i = blockIdx.x, g = blockIdx.y;
+  uint16_t* o = dst + ((long)g * s.n_blocks + i) * s.hd * s.Rp;
+  for (int e = threadIdx.x; e < s.hd * s.Rp; e += blockDim.x) {
+    const int d = e / s.Rp, r = e % s.Rp;
+    uint16_t v = 0;
+    if (r < s.R) {
+      const long src = ((long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B) * s.hd + d;
+      v = F32 ? (uint16_t)f2bf(reinterpret_cast<const float*>(x)[src]) : reinterpret_cast<const uint16_t*>(x)[src];
+    }
+    o[e] = v;
+  }
+}
+
+// dO -> bf16 copy, and D = rowsum(dO * O) per (row, head): one wave per (row, head)
+__global__ __launch_bounds__(256) void k_tr_dout(const float* dout, const float* out, int rows_heads, int hd,
+                                                  uint16_t* dob, float* dsum) {
+  const int w = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (w >= rows_heads) return;
+  const long base = (long)w * hd;
+  float acc = 0.f;
+  for (int d = lane; d < hd; d += 64) {
+    const float x = dout[base + d];
+    acc += x * out[base + d];
+    dob[base + d] = (uint16_t)f2bf(x);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) dsum[w] = acc;
+}
+
+// ---- forward and dQ: work-group (block i, KV head g), wave w takes 16-row query tiles
+// w, w + 4, ...; key tiles of 32 (the context before the anchor, then the block's own keys) ----
+template <int HD, bool DQ>
+__global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
+  const AttnShapeT& s = a.s;
+  const int i = blockIdx.x, g = blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = lane & 15, q4 = lane >> 4;
+  const int QT = (s.R + 15) / 16;
+  const int anchor = min(max(a.anchors[i], 0), s.T);
+  const int nct = (anchor + 31) / 32;
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const u32x4 z4 = {0u, 0u, 0u, 0u};
+  for (int t = w; t < QT; t += 4) {
+    const int r = 16 * t + col;
+    const bool rv = r < s.R;
+    const int h = g * s.G + (rv ? r / s.B : 0), b = rv ? r % s.B : 0;
+    const long qrow = ((long)(i * s.B + b) * s.n_q + h) * HD;
+    u32x4 qf[HD / 32], df[HD / 32];
+#pragma unroll
+    for (int ks = 0; ks < HD / 32; ++ks) {
+      qf[ks] = rv ? ld16(a.q + qrow + ks * 32 + 8 * q4) : z4;
+      if constexpr (DQ) df[ks] = rv ? ld16(a.dob + qrow + ks * 32 + 8 * q4) : z4;
+    }
+    float m = -INFINITY, l = 0.f, lse2 = 0.f, dr = 0.f;
+    if constexpr (DQ) {
+      lse2 = rv ? a.lse[(long)(i * s.B + b) * s.n_q + h] * 1.4426950408889634f : 0.f;
+      dr = rv ? a.dsum[(long)(i * s.B + b) * s.n_q + h] : 0.f;
+    }
+    f32x4 o[HD / 16];
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) o[dt] = zero4();
+    for (int kt = 0; kt <= nct; ++kt) {
+      const bool blk = kt == nct;
+      // rows of this lane's A operands: key 16 x + col of the tile (zeros where not visible)
+      const uint16_t* kbase = blk ? a.kb : a.kc;
+      const uint16_t* vbase = blk ? a.vb : a.vc;
+      bool ok[2];
+      long krow[2];
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        const int j = 16 * x + col;
+        ok[x] = blk ? j < s.B : kt * 32 + j < anchor;
+        krow[x] = ok[x] ? (blk ? ((long)(i * s.B + j) * s.n_kv + g) * HD : ((long)(kt * 32 + j) * s.n_kv + g) * HD) : 0;
+      }
+      f32x4 s0 = zero4(), s1 = zero4(), p0 = zero4(), p1 = zero4();
+#pragma unroll
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        const int ko = ks * 32 + 8 * q4;
+        const u32x4 a0 = ok[0] ? ld16(kbase + krow[0] + ko) : z4;
+        const u32x4 a1 = ok[1] ? ld16(kbase + krow[1] + ko) : z4;
+        s0 = mfma(a0, qf[ks], s0);
+        s1 = mfma(a1, qf[ks], s1);
+        if constexpr (DQ) {
+          const u32x4 v0 = ok[0] ? ld16(vbase + krow[0] + ko) : z4;
+          const u32x4 v1 = ok[1] ? ld16(vbase + krow[1] + ko) : z4;
+          p0 = mfma(v0, df[ks], p0);  // dP^T
+          p1 = mfma(v1, df[ks], p1);
+        }
+      }
+      // this lane's values: keys 4 q4 + e (tile 0) and 16 + 4 q4 + e (tile 1) of query row col
+      float x0[4], x1[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j0 = 4 * q4 + e, j1 = 16 + 4 * q4 + e;
+        const bool ok0 = blk ? j0 < s.B : kt * 32 + j0 < anchor;
+        const bool ok1 = blk ? j1 < s.B : kt * 32 + j1 < anchor;
+        x0[e] = ok0 ? s0[e] * sl2 : -INFINITY;
+        x1[e] = ok1 ? s1[e] * sl2 : -INFINITY;
+      }
+      u32x4 pb;
+      if constexpr (!DQ) {
+        float tm = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tm = fmaxf(tm, fmaxf(x0[e], x1[e]));
+        tm = fmaxf(tm, __shfl_xor(tm, 16));
+        tm = fmaxf(tm, __shfl_xor(tm, 32));
+        const float mn = fmaxf(m, tm);
+        const float corr = (mn == -INFINITY) ? 1.f : exp2f(m - mn);
+        float ps = 0.f;
+        f32x4 e0, e1;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          e0[e] = (mn == -INFINITY) ? 0.f : exp2f(x0[e] - mn);
+          e1[e] = (mn == -INFINITY) ? 0.f : exp2f(x1[e] - mn);
+          ps += e0[e] + e1[e];
+        }
+        l = l * corr + ps;
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt) o[dt] *= corr;
+        m = mn;
+        pb = pack_bf8(e0, e1);
+      } else {
+        f32x4 d0, d1;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float pp0 = exp2f(x0[e] - lse2), pp1 = exp2f(x1[e] - lse2);
+          d0[e] = pp0 * (p0[e] - dr);
+          d1[e] = pp1 * (p1[e] - dr);
+        }
+        pb = pack_bf8(d0, d1);
+      }
+      // O^T += V^T P^T (forward) or dQ^T += K^T dS^T: A rows = dims d = 16 dt + col
+#pragma unroll
+      for (int dt = 0; dt < HD / 16; ++dt) {
+        const int d = 16 * dt + col;
+        const uint16_t* src = DQ ? (blk ? a.kbt : a.kct) : (blk ? a.vbt : a.vct);
+        const long base = blk ? ((long)g * HD + d) * s.Mp + (long)i * s.B : ((long)g * HD + d) * s.Tp + kt * 32;
+        o[dt] = mfma(ld_pair(src + base + 4 * q4), pb, o[dt]);
+      }
+    }
+    if (!rv) continue;
+    float out_scale;
+    if constexpr (!DQ) {
+      l += __shfl_xor(l, 16);
+      l += __shfl_xor(l, 32);
+      out_scale = 1.f / l;
+      if (q4 == 0) a.lse[(long)(i * s.B + b) * s.n_q + h] = (m + log2f(l)) * 0.6931471805599453f;
+    } else {
+      out_scale = a.scale;
+    }
+    float* dst = (DQ ? a.dq : a.out) + qrow;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt)
+      *reinterpret_cast<f32x4*>(dst + 16 * dt + 4 * q4) = o[dt] * out_scale;
+  }
+}
+
+// ---- dK, dV: work-group (32-key tile or one block's keys, KV head g, chunk of blocks);
+// wave w takes the blocks (context keys) or 32-row pairs (block keys) w, w + 4, ... ----
+template <int HD, bool BLK>
+__global__ __launch_bounds__(kTrT) void k_aatt_kv(AttnT a) {
+  const AttnShapeT& s = a.s;
+  const int g = blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = lane & 15, q4 = lane >> 4;
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const int NP = s.Rp / 32;  // 32-row pairs of a (block, group)
+  const u32x4 z4 = {0u, 0u, 0u, 0u};
+  // keys of this work-group: context tile kt (keys 32 kt + 0..31) or block ib's B keys
+  const int kt = BLK ? 0 : blockIdx.x, ib = BLK ? blockIdx.x : 0;
+  const int i0 = BLK ? ib : blockIdx.z * kChunkBlocks;
+  const int i1 = BLK ? ib + 1 : min(s.n_blocks, i0 + kChunkBlocks);
+  f32x4 dk[HD / 16][2], dv[HD / 16][2];
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt)
+#pragma unroll
+    for (int x = 0; x < 2; ++x) dk[dt][x] = dv[dt][x] = zero4();
+  // B-operand rows (keys) of this lane: key 16x + col of the tile
+  u32x4 kf[2][HD / 32], vf[2][HD / 32];
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+    const int j = 16 * x + col;
+    const bool ok = BLK ? j < s.B : kt * 32 + j < s.T;
+    const long row = !ok ? 0 : BLK ? ((long)(ib * s.B + j) * s.n_kv + g) * HD : ((long)(kt * 32 + j) * s.n_kv + g) * HD;
+    const uint16_t* kp = (BLK ? a.kb : a.kc) + row;
+    const uint16_t* vp = (BLK ? a.vb : a.vc) + row;
+#pragma unroll
+    for (int ks = 0; ks < HD / 32; ++ks) {
+      kf[x][ks] = ok ? ld16(kp + ks * 32 + 8 * q4) : z4;
+      vf[x][ks] = ok ? ld16(vp + ks * 32 + 8 * q4) : z4;
+    }
+  }
+  // units of work: (block, row pair); wave w takes units w, w + 4, ...
+  const int units = (i1 - i0) * NP;
+  for (int u = w; u < units; u += 4) {
+    const int i = i0 + u / NP, pr = u % NP;
+    const int anchor = min(max(a.anchors[i], 0), s.T);
+    if (!BLK && anchor <= kt * 32) continue;  // no key of the tile is visible to block i
+    // S = Q K^T and dP = dO V^T for rows 32 pr + 16 y + (4 q4 + e) (y = 0, 1), keys 16x + col
+    f32x4 sc[2][2], dp[2][2];
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int x = 0; x < 2; ++x) sc[y][x] = dp[y][x] = zero4();
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+      const int r = 32 * pr + 16 * y + col;  // A row of this lane
+      const bool rv = r < s.R;
+      const long qrow = rv ? ((long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B) * HD : 0;
+#pragma unroll
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        const u32x4 qa = rv ? ld16(a.q + qrow + ks * 32 + 8 * q4) : z4;
+        const u32x4 da = rv ? ld16(a.dob + qrow + ks * 32 + 8 * q4) : z4;
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          sc[y][x] = mfma(qa, kf[x][ks], sc[y][x]);
+          dp[y][x] = mfma(da, vf[x][ks], dp[y][x]);
+        }
+      }
+    }
+    // P and dS at this lane's values: row 32 pr + 16 y + 4 q4 + e, key 16 x + col
+    f32x4 P[2][2], dS[2][2];
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 32 * pr + 16 * y + 4 * q4 + e;
+        const bool rv = r < s.R;
+        const long rh = rv ? (long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B : 0;
+        const float lse2 = rv ? a.lse[rh] * 1.4426950408889634f : 0.f;
+        const float dr = rv ? a.dsum[rh] : 0.f;
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          const int j = 16 * x + col;
+          const bool ok = rv && (BLK ? j < s.B : kt * 32 + j < anchor);
+          const float p = ok ? exp2f(sc[y][x][e] * sl2 - lse2) : 0.f;
+          P[y][x][e] = p;
+          dS[y][x][e] = p * (dp[y][x][e] - dr);
+        }
+      }
+    }
+    // dV^T += dO^T P, dK^T += Q^T dS: A rows = dims d = 16 dt + col, k = the pair's 32 rows
+    const long tb = ((long)g * s.n_blocks + i) * HD * s.Rp + 32 * pr + 4 * q4;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) {
+      const long off = tb + (long)(16 * dt + col) * s.Rp;
+      const u32x4 doa = ld_pair(a.dot + off);
+      const u32x4 qa = ld_pair(a.qt + off);
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        dv[dt][x] = mfma(doa, pack_bf8(P[0][x], P[1][x]), dv[dt][x]);
+        dk[dt][x] = mfma(qa, pack_bf8(dS[0][x], dS[1][x]), dk[dt][x]);
+      }
+    }
+  }
+  // sum the 4 waves' tiles in wave order through LDS, 8 tiles per round
+  __shared__ f32x4 red[3][8][64];
+  constexpr int NT = HD / 16 * 2 * 2;  // tiles per wave (dK, dV)
+  float* outk = BLK ? a.dkb : a.part + (long)blockIdx.z * s.T * s.n_kv * HD;
+  float* outv = BLK ? a.dvb : a.part + ((long)a.nch + blockIdx.z) * s.T * s.n_kv * HD;
+#pragma unroll
+  for (int r0 = 0; r0 < NT; r0 += 8) {
+    if (w > 0) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int tI = r0 + u, kind = tI / (HD / 16 * 2), rem = tI % (HD / 16 * 2);
+        red[w - 1][u][lane] = kind == 0 ? dk[rem / 2][rem % 2] : dv[rem / 2][rem % 2];
+      }
+    }
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int tI = r0 + u, kind = tI / (HD / 16 * 2), rem = tI % (HD / 16 * 2);
+        const int dt = rem / 2, x = rem % 2;
+        f32x4 v = kind == 0 ? dk[dt][x] : dv[dt][x];
+        v += red[0][u][lane];
+        v += red[1][u][lane];
+        v += red[2][u][lane];
+        if (kind == 0) v *= a.scale;
+        // tile (dims 16 dt + 4 q4 + e, key 16 x + col)
+        const int j = 16 * x + col;
+        const bool ok = BLK ? j < s.B : kt * 32 + j < s.T;
+        if (ok) {
+          const long row = BLK ? (long)(ib * s.B + j) : (long)(kt * 32 + j);
+          float* dst = (kind == 0 ? outk : outv) + (row * s.n_kv + g) * HD + 16 * dt + 4 * q4;
+          *reinterpret_cast<f32x4*>(dst) = v;
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// context dK, dV = the chunks' partials added in chunk order
+__global__ void k_aatt_sum(const float* part, int nch, long n, float* dk, float* dv) {
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) {
+    float sk = 0.f, sv = 0.f;
+    for (int c = 0; c < nch; ++c) {
+      sk += part[(long)c * n + e];
+      sv += part[((long)nch + c) * n + e];
+    }
+    dk[e] = sk;
+    dv[e] = sv;
+  }
+}
+
+// ---- weighted cross-entropy (Eq. 5) ----
+// per row: weight w (0 for the anchor position, b = 0, and for labels < 0, else
+// exp(-(b - 1) / gamma)), lse and CE = lse - z[label]; one work-group per row, one pass
+// with a running maximum per thread
+__global__ __launch_bounds__(256) void k_wce_rows(const float* logits, const int32_t* labels, int V, int B,
+                                                  float gamma, float* lse_out, float* w_out, float* ce_out) {
+  __shared__ float sm[4], ss[4];
+  const int row = blockIdx.x, lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const float* z = logits + (long)row * V;
+  float m = -INFINITY, sum = 0.f;
+  auto take = [&](float x) {
+    if (x > m) {
+      sum = sum * expf(m - x) + 1.f;
+      m = x;
+    } else {
+      sum += expf(x - m);
+    }
+  };
+  // 16-byte loads where the row allows them (V % 4 == 0 keeps every row 16-byte aligned)
+  const int V4 = (V % 4 == 0) ? V / 4 : 0;
+  for (int v = threadIdx.x; v < V4; v += 256) {
+    const f32x4 x = reinterpret_cast<const f32x4*>(z)[v];
+    take(x[0]);
+    take(x[1]);
+    take(x[2]);
+    take(x[3]);
+  }
+  for (int v = 4 * V4 + threadIdx.x; v < V; v += 256) take(z[v]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float om = __shfl_xor(m, off), os = __shfl_xor(sum, off);
+    const float nm = fmaxf(m, om);
+    sum = (nm == -INFINITY) ? 0.f : sum * expf(m - nm) + os * expf(om - nm);
+    m = nm;
+  }
+  if (lane == 0) {
+    sm[wv] = m;
+    ss[wv] = sum;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float M = sm[0], S = ss[0];
+    for (int k = 1; k < 4; ++k) {
+      const float nm = fmaxf(M, sm[k]);
+      S = S * expf(M - nm) + ss[k] * expf(sm[k] - nm);
+      M = nm;
+    }
+    const float lse = M + logf(S);
+    const int b = row % B, y = labels[row];
+    const bool on = b > 0 && y >= 0 && y < V;
+    lse_out[row] = lse;
+    w_out[row] = on ? expf(-(float)(b - 1) / gamma) : 0.f;
+    ce_out[row] = on ? lse - z[y] : 0.f;
+  }
+}
+
+// loss = sum w ce / sum w over the rows, in row order (one work-group), and 1 / sum w
+__global__ __launch_bounds__(256) void k_wce_loss(const float* w, const float* ce, int rows, float* loss, float* inv_wsum) {
+  __shared__ double sw[256], sl[256];
+  double a = 0.0, c = 0.0;
+  for (int r = threadIdx.x; r < rows; r += 256) {
+    a += w[r];
+    c += (double)w[r] * ce[r];
+  }
+  sw[threadIdx.x] = a;
+  sl[threadIdx.x] = c;
+  __syncthreads();
+  for (int k = 128; k > 0; k >>= 1) {
+    if ((int)threadIdx.x < k) {
+      sw[threadIdx.x] += sw[threadIdx.x + k];
+      sl[threadIdx.x] += sl[threadIdx.x + k];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    loss[0] = sw[0] > 0.0 ? (float)(sl[0] / sw[0]) : 0.f;
+    inv_wsum[0] = sw[0] > 0.0 ? (float)(1.0 / sw[0]) : 0.f;
+  }
+}
+
+// dz = (w / sum w) (softmax(z) - onehot(label)), four values per thread per step where the
+// row allows 16-byte accesses
+__global__ __launch_bounds__(256) void k_wce_grad(const float* logits, const int32_t* labels, const float* lse,
+                                                  const float* w, const float* inv_wsum, int V, float* dz) {
+  const int row = blockIdx.x;
+  const float c = w[row] * inv_wsum[0];
+  const float l = lse[row];
+  const int y = labels[row];
+  const float* z = logits + (long)row * V;
+  float* d = dz + (long)row * V;
+  const int V4 = (V % 4 == 0) ? V / 4 : 0;
+  for (int v = threadIdx.x; v < V4; v += 256) {
+    const f32x4 x = reinterpret_cast<const f32x4*>(z)[v];
+    f32x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = c == 0.f ? 0.f : c * (expf(x[e] - l) - (4 * v + e == y ? 1.f : 0.f));
+    reinterpret_cast<f32x4*>(d)[v] = o;
+  }
+  for (int v = 4 * V4 + threadIdx.x; v < V; v += 256) d[v] = c == 0.f ? 0.f : c * (expf(z[v] - l) - (v == y ? 1.f : 0.f));
+}
+
+}  // namespace
+
+// ---- entry points ----------------------------------------------------------------------
+
+static AttnShapeT att_shape(int n_blocks, int B, int T, int n_q, int n_kv, int hd) {
+  AttnShapeT s{};
+  s.n_blocks = n_blocks;
+  s.B = B;
+  s.T = T;
+  s.n_q = n_q;
+  s.n_kv = n_kv;
+  s.hd = hd;
+  s.G = n_q / n_kv;
+  s.R = s.G * B;
+  s.Rp = (s.R + 31) / 32 * 32;
+  s.Tp = (T + 31) / 32 * 32 + 32;
+  s.Mp = n_blocks * B + 32;
+  return s;
+}
+
+static int att_check(int n_blocks, int B, int T, int n_q, int n_kv, int hd) {
+  if (n_blocks < 1 || B < 1 || B > 16 || T < 0 || n_q < 1 || n_kv < 1 || n_q % n_kv) return DFLARE_ERR_INVALID_ARG;
+  if (hd != 64 && hd != 128) return DFLARE_ERR_UNSUPPORTED;
+  if ((n_q / n_kv) * B > 128) return DFLARE_ERR_UNSUPPORTED;
+  return DFLARE_OK;
+}
+
+struct WsLayout {
+  size_t kct, vct, kbt, vbt, qt, dot, dob, dsum, part, total;
+  int nch;
+};
+
+static WsLayout ws_layout(const AttnShapeT& s) {
+  WsLayout L{};
+  auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+  size_t o = 0;
+  const size_t ctx_t = (size_t)s.n_kv * s.hd * s.Tp * 2, blk_t = (size_t)s.n_kv * s.hd * s.Mp * 2;
+  const size_t grp = (size_t)s.n_kv * s.n_blocks * s.hd * s.Rp * 2;
+  const size_t rows = (size_t)s.n_blocks * s.B * s.n_q;
+  L.nch = (s.n_blocks + kChunkBlocks - 1) / kChunkBlocks;
+  L.kct = o; o = al(o + ctx_t);
+  L.vct = o; o = al(o + ctx_t);
+  L.kbt = o; o = al(o + blk_t);
+  L.vbt = o; o = al(o + blk_t);
+  L.qt = o; o = al(o + grp);
+  L.dot = o; o = al(o + grp);
+  L.dob = o; o = al(o + rows * s.hd * 2);
+  L.dsum = o; o = al(o + rows * 4);
+  L.part = o; o = al(o + (size_t)2 * L.nch * s.T * s.n_kv * s.hd * 4);
+  L.total = o;
+  return L;
+}
+
+static AttnT att_args(const AttnShapeT& s, const void* q, const void* kc, const void* vc, const void* kb,
+                      const void* vb, const int32_t* anchors, void* ws) {
+  const WsLayout L = ws_layout(s);
+  char* w = static_cast<char*>(ws);
+  AttnT a{};
+  a.s = s;
+  a.q = (const uint16_t*)q;
+  a.kc = (const uint16_t*)kc;
+  a.vc = (const uint16_t*)vc;
+  a.kb = (const uint16_t*)kb;
+  a.vb = (const uint16_t*)vb;
+  a.anchors = anchors;
+  a.kct = (uint16_t*)(w + L.kct);
+  a.vct = (uint16_t*)(w + L.vct);
+  a.kbt = (uint16_t*)(w + L.kbt);
+  a.vbt = (uint16_t*)(w + L.vbt);
+  a.qt = (uint16_t*)(w + L.qt);
+  a.dot = (uint16_t*)(w + L.dot);
+  a.dob = (uint16_t*)(w + L.dob);
+  a.dsum = (float*)(w + L.dsum);
+  a.part = (float*)(w + L.part);
+  a.nch = L.nch;
+  a.scale = 1.0f / sqrtf((float)s.hd);
+  return a;
+}
+
+static void transpose_kv(hipStream_t st, const uint16_t* src, int nrows, int cols, int ld, uint16_t* dst) {
+  hipLaunchKernelGGL(k_tr_kv_t, dim3((ld + 31) / 32, (cols + 31) / 32), dim3(256), 0, st, src, nrows, cols, ld, dst);
+}
+
+template <typename F>
+static void by_hd(int hd, F&& f) {
+  if (hd == 64) f(std::integral_constant<int, 64>{});
+  else f(std::integral_constant<int, 128>{});
+}
+
+}  // namespace dflare
+
+using namespace dflare;
+
+extern "C" {
+
+size_t dflare_anchor_attention_workspace(int32_t n_blocks, int32_t B, int32_t T, int32_t n_q, int32_t n_kv,
+                                         int32_t hd) {
+  if (att_check(n_blocks, B, T, n_q, n_kv, hd) != DFLARE_OK) return 0;
+  return ws_layout(att_shape(n_blocks, B, T, n_q, n_kv, hd)).total;
+}
+
+int dflare_anchor_attention_fwd(const void* q, const void* k_ctx, const void* v_ctx, const void* k_blk,
+                                const void* v_blk, const int32_t* anchors, int32_t n_blocks, int32_t B, int32_t T,
+                                int32_t n_q, int32_t n_kv, int32_t hd, float* out, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  const int rc = att_check(n_blocks, B, T, n_q, n_kv, hd);
+  if (rc != DFLARE_OK) return rc;
+  if (!q || !k_blk || !v_blk || !anchors || !out || !lse || !workspace || (T > 0 && (!k_ctx || !v_ctx)))
+    return DFLARE_ERR_INVALID_ARG;
+  const AttnShapeT s = att_shape(n_blocks, B, T, n_q, n_kv, hd);
+  if (workspace_bytes < ws_layout(s).total) return DFLARE_ERR_INVALID_ARG;
+  hipStream_t st = (hipStream_t)stream;
+  AttnT a = att_args(s, q, k_ctx, v_ctx, k_blk, v_blk, anchors, workspace);
+  a.out = out;
+  a.lse = lse;
+  const int cols = n_kv * hd;
+  const uint16_t* zero_src = a.kb;  // with T = 0 the context copies are all zeros
+  transpose_kv(st, T > 0 ? a.vc : zero_src, T, cols, s.Tp, a.vct);
+  transpose_kv(st, a.vb, n_blocks * B, cols, s.Mp, a.vbt);
+  by_hd(hd, [&](auto h) {
+    hipLaunchKernelGGL((k_aatt_rows<decltype(h)::value, false>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
+  });
+  return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
+}
+
+int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_ctx, const void* k_blk,
+                                const void* v_blk, const int32_t* anchors, int32_t n_blocks, int32_t B, int32_t T,
+                                int32_t n_q, int32_t n_kv, int32_t hd, const float* out, const float* lse,
+                                const float* dout, float* dq, float* dk_ctx, float* dv_ctx, float* dk_blk,
+                                float* dv_blk, void* workspace, size_t workspace_bytes, void* stream) {
+  const int rc = att_check(n_blocks, B, T, n_q, n_kv, hd);
+  if (rc != DFLARE_OK) return rc;
+  if (!q || !k_blk || !v_blk || !anchors || !out || !lse || !dout || !dq || !dk_blk || !dv_blk || !workspace ||
+      (T > 0 && (!k_ctx || !v_ctx || !dk_ctx || !dv_ctx)))
+    return DFLARE_ERR_INVALID_ARG;
+  const AttnShapeT s = att_shape(n_blocks, B, T, n_q, n_kv, hd);
+  if (workspace_bytes < ws_layout(s).total) return DFLARE_ERR_INVALID_ARG;
+  hipStream_t st = (hipStream_t)stream;
+  AttnT a = att_args(s, q, k_ctx, v_ctx, k_blk, v_blk, anchors, workspace);
+  a.out = nullptr;
+  a.lse = const_cast<float*>(lse);
+  a.dout = dout;
+  a.dq = dq;
+  a.dkc = dk_ctx;
+  a.dvc = dv_ctx;
+  a.dkb = dk_blk;
+  a.dvb = dv_blk;
+  const int cols = n_kv * hd;
+  const int M = n_blocks * B;
+  const uint16_t* zero_src = a.kb;
+  transpose_kv(st, T > 0 ? a.kc : zero_src, T, cols, s.Tp, a.kct);
+  transpose_kv(st, a.kb, M, cols, s.Mp, a.kbt);
+  hipLaunchKernelGGL((k_tr_group_t<false>), dim3(n_blocks, n_kv), dim3(256), 0, st, (const void*)q, s, a.qt);
+  hipLaunchKernelGGL((k_tr_group_t<true>), dim3(n_blocks, n_kv), dim3(256), 0, st, (const void*)dout, s, a.dot);
+  hipLaunchKernelGGL(k_tr_dout, dim3((M * n_q + 3) / 4), dim3(256), 0, st, dout, out, M * n_q, hd, a.dob, a.dsum);
+  by_hd(hd, [&](auto h) {
+    constexpr int HD = decltype(h)::value;
+    hipLaunchKernelGGL((k_aatt_rows<HD, true>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
+    hipLaunchKernelGGL((k_aatt_kv<HD, true>), dim3(n_blocks, n_kv, 1), dim3(kTrT), 0, st, a);
+    if (T > 0) hipLaunchKernelGGL((k_aatt_kv<HD, false>), dim3((T + 31) / 32, n_kv, a.nch), dim3(kTrT), 0, st, a);
+  });
+  if (T > 0) {
+    const long n = (long)T * n_kv * hd;
+    hipLaunchKernelGGL(k_aatt_sum, dim3((int)std::min<long>((n + 255) / 256, 4096)), dim3(256), 0, st, a.part, a.nch,
+                       n, dk_ctx, dv_ctx);
+  }
+  return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
+}
+
+size_t dflare_weighted_ce_workspace(int32_t rows) { return ((size_t)3 * rows + 64) * 4; }
+
+int dflare_weighted_ce(const float* logits, const int32_t* labels, int32_t rows, int32_t V, int32_t B, float gamma,
+                       float* loss, float* row_ce, float* dlogits, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  if (!logits || !labels || !loss || !row_ce || !dlogits || !workspace || rows < 1 || V < 1 || B < 1 ||
+      rows % B || !(gamma > 0.f) || !isfinite(gamma))
+    return DFLARE_ERR_INVALID_ARG;
+  if (workspace_bytes < dflare_weighted_ce_workspace(rows)) return DFLARE_ERR_INVALID_ARG;
+  hipStream_t st = (hipStream_t)stream;
+  float* lse = static_cast<float*>(workspace);
+  float* w = lse + rows;
+  float* inv = w + rows;
+  hipLaunchKernelGGL(k_wce_rows, dim3(rows), dim3(256), 0, st, logits, labels, V, B, gamma, lse, w, row_ce);
+  hipLaunchKernelGGL(k_wce_loss, dim3(1), dim3(256), 0, st, w, row_ce, rows, loss, inv);
+  hipLaunchKernelGGL(k_wce_grad, dim3(rows), dim3(256), 0, st, logits, labels, lse, w, inv, V, dlogits);
+  return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
+}
+
+}  // extern "C"

@@ -27,6 +27,8 @@ EXPORTED = (
     "dflare_kernel_stats", "dflare_profile_begin", "dflare_profile_end", "dflare_set_option",
     "dflare_fuse_append_batched", "dflare_draft_block_batched", "dflare_truncate_seq",
     "dflare_context_len_seq", "dflare_debug_read_seq", "dflare_set_sampling", "dflare_accept",
+    "dflare_anchor_attention_workspace", "dflare_anchor_attention_fwd", "dflare_anchor_attention_bwd",
+    "dflare_weighted_ce_workspace", "dflare_weighted_ce",
 )
 K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T, K_DRAFT = range(1, 10)
 (K_B_QKV, K_B_ATTN, K_B_O, K_B_GATE_UP, K_B_DOWN, K_B_LM_HEAD, K_B_KV_T, K_B_EPI, K_B_FUSE, K_B_DRAFT,
@@ -96,6 +98,14 @@ def lib() -> ctypes.CDLL:
         "dflare_truncate_seq": ([vp, i32, i32], ctypes.c_int),
         "dflare_set_sampling": ([vp, ctypes.c_float, ctypes.c_uint64], ctypes.c_int),
         "dflare_accept": ([vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+        "dflare_anchor_attention_workspace": ([ctypes.c_int32] * 6, ctypes.c_size_t),
+        "dflare_anchor_attention_fwd": ([vp] * 6 + [ctypes.c_int32] * 6 + [vp, vp, vp, ctypes.c_size_t, vp],
+                                        ctypes.c_int),
+        "dflare_anchor_attention_bwd": ([vp] * 6 + [ctypes.c_int32] * 6 + [vp] * 9 + [ctypes.c_size_t, vp],
+                                        ctypes.c_int),
+        "dflare_weighted_ce_workspace": ([ctypes.c_int32], ctypes.c_size_t),
+        "dflare_weighted_ce": ([vp, vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, vp, vp, vp,
+                                vp, ctypes.c_size_t, vp], ctypes.c_int),
         "dflare_context_len_seq": ([vp, i32, ctypes.POINTER(i32)], ctypes.c_int),
         "dflare_debug_read_seq": ([vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float),
                                    i64], ctypes.c_int),
@@ -195,6 +205,63 @@ def dflare_accept(h: int, block_ids: torch.Tensor, draft_tokens: torch.Tensor, t
     _check(lib().dflare_accept(h, _ptr(block_ids), _ptr(draft_tokens), _ptr(target_tokens), _ptr(target_hidden),
                                _ptr(next_ids), _ptr(emitted), ctypes.byref(k)), h)
     return k.value
+
+
+# ---- training-side kernels (no handle) ----
+
+def _train_check(rc: int, what: str) -> None:
+    if rc != 0:
+        raise DFlareError(rc, what)
+
+
+def anchor_attention_fwd(q, k_ctx, v_ctx, k_blk, v_blk, anchors, B: int, stream=None):
+    """Anchor attention forward (include/dflare.h).  q [n*B, n_q, hd], k/v_ctx [T, n_kv, hd],
+    k/v_blk [n*B, n_kv, hd] as bf16-bit int16/uint16 device tensors, anchors int32 [n].
+    Returns (out fp32 [n*B, n_q, hd], lse fp32 [n*B, n_q])."""
+    M, n_q, hd = q.shape
+    T, n_kv = k_ctx.shape[0], k_blk.shape[1]
+    n = M // B
+    ws_bytes = lib().dflare_anchor_attention_workspace(n, B, T, n_q, n_kv, hd)
+    if ws_bytes == 0:
+        raise DFlareError(-5, "unsupported anchor attention shape")
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    out = torch.empty((M, n_q, hd), dtype=torch.float32, device=q.device)
+    lse = torch.empty((M, n_q), dtype=torch.float32, device=q.device)
+    _train_check(lib().dflare_anchor_attention_fwd(
+        _ptr(q), _ptr(k_ctx) if T else None, _ptr(v_ctx) if T else None, _ptr(k_blk), _ptr(v_blk), _ptr(anchors),
+        n, B, T, n_q, n_kv, hd, _ptr(out), _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)), "anchor attention fwd")
+    return out, lse
+
+
+def anchor_attention_bwd(q, k_ctx, v_ctx, k_blk, v_blk, anchors, B: int, out, lse, dout, stream=None):
+    """Anchor attention backward: returns (dq, dk_ctx, dv_ctx, dk_blk, dv_blk), fp32."""
+    M, n_q, hd = q.shape
+    T, n_kv = k_ctx.shape[0], k_blk.shape[1]
+    n = M // B
+    ws_bytes = lib().dflare_anchor_attention_workspace(n, B, T, n_q, n_kv, hd)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    f = dict(dtype=torch.float32, device=q.device)
+    dq = torch.empty((M, n_q, hd), **f)
+    dkc, dvc = torch.empty((T, n_kv, hd), **f), torch.empty((T, n_kv, hd), **f)
+    dkb, dvb = torch.empty((M, n_kv, hd), **f), torch.empty((M, n_kv, hd), **f)
+    _train_check(lib().dflare_anchor_attention_bwd(
+        _ptr(q), _ptr(k_ctx) if T else None, _ptr(v_ctx) if T else None, _ptr(k_blk), _ptr(v_blk), _ptr(anchors),
+        n, B, T, n_q, n_kv, hd, _ptr(out), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dkc) if T else None,
+        _ptr(dvc) if T else None, _ptr(dkb), _ptr(dvb), _ptr(ws), ws_bytes, _stream(stream)), "anchor attention bwd")
+    return dq, dkc, dvc, dkb, dvb
+
+
+def weighted_ce(logits, labels, B: int, gamma: float, stream=None):
+    """Position-weighted cross-entropy: returns (loss fp32 [1], row_ce fp32 [rows], dlogits fp32 [rows, V])."""
+    rows, V = logits.shape
+    ws_bytes = lib().dflare_weighted_ce_workspace(rows)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=logits.device)
+    loss = torch.empty(1, dtype=torch.float32, device=logits.device)
+    ce = torch.empty(rows, dtype=torch.float32, device=logits.device)
+    dz = torch.empty_like(logits)
+    _train_check(lib().dflare_weighted_ce(_ptr(logits), _ptr(labels), rows, V, B, float(gamma), _ptr(loss), _ptr(ce),
+                                          _ptr(dz), _ptr(ws), ws_bytes, _stream(stream)), "weighted ce")
+    return loss, ce, dz
 
 
 def dflare_set_sampling(h: int, temperature: float, seed: int = 0) -> None:

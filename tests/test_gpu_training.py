@@ -1,0 +1,95 @@
+"""GPU parity of the training-side kernels against the fp64 oracle (oracle/training_oracle.py)
+on the same seeded bf16 inputs: anchor attention (Sec. 3.3) forward and backward, and the
+progressive position-weighted cross-entropy (Eq. 5).
+
+Shapes span several 32-key tiles with ragged tails, block sizes 16 and 5, GQA groups of 4 and
+3, more blocks than one 64-block gradient chunk, anchors 0 (no context) and T (all of it), and
+T = 0.  The attention's products run on bf16 matrix cores with probabilities and gradients
+rounded to bf16 as operands; the bar is the per-tensor relative error of tests/parity.py
+(2e-2 of the tensor's largest magnitude).  Gradients must repeat bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import training_oracle as tr
+from paper_2606_02091_amd import dflare as dfl
+from paper_2606_02091_amd import synth
+import parity as P
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - CPU container
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+CASES = {
+    # name: (n_blocks, B, T, n_q, n_kv, hd)
+    "b16_hd128": (5, 16, 200, 8, 2, 128),
+    "b5_hd64_gqa3": (7, 5, 77, 6, 2, 64),
+    "chunks_hd64": (150, 4, 300, 4, 1, 64),
+    "no_context": (3, 8, 0, 4, 2, 128),
+}
+
+
+def inputs(n, B, T, nq, nkv, hd, seed=0):
+    rng = np.random.default_rng(seed)
+
+    def bf(shape):
+        return synth.round_bf16(rng.standard_normal(shape).astype(np.float32))
+
+    x = dict(q=bf((n * B, nq, hd)), k_ctx=bf((T, nkv, hd)), v_ctx=bf((T, nkv, hd)),
+             k_blk=bf((n * B, nkv, hd)), v_blk=bf((n * B, nkv, hd)))
+    anchors = rng.integers(0, T + 1, size=n).astype(np.int32)
+    if n >= 2:
+        anchors[0], anchors[1] = 0, T
+    dout = rng.standard_normal((n * B, nq, hd))
+    return x, anchors, dout
+
+
+def dev(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda()
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_anchor_attention_matches_oracle(name):
+    n, B, T, nq, nkv, hd = CASES[name]
+    print(f"[training] attention {name}", flush=True)
+    x, anchors, dout = inputs(n, B, T, nq, nkv, hd)
+    f64 = {k: synth.bf16_to_f32(v).astype(np.float64) for k, v in x.items()}
+    d = {k: dev(v) for k, v in x.items()}
+    a = torch.from_numpy(anchors).cuda()
+    out, lse = dfl.anchor_attention_fwd(d["q"], d["k_ctx"], d["v_ctx"], d["k_blk"], d["v_blk"], a, B)
+    ro, rl = tr.anchor_attention_fwd(**f64, anchors=list(anchors), B=B)
+    e_out, e_lse = P.relinf(out.cpu().numpy(), ro), P.relinf(lse.cpu().numpy(), rl)
+    assert e_out <= P.REL_TOL and e_lse <= P.REL_TOL, (e_out, e_lse)
+    do = torch.from_numpy(dout.astype(np.float32)).cuda()
+    g = dfl.anchor_attention_bwd(d["q"], d["k_ctx"], d["v_ctx"], d["k_blk"], d["v_blk"], a, B, out, lse, do)
+    ref = tr.anchor_attention_bwd(**f64, anchors=list(anchors), B=B, dout=dout)
+    errs = {}
+    for nm, got, want in zip(("dq", "dk_ctx", "dv_ctx", "dk_blk", "dv_blk"), g, ref):
+        if want.size == 0:
+            continue
+        errs[nm] = P.relinf(got.cpu().numpy(), want)
+        assert errs[nm] <= P.REL_TOL, (nm, errs[nm])
+    g2 = dfl.anchor_attention_bwd(d["q"], d["k_ctx"], d["v_ctx"], d["k_blk"], d["v_blk"], a, B, out, lse, do)
+    for u, v in zip(g, g2):
+        assert torch.equal(u, v)
+    print(f"[training] {name}: out {e_out:.2e} lse {e_lse:.2e} "
+          + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
+
+
+@pytest.mark.parametrize("V", [1000, 1003])
+def test_weighted_ce_matches_oracle(V):
+    B, n = 16, 6
+    rng = np.random.default_rng(3)
+    z = (3.0 * rng.standard_normal((n * B, V))).astype(np.float32)
+    y = rng.integers(0, V, size=n * B).astype(np.int32)
+    y[rng.random(n * B) < 0.1] = -1
+    gamma = 4.5
+    loss, ce, dz = dfl.weighted_ce(torch.from_numpy(z).cuda(), torch.from_numpy(y).cuda(), B, gamma)
+    rloss, rce, rdz = tr.weighted_ce(z.astype(np.float64), y, B, gamma)
+    assert abs(float(loss.cpu()[0]) - rloss) <= 1e-5 * max(1.0, abs(rloss))
+    assert P.relinf(ce.cpu().numpy(), rce) <= 1e-5
+    assert P.relinf(dz.cpu().numpy(), rdz) <= 1e-5
+    with pytest.raises(dfl.DFlareError):
+        dfl.weighted_ce(torch.from_numpy(z[:17]).cuda(), torch.from_numpy(y[:17]).cuda(), B, gamma)
