@@ -32,7 +32,7 @@ constexpr int kChunkBlocks = 64;  // blocks per partial of the context-key gradi
 
 struct AttnShapeT {
   int n_blocks, B, T, n_q, n_kv, hd;
-  int G, R, Rp, Tp, Mp;  // heads per group, rows per (block, group), padded rows / keys
+  int G, R, Rp, Tp, Mp;  // heads per group, rows per (block, group), padded rows / context keys / block keys
 };
 
 struct AttnT {
@@ -40,7 +40,7 @@ struct AttnT {
   const uint16_t *q, *kc, *vc, *kb, *vb;  // bf16 inputs
   const int32_t* anchors;
   // workspace (bf16 transposed copies, fp32 partials)
-  uint16_t *kct, *vct, *kbt, *vbt;  // [n_kv][hd][Tp] / [n_kv][hd][Mp]
+  uint16_t *kct, *vct, *kbt, *vbt;  // [n_kv][hd][Tp] / [n_kv][hd][n_blocks * 32]
   uint16_t *qt, *dot, *dob;         // [n_kv][n_blocks][hd][Rp] x2, [M][n_q][hd]
   float* dsum;                      // [M][n_q] rowsum(dO * O)
   float* part;                      // [nch][T][n_kv][hd] x2 (dK, dV)
@@ -84,6 +84,17 @@ __global__ __launch_bounds__(256) void k_tr_kv_t(const uint16_t* src, int nrows,
   }
 }
 
+// block keys src [n_blocks*B][n_kv][hd] -> dst [n_kv][hd][n_blocks*32]: block i's keys at
+// i*32 + j (j < B), zeros for j >= B, so that every 16-byte piece of a block is aligned
+__global__ __launch_bounds__(256) void k_tr_blk_t(const uint16_t* src, int n_blocks, int B, int cols, uint16_t* dst) {
+  const int i = blockIdx.x;
+  const long ld = (long)n_blocks * 32;
+  for (int e = threadIdx.x; e < cols * 32; e += blockDim.x) {
+    const int c = e / 32, j = e % 32;
+    dst[(long)c * ld + (long)i * 32 + j] = j < B ? src[((long)i * B + j) * cols + c] : (uint16_t)0;
+  }
+}
+
 // x [M][n_q][hd] (bf16 bits, or fp32 with F32) -> dst[g][i][d][Rp]: row r of (block i, group g)
 // is block position r % B of query head g*G + r / B; zeros for r >= R
 template <bool F32>
@@ -118,10 +129,20 @@ __global__ __launch_bounds__(256) void k_tr_dout(const float* dout, const float*
   if (lane == 0) dsum[w] = acc;
 }
 
-// ---- forward and dQ: work-group (block i, KV head g), wave w takes 16-row query tiles
-// w, w + 4, ...; key tiles of 32 (the context before the anchor, then the block's own keys) ----
-template <int HD, bool DQ>
+// ---- forward and dQ: work-group (block i, KV head g); its 4 waves take the 16-row query
+// tiles w, w + 4 (TPW tiles each).  Key tiles of 32 (the context before the anchor, then the
+// block's own keys) are shared through LDS, double-buffered: LDS-direct loads fill the next
+// tile while the current one goes through the matrix cores.  Per stage: K rows (and for dQ
+// V rows), 16-byte pieces of key k in slot k*(HD/8) + (c ^ (k & 7)); and the transposed tile
+// (V^T, or K^T for dQ), piece c (8 keys) of dim row d in slot d*4 + (c ^ (d & 3)).  Keys a
+// block does not see are read from a visible row and masked in the scores.
+template <int HD, bool DQ, int TPW>
 __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
+  constexpr int PK = HD / 8;                   // 16-byte pieces of a key row
+  constexpr int KP = 32 * PK, TP = HD * 4;     // pieces of a key-row tile / of a transposed tile
+  constexpr int NP = (DQ ? 2 * KP : KP) + TP;  // pieces per stage
+  static_assert(NP % 64 == 0, "whole wave loads");
+  __shared__ u32x4 lds[2][NP];
   const AttnShapeT& s = a.s;
   const int i = blockIdx.x, g = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -131,62 +152,122 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
   const int nct = (anchor + 31) / 32;
   const float sl2 = a.scale * 1.4426950408889634f;
   const u32x4 z4 = {0u, 0u, 0u, 0u};
-  for (int t = w; t < QT; t += 4) {
-    const int r = 16 * t + col;
+  const uint16_t* tsrc_c = DQ ? a.kct : a.vct;
+  const uint16_t* tsrc_b = DQ ? a.kbt : a.vbt;
+
+  // LDS-direct loads of key tile kt into buffer bi (wave w issues wave-loads w, w + 4, ...)
+  auto stage = [&](int kt, int bi) {
+    const bool blk = kt == nct;
+    for (int ins = w; ins < NP / 64; ins += 4) {
+      const int slot = ins * 64 + lane;
+      const uint16_t* src;
+      if (slot < (DQ ? 2 * KP : KP)) {
+        const bool isv = slot >= KP;
+        const int sl = isv ? slot - KP : slot;
+        const int k = sl / PK, c = (sl % PK) ^ (k & 7);
+        long row;
+        if (blk) {
+          const int j = k < s.B ? k : 0;
+          row = ((long)(i * s.B + j) * s.n_kv + g) * HD;
+          src = (isv ? a.vb : a.kb) + row + c * 8;
+        } else {
+          const int key = kt * 32 + k < anchor ? kt * 32 + k : 0;
+          row = ((long)key * s.n_kv + g) * HD;
+          src = (isv ? a.vc : a.kc) + row + c * 8;
+        }
+      } else {
+        const int sl = slot - (DQ ? 2 * KP : KP);
+        const int d = sl / 4, c = (sl % 4) ^ (d & 3);
+        src = blk ? tsrc_b + ((long)g * HD + d) * s.Mp + (long)i * 32 + c * 8
+                  : tsrc_c + ((long)g * HD + d) * s.Tp + (long)kt * 32 + c * 8;
+      }
+      __builtin_amdgcn_global_load_lds(src, (LDSP char*)(char*)&lds[bi][ins * 64], 16, 0, 0);
+    }
+  };
+
+  // per query tile of this wave: Q (and dO) fragments, softmax state, accumulators
+  u32x4 qf[TPW][HD / 32], df[TPW][HD / 32];
+  float m[TPW], l[TPW], lse2[TPW], dr[TPW];
+  f32x4 o[TPW][HD / 16];
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) {
+    const int r = 16 * (w + 4 * tt) + col;
     const bool rv = r < s.R;
     const int h = g * s.G + (rv ? r / s.B : 0), b = rv ? r % s.B : 0;
     const long qrow = ((long)(i * s.B + b) * s.n_q + h) * HD;
-    u32x4 qf[HD / 32], df[HD / 32];
 #pragma unroll
     for (int ks = 0; ks < HD / 32; ++ks) {
-      qf[ks] = rv ? ld16(a.q + qrow + ks * 32 + 8 * q4) : z4;
-      if constexpr (DQ) df[ks] = rv ? ld16(a.dob + qrow + ks * 32 + 8 * q4) : z4;
+      qf[tt][ks] = rv ? ld16(a.q + qrow + ks * 32 + 8 * q4) : z4;
+      if constexpr (DQ) df[tt][ks] = rv ? ld16(a.dob + qrow + ks * 32 + 8 * q4) : z4;
     }
-    float m = -INFINITY, l = 0.f, lse2 = 0.f, dr = 0.f;
+    m[tt] = -INFINITY;
+    l[tt] = 0.f;
+    lse2[tt] = dr[tt] = 0.f;
     if constexpr (DQ) {
-      lse2 = rv ? a.lse[(long)(i * s.B + b) * s.n_q + h] * 1.4426950408889634f : 0.f;
-      dr = rv ? a.dsum[(long)(i * s.B + b) * s.n_q + h] : 0.f;
+      lse2[tt] = rv ? a.lse[(long)(i * s.B + b) * s.n_q + h] * 1.4426950408889634f : 0.f;
+      dr[tt] = rv ? a.dsum[(long)(i * s.B + b) * s.n_q + h] : 0.f;
     }
-    f32x4 o[HD / 16];
 #pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt) o[dt] = zero4();
-    for (int kt = 0; kt <= nct; ++kt) {
-      const bool blk = kt == nct;
-      // rows of this lane's A operands: key 16 x + col of the tile (zeros where not visible)
-      const uint16_t* kbase = blk ? a.kb : a.kc;
-      const uint16_t* vbase = blk ? a.vb : a.vc;
-      bool ok[2];
-      long krow[2];
+    for (int dt = 0; dt < HD / 16; ++dt) o[tt][dt] = zero4();
+  }
+
+  const char* L0 = reinterpret_cast<const char*>(&lds[0][0]);
+  stage(0, 0);
+  wait_vm();
+  __syncthreads();
+  for (int kt = 0; kt <= nct; ++kt) {
+    const int bi = kt & 1;
+    if (kt < nct) stage(kt + 1, bi ^ 1);
+    const bool blk = kt == nct;
+    const char* Lb = L0 + (long)bi * NP * 16;
+    // A-operand rows of this lane: keys 16 x + col
+    u32x4 ka[2][HD / 32], va[2][HD / 32];
 #pragma unroll
-      for (int x = 0; x < 2; ++x) {
-        const int j = 16 * x + col;
-        ok[x] = blk ? j < s.B : kt * 32 + j < anchor;
-        krow[x] = ok[x] ? (blk ? ((long)(i * s.B + j) * s.n_kv + g) * HD : ((long)(kt * 32 + j) * s.n_kv + g) * HD) : 0;
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        const int k = 16 * x + col;
+        const int sl = k * PK + ((ks * 4 + q4) ^ (k & 7));
+        ka[x][ks] = *reinterpret_cast<const u32x4*>(Lb + sl * 16);
+        if constexpr (DQ) va[x][ks] = *reinterpret_cast<const u32x4*>(Lb + (KP + sl) * 16);
       }
+    // validity of this lane's result values: keys 4 q4 + e and 16 + 4 q4 + e
+    bool ok0[4], ok1[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int j0 = 4 * q4 + e, j1 = 16 + 4 * q4 + e;
+      ok0[e] = blk ? j0 < s.B : kt * 32 + j0 < anchor;
+      ok1[e] = blk ? j1 < s.B : kt * 32 + j1 < anchor;
+    }
+    // transposed operand pieces of this lane (dims 16 dt + col), read once for all its tiles
+    u32x4 tpair[HD / 16];
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) {
+      const int d = 16 * dt + col;
+      const int base = (DQ ? 2 * KP : KP) + d * 4;
+      const int c0 = (q4 >> 1) ^ (d & 3), c1 = (2 + (q4 >> 1)) ^ (d & 3);
+      const u32x2 lo = *reinterpret_cast<const u32x2*>(Lb + (base + c0) * 16 + (q4 & 1) * 8);
+      const u32x2 hi = *reinterpret_cast<const u32x2*>(Lb + (base + c1) * 16 + (q4 & 1) * 8);
+      tpair[dt] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+    }
+#pragma unroll
+    for (int tt = 0; tt < TPW; ++tt) {
+      if (w + 4 * tt >= QT) continue;
       f32x4 s0 = zero4(), s1 = zero4(), p0 = zero4(), p1 = zero4();
 #pragma unroll
       for (int ks = 0; ks < HD / 32; ++ks) {
-        const int ko = ks * 32 + 8 * q4;
-        const u32x4 a0 = ok[0] ? ld16(kbase + krow[0] + ko) : z4;
-        const u32x4 a1 = ok[1] ? ld16(kbase + krow[1] + ko) : z4;
-        s0 = mfma(a0, qf[ks], s0);
-        s1 = mfma(a1, qf[ks], s1);
+        s0 = mfma(ka[0][ks], qf[tt][ks], s0);
+        s1 = mfma(ka[1][ks], qf[tt][ks], s1);
         if constexpr (DQ) {
-          const u32x4 v0 = ok[0] ? ld16(vbase + krow[0] + ko) : z4;
-          const u32x4 v1 = ok[1] ? ld16(vbase + krow[1] + ko) : z4;
-          p0 = mfma(v0, df[ks], p0);  // dP^T
-          p1 = mfma(v1, df[ks], p1);
+          p0 = mfma(va[0][ks], df[tt][ks], p0);  // dP^T
+          p1 = mfma(va[1][ks], df[tt][ks], p1);
         }
       }
-      // this lane's values: keys 4 q4 + e (tile 0) and 16 + 4 q4 + e (tile 1) of query row col
       float x0[4], x1[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int j0 = 4 * q4 + e, j1 = 16 + 4 * q4 + e;
-        const bool ok0 = blk ? j0 < s.B : kt * 32 + j0 < anchor;
-        const bool ok1 = blk ? j1 < s.B : kt * 32 + j1 < anchor;
-        x0[e] = ok0 ? s0[e] * sl2 : -INFINITY;
-        x1[e] = ok1 ? s1[e] * sl2 : -INFINITY;
+        x0[e] = ok0[e] ? s0[e] * sl2 : -INFINITY;
+        x1[e] = ok1[e] ? s1[e] * sl2 : -INFINITY;
       }
       u32x4 pb;
       if constexpr (!DQ) {
@@ -195,8 +276,8 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
         for (int e = 0; e < 4; ++e) tm = fmaxf(tm, fmaxf(x0[e], x1[e]));
         tm = fmaxf(tm, __shfl_xor(tm, 16));
         tm = fmaxf(tm, __shfl_xor(tm, 32));
-        const float mn = fmaxf(m, tm);
-        const float corr = (mn == -INFINITY) ? 1.f : exp2f(m - mn);
+        const float mn = fmaxf(m[tt], tm);
+        const float corr = (mn == -INFINITY) ? 1.f : exp2f(m[tt] - mn);
         float ps = 0.f;
         f32x4 e0, e1;
 #pragma unroll
@@ -205,44 +286,46 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
           e1[e] = (mn == -INFINITY) ? 0.f : exp2f(x1[e] - mn);
           ps += e0[e] + e1[e];
         }
-        l = l * corr + ps;
+        l[tt] = l[tt] * corr + ps;
 #pragma unroll
-        for (int dt = 0; dt < HD / 16; ++dt) o[dt] *= corr;
-        m = mn;
+        for (int dt = 0; dt < HD / 16; ++dt) o[tt][dt] *= corr;
+        m[tt] = mn;
         pb = pack_bf8(e0, e1);
       } else {
         f32x4 d0, d1;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float pp0 = exp2f(x0[e] - lse2), pp1 = exp2f(x1[e] - lse2);
-          d0[e] = pp0 * (p0[e] - dr);
-          d1[e] = pp1 * (p1[e] - dr);
+          d0[e] = exp2f(x0[e] - lse2[tt]) * (p0[e] - dr[tt]);
+          d1[e] = exp2f(x1[e] - lse2[tt]) * (p1[e] - dr[tt]);
         }
         pb = pack_bf8(d0, d1);
       }
-      // O^T += V^T P^T (forward) or dQ^T += K^T dS^T: A rows = dims d = 16 dt + col
+      // O^T += V^T P^T (forward) or dQ^T += K^T dS^T
 #pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) {
-        const int d = 16 * dt + col;
-        const uint16_t* src = DQ ? (blk ? a.kbt : a.kct) : (blk ? a.vbt : a.vct);
-        const long base = blk ? ((long)g * HD + d) * s.Mp + (long)i * s.B : ((long)g * HD + d) * s.Tp + kt * 32;
-        o[dt] = mfma(ld_pair(src + base + 4 * q4), pb, o[dt]);
-      }
+      for (int dt = 0; dt < HD / 16; ++dt) o[tt][dt] = mfma(tpair[dt], pb, o[tt][dt]);
     }
-    if (!rv) continue;
+    wait_vm();
+    __syncthreads();
+  }
+#pragma unroll
+  for (int tt = 0; tt < TPW; ++tt) {
+    const int r = 16 * (w + 4 * tt) + col;
+    if (w + 4 * tt >= QT || r >= s.R) continue;
+    const int h = g * s.G + r / s.B, b = r % s.B;
+    const long qrow = ((long)(i * s.B + b) * s.n_q + h) * HD;
     float out_scale;
     if constexpr (!DQ) {
-      l += __shfl_xor(l, 16);
-      l += __shfl_xor(l, 32);
-      out_scale = 1.f / l;
-      if (q4 == 0) a.lse[(long)(i * s.B + b) * s.n_q + h] = (m + log2f(l)) * 0.6931471805599453f;
+      float lt = l[tt];
+      lt += __shfl_xor(lt, 16);
+      lt += __shfl_xor(lt, 32);
+      out_scale = 1.f / lt;
+      if (q4 == 0) a.lse[(long)(i * s.B + b) * s.n_q + h] = (m[tt] + log2f(lt)) * 0.6931471805599453f;
     } else {
       out_scale = a.scale;
     }
     float* dst = (DQ ? a.dq : a.out) + qrow;
 #pragma unroll
-    for (int dt = 0; dt < HD / 16; ++dt)
-      *reinterpret_cast<f32x4*>(dst + 16 * dt + 4 * q4) = o[dt] * out_scale;
+    for (int dt = 0; dt < HD / 16; ++dt) *reinterpret_cast<f32x4*>(dst + 16 * dt + 4 * q4) = o[tt][dt] * out_scale;
   }
 }
 
@@ -513,7 +596,7 @@ static AttnShapeT att_shape(int n_blocks, int B, int T, int n_q, int n_kv, int h
   s.R = s.G * B;
   s.Rp = (s.R + 31) / 32 * 32;
   s.Tp = (T + 31) / 32 * 32 + 32;
-  s.Mp = n_blocks * B + 32;
+  s.Mp = n_blocks * 32;
   return s;
 }
 
@@ -615,9 +698,12 @@ int dflare_anchor_attention_fwd(const void* q, const void* k_ctx, const void* v_
   const int cols = n_kv * hd;
   const uint16_t* zero_src = a.kb;  // with T = 0 the context copies are all zeros
   transpose_kv(st, T > 0 ? a.vc : zero_src, T, cols, s.Tp, a.vct);
-  transpose_kv(st, a.vb, n_blocks * B, cols, s.Mp, a.vbt);
+  hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks), dim3(256), 0, st, a.vb, n_blocks, B, cols, a.vbt);
+  const bool two = (s.R + 15) / 16 > 4;
   by_hd(hd, [&](auto h) {
-    hipLaunchKernelGGL((k_aatt_rows<decltype(h)::value, false>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
+    constexpr int HD = decltype(h)::value;
+    if (two) hipLaunchKernelGGL((k_aatt_rows<HD, false, 2>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
+    else hipLaunchKernelGGL((k_aatt_rows<HD, false, 1>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
   });
   return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
 }
@@ -648,13 +734,14 @@ int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_
   const int M = n_blocks * B;
   const uint16_t* zero_src = a.kb;
   transpose_kv(st, T > 0 ? a.kc : zero_src, T, cols, s.Tp, a.kct);
-  transpose_kv(st, a.kb, M, cols, s.Mp, a.kbt);
+  hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks), dim3(256), 0, st, a.kb, n_blocks, B, cols, a.kbt);
   hipLaunchKernelGGL((k_tr_group_t<false>), dim3(n_blocks, n_kv), dim3(256), 0, st, (const void*)q, s, a.qt);
   hipLaunchKernelGGL((k_tr_group_t<true>), dim3(n_blocks, n_kv), dim3(256), 0, st, (const void*)dout, s, a.dot);
   hipLaunchKernelGGL(k_tr_dout, dim3((M * n_q + 3) / 4), dim3(256), 0, st, dout, out, M * n_q, hd, a.dob, a.dsum);
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
-    hipLaunchKernelGGL((k_aatt_rows<HD, true>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
+    if ((s.R + 15) / 16 > 4) hipLaunchKernelGGL((k_aatt_rows<HD, true, 2>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
+    else hipLaunchKernelGGL((k_aatt_rows<HD, true, 1>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
     hipLaunchKernelGGL((k_aatt_kv<HD, true>), dim3(n_blocks, n_kv, 1), dim3(kTrT), 0, st, a);
     if (T > 0) hipLaunchKernelGGL((k_aatt_kv<HD, false>), dim3((T + 31) / 32, n_kv, a.nch), dim3(kTrT), 0, st, a);
   });
