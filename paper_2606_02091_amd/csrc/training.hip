@@ -329,10 +329,10 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
   }
 }
 
-// ---- dK, dV: work-group (32-key tile or one block's keys, KV head g, chunk of blocks);
-// wave w takes the blocks (context keys) or 32-row pairs (block keys) w, w + 4, ... ----
-template <int HD, bool BLK>
-__global__ __launch_bounds__(kTrT) void k_aatt_kv(AttnT a) {
+// ---- block-key dK, dV: work-group (block ib, KV head g); wave w takes the block's 32-row
+// pairs w, w + 4, ... and the 4 waves' sums are added in wave order ----
+template <int HD>
+__global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
   const AttnShapeT& s = a.s;
   const int g = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -340,10 +340,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kv(AttnT a) {
   const float sl2 = a.scale * 1.4426950408889634f;
   const int NP = s.Rp / 32;  // 32-row pairs of a (block, group)
   const u32x4 z4 = {0u, 0u, 0u, 0u};
-  // keys of this work-group: context tile kt (keys 32 kt + 0..31) or block ib's B keys
-  const int kt = BLK ? 0 : blockIdx.x, ib = BLK ? blockIdx.x : 0;
-  const int i0 = BLK ? ib : blockIdx.z * kChunkBlocks;
-  const int i1 = BLK ? ib + 1 : min(s.n_blocks, i0 + kChunkBlocks);
+  const int ib = blockIdx.x;
   f32x4 dk[HD / 16][2], dv[HD / 16][2];
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt)
@@ -354,22 +351,18 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kv(AttnT a) {
 #pragma unroll
   for (int x = 0; x < 2; ++x) {
     const int j = 16 * x + col;
-    const bool ok = BLK ? j < s.B : kt * 32 + j < s.T;
-    const long row = !ok ? 0 : BLK ? ((long)(ib * s.B + j) * s.n_kv + g) * HD : ((long)(kt * 32 + j) * s.n_kv + g) * HD;
-    const uint16_t* kp = (BLK ? a.kb : a.kc) + row;
-    const uint16_t* vp = (BLK ? a.vb : a.vc) + row;
+    const bool ok = j < s.B;
+    const long row = ok ? ((long)(ib * s.B + j) * s.n_kv + g) * HD : 0;
+    const uint16_t* kp = a.kb + row;
+    const uint16_t* vp = a.vb + row;
 #pragma unroll
     for (int ks = 0; ks < HD / 32; ++ks) {
       kf[x][ks] = ok ? ld16(kp + ks * 32 + 8 * q4) : z4;
       vf[x][ks] = ok ? ld16(vp + ks * 32 + 8 * q4) : z4;
     }
   }
-  // units of work: (block, row pair); wave w takes units w, w + 4, ...
-  const int units = (i1 - i0) * NP;
-  for (int u = w; u < units; u += 4) {
-    const int i = i0 + u / NP, pr = u % NP;
-    const int anchor = min(max(a.anchors[i], 0), s.T);
-    if (!BLK && anchor <= kt * 32) continue;  // no key of the tile is visible to block i
+  const int i = ib;
+  for (int pr = w; pr < NP; pr += 4) {
     // S = Q K^T and dP = dO V^T for rows 32 pr + 16 y + (4 q4 + e) (y = 0, 1), keys 16x + col
     f32x4 sc[2][2], dp[2][2];
 #pragma unroll
@@ -406,7 +399,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kv(AttnT a) {
 #pragma unroll
         for (int x = 0; x < 2; ++x) {
           const int j = 16 * x + col;
-          const bool ok = rv && (BLK ? j < s.B : kt * 32 + j < anchor);
+          const bool ok = rv && j < s.B;
           const float p = ok ? exp2f(sc[y][x][e] * sl2 - lse2) : 0.f;
           P[y][x][e] = p;
           dS[y][x][e] = p * (dp[y][x][e] - dr);
@@ -430,8 +423,6 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kv(AttnT a) {
   // sum the 4 waves' tiles in wave order through LDS, 8 tiles per round
   __shared__ f32x4 red[3][8][64];
   constexpr int NT = HD / 16 * 2 * 2;  // tiles per wave (dK, dV)
-  float* outk = BLK ? a.dkb : a.part + (long)blockIdx.z * s.T * s.n_kv * HD;
-  float* outv = BLK ? a.dvb : a.part + ((long)a.nch + blockIdx.z) * s.T * s.n_kv * HD;
 #pragma unroll
   for (int r0 = 0; r0 < NT; r0 += 8) {
     if (w > 0) {
@@ -454,15 +445,177 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kv(AttnT a) {
         if (kind == 0) v *= a.scale;
         // tile (dims 16 dt + 4 q4 + e, key 16 x + col)
         const int j = 16 * x + col;
-        const bool ok = BLK ? j < s.B : kt * 32 + j < s.T;
-        if (ok) {
-          const long row = BLK ? (long)(ib * s.B + j) : (long)(kt * 32 + j);
-          float* dst = (kind == 0 ? outk : outv) + (row * s.n_kv + g) * HD + 16 * dt + 4 * q4;
+        if (j < s.B) {
+          const long row = (long)(ib * s.B + j);
+          float* dst = (kind == 0 ? a.dkb : a.dvb) + (row * s.n_kv + g) * HD + 16 * dt + 4 * q4;
           *reinterpret_cast<f32x4*>(dst) = v;
         }
       }
     }
     __syncthreads();
+  }
+}
+
+// ---- context dK, dV: work-group (64-key tile kt, KV head g, chunk z of 64 blocks); wave w
+// owns keys 64 kt + 16 w + (0..15) (its K and V rows held as operand fragments).  The
+// waves walk the chunk's (block, 32-row pair) units together: each unit's Q rows, dO rows,
+// Q^T and dO^T tiles go through swizzled LDS, double-buffered with LDS-direct loads one unit
+// ahead; per unit a wave forms S = Q K^T and dP = dO V^T for its keys and accumulates
+// dV^T += dO^T P and dK^T += Q^T dS.  Writes this chunk's partial dK, dV. ----
+template <int HD>
+__global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
+  constexpr int PK = HD / 8;                  // 16-byte pieces of a row
+  constexpr int RP = 32 * PK, TP = HD * 4;    // pieces of a 32-row tile / of a transposed tile
+  constexpr int NPc = 2 * RP + 2 * TP;        // Q, dO, Q^T, dO^T
+  static_assert(NPc % 64 == 0, "whole wave loads");
+  __shared__ u32x4 lds[2][NPc];
+  const AttnShapeT& s = a.s;
+  const int kt = blockIdx.x, g = blockIdx.y, z = blockIdx.z;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int col = lane & 15, q4 = lane >> 4;
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const u32x4 z4 = {0u, 0u, 0u, 0u};
+  const int NPr = s.Rp / 32;
+  const int i0 = z * kChunkBlocks, i1 = min(s.n_blocks, i0 + kChunkBlocks);
+  const int key0 = kt * 64;  // first key of the work-group
+  // this wave's key rows as B operands (key 16 w + col)
+  const int myk = key0 + 16 * w + col;
+  const bool kok = myk < s.T;
+  u32x4 kf[HD / 32], vf[HD / 32];
+  {
+    const long row = kok ? ((long)myk * s.n_kv + g) * HD : 0;
+#pragma unroll
+    for (int ks = 0; ks < HD / 32; ++ks) {
+      kf[ks] = kok ? ld16(a.kc + row + ks * 32 + 8 * q4) : z4;
+      vf[ks] = kok ? ld16(a.vc + row + ks * 32 + 8 * q4) : z4;
+    }
+  }
+  f32x4 dk[HD / 16], dv[HD / 16];
+#pragma unroll
+  for (int dt = 0; dt < HD / 16; ++dt) dk[dt] = dv[dt] = zero4();
+
+  // the next unit (block, pair) at or after u whose block sees a key of this tile
+  auto next_unit = [&](int u) {
+    for (; u < (i1 - i0) * NPr; ++u) {
+      const int i = i0 + u / NPr;
+      if (min(max(a.anchors[i], 0), s.T) > key0) return u;
+      u = (u / NPr) * NPr + NPr - 1;  // skip the rest of this block's pairs
+    }
+    return -1;
+  };
+  auto stage = [&](int u, int bi) {
+    const int i = i0 + u / NPr, pr = u % NPr;
+    for (int ins = w; ins < NPc / 64; ins += 4) {
+      const int slot = ins * 64 + lane;
+      const uint16_t* src;
+      if (slot < 2 * RP) {  // Q rows, then dO rows: row rr of the pair, piece c
+        const bool isd = slot >= RP;
+        const int sl = isd ? slot - RP : slot;
+        const int rr = sl / PK, c = (sl % PK) ^ (rr & 7);
+        int r = 32 * pr + rr;
+        if (r >= s.R) r = 0;
+        const long qrow = ((long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B) * HD;
+        src = (isd ? a.dob : a.q) + qrow + c * 8;
+      } else {  // Q^T, then dO^T: dim row d, piece c (8 rows)
+        const int sl0 = slot - 2 * RP;
+        const bool isd = sl0 >= TP;
+        const int sl = isd ? sl0 - TP : sl0;
+        const int d = sl / 4, c = (sl % 4) ^ (d & 3);
+        src = (isd ? a.dot : a.qt) + (((long)g * s.n_blocks + i) * HD + d) * s.Rp + 32 * pr + c * 8;
+      }
+      __builtin_amdgcn_global_load_lds(src, (LDSP char*)(char*)&lds[bi][ins * 64], 16, 0, 0);
+    }
+  };
+  // log2-domain lse and rowsum(dO O) of this lane's result rows: 32 pr + 16 y + 4 q4 + e
+  auto row_stats = [&](int u, float* l2, float* dr) {
+    const int i = i0 + u / NPr, pr = u % NPr;
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 32 * pr + 16 * y + 4 * q4 + e;
+        const bool rv = r < s.R;
+        const long rh = rv ? (long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B : 0;
+        l2[y * 4 + e] = rv ? a.lse[rh] * 1.4426950408889634f : INFINITY;  // +inf: P = 0
+        dr[y * 4 + e] = rv ? a.dsum[rh] : 0.f;
+      }
+  };
+
+  const char* L0 = reinterpret_cast<const char*>(&lds[0][0]);
+  int u = next_unit(0);
+  float cl[8], cd[8], nl[8], nd[8];
+  if (u >= 0) {
+    stage(u, 0);
+    row_stats(u, cl, cd);
+  }
+  wait_vm();
+  __syncthreads();
+  int bi = 0;
+  while (u >= 0) {
+    const int un = next_unit(u + 1);
+    if (un >= 0) {
+      stage(un, bi ^ 1);
+      row_stats(un, nl, nd);
+    }
+    const int i = i0 + u / NPr;
+    const int anchor = min(max(a.anchors[i], 0), s.T);
+    const bool vis = myk < anchor;  // this lane's key (column of every result tile)
+    const char* Lb = L0 + (long)bi * NPc * 16;
+    // S = Q K^T, dP = dO V^T: A rows = pair rows 16 y + col
+    f32x4 sc[2], dp[2];
+#pragma unroll
+    for (int y = 0; y < 2; ++y) {
+      sc[y] = dp[y] = zero4();
+      const int rr = 16 * y + col;
+#pragma unroll
+      for (int ks = 0; ks < HD / 32; ++ks) {
+        const int sl = rr * PK + ((ks * 4 + q4) ^ (rr & 7));
+        const u32x4 qa = *reinterpret_cast<const u32x4*>(Lb + sl * 16);
+        const u32x4 da = *reinterpret_cast<const u32x4*>(Lb + (RP + sl) * 16);
+        sc[y] = mfma(qa, kf[ks], sc[y]);
+        dp[y] = mfma(da, vf[ks], dp[y]);
+      }
+    }
+    f32x4 P[2], dS[2];
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p = vis ? exp2f(sc[y][e] * sl2 - cl[y * 4 + e]) : 0.f;
+        P[y][e] = p;
+        dS[y][e] = p * (dp[y][e] - cd[y * 4 + e]);
+      }
+    const u32x4 pb = pack_bf8(P[0], P[1]), sb = pack_bf8(dS[0], dS[1]);
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) {
+      const int d = 16 * dt + col;
+      const int c0 = (q4 >> 1) ^ (d & 3), c1 = (2 + (q4 >> 1)) ^ (d & 3);
+      const int bq = 2 * RP + d * 4, bd = 2 * RP + TP + d * 4;
+      const u32x2 q0 = *reinterpret_cast<const u32x2*>(Lb + (bq + c0) * 16 + (q4 & 1) * 8);
+      const u32x2 q1 = *reinterpret_cast<const u32x2*>(Lb + (bq + c1) * 16 + (q4 & 1) * 8);
+      const u32x2 o0 = *reinterpret_cast<const u32x2*>(Lb + (bd + c0) * 16 + (q4 & 1) * 8);
+      const u32x2 o1 = *reinterpret_cast<const u32x2*>(Lb + (bd + c1) * 16 + (q4 & 1) * 8);
+      dv[dt] = mfma(u32x4{o0[0], o0[1], o1[0], o1[1]}, pb, dv[dt]);
+      dk[dt] = mfma(u32x4{q0[0], q0[1], q1[0], q1[1]}, sb, dk[dt]);
+    }
+    wait_vm();
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      cl[e] = nl[e];
+      cd[e] = nd[e];
+    }
+    u = un;
+    bi ^= 1;
+  }
+  if (kok) {
+    float* pk = a.part + (((long)z * s.T + myk) * s.n_kv + g) * HD;
+    float* pv = a.part + ((((long)a.nch + z) * s.T + myk) * s.n_kv + g) * HD;
+#pragma unroll
+    for (int dt = 0; dt < HD / 16; ++dt) {
+      *reinterpret_cast<f32x4*>(pk + 16 * dt + 4 * q4) = dk[dt] * a.scale;
+      *reinterpret_cast<f32x4*>(pv + 16 * dt + 4 * q4) = dv[dt];
+    }
   }
 }
 
@@ -742,8 +895,8 @@ int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_
     constexpr int HD = decltype(h)::value;
     if ((s.R + 15) / 16 > 4) hipLaunchKernelGGL((k_aatt_rows<HD, true, 2>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
     else hipLaunchKernelGGL((k_aatt_rows<HD, true, 1>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
-    hipLaunchKernelGGL((k_aatt_kv<HD, true>), dim3(n_blocks, n_kv, 1), dim3(kTrT), 0, st, a);
-    if (T > 0) hipLaunchKernelGGL((k_aatt_kv<HD, false>), dim3((T + 31) / 32, n_kv, a.nch), dim3(kTrT), 0, st, a);
+    hipLaunchKernelGGL((k_aatt_kvb<HD>), dim3(n_blocks, n_kv, 1), dim3(kTrT), 0, st, a);
+    if (T > 0) hipLaunchKernelGGL((k_aatt_kvc<HD>), dim3((T + 63) / 64, n_kv, a.nch), dim3(kTrT), 0, st, a);
   });
   if (T > 0) {
     const long n = (long)T * n_kv * hd;
