@@ -42,6 +42,8 @@ struct AttnT {
   // workspace (bf16 transposed copies, fp32 partials)
   uint16_t *kct, *vct, *kbt, *vbt;  // [n_kv][hd][Tp] / [n_kv][hd][n_blocks * 32]
   uint16_t *qt, *dot, *dob;         // [n_kv][n_blocks][hd][Rp] x2, [M][n_q][hd]
+  uint16_t *qr, *dor;               // [n_kv][n_blocks][Rp][hd] x2 (rows of a (block, group))
+  float2* st;                       // [n_kv][n_blocks][Rp] (lse * log2 e, rowsum(dO O)); (+inf, 0) past R
   float* dsum;                      // [M][n_q] rowsum(dO * O)
   float* part;                      // [nch][T][n_kv][hd] x2 (dK, dV)
   int nch;
@@ -59,12 +61,28 @@ __device__ __forceinline__ u32x4 ld_pair(const uint16_t* p) {
   const u32x2 b = *reinterpret_cast<const u32x2*>(p + 16);
   return u32x4{a[0], a[1], b[0], b[1]};
 }
+// two fp32 values -> two bf16 (round to nearest even) in one word, by the packed conversion
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t cvt_bf2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
+}
 // two result tiles of a lane (4 + 4 values) as one bf16 operand (k order 0..3, then 16..19)
 __device__ __forceinline__ u32x4 pack_bf8(f32x4 x, f32x4 y) {
-  return u32x4{f2bf(x[0]) | (f2bf(x[1]) << 16), f2bf(x[2]) | (f2bf(x[3]) << 16), f2bf(y[0]) | (f2bf(y[1]) << 16),
-               f2bf(y[2]) | (f2bf(y[3]) << 16)};
+  return u32x4{cvt_bf2(x[0], x[1]), cvt_bf2(x[2], x[3]), cvt_bf2(y[0], y[1]), cvt_bf2(y[2], y[3])};
 }
+// 2^x by the hardware instruction: results below 2^-126 (far below a bf16 probability's
+// resolution) are not kept as denormals; 2^-inf = 0
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+// LDS swizzles.  Row tiles (PK 16-byte pieces per row): piece c of row k sits in slot
+// c ^ rsw(k), so that one piece of 16 consecutive rows covers all 64 banks.  Transposed tiles
+// (4 pieces of 8 keys per dim row d): piece c in slot c ^ tsw(d), the same for 16 dim rows.
+template <int PK>
+__device__ __forceinline__ int rsw(int k) {
+  return PK == 16 ? (k & 15) : ((k >> 1) & 7);
+}
+__device__ __forceinline__ int tsw(int d) { return (d >> 2) & 3; }
 
 // ---- layout helpers ------------------------------------------------------------------
 // src [rows][n_kv][hd] (bf16) -> dst [n_kv][hd][ld], zeros for rows >= nrows; block
@@ -133,8 +151,8 @@ __global__ __launch_bounds__(256) void k_tr_dout(const float* dout, const float*
 // tiles w, w + 4 (TPW tiles each).  Key tiles of 32 (the context before the anchor, then the
 // block's own keys) are shared through LDS, double-buffered: LDS-direct loads fill the next
 // tile while the current one goes through the matrix cores.  Per stage: K rows (and for dQ
-// V rows), 16-byte pieces of key k in slot k*(HD/8) + (c ^ (k & 7)); and the transposed tile
-// (V^T, or K^T for dQ), piece c (8 keys) of dim row d in slot d*4 + (c ^ (d & 3)).  Keys a
+// V rows), 16-byte pieces of key k in slot k*(HD/8) + (c ^ rsw(k)); and the transposed tile
+// (V^T, or K^T for dQ), piece c (8 keys) of dim row d in slot d*4 + (c ^ tsw(d)).  Keys a
 // block does not see are read from a visible row and masked in the scores.
 template <int HD, bool DQ, int TPW>
 __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
@@ -164,7 +182,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
       if (slot < (DQ ? 2 * KP : KP)) {
         const bool isv = slot >= KP;
         const int sl = isv ? slot - KP : slot;
-        const int k = sl / PK, c = (sl % PK) ^ (k & 7);
+        const int k = sl / PK, c = (sl % PK) ^ rsw<PK>(k);
         long row;
         if (blk) {
           const int j = k < s.B ? k : 0;
@@ -177,7 +195,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
         }
       } else {
         const int sl = slot - (DQ ? 2 * KP : KP);
-        const int d = sl / 4, c = (sl % 4) ^ (d & 3);
+        const int d = sl / 4, c = (sl % 4) ^ tsw(d);
         src = blk ? tsrc_b + ((long)g * HD + d) * s.Mp + (long)i * 32 + c * 8
                   : tsrc_c + ((long)g * HD + d) * s.Tp + (long)kt * 32 + c * 8;
       }
@@ -227,7 +245,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
 #pragma unroll
       for (int ks = 0; ks < HD / 32; ++ks) {
         const int k = 16 * x + col;
-        const int sl = k * PK + ((ks * 4 + q4) ^ (k & 7));
+        const int sl = k * PK + ((ks * 4 + q4) ^ rsw<PK>(k));
         ka[x][ks] = *reinterpret_cast<const u32x4*>(Lb + sl * 16);
         if constexpr (DQ) va[x][ks] = *reinterpret_cast<const u32x4*>(Lb + (KP + sl) * 16);
       }
@@ -245,7 +263,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
     for (int dt = 0; dt < HD / 16; ++dt) {
       const int d = 16 * dt + col;
       const int base = (DQ ? 2 * KP : KP) + d * 4;
-      const int c0 = (q4 >> 1) ^ (d & 3), c1 = (2 + (q4 >> 1)) ^ (d & 3);
+      const int c0 = (q4 >> 1) ^ tsw(d), c1 = (2 + (q4 >> 1)) ^ tsw(d);
       const u32x2 lo = *reinterpret_cast<const u32x2*>(Lb + (base + c0) * 16 + (q4 & 1) * 8);
       const u32x2 hi = *reinterpret_cast<const u32x2*>(Lb + (base + c1) * 16 + (q4 & 1) * 8);
       tpair[dt] = u32x4{lo[0], lo[1], hi[0], hi[1]};
@@ -277,13 +295,13 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
         tm = fmaxf(tm, __shfl_xor(tm, 16));
         tm = fmaxf(tm, __shfl_xor(tm, 32));
         const float mn = fmaxf(m[tt], tm);
-        const float corr = (mn == -INFINITY) ? 1.f : exp2f(m[tt] - mn);
+        const float corr = (mn == -INFINITY) ? 1.f : ex2(m[tt] - mn);
         float ps = 0.f;
         f32x4 e0, e1;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          e0[e] = (mn == -INFINITY) ? 0.f : exp2f(x0[e] - mn);
-          e1[e] = (mn == -INFINITY) ? 0.f : exp2f(x1[e] - mn);
+          e0[e] = (mn == -INFINITY) ? 0.f : ex2(x0[e] - mn);
+          e1[e] = (mn == -INFINITY) ? 0.f : ex2(x1[e] - mn);
           ps += e0[e] + e1[e];
         }
         l[tt] = l[tt] * corr + ps;
@@ -295,8 +313,8 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
         f32x4 d0, d1;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          d0[e] = exp2f(x0[e] - lse2[tt]) * (p0[e] - dr[tt]);
-          d1[e] = exp2f(x1[e] - lse2[tt]) * (p1[e] - dr[tt]);
+          d0[e] = ex2(x0[e] - lse2[tt]) * (p0[e] - dr[tt]);
+          d1[e] = ex2(x1[e] - lse2[tt]) * (p1[e] - dr[tt]);
         }
         pb = pack_bf8(d0, d1);
       }
@@ -400,7 +418,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
         for (int x = 0; x < 2; ++x) {
           const int j = 16 * x + col;
           const bool ok = rv && j < s.B;
-          const float p = ok ? exp2f(sc[y][x][e] * sl2 - lse2) : 0.f;
+          const float p = ok ? ex2(sc[y][x][e] * sl2 - lse2) : 0.f;
           P[y][x][e] = p;
           dS[y][x][e] = p * (dp[y][x][e] - dr);
         }
@@ -456,29 +474,68 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
   }
 }
 
+// Q and dO rows of every (block, group) in row order -> qr, dor [g][i][Rp][hd] (zeros past R),
+// and per row (lse * log2 e, rowsum(dO O)) -> st [g][i][Rp], (+inf, 0) past R
+__global__ __launch_bounds__(256) void k_grp_rows(const uint16_t* q, const uint16_t* dob, const float* lse,
+                                                   const float* dsum, AttnShapeT s, uint16_t* qr, uint16_t* dor,
+                                                   float2* st) {
+  const int i = blockIdx.x, g = blockIdx.y;
+  const int PK = s.hd / 8;
+  const long tile = ((long)g * s.n_blocks + i) * s.Rp;
+  const u32x4 z4 = {0u, 0u, 0u, 0u};
+  for (int e = threadIdx.x; e < s.Rp * PK; e += blockDim.x) {
+    const int r = e / PK, c = e % PK;
+    u32x4 vq = z4, vd = z4;
+    if (r < s.R) {
+      const long src = ((long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B) * s.hd + c * 8;
+      vq = ld16(q + src);
+      vd = ld16(dob + src);
+    }
+    const long dst = (tile + r) * s.hd + c * 8;
+    *reinterpret_cast<u32x4*>(qr + dst) = vq;
+    *reinterpret_cast<u32x4*>(dor + dst) = vd;
+  }
+  for (int r = threadIdx.x; r < s.Rp; r += blockDim.x) {
+    float2 v = make_float2(INFINITY, 0.f);
+    if (r < s.R) {
+      const long rh = (long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B;
+      v = make_float2(lse[rh] * 1.4426950408889634f, dsum[rh]);
+    }
+    st[tile + r] = v;
+  }
+}
+
 // ---- context dK, dV: work-group (64-key tile kt, KV head g, chunk z of 64 blocks); wave w
 // owns keys 64 kt + 16 w + (0..15) (its K and V rows held as operand fragments).  The
 // waves walk the chunk's (block, 32-row pair) units together: each unit's Q rows, dO rows,
-// Q^T and dO^T tiles go through swizzled LDS, double-buffered with LDS-direct loads one unit
-// ahead; per unit a wave forms S = Q K^T and dP = dO V^T for its keys and accumulates
-// dV^T += dO^T P and dK^T += Q^T dS.  Writes this chunk's partial dK, dV. ----
+// Q^T and dO^T tiles (from the grouped copies) go through swizzled LDS, double-buffered with
+// LDS-direct loads one unit ahead; per unit a wave forms S = Q K^T and dP = dO V^T for its keys
+// and accumulates dV^T += dO^T P and dK^T += Q^T dS.  Writes this chunk's partial dK, dV.
+// Work-groups are numbered so that the 8 XCDs (which take work-groups round-robin) each run
+// whole (group, chunk) sets, whose units then stay in that XCD's L2. ----
 template <int HD>
 __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
   constexpr int PK = HD / 8;                  // 16-byte pieces of a row
-  constexpr int RP = 32 * PK, TP = HD * 4;    // pieces of a 32-row tile / of a transposed tile
-  constexpr int NPc = 2 * RP + 2 * TP;        // Q, dO, Q^T, dO^T
-  static_assert(NPc % 64 == 0, "whole wave loads");
+  constexpr int RW = HD / 16;                 // wave-loads of one 32-row (or transposed) tile
+  constexpr int PW = RW / 4;                  // of them per wave
+  constexpr int NPc = 4 * RW * 64;            // Q, dO, Q^T, dO^T
   __shared__ u32x4 lds[2][NPc];
   const AttnShapeT& s = a.s;
-  const int kt = blockIdx.x, g = blockIdx.y, z = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = lane & 15, q4 = lane >> 4;
+  // work-group -> (kt, g, z)
+  const int nkt = gridDim.x;
+  const int N = nkt * gridDim.y * gridDim.z;
+  const int n = blockIdx.x + nkt * (blockIdx.y + gridDim.y * blockIdx.z);
+  const int xq = N / 8, xr = N % 8, x8 = n % 8;
+  const int lg = x8 * xq + min(x8, xr) + n / 8;
+  const int kt = lg % nkt, g = (lg / nkt) % s.n_kv, z = lg / (nkt * s.n_kv);
+
   const float sl2 = a.scale * 1.4426950408889634f;
   const u32x4 z4 = {0u, 0u, 0u, 0u};
   const int NPr = s.Rp / 32;
   const int i0 = z * kChunkBlocks, i1 = min(s.n_blocks, i0 + kChunkBlocks);
-  const int key0 = kt * 64;  // first key of the work-group
-  // this wave's key rows as B operands (key 16 w + col)
+  const int key0 = kt * 64;
   const int myk = key0 + 16 * w + col;
   const bool kok = myk < s.T;
   u32x4 kf[HD / 32], vf[HD / 32];
@@ -494,7 +551,16 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt) dk[dt] = dv[dt] = zero4();
 
-  // the next unit (block, pair) at or after u whose block sees a key of this tile
+  // this lane's source offsets of its wave-loads t of a tile (same for every unit): row tiles
+  // (32 rows x HD, row-major) and transposed tiles (HD dim rows x Rp)
+  int roff[PW], toff[PW];
+#pragma unroll
+  for (int t = 0; t < PW; ++t) {
+    const int sl = (w + 4 * t) * 64 + lane;
+    const int rr = sl / PK, d = sl / 4;
+    roff[t] = rr * HD + ((sl % PK) ^ rsw<PK>(rr)) * 8;
+    toff[t] = d * s.Rp + ((sl % 4) ^ tsw(d)) * 8;
+  }
   auto next_unit = [&](int u) {
     for (; u < (i1 - i0) * NPr; ++u) {
       const int i = i0 + u / NPr;
@@ -505,48 +571,43 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
   };
   auto stage = [&](int u, int bi) {
     const int i = i0 + u / NPr, pr = u % NPr;
-    for (int ins = w; ins < NPc / 64; ins += 4) {
-      const int slot = ins * 64 + lane;
-      const uint16_t* src;
-      if (slot < 2 * RP) {  // Q rows, then dO rows: row rr of the pair, piece c
-        const bool isd = slot >= RP;
-        const int sl = isd ? slot - RP : slot;
-        const int rr = sl / PK, c = (sl % PK) ^ (rr & 7);
-        int r = 32 * pr + rr;
-        if (r >= s.R) r = 0;
-        const long qrow = ((long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B) * HD;
-        src = (isd ? a.dob : a.q) + qrow + c * 8;
-      } else {  // Q^T, then dO^T: dim row d, piece c (8 rows)
-        const int sl0 = slot - 2 * RP;
-        const bool isd = sl0 >= TP;
-        const int sl = isd ? sl0 - TP : sl0;
-        const int d = sl / 4, c = (sl % 4) ^ (d & 3);
-        src = (isd ? a.dot : a.qt) + (((long)g * s.n_blocks + i) * HD + d) * s.Rp + 32 * pr + c * 8;
-      }
-      __builtin_amdgcn_global_load_lds(src, (LDSP char*)(char*)&lds[bi][ins * 64], 16, 0, 0);
+    const long tile = (long)g * s.n_blocks + i;
+    const uint16_t* rq = a.qr + (tile * s.Rp + 32 * pr) * HD;
+    const uint16_t* rd = a.dor + (tile * s.Rp + 32 * pr) * HD;
+    const uint16_t* tq = a.qt + tile * HD * s.Rp + 32 * pr;
+    const uint16_t* td = a.dot + tile * HD * s.Rp + 32 * pr;
+#pragma unroll
+    for (int t = 0; t < PW; ++t) {
+      const int ins = w + 4 * t;
+      // (source pointers through locals: an array element inside the builtin's argument left
+      // the host-side launch stub of this kernel undefined)
+      const uint16_t* sq = rq + roff[t];
+      const uint16_t* sd = rd + roff[t];
+      const uint16_t* sqt = tq + toff[t];
+      const uint16_t* sdt = td + toff[t];
+      __builtin_amdgcn_global_load_lds(sq, (LDSP char*)(char*)&lds[bi][(0 * RW + ins) * 64], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(sd, (LDSP char*)(char*)&lds[bi][(1 * RW + ins) * 64], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(sqt, (LDSP char*)(char*)&lds[bi][(2 * RW + ins) * 64], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(sdt, (LDSP char*)(char*)&lds[bi][(3 * RW + ins) * 64], 16, 0, 0);
     }
   };
-  // log2-domain lse and rowsum(dO O) of this lane's result rows: 32 pr + 16 y + 4 q4 + e
-  auto row_stats = [&](int u, float* l2, float* dr) {
+  // (lse * log2 e, D) of this lane's result rows 32 pr + 16 y + 4 q4 + (0..3)
+  auto row_stats = [&](int u, f32x4* st4) {
     const int i = i0 + u / NPr, pr = u % NPr;
+    const float2* p = a.st + ((long)g * s.n_blocks + i) * s.Rp + 32 * pr + 4 * q4;
 #pragma unroll
-    for (int y = 0; y < 2; ++y)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = 32 * pr + 16 * y + 4 * q4 + e;
-        const bool rv = r < s.R;
-        const long rh = rv ? (long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B : 0;
-        l2[y * 4 + e] = rv ? a.lse[rh] * 1.4426950408889634f : INFINITY;  // +inf: P = 0
-        dr[y * 4 + e] = rv ? a.dsum[rh] : 0.f;
-      }
+    for (int y = 0; y < 2; ++y) {
+      st4[2 * y] = *reinterpret_cast<const f32x4*>(p + 16 * y);
+      st4[2 * y + 1] = *reinterpret_cast<const f32x4*>(p + 16 * y + 2);
+    }
   };
 
   const char* L0 = reinterpret_cast<const char*>(&lds[0][0]);
   int u = next_unit(0);
-  float cl[8], cd[8], nl[8], nd[8];
+  f32x4 cst[4], nst[4];
   if (u >= 0) {
     stage(u, 0);
-    row_stats(u, cl, cd);
+    row_stats(u, cst);
   }
   wait_vm();
   __syncthreads();
@@ -555,7 +616,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
     const int un = next_unit(u + 1);
     if (un >= 0) {
       stage(un, bi ^ 1);
-      row_stats(un, nl, nd);
+      row_stats(un, nst);
     }
     const int i = i0 + u / NPr;
     const int anchor = min(max(a.anchors[i], 0), s.T);
@@ -569,9 +630,9 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
       const int rr = 16 * y + col;
 #pragma unroll
       for (int ks = 0; ks < HD / 32; ++ks) {
-        const int sl = rr * PK + ((ks * 4 + q4) ^ (rr & 7));
+        const int sl = rr * PK + ((ks * 4 + q4) ^ rsw<PK>(rr));
         const u32x4 qa = *reinterpret_cast<const u32x4*>(Lb + sl * 16);
-        const u32x4 da = *reinterpret_cast<const u32x4*>(Lb + (RP + sl) * 16);
+        const u32x4 da = *reinterpret_cast<const u32x4*>(Lb + (RW * 64 + sl) * 16);
         sc[y] = mfma(qa, kf[ks], sc[y]);
         dp[y] = mfma(da, vf[ks], dp[y]);
       }
@@ -581,16 +642,18 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
     for (int y = 0; y < 2; ++y)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p = vis ? exp2f(sc[y][e] * sl2 - cl[y * 4 + e]) : 0.f;
+        const f32x4 sv = cst[2 * y + (e >> 1)];
+        const float l2 = sv[2 * (e & 1)], dr = sv[2 * (e & 1) + 1];
+        const float p = vis ? ex2(sc[y][e] * sl2 - l2) : 0.f;
         P[y][e] = p;
-        dS[y][e] = p * (dp[y][e] - cd[y * 4 + e]);
+        dS[y][e] = p * (dp[y][e] - dr);
       }
     const u32x4 pb = pack_bf8(P[0], P[1]), sb = pack_bf8(dS[0], dS[1]);
 #pragma unroll
     for (int dt = 0; dt < HD / 16; ++dt) {
       const int d = 16 * dt + col;
-      const int c0 = (q4 >> 1) ^ (d & 3), c1 = (2 + (q4 >> 1)) ^ (d & 3);
-      const int bq = 2 * RP + d * 4, bd = 2 * RP + TP + d * 4;
+      const int c0 = (q4 >> 1) ^ tsw(d), c1 = (2 + (q4 >> 1)) ^ tsw(d);
+      const int bq = 2 * RW * 64 + d * 4, bd = 3 * RW * 64 + d * 4;
       const u32x2 q0 = *reinterpret_cast<const u32x2*>(Lb + (bq + c0) * 16 + (q4 & 1) * 8);
       const u32x2 q1 = *reinterpret_cast<const u32x2*>(Lb + (bq + c1) * 16 + (q4 & 1) * 8);
       const u32x2 o0 = *reinterpret_cast<const u32x2*>(Lb + (bd + c0) * 16 + (q4 & 1) * 8);
@@ -601,10 +664,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
     wait_vm();
     __syncthreads();
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      cl[e] = nl[e];
-      cd[e] = nd[e];
-    }
+    for (int e = 0; e < 4; ++e) cst[e] = nst[e];
     u = un;
     bi ^= 1;
   }
@@ -761,7 +821,7 @@ static int att_check(int n_blocks, int B, int T, int n_q, int n_kv, int hd) {
 }
 
 struct WsLayout {
-  size_t kct, vct, kbt, vbt, qt, dot, dob, dsum, part, total;
+  size_t kct, vct, kbt, vbt, qt, dot, qr, dor, st, dob, dsum, part, total;
   int nch;
 };
 
@@ -779,6 +839,9 @@ static WsLayout ws_layout(const AttnShapeT& s) {
   L.vbt = o; o = al(o + blk_t);
   L.qt = o; o = al(o + grp);
   L.dot = o; o = al(o + grp);
+  L.qr = o; o = al(o + grp);
+  L.dor = o; o = al(o + grp);
+  L.st = o; o = al(o + (size_t)s.n_kv * s.n_blocks * s.Rp * 8);
   L.dob = o; o = al(o + rows * s.hd * 2);
   L.dsum = o; o = al(o + rows * 4);
   L.part = o; o = al(o + (size_t)2 * L.nch * s.T * s.n_kv * s.hd * 4);
@@ -805,6 +868,9 @@ static AttnT att_args(const AttnShapeT& s, const void* q, const void* kc, const 
   a.qt = (uint16_t*)(w + L.qt);
   a.dot = (uint16_t*)(w + L.dot);
   a.dob = (uint16_t*)(w + L.dob);
+  a.qr = (uint16_t*)(w + L.qr);
+  a.dor = (uint16_t*)(w + L.dor);
+  a.st = (float2*)(w + L.st);
   a.dsum = (float*)(w + L.dsum);
   a.part = (float*)(w + L.part);
   a.nch = L.nch;
@@ -891,6 +957,9 @@ int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_
   hipLaunchKernelGGL((k_tr_group_t<false>), dim3(n_blocks, n_kv), dim3(256), 0, st, (const void*)q, s, a.qt);
   hipLaunchKernelGGL((k_tr_group_t<true>), dim3(n_blocks, n_kv), dim3(256), 0, st, (const void*)dout, s, a.dot);
   hipLaunchKernelGGL(k_tr_dout, dim3((M * n_q + 3) / 4), dim3(256), 0, st, dout, out, M * n_q, hd, a.dob, a.dsum);
+  if (T > 0)
+    hipLaunchKernelGGL(k_grp_rows, dim3(n_blocks, n_kv), dim3(256), 0, st, a.q, (const uint16_t*)a.dob,
+                       (const float*)a.lse, (const float*)a.dsum, s, a.qr, a.dor, a.st);
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
     if ((s.R + 15) / 16 > 4) hipLaunchKernelGGL((k_aatt_rows<HD, true, 2>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
