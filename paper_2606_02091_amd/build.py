@@ -13,6 +13,9 @@ INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "libdflare.so")
 SOURCES = ["kernels.hip", "batched.hip", "runtime.hip", "training.hip"]
+# per-source flags: the training kernels keep their matrix-core accumulators in ordinary
+# vector registers (the accumulation-register form made the compiler copy them every tile)
+EXTRA_FLAGS = {"training.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 ARCH = os.environ.get("DFLARE_OFFLOAD_ARCH", "gfx950")
 
 
@@ -33,7 +36,7 @@ def build(verbose: bool = False) -> str:
               "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function"]
     for src in SOURCES:
         obj = os.path.join(LIBDIR, src.replace(".hip", ".o"))
-        cmd = [hipcc(), *common, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc(), *common, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         _run(cmd, verbose)
         objs.append(obj)
     tmp = LIB + f".tmp{os.getpid()}"

@@ -218,7 +218,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
       qf[tt][ks] = rv ? ld16(a.q + qrow + ks * 32 + 8 * q4) : z4;
       if constexpr (DQ) df[tt][ks] = rv ? ld16(a.dob + qrow + ks * 32 + 8 * q4) : z4;
     }
-    m[tt] = -INFINITY;
+    m[tt] = -1e30f;  // finite: 2^(-inf - m) = 0 for masked keys before any visible one
     l[tt] = 0.f;
     lse2[tt] = dr[tt] = 0.f;
     if constexpr (DQ) {
@@ -249,14 +249,8 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
         ka[x][ks] = *reinterpret_cast<const u32x4*>(Lb + sl * 16);
         if constexpr (DQ) va[x][ks] = *reinterpret_cast<const u32x4*>(Lb + (KP + sl) * 16);
       }
-    // validity of this lane's result values: keys 4 q4 + e and 16 + 4 q4 + e
-    bool ok0[4], ok1[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int j0 = 4 * q4 + e, j1 = 16 + 4 * q4 + e;
-      ok0[e] = blk ? j0 < s.B : kt * 32 + j0 < anchor;
-      ok1[e] = blk ? j1 < s.B : kt * 32 + j1 < anchor;
-    }
+    // every key of the tile visible (all context tiles but the last): no masking
+    const bool full = !blk && (kt + 1) * 32 <= anchor;
     // transposed operand pieces of this lane (dims 16 dt + col), read once for all its tiles
     u32x4 tpair[HD / 16];
 #pragma unroll
@@ -281,33 +275,48 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
           p1 = mfma(va[1][ks], df[tt][ks], p1);
         }
       }
+      // log2-domain scores of this lane: keys 4 q4 + e and 16 + 4 q4 + e; -inf where masked
       float x0[4], x1[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        x0[e] = ok0[e] ? s0[e] * sl2 : -INFINITY;
-        x1[e] = ok1[e] ? s1[e] * sl2 : -INFINITY;
+        x0[e] = s0[e] * sl2;
+        x1[e] = s1[e] * sl2;
+      }
+      if (!full) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j0 = 4 * q4 + e, j1 = 16 + 4 * q4 + e;
+          if (!(blk ? j0 < s.B : kt * 32 + j0 < anchor)) x0[e] = -INFINITY;
+          if (!(blk ? j1 < s.B : kt * 32 + j1 < anchor)) x1[e] = -INFINITY;
+        }
       }
       u32x4 pb;
       if constexpr (!DQ) {
-        float tm = -INFINITY;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) tm = fmaxf(tm, fmaxf(x0[e], x1[e]));
+        // the running maximum moves only when the tile's maximum exceeds it by more than 8
+        // (so unnormalised probabilities stay below 2^8); the rescale of O and l then runs
+        // for the whole wave, with factor 1 on rows that did not move
+        float tm = fmaxf(fmaxf(x0[0], x1[0]), fmaxf(x0[1], x1[1]));
+        tm = fmaxf(tm, fmaxf(fmaxf(x0[2], x1[2]), fmaxf(x0[3], x1[3])));
         tm = fmaxf(tm, __shfl_xor(tm, 16));
         tm = fmaxf(tm, __shfl_xor(tm, 32));
-        const float mn = fmaxf(m[tt], tm);
-        const float corr = (mn == -INFINITY) ? 1.f : ex2(m[tt] - mn);
+        const bool grow = tm > m[tt] + 8.f;
+        if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+          const float mn = grow ? tm : m[tt];
+          const float corr = ex2(m[tt] - mn);
+          l[tt] *= corr;
+#pragma unroll
+          for (int dt = 0; dt < HD / 16; ++dt) o[tt][dt] *= corr;
+          m[tt] = mn;
+        }
         float ps = 0.f;
         f32x4 e0, e1;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          e0[e] = (mn == -INFINITY) ? 0.f : ex2(x0[e] - mn);
-          e1[e] = (mn == -INFINITY) ? 0.f : ex2(x1[e] - mn);
+          e0[e] = ex2(x0[e] - m[tt]);
+          e1[e] = ex2(x1[e] - m[tt]);
           ps += e0[e] + e1[e];
         }
-        l[tt] = l[tt] * corr + ps;
-#pragma unroll
-        for (int dt = 0; dt < HD / 16; ++dt) o[tt][dt] *= corr;
-        m[tt] = mn;
+        l[tt] += ps;
         pb = pack_bf8(e0, e1);
       } else {
         f32x4 d0, d1;
