@@ -701,64 +701,110 @@ __global__ void k_aatt_sum(const float* part, int nch, long n, float* dk, float*
   }
 }
 
-// ---- weighted cross-entropy (Eq. 5) ----
-// per row: weight w (0 for the anchor position, b = 0, and for labels < 0, else
-// exp(-(b - 1) / gamma)), lse and CE = lse - z[label]; one work-group per row, one pass
-// with a running maximum per thread
-__global__ __launch_bounds__(256) void k_wce_rows(const float* logits, const int32_t* labels, int V, int B,
-                                                  float gamma, float* lse_out, float* w_out, float* ce_out) {
-  __shared__ float sm[4], ss[4];
-  const int row = blockIdx.x, lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const float* z = logits + (long)row * V;
-  float m = -INFINITY, sum = 0.f;
-  auto take = [&](float x) {
-    if (x > m) {
-      sum = sum * expf(m - x) + 1.f;
-      m = x;
-    } else {
-      sum += expf(x - m);
-    }
-  };
-  // 16-byte loads where the row allows them (V % 4 == 0 keeps every row 16-byte aligned)
-  const int V4 = (V % 4 == 0) ? V / 4 : 0;
-  for (int v = threadIdx.x; v < V4; v += 256) {
-    const f32x4 x = reinterpret_cast<const f32x4*>(z)[v];
-    take(x[0]);
-    take(x[1]);
-    take(x[2]);
-    take(x[3]);
+// ---- weighted CE (Eq. 5).  The row weights and 1 / sum w depend on labels and block positions
+// only and come first; then each row's log-sum-exp, CE and gradient in one work-group pass over
+// the row twice (the second read finds the row in the memory-side cache: gridDim.x rows are in
+// flight at a time); last, the loss in row order. ----
+constexpr int kCeT = 1024;       // threads of the row work-group
+constexpr int kCeRows = 256;     // rows in flight (work-groups)
+
+// w[r] = exp(-(b - 1) / gamma) for block position b = r mod B > 0 with a label in range, else 0;
+// 1 / sum w in fp64, summed in the loss kernel's order
+__global__ __launch_bounds__(256) void k_wce_weights(const int32_t* labels, int rows, int V, int B, float gamma,
+                                                     float* w, float* inv_wsum) {
+  __shared__ double sw[256];
+  double a = 0.0;
+  for (int r = threadIdx.x; r < rows; r += 256) {
+    const int b = r % B, y = labels[r];
+    const float wr = (b > 0 && y >= 0 && y < V) ? expf(-(float)(b - 1) / gamma) : 0.f;
+    w[r] = wr;
+    a += wr;
   }
-  for (int v = 4 * V4 + threadIdx.x; v < V; v += 256) take(z[v]);
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const float om = __shfl_xor(m, off), os = __shfl_xor(sum, off);
-    const float nm = fmaxf(m, om);
-    sum = (nm == -INFINITY) ? 0.f : sum * expf(m - nm) + os * expf(om - nm);
-    m = nm;
-  }
-  if (lane == 0) {
-    sm[wv] = m;
-    ss[wv] = sum;
-  }
+  sw[threadIdx.x] = a;
   __syncthreads();
-  if (threadIdx.x == 0) {
+  for (int k = 128; k > 0; k >>= 1) {
+    if ((int)threadIdx.x < k) sw[threadIdx.x] += sw[threadIdx.x + k];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) inv_wsum[0] = sw[0] > 0.0 ? (float)(1.0 / sw[0]) : 0.f;
+}
+
+// per row: lse (log2 domain: max of z log2 e, sum of 2^(z log2 e - max)), ce = lse - z[label]
+// for rows that take part, and dz = (w / sum w) (softmax(z) - onehot(label)), four values per
+// thread per step where the row allows 16-byte accesses (V % 4 == 0)
+__global__ __launch_bounds__(kCeT) void k_wce_fused(const float* logits, const int32_t* labels, int rows, int V,
+                                                    int B, const float* w, const float* inv_wsum, float* ce_out,
+                                                    float* dz) {
+  __shared__ float sm[kCeT / 64], ss[kCeT / 64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const float L2E = 1.4426950408889634f;
+  const int V4 = (V % 4 == 0) ? V / 4 : 0;
+  const float inv = inv_wsum[0];
+  for (int row = blockIdx.x; row < rows; row += gridDim.x) {
+    const float* z = logits + (long)row * V;
+    float m = -INFINITY, sum = 0.f;
+    for (int v = threadIdx.x; v < V4; v += kCeT) {
+      const f32x4 x = reinterpret_cast<const f32x4*>(z)[v];
+      const float t0 = x[0] * L2E, t1 = x[1] * L2E, t2 = x[2] * L2E, t3 = x[3] * L2E;
+      const float m4 = fmaxf(fmaxf(t0, t1), fmaxf(t2, t3));
+      if (m4 > m) {
+        sum *= ex2(m - m4);
+        m = m4;
+      }
+      sum += (ex2(t0 - m) + ex2(t1 - m)) + (ex2(t2 - m) + ex2(t3 - m));
+    }
+    for (int v = 4 * V4 + threadIdx.x; v < V; v += kCeT) {
+      const float t = z[v] * L2E;
+      if (t > m) {
+        sum *= ex2(m - t);
+        m = t;
+      }
+      sum += ex2(t - m);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float om = __shfl_xor(m, off), os = __shfl_xor(sum, off);
+      const float nm = fmaxf(m, om);
+      sum = (nm == -INFINITY) ? 0.f : sum * ex2(m - nm) + os * ex2(om - nm);
+      m = nm;
+    }
+    if (lane == 0) {
+      sm[wv] = m;
+      ss[wv] = sum;
+    }
+    __syncthreads();
     float M = sm[0], S = ss[0];
-    for (int k = 1; k < 4; ++k) {
+#pragma unroll
+    for (int k = 1; k < kCeT / 64; ++k) {
       const float nm = fmaxf(M, sm[k]);
-      S = S * expf(M - nm) + ss[k] * expf(sm[k] - nm);
+      S = S * ex2(M - nm) + ss[k] * ex2(sm[k] - nm);
       M = nm;
     }
-    const float lse = M + logf(S);
-    const int b = row % B, y = labels[row];
-    const bool on = b > 0 && y >= 0 && y < V;
-    lse_out[row] = lse;
-    w_out[row] = on ? expf(-(float)(b - 1) / gamma) : 0.f;
-    ce_out[row] = on ? lse - z[y] : 0.f;
+    __syncthreads();  // sm, ss are rewritten by the next row
+    const float lse2 = M + log2f(S);
+    const int y = labels[row];
+    const bool on = row % B > 0 && y >= 0 && y < V;
+    if (threadIdx.x == 0) ce_out[row] = on ? lse2 * 0.6931471805599453f - z[y] : 0.f;
+    const float c = w[row] * inv;
+    float* d = dz + (long)row * V;
+    const int y4 = (on && c != 0.f) ? y >> 2 : -1;
+    for (int v = threadIdx.x; v < V4; v += kCeT) {
+      f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (c != 0.f) {
+        const f32x4 x = reinterpret_cast<const f32x4*>(z)[v];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = c * ex2(fmaf(x[e], L2E, -lse2));
+        if (v == y4) o[y & 3] -= c;
+      }
+      __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(d) + v);
+    }
+    for (int v = 4 * V4 + threadIdx.x; v < V; v += kCeT)
+      d[v] = c == 0.f ? 0.f : c * ex2(fmaf(z[v], L2E, -lse2)) - (on && v == y ? c : 0.f);
   }
 }
 
-// loss = sum w ce / sum w over the rows, in row order (one work-group), and 1 / sum w
-__global__ __launch_bounds__(256) void k_wce_loss(const float* w, const float* ce, int rows, float* loss, float* inv_wsum) {
+// loss = sum w ce / sum w over the rows, in row order (one work-group)
+__global__ __launch_bounds__(256) void k_wce_loss(const float* w, const float* ce, int rows, float* loss) {
   __shared__ double sw[256], sl[256];
   double a = 0.0, c = 0.0;
   for (int r = threadIdx.x; r < rows; r += 256) {
@@ -777,29 +823,7 @@ __global__ __launch_bounds__(256) void k_wce_loss(const float* w, const float* c
   }
   if (threadIdx.x == 0) {
     loss[0] = sw[0] > 0.0 ? (float)(sl[0] / sw[0]) : 0.f;
-    inv_wsum[0] = sw[0] > 0.0 ? (float)(1.0 / sw[0]) : 0.f;
   }
-}
-
-// dz = (w / sum w) (softmax(z) - onehot(label)), four values per thread per step where the
-// row allows 16-byte accesses
-__global__ __launch_bounds__(256) void k_wce_grad(const float* logits, const int32_t* labels, const float* lse,
-                                                  const float* w, const float* inv_wsum, int V, float* dz) {
-  const int row = blockIdx.x;
-  const float c = w[row] * inv_wsum[0];
-  const float l = lse[row];
-  const int y = labels[row];
-  const float* z = logits + (long)row * V;
-  float* d = dz + (long)row * V;
-  const int V4 = (V % 4 == 0) ? V / 4 : 0;
-  for (int v = threadIdx.x; v < V4; v += 256) {
-    const f32x4 x = reinterpret_cast<const f32x4*>(z)[v];
-    f32x4 o;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = c == 0.f ? 0.f : c * (expf(x[e] - l) - (4 * v + e == y ? 1.f : 0.f));
-    reinterpret_cast<f32x4*>(d)[v] = o;
-  }
-  for (int v = 4 * V4 + threadIdx.x; v < V; v += 256) d[v] = c == 0.f ? 0.f : c * (expf(z[v] - l) - (v == y ? 1.f : 0.f));
 }
 
 }  // namespace
@@ -994,12 +1018,12 @@ int dflare_weighted_ce(const float* logits, const int32_t* labels, int32_t rows,
     return DFLARE_ERR_INVALID_ARG;
   if (workspace_bytes < dflare_weighted_ce_workspace(rows)) return DFLARE_ERR_INVALID_ARG;
   hipStream_t st = (hipStream_t)stream;
-  float* lse = static_cast<float*>(workspace);
-  float* w = lse + rows;
+  float* w = static_cast<float*>(workspace);
   float* inv = w + rows;
-  hipLaunchKernelGGL(k_wce_rows, dim3(rows), dim3(256), 0, st, logits, labels, V, B, gamma, lse, w, row_ce);
-  hipLaunchKernelGGL(k_wce_loss, dim3(1), dim3(256), 0, st, w, row_ce, rows, loss, inv);
-  hipLaunchKernelGGL(k_wce_grad, dim3(rows), dim3(256), 0, st, logits, labels, lse, w, inv, V, dlogits);
+  hipLaunchKernelGGL(k_wce_weights, dim3(1), dim3(256), 0, st, labels, rows, V, B, gamma, w, inv);
+  hipLaunchKernelGGL(k_wce_fused, dim3(std::min(rows, kCeRows)), dim3(kCeT), 0, st, logits, labels, rows, V, B,
+                     (const float*)w, (const float*)inv, row_ce, dlogits);
+  hipLaunchKernelGGL(k_wce_loss, dim3(1), dim3(256), 0, st, w, row_ce, rows, loss);
   return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
 }
 
