@@ -113,38 +113,65 @@ __global__ __launch_bounds__(256) void k_tr_blk_t(const uint16_t* src, int n_blo
   }
 }
 
-// x [M][n_q][hd] (bf16 bits, or fp32 with F32) -> dst[g][i][d][Rp]: row r of (block i, group g)
-// is block position r % B of query head g*G + r / B; zeros for r >= R
-template <bool F32>
-__global__ __launch_bounds__(256) void k_tr_group_t(const void* x, AttnShapeT s, uint16_t* dst) {
+// ---- backward operands of (block i, KV head g), one work-group each.  Row r < R of the pair
+// is block position r % B of query head g G + r / B; a row is read once (Q, dO, O: HD / 4
+// threads, four dims each) and gives dO in bf16 (dob, the input layout), D = rowsum(dO O)
+// (dsum), the grouped row copies qr and dor, the pair (lse log2 e, D) (st), and, through an
+// LDS tile, the transposed copies qt and dot.  Rows R .. Rp-1 are zeros (st: (+inf, 0)).  The
+// LDS tiles [2][HD][Rp] keep each 32-row group with its rows permuted per dim row (r ^ (2
+// (d / 4) mod 32)), so that the row-wise writes spread over the banks. ----
+template <int HD>
+__global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t* q, const float* dout, const float* out,
+                                                   const float* lse, AttnShapeT s, uint16_t* dob, float* dsum,
+                                                   uint16_t* qr, uint16_t* dor, float2* st, uint16_t* qt,
+                                                   uint16_t* dot) {
+  extern __shared__ uint16_t tl[];
+  constexpr int TPR = HD / 4, RPS = 256 / TPR;
   const int i = blockIdx.x, g = blockIdx.y;
-  uint16_t* o = dst + ((long)g * s.n_blocks + i) * s.hd * s.Rp;
-  for (int e = threadIdx.x; e < s.hd * s.Rp; e += blockDim.x) {
-    const int d = e / s.Rp, r = e % s.Rp;
-    uint16_t v = 0;
-    if (r < s.R) {
-      const long src = ((long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B) * s.hd + d;
-      v = F32 ? (uint16_t)f2bf(reinterpret_cast<const float*>(x)[src]) : reinterpret_cast<const uint16_t*>(x)[src];
+  const int c4 = threadIdx.x % TPR, rs = threadIdx.x / TPR;
+  const int d0 = 4 * c4;
+  const int swz = (2 * c4) & 31;
+  const long tile = (long)g * s.n_blocks + i;
+  uint16_t* tlq = tl;
+  uint16_t* tld = tl + HD * s.Rp;
+  for (int r = rs; r < s.Rp; r += RPS) {
+    const bool rv = r < s.R;
+    const long rh = rv ? (long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B : 0;
+    f32x4 x = zero4(), o = zero4();
+    u32x2 qv = {0u, 0u};
+    if (rv) {
+      x = *reinterpret_cast<const f32x4*>(dout + rh * HD + d0);
+      o = *reinterpret_cast<const f32x4*>(out + rh * HD + d0);
+      qv = *reinterpret_cast<const u32x2*>(q + rh * HD + d0);
     }
-    o[e] = v;
-  }
-}
-
-// dO -> bf16 copy, and D = rowsum(dO * O) per (row, head): one wave per (row, head)
-__global__ __launch_bounds__(256) void k_tr_dout(const float* dout, const float* out, int rows_heads, int hd,
-                                                  uint16_t* dob, float* dsum) {
-  const int w = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (w >= rows_heads) return;
-  const long base = (long)w * hd;
-  float acc = 0.f;
-  for (int d = lane; d < hd; d += 64) {
-    const float x = dout[base + d];
-    acc += x * out[base + d];
-    dob[base + d] = (uint16_t)f2bf(x);
-  }
+    float acc = (x[0] * o[0] + x[1] * o[1]) + (x[2] * o[2] + x[3] * o[3]);
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (lane == 0) dsum[w] = acc;
+    for (int off = TPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    const u32x2 dv = {f2bf(x[0]) | (f2bf(x[1]) << 16), f2bf(x[2]) | (f2bf(x[3]) << 16)};
+    if (rv) *reinterpret_cast<u32x2*>(dob + rh * HD + d0) = dv;
+    *reinterpret_cast<u32x2*>(qr + (tile * s.Rp + r) * HD + d0) = qv;
+    *reinterpret_cast<u32x2*>(dor + (tile * s.Rp + r) * HD + d0) = dv;
+    const int rr = (r & ~31) | ((r & 31) ^ swz);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      tlq[(d0 + e) * s.Rp + rr] = (uint16_t)(qv[e >> 1] >> (16 * (e & 1)));
+      tld[(d0 + e) * s.Rp + rr] = (uint16_t)(dv[e >> 1] >> (16 * (e & 1)));
+    }
+    if (c4 == 0) {
+      if (rv) dsum[rh] = acc;
+      st[tile * s.Rp + r] = rv ? make_float2(lse[rh] * 1.4426950408889634f, acc) : make_float2(INFINITY, 0.f);
+    }
+  }
+  __syncthreads();
+  // transposed copies [g][i][d][Rp]: rows r, r + 1 of dim row d per 4-byte store
+  const int half = s.Rp / 2;
+  for (int e = threadIdx.x; e < HD * half; e += 256) {
+    const int d = e / half, r = 2 * (e % half);
+    const int rr = (r & ~31) | ((r & 31) ^ ((2 * (d >> 2)) & 31));
+    const long dst = (tile * HD + d) * s.Rp + r;
+    *reinterpret_cast<uint32_t*>(qt + dst) = *reinterpret_cast<const uint32_t*>(tlq + d * s.Rp + rr);
+    *reinterpret_cast<uint32_t*>(dot + dst) = *reinterpret_cast<const uint32_t*>(tld + d * s.Rp + rr);
+  }
 }
 
 // ---- forward and dQ: work-group (block i, KV head g); its 4 waves take the 16-row query
@@ -173,33 +200,51 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
   const uint16_t* tsrc_c = DQ ? a.kct : a.vct;
   const uint16_t* tsrc_b = DQ ? a.kbt : a.vbt;
 
-  // LDS-direct loads of key tile kt into buffer bi (wave w issues wave-loads w, w + 4, ...)
+  // LDS-direct loads of key tile kt into buffer bi.  Each region (K rows, V rows for dQ, the
+  // transposed tile) is RW wave-loads; wave w issues loads w, w + 4, ... of each, from a
+  // per-tile base plus a per-lane offset fixed for the whole kernel.  Keys past T (the last
+  // context tile) and block keys past B read row 0; their scores are masked.
+  constexpr int RW = HD / 16, PW = RW / 4;
+  int kk[PW], cofs[PW], rofs_b[PW], tofs_c[PW], tofs_b[PW];
+#pragma unroll
+  for (int t = 0; t < PW; ++t) {
+    const int sl = (w + 4 * t) * 64 + lane;
+    const int k = sl / PK, d = sl / 4;
+    kk[t] = k;
+    cofs[t] = ((sl % PK) ^ rsw<PK>(k)) * 8;
+    rofs_b[t] = (k < s.B ? k : 0) * s.n_kv * HD + cofs[t];
+    const int ct = ((sl % 4) ^ tsw(d)) * 8;
+    tofs_c[t] = d * s.Tp + ct;
+    tofs_b[t] = d * s.Mp + ct;
+  }
+  // (source pointers through locals: an array element inside the builtin's argument left the
+  // host-side launch stub undefined)
+  auto issue = [&](int bi, int t, const uint16_t* sk, const uint16_t* sv, const uint16_t* stt) {
+    const int ins = w + 4 * t;
+    __builtin_amdgcn_global_load_lds(sk, (LDSP char*)(char*)&lds[bi][ins * 64], 16, 0, 0);
+    if constexpr (DQ) __builtin_amdgcn_global_load_lds(sv, (LDSP char*)(char*)&lds[bi][(RW + ins) * 64], 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(stt, (LDSP char*)(char*)&lds[bi][((DQ ? 2 : 1) * RW + ins) * 64], 16, 0, 0);
+  };
   auto stage = [&](int kt, int bi) {
-    const bool blk = kt == nct;
-    for (int ins = w; ins < NP / 64; ins += 4) {
-      const int slot = ins * 64 + lane;
-      const uint16_t* src;
-      if (slot < (DQ ? 2 * KP : KP)) {
-        const bool isv = slot >= KP;
-        const int sl = isv ? slot - KP : slot;
-        const int k = sl / PK, c = (sl % PK) ^ rsw<PK>(k);
-        long row;
-        if (blk) {
-          const int j = k < s.B ? k : 0;
-          row = ((long)(i * s.B + j) * s.n_kv + g) * HD;
-          src = (isv ? a.vb : a.kb) + row + c * 8;
-        } else {
-          const int key = kt * 32 + k < anchor ? kt * 32 + k : 0;
-          row = ((long)key * s.n_kv + g) * HD;
-          src = (isv ? a.vc : a.kc) + row + c * 8;
-        }
-      } else {
-        const int sl = slot - (DQ ? 2 * KP : KP);
-        const int d = sl / 4, c = (sl % 4) ^ tsw(d);
-        src = blk ? tsrc_b + ((long)g * HD + d) * s.Mp + (long)i * 32 + c * 8
-                  : tsrc_c + ((long)g * HD + d) * s.Tp + (long)kt * 32 + c * 8;
+    if (kt == nct) {  // the block's own keys
+      const long r0 = ((long)i * s.B * s.n_kv + g) * HD;
+      const uint16_t* bt = tsrc_b + (long)g * HD * s.Mp + (long)i * 32;
+#pragma unroll
+      for (int t = 0; t < PW; ++t) {
+        const int ro = rofs_b[t], to = tofs_b[t];
+        issue(bi, t, a.kb + r0 + ro, a.vb + r0 + ro, bt + to);
       }
-      __builtin_amdgcn_global_load_lds(src, (LDSP char*)(char*)&lds[bi][ins * 64], 16, 0, 0);
+    } else {
+      const long r0 = ((long)kt * 32 * s.n_kv + g) * HD;
+      const uint16_t* bt = tsrc_c + (long)g * HD * s.Tp + (long)kt * 32;
+      const bool tail = (kt + 1) * 32 > s.T;
+#pragma unroll
+      for (int t = 0; t < PW; ++t) {
+        long ro = r0 + (long)kk[t] * s.n_kv * HD + cofs[t];
+        if (tail && kt * 32 + kk[t] >= s.T) ro = (long)g * HD + cofs[t];  // key 0
+        const int to = tofs_c[t];
+        issue(bi, t, a.kc + ro, a.vc + ro, bt + to);
+      }
     }
   };
 
@@ -480,37 +525,6 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
       }
     }
     __syncthreads();
-  }
-}
-
-// Q and dO rows of every (block, group) in row order -> qr, dor [g][i][Rp][hd] (zeros past R),
-// and per row (lse * log2 e, rowsum(dO O)) -> st [g][i][Rp], (+inf, 0) past R
-__global__ __launch_bounds__(256) void k_grp_rows(const uint16_t* q, const uint16_t* dob, const float* lse,
-                                                   const float* dsum, AttnShapeT s, uint16_t* qr, uint16_t* dor,
-                                                   float2* st) {
-  const int i = blockIdx.x, g = blockIdx.y;
-  const int PK = s.hd / 8;
-  const long tile = ((long)g * s.n_blocks + i) * s.Rp;
-  const u32x4 z4 = {0u, 0u, 0u, 0u};
-  for (int e = threadIdx.x; e < s.Rp * PK; e += blockDim.x) {
-    const int r = e / PK, c = e % PK;
-    u32x4 vq = z4, vd = z4;
-    if (r < s.R) {
-      const long src = ((long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B) * s.hd + c * 8;
-      vq = ld16(q + src);
-      vd = ld16(dob + src);
-    }
-    const long dst = (tile + r) * s.hd + c * 8;
-    *reinterpret_cast<u32x4*>(qr + dst) = vq;
-    *reinterpret_cast<u32x4*>(dor + dst) = vd;
-  }
-  for (int r = threadIdx.x; r < s.Rp; r += blockDim.x) {
-    float2 v = make_float2(INFINITY, 0.f);
-    if (r < s.R) {
-      const long rh = (long)(i * s.B + r % s.B) * s.n_q + g * s.G + r / s.B;
-      v = make_float2(lse[rh] * 1.4426950408889634f, dsum[rh]);
-    }
-    st[tile + r] = v;
   }
 }
 
@@ -983,18 +997,13 @@ int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_
   a.dkb = dk_blk;
   a.dvb = dv_blk;
   const int cols = n_kv * hd;
-  const int M = n_blocks * B;
   const uint16_t* zero_src = a.kb;
   transpose_kv(st, T > 0 ? a.kc : zero_src, T, cols, s.Tp, a.kct);
   hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks), dim3(256), 0, st, a.kb, n_blocks, B, cols, a.kbt);
-  hipLaunchKernelGGL((k_tr_group_t<false>), dim3(n_blocks, n_kv), dim3(256), 0, st, (const void*)q, s, a.qt);
-  hipLaunchKernelGGL((k_tr_group_t<true>), dim3(n_blocks, n_kv), dim3(256), 0, st, (const void*)dout, s, a.dot);
-  hipLaunchKernelGGL(k_tr_dout, dim3((M * n_q + 3) / 4), dim3(256), 0, st, dout, out, M * n_q, hd, a.dob, a.dsum);
-  if (T > 0)
-    hipLaunchKernelGGL(k_grp_rows, dim3(n_blocks, n_kv), dim3(256), 0, st, a.q, (const uint16_t*)a.dob,
-                       (const float*)a.lse, (const float*)a.dsum, s, a.qr, a.dor, a.st);
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
+    hipLaunchKernelGGL((k_bwd_prep<HD>), dim3(n_blocks, n_kv), dim3(256), (size_t)4 * HD * s.Rp, st, a.q, dout, out,
+                       (const float*)a.lse, s, a.dob, a.dsum, a.qr, a.dor, a.st, a.qt, a.dot);
     if ((s.R + 15) / 16 > 4) hipLaunchKernelGGL((k_aatt_rows<HD, true, 2>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
     else hipLaunchKernelGGL((k_aatt_rows<HD, true, 1>), dim3(n_blocks, n_kv), dim3(kTrT), 0, st, a);
     hipLaunchKernelGGL((k_aatt_kvb<HD>), dim3(n_blocks, n_kv, 1), dim3(kTrT), 0, st, a);
