@@ -584,16 +584,19 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
     roff[t] = rr * HD + ((sl % PK) ^ rsw<PK>(rr)) * 8;
     toff[t] = d * s.Rp + ((sl % 4) ^ tsw(d)) * 8;
   }
-  auto next_unit = [&](int u) {
-    for (; u < (i1 - i0) * NPr; ++u) {
-      const int i = i0 + u / NPr;
-      if (min(max(a.anchors[i], 0), s.T) > key0) return u;
-      u = (u / NPr) * NPr + NPr - 1;  // skip the rest of this block's pairs
-    }
-    return -1;
+  // the chunk's anchors, one block per lane (a chunk is 64 blocks), and the blocks that see a
+  // key of this tile as a bit mask, walked in block order
+  static_assert(kChunkBlocks == 64, "one block per lane");
+  const int anc = lane < i1 - i0 ? min(max(a.anchors[i0 + lane], 0), s.T) : 0;
+  uint64_t left = __builtin_amdgcn_ballot_w64(anc > key0);
+  auto take_block = [&]() {
+    if (left == 0) return -1;
+    const int j = __builtin_ctzll(left);
+    left &= left - 1;
+    return j;
   };
-  auto stage = [&](int u, int bi) {
-    const int i = i0 + u / NPr, pr = u % NPr;
+  auto stage = [&](int j, int pr, int bi) {
+    const int i = i0 + j;
     const long tile = (long)g * s.n_blocks + i;
     const uint16_t* rq = a.qr + (tile * s.Rp + 32 * pr) * HD;
     const uint16_t* rd = a.dor + (tile * s.Rp + 32 * pr) * HD;
@@ -615,8 +618,8 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
     }
   };
   // (lse * log2 e, D) of this lane's result rows 32 pr + 16 y + 4 q4 + (0..3)
-  auto row_stats = [&](int u, f32x4* st4) {
-    const int i = i0 + u / NPr, pr = u % NPr;
+  auto row_stats = [&](int j, int pr, f32x4* st4) {
+    const int i = i0 + j;
     const float2* p = a.st + ((long)g * s.n_blocks + i) * s.Rp + 32 * pr + 4 * q4;
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
@@ -626,23 +629,26 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
   };
 
   const char* L0 = reinterpret_cast<const char*>(&lds[0][0]);
-  int u = next_unit(0);
+  int cj = take_block(), cp = 0;  // current unit: block i0 + cj, row pair cp
   f32x4 cst[4], nst[4];
-  if (u >= 0) {
-    stage(u, 0);
-    row_stats(u, cst);
+  if (cj >= 0) {
+    stage(cj, cp, 0);
+    row_stats(cj, cp, cst);
   }
   wait_vm();
   __syncthreads();
   int bi = 0;
-  while (u >= 0) {
-    const int un = next_unit(u + 1);
-    if (un >= 0) {
-      stage(un, bi ^ 1);
-      row_stats(un, nst);
+  while (cj >= 0) {
+    int nj = cj, np = cp + 1;
+    if (np == NPr) {
+      np = 0;
+      nj = take_block();
     }
-    const int i = i0 + u / NPr;
-    const int anchor = min(max(a.anchors[i], 0), s.T);
+    if (nj >= 0) {
+      stage(nj, np, bi ^ 1);
+      row_stats(nj, np, nst);
+    }
+    const int anchor = __builtin_amdgcn_readlane(anc, cj);
     const bool vis = myk < anchor;  // this lane's key (column of every result tile)
     const char* Lb = L0 + (long)bi * NPc * 16;
     // S = Q K^T, dP = dO V^T: A rows = pair rows 16 y + col
@@ -688,7 +694,8 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < 4; ++e) cst[e] = nst[e];
-    u = un;
+    cj = nj;
+    cp = np;
     bi ^= 1;
   }
   if (kok) {
