@@ -824,6 +824,102 @@ __global__ __launch_bounds__(kCeT) void k_wce_fused(const float* logits, const i
   }
 }
 
+// The same per row with the whole row held on chip: one work-group per CU (its LDS share is
+// the CU's), kCeOR 16-byte pieces per thread in registers and kCeOL in LDS, so that the row is
+// read from memory once; the max, sum and gradient sweeps run over the held values.  Piece v of
+// the row: registers slot k of thread t for v = k kCeOT + t, else LDS slot v - kCeOR kCeOT.  For
+// rows of kCeOMin .. kCeOCap values (a multiple of 4), so that every register slot is inside the
+// row (no per-slot bounds masks to keep).
+constexpr int kCeOT = 256;
+constexpr int kCeOR = 109;
+constexpr int kCeOL = 10224;
+constexpr long kCeOCap = ((long)kCeOR * kCeOT + kCeOL) * 4;  // values of a row held on chip
+constexpr long kCeOMin = (long)kCeOR * kCeOT * 4;
+
+__global__ __launch_bounds__(kCeOT) void k_wce_chip(const float* logits, const int32_t* labels, int rows, int V,
+                                                   int B, const float* w, const float* inv_wsum, float* ce_out,
+                                                   float* dz) {
+  __shared__ f32x4 lrow[kCeOL];
+  __shared__ float red[kCeOT / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const float L2E = 1.4426950408889634f;
+  const int V4 = V / 4;
+  const float inv = inv_wsum[0];
+  auto block_reduce = [&](float x, bool is_max) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float o = __shfl_xor(x, off);
+      x = is_max ? fmaxf(x, o) : x + o;
+    }
+    if (lane == 0) red[wv] = x;
+    __syncthreads();
+    float r = red[0];
+#pragma unroll
+    for (int k = 1; k < kCeOT / 64; ++k) r = is_max ? fmaxf(r, red[k]) : r + red[k];
+    __syncthreads();
+    return r;
+  };
+  for (int row = blockIdx.x; row < rows; row += gridDim.x) {
+    const f32x4* z4 = reinterpret_cast<const f32x4*>(logits + (long)row * V);
+    f32x4 r[kCeOR];
+#pragma unroll
+    for (int k = 0; k < kCeOR; ++k) r[k] = z4[k * kCeOT + tid];
+    // the rest of the row into LDS (pieces past the row re-read piece 0 and are skipped below)
+    for (int m0 = wv * 64; m0 < kCeOL; m0 += kCeOT) {
+      const int v = kCeOR * kCeOT + m0 + lane;
+      const f32x4* src = z4 + (v < V4 ? v : 0);
+      __builtin_amdgcn_global_load_lds(src, (LDSP char*)(char*)&lrow[m0], 16, 0, 0);
+    }
+    wait_vm();
+    __syncthreads();
+    const int nl = min(kCeOL, max(0, V4 - kCeOR * kCeOT));  // LDS pieces of this row
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < kCeOR; ++k) m = fmaxf(m, fmaxf(fmaxf(r[k][0], r[k][1]), fmaxf(r[k][2], r[k][3])));
+    for (int j = tid; j < nl; j += kCeOT) {
+      const f32x4 x = lrow[j];
+      m = fmaxf(m, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+    }
+    const float M = block_reduce(m, true) * L2E;  // max of z log2 e
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < kCeOR; ++k)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum += ex2(fmaf(r[k][e], L2E, -M));
+    for (int j = tid; j < nl; j += kCeOT) {
+      const f32x4 x = lrow[j];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum += ex2(fmaf(x[e], L2E, -M));
+    }
+    const float lse2 = M + log2f(block_reduce(sum, false));
+    const int y = labels[row];
+    const bool on = row % B > 0 && y >= 0 && y < V;
+    if (tid == 0) ce_out[row] = on ? lse2 * 0.6931471805599453f - logits[(long)row * V + y] : 0.f;
+    const float c = w[row] * inv;
+    // (c = 0 rows: c p = 0 for every value, so no branch per piece)
+    f32x4* d4 = reinterpret_cast<f32x4*>(dz + (long)row * V);
+    auto grad = [&](f32x4 x, int v) {
+      f32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = c * ex2(fmaf(x[e], L2E, -lse2));
+      __builtin_nontemporal_store(o, d4 + v);
+    };
+#pragma unroll
+    for (int k = 0; k < kCeOR; ++k) grad(r[k], k * kCeOT + tid);
+    for (int j = tid; j < nl; j += kCeOT) grad(lrow[j], kCeOR * kCeOT + j);
+    // the label's value, c p - c, rewritten by the thread that stored its piece (a thread's
+    // stores to one address land in program order)
+    if (on) {
+      const int y4 = y >> 2, rest = y4 - kCeOR * kCeOT;
+      if ((rest < 0 ? y4 % kCeOT : rest % kCeOT) == tid) {
+        const float zy = logits[(long)row * V + y];
+        dz[(long)row * V + y] = c * ex2(fmaf(zy, L2E, -lse2)) - c;
+      }
+    }
+    __syncthreads();  // lrow is refilled by the next row
+  }
+}
+
 // loss = sum w ce / sum w over the rows, in row order (one work-group)
 __global__ __launch_bounds__(256) void k_wce_loss(const float* w, const float* ce, int rows, float* loss) {
   __shared__ double sw[256], sl[256];
@@ -1037,8 +1133,12 @@ int dflare_weighted_ce(const float* logits, const int32_t* labels, int32_t rows,
   float* w = static_cast<float*>(workspace);
   float* inv = w + rows;
   hipLaunchKernelGGL(k_wce_weights, dim3(1), dim3(256), 0, st, labels, rows, V, B, gamma, w, inv);
-  hipLaunchKernelGGL(k_wce_fused, dim3(std::min(rows, kCeRows)), dim3(kCeT), 0, st, logits, labels, rows, V, B,
-                     (const float*)w, (const float*)inv, row_ce, dlogits);
+  if (V % 4 == 0 && (long)V >= kCeOMin && (long)V <= kCeOCap)
+    hipLaunchKernelGGL(k_wce_chip, dim3(std::min(rows, kCeRows)), dim3(kCeOT), 0, st, logits, labels, rows, V, B,
+                       (const float*)w, (const float*)inv, row_ce, dlogits);
+  else
+    hipLaunchKernelGGL(k_wce_fused, dim3(std::min(rows, kCeRows)), dim3(kCeT), 0, st, logits, labels, rows, V, B,
+                       (const float*)w, (const float*)inv, row_ce, dlogits);
   hipLaunchKernelGGL(k_wce_loss, dim3(1), dim3(256), 0, st, w, row_ce, rows, loss);
   return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
 }

@@ -78,13 +78,17 @@ def test_anchor_attention_matches_oracle(name):
           + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
 
 
-@pytest.mark.parametrize("V", [1000, 1003])
-def test_weighted_ce_matches_oracle(V):
-    B, n = 16, 6
+# (V, blocks): rows streamed twice (V = 1000, 1003), and rows held on chip (V a multiple of 4 in
+# 111,616 .. 152,512): none in LDS, the Qwen3 vocabulary, LDS full; 17 blocks = 272 rows give
+# work-groups a second row
+@pytest.mark.parametrize("V,n", [(1000, 6), (1003, 6), (111616, 17), (151936, 2), (152512, 2)])
+def test_weighted_ce_matches_oracle(V, n):
+    B = 16
     rng = np.random.default_rng(3)
     z = (3.0 * rng.standard_normal((n * B, V))).astype(np.float32)
     y = rng.integers(0, V, size=n * B).astype(np.int32)
     y[rng.random(n * B) < 0.1] = -1
+    y[1], y[2], y[3] = V - 1, 0, min(V - 1, 111616)  # last value, first value, first value past the registers
     gamma = 4.5
     loss, ce, dz = dfl.weighted_ce(torch.from_numpy(z).cuda(), torch.from_numpy(y).cuda(), B, gamma)
     rloss, rce, rdz = tr.weighted_ce(z.astype(np.float64), y, B, gamma)
