@@ -278,11 +278,13 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
   stage(0, 0);
   wait_vm();
   __syncthreads();
-  for (int kt = 0; kt <= nct; ++kt) {
-    const int bi = kt & 1;
+  // one key tile; the buffer index is a compile-time constant (the loop below runs tiles in
+  // pairs), so every LDS read takes its buffer offset as an immediate
+  auto tile = [&](int kt, auto BI) {
+    constexpr int bi = decltype(BI)::value;
     if (kt < nct) stage(kt + 1, bi ^ 1);
     const bool blk = kt == nct;
-    const char* Lb = L0 + (long)bi * NP * 16;
+    const char* Lb = L0 + bi * NP * 16;
     // A-operand rows of this lane: keys 16 x + col
     u32x4 ka[2][HD / 32], va[2][HD / 32];
 #pragma unroll
@@ -378,6 +380,10 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
     }
     wait_vm();
     __syncthreads();
+  };
+  for (int kt = 0; kt <= nct; kt += 2) {
+    tile(kt, std::integral_constant<int, 0>{});
+    if (kt + 1 <= nct) tile(kt + 1, std::integral_constant<int, 1>{});
   }
 #pragma unroll
   for (int tt = 0; tt < TPW; ++tt) {
