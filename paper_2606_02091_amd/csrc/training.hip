@@ -543,7 +543,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
 // Work-groups are numbered so that the 8 XCDs (which take work-groups round-robin) each run
 // whole (group, chunk) sets, whose units then stay in that XCD's L2. ----
 template <int HD>
-__global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
+__global__ __launch_bounds__(kTrT, 2) void k_aatt_kvc(AttnT a) {
   constexpr int PK = HD / 8;                  // 16-byte pieces of a row
   constexpr int RW = HD / 16;                 // wave-loads of one 32-row (or transposed) tile
   constexpr int PW = RW / 4;                  // of them per wave
@@ -643,8 +643,10 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
   }
   wait_vm();
   __syncthreads();
-  int bi = 0;
-  while (cj >= 0) {
+  // one unit; the buffer index is a compile-time constant (units run in pairs), so every LDS
+  // read takes its buffer offset as an immediate
+  auto unit = [&](auto BI) {
+    constexpr int bi = decltype(BI)::value;
     int nj = cj, np = cp + 1;
     if (np == NPr) {
       np = 0;
@@ -656,7 +658,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
     }
     const int anchor = __builtin_amdgcn_readlane(anc, cj);
     const bool vis = myk < anchor;  // this lane's key (column of every result tile)
-    const char* Lb = L0 + (long)bi * NPc * 16;
+    const char* Lb = L0 + bi * NPc * 16;
     // S = Q K^T, dP = dO V^T: A rows = pair rows 16 y + col
     f32x4 sc[2], dp[2];
 #pragma unroll
@@ -702,7 +704,11 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvc(AttnT a) {
     for (int e = 0; e < 4; ++e) cst[e] = nst[e];
     cj = nj;
     cp = np;
-    bi ^= 1;
+  };
+  while (cj >= 0) {
+    unit(std::integral_constant<int, 0>{});
+    if (cj < 0) break;
+    unit(std::integral_constant<int, 1>{});
   }
   if (kok) {
     float* pk = a.part + (((long)z * s.T + myk) * s.n_kv + g) * HD;
