@@ -322,12 +322,13 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
           p1 = mfma(va[1][ks], df[tt][ks], p1);
         }
       }
-      // log2-domain scores of this lane: keys 4 q4 + e and 16 + 4 q4 + e; -inf where masked
+      // raw scores of this lane (keys 4 q4 + e and 16 + 4 q4 + e), -inf where masked; the
+      // log2-domain scale sl2 > 0 goes into each exponent as one fma
       float x0[4], x1[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        x0[e] = s0[e] * sl2;
-        x1[e] = s1[e] * sl2;
+        x0[e] = s0[e];
+        x1[e] = s1[e];
       }
       if (!full) {
 #pragma unroll
@@ -346,6 +347,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
         tm = fmaxf(tm, fmaxf(fmaxf(x0[2], x1[2]), fmaxf(x0[3], x1[3])));
         tm = fmaxf(tm, __shfl_xor(tm, 16));
         tm = fmaxf(tm, __shfl_xor(tm, 32));
+        tm *= sl2;  // max of the log2-domain scores (scaling by sl2 > 0 keeps the maximum)
         const bool grow = tm > m[tt] + 8.f;
         if (__builtin_amdgcn_ballot_w64(grow) != 0) {
           const float mn = grow ? tm : m[tt];
@@ -359,8 +361,8 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
         f32x4 e0, e1;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          e0[e] = ex2(x0[e] - m[tt]);
-          e1[e] = ex2(x1[e] - m[tt]);
+          e0[e] = ex2(fmaf(x0[e], sl2, -m[tt]));
+          e1[e] = ex2(fmaf(x1[e], sl2, -m[tt]));
           ps += e0[e] + e1[e];
         }
         l[tt] += ps;
@@ -369,8 +371,8 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
         f32x4 d0, d1;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          d0[e] = ex2(x0[e] - lse2[tt]) * (p0[e] - dr[tt]);
-          d1[e] = ex2(x1[e] - lse2[tt]) * (p1[e] - dr[tt]);
+          d0[e] = ex2(fmaf(x0[e], sl2, -lse2[tt])) * (p0[e] - dr[tt]);
+          d1[e] = ex2(fmaf(x1[e], sl2, -lse2[tt])) * (p1[e] - dr[tt]);
         }
         pb = pack_bf8(d0, d1);
       }
@@ -478,7 +480,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
         for (int x = 0; x < 2; ++x) {
           const int j = 16 * x + col;
           const bool ok = rv && j < s.B;
-          const float p = ok ? ex2(sc[y][x][e] * sl2 - lse2) : 0.f;
+          const float p = ok ? ex2(fmaf(sc[y][x][e], sl2, -lse2)) : 0.f;
           P[y][x][e] = p;
           dS[y][x][e] = p * (dp[y][x][e] - dr);
         }
@@ -681,7 +683,7 @@ __global__ __launch_bounds__(kTrT, 2) void k_aatt_kvc(AttnT a) {
       for (int e = 0; e < 4; ++e) {
         const f32x4 sv = cst[2 * y + (e >> 1)];
         const float l2 = sv[2 * (e & 1)], dr = sv[2 * (e & 1) + 1];
-        const float p = vis ? ex2(sc[y][e] * sl2 - l2) : 0.f;
+        const float p = vis ? ex2(fmaf(sc[y][e], sl2, -l2)) : 0.f;
         P[y][e] = p;
         dS[y][e] = p * (dp[y][e] - dr);
       }
