@@ -29,6 +29,7 @@ namespace {
 
 constexpr int kTrT = 256;  // threads per work-group (4 waves)
 constexpr int kChunkBlocks = 64;  // blocks per partial of the context-key gradients
+constexpr int kMaxBlockKeys = 16;  // block size B the training entry points accept
 
 struct AttnShapeT {
   int n_blocks, B, T, n_q, n_kv, hd;
@@ -413,6 +414,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
 // pairs w, w + 4, ... and the 4 waves' sums are added in wave order ----
 template <int HD>
 __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
+  constexpr int NX = kMaxBlockKeys / 16;  // 16-key tiles of a block's keys (B <= kMaxBlockKeys)
   const AttnShapeT& s = a.s;
   const int g = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -421,15 +423,15 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
   const int NP = s.Rp / 32;  // 32-row pairs of a (block, group)
   const u32x4 z4 = {0u, 0u, 0u, 0u};
   const int ib = blockIdx.x;
-  f32x4 dk[HD / 16][2], dv[HD / 16][2];
+  f32x4 dk[HD / 16][NX], dv[HD / 16][NX];
 #pragma unroll
   for (int dt = 0; dt < HD / 16; ++dt)
 #pragma unroll
-    for (int x = 0; x < 2; ++x) dk[dt][x] = dv[dt][x] = zero4();
+    for (int x = 0; x < NX; ++x) dk[dt][x] = dv[dt][x] = zero4();
   // B-operand rows (keys) of this lane: key 16x + col of the tile
-  u32x4 kf[2][HD / 32], vf[2][HD / 32];
+  u32x4 kf[NX][HD / 32], vf[NX][HD / 32];
 #pragma unroll
-  for (int x = 0; x < 2; ++x) {
+  for (int x = 0; x < NX; ++x) {
     const int j = 16 * x + col;
     const bool ok = j < s.B;
     const long row = ok ? ((long)(ib * s.B + j) * s.n_kv + g) * HD : 0;
@@ -444,11 +446,11 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
   const int i = ib;
   for (int pr = w; pr < NP; pr += 4) {
     // S = Q K^T and dP = dO V^T for rows 32 pr + 16 y + (4 q4 + e) (y = 0, 1), keys 16x + col
-    f32x4 sc[2][2], dp[2][2];
+    f32x4 sc[2][NX], dp[2][NX];
 #pragma unroll
     for (int y = 0; y < 2; ++y)
 #pragma unroll
-      for (int x = 0; x < 2; ++x) sc[y][x] = dp[y][x] = zero4();
+      for (int x = 0; x < NX; ++x) sc[y][x] = dp[y][x] = zero4();
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
       const int r = 32 * pr + 16 * y + col;  // A row of this lane
@@ -459,14 +461,14 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
         const u32x4 qa = rv ? ld16(a.q + qrow + ks * 32 + 8 * q4) : z4;
         const u32x4 da = rv ? ld16(a.dob + qrow + ks * 32 + 8 * q4) : z4;
 #pragma unroll
-        for (int x = 0; x < 2; ++x) {
+        for (int x = 0; x < NX; ++x) {
           sc[y][x] = mfma(qa, kf[x][ks], sc[y][x]);
           dp[y][x] = mfma(da, vf[x][ks], dp[y][x]);
         }
       }
     }
     // P and dS at this lane's values: row 32 pr + 16 y + 4 q4 + e, key 16 x + col
-    f32x4 P[2][2], dS[2][2];
+    f32x4 P[2][NX], dS[2][NX];
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
 #pragma unroll
@@ -477,7 +479,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
         const float lse2 = rv ? a.lse[rh] * 1.4426950408889634f : 0.f;
         const float dr = rv ? a.dsum[rh] : 0.f;
 #pragma unroll
-        for (int x = 0; x < 2; ++x) {
+        for (int x = 0; x < NX; ++x) {
           const int j = 16 * x + col;
           const bool ok = rv && j < s.B;
           const float p = ok ? ex2(fmaf(sc[y][x][e], sl2, -lse2)) : 0.f;
@@ -494,7 +496,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
       const u32x4 doa = ld_pair(a.dot + off);
       const u32x4 qa = ld_pair(a.qt + off);
 #pragma unroll
-      for (int x = 0; x < 2; ++x) {
+      for (int x = 0; x < NX; ++x) {
         dv[dt][x] = mfma(doa, pack_bf8(P[0][x], P[1][x]), dv[dt][x]);
         dk[dt][x] = mfma(qa, pack_bf8(dS[0][x], dS[1][x]), dk[dt][x]);
       }
@@ -502,22 +504,23 @@ __global__ __launch_bounds__(kTrT) void k_aatt_kvb(AttnT a) {
   }
   // sum the 4 waves' tiles in wave order through LDS, 8 tiles per round
   __shared__ f32x4 red[3][8][64];
-  constexpr int NT = HD / 16 * 2 * 2;  // tiles per wave (dK, dV)
+  constexpr int NT = HD / 16 * NX * 2;  // tiles per wave (dK, dV)
+  static_assert(NT % 8 == 0, "8 tiles per round");
 #pragma unroll
   for (int r0 = 0; r0 < NT; r0 += 8) {
     if (w > 0) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int tI = r0 + u, kind = tI / (HD / 16 * 2), rem = tI % (HD / 16 * 2);
-        red[w - 1][u][lane] = kind == 0 ? dk[rem / 2][rem % 2] : dv[rem / 2][rem % 2];
+        const int tI = r0 + u, kind = tI / (HD / 16 * NX), rem = tI % (HD / 16 * NX);
+        red[w - 1][u][lane] = kind == 0 ? dk[rem / NX][rem % NX] : dv[rem / NX][rem % NX];
       }
     }
     __syncthreads();
     if (w == 0) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int tI = r0 + u, kind = tI / (HD / 16 * 2), rem = tI % (HD / 16 * 2);
-        const int dt = rem / 2, x = rem % 2;
+        const int tI = r0 + u, kind = tI / (HD / 16 * NX), rem = tI % (HD / 16 * NX);
+        const int dt = rem / NX, x = rem % NX;
         f32x4 v = kind == 0 ? dk[dt][x] : dv[dt][x];
         v += red[0][u][lane];
         v += red[1][u][lane];
@@ -978,7 +981,7 @@ static AttnShapeT att_shape(int n_blocks, int B, int T, int n_q, int n_kv, int h
 }
 
 static int att_check(int n_blocks, int B, int T, int n_q, int n_kv, int hd) {
-  if (n_blocks < 1 || B < 1 || B > 16 || T < 0 || n_q < 1 || n_kv < 1 || n_q % n_kv) return DFLARE_ERR_INVALID_ARG;
+  if (n_blocks < 1 || B < 1 || B > kMaxBlockKeys || T < 0 || n_q < 1 || n_kv < 1 || n_q % n_kv) return DFLARE_ERR_INVALID_ARG;
   if (hd != 64 && hd != 128) return DFLARE_ERR_UNSUPPORTED;
   if ((n_q / n_kv) * B > 128) return DFLARE_ERR_UNSUPPORTED;
   return DFLARE_OK;
