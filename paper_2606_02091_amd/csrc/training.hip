@@ -104,13 +104,26 @@ __global__ __launch_bounds__(256) void k_tr_kv_t(const uint16_t* src, int nrows,
 }
 
 // block keys src [n_blocks*B][n_kv][hd] -> dst [n_kv][hd][n_blocks*32]: block i's keys at
-// i*32 + j (j < B), zeros for j >= B, so that every 16-byte piece of a block is aligned
+// i*32 + j (j < B), zeros for j >= B, so that every 16-byte piece of a block is aligned.
+// Work-group = (block i, 256 columns): rows read along the columns into an LDS tile, then each
+// column's 32 keys written as four 16-byte pieces.
 __global__ __launch_bounds__(256) void k_tr_blk_t(const uint16_t* src, int n_blocks, int B, int cols, uint16_t* dst) {
-  const int i = blockIdx.x;
+  __shared__ uint16_t tl[256][kMaxBlockKeys + 2];
+  const int i = blockIdx.x, c0 = blockIdx.y * 256, t = threadIdx.x;
   const long ld = (long)n_blocks * 32;
-  for (int e = threadIdx.x; e < cols * 32; e += blockDim.x) {
-    const int c = e / 32, j = e % 32;
-    dst[(long)c * ld + (long)i * 32 + j] = j < B ? src[((long)i * B + j) * cols + c] : (uint16_t)0;
+  for (int j = 0; j < B; ++j) tl[t][j] = c0 + t < cols ? src[((long)i * B + j) * cols + c0 + t] : (uint16_t)0;
+  __syncthreads();
+  for (int e = t; e < 256 * 4; e += 256) {
+    const int c = e / 4, pc = e % 4;  // column c0 + c, keys 8 pc .. 8 pc + 7
+    if (c0 + c >= cols) continue;
+    uint32_t w[4];
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const int j = 8 * pc + 2 * h;
+      const uint32_t lo = j < B ? tl[c][j] : 0u, hi = j + 1 < B ? tl[c][j + 1] : 0u;
+      w[h] = lo | (hi << 16);
+    }
+    *reinterpret_cast<u32x4*>(dst + (long)(c0 + c) * ld + (long)i * 32 + 8 * pc) = u32x4{w[0], w[1], w[2], w[3]};
   }
 }
 
@@ -1084,7 +1097,7 @@ int dflare_anchor_attention_fwd(const void* q, const void* k_ctx, const void* v_
   const int cols = n_kv * hd;
   const uint16_t* zero_src = a.kb;  // with T = 0 the context copies are all zeros
   transpose_kv(st, T > 0 ? a.vc : zero_src, T, cols, s.Tp, a.vct);
-  hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks), dim3(256), 0, st, a.vb, n_blocks, B, cols, a.vbt);
+  hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks, (cols + 255) / 256), dim3(256), 0, st, a.vb, n_blocks, B, cols, a.vbt);
   const bool two = (s.R + 15) / 16 > 4;
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
@@ -1119,7 +1132,7 @@ int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_
   const int cols = n_kv * hd;
   const uint16_t* zero_src = a.kb;
   transpose_kv(st, T > 0 ? a.kc : zero_src, T, cols, s.Tp, a.kct);
-  hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks), dim3(256), 0, st, a.kb, n_blocks, B, cols, a.kbt);
+  hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks, (cols + 255) / 256), dim3(256), 0, st, a.kb, n_blocks, B, cols, a.kbt);
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
     hipLaunchKernelGGL((k_bwd_prep<HD>), dim3(n_blocks, n_kv), dim3(256), (size_t)4 * HD * s.Rp, st, a.q, dout, out,
