@@ -129,3 +129,56 @@ def test_calls_on_invalid_handles(L):
     assert L.dflare_context_len_seq(None, 0, ctypes.byref(out)) == dfl.ERR_INVALID_ARG
     buf = (ctypes.c_float * 4)()
     assert L.dflare_debug_read_seq(None, dfl.DBG_KCACHE, 0, 0, buf, 4) == dfl.ERR_INVALID_ARG
+
+
+# ---- training-side entry points: shape and argument checks (no HIP call is made) ----
+
+def test_anchor_attention_workspace_sizes(L):
+    ws = L.dflare_anchor_attention_workspace
+    ok = ws(4, 16, 100, 8, 2, 128)
+    assert ok > 0
+    assert ws(4, 16, 200, 8, 2, 128) > ok          # more context keys, more workspace
+    assert ws(4, 16, 0, 8, 2, 128) > 0             # no context at all is a valid call
+    for bad in [(0, 16, 100, 8, 2, 128),            # no block
+                (4, 17, 100, 8, 2, 128),            # B above 16
+                (4, 0, 100, 8, 2, 128),
+                (4, 16, -1, 8, 2, 128),
+                (4, 16, 100, 9, 2, 128),            # query heads not a multiple of KV heads
+                (4, 16, 100, 8, 2, 96),             # head size other than 64 or 128
+                (4, 16, 100, 18, 2, 128)]:          # 9 query heads per group x 16 rows > 128
+        assert ws(*bad) == 0, bad
+
+
+def test_anchor_attention_rejects_bad_arguments(L):
+    p = ctypes.c_void_p(0x1000)  # never dereferenced: every case fails its checks first
+    f = ctypes.cast(0x1000, ctypes.POINTER(ctypes.c_float))
+    i32 = ctypes.cast(0x1000, ctypes.POINTER(ctypes.c_int32))
+    need = L.dflare_anchor_attention_workspace(4, 16, 100, 8, 2, 128)
+    fwd = L.dflare_anchor_attention_fwd
+    assert fwd(p, p, p, p, p, i32, 4, 16, 100, 8, 2, 96, f, f, p, need, None) == dfl.ERR_UNSUPPORTED
+    assert fwd(p, p, p, p, p, i32, 4, 17, 100, 8, 2, 128, f, f, p, need, None) == dfl.ERR_INVALID_ARG
+    assert fwd(None, p, p, p, p, i32, 4, 16, 100, 8, 2, 128, f, f, p, need, None) == dfl.ERR_INVALID_ARG
+    assert fwd(p, None, p, p, p, i32, 4, 16, 100, 8, 2, 128, f, f, p, need, None) == dfl.ERR_INVALID_ARG
+    assert fwd(p, p, p, p, p, i32, 4, 16, 100, 8, 2, 128, f, f, p, need - 1, None) == dfl.ERR_INVALID_ARG
+    bwd = L.dflare_anchor_attention_bwd
+    assert bwd(p, p, p, p, p, i32, 4, 16, 100, 8, 2, 128, f, f, None, f, f, f, f, f, p, need, None) \
+        == dfl.ERR_INVALID_ARG                    # no output gradient
+    assert bwd(p, p, p, p, p, i32, 4, 16, 100, 8, 2, 128, f, f, f, f, f, f, f, f, p, need - 1, None) \
+        == dfl.ERR_INVALID_ARG
+    assert bwd(p, p, p, p, p, i32, 4, 16, 100, 8, 2, 64, f, f, f, f, None, f, f, f, p, need, None) \
+        == dfl.ERR_INVALID_ARG                    # context keys (T > 0) without their gradient
+
+
+def test_weighted_ce_rejects_bad_arguments(L):
+    p = ctypes.c_void_p(0x1000)
+    f = ctypes.cast(0x1000, ctypes.POINTER(ctypes.c_float))
+    i32 = ctypes.cast(0x1000, ctypes.POINTER(ctypes.c_int32))
+    need = L.dflare_weighted_ce_workspace(64)
+    assert need >= 3 * 64 * 4
+    ce = L.dflare_weighted_ce
+    assert ce(f, i32, 64, 1000, 16, 4.5, f, f, f, p, need - 1, None) == dfl.ERR_INVALID_ARG
+    assert ce(f, i32, 60, 1000, 16, 4.5, f, f, f, p, need, None) == dfl.ERR_INVALID_ARG  # rows % B
+    for gamma in (0.0, -1.0, float("nan"), float("inf")):
+        assert ce(f, i32, 64, 1000, 16, gamma, f, f, f, p, need, None) == dfl.ERR_INVALID_ARG
+    assert ce(None, i32, 64, 1000, 16, 4.5, f, f, f, p, need, None) == dfl.ERR_INVALID_ARG
+    assert ce(f, i32, 64, 0, 16, 4.5, f, f, f, p, need, None) == dfl.ERR_INVALID_ARG
