@@ -97,3 +97,52 @@ def test_weighted_ce_matches_oracle(V, n):
     assert P.relinf(dz.cpu().numpy(), rdz) <= 1e-5
     with pytest.raises(dfl.DFlareError):
         dfl.weighted_ce(torch.from_numpy(z[:17]).cuda(), torch.from_numpy(y[:17]).cuda(), B, gamma)
+
+
+def test_anchor_attention_full_training_shape_sampled():
+    """The training shape the benchmark times (T = 3,072, 512 blocks of B = 16, 32 query / 8 KV
+    heads x 128): every kernel runs on the whole problem in its benchmark launch configuration
+    (8 gradient chunks, XCD-grouped work order), and sampled blocks are checked against the
+    oracle run on that block alone — its outputs, lse, dQ and block-key gradients depend on
+    nothing else.  Anchors lie in 0 .. 2,900 except one block's, T - B: the context keys from
+    2,901 up to it are seen by that block only, so their gradients are that block's too, and
+    keys at or past T - B are seen by no block (zero gradients)."""
+    n, B, T, nq, nkv, hd = 512, 16, 3072, 32, 8, 128
+    print("[training] full shape sampled", flush=True)
+    rng = np.random.default_rng(11)
+
+    def bf(shape):
+        return synth.round_bf16(rng.standard_normal(shape).astype(np.float32))
+
+    x = dict(q=bf((n * B, nq, hd)), k_ctx=bf((T, nkv, hd)), v_ctx=bf((T, nkv, hd)),
+             k_blk=bf((n * B, nkv, hd)), v_blk=bf((n * B, nkv, hd)))
+    anchors = rng.integers(0, 2901, size=n).astype(np.int32)
+    top = 7
+    anchors[0], anchors[top] = 0, T - B
+    dout = rng.standard_normal((n * B, nq, hd)).astype(np.float32)
+    d = {k: dev(v) for k, v in x.items()}
+    a = torch.from_numpy(anchors).cuda()
+    out, lse = dfl.anchor_attention_fwd(d["q"], d["k_ctx"], d["v_ctx"], d["k_blk"], d["v_blk"], a, B)
+    g = dfl.anchor_attention_bwd(d["q"], d["k_ctx"], d["v_ctx"], d["k_blk"], d["v_blk"], a, B, out, lse,
+                                 torch.from_numpy(dout).cuda())
+    out, lse = out.cpu().numpy(), lse.cpu().numpy()
+    dq, dkc, dvc, dkb, dvb = (t.cpu().numpy() for t in g)
+    assert not dkc[T - B:].any() and not dvc[T - B:].any()
+    kc64 = synth.bf16_to_f32(x["k_ctx"]).astype(np.float64)
+    vc64 = synth.bf16_to_f32(x["v_ctx"]).astype(np.float64)
+    for i in (0, top, 200, n - 1):
+        rows = slice(i * B, (i + 1) * B)
+        blk = {k: synth.bf16_to_f32(x[k][rows]).astype(np.float64) for k in ("q", "k_blk", "v_blk")}
+        ro, rl = tr.anchor_attention_fwd(blk["q"], kc64, vc64, blk["k_blk"], blk["v_blk"], [int(anchors[i])], B)
+        rdq, rdkc, rdvc, rdkb, rdvb = tr.anchor_attention_bwd(blk["q"], kc64, vc64, blk["k_blk"], blk["v_blk"],
+                                                               [int(anchors[i])], B, dout[rows].astype(np.float64))
+        errs = {"out": P.relinf(out[rows], ro), "lse": P.relinf(lse[rows], rl), "dq": P.relinf(dq[rows], rdq),
+                "dk_blk": P.relinf(dkb[rows], rdkb), "dv_blk": P.relinf(dvb[rows], rdvb)}
+        if i == top:
+            only = slice(2901, T - B)
+            errs["dk_ctx_own"] = P.relinf(dkc[only], rdkc[only])
+            errs["dv_ctx_own"] = P.relinf(dvc[only], rdvc[only])
+        print(f"[training] full shape block {i} (anchor {anchors[i]}): "
+              + " ".join(f"{k} {v:.2e}" for k, v in errs.items()), flush=True)
+        for k, v in errs.items():
+            assert v <= P.REL_TOL, (i, k, v)
