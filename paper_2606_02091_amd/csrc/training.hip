@@ -870,25 +870,11 @@ __global__ __launch_bounds__(kCeOT) void k_wce_chip(const float* logits, const i
                                                    int B, const float* w, const float* inv_wsum, float* ce_out,
                                                    float* dz) {
   __shared__ f32x4 lrow[kCeOL];
-  __shared__ float red[kCeOT / 64];
+  __shared__ float red[kCeOT / 64], redm[kCeOT / 64];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const float L2E = 1.4426950408889634f;
   const int V4 = V / 4;
   const float inv = inv_wsum[0];
-  auto block_reduce = [&](float x, bool is_max) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const float o = __shfl_xor(x, off);
-      x = is_max ? fmaxf(x, o) : x + o;
-    }
-    if (lane == 0) red[wv] = x;
-    __syncthreads();
-    float r = red[0];
-#pragma unroll
-    for (int k = 1; k < kCeOT / 64; ++k) r = is_max ? fmaxf(r, red[k]) : r + red[k];
-    __syncthreads();
-    return r;
-  };
   for (int row = blockIdx.x; row < rows; row += gridDim.x) {
     const f32x4* z4 = reinterpret_cast<const f32x4*>(logits + (long)row * V);
     f32x4 r[kCeOR];
@@ -900,28 +886,46 @@ __global__ __launch_bounds__(kCeOT) void k_wce_chip(const float* logits, const i
       const f32x4* src = z4 + (v < V4 ? v : 0);
       __builtin_amdgcn_global_load_lds(src, (LDSP char*)(char*)&lrow[m0], 16, 0, 0);
     }
+    const int nl = min(kCeOL, max(0, V4 - kCeOR * kCeOT));  // LDS pieces of this row
+    // running (max, sum) of the log2-domain values, one 16-byte piece at a time (the register
+    // pieces in load order, so the sweep follows their arrival), then the LDS pieces
+    float m = -INFINITY, sum = 0.f;
+    auto take4 = [&](f32x4 x) {
+      const float t0 = x[0] * L2E, t1 = x[1] * L2E, t2 = x[2] * L2E, t3 = x[3] * L2E;
+      const float m4 = fmaxf(fmaxf(t0, t1), fmaxf(t2, t3));
+      if (m4 > m) {
+        sum *= ex2(m - m4);
+        m = m4;
+      }
+      sum += (ex2(t0 - m) + ex2(t1 - m)) + (ex2(t2 - m) + ex2(t3 - m));
+    };
+#pragma unroll
+    for (int k = 0; k < kCeOR; ++k) take4(r[k]);
     wait_vm();
     __syncthreads();
-    const int nl = min(kCeOL, max(0, V4 - kCeOR * kCeOT));  // LDS pieces of this row
-    float m = -INFINITY;
+    for (int j = tid; j < nl; j += kCeOT) take4(lrow[j]);
+    // combine the threads' (max, sum) pairs
 #pragma unroll
-    for (int k = 0; k < kCeOR; ++k) m = fmaxf(m, fmaxf(fmaxf(r[k][0], r[k][1]), fmaxf(r[k][2], r[k][3])));
-    for (int j = tid; j < nl; j += kCeOT) {
-      const f32x4 x = lrow[j];
-      m = fmaxf(m, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+    for (int off = 32; off > 0; off >>= 1) {
+      const float om = __shfl_xor(m, off), os = __shfl_xor(sum, off);
+      const float nm = fmaxf(m, om);
+      sum = (nm == -INFINITY) ? 0.f : sum * ex2(m - nm) + os * ex2(om - nm);
+      m = nm;
     }
-    const float M = block_reduce(m, true) * L2E;  // max of z log2 e
-    float sum = 0.f;
-#pragma unroll
-    for (int k = 0; k < kCeOR; ++k)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) sum += ex2(fmaf(r[k][e], L2E, -M));
-    for (int j = tid; j < nl; j += kCeOT) {
-      const f32x4 x = lrow[j];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) sum += ex2(fmaf(x[e], L2E, -M));
+    if (lane == 0) {
+      redm[wv] = m;
+      red[wv] = sum;
     }
-    const float lse2 = M + log2f(block_reduce(sum, false));
+    __syncthreads();
+    float M = redm[0], S = red[0];
+#pragma unroll
+    for (int k = 1; k < kCeOT / 64; ++k) {
+      const float nm = fmaxf(M, redm[k]);
+      S = S * ex2(M - nm) + red[k] * ex2(redm[k] - nm);
+      M = nm;
+    }
+    __syncthreads();  // red, redm are rewritten by the next row
+    const float lse2 = M + log2f(S);
     const int y = labels[row];
     const bool on = row % B > 0 && y >= 0 && y < V;
     if (tid == 0) ce_out[row] = on ? lse2 * 0.6931471805599453f - logits[(long)row * V + y] : 0.f;
