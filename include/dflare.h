@@ -308,7 +308,8 @@ const char* dflare_last_error(const dflare_handle* h);
  *                             no such mark.  Needs DFLARE_OPT_TRACE (sizes from
  *                             dflare_kernel_stats)
  * `count` is the number of floats host_out can hold; too small is INVALID_ARG.
- * Debug capture makes draft_block run one launch per phase.  FUSED after a
+ * Debug capture makes draft_block run one launch per phase, unless
+ * DFLARE_OPT_CAPTURE_PERSISTENT is set.  FUSED after a
  * batched append holds all sum(n_new) rows of that call.
  * dflare_debug_read_seq reads DFLARE_DBG_KCACHE / DFLARE_DBG_VCACHE of slot `seq`
  * ([L_seq, n_kv, hd]); dflare_debug_read reads those of slot 0.
@@ -372,8 +373,14 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches);
  *                          1 is refused (UNSUPPORTED) when the device cannot keep one
  *                          work-group per CU resident.
  *   DFLARE_OPT_TRACE       1: record per-work-group phase start times (DFLARE_DBG_TRACE).
+ *   DFLARE_OPT_CAPTURE_PERSISTENT
+ *                          1: debug capture keeps the persistent launch: the draft-block
+ *                          kernel itself writes the logits and the block rows after each
+ *                          layer (DFLARE_DBG_LOGITS, DFLARE_DBG_HIDDEN) in the launch
+ *                          configuration that is timed; 0 (default): debug capture runs
+ *                          one launch per phase.
  */
-enum { DFLARE_OPT_PERSISTENT = 1, DFLARE_OPT_TRACE = 2 };
+enum { DFLARE_OPT_PERSISTENT = 1, DFLARE_OPT_TRACE = 2, DFLARE_OPT_CAPTURE_PERSISTENT = 3 };
 int dflare_set_option(dflare_handle* h, int option, int value);
 
 /*

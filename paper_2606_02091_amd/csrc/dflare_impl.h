@@ -68,6 +68,7 @@ struct DraftCall {
   const int* ids;       // [B] block token ids
   int* tokens;          // [B] output: greedy draft tokens
   float* logits;        // optional [B, V]
+  float* hidden;        // optional [D, B, H]: block rows after each draft layer
   unsigned bar_epoch;   // grid barriers completed by earlier launches
   unsigned done_epoch;  // launches that ran the LM phase before this one
   unsigned long long* trace;  // optional [blocks][phases][kTraceSlots] wall clock at marks of each phase

@@ -469,6 +469,7 @@ struct GemmJob {
   uint32_t* na_lo;
   int na_Kt;
   const float* gain;   // RESID: gain of the next RMSNorm
+  float* hid_out;      // RESID after the MLP: optional copy of the layer's output rows [B, H]
   // QKV
   float* q_out;        // [16, q_dim]
   uint16_t* kc;        // cache of this layer
@@ -509,6 +510,7 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
         float* p = a->X + (long)row * a->H + k;
         x = ld_coh(p) + v[i];
         st_wt(p, x);
+        if (g.hid_out) st_wt(g.hid_out + (long)row * a->H + k, x);
       }
       sq[i] = x * x;
       const float y = x * gn;
@@ -619,7 +621,7 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
 __host__ __device__ constexpr int gemm_ns(int TN) { return TN >= 8 ? 2 : 4; }  // steps in flight
 
 // The GEMM job of phase (kind, layer): weights, input fragments and epilogue targets.
-__device__ __forceinline__ GemmJob make_job(Args a, int kind, int layer) {
+__device__ __forceinline__ GemmJob make_job(Args a, Call c, int kind, int layer) {
   GemmJob g{};
   const int H = a->H, Kt_H = H / 32, q_Kt = a->n_q * a->hd / 32, F_Kt = a->F / 32;
   switch (kind) {
@@ -651,6 +653,7 @@ __device__ __forceinline__ GemmJob make_job(Args a, int kind, int layer) {
       g.na_lo = reinterpret_cast<uint32_t*>(a->XA + s * a->xa_stride + (long)(Kt_H + kKtPad) * 64);
       g.na_Kt = Kt_H;
       g.gain = o ? a->g_mlp + (long)layer * H : (layer + 1 < a->D ? a->g_attn + (long)(layer + 1) * H : a->g_final);
+      g.hid_out = (!o && c->hidden) ? c->hidden + (long)layer * a->B * H : nullptr;
       break;
     }
     case PH_GU: {
@@ -1394,7 +1397,7 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
 template <int EPI>
 __device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int layer, const PhaseCtl& pc, bool& failed,
                                               u32x4* smem) {
-  GemmJob g = make_job(a, kind, layer);
+  GemmJob g = make_job(a, c, kind, layer);
   const int kg = kind == PH_LM ? 1 : a->kg[kind];
   const int slot = kind == PH_QKV ? 0 : kind == PH_O ? 1 : kind == PH_GU ? 2 : 3;
   g.cnt = a->kcnt + (long)slot * kMaxBlocks * 32;

@@ -111,6 +111,7 @@ struct dflare_handle {
   int* err_host = nullptr;   // host-mapped barrier time-out flag
   int* err_dev = nullptr;
   bool trace = false;
+  bool capture_persistent = false;  // debug capture written by the persistent launch itself
   unsigned long long* trace_buf = nullptr;
   // debug capture
   bool debug = false;
@@ -660,6 +661,7 @@ DraftCall draft_call(const dflare_handle* h, const int32_t* ids, const int32_t* 
   d.ids = ids;
   d.tokens = out;
   d.logits = h->debug ? h->dbg_logits : nullptr;
+  d.hidden = (h->debug && h->capture_persistent && h->persistent) ? h->dbg_hidden : nullptr;
   d.bar_epoch = h->bar_epoch;
   d.done_epoch = h->done_epoch;
   d.trace = h->trace ? h->trace_buf : nullptr;
@@ -708,7 +710,8 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   if (h->trace) HIP_OR_FAIL(h, hipMemsetAsync(h->trace_buf, 0, (size_t)h->blocks * kTraceSlots * P * 8, s));
   const DraftCall dc = draft_call(h, ids, positions_host, out);
   const int hd = c.head_dim;
-  const bool split = !h->persistent || h->debug || (h->prof_kind >= DFLARE_K_QKV && h->prof_kind <= DFLARE_K_LM_HEAD);
+  const bool split = !h->persistent || (h->debug && !h->capture_persistent) ||
+                     (h->prof_kind >= DFLARE_K_QKV && h->prof_kind <= DFLARE_K_LM_HEAD);
   prof_mark(h, DFLARE_K_DRAFT, true);
   if (!split) {
     HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, h->blocks, 0, P, true));
@@ -1379,6 +1382,9 @@ int dflare_set_option(dflare_handle* h, int option, int value) {
       return DFLARE_OK;
     case DFLARE_OPT_TRACE:
       h->trace = value != 0;
+      return DFLARE_OK;
+    case DFLARE_OPT_CAPTURE_PERSISTENT:
+      h->capture_persistent = value != 0;
       return DFLARE_OK;
     default: return fail(h, DFLARE_ERR_INVALID_ARG, "unknown option");
   }

@@ -61,12 +61,29 @@ def test_fullsize_parity(name):
             assert dfl.dflare_kernel_stats(model.h)[0] == 1
             persistent_tokens = out.cpu().numpy().copy()
             dfl.dflare_debug_capture(model.h, True)
+            # the timed launch configuration writing its own logits and block rows
+            dfl.dflare_set_option(model.h, dfl.OPT_CAPTURE_PERSISTENT, 1)
+            model.draft_block(ids_t, out)
+            side.synchronize()
+            assert dfl.dflare_kernel_stats(model.h)[0] == 1
+            assert np.array_equal(out.cpu().numpy(), persistent_tokens)
+            p_logits = dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0, (cfg.block_size, cfg.vocab))
+            p_hidden = [dfl.dflare_debug_read(model.h, dfl.DBG_HIDDEN, i, (cfg.block_size, cfg.hidden))
+                        for i in range(cfg.n_draft_layers)]
+            dfl.dflare_set_option(model.h, dfl.OPT_CAPTURE_PERSISTENT, 0)
             eager = model.draft_block(ids_t).cpu().numpy()
             side.synchronize()
             dfl.dflare_debug_capture(model.h, False)
             assert np.array_equal(persistent_tokens, eager)
             ref = orc.draft_block(ids)
             print(f"[fullsize] {name}: step {step} oracle done", flush=True)
+            e = P.relinf(p_logits, ref["logits"])
+            assert e <= P.REL_TOL, (name, step, "persistent logits", e)
+            for i in range(cfg.n_draft_layers):
+                assert P.relinf(p_hidden[i], ref["hidden"][i]) <= P.REL_TOL, (name, step, "persistent", i)
+            # the per-phase launches of the debug run give the same numbers bitwise
+            assert np.array_equal(p_logits, dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0,
+                                                                  (cfg.block_size, cfg.vocab)))
             for i in range(cfg.n_draft_layers):
                 g = dfl.dflare_debug_read(model.h, dfl.DBG_HIDDEN, i, (cfg.block_size, cfg.hidden))
                 e = P.relinf(g, ref["hidden"][i])
