@@ -438,6 +438,24 @@ int dflare_weighted_ce(const float* logits, const int32_t* labels, int32_t rows,
                        float* loss, float* row_ce, float* dlogits, void* workspace, size_t workspace_bytes,
                        void* stream);
 
+/*
+ * dflare_weighted_ce_noalloc -- the weighted CE above for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, results and kernels as dflare_weighted_ce, without the
+ * workspace: the row weights and 1 / sum w live in a fixed device array of the library
+ * (DFLARE_WEIGHTED_CE_NOALLOC_MAX_ROWS + 64 floats, 256 KiB + 256 B; each GPU the library
+ * runs on holds its own copy until the process ends).  Calls no hipMalloc, hipFree or other
+ * allocating routine.  rows > DFLARE_WEIGHTED_CE_NOALLOC_MAX_ROWS: INVALID_ARG; a non-NULL
+ * `stream` must belong to the current device (else INVALID_ARG).  The array is shared by
+ * every call on a GPU and keeps the last call's contents (each call writes every value it
+ * reads before reading it): calls that overlap in time on one GPU (different streams, or
+ * different host threads) race and give undefined results; calls ordered on one stream do
+ * not.
+ */
+#define DFLARE_WEIGHTED_CE_NOALLOC_MAX_ROWS 65536
+int dflare_weighted_ce_noalloc(const float* logits, const int32_t* labels, int32_t rows, int32_t V, int32_t B,
+                               float gamma, float* loss, float* row_ce, float* dlogits, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,6 +18,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "device_common.h"
@@ -1156,15 +1157,14 @@ int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_
 
 size_t dflare_weighted_ce_workspace(int32_t rows) { return ((size_t)3 * rows + 64) * 4; }
 
-int dflare_weighted_ce(const float* logits, const int32_t* labels, int32_t rows, int32_t V, int32_t B, float gamma,
-                       float* loss, float* row_ce, float* dlogits, void* workspace, size_t workspace_bytes,
-                       void* stream) {
-  if (!logits || !labels || !loss || !row_ce || !dlogits || !workspace || rows < 1 || V < 1 || B < 1 ||
-      rows % B || !(gamma > 0.f) || !isfinite(gamma))
-    return DFLARE_ERR_INVALID_ARG;
-  if (workspace_bytes < dflare_weighted_ce_workspace(rows)) return DFLARE_ERR_INVALID_ARG;
-  hipStream_t st = (hipStream_t)stream;
-  float* w = static_cast<float*>(workspace);
+}  // extern "C"
+
+namespace {
+
+// The four launches of the weighted CE; w holds at least rows + 1 floats (the row weights,
+// then 1 / sum w), every one written by the first launch before any other reads it.
+void launch_weighted_ce(hipStream_t st, const float* logits, const int32_t* labels, int32_t rows, int32_t V,
+                        int32_t B, float gamma, float* loss, float* row_ce, float* dlogits, float* w) {
   float* inv = w + rows;
   hipLaunchKernelGGL(k_wce_weights, dim3(1), dim3(256), 0, st, labels, rows, V, B, gamma, w, inv);
   if (V % 4 == 0 && (long)V >= kCeOMin && (long)V <= kCeOCap)
@@ -1174,6 +1174,69 @@ int dflare_weighted_ce(const float* logits, const int32_t* labels, int32_t rows,
     hipLaunchKernelGGL(k_wce_fused, dim3(std::min(rows, kCeRows)), dim3(kCeT), 0, st, logits, labels, rows, V, B,
                        (const float*)w, (const float*)inv, row_ce, dlogits);
   hipLaunchKernelGGL(k_wce_loss, dim3(1), dim3(256), 0, st, w, row_ce, rows, loss);
+}
+
+bool ce_args_ok(const float* logits, const int32_t* labels, int32_t rows, int32_t V, int32_t B, float gamma,
+                const float* loss, const float* row_ce, const float* dlogits) {
+  return logits && labels && loss && row_ce && dlogits && rows >= 1 && V >= 1 && B >= 1 && rows % B == 0 &&
+         gamma > 0.f && isfinite(gamma);
+}
+
+// Scratch of the allocation-free weighted CE: the row weights and 1 / sum w of one call.
+// Each GPU the library runs on holds its own copy until the process ends.  In host code the
+// array's name is not a device address: kernels get the address hipGetSymbolAddress returns
+// for the current device, looked up once per device.
+constexpr int kCeNoAllocMaxRows = DFLARE_WEIGHTED_CE_NOALLOC_MAX_ROWS;
+__device__ __align__(256) float scratch[kCeNoAllocMaxRows + 64];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float* g_scratch[kMaxDevices];
+
+// address of this device's scratch array (the device of `st`, which must be current)
+int scratch_address(hipStream_t st, float** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return DFLARE_ERR_HIP;
+  if (st) {
+    int sdev = -1;
+    if (hipStreamGetDevice(st, &sdev) != hipSuccess) return DFLARE_ERR_HIP;
+    if (sdev != dev) return DFLARE_ERR_INVALID_ARG;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return DFLARE_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DFLARE_ERR_HIP;
+    g_scratch[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch[dev];
+  return DFLARE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dflare_weighted_ce(const float* logits, const int32_t* labels, int32_t rows, int32_t V, int32_t B, float gamma,
+                       float* loss, float* row_ce, float* dlogits, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  if (!ce_args_ok(logits, labels, rows, V, B, gamma, loss, row_ce, dlogits) || !workspace)
+    return DFLARE_ERR_INVALID_ARG;
+  if (workspace_bytes < dflare_weighted_ce_workspace(rows)) return DFLARE_ERR_INVALID_ARG;
+  launch_weighted_ce((hipStream_t)stream, logits, labels, rows, V, B, gamma, loss, row_ce, dlogits,
+                     static_cast<float*>(workspace));
+  return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
+}
+
+int dflare_weighted_ce_noalloc(const float* logits, const int32_t* labels, int32_t rows, int32_t V, int32_t B,
+                               float gamma, float* loss, float* row_ce, float* dlogits, void* stream) {
+  if (!ce_args_ok(logits, labels, rows, V, B, gamma, loss, row_ce, dlogits)) return DFLARE_ERR_INVALID_ARG;
+  if (rows > kCeNoAllocMaxRows) return DFLARE_ERR_INVALID_ARG;
+  hipStream_t st = (hipStream_t)stream;
+  float* w = nullptr;
+  const int rc = scratch_address(st, &w);
+  if (rc != DFLARE_OK) return rc;
+  launch_weighted_ce(st, logits, labels, rows, V, B, gamma, loss, row_ce, dlogits, w);
   return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
 }
 

@@ -182,3 +182,17 @@ def test_weighted_ce_rejects_bad_arguments(L):
         assert ce(f, i32, 64, 1000, 16, gamma, f, f, f, p, need, None) == dfl.ERR_INVALID_ARG
     assert ce(None, i32, 64, 1000, 16, 4.5, f, f, f, p, need, None) == dfl.ERR_INVALID_ARG
     assert ce(f, i32, 64, 0, 16, 4.5, f, f, f, p, need, None) == dfl.ERR_INVALID_ARG
+
+
+def test_weighted_ce_noalloc_rejects_bad_arguments(L):
+    """Argument checks of the allocation-free CE come before any HIP call."""
+    f = ctypes.cast(0x1000, ctypes.POINTER(ctypes.c_float))
+    i32 = ctypes.cast(0x1000, ctypes.POINTER(ctypes.c_int32))
+    ce = L.dflare_weighted_ce_noalloc
+    big = dfl.WEIGHTED_CE_NOALLOC_MAX_ROWS + 16
+    assert ce(f, i32, big, 1000, 16, 4.5, f, f, f, None) == dfl.ERR_INVALID_ARG  # beyond the scratch
+    assert ce(f, i32, 60, 1000, 16, 4.5, f, f, f, None) == dfl.ERR_INVALID_ARG   # rows % B
+    for gamma in (0.0, -1.0, float("nan"), float("inf")):
+        assert ce(f, i32, 64, 1000, 16, gamma, f, f, f, None) == dfl.ERR_INVALID_ARG
+    assert ce(None, i32, 64, 1000, 16, 4.5, f, f, f, None) == dfl.ERR_INVALID_ARG
+    assert ce(f, i32, 64, 1000, 16, 4.5, f, f, None, None) == dfl.ERR_INVALID_ARG
