@@ -36,7 +36,10 @@ constexpr int kMaxBlocks = 1024;  // work-groups of the draft-block kernel
 // Split-K arrival counters: one per (GEMM phase kind, output range), each on its own
 // 128 B line, after the grid-barrier counters and the LM-head completion counter.
 constexpr int kSplitKinds = 4;    // QKV, O, gate/up, down
-constexpr long kSyncBytes = 4096 + (long)kSplitKinds * kMaxBlocks * 128;
+// Attention arrival counters: one per KV head, each on its own 128 B line, after the split-K ones.
+constexpr int kMaxKvHeads = 128;
+constexpr long kAttnCntOff = 4096 + (long)kSplitKinds * kMaxBlocks * 128;  // bytes
+constexpr long kSyncBytes = kAttnCntOff + (long)kMaxKvHeads * 128;
 // Zero k-tiles after the K real ones in every draft-block activation (A-fragment) plane:
 // a GEMM wave's run of k-tiles may reach past K, by less than 2 * 8 + 1 batches of 4.
 constexpr int kKtPad = 72;
@@ -71,6 +74,7 @@ struct DraftCall {
   float* hidden;        // optional [D, B, H]: block rows after each draft layer
   unsigned bar_epoch;   // grid barriers completed by earlier launches
   unsigned done_epoch;  // launches that ran the LM phase before this one
+  unsigned acnt_base;   // value of every attention arrival counter before this launch
   unsigned long long* trace;  // optional [blocks][phases][kTraceSlots] wall clock at marks of each phase
   // candidate selection: inv_temp = 0 greedy argmax; otherwise argmax of z * inv_temp plus
   // Gumbel noise of draw `draw` under `seed` (sequence slot 0)
@@ -88,6 +92,8 @@ struct DraftCall {
 // the LM-head partial maxima); see the kernel source for the rule.
 struct DraftArgs {
   // shapes
+  // nch: attention chunks per layer the partial buffers hold (context keys per chunk: 128 at
+  // head size 128, 256 at head size 64)
   int H, F, V, D, B, hd, n_q, n_kv, Lcap, Rpad, chunk, nch;
   float eps, qscale;
   // GEMM plan of each phase kind: the work-groups form blocks / kg output ranges of
@@ -115,8 +121,9 @@ struct DraftArgs {
   long xa_stride;
   float* Q;              // per layer: rotated queries [16, q_dim]
   long q_stride;
-  float* OP;             // attention partials [nch, n_kv, Rpad, hd]
-  float2* ML;            // [nch, n_kv, Rpad] (running max, sum), log2 domain
+  uint16_t* OP;          // attention partials [D, nch, n_kv, G * 16, hd] fp16, divided by their sums
+                         // (row t*16 + b: query head t of the KV head, block position b)
+  float2* ML;            // [D, nch, n_kv, G * 16] (running max, sum), log2 domain
   u32x4* OA;             // per layer: A fragments of the attention output
   long oa_stride;
   u32x4* HA;             // per layer: A fragments of the SwiGLU output
@@ -125,6 +132,7 @@ struct DraftArgs {
   int* pidx;
   float* part;           // split-K partial sums [blocks][kTNMax][64 lanes][4]
   unsigned* kcnt;        // split-K arrival counters [kSplitKinds][kMaxBlocks], 32 words apart
+  unsigned* acnt;        // attention arrival counters [n_kv], 32 words apart, monotonic across launches
   // synchronisation
   unsigned* bar;          // kBarCounters counters, 32 words apart, monotonic across launches
   unsigned* done;         // LM-head completion counter, monotonic across launches

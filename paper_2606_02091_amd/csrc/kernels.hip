@@ -416,16 +416,19 @@ __device__ __forceinline__ void phase_begin(Args a, Call c, const PhaseCtl& pc,
 }
 
 // ---- EMBED: X = E[ids] (fp32), sums of squares and A fragments of X * g_attn^(0) (stage 0)
+// Item = 8 columns of one row; items 2m and 2m + 1 (one 16-column tile) go to threads 2k and
+// 2k + 1 of work-group m % blocks, so the work spreads over every work-group and the two
+// halves of a tile meet in one shuffle.
 __device__ void phase_embed(Args a, Call c) {
   const int H = a->H, Kt = H / 32, per_row = H / 8;
-  const int total = a->B * per_row;
+  const int pairs = a->B * per_row / 2;
   const float* gain = a->g_attn;
   float* XS = a->XS;
   uint32_t* xhi = reinterpret_cast<uint32_t*>(a->XA);
   uint32_t* xlo = reinterpret_cast<uint32_t*>(a->XA + (long)(Kt + kKtPad) * 64);
-  // Item = 8 columns of one row.  total is even and so is the stride, so the two lanes of
-  // a 16-column tile (items 2j, 2j+1) always run the loop body together.
-  for (int item = blockIdx.x * kThreads + opaque(threadIdx.x); item < total; item += gridDim.x * kThreads) {
+  const int tid = opaque(threadIdx.x);
+  for (int m = blockIdx.x + (tid >> 1) * gridDim.x; m < pairs; m += (kThreads / 2) * gridDim.x) {
+    const int item = 2 * m + (tid & 1);
     const int row = item / per_row, k0 = (item % per_row) * 8;
     int id = gbl(c->ids)[row];
     id = id < 0 ? 0 : (id >= a->V ? a->V - 1 : id);
@@ -443,8 +446,8 @@ __device__ void phase_embed(Args a, Call c) {
     }
     sq += __shfl_xor(sq, 1);
     float* xo = a->X + (long)row * H + k0;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) st_wt(xo + e, f[e]);
+    st_wt16(xo, u32x4{__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]), __float_as_uint(f[3])});
+    st_wt16(xo + 4, u32x4{__float_as_uint(f[4]), __float_as_uint(f[5]), __float_as_uint(f[6]), __float_as_uint(f[7])});
     u32x4 hi, lo;
     split_pack8(y, hi, lo);
     const long fo = frag_off(row, k0, Kt);  // in bf16 elements
@@ -970,203 +973,162 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
   }
 }
 
-// ---- ATTN: block attention, split over the key axis ----
+// ---- ATTN + COMB: block attention split over the key axis, and the merge of the splits ----
 // Sec. 3.2: no mask; every block row attends to the whole context and the whole block.
-// Work item (chunk c, KV head g): keys [c*CK, (c+1)*CK) of the context, the last chunk also
-// the B block keys (cache slots L .. L+B-1, written by the QKV phase).  K rows and V^T rows
-// of the chunk (fp16) are staged in LDS (16-byte pieces, XOR-swizzled columns so that
-// fragment reads of 16 different rows hit different banks).  The pieces of context keys
-// are requested before the grid barrier; only the block keys and the queries depend on the
-// QKV phase, and the early requests never touch a cache line that the QKV phase writes (K
-// rows are whole lines; a V^T line is requested early only if all its 64 slots are
-// context).  The G*B query rows that share head g form QT tiles of 16 (row r -> query head
-// g*G + r/B, block row r%B); the waves form KS = 8 / QT groups of QT, group k taking the
-// k-th of KS runs of 32-key blocks, so that all waves share the work.  Scores are formed
-// transposed, S^T = K Q^T, so that the probabilities land in exactly the B-operand layout
-// of the P V product and never leave registers.  Queries and probabilities enter the fp16
-// matrix cores as hi/lo pairs (about 22 significant bits) against the fp16 keys and values.
-// The KS partial results of a query tile (running max, sum, unnormalised output) are
-// merged through LDS in group order.
-// Shape of an attention work item.
+//
+// Work item (chunk c, KV head g): context keys [c*CK, c*CK + CK); the last chunk holds keys
+// [c*CK, L + B): its context tail, then the B block keys (cache slots L .. L+B-1, written by
+// the QKV phase).  Rows of an item: the G query heads of g times 16 block positions (row
+// t*16 + b is query head g*G + t at position b; rows b >= B are zero queries, dropped).
+// K rows and V^T rows of the item (fp16) sit in the LDS staging area in 16-byte pieces with
+// XOR-swizzled columns (kswz, vswz: the eight lanes of every 16-byte LDS access read eight
+// different 16-byte bank groups).  The context pieces are streamed in ahead, in an earlier
+// phase, by waves that issue no other loads there; pieces that hold slot L or later (K rows of the block keys and beyond, V^T lines of
+// 64 keys that reach slot L) are not fetched then, because the QKV phase writes them (a cache
+// line is read in a launch only after its last write there), and are loaded after it.
+// Wave w takes query head t = w % G against part w / G of the item's 32-key blocks.  Scores
+// are formed transposed, S^T = K Q^T, so that the probabilities land in the B-operand layout
+// of the P V product and never leave registers: the A rows of the two 16-key score tiles of
+// a block are keys 8*(i/4) + (i%4) and 8*(i/4) + 4 + (i%4), so lane group qd ends up holding
+// keys 8 qd .. 8 qd + 7, one 16-byte V^T piece per lane for the P V product.  Queries and
+// probabilities enter the fp16 matrix cores as hi/lo pairs (about 22 significant bits).  The
+// parts meet in LDS, and the item's partial (running max and sum in the log2 domain, output
+// divided by the sum, in fp16) is stored.
+// COMB: once every item of KV head g is stored (one counter per KV head in the persistent
+// launch, instead of a grid barrier), the work-groups that held them merge the chunks, each
+// a share of the rows, and write the A fragments of the output projection.
 template <int HD>
 struct AttnShape {
-  static constexpr int CK = kChunk;
-  static constexpr int CKM = CK + 32;   // keys held by a work-group (room for the B <= 16 block keys)
-  static constexpr int NKB = CKM / 32;  // 32-key blocks of a work item
-  static constexpr int KC = HD / 8;     // 16-byte columns of a K row
-  static constexpr int VC = CKM / 8;    // 16-byte columns of a V^T row (a multiple of 4)
+  static constexpr int CK = HD == 64 ? 256 : 128;  // context keys per chunk
+  static constexpr int CKM = CK + 32;              // key slots held (room for the B <= 16 block keys)
+  static constexpr int NKB = CKM / 32;             // 32-key blocks
+  static constexpr int KC = HD / 8;                // 16-byte pieces of a K row
+  static constexpr int VC = CKM / 8;               // 16-byte pieces of a V^T row (a multiple of 4)
   static constexpr int KP = CKM * KC, VP = HD * VC;
-  static constexpr int PER = (KP + VP) / kThreads;  // pieces per thread
-  static_assert((KP + VP) % kThreads == 0, "pieces must split evenly over the work-group");
+  static constexpr int KB = KP / 64, VB = VP / 64;  // 1 KiB staging blocks
+  static_assert(KP % 64 == 0 && VP % 64 == 0, "whole staging blocks");
+  static_assert(kStageOff + (KP + VP) * 16 <= kLdsBytes, "LDS staging");
 };
 
-// Request the pieces of attention item j (chunk j / n_kv, KV head j % n_kv) of a layer:
-// pass 0 = context keys only, pass 1 = the rest.  Pieces that a pass does not load keep
-// their value.  The thread index is laundered so that the compiler recomputes the piece
-// coordinates here instead of keeping them in registers for the whole kernel.
-template <int HD>
-__device__ __forceinline__ void attn_issue(Args a, Call dc, int layer, int j, int pass, u32x4* pcs) {
-  using A = AttnShape<HD>;
-  int t = threadIdx.x;
-  asm volatile("" : "+v"(t));
-  const int L = dc->L;
-  const int nch = max(1, (L + A::CK - 1) / A::CK);
-  const int c = j / a->n_kv, g = j % a->n_kv;
-  const int kbeg = c * A::CK;
-  const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + A::CK) - kbeg;
-  const uint16_t* kc = a->kc + layer * a->cache_layer;
-  const uint16_t* vt = a->vt + layer * a->cache_layer;
-#pragma unroll
-  for (int i = 0; i < A::PER; ++i) {
-    const int p = i * kThreads + t;
-    if (p < A::KP) {
-      const int r = p / A::KC, col = p % A::KC;
-      const bool ctx = kbeg + r < L;
-      if (r < nkeys && (pass == 0 ? ctx : !ctx))
-        pcs[i] = *gbl(reinterpret_cast<const u32x4*>(kc + ((long)g * a->Lcap + kbeg + r) * HD + col * 8));
-    } else {
-      const int pv = p - A::KP;
-      const int d = pv / A::VC, col = pv % A::VC;
-      // requested early only if its whole 128-byte line (64 keys) precedes slot L: the line
-      // holding slot L also receives the block's values in the QKV phase
-      const bool ctx = ((kbeg + col * 8) & ~63) + 64 <= L;
-      if (col * 8 < nkeys && (pass == 0 ? ctx : !ctx))
-        pcs[i] = *gbl(reinterpret_cast<const u32x4*>(vt + ((long)g * HD + d) * a->Lcap + kbeg + col * 8));
-    }
-  }
-}
+__device__ __forceinline__ int attn_chunks(int L, int CK) { return L > 0 ? (L + CK - 1) / CK : 1; }
+// LDS column swizzles of the staging area: K row r, V^T row d
+__device__ __forceinline__ int kswz(int r) { return (r & 3) | ((r >> 1) & 4); }
+__device__ __forceinline__ int vswz(int d) { return (d >> 1) & 3; }
 
 // Stream the context pieces of attention item j of `layer` into the LDS staging area with
 // LDS-direct loads, by waves w0 .. 7: one instruction fills 64 consecutive staging slots
 // (1 KiB), lane l fetching the piece that belongs in slot l, so the swizzled layout comes
-// for free.  Slots whose piece is not a context piece (block keys, lines shared with them,
-// keys past the end) are filled with some cache piece; the attention phase overwrites
-// them.  Issued in a phase that does not touch the staging area, by waves that wait for no
-// memory until the phase ends (their arrival at the grid barrier completes the loads).
+// for free.  Slots whose piece is not fetched early get the cache's first piece.
 template <int HD>
-__device__ __forceinline__ void attn_dma(Args a, Call dc, int layer, int j, u32x4* smem, int w0) {
+__device__ __forceinline__ void attn_stage(Args a, Call dc, int layer, int j, u32x4* smem, int w0) {
   using A = AttnShape<HD>;
-  static_assert(A::KP % 64 == 0 && A::VP % 64 == 0, "whole 64-slot blocks");
-  constexpr int NB = (A::KP + A::VP) / 64;
-  const int L = dc->L;
-  const int nch = max(1, (L + A::CK - 1) / A::CK);
+  const int L = dc->L, nkv = a->n_kv;
   const int wave = __builtin_amdgcn_readfirstlane(opaque(threadIdx.x) >> 6);
-  if (j >= nch * a->n_kv || wave < w0) return;
-  const int c = j / a->n_kv, g = j % a->n_kv;
-  const int kbeg = c * A::CK;
-  const int nkeys = ((c == nch - 1) ? L + a->B : kbeg + A::CK) - kbeg;
-  const uint16_t* kc = a->kc + layer * a->cache_layer;
-  const uint16_t* vt = a->vt + layer * a->cache_layer;
+  if (wave < w0 || j >= attn_chunks(L, A::CK) * nkv) return;
+  const int c = j / nkv, g = j - (j / nkv) * nkv;
+  const int kbeg = c * A::CK, Lcap = a->Lcap;
+  const uint16_t* kc = a->kc + layer * a->cache_layer + (long)g * Lcap * HD + (long)kbeg * HD;
+  const uint16_t* vt = a->vt + layer * a->cache_layer + (long)g * HD * Lcap + kbeg;
   const int lane = opaque(threadIdx.x) & 63;
+  constexpr int RPB = 64 / A::KC;  // K rows per staging block
+  const int lr = lane / A::KC, lcol = lane % A::KC;
+  const int ctx = L - kbeg;        // item-relative slots below ctx are context
   LDSP char* stage = (LDSP char*)(char*)smem + kStageOff;
-  for (int bl = wave - w0; bl < NB; bl += kWaves - w0) {
-    const int p = bl * 64 + lane;  // staging slot
+  for (int bl = wave - w0; bl < A::KB + A::VB; bl += kWaves - w0) {
     const uint16_t* src;
-    bool ok;
-    if (bl * 64 < A::KP) {
-      const int r = p / A::KC, col = (p % A::KC) ^ (r & 7);
-      ok = r < nkeys && kbeg + r < L;
-      src = kc + ((long)g * a->Lcap + kbeg + r) * HD + col * 8;
+    if (bl < A::KB) {
+      const int r = bl * RPB + lr;
+      src = r < ctx ? kc + r * HD + ((lcol ^ kswz(r)) << 3) : a->kc;
     } else {
-      const int pv = p - A::KP;
-      const int d = pv / A::VC, col = (pv % A::VC) ^ (d & 3);
-      ok = col * 8 < nkeys && ((kbeg + col * 8) & ~63) + 64 <= L;
-      src = vt + ((long)g * HD + d) * a->Lcap + kbeg + col * 8;
+      const int p = (bl - A::KB) * 64 + lane;
+      const int d = p / A::VC;
+      const int col = (p - d * A::VC) ^ vswz(d);
+      // a V^T line (64 keys) is fetched early only if all its keys are context
+      const int line_end = ((kbeg + col * 8) & ~63) + 64 - kbeg;
+      src = line_end <= ctx ? vt + d * Lcap + col * 8 : a->kc;
     }
-    // every lane loads; slots that are not context pieces get the cache's first piece, and
-    // the attention phase overwrites them
-    __builtin_amdgcn_global_load_lds(ok ? src : kc, stage + bl * 1024, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(src, stage + bl * 1024, 16, 0, 0);
   }
 }
 
 template <int HD>
 __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed,
-                                           u32x4* smem, bool have_dma) {
+                                           u32x4* smem, bool staged) {
   using A = AttnShape<HD>;
-  constexpr int CK = A::CK, CKM = A::CKM, NKB = A::NKB, KC = A::KC, VC = A::VC, KP = A::KP, VP = A::VP,
-                PER = A::PER;
-  constexpr int DT = HD / 16;                // 16-dim tiles of an output row
+  constexpr int CK = A::CK, NKB = A::NKB, KC = A::KC, VC = A::VC, KP = A::KP;
+  constexpr int DT = HD / 16;  // 16-dim tiles of an output row
   static_assert(KC >= 8, "K swizzle needs 8 columns");
-  u32x4* sK = smem + kStageOff / 16;                       // (row r, column c) at r*KC + (c ^ (r & 7))
-  u32x4* sV = sK + KP;                                     // (row d, column c) at d*VC + (c ^ (d & 3))
-  f32x4* sO = reinterpret_cast<f32x4*>(smem);              // merge: [kWaves][DT][64]
+  u32x4* sK = smem + kStageOff / 16;                               // (row r, col) at r*KC + (col ^ kswz(r))
+  u32x4* sV = sK + KP;                                             // (row d, col) at d*VC + (col ^ vswz(d))
+  f32x4* sO = reinterpret_cast<f32x4*>(smem);                      // merge: [kWaves][DT][64]
   float2* sML = reinterpret_cast<float2*>(sO + kWaves * DT * 64);  // [kWaves][16]
-  static_assert(kStageOff + (KP + VP) * 16 <= kLdsBytes, "LDS staging");
   static_assert(kWaves * DT * 64 * 16 + kWaves * 16 * 8 <= kStageOff, "LDS merge area");
-  (void)CKM;
 
+  const int L = dc->L, B = a->B, nkv = a->n_kv, G = a->n_q / a->n_kv, Lcap = a->Lcap;
+  const int nch = attn_chunks(L, CK);
+  const int items = nch * nkv;
+  const int KS = kWaves / G;  // key parts
   const int tid = opaque(threadIdx.x), lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int L = dc->L;
-  const int nch = max(1, (L + CK - 1) / CK);
-  const int items = nch * a->n_kv;
-  const int G = a->n_q / a->n_kv;
-  const int R = G * a->B;
-  const int QT = (R + 15) / 16, KS = kWaves / QT;
-  const float* Q = a->Q + layer * a->q_stride;
+  const int t = w % G, kh = w / G;
+  const bool active = kh < KS;
+  const int q = lane & 15, qd = lane >> 4;
+  const float* Qg = a->Q + layer * a->q_stride;
   const int q_dim = a->n_q * HD;
-  auto issue = [&](int j, int pass, u32x4* pcs) { attn_issue<HD>(a, dc, layer, j, pass, pcs); };
 
-  // everything of item j after its context pieces were requested
-  auto finish = [&](int j, u32x4* pcs, bool dma) {
-    issue(j, 1, pcs);
-    const int c = j / a->n_kv, g = j % a->n_kv;
-    const int nkeys = ((c == nch - 1) ? L + a->B : c * CK + CK) - c * CK;
-    const int qt = w % QT, kh = w / QT;
-    const bool active = kh < KS;  // wave-uniform
-    const int q = lane & 15, quad = lane >> 4;
-    const int r = qt * 16 + q;
-    const bool rv = r < R;
-    // this wave's 32-key blocks [kb0, kb1)
-    const int nkb = (nkeys + 31) / 32, bps = (nkb + KS - 1) / KS;
-    const int kb0 = min(kh * bps, nkb), kb1 = min(kb0 + bps, nkb);
-    float4 qx[HD / 16];
+  // one item: everything after its context pieces are in LDS (or, without staging, all of it)
+  auto item = [&](int j, bool ctx_staged) {
+    const int c = j / nkv, g = j - (j / nkv) * nkv;
+    const int kbeg = c * CK;
+    const bool last = c == nch - 1;
+    const int nkeys = last ? L + B - kbeg : CK;
+    const uint16_t* kc = a->kc + layer * a->cache_layer + (long)g * Lcap * HD + (long)kbeg * HD;
+    const uint16_t* vt = a->vt + layer * a->cache_layer + (long)g * HD * Lcap + kbeg;
+    // queries of this wave's head: lane (row q, dims 8 qd .. 8 qd + 7 of each 32-dim slice)
+    u32x4 qx[HD / 16];
     {
-      const int bb = rv ? r % a->B : 0;
-      const int h = g * G + (rv ? r / a->B : 0);
+      const float* src = Qg + q * q_dim + (g * G + t) * HD + qd * 8;
 #pragma unroll
       for (int ks = 0; ks < HD / 32; ++ks) {
-        const float* src = Q + (long)bb * q_dim + h * HD + ks * 32 + quad * 8;
-        qx[2 * ks] = make_float4(0.f, 0.f, 0.f, 0.f);
-        qx[2 * ks + 1] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (active && rv) {
-          const u32x4 q0 = *gbl(reinterpret_cast<const u32x4*>(src));
-          const u32x4 q1 = *gbl(reinterpret_cast<const u32x4*>(src + 4));
-          qx[2 * ks] = make_float4(__uint_as_float(q0[0]), __uint_as_float(q0[1]), __uint_as_float(q0[2]),
-                                   __uint_as_float(q0[3]));
-          qx[2 * ks + 1] = make_float4(__uint_as_float(q1[0]), __uint_as_float(q1[1]), __uint_as_float(q1[2]),
-                                       __uint_as_float(q1[3]));
-        }
+        qx[2 * ks] = *gbl(reinterpret_cast<const u32x4*>(src + ks * 32));
+        qx[2 * ks + 1] = *gbl(reinterpret_cast<const u32x4*>(src + ks * 32 + 4));
       }
     }
-    // pieces to LDS (values of keys past the end become zeros)
-    int tid2 = threadIdx.x;
-    asm volatile("" : "+v"(tid2));
-    const int kbeg = c * CK;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int p = i * kThreads + tid2;
-      if (p < KP) {
-        const int rr = p / KC, col = p % KC;
-        if (!(dma && rr < nkeys && kbeg + rr < L)) sK[rr * KC + (col ^ (rr & 7))] = pcs[i];
-      } else {
-        const int pv = p - KP;
-        const int d = pv / VC, col = pv % VC;
-        if (dma && col * 8 < nkeys && ((kbeg + col * 8) & ~63) + 64 <= L) continue;  // streamed in already
-        u32x4 v = pcs[i];
-        const int nv = nkeys - col * 8;  // valid keys in this piece
-        if (nv < 8) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (2 * e >= nv) v[e] = 0u;
-            else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;
-          }
-        }
-        sV[d * VC + (col ^ (d & 3))] = v;
+    // pieces still missing: without staging every piece of the item's keys; with staging those
+    // holding slot L or later (only the last chunk has them)
+    if (!ctx_staged) {
+      const int nkr = min(nkeys, A::CKM);
+      for (int p = tid; p < nkr * KC; p += kThreads) {
+        const int r = p / KC, col = p % KC;
+        sK[r * KC + (col ^ kswz(r))] = *gbl(reinterpret_cast<const u32x4*>(kc + r * HD + col * 8));
+      }
+      // V^T pieces of every 32-key block that is processed (keys past the end must be finite)
+      const int nvc = ((nkeys + 31) >> 5) * 4;
+      for (int p = tid; p < HD * nvc; p += kThreads) {
+        const int d = p / nvc, col = p - (p / nvc) * nvc;
+        sV[d * VC + (col ^ vswz(d))] = *gbl(reinterpret_cast<const u32x4*>(vt + d * Lcap + col * 8));
+      }
+    } else if (last) {
+      const int rL = L - kbeg;  // first block row
+      for (int p = tid; p < B * KC; p += kThreads) {
+        const int r = rL + p / KC, col = p % KC;
+        sK[r * KC + (col ^ kswz(r))] = *gbl(reinterpret_cast<const u32x4*>(kc + r * HD + col * 8));
+      }
+      // V^T pieces of the 64-key lines that reach slot L, inside the item's window
+      const int c0 = (((L & ~63) - kbeg) >> 3) > 0 ? ((L & ~63) - kbeg) >> 3 : 0;
+      const int c1 = min(VC, (((L + B + 63) & ~63) - kbeg) >> 3);
+      const int nv = c1 - c0;
+      for (int p = tid; p < HD * nv; p += kThreads) {
+        const int d = p / nv, col = c0 + p - (p / nv) * nv;
+        sV[d * VC + (col ^ vswz(d))] = *gbl(reinterpret_cast<const u32x4*>(vt + d * Lcap + col * 8));
       }
     }
     __syncthreads();
     if (j == (int)blockIdx.x) trace_mark(dc, pc.slot + 1, pc.nslots);
+
+    // this wave's 32-key blocks [kb0, kb1)
+    const int nkb = (nkeys + 31) >> 5, bps = (nkb + KS - 1) / KS;
+    const int kb0 = min(kh * bps, nkb), kb1 = min(kb0 + bps, nkb);
     float m = -INFINITY, l = 0.f;
     f32x4 o[DT];
 #pragma unroll
@@ -1175,27 +1137,26 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
       u32x4 qh[HD / 32], ql[HD / 32];
 #pragma unroll
       for (int ks = 0; ks < HD / 32; ++ks) {
-        const float4 x0 = qx[2 * ks], x1 = qx[2 * ks + 1];
-        float v[8] = {x0.x * a->qscale, x0.y * a->qscale, x0.z * a->qscale, x0.w * a->qscale,
-                      x1.x * a->qscale, x1.y * a->qscale, x1.z * a->qscale, x1.w * a->qscale};
+        const float s = a->qscale;
+        const u32x4 x0 = qx[2 * ks], x1 = qx[2 * ks + 1];
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = __uint_as_float(x0[e]) * s;
+          v[4 + e] = __uint_as_float(x1[e]) * s;
+        }
         split_pack8_h(v, qh[ks], ql[ks]);
       }
-      // LDS read addresses: per-lane byte bases plus compile-time offsets, so that every read
-      // takes its offset as an immediate (row kt*16 + q has swizzle key q & 7; row
-      // d = dt*16 + q has key q & 3).  The bases are laundered so that the compiler neither
-      // folds them into per-read registers nor keeps them alive outside this block.
+      // LDS read addresses: per-lane byte bases plus compile-time offsets.  Score tile kt of a
+      // block reads K row 8*(q/4) + 4*kt + (q%4) (its swizzle is kswz of that row, the same for
+      // every block and tile); V^T row d = dt*16 + q has swizzle vswz(q).
       const char* lds = reinterpret_cast<const char*>(smem);
-      const int ln = opaque(threadIdx.x & 63);
-      const int qq = ln & 15, qd = ln >> 4;
+      const int kr = 8 * (q >> 2) + (q & 3), ksw = kswz(kr);
       int k_at[HD / 32];
 #pragma unroll
-      for (int ks = 0; ks < HD / 32; ++ks) k_at[ks] = opaque(kStageOff + (qq * KC + ((ks * 4 + qd) ^ (qq & 7))) * 16);
-      const int vx = (qd >> 1) ^ (qq & 3);
-      const int vbase = kStageOff + KP * 16 + (qd & 1) * 8;  // sV, half of a 16-byte column
-      const int v0 = opaque(vbase + (qq * VC + vx) * 16), v1 = opaque(vbase + (qq * VC + (vx ^ 2)) * 16);
-      // scores of the wave's blocks (blocks outside [kb0, kb1) and keys past the end: -inf).
-      // Per 32-key block, four independent accumulation chains (two key tiles x hi/lo query
-      // parts) keep the matrix cores busy.
+      for (int ks = 0; ks < HD / 32; ++ks) k_at[ks] = opaque(kStageOff + (kr * KC + ((ks * 4 + qd) ^ ksw)) * 16);
+      const int v_at = opaque(kStageOff + KP * 16 + (q * VC + (qd ^ vswz(q))) * 16);
+      // scores of the wave's blocks; other blocks and keys past the end: -inf
       f32x4 sc[2 * NKB];
 #pragma unroll
       for (int kk = 0; kk < NKB; ++kk) {
@@ -1205,8 +1166,8 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
           u32x4 k0v[HD / 32], k1v[HD / 32];
 #pragma unroll
           for (int ks = 0; ks < HD / 32; ++ks) {
-            k0v[ks] = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + (2 * kk) * 16 * KC * 16);
-            k1v[ks] = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + (2 * kk + 1) * 16 * KC * 16);
+            k0v[ks] = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + (kk * 32) * KC * 16);
+            k1v[ks] = *reinterpret_cast<const u32x4*>(lds + k_at[ks] + (kk * 32 + 4) * KC * 16);
           }
 #pragma unroll
           for (int ks = 0; ks < HD / 32; ++ks) {
@@ -1217,10 +1178,12 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
           }
           a0 = h0 + l0;
           a1 = h1 + l1;
+          if ((kk + 1) * 32 > nkeys) {  // the block reaches past the item's keys
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if (2 * kk * 16 + qd * 4 + i >= nkeys) a0[i] = -INFINITY;
-            if ((2 * kk + 1) * 16 + qd * 4 + i >= nkeys) a1[i] = -INFINITY;
+            for (int i = 0; i < 4; ++i) {
+              if (kk * 32 + qd * 8 + i >= nkeys) a0[i] = -INFINITY;
+              if (kk * 32 + qd * 8 + 4 + i >= nkeys) a1[i] = -INFINITY;
+            }
           }
         }
         sc[2 * kk] = a0;
@@ -1251,13 +1214,10 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
                          sc[2 * kk + 1][0], sc[2 * kk + 1][1], sc[2 * kk + 1][2], sc[2 * kk + 1][3]};
           u32x4 ph, pl;
           split_pack8_h(pv, ph, pl);
-          // keys kk*32 + 4*qd + 0..3 and + 16: 16-byte columns kk*4 + qd/2 and + 2, halves qd & 1
+          // keys kk*32 + 8*qd .. + 7: the 16-byte V^T piece kk*4 + qd of row dt*16 + q
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) {
-            const int off = (dt * 16 * VC + kk * 4) * 16;
-            const u32x2 h0 = *reinterpret_cast<const u32x2*>(lds + v0 + off);
-            const u32x2 h1 = *reinterpret_cast<const u32x2*>(lds + v1 + off);
-            const u32x4 vv = {h0[0], h0[1], h1[0], h1[1]};
+            const u32x4 vv = *reinterpret_cast<const u32x4*>(lds + v_at + (dt * 16 * VC + kk * 4) * 16);
             o[dt] = mfma_h(vv, ph, o[dt]);
             o[dt] = mfma_h(vv, pl, o[dt]);
           }
@@ -1265,130 +1225,184 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
       }
     }
     if (j == (int)blockIdx.x && w == 0) trace_mark(dc, pc.slot + 2, pc.nslots);
-    // merge the KS key runs of each query tile (group order), then store the item's partial
+    // merge the key parts of each head (part order), then store the item's partial
     if (KS > 1) {
-      if (active) {
+      if (active && kh > 0) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) sO[(w * DT + dt) * 64 + lane] = o[dt];
-        if (quad == 0) sML[w * 16 + q] = make_float2(m, l);
+        if (qd == 0) sML[w * 16 + q] = make_float2(m, l);
       }
       __syncthreads();
-      if (active && kh == 0) {
-        float M = -INFINITY;
-        for (int k = 0; k < KS; ++k) M = fmaxf(M, sML[(qt + k * QT) * 16 + q].x);
-        float lt = 0.f;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int k = 0; k < KS; ++k) {
-          const int wk = qt + k * QT;
+      if (kh == 0) {
+        for (int k = 1; k < KS; ++k) {
+          const int wk = t + k * G;
           const float2 mlk = sML[wk * 16 + q];
-          const float f = exp2f(mlk.x - M);  // 0 for a run without keys
-          lt += f * mlk.y;
+          const float M = fmaxf(m, mlk.x);
+          const float f0 = exp2f(m - M), f1 = exp2f(mlk.x - M);  // 0 for a part without keys
+          l = f0 * l + f1 * mlk.y;
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) o[dt] += f * sO[(wk * DT + dt) * 64 + lane];
+          for (int dt = 0; dt < DT; ++dt) o[dt] = f0 * o[dt] + f1 * sO[(wk * DT + dt) * 64 + lane];
+          m = M;
         }
-        m = M;
-        l = lt;
       }
     }
-    if (active && kh == 0 && rv) {
-      const long base = ((long)c * a->n_kv + g) * a->Rpad + r;
+    if (kh == 0 && q < B) {
+      const long row = ((long)layer * a->nch * nkv + (long)c * nkv + g) * (G * 16) + t * 16 + q;
+      uint16_t* op = a->OP + row * HD + qd * 4;
+      const float inv = 1.0f / l;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        st_wt16(a->OP + base * HD + dt * 16 + quad * 4, __builtin_bit_cast(u32x4, o[dt]));
-      if (quad == 0) st_wt8(a->ML + base, (uint64_t)__float_as_uint(m) | ((uint64_t)__float_as_uint(l) << 32));
+      for (int dt = 0; dt < DT; ++dt) {
+        const uint64_t hv = (uint64_t)f2h(o[dt][0] * inv) | ((uint64_t)f2h(o[dt][1] * inv) << 16) |
+                            ((uint64_t)f2h(o[dt][2] * inv) << 32) | ((uint64_t)f2h(o[dt][3] * inv) << 48);
+        st_wt8(op + dt * 16, hv);
+      }
+      if (qd == 0) st_wt8(a->ML + row, (uint64_t)__float_as_uint(m) | ((uint64_t)__float_as_uint(l) << 32));
     }
-    __syncthreads();  // LDS is refilled by the next item
+    // the item is stored: count it for its KV head
+    wait_vm();
+    __syncthreads();
+    if (tid == 0) __hip_atomic_fetch_add(a->acnt + g * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   };
 
-  // The first item's context pieces were streamed into LDS during an earlier phase
-  // (have_dma), or are requested here, before the barrier.  One call site for the item
-  // body keeps the phase's code small (it runs from a cold instruction cache).
-  const int j0 = blockIdx.x;
-  u32x4 pcs[PER];
-#pragma unroll
-  for (int i = 0; i < PER; ++i) pcs[i] = u32x4{0u, 0u, 0u, 0u};
-  if (!have_dma && j0 < items) issue(j0, 0, pcs);
+  // One call site for the item body keeps the phase's code small.
   phase_begin(a, dc, pc, failed);
-  for (int j = j0; j < items; j += gridDim.x) {
-    const bool dma = have_dma && j == j0;
-    if (j != j0) {
-#pragma unroll
-      for (int i = 0; i < PER; ++i) pcs[i] = u32x4{0u, 0u, 0u, 0u};
-      issue(j, 0, pcs);
-    }
-    finish(j, pcs, dma);
-  }
+  for (int j = blockIdx.x; j < items; j += gridDim.x) item(j, staged && j == (int)blockIdx.x);
 }
 
-// whether the combine phase leaves waves idle (they stage the next layer's attention item)
-__device__ __forceinline__ bool comb_stages(Args a) {
-  const int items = a->n_q * a->B;  // (query head, block row) pairs
-  return (items + (int)gridDim.x - 1) / (int)gridDim.x < kWaves;
-}
-
+// COMB: work-groups b < W * n_kv (W = work-groups per KV head) merge the chunks of KV head
+// g = b % n_kv for a share of its G*B rows, on waves 0-3: a row's chunks are split into S
+// runs over S waves (S = 4 / rows per work-group), which meet in LDS in run order.  Waves
+// 4-7 meanwhile stream the context of the next layer's attention item into LDS (stage).
 template <int HD>
-__device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed, u32x4* smem) {
-  constexpr int DPL = HD / 64;  // dims per lane
-  phase_begin(a, dc, pc, failed);
+__device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed, u32x4* smem,
+                           bool stage) {
+  using A = AttnShape<HD>;
+  constexpr int DPL = HD / 64;                 // dims per lane
+  constexpr int CB = DPL == 2 ? 16 : 32;       // chunks whose loads are in flight together
+  constexpr int CW = 4;                        // waves that merge
+  const int L = dc->L, B = a->B, nkv = a->n_kv, G = a->n_q / a->n_kv;
+  const int nch = attn_chunks(L, A::CK);
+  const int W = min(nch, (int)gridDim.x / nkv);
+  const int b = blockIdx.x;
+  if (stage) attn_stage<HD>(a, dc, layer + 1, b, smem, CW);
+  // the group wait: all items of KV head g stored (persistent launch; else the launch boundary)
+  if (pc.wait) {
+    if (b < W * nkv && threadIdx.x < 64 && !failed) {
+      const unsigned* cnt = a->acnt + (b % nkv) * 32;
+      const unsigned target = dc->acnt_base + (unsigned)(layer + 1) * (unsigned)nch;
+      const long long t0 = wall_clock64();
+      while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        __builtin_amdgcn_s_sleep(1);
+        if (wall_clock64() - t0 > kBarrierTimeout) {
+          failed = true;
+          if (threadIdx.x == 0) __hip_atomic_store(a->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          break;
+        }
+      }
+    }
+    __syncthreads();
+  }
+  trace_mark(dc, pc.slot, pc.nslots);
+  if (b >= W * nkv) return;
+  const int g = b % nkv, wi = b / nkv;
+  const int nrows = G * B;
+  const int rpw = (nrows + W - 1) / W;                 // rows of this work-group
+  const int r0 = wi * rpw, r1 = min(nrows, r0 + rpw);
+  const int S = rpw >= CW ? 1 : CW / rpw;              // runs per row
+  const int cps = (nch + S - 1) / S;                   // chunks per run
   const int lane = opaque(threadIdx.x) & 63;
-  const int G = a->n_q / a->n_kv, R = G * a->B;
-  const int nch = max(1, (dc->L + kChunk - 1) / kChunk);
-  const int items = a->n_kv * R;
-  // waves without a row to combine stream the next layer's first attention item into LDS
-  // (HBM is otherwise idle in this phase); with no idle wave, the attention phase loads it
-  if (comb_stages(a) && layer + 1 < a->D)
-    attn_dma<HD>(a, dc, layer + 1, blockIdx.x, smem, (items + (int)gridDim.x - 1) / (int)gridDim.x);
+  const int w = __builtin_amdgcn_readfirstlane(opaque(threadIdx.x) >> 6);
+  float* sN = reinterpret_cast<float*>(smem);          // [CW][64][DPL] run numerators
+  float2* sMD = reinterpret_cast<float2*>(sN + CW * 64 * DPL);  // [CW] run (max, denominator)
   const int q_Kt = a->n_q * HD / 32;
   uint32_t* ohi = reinterpret_cast<uint32_t*>(a->OA + layer * a->oa_stride);
   uint32_t* olo = reinterpret_cast<uint32_t*>(a->OA + layer * a->oa_stride + (long)(q_Kt + kKtPad) * 64);
-  const long cstride = (long)a->n_kv * a->Rpad;
-  // item i goes to wave i / blocks of work-group i % blocks: the items spread over all CUs
-  for (int it = blockIdx.x + (threadIdx.x >> 6) * gridDim.x; it < items; it += gridDim.x * kWaves) {
-    const int g = it / R, r = it % R;
-    const float2* ml = a->ML + (long)g * a->Rpad + r;
-    float M = -INFINITY;
-    for (int c = lane; c < nch; c += 64) M = fmaxf(M, ld_coh2(ml + c * cstride).x);
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
-    float num[DPL], den = 0.f;
+  const long cstride = (long)nkv * G * 16;  // rows between chunks
+  const long lbase = (long)layer * a->nch * cstride + (long)g * G * 16;
+  // rounds of (row, run) units: unit u = w + CW k -> row r0 + u / S, run u % S
+  const int units = (r1 - r0) * S;
+  for (int u0 = 0; u0 < units; u0 += CW) {
+    const int u = u0 + w;
+    const bool has = w < CW && u < units;
+    const int rr = r0 + (has ? u / S : 0), run = has ? u % S : 0;
+    const int tt = rr / B, bb = rr - (rr / B) * B;
+    const long row = lbase + tt * 16 + bb;
+    const int cb = run * cps, ce = has ? min(nch, cb + cps) : cb;
+    float M = -INFINITY, den = 0.f, num[DPL];
 #pragma unroll
     for (int e = 0; e < DPL; ++e) num[e] = 0.f;
-    const float* op = a->OP + ((long)g * a->Rpad + r) * HD + lane * DPL;
-    // 16 chunks per batch, all their loads in flight together (one memory round trip)
-    for (int c0 = 0; c0 < nch; c0 += 16) {
-      float2 mc[16];
-      float ov[16][DPL];
+    for (int c0 = cb; c0 < ce; c0 += CB) {
+      float2 mc[CB];
+      float ov[CB][DPL];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        const int c = min(c0 + u, nch - 1);
-        mc[u] = ld_coh2(ml + c * cstride);
+      for (int k = 0; k < CB; ++k) {
+        const long rc = row + (long)min(c0 + k, ce - 1) * cstride;
+        const uint64_t mlv = *gbl(reinterpret_cast<const uint64_t*>(a->ML + rc));
+        mc[k] = make_float2(__uint_as_float((uint32_t)mlv), __uint_as_float((uint32_t)(mlv >> 32)));
         if constexpr (DPL == 2) {
-          const float2 t = ld_coh2(op + c * cstride * HD);
-          ov[u][0] = t.x;
-          ov[u][1] = t.y;
+          const uint32_t v = *gbl(reinterpret_cast<const uint32_t*>(a->OP + rc * HD + 2 * lane));
+          ov[k][0] = h2f(v & 0xFFFFu);
+          ov[k][1] = h2f(v >> 16);
         } else {
-          ov[u][0] = ld_coh(op + c * cstride * HD);
+          ov[k][0] = h2f(*gbl(a->OP + rc * HD + lane));
         }
       }
+      float Mb = M;
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
-        if (c0 + u < nch) {
-          const float wgt = exp2f(mc[u].x - M);
-          den += wgt * mc[u].y;
+      for (int k = 0; k < CB; ++k) Mb = fmaxf(Mb, mc[k].x);
+      const float f = exp2f(M - Mb);  // rescale of the run so far (0 when it is empty)
+      den *= f;
 #pragma unroll
-          for (int e = 0; e < DPL; ++e) num[e] += wgt * ov[u][e];
+      for (int e = 0; e < DPL; ++e) num[e] *= f;
+#pragma unroll
+      for (int k = 0; k < CB; ++k) {
+        if (c0 + k < ce) {
+          const float wgt = exp2f(mc[k].x - Mb) * mc[k].y;  // a chunk's sum times its normalised output
+          den += wgt;
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) num[e] += wgt * ov[k][e];
         }
       }
+      M = Mb;
     }
-    const float inv = 1.0f / den;
-    const int bb = r % a->B, h = g * G + r / a->B;
-    if constexpr (DPL == 2) {
-      store_frag_pair_wt(ohi, olo, bb, h * HD + 2 * lane, q_Kt, num[0] * inv, num[1] * inv);
-    } else {
-      const float y = num[0] * inv;
-      const float y1 = __shfl_xor(y, 1);
-      if ((lane & 1) == 0) store_frag_pair_wt(ohi, olo, bb, h * HD + lane, q_Kt, y, y1);
+    if (w == 0 && u0 == 0) trace_mark(dc, pc.slot + 1, pc.nslots);
+    if (S > 1) {
+      // the runs of a row meet in LDS; the wave of run 0 finishes the row
+      if (w < CW) {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) sN[(w * 64 + lane) * DPL + e] = num[e];
+        if (lane == 0) sMD[w] = make_float2(M, den);
+      }
+      __syncthreads();
+      if (has && run == 0) {
+        float Mt = M;
+        for (int k = 1; k < S; ++k) Mt = fmaxf(Mt, sMD[w + k].x);
+        float dt = 0.f, nt[DPL];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) nt[e] = 0.f;
+        for (int k = 0; k < S; ++k) {
+          const float2 md = sMD[w + k];
+          const float f = exp2f(md.x - Mt);
+          dt += f * md.y;
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) nt[e] += f * sN[((w + k) * 64 + lane) * DPL + e];
+        }
+        den = dt;
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) num[e] = nt[e];
+      }
+      __syncthreads();
+    }
+    if (has && run == 0) {
+      const float inv = 1.0f / den;
+      const int k = (g * G + tt) * HD;
+      if constexpr (DPL == 2) {
+        store_frag_pair_wt(ohi, olo, bb, k + 2 * lane, q_Kt, num[0] * inv, num[1] * inv);
+      } else {
+        const float y = num[0] * inv;
+        const float y1 = __shfl_xor(y, 1);
+        if ((lane & 1) == 0) store_frag_pair_wt(ohi, olo, bb, k + lane, q_Kt, y, y1);
+      }
     }
   }
 }
@@ -1427,33 +1441,30 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
   const int nphase = phase_count(a->D);
   const int nslots = kTraceSlots * nphase;
   bool failed = false;
+  unsigned epoch = c->bar_epoch;  // grid barriers passed
   for (int p = p0; p < p1; ++p) {
     int kind, layer;
     phase_of(p, a->D, kind, layer);
     PhaseCtl pc;
-    pc.wait = p > p0;
-    pc.epoch = c->bar_epoch + (unsigned)(p - p0);
+    pc.wait = p > p0;  // the combine phase waits for its KV head's items, every other phase at a grid barrier
+    if (pc.wait && kind != PH_COMB) ++epoch;
+    pc.epoch = epoch;
     pc.slot = kTraceSlots * p;
     pc.nslots = nslots;
-    // The context pieces of a layer's first attention item are streamed into LDS during the
-    // previous layer's combine phase by its idle waves (the embedding phase for layer 0);
-    // the attention phase uses them when that phase ran in this launch.
     switch (kind) {
       case PH_EMBED:
         phase_begin(a, c, pc, failed);
         phase_embed(a, c);
-        attn_dma<HD>(a, c, 0, blockIdx.x, smem, 0);
+        attn_stage<HD>(a, c, 0, blockIdx.x, smem, 0);
         break;
       case PH_QKV:
         gemm_dispatch<EPI_QKV>(a, c, kind, layer, pc, failed, smem);
         break;
-      case PH_ATTN:
-        // staged by the embedding phase (layer 0) or by the previous layer's combine phase
-        phase_attn<HD>(a, c, layer, pc, failed, smem,
-                       layer == 0 ? p - 2 >= p0 : (p - 5 >= p0 && comb_stages(a)));
+      case PH_ATTN:  // staged by the embedding phase (layer 0) or the previous layer's combine phase
+        phase_attn<HD>(a, c, layer, pc, failed, smem, layer == 0 ? p - 2 >= p0 : p - 5 >= p0);
         break;
-      case PH_COMB:
-        phase_comb<HD>(a, c, layer, pc, failed, smem);
+      case PH_COMB:  // stages the next layer's first attention item when that phase runs in this launch
+        phase_comb<HD>(a, c, layer, pc, failed, smem, layer + 1 < a->D && p + 5 < p1);
         break;
       case PH_O:
         gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem);
@@ -1468,7 +1479,8 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
         gemm_dispatch<EPI_ARGMAX>(a, c, kind, layer, pc, failed, smem);
         break;
     }
-    if (p + 1 < p1) grid_arrive(a);
+    // the attention phase hands over to the combine phase through the per-KV-head counters
+    if (p + 1 < p1 && kind != PH_ATTN) grid_arrive(a);
     else wait_vm();
     trace_mark(c, kTraceSlots * p + kTraceSlots - 1, nslots);
   }

@@ -89,6 +89,7 @@ struct dflare_handle {
   bool coop_ok = false;    // the device keeps one work-group per CU resident
   GemmPlan plan[PH_COUNT];
   int attn_nch = 1;
+  int attn_chunk = 128;
   float* X = nullptr;
   float* XS = nullptr;
   long xs_stride = 0;
@@ -96,7 +97,7 @@ struct dflare_handle {
   long xa_stride = 0;
   float* Q = nullptr;
   long q_stride = 0;
-  float* OP = nullptr;
+  uint16_t* OP = nullptr;  // draft-block attention partials (fp16)
   float2* ML = nullptr;
   u32x4* OA = nullptr;
   long oa_stride = 0;
@@ -108,6 +109,7 @@ struct dflare_handle {
   DraftArgs* args_dev = nullptr;  // device copy of the draft kernel's fixed arguments
   unsigned* sync = nullptr;  // barrier counters, the LM-head completion counter, split-K counters
   unsigned bar_epoch = 0, done_epoch = 0;
+  unsigned acnt_epoch = 0;  // value of every attention arrival counter (grows by D * chunks per draft block)
   int* err_host = nullptr;   // host-mapped barrier time-out flag
   int* err_dev = nullptr;
   bool trace = false;
@@ -249,6 +251,8 @@ int validate_config(const dflare_config* c) {
     return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "hidden, ffn and n_q_heads*head_dim must be multiples of 32");
   if ((c->n_q_heads / c->n_kv_heads) * c->block_size > 128)
     return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "(n_q_heads / n_kv_heads) * block_size must be <= 128");
+  if (c->n_q_heads / c->n_kv_heads > 8 || c->n_kv_heads > kMaxKvHeads)
+    return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "n_q_heads / n_kv_heads must be <= 8 and n_kv_heads <= 128");
   if (c->n_target_layers > 64) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "n_target_layers must be <= 64");
   if (c->hidden > 8192) return fail(nullptr, DFLARE_ERR_UNSUPPORTED, "hidden must be <= 8192");
   if ((long)c->max_context + c->block_size > (1L << 30))
@@ -395,7 +399,9 @@ int build(dflare_handle* h, const dflare_weights* w) {
       h->kvt_waves = y;
     }
   }
-  h->attn_nch = std::max(1, ceil_div((long)c.max_context, 128));
+  // attention chunks of the draft block: 128 context keys per chunk at head size 128, 256 at 64
+  h->attn_chunk = hd == 64 ? 256 : 128;
+  h->attn_nch = std::max(1, ceil_div((long)c.max_context, h->attn_chunk));
 
   // ---- packed weights
   h->s_qkv = (long)Nt_qkv * Kt_H * 64;
@@ -512,8 +518,11 @@ int build(dflare_handle* h, const dflare_weights* w) {
   TRY(dev_zalloc(h, &h->XA, (size_t)stages * h->xa_stride * 16));
   h->q_stride = (long)kMaxBlock * q;
   TRY(dev_zalloc(h, &h->Q, (size_t)D * h->q_stride * 4));
-  TRY(dev_zalloc(h, &h->OP, (size_t)h->attn_nch * c.n_kv_heads * h->Rpad * hd * 4));
-  TRY(dev_zalloc(h, &h->ML, (size_t)h->attn_nch * c.n_kv_heads * h->Rpad * sizeof(float2)));
+  {  // per layer and chunk: G * 16 rows for every KV head
+    const size_t rows = (size_t)D * h->attn_nch * c.n_q_heads * 16;
+    TRY(dev_zalloc(h, &h->OP, rows * hd * 2));
+    TRY(dev_zalloc(h, &h->ML, rows * sizeof(float2)));
+  }
   h->oa_stride = 2L * (Kt_q + kKtPad) * 64;
   TRY(dev_zalloc(h, &h->OA, (size_t)D * h->oa_stride * 16));
   h->ha_stride = 2L * (Kt_F + kKtPad) * 64;
@@ -589,7 +598,7 @@ DraftArgs draft_args(const dflare_handle* h) {
   a.n_kv = c.n_kv_heads;
   a.Lcap = h->Lcap;
   a.Rpad = h->Rpad;
-  a.chunk = 128;
+  a.chunk = h->attn_chunk;
   a.nch = h->attn_nch;
   a.eps = c.rms_eps;
   a.qscale = (float)(1.4426950408889634 / sqrt((double)c.head_dim));
@@ -649,6 +658,7 @@ DraftArgs draft_args(const dflare_handle* h) {
   a.done = h->sync + kBarCounters * 32;
   a.part = h->part;
   a.kcnt = h->sync + 1024;
+  a.acnt = h->sync + kAttnCntOff / 4;
   a.err = h->err_dev;
   return a;
 }
@@ -664,6 +674,7 @@ DraftCall draft_call(const dflare_handle* h, const int32_t* ids, const int32_t* 
   d.hidden = (h->debug && h->capture_persistent && h->persistent) ? h->dbg_hidden : nullptr;
   d.bar_epoch = h->bar_epoch;
   d.done_epoch = h->done_epoch;
+  d.acnt_base = h->acnt_epoch;
   d.trace = h->trace ? h->trace_buf : nullptr;
   d.inv_temp = h->temperature > 0.f ? 1.0f / h->temperature : 0.f;
   d.draw = h->draw;
@@ -691,7 +702,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
     HIP_OR_FAIL(h, hipStreamSynchronize(s));
     HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
     HIP_OR_FAIL(h, hipStreamSynchronize(s));
-    h->bar_epoch = h->done_epoch = 0;
+    h->bar_epoch = h->done_epoch = h->acnt_epoch = 0;
     *(volatile int*)h->err_host = 0;
     h->persistent = false;
     return fail(h, DFLARE_ERR_HIP,
@@ -701,10 +712,12 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   const int P = h->phases;
   // counters are monotonic across launches; start again from zero long before they wrap
   // (split-K counters reach (done_epoch + 1) * D * kg <= (done_epoch + 1) * D * 8)
+  const unsigned attn_adds = (unsigned)c.n_draft_layers * (unsigned)std::max(1, ceil_div(h->Ls[0], h->attn_chunk));
   if (h->bar_epoch + (unsigned)P > (1u << 24) || h->done_epoch + 1u > (1u << 22) ||
-      ((uint64_t)h->done_epoch + 1u) * (uint64_t)c.n_draft_layers * kMaxSplit >= (1ull << 31)) {
+      ((uint64_t)h->done_epoch + 1u) * (uint64_t)c.n_draft_layers * kMaxSplit >= (1ull << 31) ||
+      (uint64_t)h->acnt_epoch + attn_adds >= (1ull << 31)) {
     HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
-    h->bar_epoch = h->done_epoch = 0;
+    h->bar_epoch = h->done_epoch = h->acnt_epoch = 0;
   }
   if (h->trace && !h->trace_buf) TRY(dev_zalloc(h, &h->trace_buf, (size_t)h->blocks * kTraceSlots * P * 8));
   if (h->trace) HIP_OR_FAIL(h, hipMemsetAsync(h->trace_buf, 0, (size_t)h->blocks * kTraceSlots * P * 8, s));
@@ -715,7 +728,8 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   prof_mark(h, DFLARE_K_DRAFT, true);
   if (!split) {
     HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, h->blocks, 0, P, true));
-    h->bar_epoch += (unsigned)(P - 1);
+    // a grid barrier before every phase but the first and the combine phases
+    h->bar_epoch += (unsigned)(P - 1 - c.n_draft_layers);
   } else {
     for (int p = 0; p < P; ++p) {
       int kind, layer;
@@ -731,6 +745,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
     }
   }
   h->done_epoch += 1;
+  h->acnt_epoch += attn_adds;  // every attention item of every layer counted once
   if (h->temperature > 0.f) ++h->draw;
   prof_mark(h, DFLARE_K_DRAFT, false);
   return check_launch(h, "draft_block");
