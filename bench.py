@@ -60,11 +60,15 @@ def parse():
     ap.add_argument("--training", action="store_true",
                     help="time the training-side kernels (anchor attention fwd/bwd, weighted CE) instead")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-context", type=int, default=256,
-                    help="context rows of the oracle's timed sample")
+    ap.add_argument("--cpu-context", type=int, default=0,
+                    help="context rows of the oracle's timed sample (default: the workload's own)")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write profiles/hbm_counters_<config>.json from two rocprofv3 --pmc output folders")
+    ap.add_argument("--counter-scale", default="2.0,1.0",
+                    help="bytes per counted FETCH_SIZE and WRITE_SIZE byte (from --calibrate-copy)")
     return ap.parse_args()
 
 
@@ -115,24 +119,88 @@ def source_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def counter_traffic(kernel: str, record: str = "hbm_counters_qwen3_8b.json"):
-    """HBM bytes per launch of `kernel` measured with rocprofv3 byte counters, if the
-    recorded measurement belongs to the device sources of this build; else None."""
+def counter_record_path(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"hbm_counters_{workload}.json")
+
+
+def counter_traffic(kernel: str, workload: str, context: int):
+    """HBM bytes per launch of `kernel` measured with rocprofv3 byte counters on this very
+    workload (config name and context length), if the recorded measurement belongs to the
+    device sources of this build; else None."""
     try:
-        rec = json.load(open(os.path.join(ROOT, "profiles", record)))
+        rec = json.load(open(counter_record_path(workload)))
         sha = source_sha()
     except (OSError, ValueError):
         return None
     k = rec.get("kernels", {}).get(kernel)
-    if rec.get("sources_sha256_16") != sha or k is None:
+    if (rec.get("sources_sha256_16") != sha or k is None or rec.get("workload") != workload
+            or rec.get("context") != context):
         return None
     return int(k["fetch_kib"] * 1024 * rec["fetch_scale"] + k["write_kib"] * 1024 * rec["write_scale"])
+
+
+# rocprofv3 kernel-name fragments of the kernels whose counters are recorded
+COUNTER_KERNELS = {"draft_block": "k_draft", "kv_t": "k_kvt", "fuse": "k_fuse", "qkv": "BEPI_QKV",
+                   "gate_up": "BEPI_SWIGLU", "attn": "k_battn"}
+
+
+def summarize_counters(fetch_dir: str, write_dir: str, workload: str, context: int, scale: dict):
+    """Write profiles/hbm_counters_<workload>.json from two rocprofv3 --pmc runs of this script
+    (FETCH_SIZE, then WRITE_SIZE): per kernel the median KiB per dispatch over the step's
+    launches.  Whole draft blocks are told from the single-phase launches of the per-phase
+    pass by their fetch (over half the largest); appends and fusions from the untimed
+    prefill's by their grid (the smallest)."""
+    import csv
+    import glob
+    import statistics
+
+    def load(d, counter):
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] == counter:
+                    rows.append((r["Kernel_Name"], int(r["Grid_Size"]), float(r["Counter_Value"])))
+        return rows
+
+    out = {"kernels": {}}
+    for kname, frag in COUNTER_KERNELS.items():
+        vals = {}
+        for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+            rows = [(g, v) for n, g, v in load(d, counter) if frag in n]
+            if not rows:
+                break
+            if kname == "draft_block":
+                top = max(v for _, v in rows) if counter == "FETCH_SIZE" else None
+                keep = [v for g, v in rows if (counter != "FETCH_SIZE" or v > 0.5 * top)]
+                if counter == "WRITE_SIZE":  # same dispatches: the largest half of the writes
+                    keep = sorted(v for _, v in rows)[len(rows) // 2:]
+            else:
+                gmin = min(g for g, _ in rows)
+                keep = [v for g, v in rows if g == gmin]
+            vals[counter] = statistics.median(keep)
+        if len(vals) == 2:
+            out["kernels"][kname] = {"fetch_kib": int(vals["FETCH_SIZE"]), "write_kib": int(vals["WRITE_SIZE"])}
+    out.update({"workload": workload, "context": context, "sources_sha256_16": source_sha(),
+                "fetch_scale": scale["fetch"], "write_scale": scale["write"],
+                "_comment": "HBM KiB per dispatch from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of bench.py on "
+                            "this workload, scaled to bytes by a plain 1 GiB device copy read with the same counters; "
+                            "valid only for the device sources with this sha256 prefix"})
+    with open(counter_record_path(workload), "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
 
 
 def main():
     args = parse()
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.summarize_counters:
+        from paper_2606_02091_amd import synth
+        fs, ws = (float(x) for x in args.counter_scale.split(","))
+        ctx = synth.CONFIGS[synth.BATCHED["model"]].context if args.config == "batched" else \
+            synth.CONFIGS[args.config].context
+        summarize_counters(*args.summarize_counters, args.config, ctx, {"fetch": fs, "write": ws})
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -269,7 +337,7 @@ def main():
                    "global_batch": 1, "seq_len": L, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(d["achieved_GBs"], 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(d["achieved_GBs"] / HBM_PEAK_GBS, 4),
-                     "traffic": counter_traffic(dom),
+                     "traffic": counter_traffic(dom, args.config, L),
                      "kernel": dom, "bytes_per_launch": d["bytes_per_launch"], "avg_us": d["avg_us"]},
         "step_roofline": {"bytes_per_step": int(step_bytes), "achieved_GBs": round(step_gbs, 1),
                           "frac": round(step_gbs / HBM_PEAK_GBS, 4)},
@@ -279,8 +347,12 @@ def main():
         "per_phase_launches": per_phase,
     }
 
+    probe = read_probe_gbs(dfl)
+    result["roofline"]["probe_GBs"] = round(probe, 1)
+    result["roofline"]["frac_of_probe"] = round(d["achieved_GBs"] / probe, 4)
+    result["step_roofline"]["frac_of_probe"] = round(step_gbs / probe, 4)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context, variant)
+        result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context or L, variant)
     print(json.dumps(result), flush=True)
     model.close()
 
@@ -568,7 +640,7 @@ def bench_batched(args):
                    "global_batch": n_seq, "seq_len": int(max(lengths)), "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": d["TFLOPs"], "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(d["TFLOPs"] / MFMA_PEAK_TFLOPS, 4),
-                     "traffic": counter_traffic(dom, "hbm_counters_batched.json"), "kernel": dom,
+                     "traffic": counter_traffic(dom, "batched", cfg.context), "kernel": dom,
                      "flops_per_launch": d["flops_per_launch"], "avg_us": d["avg_us"]},
         "step_roofline": {"flops_per_step": int(step_flops), "bytes_per_step": int(step_bytes),
                           "mfma_frac": round(step_flops / (ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS, 4),
@@ -576,7 +648,7 @@ def bench_batched(args):
         "kernels": kern,
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context)
+        result["cpu_baseline"] = cpu_baseline(cfg, w, fusion_logits, args.cpu_context or cfg.context)
     print(json.dumps(result), flush=True)
     model.close()
 
@@ -629,27 +701,38 @@ def phase_trace(dfl, h, step, cfg, kb, steps):
 
 
 def cpu_baseline(cfg, w, fusion_logits, ctx, variant=0):
-    """The fp64 oracle, as it stands, timed on this host for one draft step."""
+    """The fp64 oracle, as it stands, timed on this host: whole draft steps (truncate back,
+    append 8 rows, draft a block) at context ctx after an untimed prefill, first with every
+    core this process may run on, then one step on one thread."""
     import numpy as np
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import dflare_oracle as orc
     from paper_2606_02091_amd import synth
 
+    cores = len(os.sched_getaffinity(0))
     o = orc.DraftOracle(cfg, w, None if variant & 8 else fusion_logits, max_context=ctx + 64, variant=variant)
-    o.append(synth.hidden_rows(cfg, 0, ctx))
+    with threadpool_limits(cores):
+        t = time.perf_counter()
+        for s0 in range(0, ctx, 512):
+            o.append(synth.hidden_rows(cfg, s0, min(512, ctx - s0)))
+        prefill_s = time.perf_counter() - t
+        used = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     rows = synth.hidden_rows(cfg, ctx, 8)
     ids = synth.block_ids(cfg)
-    # whole steps (truncate back, append 8 rows, draft a block) until at least 10 s have passed
-    steps = 0
-    t = time.perf_counter()
-    while steps == 0 or time.perf_counter() - t < 10.0:
-        o.truncate(ctx)
-        o.append(rows)
-        o.draft_block(ids, keep_logits=False)
-        steps += 1
-    sec = (time.perf_counter() - t) / steps
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+
+    def timed(threads, min_seconds, max_steps):
+        with threadpool_limits(threads):
+            steps, t = 0, time.perf_counter()
+            while steps == 0 or (time.perf_counter() - t < min_seconds and steps < max_steps):
+                o.truncate(ctx)
+                o.append(rows)
+                o.draft_block(ids, keep_logits=False)
+                steps += 1
+            return (time.perf_counter() - t) / steps, steps
+
+    sec, steps = timed(cores, 10.0, 100)
+    sec1, steps1 = timed(1, 0.0, 1)
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as fh:
@@ -659,10 +742,33 @@ def cpu_baseline(cfg, w, fusion_logits, ctx, variant=0):
                     break
     except OSError:
         pass
-    return {"value": round(1.0 / sec, 5), "unit": "blocks/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{steps} steps (fuse_append of 8 rows + draft_block each) of the same model at context "
-                      f"{ctx}; {sec:.2f} s per step, {sec * steps:.1f} s in all, on {cpu} ({platform.machine()})",
-            "seconds": round(sec, 3)}
+    return {"value": round(1.0 / sec, 5), "unit": "blocks/s", "cores": int(used), "kind": "oracle",
+            "sample": f"{steps} steps (fuse_append of 8 rows + draft_block each) of the same model at context {ctx} "
+                      f"after an untimed {prefill_s:.0f} s prefill, {sec:.2f} s per step on {used} threads "
+                      f"({cores} cores in the affinity mask); then {steps1} step on 1 thread, {sec1:.2f} s; "
+                      f"{cpu} ({platform.machine()})",
+            "seconds": round(sec, 3), "affinity_cores": cores,
+            "value_1thread": round(1.0 / sec1, 5), "seconds_1thread": round(sec1, 3)}
+
+
+def read_probe_gbs(dfl, nbytes=2 << 30, reps=6):
+    """The best rate of a plain streaming read of nbytes of device memory (the library's
+    read probe), GB/s: the HBM read ceiling of this machine."""
+    import torch
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    st = torch.cuda.current_stream()
+    best = 1e30
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        dfl.read_probe(buf, sink)
+        e1.record(st)
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1) * 1e-3)
+    del buf
+    return nbytes / best / 1e9
 
 
 if __name__ == "__main__":

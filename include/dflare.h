@@ -384,6 +384,16 @@ enum { DFLARE_OPT_PERSISTENT = 1, DFLARE_OPT_TRACE = 2, DFLARE_OPT_CAPTURE_PERSI
 int dflare_set_option(dflare_handle* h, int option, int value);
 
 /*
+ * dflare_read_probe -- measurement helper, no handle: one plain streaming read of `bytes`
+ * (a positive multiple of 16) of DEVICE memory at `buf` with 16-byte nontemporal loads,
+ * eight per thread in flight, on eight 256-thread work-groups per CU; `sink` is one DEVICE
+ * uint32 that the kernel writes only in a case that practically never occurs.  The rate it
+ * reaches is the HBM read ceiling the draft kernels are quoted against next to the 8 TB/s
+ * specification.  Asynchronous on `stream` (NULL = default); INVALID_ARG on a bad argument.
+ */
+int dflare_read_probe(const void* buf, int64_t bytes, uint32_t* sink, void* stream);
+
+/*
  * ---- Training-side kernels (no handle) ----
  * Anchor attention of one draft layer (Sec. 3.3): the n_blocks sampled blocks of one
  * training sequence are processed together; the rows of block i, anchored at sequence

@@ -192,5 +192,7 @@ void launch_kvt(hipStream_t s, int nt_per_block, int waves, const KvtArgs& a, in
 hipError_t launch_draft(hipStream_t s, const DraftArgs* a_dev, const DraftCall& c, int hd, int blocks, int p0,
                         int p1, bool cooperative);
 int draft_blocks_per_cu(int hd);
+// measurement: streaming read of `bytes` (a multiple of 16) on `blocks` work-groups of 256
+void launch_read_probe(hipStream_t s, const void* buf, long bytes, uint32_t* sink, int blocks);
 
 }  // namespace dflare

@@ -73,11 +73,12 @@ __global__ void k_bf16_to_f32(float* dst, const uint16_t* src, long n) {
 
 // ------------------------------------------------------------------------------------------
 // layer fusion (Eq. 3): u^(i)[r, k] = sum_j alpha[i, j] h^(j)[r, k], accumulated in j order.
-// Block (512 columns, row r, draft layer i); a lane owns 8 columns and keeps twelve 16-byte
-// loads in flight.  Writes the A fragments of u^(i) * g_fuse^(i) and per-16-column sums of
+// Block (512 columns, row r, draft layer i); a lane owns 8 columns and keeps up to forty
+// 16-byte loads in flight (every target layer at once for S <= 40: one memory round trip).  Writes the A fragments of u^(i) * g_fuse^(i) and per-16-column sums of
 // squares of u^(i); the 1/rms of Eq. 3 is applied in the K/V projection.  The S target rows
 // are read from HBM once; the blocks of the other draft layers find them in L2.
 // ------------------------------------------------------------------------------------------
+constexpr int kFuseBatch = 40;  // target layers whose loads are in flight together
 __global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int ld, int S, int H,
                                              const float* __restrict__ alpha, const float* __restrict__ gain,
                                              float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
@@ -87,15 +88,15 @@ __global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden
   const bool ok = k0 < H;
   const int Kt = H / 32;
   float u[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int j0 = 0; j0 < S; j0 += 12) {
-    u32x4 v[12];
+  for (int j0 = 0; j0 < S; j0 += kFuseBatch) {
+    u32x4 v[kFuseBatch];
 #pragma unroll
-    for (int qq = 0; qq < 12; ++qq) {
+    for (int qq = 0; qq < kFuseBatch; ++qq) {
       v[qq] = u32x4{0u, 0u, 0u, 0u};
       if (ok && j0 + qq < S) v[qq] = *reinterpret_cast<const u32x4*>(hidden + ((long)(j0 + qq) * ld + r) * H + k0);
     }
 #pragma unroll
-    for (int qq = 0; qq < 12; ++qq) {
+    for (int qq = 0; qq < kFuseBatch; ++qq) {
       if (j0 + qq < S) {
         const float a = alpha[i * S + j0 + qq];
 #pragma unroll
@@ -368,8 +369,8 @@ typedef const CONSTANT DraftCall* Call;
 // holds its share of arrivals times the barrier's epoch.  A wait that exceeds the time
 // limit raises the host-visible error flag and lets the work-group go on (results are then
 // wrong, and the host reports the failure), so a launch always terminates.
-__device__ __forceinline__ void grid_arrive(Args a) {
-  wait_vm();
+__device__ __forceinline__ void grid_arrive(Args a, bool wait_own = true) {
+  if (wait_own) wait_vm();
   __syncthreads();
   if (threadIdx.x == 0)
     __hip_atomic_fetch_add(a->bar + (blockIdx.x % kBarCounters) * 32, 1u, __ATOMIC_RELAXED,
@@ -416,9 +417,9 @@ __device__ __forceinline__ void phase_begin(Args a, Call c, const PhaseCtl& pc,
 }
 
 // ---- EMBED: X = E[ids] (fp32), sums of squares and A fragments of X * g_attn^(0) (stage 0)
-// Item = 8 columns of one row; items 2m and 2m + 1 (one 16-column tile) go to threads 2k and
-// 2k + 1 of work-group m % blocks, so the work spreads over every work-group and the two
-// halves of a tile meet in one shuffle.
+// Run by wave 0.  Item = 8 columns of one row; items 2m and 2m + 1 (one 16-column tile) go to
+// lanes 2k and 2k + 1 of work-group m % blocks, so the work spreads over every work-group and
+// the two halves of a tile meet in one shuffle.
 __device__ void phase_embed(Args a, Call c) {
   const int H = a->H, Kt = H / 32, per_row = H / 8;
   const int pairs = a->B * per_row / 2;
@@ -426,8 +427,8 @@ __device__ void phase_embed(Args a, Call c) {
   float* XS = a->XS;
   uint32_t* xhi = reinterpret_cast<uint32_t*>(a->XA);
   uint32_t* xlo = reinterpret_cast<uint32_t*>(a->XA + (long)(Kt + kKtPad) * 64);
-  const int tid = opaque(threadIdx.x);
-  for (int m = blockIdx.x + (tid >> 1) * gridDim.x; m < pairs; m += (kThreads / 2) * gridDim.x) {
+  const int tid = opaque(threadIdx.x);  // threads of wave 0
+  for (int m = blockIdx.x + (tid >> 1) * gridDim.x; m < pairs; m += 32 * gridDim.x) {
     const int item = 2 * m + (tid & 1);
     const int row = item / per_row, k0 = (item % per_row) * 8;
     int id = gbl(c->ids)[row];
@@ -1452,10 +1453,10 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
     pc.slot = kTraceSlots * p;
     pc.nslots = nslots;
     switch (kind) {
-      case PH_EMBED:
+      case PH_EMBED:  // wave 0 embeds (its threads hold every item), waves 1-7 stage layer 0's attention item
         phase_begin(a, c, pc, failed);
-        phase_embed(a, c);
-        attn_stage<HD>(a, c, 0, blockIdx.x, smem, 0);
+        if (threadIdx.x < 64) phase_embed(a, c);
+        attn_stage<HD>(a, c, 0, blockIdx.x, smem, 1);
         break;
       case PH_QKV:
         gemm_dispatch<EPI_QKV>(a, c, kind, layer, pc, failed, smem);
@@ -1480,7 +1481,8 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
         break;
     }
     // the attention phase hands over to the combine phase through the per-KV-head counters
-    if (p + 1 < p1 && kind != PH_ATTN) grid_arrive(a);
+    // the staging waves of the embedding phase issued loads only: they need not wait for them
+    if (p + 1 < p1 && kind != PH_ATTN) grid_arrive(a, kind != PH_EMBED || threadIdx.x < 64);
     else wait_vm();
     trace_mark(c, kTraceSlots * p + kTraceSlots - 1, nslots);
   }
@@ -1558,6 +1560,31 @@ void launch_kvt(hipStream_t s, int nt_per_block, int waves, const KvtArgs& a, in
   const dim3 grid((a.Nt + nt_per_block - 1) / nt_per_block, layers, mtiles);
   if (nt_per_block == 2 && waves == 8) hipLaunchKernelGGL((k_kvt<2, 8>), grid, dim3(512), 0, s, a);
   else hipLaunchKernelGGL((k_kvt<1, 16>), grid, dim3(1024), 0, s, a);
+}
+
+// Measurement: a plain streaming read of n16 16-byte words (eight nontemporal loads in flight
+// per thread, grid-stride), the HBM read ceiling the draft kernels are compared with.  The
+// XOR of the data is stored only if it equals a value it cannot be made to equal by chance
+// often enough to matter, so that the loads are not removed.
+__global__ __launch_bounds__(256) void k_read_probe(const u32x4* __restrict__ p, long n16, uint32_t* sink) {
+  uint32_t acc = 0;
+  const long stride = (long)gridDim.x * 256 * 8;
+  for (long i0 = (long)blockIdx.x * 256 * 8 + threadIdx.x; i0 < n16; i0 += stride) {
+    u32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const long i = i0 + u * 256;
+      v[u] = i < n16 ? __builtin_nontemporal_load(p + i) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+  }
+  if (acc == 0x9E3779B9u) sink[0] = acc;
+}
+
+void launch_read_probe(hipStream_t s, const void* buf, long bytes, uint32_t* sink, int blocks) {
+  hipLaunchKernelGGL(k_read_probe, dim3(blocks), dim3(256), 0, s, reinterpret_cast<const u32x4*>(buf), bytes / 16,
+                     sink);
 }
 
 static const void* draft_kernel(int hd) {

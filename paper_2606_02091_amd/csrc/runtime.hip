@@ -1387,6 +1387,16 @@ int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count) {
   return DFLARE_OK;
 }
 
+int dflare_read_probe(const void* buf, int64_t bytes, uint32_t* sink, void* stream) {
+  if (!buf || !sink || bytes <= 0 || bytes % 16) return DFLARE_ERR_INVALID_ARG;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return DFLARE_ERR_HIP;
+  launch_read_probe((hipStream_t)stream, buf, (long)bytes, sink, 8 * cus);
+  return hipGetLastError() == hipSuccess ? DFLARE_OK : DFLARE_ERR_HIP;
+}
+
 int dflare_set_option(dflare_handle* h, int option, int value) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
   switch (option) {

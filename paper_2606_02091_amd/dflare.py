@@ -28,7 +28,7 @@ EXPORTED = (
     "dflare_fuse_append_batched", "dflare_draft_block_batched", "dflare_truncate_seq",
     "dflare_context_len_seq", "dflare_debug_read_seq", "dflare_set_sampling", "dflare_accept",
     "dflare_anchor_attention_workspace", "dflare_anchor_attention_fwd", "dflare_anchor_attention_bwd",
-    "dflare_weighted_ce_workspace", "dflare_weighted_ce", "dflare_weighted_ce_noalloc",
+    "dflare_weighted_ce_workspace", "dflare_weighted_ce", "dflare_weighted_ce_noalloc", "dflare_read_probe",
 )
 K_QKV, K_ATTN, K_O, K_GATE_UP, K_DOWN, K_LM_HEAD, K_FUSE, K_KV_T, K_DRAFT = range(1, 10)
 (K_B_QKV, K_B_ATTN, K_B_O, K_B_GATE_UP, K_B_DOWN, K_B_LM_HEAD, K_B_KV_T, K_B_EPI, K_B_FUSE, K_B_DRAFT,
@@ -108,6 +108,7 @@ def lib() -> ctypes.CDLL:
                                 vp, ctypes.c_size_t, vp], ctypes.c_int),
         "dflare_weighted_ce_noalloc": ([vp, vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_float, vp,
                                         vp, vp, vp], ctypes.c_int),
+        "dflare_read_probe": ([vp, i64, vp, vp], ctypes.c_int),
         "dflare_context_len_seq": ([vp, i32, ctypes.POINTER(i32)], ctypes.c_int),
         "dflare_debug_read_seq": ([vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_float),
                                    i64], ctypes.c_int),
@@ -264,6 +265,12 @@ def weighted_ce(logits, labels, B: int, gamma: float, stream=None):
     _train_check(lib().dflare_weighted_ce(_ptr(logits), _ptr(labels), rows, V, B, float(gamma), _ptr(loss), _ptr(ce),
                                           _ptr(dz), _ptr(ws), ws_bytes, _stream(stream)), "weighted ce")
     return loss, ce, dz
+
+
+def read_probe(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """Measurement: one streaming read of the device tensor buf (the HBM read ceiling)."""
+    _train_check(lib().dflare_read_probe(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)),
+                 "read probe")
 
 
 WEIGHTED_CE_NOALLOC_MAX_ROWS = 65536  # DFLARE_WEIGHTED_CE_NOALLOC_MAX_ROWS

@@ -369,3 +369,58 @@ def test_gemm_plans(plan, monkeypatch):
         dfl.dflare_debug_capture(model.h, True)
         assert np.array_equal(persistent, per_phase), (plan, k)
     model.close()
+
+
+def test_many_attention_items_per_work_group(monkeypatch):
+    """16 work-groups and a 3,000-row context: 24 chunks x 2 KV heads = 48 attention items,
+    three per work-group (only the first is staged ahead; the others load everything after
+    the barrier), and the merge of 24 chunks by 8 work-groups per KV head.  Per-phase
+    launches match the oracle; the persistent launch matches them bitwise."""
+    cfg = SPLIT_CFG.replace(context=3000)
+    monkeypatch.setenv("DFLARE_BLOCKS", "16")
+    model, orc, w, lg = build_pair(cfg, cfg.context, "random", max_new=16)
+    for k in range(2):
+        ids = synth.block_ids(cfg, step=k)
+        _, per_phase, _ = compare_step(model, orc, cfg, ids, tag=f"items step={k}")
+        dfl.dflare_debug_capture(model.h, False)
+        persistent = model.draft_block(ids_tensor(ids)).cpu().numpy()
+        torch.cuda.synchronize()
+        dfl.dflare_debug_capture(model.h, True)
+        assert np.array_equal(persistent, per_phase), k
+    model.close()
+
+
+def test_large_magnitude_cache():
+    """The fp16 context cache at large magnitudes: fusion-norm gains scaled by 2000 give
+    context keys and values in the thousands (fp16 keeps its relative precision there); the
+    cache, the block rows and the logits stay within the bar of the fp64 oracle, and the
+    timed (persistent) launch gives the same tokens.  Values beyond +-65504 would saturate
+    (the cache format's range; not reached here)."""
+    cfg = CASES["hd128"][0]
+    L = 200
+    w, lg = P.weights_for(cfg)
+    g = synth.bf16_to_f32(w["fuse_norm"]) * 2000.0
+    w["fuse_norm"] = synth.round_bf16(g)
+    model = dfl.DraftModel(cfg, w, lg, max_context=L + 64, max_new=16)
+    dfl.dflare_debug_capture(model.h, True)
+    orc = P.oracle_for(cfg, w, lg, L + 64)
+    s = 0
+    for n in append_plan(cfg, L, "random"):
+        rows = synth.hidden_rows(cfg, s, n)
+        model.fuse_append(dev(rows))
+        orc.append(rows)
+        s += n
+    kmax = 0.0
+    for i in range(cfg.n_draft_layers):
+        k = dfl.dflare_debug_read(model.h, dfl.DBG_KCACHE, i, (L, cfg.n_kv_heads, cfg.head_dim))
+        v = dfl.dflare_debug_read(model.h, dfl.DBG_VCACHE, i, (L, cfg.n_kv_heads, cfg.head_dim))
+        assert P.relinf(k, orc.k_cache[i]) <= P.REL_TOL and P.relinf(v, orc.v_cache[i]) <= P.REL_TOL, i
+        kmax = max(kmax, float(np.abs(orc.k_cache[i]).max()), float(np.abs(orc.v_cache[i]).max()))
+    assert 1000.0 < kmax < 65504.0, kmax
+    ids = synth.block_ids(cfg, step=0)
+    _, per_phase, _ = compare_step(model, orc, cfg, ids, tag="large")
+    dfl.dflare_debug_capture(model.h, False)
+    persistent = model.draft_block(ids_tensor(ids)).cpu().numpy()
+    torch.cuda.synchronize()
+    assert np.array_equal(persistent, per_phase)
+    model.close()
