@@ -148,8 +148,10 @@ def summarize_counters(fetch_dir: str, write_dir: str, workload: str, context: i
     """Write profiles/hbm_counters_<workload>.json from two rocprofv3 --pmc runs of this script
     (FETCH_SIZE, then WRITE_SIZE): per kernel the median KiB per dispatch over the step's
     launches.  Whole draft blocks are told from the single-phase launches of the per-phase
-    pass by their fetch (over half the largest); appends and fusions from the untimed
-    prefill's by their grid (the smallest)."""
+    pass by their fetch (over 0.8 of the largest; the LM head alone reads up to
+    0.55 of a block); the step's appends and fusions from the
+    untimed prefill's by their grid (at most 16 times the smallest); both runs launch the
+    same sequence, so the write counters are taken at the same positions."""
     import csv
     import glob
     import statistics
@@ -159,27 +161,28 @@ def summarize_counters(fetch_dir: str, write_dir: str, workload: str, context: i
         for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
             for r in csv.DictReader(open(f)):
                 if r["Counter_Name"] == counter:
-                    rows.append((r["Kernel_Name"], int(r["Grid_Size"]), float(r["Counter_Value"])))
+                    rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], int(r["Grid_Size"]),
+                                 float(r["Counter_Value"])))
+        rows.sort()
         return rows
 
+    fetch_rows, write_rows = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
     out = {"kernels": {}}
     for kname, frag in COUNTER_KERNELS.items():
-        vals = {}
-        for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
-            rows = [(g, v) for n, g, v in load(d, counter) if frag in n]
-            if not rows:
-                break
-            if kname == "draft_block":
-                top = max(v for _, v in rows) if counter == "FETCH_SIZE" else None
-                keep = [v for g, v in rows if (counter != "FETCH_SIZE" or v > 0.5 * top)]
-                if counter == "WRITE_SIZE":  # same dispatches: the largest half of the writes
-                    keep = sorted(v for _, v in rows)[len(rows) // 2:]
-            else:
-                gmin = min(g for g, _ in rows)
-                keep = [v for g, v in rows if g == gmin]
-            vals[counter] = statistics.median(keep)
-        if len(vals) == 2:
-            out["kernels"][kname] = {"fetch_kib": int(vals["FETCH_SIZE"]), "write_kib": int(vals["WRITE_SIZE"])}
+        # the kernel's dispatches in launch order; both runs launch the same sequence
+        fr = [(g, v) for _, n, g, v in fetch_rows if frag in n]
+        wr = [(g, v) for _, n, g, v in write_rows if frag in n]
+        if not fr or len(fr) != len(wr):
+            continue
+        if kname == "draft_block":
+            top = max(v for _, v in fr)
+            pick = [i for i, (_, v) in enumerate(fr) if v > 0.8 * top]
+        else:  # the step's appends (1 to 16 rows), not the prefill's 512-row ones
+            gmin = min(g for g, _ in fr)
+            pick = [i for i, (g, _) in enumerate(fr) if g <= 16 * gmin]
+        out["kernels"][kname] = {"fetch_kib": int(statistics.median(fr[i][1] for i in pick)),
+                                 "write_kib": int(statistics.median(wr[i][1] for i in pick)),
+                                 "dispatches": len(pick)}
     out.update({"workload": workload, "context": context, "sources_sha256_16": source_sha(),
                 "fetch_scale": scale["fetch"], "write_scale": scale["write"],
                 "_comment": "HBM KiB per dispatch from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of bench.py on "

@@ -74,17 +74,25 @@ __global__ void k_bf16_to_f32(float* dst, const uint16_t* src, long n) {
 // ------------------------------------------------------------------------------------------
 // layer fusion (Eq. 3): u^(i)[r, k] = sum_j alpha[i, j] h^(j)[r, k], accumulated in j order.
 // Block (512 columns, row r, draft layer i); a lane owns 8 columns and keeps up to forty
-// 16-byte loads in flight (every target layer at once for S <= 40: one memory round trip).  Writes the A fragments of u^(i) * g_fuse^(i) and per-16-column sums of
-// squares of u^(i); the 1/rms of Eq. 3 is applied in the K/V projection.  The S target rows
-// are read from HBM once; the blocks of the other draft layers find them in L2.
+// 16-byte loads in flight (every target layer at once for S <= 40: one memory round trip).
+// Writes the A fragments of u^(i) * g_fuse^(i) and per-16-column sums of squares of u^(i);
+// the 1/rms of Eq. 3 is applied in the K/V projection.  The D blocks of one (512 columns,
+// row) pair read the same target row pieces; consecutive block ids are dealt to the 8 XCDs
+// in turn, so the pair's D blocks get ids 8 apart (one XCD, one L2) and the pieces come
+// from HBM once per pair.  Ids past the last pair are idle.
 // ------------------------------------------------------------------------------------------
 constexpr int kFuseBatch = 40;  // target layers whose loads are in flight together
-__global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int ld, int S, int H,
+constexpr int kXcds = 8;
+__global__ __launch_bounds__(64) void k_fuse(const uint16_t* __restrict__ hidden, int ld, int S, int H, int n, int D,
                                              const float* __restrict__ alpha, const float* __restrict__ gain,
                                              float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
   const int lane = threadIdx.x;
-  const int r = blockIdx.y, i = blockIdx.z;
-  const int k0 = blockIdx.x * 512 + lane * 8;
+  // block id b = x + 8 (i + D g): pair m = 8 g + x (x = b % 8), draft layer i
+  const int b = blockIdx.x, x = b % kXcds, i = (b / kXcds) % D, m = kXcds * (b / (kXcds * D)) + x;
+  const int cbs = (H + 511) / 512;
+  if (m >= cbs * n) return;
+  const int r = m / cbs, cb = m % cbs;
+  const int k0 = cb * 512 + lane * 8;
   const bool ok = k0 < H;
   const int Kt = H / 32;
   float u[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -1516,7 +1524,9 @@ void launch_bf16_to_f32(hipStream_t s, float* dst, const uint16_t* src, long n) 
 
 void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int ld, int S, int H, int D, const float* alpha,
                  const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max) {
-  hipLaunchKernelGGL(k_fuse, dim3((H + 511) / 512, n, D), dim3(64), 0, s, hidden, ld, S, H, alpha, gain, ustats,
+  const int pairs = ((H + 511) / 512) * n;
+  const int groups = (pairs + kXcds - 1) / kXcds;
+  hipLaunchKernelGGL(k_fuse, dim3(groups * kXcds * D), dim3(64), 0, s, hidden, ld, S, H, n, D, alpha, gain, ustats,
                      ua_hi, ua_lo, n_max, mt_max);
 }
 
