@@ -55,6 +55,8 @@ def parse():
                     help="number S of fused target layers (default: the model's)")
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="0 (default): greedy drafts; > 0: Gumbel-max draws from softmax(z / T)")
+    ap.add_argument("--loop-sync", action="store_true",
+                    help="with --loop: verify with dflare_accept, which waits for k every iteration")
     ap.add_argument("--loop", action="store_true",
                     help="time the draft-then-verify loop (draft_block, a synthetic target, accept) instead")
     ap.add_argument("--training", action="store_true",
@@ -364,8 +366,10 @@ def bench_loop(args):
     """The draft-then-verify loop at batch 1: per iteration draft_block, a synthetic target
     (its predictions agree with the first k candidates, k drawn ~ U{0..B-1} from a seeded
     generator and applied on the device; its hidden rows are a fixed seeded block), then
-    dflare_accept, which appends the k + 1 verified rows and waits once for k.  The target
-    model's own forward pass is not part of the loop (no target weights exist here)."""
+    dflare_accept_async, which appends the verified rows with the context length kept on
+    the device, so the host enqueues iteration after iteration without waiting (with
+    --loop-sync: dflare_accept, which waits once per iteration for k).  The target model's
+    own forward pass is not part of the loop (no target weights exist here)."""
     import numpy as np
     import torch
 
@@ -391,26 +395,30 @@ def bench_loop(args):
     draft = torch.empty(B, dtype=torch.int32, device="cuda")
     nxt = torch.empty(B, dtype=torch.int32, device="cuda")
     em = torch.empty(B, dtype=torch.int32, device="cuda")
-    accepted = []
+    k_dev = torch.zeros(total, dtype=torch.int32, device="cuda")
 
     def it(i):
         dfl.dflare_draft_block(h, ids, draft)
         # synthetic target: agrees with candidates 1..k, then predicts another token
         shifted = torch.roll(draft, -1)
         tgt = torch.where(pos < ks[i], shifted, (shifted + 1) % V).to(torch.int32)
-        k = dfl.dflare_accept(h, ids, draft, tgt, hid, nxt, em)
+        if args.loop_sync:
+            k_dev[i] = dfl.dflare_accept(h, ids, draft, tgt, hid, nxt, em)
+        else:
+            dfl.dflare_accept_async(h, ids, draft, tgt, hid, nxt, em, k_dev[i:i + 1])
         ids.copy_(nxt)
-        accepted.append(k)
 
     for i in range(args.warmup):
         it(i)
     torch.cuda.synchronize()
-    accepted.clear()
     t0 = time.perf_counter()
     for i in range(args.warmup, total):
         it(i)
     torch.cuda.synchronize()
     sec = time.perf_counter() - t0
+    accepted = [int(x) for x in k_dev[args.warmup:].cpu()]
+    assert accepted == [int(x) for x in ks[args.warmup:].cpu()], "the loop accepted other lengths than the target's"
+    assert dfl.dflare_context_len(h) == L + sum(int(x) + 1 for x in ks.cpu())
     ms = 1000.0 * sec / args.steps
     tokens = sum(k + 1 for k in accepted)
     print(f"[bench] loop: {args.steps} iterations, {ms:.4f} ms each, {tokens / sec:.0f} tokens/s",
@@ -421,11 +429,14 @@ def bench_loop(args):
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{cfg.name}-shaped draft-then-verify loop from context {L}: draft_block, "
-                               f"a synthetic target accepting k ~ U{{0..{B - 1}}} candidates, dflare_accept "
-                               f"(k + 1 rows appended, one host wait per iteration)",
+                               f"a synthetic target accepting k ~ U{{0..{B - 1}}} candidates, "
+                               + ("dflare_accept (k + 1 rows appended, one host wait per iteration)" if args.loop_sync
+                                  else "dflare_accept_async (k + 1 rows appended, length kept on the device, "
+                                       "no host wait)"),
                    "global_batch": 1, "seq_len": L, "parallelism": "single GPU"},
         "tokens_per_s": round(tokens / sec, 1), "mean_accepted": round(float(np.mean(accepted)), 3),
-        "timing": "host wall clock (the loop waits for k every iteration)",
+        "timing": "host wall clock over the enqueued iterations, synchronized at both ends"
+                  + (" (the loop waits for k every iteration)" if args.loop_sync else ""),
     }), flush=True)
 
 

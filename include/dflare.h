@@ -191,6 +191,27 @@ int dflare_accept(dflare_handle* h, const int32_t* block_ids, const int32_t* dra
                   int32_t* emitted, int32_t* accepted);
 
 /*
+ * dflare_accept_async -- dflare_accept without the wait (Sec. 3.2, verification phase):
+ * the whole draft-then-verify loop stays on the stream, the host never learns k.
+ *   block_ids .. emitted   as for dflare_accept.
+ *   accepted_dev   DEVICE int32 out, or NULL: k.
+ * The new context length L + k + 1 is kept on the device, and the next dflare_draft_block
+ * and dflare_accept_async read it there.  All B target rows are fused and their K/V written
+ * to slots L .. L + B - 1; the k + 1 verified ones become the context, the others lie past
+ * it and are overwritten by the next draft block's own keys before anything reads them.
+ * Every other call that needs L (dflare_context_len, dflare_truncate, dflare_fuse_append,
+ * dflare_accept, dflare_draft_block_pos, the batched and debug calls) first waits for the
+ * stream and takes the length back to the host.  The host keeps an upper bound (L + B per
+ * call); when the bound leaves no room for B more rows it reads the length first, and
+ * L + B > max_context then gives CONTEXT_FULL with nothing changed.  max_new < B:
+ * INVALID_ARG.  For the DFlash variant (whose fusion takes host lengths) the call waits as
+ * dflare_accept does.
+ */
+int dflare_accept_async(dflare_handle* h, const int32_t* block_ids, const int32_t* draft_tokens,
+                        const int32_t* target_tokens, const void* target_hidden, int32_t* next_ids,
+                        int32_t* emitted, int32_t* accepted_dev);
+
+/*
  * dflare_draft_block -- one drafting forward pass (Sec. 3.2, drafting phase).
  *   block_ids      DEVICE int32 [B]: x_t at index 0, the mask id at 1..B-1 (the
  *                  library treats all ids alike; ids outside [0, V) are clamped).
@@ -218,7 +239,8 @@ int dflare_draft_block_pos(dflare_handle* h, const int32_t* block_ids, const int
 /* dflare_truncate -- roll the context back to new_len (0 <= new_len <= L). */
 int dflare_truncate(dflare_handle* h, int32_t new_len);
 
-/* dflare_context_len -- current context length L into *out. */
+/* dflare_context_len -- current context length L into *out (waits for the stream when the
+ * length is on the device, after dflare_accept_async). */
 int dflare_context_len(const dflare_handle* h, int32_t* out);
 
 /*

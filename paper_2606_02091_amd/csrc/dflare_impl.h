@@ -66,8 +66,9 @@ __host__ __device__ inline void phase_of(int p, int D, int& kind, int& layer) {
 
 // What changes from one draft block to the next: passed by value at every launch.
 struct DraftCall {
-  int L;                // context length
-  int pos[kMaxBlock];   // positions of the block rows
+  int L;                // context length (when Lp is NULL)
+  const int* Lp;        // device-resident context length, or NULL: then L above
+  int pos[kMaxBlock];   // positions of the block rows (with Lp: offsets added to *Lp)
   const int* ids;       // [B] block token ids
   int* tokens;          // [B] output: greedy draft tokens
   float* logits;        // optional [B, V]
@@ -161,6 +162,7 @@ struct KvtArgs {
   int n_stat;
   float inv_dim, eps;
   int L, n_new;
+  const int* Lp;           // device-resident context length, or NULL: then L (rows go to slots L + row)
   uint16_t *kc, *vt;
   long cache_layer_stride;
   int Lcap, hd, kv_tiles;
@@ -180,8 +182,10 @@ void launch_matvec(hipStream_t s, float* y, const uint16_t* A, const uint16_t* b
 void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int ld, int S, int H, int D, const float* alpha,
                  const float* gain, float* ustats, u32x4* ua_hi, u32x4* ua_lo, int n_max, int mt_max);
 // verification (Sec. 3.2): accepted count k (to host-visible memory), next block, emitted tokens
+// L_next (optional): receives L + k + 1, L being *Lp or, with Lp NULL, L_imm
 void launch_accept(hipStream_t s, const int32_t* block_ids, const int32_t* draft, const int32_t* target, int B,
-                   int32_t* next_ids, int32_t* emitted, int32_t* k_out);
+                   int32_t* next_ids, int32_t* emitted, int32_t* k_out, const int32_t* Lp, int L_imm,
+                   int32_t* L_next);
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n,
                        int H, int D, int n_max, int mt_max, float eps, float* out);
 bool kvt_shape_supported(int nt_per_block, int waves);

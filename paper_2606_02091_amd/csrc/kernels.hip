@@ -278,6 +278,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_kvt(KvtArgs a) {
 
   if (has_tile) {
     const int tph = a.hd / 16, half = a.hd / 2;
+    const int L0 = a.Lp ? *a.Lp : a.L;  // rows go to cache slots L0 + row
     uint16_t* kc = a.kc + layer * a.cache_layer_stride;
     uint16_t* vt = a.vt + layer * a.cache_layer_stride;
     const bool is_k = nt < a.kv_tiles;
@@ -292,7 +293,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_kvt(KvtArgs a) {
     for (int i = 0; i < 4; ++i) {
       const int row = mt * 16 + quad * 4 + i;
       const bool valid = row < M;
-      const int slot = a.L + row;
+      const int slot = L0 + row;
       const float x = v[i] + bcol;
       const float partner = __shfl_xor(x, 8);
       if (is_k) {
@@ -424,6 +425,10 @@ __device__ __forceinline__ void phase_begin(Args a, Call c, const PhaseCtl& pc,
   trace_mark(c, pc.slot, pc.nslots);
 }
 
+// Context length of the call: the host's value or, when the length is kept on the device
+// (after a verification step that did not wait), the word written by that step.
+__device__ __forceinline__ int ctx_len(Call c) { return c->Lp ? *c->Lp : c->L; }
+
 // ---- EMBED: X = E[ids] (fp32), sums of squares and A fragments of X * g_attn^(0) (stage 0)
 // Run by wave 0.  Item = 8 columns of one row; items 2m and 2m + 1 (one 16-column tile) go to
 // lanes 2k and 2k + 1 of work-group m % blocks, so the work spreads over every work-group and
@@ -550,7 +555,7 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
       if (col < 8 && (col & 1) == 0 && row < M) store_frag_pair_wt(g.na_hi, g.na_lo, row, nt * 8 + col, g.na_Kt, hv, h1);
     }
   } else if constexpr (EPI == EPI_QKV) {
-    const int L = c->L, hd = a->hd;
+    const int L = ctx_len(c), hd = a->hd;
     const int tph = hd / 16, half = hd / 2;
     const int q_tiles = a->n_q * tph, kv_tiles = a->n_kv * tph;
     int region, t;  // 0 = Q, 1 = K, 2 = V
@@ -570,7 +575,7 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
     for (int i = 0; i < 4; ++i) {
       const int row = quad * 4 + i;
       const bool valid = row < M;
-      const int pos = valid ? c->pos[row] : 0;
+      const int pos = valid ? c->pos[row] + (c->Lp ? L : 0) : 0;
       const int slot = L + row;
       const float x = v[i];
       const float partner = __shfl_xor(x, 8);
@@ -1031,7 +1036,7 @@ __device__ __forceinline__ int vswz(int d) { return (d >> 1) & 3; }
 template <int HD>
 __device__ __forceinline__ void attn_stage(Args a, Call dc, int layer, int j, u32x4* smem, int w0) {
   using A = AttnShape<HD>;
-  const int L = dc->L, nkv = a->n_kv;
+  const int L = ctx_len(dc), nkv = a->n_kv;
   const int wave = __builtin_amdgcn_readfirstlane(opaque(threadIdx.x) >> 6);
   if (wave < w0 || j >= attn_chunks(L, A::CK) * nkv) return;
   const int c = j / nkv, g = j - (j / nkv) * nkv;
@@ -1073,7 +1078,7 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
   float2* sML = reinterpret_cast<float2*>(sO + kWaves * DT * 64);  // [kWaves][16]
   static_assert(kWaves * DT * 64 * 16 + kWaves * 16 * 8 <= kStageOff, "LDS merge area");
 
-  const int L = dc->L, B = a->B, nkv = a->n_kv, G = a->n_q / a->n_kv, Lcap = a->Lcap;
+  const int L = ctx_len(dc), B = a->B, nkv = a->n_kv, G = a->n_q / a->n_kv, Lcap = a->Lcap;
   const int nch = attn_chunks(L, CK);
   const int items = nch * nkv;
   const int KS = kWaves / G;  // key parts
@@ -1270,7 +1275,11 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
     // the item is stored: count it for its KV head
     wait_vm();
     __syncthreads();
-    if (tid == 0) __hip_atomic_fetch_add(a->acnt + g * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // (chunk 0 also adds the chunks this context does not have, so that every layer adds
+    // a->nch per KV head whatever the context length, and the host's count needs no length)
+    if (tid == 0)
+      __hip_atomic_fetch_add(a->acnt + g * 32, c == 0 ? 1u + (unsigned)(a->nch - nch) : 1u, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
   };
 
   // One call site for the item body keeps the phase's code small.
@@ -1289,7 +1298,7 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
   constexpr int DPL = HD / 64;                 // dims per lane
   constexpr int CB = DPL == 2 ? 16 : 32;       // chunks whose loads are in flight together
   constexpr int CW = 4;                        // waves that merge
-  const int L = dc->L, B = a->B, nkv = a->n_kv, G = a->n_q / a->n_kv;
+  const int L = ctx_len(dc), B = a->B, nkv = a->n_kv, G = a->n_q / a->n_kv;
   const int nch = attn_chunks(L, A::CK);
   const int W = min(nch, (int)gridDim.x / nkv);
   const int b = blockIdx.x;
@@ -1298,7 +1307,7 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
   if (pc.wait) {
     if (b < W * nkv && threadIdx.x < 64 && !failed) {
       const unsigned* cnt = a->acnt + (b % nkv) * 32;
-      const unsigned target = dc->acnt_base + (unsigned)(layer + 1) * (unsigned)nch;
+      const unsigned target = dc->acnt_base + (unsigned)(layer + 1) * (unsigned)a->nch;
       const long long t0 = wall_clock64();
       while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
         __builtin_amdgcn_s_sleep(1);
@@ -1533,9 +1542,11 @@ void launch_fuse(hipStream_t s, const uint16_t* hidden, int n, int ld, int S, in
 // Verification (Sec. 3.2): one wave.  k = the number of leading candidates j = 1.. that
 // equal the target's prediction after position j - 1; the bonus is the target's
 // prediction after position k.  Writes the next block (bonus, then the mask ids), the
-// emitted tokens (k candidates, bonus, then -1) and k to host-visible memory.
+// emitted tokens (k candidates, bonus, then -1), k (to host-visible memory or a device
+// word) and, when L_next is given, the context length after the k + 1 verified rows.
 __global__ __launch_bounds__(64) void k_accept(const int32_t* block_ids, const int32_t* draft, const int32_t* target,
-                                               int B, int32_t* next_ids, int32_t* emitted, int32_t* k_out) {
+                                               int B, int32_t* next_ids, int32_t* emitted, int32_t* k_out,
+                                               const int32_t* Lp, int L_imm, int32_t* L_next) {
   const int b = threadIdx.x;
   const bool in = b < B;
   const int d = in ? draft[b] : 0;
@@ -1549,11 +1560,14 @@ __global__ __launch_bounds__(64) void k_accept(const int32_t* block_ids, const i
     emitted[b] = b < k ? dn : (b == k ? bonus : -1);
   }
   if (b == 0) __hip_atomic_store(k_out, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  if (b == 0 && L_next) *L_next = (Lp ? *Lp : L_imm) + k + 1;  // the context after the k + 1 rows
 }
 
 void launch_accept(hipStream_t s, const int32_t* block_ids, const int32_t* draft, const int32_t* target, int B,
-                   int32_t* next_ids, int32_t* emitted, int32_t* k_out) {
-  hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, block_ids, draft, target, B, next_ids, emitted, k_out);
+                   int32_t* next_ids, int32_t* emitted, int32_t* k_out, const int32_t* Lp, int L_imm,
+                   int32_t* L_next) {
+  hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, block_ids, draft, target, B, next_ids, emitted, k_out, Lp,
+                     L_imm, L_next);
 }
 
 void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, const float* ustats, int n, int H,

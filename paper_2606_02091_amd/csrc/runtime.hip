@@ -112,6 +112,15 @@ struct dflare_handle {
   unsigned acnt_epoch = 0;  // value of every attention arrival counter (grows by D * chunks per draft block)
   int* err_host = nullptr;   // host-mapped barrier time-out flag
   int* err_dev = nullptr;
+  // Context length of slot 0 kept on the device (after dflare_accept_async): two words used
+  // in turn, Ldev[lcur] the current one, so that a verification step reads the length the
+  // draft step used while it writes the next one; L_hi bounds it from above.  kdev: k when
+  // the caller passes no word for it.
+  int32_t* Ldev = nullptr;
+  int32_t* kdev = nullptr;
+  bool dev_len = false;
+  int lcur = 0;
+  long L_hi = 0;
   bool trace = false;
   bool capture_persistent = false;  // debug capture written by the persistent launch itself
   unsigned long long* trace_buf = nullptr;
@@ -531,6 +540,8 @@ int build(dflare_handle* h, const dflare_weights* w) {
   TRY(dev_zalloc(h, &h->pidx, (size_t)h->blocks * kStatsPad * 4));
   TRY(dev_zalloc(h, &h->part, (size_t)h->blocks * kTNMax * 1024));
   TRY(dev_zalloc(h, &h->sync, kSyncBytes));
+  TRY(dev_zalloc(h, &h->Ldev, 4 * sizeof(int32_t)));
+  h->kdev = h->Ldev + 2;
 
   // ---- batched draft step: activations of max_batch * B rows
   {
@@ -666,8 +677,10 @@ DraftArgs draft_args(const dflare_handle* h) {
 DraftCall draft_call(const dflare_handle* h, const int32_t* ids, const int32_t* positions_host, int32_t* out) {
   const dflare_config& c = h->cfg;
   DraftCall d{};
-  d.L = h->Ls[0];
-  for (int b = 0; b < kMaxBlock; ++b) d.pos[b] = (b < c.block_size) ? (positions_host ? positions_host[b] : h->Ls[0] + b) : 0;
+  // with the length on the device (never together with host positions) the kernel adds it
+  d.L = h->dev_len ? 0 : h->Ls[0];
+  d.Lp = h->dev_len ? h->Ldev + h->lcur : nullptr;
+  for (int b = 0; b < kMaxBlock; ++b) d.pos[b] = (b < c.block_size) ? (positions_host ? positions_host[b] : d.L + b) : 0;
   d.ids = ids;
   d.tokens = out;
   d.logits = h->debug ? h->dbg_logits : nullptr;
@@ -712,7 +725,8 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   const int P = h->phases;
   // counters are monotonic across launches; start again from zero long before they wrap
   // (split-K counters reach (done_epoch + 1) * D * kg <= (done_epoch + 1) * D * 8)
-  const unsigned attn_adds = (unsigned)c.n_draft_layers * (unsigned)std::max(1, ceil_div(h->Ls[0], h->attn_chunk));
+  // (every layer adds the chunk capacity to each attention counter, whatever the length)
+  const unsigned attn_adds = (unsigned)c.n_draft_layers * (unsigned)h->attn_nch;
   if (h->bar_epoch + (unsigned)P > (1u << 24) || h->done_epoch + 1u > (1u << 22) ||
       ((uint64_t)h->done_epoch + 1u) * (uint64_t)c.n_draft_layers * kMaxSplit >= (1ull << 31) ||
       (uint64_t)h->acnt_epoch + attn_adds >= (1ull << 31)) {
@@ -751,8 +765,21 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   return check_launch(h, "draft_block");
 }
 
+// Bring a device-resident length of slot 0 back to the host (waits for the stream).
+int settle_len(dflare_handle* h) {
+  if (!h->dev_len) return DFLARE_OK;
+  HIP_OR_FAIL(h, hipStreamSynchronize(h->stream));
+  int32_t L = 0;
+  HIP_OR_FAIL(h, hipMemcpy(&L, h->Ldev + h->lcur, sizeof(L), hipMemcpyDeviceToHost));
+  if (L < 0 || L > h->L_hi) return fail(h, DFLARE_ERR_HIP, "device-resident context length out of range");
+  h->Ls[0] = L;
+  h->dev_len = false;
+  return DFLARE_OK;
+}
+
 // n_seq distinct slots in range
 int check_seqs(dflare_handle* h, int32_t n_seq, const int32_t* seq) {
+  TRY(settle_len(h));
   if (n_seq < 1 || n_seq > h->cfg.max_batch) return fail(h, DFLARE_ERR_INVALID_ARG, "n_seq must be in [1, max_batch]");
   if (!seq) return fail(h, DFLARE_ERR_INVALID_ARG, "seq is NULL");
   std::vector<char> seen(h->cfg.max_batch, 0);
@@ -1047,8 +1074,9 @@ int dflare_init(const dflare_config* cfg, const dflare_weights* w, const float* 
   return DFLARE_OK;
 }
 
-// Append rows 0 .. n_new-1 of target_hidden [S, ld, H] to slot 0 (arguments validated)
-int append_rows(dflare_handle* h, const void* target_hidden, int32_t n_new, int ld) {
+// Append rows 0 .. n_new-1 of target_hidden [S, ld, H] to slot 0 (arguments validated).
+// With Lp the rows go to slots *Lp + row, and the host's length is left alone.
+int append_rows(dflare_handle* h, const void* target_hidden, int32_t n_new, int ld, const int32_t* Lp = nullptr) {
   const dflare_config& c = h->cfg;
   if (c.variant & DFLARE_VARIANT_DFLASH) {  // the FC fusion runs on the batched GEMM, slot 0
     const int32_t seq0 = 0;
@@ -1074,7 +1102,8 @@ int append_rows(dflare_handle* h, const void* target_hidden, int32_t n_new, int 
   a.n_stat = H / 16;
   a.inv_dim = 1.0f / H;
   a.eps = c.rms_eps;
-  a.L = h->Ls[0];
+  a.L = Lp ? 0 : h->Ls[0];
+  a.Lp = Lp;
   a.n_new = n_new;
   a.kc = h->kc;
   a.vt = h->vt;
@@ -1094,12 +1123,14 @@ int append_rows(dflare_handle* h, const void* target_hidden, int32_t n_new, int 
   }
   int rc = check_launch(h, "fuse_append");
   if (rc != DFLARE_OK) return rc;
-  h->Ls[0] += n_new;
+  if (!Lp) h->Ls[0] += n_new;
   return DFLARE_OK;
 }
 
+
 int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_new) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  TRY(settle_len(h));
   if (!target_hidden) return fail(h, DFLARE_ERR_INVALID_ARG, "target_hidden is NULL");
   if (n_new < 1 || n_new > h->cfg.max_new)
     return fail(h, DFLARE_ERR_INVALID_ARG, "n_new must be in [1, max_new]");
@@ -1111,6 +1142,7 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
 int dflare_accept(dflare_handle* h, const int32_t* block_ids, const int32_t* draft_tokens, const int32_t* target_tokens,
                   const void* target_hidden, int32_t* next_ids, int32_t* emitted, int32_t* accepted) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  TRY(settle_len(h));
   if (!block_ids || !draft_tokens || !target_tokens || !target_hidden || !next_ids || !emitted)
     return fail(h, DFLARE_ERR_INVALID_ARG, "a device pointer is NULL");
   const dflare_config& c = h->cfg;
@@ -1121,13 +1153,58 @@ int dflare_accept(dflare_handle* h, const int32_t* block_ids, const int32_t* dra
   int32_t* k_host = h->err_host + 8;  // host-mapped word next to the barrier flag
   int32_t* k_dev = h->err_dev + 8;
   *(volatile int32_t*)k_host = -1;
-  launch_accept(h->stream, block_ids, draft_tokens, target_tokens, B, next_ids, emitted, k_dev);
+  launch_accept(h->stream, block_ids, draft_tokens, target_tokens, B, next_ids, emitted, k_dev, nullptr, 0, nullptr);
   TRY(check_launch(h, "accept"));
   HIP_OR_FAIL(h, hipStreamSynchronize(h->stream));
   const int k = *(volatile int32_t*)k_host;
   if (k < 0 || k >= B) return fail(h, DFLARE_ERR_HIP, "verification result not received");
   TRY(append_rows(h, target_hidden, k + 1, B));
   if (accepted) *accepted = k;
+  return DFLARE_OK;
+}
+
+int dflare_accept_async(dflare_handle* h, const int32_t* block_ids, const int32_t* draft_tokens,
+                        const int32_t* target_tokens, const void* target_hidden, int32_t* next_ids,
+                        int32_t* emitted, int32_t* accepted_dev) {
+  if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  if (!block_ids || !draft_tokens || !target_tokens || !target_hidden || !next_ids || !emitted)
+    return fail(h, DFLARE_ERR_INVALID_ARG, "a device pointer is NULL");
+  const dflare_config& c = h->cfg;
+  const int B = c.block_size;
+  if (c.max_new < B) return fail(h, DFLARE_ERR_INVALID_ARG, "dflare_accept_async needs max_new >= block_size");
+  if (c.variant & DFLARE_VARIANT_DFLASH) {  // its fusion runs on the batched path, which takes host lengths
+    int32_t k = 0;
+    TRY(dflare_accept(h, block_ids, draft_tokens, target_tokens, target_hidden, next_ids, emitted, &k));
+    if (accepted_dev) {
+      HIP_OR_FAIL(h, hipMemcpyAsync(accepted_dev, &k, sizeof(k), hipMemcpyHostToDevice, h->stream));
+      HIP_OR_FAIL(h, hipStreamSynchronize(h->stream));
+    }
+    return DFLARE_OK;
+  }
+  if (!h->dev_len) h->L_hi = h->Ls[0];
+  if (h->L_hi + B > c.max_context) {  // the bound is too loose to promise room: look at the length itself
+    TRY(settle_len(h));
+    h->L_hi = h->Ls[0];
+    if (h->L_hi + B > c.max_context)
+      return fail(h, DFLARE_ERR_CONTEXT_FULL, "a verified block could exceed max_context");
+  }
+  const int32_t* Lp = h->dev_len ? h->Ldev + h->lcur : nullptr;
+  launch_accept(h->stream, block_ids, draft_tokens, target_tokens, B, next_ids, emitted,
+                accepted_dev ? accepted_dev : h->kdev, Lp, h->Ls[0], h->Ldev + (h->lcur ^ 1));
+  TRY(check_launch(h, "accept"));
+  // all B rows go to slots L .. L + B - 1; the ones past the k + 1 verified rows lie beyond
+  // the new length, where the next draft block writes its own keys before anything reads them
+  const int32_t L_now = h->Ls[0];
+  const int32_t* base = Lp;
+  if (!base) {  // first step with the length on the device: the host value is still exact
+    TRY(append_rows(h, target_hidden, B, B));
+    h->Ls[0] = L_now;
+  } else {
+    TRY(append_rows(h, target_hidden, B, B, base));
+  }
+  h->lcur ^= 1;
+  h->dev_len = true;
+  h->L_hi += B;
   return DFLARE_OK;
 }
 
@@ -1140,6 +1217,7 @@ int dflare_draft_block(dflare_handle* h, const int32_t* block_ids, int32_t* draf
 int dflare_draft_block_pos(dflare_handle* h, const int32_t* block_ids, const int32_t* positions,
                            int32_t* draft_tokens) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  TRY(settle_len(h));
   if (!block_ids || !draft_tokens || !positions)
     return fail(h, DFLARE_ERR_INVALID_ARG, "block_ids / positions / draft_tokens is NULL");
   for (int b = 0; b < h->cfg.block_size; ++b)
@@ -1193,6 +1271,7 @@ int dflare_set_sampling(dflare_handle* h, float temperature, uint64_t seed) {
 
 int dflare_truncate_seq(dflare_handle* h, int32_t seq, int32_t new_len) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  TRY(settle_len(h));
   if (seq < 0 || seq >= h->cfg.max_batch) return fail(h, DFLARE_ERR_INVALID_ARG, "seq must be in [0, max_batch)");
   if (new_len < 0 || new_len > h->Ls[seq]) return fail(h, DFLARE_ERR_INVALID_ARG, "new_len must be in [0, L]");
   h->Ls[seq] = new_len;
@@ -1201,12 +1280,14 @@ int dflare_truncate_seq(dflare_handle* h, int32_t seq, int32_t new_len) {
 
 int dflare_context_len_seq(const dflare_handle* h, int32_t seq, int32_t* out) {
   if (!live(h) || !out || seq < 0 || seq >= h->cfg.max_batch) return DFLARE_ERR_INVALID_ARG;
+  if (seq == 0 && settle_len(const_cast<dflare_handle*>(h)) != DFLARE_OK) return DFLARE_ERR_HIP;
   *out = h->Ls[seq];
   return DFLARE_OK;
 }
 
 int dflare_truncate(dflare_handle* h, int32_t new_len) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  TRY(settle_len(h));
   if (new_len < 0 || new_len > h->Ls[0]) return fail(h, DFLARE_ERR_INVALID_ARG, "new_len must be in [0, L]");
   h->Ls[0] = new_len;
   return DFLARE_OK;
@@ -1214,6 +1295,7 @@ int dflare_truncate(dflare_handle* h, int32_t new_len) {
 
 int dflare_context_len(const dflare_handle* h, int32_t* out) {
   if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
+  if (settle_len(const_cast<dflare_handle*>(h)) != DFLARE_OK) return DFLARE_ERR_HIP;
   *out = h->Ls[0];
   return DFLARE_OK;
 }
@@ -1274,6 +1356,7 @@ int dflare_debug_read(dflare_handle* h, int what, int layer, float* host_out, in
 
 int dflare_debug_read_seq(dflare_handle* h, int what, int seq, int layer, float* host_out, int64_t count) {
   if (!live(h)) return fail(nullptr, DFLARE_ERR_INVALID_ARG, "invalid handle");
+  TRY(settle_len(h));
   if (!host_out) return fail(h, DFLARE_ERR_INVALID_ARG, "host_out is NULL");
   if (seq < 0 || seq >= h->cfg.max_batch) return fail(h, DFLARE_ERR_INVALID_ARG, "seq must be in [0, max_batch)");
   if (seq != 0 && what != DFLARE_DBG_KCACHE && what != DFLARE_DBG_VCACHE)

@@ -26,7 +26,7 @@ EXPORTED = (
     "dflare_status_str", "dflare_last_error", "dflare_debug_capture", "dflare_debug_read",
     "dflare_kernel_stats", "dflare_profile_begin", "dflare_profile_end", "dflare_set_option",
     "dflare_fuse_append_batched", "dflare_draft_block_batched", "dflare_truncate_seq",
-    "dflare_context_len_seq", "dflare_debug_read_seq", "dflare_set_sampling", "dflare_accept",
+    "dflare_context_len_seq", "dflare_debug_read_seq", "dflare_set_sampling", "dflare_accept", "dflare_accept_async",
     "dflare_anchor_attention_workspace", "dflare_anchor_attention_fwd", "dflare_anchor_attention_bwd",
     "dflare_weighted_ce_workspace", "dflare_weighted_ce", "dflare_weighted_ce_noalloc", "dflare_read_probe",
 )
@@ -98,6 +98,7 @@ def lib() -> ctypes.CDLL:
         "dflare_truncate_seq": ([vp, i32, i32], ctypes.c_int),
         "dflare_set_sampling": ([vp, ctypes.c_float, ctypes.c_uint64], ctypes.c_int),
         "dflare_accept": ([vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+        "dflare_accept_async": ([vp, vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
         "dflare_anchor_attention_workspace": ([ctypes.c_int32] * 6, ctypes.c_size_t),
         "dflare_anchor_attention_fwd": ([vp] * 6 + [ctypes.c_int32] * 6 + [vp, vp, vp, ctypes.c_size_t, vp],
                                         ctypes.c_int),
@@ -208,6 +209,16 @@ def dflare_accept(h: int, block_ids: torch.Tensor, draft_tokens: torch.Tensor, t
     _check(lib().dflare_accept(h, _ptr(block_ids), _ptr(draft_tokens), _ptr(target_tokens), _ptr(target_hidden),
                                _ptr(next_ids), _ptr(emitted), ctypes.byref(k)), h)
     return k.value
+
+
+def dflare_accept_async(h: int, block_ids: torch.Tensor, draft_tokens: torch.Tensor, target_tokens: torch.Tensor,
+                        target_hidden: torch.Tensor, next_ids: torch.Tensor, emitted: torch.Tensor,
+                        accepted: torch.Tensor | None = None) -> None:
+    """As dflare_accept without the host wait: k goes to the device int32 `accepted` (if
+    given) and the context length stays on the device (see include/dflare.h)."""
+    _check(lib().dflare_accept_async(h, _ptr(block_ids), _ptr(draft_tokens), _ptr(target_tokens),
+                                     _ptr(target_hidden), _ptr(next_ids), _ptr(emitted),
+                                     _ptr(accepted) if accepted is not None else None), h)
 
 
 # ---- training-side kernels (no handle) ----

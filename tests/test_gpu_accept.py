@@ -95,3 +95,99 @@ def test_accept_limits():
     k = dfl.dflare_accept(model.h, z, z, z, hid, z.clone(), z.clone())  # all candidates 0 == target 0
     assert k == B - 1 and model.context_len == 3 + B
     model.close()
+
+
+@pytest.mark.parametrize("case,variant", [("hd128", 0), ("ragged", 0), ("gqa8_hd64", 0),
+                                          ("gqa8_hd64", dfl.VARIANT_DFLASH)])
+def test_async_accept_matches_sync(case, variant):
+    """dflare_accept_async keeps the context length on the device.  A loop of draft_block,
+    a target built on the device and accept_async, enqueued with no host wait, must give the
+    same draft tokens, k, emitted tokens and next blocks, bit for bit, as the same loop with
+    dflare_accept (pinned to the oracle above), and the same length and caches after it.
+    max_context is tight, so the host's upper bound on the length runs out and the call
+    reads the length back several times."""
+    cfg, L, mode = TP.CASES[case]
+    B, V = cfg.block_size, cfg.vocab
+    print(f"[accept_async] {case} variant {variant}", flush=True)
+    kinds = synth.BASE_KINDS + (("fc", "fc_bias") if variant else ())
+    w = synth.make_weights(cfg, kinds=kinds)
+    lg = w.pop("fusion_logits")
+    if variant:  # DFlash: no fusion logits; the call waits as dflare_accept does
+        lg = None
+    plan = [min(k, B - 1) for k in (B - 1, 0, 1, 0, 2, 0, 0, 1, 3, 0)]
+    grow = sum(k + 1 for k in plan)
+    max_context = L + grow + B + 2
+    hids = [dfl.bf16_tensor(synth.hidden_rows(cfg, 1000 + i * B, B, seed=11)) for i in range(len(plan))]
+    kw = torch.tensor(plan, dtype=torch.int64, device="cuda")
+    pos = torch.arange(B, device="cuda")
+
+    def run(use_async):
+        model = dfl.DraftModel(cfg, w, lg, max_context=max_context, max_new=16, variant=variant)
+        s = 0
+        for n in TP.append_plan(cfg, L, mode):
+            model.fuse_append(dfl.bf16_tensor(synth.hidden_rows(cfg, s, n)))
+            s += n
+        ids = TP.ids_tensor(synth.block_ids(cfg, step=0))
+        out = {x: torch.empty(len(plan), B, dtype=torch.int32, device="cuda") for x in ("draft", "em", "next")}
+        ks = torch.empty(len(plan), dtype=torch.int32, device="cuda")
+        draft = torch.empty(B, dtype=torch.int32, device="cuda")
+        for i in range(len(plan)):
+            dfl.dflare_draft_block(model.h, ids, draft)
+            shifted = torch.roll(draft, -1)
+            tgt = torch.where(pos < kw[i], shifted, (shifted + 1) % V).to(torch.int32)
+            nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+            if use_async:
+                dfl.dflare_accept_async(model.h, ids, draft, tgt, hids[i], nxt, out["em"][i], ks[i:i + 1])
+            else:
+                ks[i] = dfl.dflare_accept(model.h, ids, draft, tgt, hids[i], nxt, out["em"][i])
+            out["draft"][i].copy_(draft)
+            out["next"][i].copy_(nxt)
+            ids = nxt
+        torch.cuda.synchronize()
+        res = {x: t.cpu().numpy() for x, t in out.items()}
+        res["k"] = ks.cpu().numpy()
+        res["L"] = model.context_len
+        res["cache"] = [dfl.dflare_debug_read(model.h, what, i, (res["L"], cfg.n_kv_heads, cfg.head_dim))
+                        for i in range(cfg.n_draft_layers) for what in (dfl.DBG_KCACHE, dfl.DBG_VCACHE)]
+        return model, res
+
+    m_sync, ref = run(False)
+    m_async, got = run(True)
+    assert list(ref["k"]) == plan and list(got["k"]) == plan
+    for x in ("draft", "em", "next"):
+        assert np.array_equal(got[x], ref[x]), x
+    assert got["L"] == ref["L"] == L + grow
+    for a, b in zip(got["cache"], ref["cache"]):
+        assert np.array_equal(a, b)
+    # the host calls see the device's length: truncate, then an ordinary append and a block
+    m_async.truncate(L + 1)
+    m_sync.truncate(L + 1)
+    rows = dfl.bf16_tensor(synth.hidden_rows(cfg, 5000, 3, seed=3))
+    ids = TP.ids_tensor(synth.block_ids(cfg, step=1))
+    toks = []
+    for m in (m_sync, m_async):
+        m.fuse_append(rows)
+        toks.append(m.draft_block(ids).cpu().numpy())
+        assert m.context_len == L + 4
+    assert np.array_equal(toks[0], toks[1])
+    m_sync.close()
+    m_async.close()
+
+
+def test_async_accept_context_full():
+    """accept_async with no room left: CONTEXT_FULL after reading the length back, and
+    nothing changes."""
+    cfg, L, mode = TP.CASES["tiny"]
+    B = cfg.block_size
+    w, lg = P.weights_for(cfg)
+    model = dfl.DraftModel(cfg, w, lg, max_context=B + 3, max_new=16)
+    model.fuse_append(dfl.bf16_tensor(synth.hidden_rows(cfg, 0, 3)))
+    z = torch.zeros(B, dtype=torch.int32, device="cuda")
+    hid = dfl.bf16_tensor(synth.hidden_rows(cfg, 0, B))
+    kd = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    dfl.dflare_accept_async(model.h, z, z, z, hid, z.clone(), z.clone(), kd)  # all candidates 0 == target 0
+    with pytest.raises(dfl.DFlareError) as e:
+        dfl.dflare_accept_async(model.h, z, z, z, hid, z.clone(), z.clone(), kd)
+    assert e.value.status == dfl.ERR_CONTEXT_FULL
+    assert int(kd.item()) == B - 1 and model.context_len == 3 + B
+    model.close()
