@@ -5,6 +5,7 @@ import os
 import shutil
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -29,16 +30,17 @@ def hipcc() -> str:
 def build(verbose: bool = False) -> str:
     """Compile every HIP source of the library for gfx950 and link the shared object."""
     os.makedirs(LIBDIR, exist_ok=True)
-    objs = []
     common = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
               # keep the compiler away from packed fp32 instructions
               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
               "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function"]
-    for src in SOURCES:
-        obj = os.path.join(LIBDIR, src.replace(".hip", ".o"))
-        cmd = [hipcc(), *common, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
-        _run(cmd, verbose)
-        objs.append(obj)
+    objs = [os.path.join(LIBDIR, src.replace(".hip", ".o")) for src in SOURCES]
+    cmds = [[hipcc(), *common, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
+            for src, obj in zip(SOURCES, objs)]
+    # the translation units are independent: compile them side by side
+    with ThreadPoolExecutor(max_workers=len(cmds)) as ex:
+        for f in [ex.submit(_run, cmd, verbose) for cmd in cmds]:
+            f.result()
     tmp = LIB + f".tmp{os.getpid()}"
     _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)

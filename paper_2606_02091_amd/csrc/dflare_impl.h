@@ -33,8 +33,9 @@ constexpr int kTraceSlots = 4;
 constexpr int kTNMax = 8;         // output tiles a GEMM work-group accumulates at once
 constexpr int kMaxSplit = 8;      // work-groups that split one GEMM output range along K
 constexpr int kMaxBlocks = 1024;  // work-groups of the draft-block kernel
-// Split-K arrival counters: one per (GEMM phase kind, output range), each on its own
-// 128 B line, after the grid-barrier counters and the LM-head completion counter.
+// GEMM phase kinds that may split K (one tagged partial area each); a reserved block of
+// kSplitKinds x kMaxBlocks counter lines follows the grid-barrier counters and the LM-head
+// completion counter in the synchronisation area.
 constexpr int kSplitKinds = 4;    // QKV, O, gate/up, down
 // Attention arrival counters: one per KV head, each on its own 128 B line, after the split-K ones.
 constexpr int kMaxKvHeads = 128;
@@ -131,8 +132,8 @@ struct DraftArgs {
   long ha_stride;
   float* pmax;           // [blocks][kStatsPad] best logit of each work-group per row
   int* pidx;
-  float* part;           // split-K partial sums [blocks][kTNMax][64 lanes][4]
-  unsigned* kcnt;        // split-K arrival counters [kSplitKinds][kMaxBlocks], 32 words apart
+  float* part;           // split-K partial sums [kSplitKinds][blocks][kTNMax][64 lanes][4], tagged per use
+  unsigned* kcnt;        // spare counters [kSplitKinds][kMaxBlocks], 32 words apart (unused by the draft block)
   unsigned* acnt;        // attention arrival counters [n_kv], 32 words apart, monotonic across launches
   // synchronisation
   unsigned* bar;          // kBarCounters counters, 32 words apart, monotonic across launches

@@ -371,6 +371,12 @@ __global__ __launch_bounds__(256) void k_matvec(float* y, const uint16_t* A, con
 typedef const CONSTANT DraftArgs* Args;
 typedef const CONSTANT DraftCall* Call;
 
+// The work-group's barrier-failure flag lives in LDS (written and read by wave 0 only): a
+// flag in private memory would be read with a vector load, which completes only after every
+// load the wave issued before it, so a poll behind weight requests could not start early.
+typedef volatile LDSP int* Failed;
+constexpr int kFailOff = 80 * 1024 - 16;  // just below the attention staging area
+
 // ---- grid barrier ----
 // Arrival: every wave waits for its own stores, then one atomic add per work-group on one
 // of kBarCounters counters (spreading the arrivals keeps same-address atomics from
@@ -390,8 +396,8 @@ __device__ __forceinline__ void trace_mark(Call c, int slot, int nslots) {
   if (c->trace && threadIdx.x == 0) c->trace[(long)blockIdx.x * nslots + slot] = wall_clock64();
 }
 
-__device__ __forceinline__ void grid_wait(Args a, unsigned epoch, bool& failed) {
-  if (threadIdx.x < 64 && !failed) {
+__device__ __forceinline__ void grid_wait(Args a, unsigned epoch, Failed failed) {
+  if (threadIdx.x < 64 && !*failed) {
     const int lane = threadIdx.x;
     const unsigned n = gridDim.x;
     const unsigned share = n / kBarCounters + ((unsigned)lane < n % kBarCounters ? 1u : 0u);
@@ -404,8 +410,10 @@ __device__ __forceinline__ void grid_wait(Args a, unsigned epoch, bool& failed) 
       if (__all(ok)) break;
       __builtin_amdgcn_s_sleep(1);
       if (wall_clock64() - t0 > kBarrierTimeout) {
-        failed = true;
-        if (lane == 0) __hip_atomic_store(a->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        if (lane == 0) {
+          *failed = 1;
+          __hip_atomic_store(a->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
         break;
       }
     }
@@ -420,7 +428,7 @@ struct PhaseCtl {
 };
 
 __device__ __forceinline__ void phase_begin(Args a, Call c, const PhaseCtl& pc,
-                                            bool& failed) {
+                                            Failed failed) {
   if (pc.wait) grid_wait(a, pc.epoch, failed);
   trace_mark(c, pc.slot, pc.nslots);
 }
@@ -492,8 +500,8 @@ struct GemmJob {
   uint16_t* kc;        // cache of this layer
   uint16_t* vt;
   // split-K
-  unsigned* cnt;       // arrival counters of this phase kind, 32 words apart
-  unsigned target;     // counter value once every work-group of a range has arrived
+  float* part;         // partial tiles of this phase kind [blocks][kTNMax][64 lanes][4]
+  unsigned tag;        // low mantissa bit every partial of this use carries
 };
 
 // LDS of a GEMM phase: partial tiles [kWaves][TN][64 lanes] (64 KiB at most), then the
@@ -503,7 +511,8 @@ constexpr int kLdsRedBytes = kWaves * kTNMax * 1024;
 // K / V^T staging area from kStageOff to the end.  GEMM phases never touch the staging
 // area, so the next layer's context pieces can be streamed into it during them.
 constexpr int kStageOff = 80 * 1024;
-static_assert(kLdsRedBytes + 2048 <= kStageOff, "GEMM scratch stays below the attention staging area");
+static_assert(kLdsRedBytes + 2048 <= kFailOff && kFailOff + 16 == kStageOff,
+              "GEMM scratch, the failure flag and the attention staging area do not overlap");
 
 
 // Epilogue of one finished 16 x 16 output tile nt (lane holds rows quad*4 .. +3 of column
@@ -742,13 +751,14 @@ __device__ __forceinline__ GemmGeom gemm_geom(Args a, int kind, int kg, int wave
 // fragments (the weight loads of padding steps re-read a real tile).  The loop body has
 // no conditional loads, so the compiler's memory wait counts stay exact.  At the end of a
 // chunk the waves' sums meet in LDS and are added in wave order; with kg = 1 wave j then
-// finishes tile j of the chunk, otherwise it stores the work-group's partial tile and the
-// last work-group of the range to arrive adds the kg partials in K order and finishes the
-// range's tiles, so results never depend on timing.  The first NS steps of weights are
-// requested before the grid barrier: they do not depend on the previous phase.
+// finishes tile j of the chunk, otherwise the work-groups but the range's first store their
+// partial tiles (tagged, see the split-K combine below) and the first adds the kg partials in
+// K order and finishes the range's tiles, so results never depend on timing.  The first NS
+// steps of weights are requested before the grid barrier: they do not depend on the previous
+// phase.
 template <int EPI, int TN>
 __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int kind, int kg, const PhaseCtl& pc,
-                                           bool& failed, u32x4* smem) {
+                                           Failed failed, u32x4* smem) {
   constexpr int NS = gemm_ns(TN);
   static_assert(TN <= kTNMax && TN <= kWaves, "one tile per wave in the chunk epilogue");
   f32x4* red = reinterpret_cast<f32x4*>(smem);
@@ -798,7 +808,7 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
   // The first NS steps' weights go out before the grid barrier (they do not depend on the
   // previous phase), their A fragments after it.
   u32x4 w[NS][TN], ah[NS], al[NS];
-  if (total > 0) {
+  auto first_weights = [&]() {
     chunk_bases(0);
 #pragma unroll
     for (int i = 0; i < NS; ++i) {
@@ -807,7 +817,8 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
       for (int j = 0; j < TN; ++j) w[i][j] = __builtin_nontemporal_load(Wg + wb[j] + ko);
       __builtin_amdgcn_sched_barrier(0);
     }
-  }
+  };
+  if (total > 0) first_weights();
   phase_begin(a, c, pc, failed);
   if (total > 0) {
 #pragma unroll
@@ -834,6 +845,7 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
 #pragma unroll
   for (int j = 0; j < TN; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  f32x4 own = f32x4{0.f, 0.f, 0.f, 0.f};  // split K: the reducer's own partial of tile `wave`
   // end of chunk ch: the waves' partial sums meet in LDS; wave j finishes tile j
   auto chunk_end = [&](int ch) {
 #pragma unroll
@@ -867,8 +879,12 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
         for (int i = 0; i < 4; ++i) v[i] *= s_rstd[quad * 4 + i];
       }
       if (kg > 1) {
-        f32x4* pp = reinterpret_cast<f32x4*>(a->part) + (((long)b * kTNMax + wave) * 64 + lane);
-        st_wt16(pp, __builtin_bit_cast(u32x4, v));
+        // the partial, its low mantissa bits replaced by this use's tag (2^-23 relative)
+        u32x4 t = __builtin_bit_cast(u32x4, v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) t[e] = (t[e] & ~1u) | g.tag;
+        if (geo.kgi == 0) own = __builtin_bit_cast(f32x4, t);
+        else st_wt16(reinterpret_cast<f32x4*>(g.part) + (((long)b * kTNMax + wave) * 64 + lane), t);
       } else {
         gemm_epilogue<EPI>(a, c, g, t0 + ch * TN + wave, v, wave, s_bv, s_bi);
       }
@@ -931,21 +947,36 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
     trace_mark(c, pc.slot + 2, pc.nslots);
   }
 
-  if (kg > 1 && total > 0) {
-    // split K: the last work-group of the range to arrive adds the partials in K order
-    wait_vm();
-    __syncthreads();
-    if (tid == 0) {
-      const unsigned old = __hip_atomic_fetch_add(g.cnt + rg * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      *s_flag = (old + 1u == g.target) ? 1 : 0;
+  if (kg > 1 && total > 0 && geo.kgi == 0 && wave < T) {
+    // split K: work-group 0 of the range adds the kg partials of its tiles in K order.  Every
+    // partial word carries the tag of this use of the partial area (the area of a phase kind
+    // is used once per layer, and the tag alternates between uses), so a load that returns
+    // the tag returns this use's value: the other work-groups store and go on, and the
+    // reducer polls their partials directly, with no counter in between.
+    const f32x4* pp = reinterpret_cast<const f32x4*>(g.part) + (((long)rg * kg * kTNMax + wave) * 64 + lane);
+    f32x4 pq[kMaxSplit];
+    const long long tw = wall_clock64();
+    while (true) {
+      bool ok = true;
+#pragma unroll
+      for (int q = 1; q < kMaxSplit; ++q)
+        if (q < kg) {
+          pq[q] = ld_coh16(pp + (long)q * kTNMax * 64);
+          const u32x4 t = __builtin_bit_cast(u32x4, pq[q]);
+          ok = ok && ((t[0] & t[1] & t[2] & t[3] & 1u) == g.tag) && (((t[0] | t[1] | t[2] | t[3]) & 1u) == g.tag);
+        }
+      if (__all(ok)) break;
+      __builtin_amdgcn_s_sleep(1);
+      if (wall_clock64() - tw > kBarrierTimeout) {
+        if (lane == 0) __hip_atomic_store(a->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        break;
+      }
     }
-    __syncthreads();
-    if (*s_flag && wave < T) {
-      const f32x4* pp = reinterpret_cast<const f32x4*>(a->part) + (((long)rg * kg * kTNMax + wave) * 64 + lane);
-      f32x4 v = ld_coh16(pp);
-      for (int q = 1; q < kg; ++q) v += ld_coh16(pp + (long)q * kTNMax * 64);
-      gemm_epilogue<EPI>(a, c, g, t0 + wave, v, wave, s_bv, s_bi);
-    }
+    f32x4 v = own;
+#pragma unroll
+    for (int q = 1; q < kMaxSplit; ++q)
+      if (q < kg) v += pq[q];
+    gemm_epilogue<EPI>(a, c, g, t0 + wave, v, wave, s_bv, s_bi);
   }
 
   if constexpr (EPI == EPI_ARGMAX) {
@@ -1066,7 +1097,7 @@ __device__ __forceinline__ void attn_stage(Args a, Call dc, int layer, int j, u3
 }
 
 template <int HD>
-__device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed,
+__device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const PhaseCtl& pc, Failed failed,
                                            u32x4* smem, bool staged) {
   using A = AttnShape<HD>;
   constexpr int CK = A::CK, NKB = A::NKB, KC = A::KC, VC = A::VC, KP = A::KP;
@@ -1076,7 +1107,7 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
   u32x4* sV = sK + KP;                                             // (row d, col) at d*VC + (col ^ vswz(d))
   f32x4* sO = reinterpret_cast<f32x4*>(smem);                      // merge: [kWaves][DT][64]
   float2* sML = reinterpret_cast<float2*>(sO + kWaves * DT * 64);  // [kWaves][16]
-  static_assert(kWaves * DT * 64 * 16 + kWaves * 16 * 8 <= kStageOff, "LDS merge area");
+  static_assert(kWaves * DT * 64 * 16 + kWaves * 16 * 8 <= kFailOff, "LDS merge area");
 
   const int L = ctx_len(dc), B = a->B, nkv = a->n_kv, G = a->n_q / a->n_kv, Lcap = a->Lcap;
   const int nch = attn_chunks(L, CK);
@@ -1292,7 +1323,7 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
 // runs over S waves (S = 4 / rows per work-group), which meet in LDS in run order.  Waves
 // 4-7 meanwhile stream the context of the next layer's attention item into LDS (stage).
 template <int HD>
-__device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool& failed, u32x4* smem,
+__device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, Failed failed, u32x4* smem,
                            bool stage) {
   using A = AttnShape<HD>;
   constexpr int DPL = HD / 64;                 // dims per lane
@@ -1305,15 +1336,17 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
   if (stage) attn_stage<HD>(a, dc, layer + 1, b, smem, CW);
   // the group wait: all items of KV head g stored (persistent launch; else the launch boundary)
   if (pc.wait) {
-    if (b < W * nkv && threadIdx.x < 64 && !failed) {
+    if (b < W * nkv && threadIdx.x < 64 && !*failed) {
       const unsigned* cnt = a->acnt + (b % nkv) * 32;
       const unsigned target = dc->acnt_base + (unsigned)(layer + 1) * (unsigned)a->nch;
       const long long t0 = wall_clock64();
       while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
         __builtin_amdgcn_s_sleep(1);
         if (wall_clock64() - t0 > kBarrierTimeout) {
-          failed = true;
-          if (threadIdx.x == 0) __hip_atomic_store(a->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          if (threadIdx.x == 0) {
+            *failed = 1;
+            __hip_atomic_store(a->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          }
           break;
         }
       }
@@ -1427,13 +1460,13 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, bool&
 
 // GEMM phase with the plan's chunk width (the LM head always uses 8)
 template <int EPI>
-__device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int layer, const PhaseCtl& pc, bool& failed,
+__device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int layer, const PhaseCtl& pc, Failed failed,
                                               u32x4* smem) {
   GemmJob g = make_job(a, c, kind, layer);
   const int kg = kind == PH_LM ? 1 : a->kg[kind];
   const int slot = kind == PH_QKV ? 0 : kind == PH_O ? 1 : kind == PH_GU ? 2 : 3;
-  g.cnt = a->kcnt + (long)slot * kMaxBlocks * 32;
-  g.target = (c->done_epoch * (unsigned)a->D + (unsigned)layer + 1u) * (unsigned)kg;
+  g.part = a->part + (long)slot * gridDim.x * kTNMax * 256;
+  g.tag = (c->done_epoch * (unsigned)a->D + (unsigned)layer + 1u) & 1u;
   if constexpr (EPI == EPI_ARGMAX) {
     gemm_phase<EPI, 8>(a, c, g, kind, 1, pc, failed, smem);
   } else {
@@ -1458,7 +1491,8 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
   const int p0 = ka->p0, p1 = ka->p1;
   const int nphase = phase_count(a->D);
   const int nslots = kTraceSlots * nphase;
-  bool failed = false;
+  const Failed failed = (Failed)((LDSP char*)(char*)smem + kFailOff);
+  if (threadIdx.x == 0) *failed = 0;
   unsigned epoch = c->bar_epoch;  // grid barriers passed
   for (int p = p0; p < p1; ++p) {
     int kind, layer;

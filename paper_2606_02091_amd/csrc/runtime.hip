@@ -538,7 +538,8 @@ int build(dflare_handle* h, const dflare_weights* w) {
   TRY(dev_zalloc(h, &h->HA, (size_t)D * h->ha_stride * 16));
   TRY(dev_zalloc(h, &h->pmax, (size_t)h->blocks * kStatsPad * 4));
   TRY(dev_zalloc(h, &h->pidx, (size_t)h->blocks * kStatsPad * 4));
-  TRY(dev_zalloc(h, &h->part, (size_t)h->blocks * kTNMax * 1024));
+  // split-K partial tiles: one area per GEMM phase kind (tagged per use, see gemm_phase)
+  TRY(dev_zalloc(h, &h->part, (size_t)kSplitKinds * h->blocks * kTNMax * 1024));
   TRY(dev_zalloc(h, &h->sync, kSyncBytes));
   TRY(dev_zalloc(h, &h->Ldev, 4 * sizeof(int32_t)));
   h->kdev = h->Ldev + 2;
@@ -714,6 +715,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   if (*(volatile int*)h->err_host) {  // an earlier persistent launch timed out at a grid barrier
     HIP_OR_FAIL(h, hipStreamSynchronize(s));
     HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
+    HIP_OR_FAIL(h, hipMemsetAsync(h->part, 0, (size_t)kSplitKinds * h->blocks * kTNMax * 1024, s));
     HIP_OR_FAIL(h, hipStreamSynchronize(s));
     h->bar_epoch = h->done_epoch = h->acnt_epoch = 0;
     *(volatile int*)h->err_host = 0;
@@ -730,7 +732,9 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   if (h->bar_epoch + (unsigned)P > (1u << 24) || h->done_epoch + 1u > (1u << 22) ||
       ((uint64_t)h->done_epoch + 1u) * (uint64_t)c.n_draft_layers * kMaxSplit >= (1ull << 31) ||
       (uint64_t)h->acnt_epoch + attn_adds >= (1ull << 31)) {
+    // the split-K partial tags follow done_epoch: start them again from cleared areas
     HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
+    HIP_OR_FAIL(h, hipMemsetAsync(h->part, 0, (size_t)kSplitKinds * h->blocks * kTNMax * 1024, s));
     h->bar_epoch = h->done_epoch = h->acnt_epoch = 0;
   }
   if (h->trace && !h->trace_buf) TRY(dev_zalloc(h, &h->trace_buf, (size_t)h->blocks * kTraceSlots * P * 8));
