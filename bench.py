@@ -108,14 +108,17 @@ def kernel_bytes(cfg, L, n_mean, variant="dflare"):
     }
 
 
-KERNEL_SOURCES = ("kernels.hip", "batched.hip", "device_common.h", "dflare_impl.h", "batched.h")
+# device sources of the kernels a workload's counter record covers: the batch-1 step runs the
+# draft-block, fusion and context K/V kernels; the batched step the batched kernels
+KERNEL_SOURCES = {"batch1": ("kernels.hip", "device_common.h", "dflare_impl.h"),
+                  "batched": ("batched.hip", "batched.h", "device_common.h", "dflare_impl.h")}
 
 
-def source_sha() -> str:
-    """sha256 prefix of the device sources the recorded counter values belong to."""
+def source_sha(workload: str = "qwen3_8b") -> str:
+    """sha256 prefix of the device sources the recorded counter values of `workload` belong to."""
     import hashlib
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in KERNEL_SOURCES["batched" if workload == "batched" else "batch1"]:
         with open(os.path.join(ROOT, "paper_2606_02091_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -131,7 +134,7 @@ def counter_traffic(kernel: str, workload: str, context: int):
     device sources of this build; else None."""
     try:
         rec = json.load(open(counter_record_path(workload)))
-        sha = source_sha()
+        sha = source_sha(workload)
     except (OSError, ValueError):
         return None
     k = rec.get("kernels", {}).get(kernel)
@@ -185,7 +188,7 @@ def summarize_counters(fetch_dir: str, write_dir: str, workload: str, context: i
         out["kernels"][kname] = {"fetch_kib": int(statistics.median(fr[i][1] for i in pick)),
                                  "write_kib": int(statistics.median(wr[i][1] for i in pick)),
                                  "dispatches": len(pick)}
-    out.update({"workload": workload, "context": context, "sources_sha256_16": source_sha(),
+    out.update({"workload": workload, "context": context, "sources_sha256_16": source_sha(workload),
                 "fetch_scale": scale["fetch"], "write_scale": scale["write"],
                 "_comment": "HBM KiB per dispatch from rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs of bench.py on "
                             "this workload, scaled to bytes by a plain 1 GiB device copy read with the same counters; "
