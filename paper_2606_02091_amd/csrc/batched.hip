@@ -629,6 +629,78 @@ __global__ __launch_bounds__(256) void k_bfuse(const uint16_t* hidden, int ld, i
   }
 }
 
+// The same fusion for all D <= 8 layers of appended row r in one work-group of 512 threads
+// (H <= 4096, 8 columns per thread): the S target rows of r are read once and each value
+// feeds the D weighted sums, so HBM sees the rows once however the work-groups are placed.
+// The sums are formed in the same order as k_bfuse forms them for one layer; the RMS
+// statistics over the 8 waves.
+constexpr int kBFuseMaxD = 8;
+__global__ __launch_bounds__(512) void k_bfuse_all(const uint16_t* hidden, int ld, int S, int H, int D,
+                                                   const float* alpha, const float* gain, float eps, u32x4* A,
+                                                   int mt_max) {
+  constexpr int JB = 12;  // target rows in flight
+  __shared__ float red[kBFuseMaxD][8];
+  const int r = blockIdx.x;
+  const int Kt = H / 32;
+  const bool has = threadIdx.x * 8 < H;
+  const int k0 = has ? threadIdx.x * 8 : 0;
+  float u[kBFuseMaxD][8];
+#pragma unroll
+  for (int i = 0; i < kBFuseMaxD; ++i)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) u[i][e] = 0.f;
+  for (int j0 = 0; j0 < S; j0 += JB) {
+    u32x4 v[JB];
+#pragma unroll
+    for (int jj = 0; jj < JB; ++jj)
+      v[jj] = *reinterpret_cast<const u32x4*>(hidden + ((long)min(j0 + jj, S - 1) * ld + r) * H + k0);
+#pragma unroll
+    for (int jj = 0; jj < JB; ++jj) {
+      if (j0 + jj < S) {
+#pragma unroll
+        for (int i = 0; i < kBFuseMaxD; ++i) {
+          if (i < D) {
+            const float a = alpha[i * S + j0 + jj];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              u[i][2 * e] = fmaf(a, bf2f(v[jj][e] & 0xFFFFu), u[i][2 * e]);
+              u[i][2 * e + 1] = fmaf(a, bf2f(v[jj][e] >> 16), u[i][2 * e + 1]);
+            }
+          }
+        }
+      }
+    }
+  }
+  float sq[kBFuseMaxD];
+#pragma unroll
+  for (int i = 0; i < kBFuseMaxD; ++i) {
+    sq[i] = 0.f;
+    if (has)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sq[i] += u[i][e] * u[i][e];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) sq[i] += __shfl_xor(sq[i], off);
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int i = 0; i < kBFuseMaxD; ++i) red[i][w] = sq[i];
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kBFuseMaxD; ++i) {
+    if (i >= D) break;
+    const float tot = ((red[i][0] + red[i][1]) + (red[i][2] + red[i][3])) + ((red[i][4] + red[i][5]) + (red[i][6] + red[i][7]));
+    const float rstd = rsqrtf(tot / H + eps);
+    if (has) {
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = u[i][e] * rstd * gain[(long)i * H + k0 + e];
+      u32x4* Ai = A + (long)i * mt_max * Kt * 64;
+      Ai[frag_off(r, k0, Kt) >> 3] = pack_h8(v);
+    }
+  }
+}
+
 // debug: fp16 A fragments of D layers -> rows [D, n, H] fp32
 __global__ void k_bfrag_rows(const u32x4* A, int n, int H, int mt_max, float* out) {
   const int r = blockIdx.x, i = blockIdx.y, Kt = H / 32;
@@ -933,7 +1005,10 @@ void launch_bembed_norm(hipStream_t s, const uint16_t* embed, const int32_t* ids
 
 void launch_bfuse(hipStream_t s, const uint16_t* hidden, int N, int ld, int S, int H, int D, const float* alpha,
                   const float* gain, float eps, u32x4* A, int mt_max) {
-  hipLaunchKernelGGL(k_bfuse, dim3(N, D), dim3(256), 0, s, hidden, ld, S, H, alpha, gain, eps, A, mt_max);
+  if (D <= kBFuseMaxD && H <= 4096)
+    hipLaunchKernelGGL(k_bfuse_all, dim3(N), dim3(512), 0, s, hidden, ld, S, H, D, alpha, gain, eps, A, mt_max);
+  else
+    hipLaunchKernelGGL(k_bfuse, dim3(N, D), dim3(256), 0, s, hidden, ld, S, H, alpha, gain, eps, A, mt_max);
 }
 
 void launch_bfrag_cat(hipStream_t s, const uint16_t* hidden, int N, int ld, int S, int H, u32x4* A) {
