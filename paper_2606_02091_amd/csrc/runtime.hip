@@ -324,25 +324,18 @@ GemmPlan choose_plan(const char* name, int Nt, int Kt, int blocks, bool allow_sp
 }
 
 // K split of a batched GEMM (1 where the epilogue needs whole sums before it can start
-// or the tiles outnumber the arrival counters): the smallest estimated time, counted in
-// k-tiles per work-group as (rounds of work-groups over the resident slots, two per CU)
-// x (k-tiles per part), plus 20 k-tiles per extra part for writing and reading back its
-// partial tile (a measured fit).
+// or the tiles outnumber the arrival counters): the deepest split whose work-groups still
+// fit one per CU (tiles x kg <= CUs), each part keeping at least 8 k-tiles.  A sweep of the
+// split at the Qwen3-8B shape with 512 rows picked exactly these (Q/K/V 2, output 4, down 4,
+// gate/up 1, the 8-layer context K/V of a ~270-row append 1); an earlier cost fit in k-tiles
+// per work-group chose 3 for Q/K/V, 23% slower.
 // DFLARE_BSPLIT_<NAME>=kg overrides the choice (tuning).
 int bgemm_split(int cus, const char* name, int Nt, int Mt, int Kt, int layers, bool allow) {
   const long tiles = (long)bgemm_groups(Nt, Mt) * layers;
   if (!allow || tiles > kBCounters) return 1;
   int best = 1;
-  double best_t = 1e300;
-  for (int kg : {1, 2, 3, 4, 6, 8}) {
-    if (kg > 1 && Kt < 8 * kg) continue;
-    const double t = (double)ceil_div(tiles * kg, (long)cus * kBWavesPerSimd) * ceil_div(Kt, kg) +
-                     (kg > 1 ? 4.0 + 20.0 * (kg - 1) : 0.0);
-    if (t < best_t - 1e-9) {
-      best_t = t;
-      best = kg;
-    }
-  }
+  for (int kg : {2, 3, 4, 6, 8})
+    if (tiles * kg <= cus && Kt >= 8 * kg) best = kg;
   char key[64];
   snprintf(key, sizeof key, "DFLARE_BSPLIT_%s", name);
   if (const char* env = getenv(key)) {
