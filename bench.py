@@ -414,22 +414,25 @@ def bench_loop(args):
     hid = dfl.bf16_tensor(synth.hidden_rows(cfg, L, B, seed=11))
     ks = torch.from_numpy(np.random.default_rng(5).integers(0, B, size=total).astype(np.int64)).cuda()
     pos = torch.arange(B, device="cuda")
+    # the target's disagreement pattern of every iteration, made before the timed region: XOR 1
+    # at positions >= k changes a token and keeps it in the vocabulary (V is even)
+    assert V % 2 == 0
+    flip = (pos[None, :] >= ks[:, None]).to(torch.int32)
     ids = torch.from_numpy(synth.block_ids(cfg)).cuda()
     draft = torch.empty(B, dtype=torch.int32, device="cuda")
-    nxt = torch.empty(B, dtype=torch.int32, device="cuda")
+    tgt = torch.empty(B, dtype=torch.int32, device="cuda")
     em = torch.empty(B, dtype=torch.int32, device="cuda")
     k_dev = torch.zeros(total, dtype=torch.int32, device="cuda")
 
     def it(i):
         dfl.dflare_draft_block(h, ids, draft)
         # synthetic target: agrees with candidates 1..k, then predicts another token
-        shifted = torch.roll(draft, -1)
-        tgt = torch.where(pos < ks[i], shifted, (shifted + 1) % V).to(torch.int32)
+        torch.bitwise_xor(torch.roll(draft, -1), flip[i], out=tgt)
+        # the next block's ids are written over this block's (each position is read first)
         if args.loop_sync:
-            k_dev[i] = dfl.dflare_accept(h, ids, draft, tgt, hid, nxt, em)
+            k_dev[i] = dfl.dflare_accept(h, ids, draft, tgt, hid, ids, em)
         else:
-            dfl.dflare_accept_async(h, ids, draft, tgt, hid, nxt, em, k_dev[i:i + 1])
-        ids.copy_(nxt)
+            dfl.dflare_accept_async(h, ids, draft, tgt, hid, ids, em, k_dev[i:i + 1])
 
     for i in range(args.warmup):
         it(i)

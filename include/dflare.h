@@ -174,7 +174,7 @@ int dflare_fuse_append(dflare_handle* h, const void* target_hidden, int32_t n_ne
  *                  position b (given x_t and candidates 1..b).
  *   target_hidden  DEVICE bf16 [S, B, H]: the target's hidden rows at the B positions.
  *   next_ids       DEVICE int32 [B], out: the next block -- the bonus token, then
- *                  block_ids[1..B-1].
+ *                  block_ids[1..B-1].  May be block_ids itself (updated in place).
  *   emitted        DEVICE int32 [B], out: the k accepted candidates, the bonus token,
  *                  then -1 (k + 1 tokens: what the target alone would emit greedily).
  *   accepted       HOST int32 out, or NULL: k.
@@ -220,11 +220,12 @@ int dflare_accept_async(dflare_handle* h, const int32_t* block_ids, const int32_
  *                  candidate (the B-1 candidates are 1..B-1).
  * Block row b sits at position L + b.  The context cache is not modified, so the
  * call can be repeated.  An empty context (L = 0) is allowed.
- * By default the whole pass is one cooperative launch of one work-group per CU
- * whose phases are separated by grid barriers (see DFLARE_OPT_PERSISTENT).  If a
- * grid barrier of an earlier call timed out (the work-groups were not all
- * resident), this call returns DFLARE_ERR_HIP without enqueuing work and the
- * handle switches to one launch per phase.
+ * By default the whole pass is one launch of one work-group per CU whose phases
+ * are separated by grid barriers (see DFLARE_OPT_PERSISTENT); the barriers need
+ * every work-group resident at once (DFLARE_OPT_COOPERATIVE).  If a grid barrier
+ * of an earlier call timed out (the work-groups were not all resident within
+ * 0.25 s), this call returns DFLARE_ERR_HIP without enqueuing work and the handle
+ * switches to one launch per phase.
  */
 int dflare_draft_block(dflare_handle* h, const int32_t* block_ids, int32_t* draft_tokens);
 
@@ -390,10 +391,19 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches);
 
 /*
  * dflare_set_option -- execution options of a handle (they do not change results):
- *   DFLARE_OPT_PERSISTENT  1 (default): a draft_block is one cooperative launch whose
- *                          phases wait at grid barriers; 0: one launch per phase.
- *                          1 is refused (UNSUPPORTED) when the device cannot keep one
- *                          work-group per CU resident.
+ *   DFLARE_OPT_PERSISTENT  1 (default): a draft_block is one launch whose phases wait
+ *                          at grid barriers; 0: one launch per phase.  1 is refused
+ *                          (UNSUPPORTED) when the device cannot keep one work-group per
+ *                          CU resident.
+ *   DFLARE_OPT_COOPERATIVE 0 (default): the persistent launch is a plain launch of one
+ *                          work-group per CU (each takes a whole CU's LDS).  The stream's
+ *                          earlier work has ended when it starts, so all work-groups are
+ *                          placed at once unless kernels of other streams or processes
+ *                          hold CUs; those delay the late work-groups until they end, and
+ *                          past 0.25 s at a barrier the call fails as described under
+ *                          dflare_draft_block.  1: a cooperative launch, for which the
+ *                          runtime guarantees co-residency, at about 13 us more per call
+ *                          (it is ordered against the device's other queues).
  *   DFLARE_OPT_TRACE       1: record per-work-group phase start times (DFLARE_DBG_TRACE).
  *   DFLARE_OPT_CAPTURE_PERSISTENT
  *                          1: debug capture keeps the persistent launch: the draft-block
@@ -402,7 +412,7 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches);
  *                          configuration that is timed; 0 (default): debug capture runs
  *                          one launch per phase.
  */
-enum { DFLARE_OPT_PERSISTENT = 1, DFLARE_OPT_TRACE = 2, DFLARE_OPT_CAPTURE_PERSISTENT = 3 };
+enum { DFLARE_OPT_PERSISTENT = 1, DFLARE_OPT_TRACE = 2, DFLARE_OPT_CAPTURE_PERSISTENT = 3, DFLARE_OPT_COOPERATIVE = 4 };
 int dflare_set_option(dflare_handle* h, int option, int value);
 
 /*

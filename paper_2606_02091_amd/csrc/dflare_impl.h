@@ -191,9 +191,10 @@ void launch_fused_rows(hipStream_t s, const u32x4* ua_hi, const u32x4* ua_lo, co
                        int H, int D, int n_max, int mt_max, float eps, float* out);
 bool kvt_shape_supported(int nt_per_block, int waves);
 void launch_kvt(hipStream_t s, int nt_per_block, int waves, const KvtArgs& a, int layers, int mtiles);
-// Phases [p0, p1) of a draft block on `blocks` work-groups of kThreads threads.  With
-// cooperative = true the work-groups are guaranteed co-resident and wait at grid barriers
-// between phases; otherwise p1 must be p0 + 1.
+// Phases [p0, p1) of a draft block on `blocks` work-groups of kThreads threads, which wait at
+// grid barriers between phases (p1 > p0 + 1 needs all of them resident: one per CU, placed
+// at once when no other stream holds CUs).  cooperative = true asks the runtime to
+// guarantee that co-residency.
 hipError_t launch_draft(hipStream_t s, const DraftArgs* a_dev, const DraftCall& c, int hd, int blocks, int p0,
                         int p1, bool cooperative);
 int draft_blocks_per_cu(int hd);

@@ -4,8 +4,8 @@
 // per-draft-layer context cache of every sequence slot (K as [n_kv, Lcap, hd], V
 // transposed as [n_kv, hd, Lcap], fp16), a rotary table, and the activation buffers of
 // one draft block and of one batched draft step.  fuse_append enqueues two kernels (fusion,
-// context K/V projection); draft_block enqueues one persistent cooperative kernel (or,
-// on request, the same kernel once per phase).  Values that change between calls (L,
+// context K/V projection); draft_block enqueues one persistent kernel (or, on request,
+// the same kernel once per phase).  Values that change between calls (L,
 // n_new, positions, the block ids pointer) travel as kernel arguments.
 #include <math.h>
 #include <stdio.h>
@@ -87,6 +87,7 @@ struct dflare_handle {
   int phases = 0;
   bool persistent = true;
   bool coop_ok = false;    // the device keeps one work-group per CU resident
+  bool coop_launch = false;  // DFLARE_OPT_COOPERATIVE: the persistent kernel through the cooperative launch
   GemmPlan plan[PH_COUNT];
   int attn_nch = 1;
   int attn_chunk = 128;
@@ -738,7 +739,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
                      (h->prof_kind >= DFLARE_K_QKV && h->prof_kind <= DFLARE_K_LM_HEAD);
   prof_mark(h, DFLARE_K_DRAFT, true);
   if (!split) {
-    HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, h->blocks, 0, P, true));
+    HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, h->blocks, 0, P, h->coop_launch));
     // a grid barrier before every phase but the first and the combine phases
     h->bar_epoch += (unsigned)(P - 1 - c.n_draft_layers);
   } else {
@@ -1490,6 +1491,9 @@ int dflare_set_option(dflare_handle* h, int option, int value) {
       return DFLARE_OK;
     case DFLARE_OPT_CAPTURE_PERSISTENT:
       h->capture_persistent = value != 0;
+      return DFLARE_OK;
+    case DFLARE_OPT_COOPERATIVE:
+      h->coop_launch = value != 0;
       return DFLARE_OK;
     default: return fail(h, DFLARE_ERR_INVALID_ARG, "unknown option");
   }

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "lib
 
 OK, ERR_INVALID_ARG, ERR_OUT_OF_MEMORY, ERR_CONTEXT_FULL, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 DBG_FUSED, DBG_KCACHE, DBG_VCACHE, DBG_HIDDEN, DBG_LOGITS, DBG_ALPHA, DBG_TRACE, DBG_BLOGITS = range(8)
-OPT_PERSISTENT, OPT_TRACE, OPT_CAPTURE_PERSISTENT = 1, 2, 3
+OPT_PERSISTENT, OPT_TRACE, OPT_CAPTURE_PERSISTENT, OPT_COOPERATIVE = 1, 2, 3, 4
 
 EXPORTED = (
     "dflare_init", "dflare_fuse_append", "dflare_draft_block", "dflare_draft_block_pos",

@@ -103,7 +103,8 @@ def test_async_accept_matches_sync(case, variant):
     """dflare_accept_async keeps the context length on the device.  A loop of draft_block,
     a target built on the device and accept_async, enqueued with no host wait, must give the
     same draft tokens, k, emitted tokens and next blocks, bit for bit, as the same loop with
-    dflare_accept (pinned to the oracle above), and the same length and caches after it.
+    dflare_accept (pinned to the oracle above), and the same length and caches after it.  The
+    async loop passes block_ids as next_ids (updated in place), the sync loop a new buffer.
     max_context is tight, so the host's upper bound on the length runs out and the call
     reads the length back several times."""
     cfg, L, mode = TP.CASES[case]
@@ -136,7 +137,8 @@ def test_async_accept_matches_sync(case, variant):
             shifted = torch.roll(draft, -1)
             tgt = torch.where(pos < kw[i], shifted, (shifted + 1) % V).to(torch.int32)
             nxt = torch.empty(B, dtype=torch.int32, device="cuda")
-            if use_async:
+            if use_async:  # the next block's ids written over this block's
+                nxt = ids
                 dfl.dflare_accept_async(model.h, ids, draft, tgt, hids[i], nxt, out["em"][i], ks[i:i + 1])
             else:
                 ks[i] = dfl.dflare_accept(model.h, ids, draft, tgt, hids[i], nxt, out["em"][i])

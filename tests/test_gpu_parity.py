@@ -302,6 +302,12 @@ def test_persistent_matches_per_phase(case):
             model.draft_block(ids, out)  # repeated: the block slots are rewritten, the context is not
             side.synchronize()
             persistent = out.cpu().numpy().copy()
+            # the same kernel through the cooperative launch
+            dfl.dflare_set_option(model.h, dfl.OPT_COOPERATIVE, 1)
+            model.draft_block(ids, out)
+            side.synchronize()
+            dfl.dflare_set_option(model.h, dfl.OPT_COOPERATIVE, 0)
+            assert np.array_equal(out.cpu().numpy(), persistent), (case, k)
             # the persistent launch again, writing its own logits and block rows
             dfl.dflare_debug_capture(model.h, True)
             dfl.dflare_set_option(model.h, dfl.OPT_CAPTURE_PERSISTENT, 1)
