@@ -515,18 +515,59 @@ static_assert(kLdsRedBytes + 2048 <= kFailOff && kFailOff + 16 == kStageOff,
               "GEMM scratch, the failure flag and the attention staging area do not overlap");
 
 
-// Epilogue of one finished 16 x 16 output tile nt (lane holds rows quad*4 .. +3 of column
-// col); v already carries the RMSNorm row scale.  ARGMAX leaves the tile's best (logit,
-// id) per row in s_bv / s_bi at slot j.
+// Inputs of a tile's epilogue that do not depend on its sums: the residual rows and the next
+// norm's gain (RESID), the rotary (cos, sin) of the lane's rows (Q and K tiles of QKV).  They
+// are loaded before the tile's sums are complete, so that their latency overlaps the waves'
+// reduction and the wait for the split-K partials.  (The residual rows were last written in
+// an earlier phase, before a grid barrier.)
+struct EpiIn {
+  float x[4];
+  float gn;
+  float2 cs[4];
+};
 template <int EPI>
-__device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, int nt, f32x4 v, int j,
-                                              float* s_bv, int* s_bi) {
+__device__ __forceinline__ EpiIn epilogue_inputs(Args a, Call c, const GemmJob& g, int nt) {
+  EpiIn in{};
+  const int lane = opaque(threadIdx.x) & 63;
+  const int quad = lane >> 4, col = lane & 15;
+  const int M = a->B;
+  if constexpr (EPI == EPI_RESID) {
+    const int k = nt * 16 + col;
+    in.gn = gbl(g.gain)[k];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = quad * 4 + i;
+      in.x[i] = row < M ? ld_coh(a->X + (long)row * a->H + k) : 0.f;
+    }
+  } else if constexpr (EPI == EPI_QKV) {
+    const int hd = a->hd, tph = hd / 16, half = hd / 2;
+    if (nt < (a->n_q + a->n_kv) * tph) {  // Q and K tiles (tph divides the Q tile count)
+      const int L = ctx_len(c);
+      const int m = 8 * (nt % tph) + (col & 7);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = quad * 4 + i;
+        const int pos = row < M ? c->pos[row] + (c->Lp ? L : 0) : 0;
+        const uint64_t csb = gbl(reinterpret_cast<const uint64_t*>(a->rope))[(long)pos * half + m];
+        in.cs[i] = make_float2(__uint_as_float((uint32_t)csb), __uint_as_float((uint32_t)(csb >> 32)));
+      }
+    }
+  }
+  return in;
+}
+
+// Epilogue of one finished 16 x 16 output tile nt (lane holds rows quad*4 .. +3 of column
+// col); v already carries the RMSNorm row scale, `in` the tile's epilogue_inputs.  ARGMAX
+// leaves the tile's best (logit, id) per row in s_bv / s_bi at slot j.
+template <int EPI>
+__device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, int nt, f32x4 v, const EpiIn& in,
+                                              int j, float* s_bv, int* s_bi) {
   const int lane = opaque(threadIdx.x) & 63;  // epilogue values are not hoisted above the main loop
   const int quad = lane >> 4, col = lane & 15;
   const int M = a->B;
   if constexpr (EPI == EPI_RESID) {
     const int k = nt * 16 + col;
-    const float gn = gbl(g.gain)[k];
+    const float gn = in.gn;
     float sq[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -534,7 +575,7 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
       float x = 0.f;
       if (row < M) {
         float* p = a->X + (long)row * a->H + k;
-        x = ld_coh(p) + v[i];
+        x = in.x[i] + v[i];
         st_wt(p, x);
         if (g.hid_out) st_wt(g.hid_out + (long)row * a->H + k, x);
       }
@@ -584,15 +625,13 @@ __device__ __forceinline__ void gemm_epilogue(Args a, Call c, const GemmJob& g, 
     for (int i = 0; i < 4; ++i) {
       const int row = quad * 4 + i;
       const bool valid = row < M;
-      const int pos = valid ? c->pos[row] + (c->Lp ? L : 0) : 0;
       const int slot = L + row;
       const float x = v[i];
       const float partner = __shfl_xor(x, 8);
       if (region < 2) {
         const int m = 8 * jj + (col & 7);
         const int dim = (col < 8) ? m : half + m;
-        const uint64_t csb = gbl(reinterpret_cast<const uint64_t*>(a->rope))[(long)pos * half + m];
-        const float2 cs = make_float2(__uint_as_float((uint32_t)csb), __uint_as_float((uint32_t)(csb >> 32)));
+        const float2 cs = in.cs[i];
         const float y = (col < 8) ? (x * cs.x - partner * cs.y) : (x * cs.x + partner * cs.y);
         if (valid) {
           if (region == 0) {
@@ -846,8 +885,11 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
   for (int j = 0; j < TN; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   f32x4 own = f32x4{0.f, 0.f, 0.f, 0.f};  // split K: the reducer's own partial of tile `wave`
+  EpiIn ein{};                             // epilogue inputs of the tile this wave finishes
   // end of chunk ch: the waves' partial sums meet in LDS; wave j finishes tile j
   auto chunk_end = [&](int ch) {
+    if (wave < min(TN, T - ch * TN) && (kg == 1 || geo.kgi == 0))
+      ein = epilogue_inputs<EPI>(a, c, g, t0 + ch * TN + wave);
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       red[(wave * TN + j) * 64 + lane] = acc[j];
@@ -886,7 +928,7 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
         if (geo.kgi == 0) own = __builtin_bit_cast(f32x4, t);
         else st_wt16(reinterpret_cast<f32x4*>(g.part) + (((long)b * kTNMax + wave) * 64 + lane), t);
       } else {
-        gemm_epilogue<EPI>(a, c, g, t0 + ch * TN + wave, v, wave, s_bv, s_bi);
+        gemm_epilogue<EPI>(a, c, g, t0 + ch * TN + wave, v, ein, wave, s_bv, s_bi);
       }
     }
     if constexpr (EPI == EPI_ARGMAX) {
@@ -976,7 +1018,7 @@ __device__ __forceinline__ void gemm_phase(Args a, Call c, const GemmJob& g, int
 #pragma unroll
     for (int q = 1; q < kMaxSplit; ++q)
       if (q < kg) v += pq[q];
-    gemm_epilogue<EPI>(a, c, g, t0 + wave, v, wave, s_bv, s_bi);
+    gemm_epilogue<EPI>(a, c, g, t0 + wave, v, ein, wave, s_bv, s_bi);
   }
 
   if constexpr (EPI == EPI_ARGMAX) {
