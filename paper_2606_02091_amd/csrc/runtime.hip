@@ -16,7 +16,10 @@
 #include <mutex>
 #include <string>
 #include <unordered_set>
+#include <utility>
 #include <vector>
+
+#include <hip/hip_ext.h>
 
 #include "batched.h"
 #include "dflare.h"
@@ -161,6 +164,7 @@ struct dflare_handle {
   float* dbg_blogits = nullptr;
   int dbg_blogits_rows = 0;
   std::vector<void*> allocs;
+  std::vector<std::pair<void*, size_t>> uc_blocks;  // uncached counter blocks (returned to the pool)
   std::string err;
 };
 
@@ -207,9 +211,49 @@ int dev_zalloc(dflare_handle* h, T** p, size_t bytes) {
   return DFLARE_OK;
 }
 
+// Uncached device memory for the arrival counters that work-groups poll (grid barriers,
+// attention and LM-head counts): a poll of uncached memory returns sooner while the CU
+// streams weights (about 1 us per barrier under load; 10 us per Qwen3-8B-shaped draft
+// block).  A block that a kernel has read is never handed back to the driver (freeing
+// uncached memory has been followed by wrong contents in later allocations on this
+// platform): released blocks stay in a per-device pool for the next handle until the process
+// ends.
+std::mutex g_uc_mu;
+std::vector<std::pair<int, std::pair<void*, size_t>>> g_uc_pool;  // (device, (block, bytes))
+
+template <typename T>
+int uc_zalloc(dflare_handle* h, T** p, size_t bytes) {
+  void* q = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_uc_mu);
+    for (size_t i = 0; i < g_uc_pool.size(); ++i)
+      if (g_uc_pool[i].first == h->device && g_uc_pool[i].second.second == bytes) {
+        q = g_uc_pool[i].second.first;
+        g_uc_pool.erase(g_uc_pool.begin() + (long)i);
+        break;
+      }
+  }
+  if (!q) {
+    hipError_t e = hipExtMallocWithFlags(&q, bytes, hipDeviceMallocUncached);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(h, DFLARE_ERR_OUT_OF_MEMORY, "uncached allocation of " + std::to_string(bytes) + " bytes failed");
+    }
+  }
+  h->uc_blocks.push_back({q, bytes});
+  *p = static_cast<T*>(q);
+  HIP_OR_FAIL(h, hipMemsetAsync(q, 0, bytes, h->stream));
+  return DFLARE_OK;
+}
+
 void free_all(dflare_handle* h) {
   for (void* p : h->allocs) (void)hipFree(p);
   h->allocs.clear();
+  {
+    std::lock_guard<std::mutex> lk(g_uc_mu);
+    for (const auto& b : h->uc_blocks) g_uc_pool.push_back({h->device, b});
+  }
+  h->uc_blocks.clear();
   if (h->err_host) (void)hipHostFree(h->err_host);
   h->err_host = nullptr;
   for (hipEvent_t e : h->prof_ev) (void)hipEventDestroy(e);
@@ -534,7 +578,7 @@ int build(dflare_handle* h, const dflare_weights* w) {
   TRY(dev_zalloc(h, &h->pidx, (size_t)h->blocks * kStatsPad * 4));
   // split-K partial tiles: one area per GEMM phase kind (tagged per use, see gemm_phase)
   TRY(dev_zalloc(h, &h->part, (size_t)kSplitKinds * h->blocks * kTNMax * 1024));
-  TRY(dev_zalloc(h, &h->sync, kSyncBytes));
+  TRY(uc_zalloc(h, &h->sync, kSyncBytes));
   TRY(dev_zalloc(h, &h->Ldev, 4 * sizeof(int32_t)));
   h->kdev = h->Ldev + 2;
 
