@@ -28,6 +28,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "draft blocks/sec (B=16, Qwen3-8B shape, batch 1) + % HBM roofline"
+SHAPE_NAMES = {"qwen3_8b": "Qwen3-8B", "qwen3_4b": "Qwen3-4B", "gpt_oss_20b": "GPT-OSS-20B"}
+
+
+def shape_name(cfg):
+    return SHAPE_NAMES.get(cfg.name, cfg.name)
 HBM_PEAK_GBS = 8000.0
 
 
@@ -71,7 +76,10 @@ def parse():
                     help="write profiles/hbm_counters_<config>.json from two rocprofv3 --pmc output folders")
     ap.add_argument("--counter-scale", default="2.0,1.0",
                     help="bytes per counted FETCH_SIZE and WRITE_SIZE byte (from --calibrate-copy)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.profile_steps < 1:
+        ap.error("--profile-steps must be at least 1: the per-kernel table and the roofline are timed over them")
+    return args
 
 
 def calibrate_copy():
@@ -345,7 +353,7 @@ def main():
     step_bytes = cfg.block_bytes(L) + cfg.append_bytes(n_mean) + (H * S * H * 2 if dflash else 0)
     step_gbs = step_bytes / (ms * 1e-3) / 1e9
     result = {
-        "metric": METRIC,
+        "metric": METRIC.replace("Qwen3-8B", shape_name(cfg)),
         "value": round(1000.0 / ms, 2),
         "unit": "blocks/s",
         "n_gpus": 1,
@@ -450,7 +458,7 @@ def bench_loop(args):
     print(f"[bench] loop: {args.steps} iterations, {ms:.4f} ms each, {tokens / sec:.0f} tokens/s",
           file=sys.stderr, flush=True)
     print(json.dumps({
-        "metric": "draft-then-verify iterations/sec (draft side; B=16, Qwen3-8B shape, batch 1)",
+        "metric": f"draft-then-verify iterations/sec (draft side; B=16, {shape_name(cfg)} shape, batch 1)",
         "value": round(1000.0 / ms, 2), "unit": "iterations/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
