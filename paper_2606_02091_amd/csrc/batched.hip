@@ -802,6 +802,9 @@ __global__ __launch_bounds__(256, 2) void k_battn(BAttnArgs a, BRows rows) {
           const uint32_t lo = (2 * e < nv) ? 0xFFFFu : 0u, hi = (2 * e + 1 < nv) ? 0xFFFF0000u : 0u;
           z[e] = v[e] & (lo | hi);
         }
+        // rows with bit 3 of d set hold the piece's two 8-byte halves swapped, so that the 16
+        // lanes of one read (16 dim rows, one half each) reach 16 different bank pairs
+        if (d & 8) z = u32x4{z[2], z[3], z[0], z[1]};
         st[buf][KP + d * VC + (c ^ (d & 7))] = z;
       }
     }
@@ -860,9 +863,13 @@ __global__ __launch_bounds__(256, 2) void k_battn(BAttnArgs a, BRows rows) {
           lacc = mfma_h(kv, ql[t][ks], lacc);
         }
         sc[kt] = hacc + lacc;
+      }
+      if (k0 + KB > kend) {  // the block reaches past the item's last key
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (k0 + kt * 16 + quad * 4 + e >= kend) sc[kt][e] = -INFINITY;
+        for (int kt = 0; kt < KB / 16; ++kt)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (k0 + kt * 16 + quad * 4 + e >= kend) sc[kt][e] = -INFINITY;
       }
       float mb = -INFINITY;
 #pragma unroll
@@ -871,35 +878,42 @@ __global__ __launch_bounds__(256, 2) void k_battn(BAttnArgs a, BRows rows) {
         for (int e = 0; e < 4; ++e) mb = fmaxf(mb, sc[kt][e]);
       mb = fmaxf(mb, __shfl_xor(mb, 16));
       mb = fmaxf(mb, __shfl_xor(mb, 32));
-      const float mn = fmaxf(m_run[t], mb);
-      const float scale = exp2f(m_run[t] - mn);
+      // the running maximum moves only when the block's maximum exceeds it by more than 8 (so
+      // the unnormalised probabilities stay below 2^8); the rescale of the output and the sum
+      // then runs for the whole wave, with factor 1 on rows that did not move
+      const bool grow = mb > m_run[t] + 8.f;
+      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+        const float mn = grow ? mb : m_run[t];
+        const float scale = __builtin_amdgcn_exp2f(m_run[t] - mn);
+        l_run[t] *= scale;
+#pragma unroll
+        for (int dt = 0; dt < HD / 16; ++dt) o[t][dt] *= scale;
+        m_run[t] = mn;
+      }
       float ls = 0.f;
 #pragma unroll
       for (int kt = 0; kt < KB / 16; ++kt)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p = exp2f(sc[kt][e] - mn);
+          const float p = __builtin_amdgcn_exp2f(sc[kt][e] - m_run[t]);
           sc[kt][e] = p;
           ls += p;
         }
       ls += __shfl_xor(ls, 16);
       ls += __shfl_xor(ls, 32);
-      l_run[t] = l_run[t] * scale + ls;
-      m_run[t] = mn;
-#pragma unroll
-      for (int dt = 0; dt < HD / 16; ++dt) o[t][dt] *= scale;
+      l_run[t] += ls;
       // O^T += V^T P^T, 32 keys per step
 #pragma unroll
       for (int kk = 0; kk < KB / 32; ++kk) {
         float pv[8] = {sc[2 * kk][0], sc[2 * kk][1], sc[2 * kk][2], sc[2 * kk][3],
                        sc[2 * kk + 1][0], sc[2 * kk + 1][1], sc[2 * kk + 1][2], sc[2 * kk + 1][3]};
         u32x4 ph, pl;
-        split_pack8_h(pv, ph, pl);
+        split_pack8_hz(pv, ph, pl);
 #pragma unroll
         for (int dt = 0; dt < HD / 16; ++dt) {
           const int d = dt * 16 + q;
           const int p0 = (4 * kk + vx) ^ (d & 7), p1 = (4 * kk + 2 + vx) ^ (d & 7);
-          const char* vrow = lds + (KP + d * VC) * 16 + (quad & 1) * 8;
+          const char* vrow = lds + (KP + d * VC) * 16 + (((quad & 1) ^ ((d >> 3) & 1)) * 8);
           const u32x2 x0 = *reinterpret_cast<const u32x2*>(vrow + p0 * 16);
           const u32x2 x1 = *reinterpret_cast<const u32x2*>(vrow + p1 * 16);
           const u32x4 vv = {x0[0], x0[1], x1[0], x1[1]};

@@ -52,6 +52,19 @@ __device__ __forceinline__ uint16_t f2h(float x) {
 }
 __device__ __forceinline__ float h2f(uint32_t b) { return (float)__builtin_bit_cast(_Float16, (uint16_t)b); }
 
+// fp16 hi/lo split of 8 values inside the fp16 range (attention probabilities): hi rounded
+// toward zero by the packed two-value conversion, lo = x - hi (exact in fp32) converted the same
+// way; hi + lo keeps about 21 significant bits
+__device__ __forceinline__ void split_pack8_hz(const float* v, u32x4& hi, u32x4& lo) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const auto h = __builtin_amdgcn_cvt_pkrtz(v[2 * e], v[2 * e + 1]);
+    const auto l = __builtin_amdgcn_cvt_pkrtz(v[2 * e] - (float)h[0], v[2 * e + 1] - (float)h[1]);
+    hi[e] = __builtin_bit_cast(uint32_t, h);
+    lo[e] = __builtin_bit_cast(uint32_t, l);
+  }
+}
+
 // fp16 hi/lo split of 8 floats (x ~= hi + lo with about 22 significant bits)
 __device__ __forceinline__ void split_pack8_h(const float* v, u32x4& hi, u32x4& lo) {
 #pragma unroll
