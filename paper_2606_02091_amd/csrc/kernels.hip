@@ -1284,13 +1284,18 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
       m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
 #pragma unroll
-      for (int kt = 0; kt < 2 * NKB; ++kt)
+      for (int kk = 0; kk < NKB; ++kk) {
+        if (kk >= kb0 && kk < kb1) {  // the other blocks' probabilities are never used
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float p = exp2f(sc[kt][i] - m);
-          sc[kt][i] = p;
-          l += p;
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float p = __builtin_amdgcn_exp2f(sc[2 * kk + h][i] - m);
+              sc[2 * kk + h][i] = p;
+              l += p;
+            }
         }
+      }
       l += __shfl_xor(l, 16);
       l += __shfl_xor(l, 32);
       // O^T = V^T P^T over the wave's blocks
@@ -1300,7 +1305,7 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
           float pv[8] = {sc[2 * kk][0], sc[2 * kk][1], sc[2 * kk][2], sc[2 * kk][3],
                          sc[2 * kk + 1][0], sc[2 * kk + 1][1], sc[2 * kk + 1][2], sc[2 * kk + 1][3]};
           u32x4 ph, pl;
-          split_pack8_h(pv, ph, pl);
+          split_pack8_hz(pv, ph, pl);
           // keys kk*32 + 8*qd .. + 7: the 16-byte V^T piece kk*4 + qd of row dt*16 + q
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) {
@@ -1325,7 +1330,7 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
           const int wk = t + k * G;
           const float2 mlk = sML[wk * 16 + q];
           const float M = fmaxf(m, mlk.x);
-          const float f0 = exp2f(m - M), f1 = exp2f(mlk.x - M);  // 0 for a part without keys
+          const float f0 = __builtin_amdgcn_exp2f(m - M), f1 = __builtin_amdgcn_exp2f(mlk.x - M);  // 0 for a part without keys
           l = f0 * l + f1 * mlk.y;
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) o[dt] = f0 * o[dt] + f1 * sO[(wk * DT + dt) * 64 + lane];
@@ -1443,14 +1448,14 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, Faile
       float Mb = M;
 #pragma unroll
       for (int k = 0; k < CB; ++k) Mb = fmaxf(Mb, mc[k].x);
-      const float f = exp2f(M - Mb);  // rescale of the run so far (0 when it is empty)
+      const float f = __builtin_amdgcn_exp2f(M - Mb);  // rescale of the run so far (0 when it is empty)
       den *= f;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) num[e] *= f;
 #pragma unroll
       for (int k = 0; k < CB; ++k) {
         if (c0 + k < ce) {
-          const float wgt = exp2f(mc[k].x - Mb) * mc[k].y;  // a chunk's sum times its normalised output
+          const float wgt = __builtin_amdgcn_exp2f(mc[k].x - Mb) * mc[k].y;  // a chunk's sum times its normalised output
           den += wgt;
 #pragma unroll
           for (int e = 0; e < DPL; ++e) num[e] += wgt * ov[k][e];
@@ -1475,7 +1480,7 @@ __device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, Faile
         for (int e = 0; e < DPL; ++e) nt[e] = 0.f;
         for (int k = 0; k < S; ++k) {
           const float2 md = sMD[w + k];
-          const float f = exp2f(md.x - Mt);
+          const float f = __builtin_amdgcn_exp2f(md.x - Mt);
           dt += f * md.y;
 #pragma unroll
           for (int e = 0; e < DPL; ++e) nt[e] += f * sN[((w + k) * 64 + lane) * DPL + e];
