@@ -11,7 +11,7 @@ constexpr int kBWaves = 4;               // GEMM work-group: 4 waves
 constexpr int kBWavesPerSimd = 2;        // GEMM work-groups resident per CU (waves per SIMD)
 constexpr int kBPrefetch = 3;            // k-tiles of GEMM operand loads in flight per wave
 constexpr int kBM = 8;                   // m-tiles per work-group (128 rows); every wave covers all of them
-constexpr int kBNW = 4;                  // n-tiles per wave (64 columns)
+constexpr int kBNW = 4;                  // n-tiles per wave (64 columns); 3 for some shapes (BGemmArgs::nw)
 constexpr int kBN = kBWaves * kBNW;      // n-tiles per work-group (256 columns)
 constexpr int kMaxSeq = 64;              // sequences in one batched call
 constexpr int kBKeys = 512;              // keys (context and block) per batched attention work item
@@ -43,6 +43,7 @@ struct BGemmArgs {
   const u32x4* W;
   long w_layer;
   int Nt, Kt, Mt, M, kg, layers;
+  int nw;              // n-tiles per wave: kBNW, or 3 where that fills the CUs better
   const u32x4* zero;   // one zero fragment
   float* part;         // partial tiles [tiles][kg][kBPartFloats]
   unsigned* cnt;       // arrival counters [tiles], 32 words apart, zero between launches
@@ -89,7 +90,7 @@ struct BAttnArgs {
   float2* ML;   // [items][Rpad] (max, sum), log2 domain
 };
 
-int bgemm_groups(int Nt, int Mt);  // output tiles of one layer
+int bgemm_groups(int Nt, int Mt, int nw = kBNW);  // output tiles of one layer
 // n 16-byte slots of packed bf16 weight tiles -> fp16 (same layout)
 void launch_tiles_to_f16(hipStream_t s, u32x4* dst, const u32x4* src, long n);
 void launch_bgemm(hipStream_t s, int epi, const BGemmArgs& g, const BRows& rows);

@@ -95,11 +95,11 @@ __device__ __forceinline__ void row_best_to_lds(float bv[4], int bi[4], int col,
 }
 
 // ------------------------------------------------------------------------------------------
-// GEMM.  Work-group: 4 waves; output tile 128 rows x 256 columns, wave w owning columns
-// 64 w .. 64 w + 63 for all 128 rows (8 x 4 MFMA tiles, 128 accumulators per lane); two
-// work-groups share a CU (two waves per SIMD), so one wave's MFMAs run while the other
-// waits for LDS or the barrier.  Per k-tile (32 deep) a wave reads its 4 weight
-// fragments straight from memory (each a coalesced 1 KiB load of its own columns, used
+// GEMM.  Work-group: 4 waves; output tile 128 rows x 64 NW columns (NW = 4, or 3 where the
+// narrower tiles fill the CUs better), wave w owning NW 16-column tiles for all 128 rows
+// (8 x NW MFMA tiles, 32 NW accumulators per lane); two work-groups share a CU (two waves
+// per SIMD), so one wave's MFMAs run while the other waits for LDS or the barrier.  Per
+// k-tile (32 deep) a wave reads its NW weight fragments straight from memory (each a coalesced 1 KiB load of its own columns, used
 // directly as MFMA operands; the work-groups of the other m-groups of the same columns
 // run on the same XCD and meet in its L2) and loads 2 of the 8 A fragments, which go
 // through a 2-slot LDS ring so that every wave reads all 8 with one barrier per k-tile.
@@ -107,7 +107,7 @@ __device__ __forceinline__ void row_best_to_lds(float bv[4], int bi[4], int col,
 // skipped (past the last k-tile they repeat it), so the compiler can wait for exactly the
 // loads a step needs.
 // ------------------------------------------------------------------------------------------
-template <int EPI>
+template <int EPI, int NW>
 __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerSimd, kBWavesPerSimd))) void k_bgemm(
     BGemmArgs g, BRows rows) {
   constexpr int P = kBPrefetch;
@@ -124,7 +124,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
   // work-group -> (layer, K part, n-group, m-group).  Work-groups go to the 8 XCDs in
   // turn (id % 8); the m-groups of one (layer, K part, n-group) read the same weight
   // tiles, so they get consecutive ids on one XCD.
-  const int Ng = (g.Nt + kBN - 1) / kBN, Mg = (g.Mt + kBM - 1) / kBM;
+  const int Ng = (g.Nt + kBWaves * NW - 1) / (kBWaves * NW), Mg = (g.Mt + kBM - 1) / kBM;
   const int nb = Ng * Mg * g.kg * g.layers;
   const int bid = blockIdx.x;
   const int t = (nb % 8 == 0) ? (bid % 8) * (nb / 8) + bid / 8 : bid;
@@ -135,10 +135,10 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
 
   const u32x4* A = g.A + layer * g.a_layer;
   const u32x4* W = g.W + layer * g.w_layer;
-  const int nt0 = ng * kBN + w * kBNW;
-  const u32x4* wp[kBNW];
+  const int nt0 = ng * (kBWaves * NW) + w * NW;
+  const u32x4* wp[NW];
 #pragma unroll
-  for (int n = 0; n < kBNW; ++n) wp[n] = W + ((long)min(nt0 + n, g.Nt - 1) * g.Kt + kb) * 64 + lane;
+  for (int n = 0; n < NW; ++n) wp[n] = W + ((long)min(nt0 + n, g.Nt - 1) * g.Kt + kb) * 64 + lane;
   const u32x4* ap[2];
   int astep[2];
 #pragma unroll
@@ -150,20 +150,20 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
   }
   const int klast = max(nk - 1, 0);
 
-  f32x4 acc[kBM][kBNW];
+  f32x4 acc[kBM][NW];
 #pragma unroll
   for (int m = 0; m < kBM; ++m)
 #pragma unroll
-    for (int n = 0; n < kBNW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int n = 0; n < NW; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   auto kidx = [&](int i) -> long { return min(i, klast); };
   if (nk > 0) {
-    u32x4 wr[P][kBNW], ar[P][2];
+    u32x4 wr[P][NW], ar[P][2];
 #pragma unroll
     for (int j = 0; j < P; ++j) {
       const long kt = kidx(j);
 #pragma unroll
-      for (int n = 0; n < kBNW; ++n) wr[j][n] = wp[n][kt * 64];
+      for (int n = 0; n < NW; ++n) wr[j][n] = wp[n][kt * 64];
       ar[j][0] = ap[0][kt * astep[0]];
       ar[j][1] = ap[1][kt * astep[1]];
     }
@@ -181,12 +181,12 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
           for (int m = 0; m < kBM; ++m) {
             const u32x4 a = slot[m * 64 + lane];
 #pragma unroll
-            for (int n = 0; n < kBNW; ++n) acc[m][n] = mfma_h(a, wr[j][n], acc[m][n]);
+            for (int n = 0; n < NW; ++n) acc[m][n] = mfma_h(a, wr[j][n], acc[m][n]);
           }
         }
         const long kt = kidx(tk + P);
 #pragma unroll
-        for (int n = 0; n < kBNW; ++n) wr[j][n] = wp[n][kt * 64];
+        for (int n = 0; n < NW; ++n) wr[j][n] = wp[n][kt * 64];
         ar[j][0] = ap[0][kt * astep[0]];
         ar[j][1] = ap[1][kt * astep[1]];
       }
@@ -197,12 +197,12 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
     // split K: leave this part's tile, then the last part to arrive sums all parts in K order
     // (each 1 KiB block: elements 0-1 of the 64 lanes, then elements 2-3, so that every
     // 8-byte store or load instruction covers 512 contiguous bytes)
-    float* mine = g.part + (((long)tile * g.kg + kz) * kBWaves + w) * (kBM * kBNW * 256);
+    float* mine = g.part + (((long)tile * g.kg + kz) * kBWaves + w) * (kBM * NW * 256);
 #pragma unroll
     for (int m = 0; m < kBM; ++m)
 #pragma unroll
-      for (int n = 0; n < kBNW; ++n) {
-        float* blk = mine + (m * kBNW + n) * 256;
+      for (int n = 0; n < NW; ++n) {
+        float* blk = mine + (m * NW + n) * 256;
         const u32x4 v = __builtin_bit_cast(u32x4, acc[m][n]);
         st_wt8(blk + lane * 2, (uint64_t)v[0] | ((uint64_t)v[1] << 32));
         st_wt8(blk + 128 + lane * 2, (uint64_t)v[2] | ((uint64_t)v[3] << 32));
@@ -220,38 +220,38 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
     // together, then added
 #pragma unroll
     for (int m0 = 0; m0 < kBM; m0 += 2) {
-      f32x4 sm[2][kBNW];
+      f32x4 sm[2][NW];
 #pragma unroll
       for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-        for (int n = 0; n < kBNW; ++n) sm[mi][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int n = 0; n < NW; ++n) sm[mi][n] = f32x4{0.f, 0.f, 0.f, 0.f};
       for (int z = 0; z < g.kg; ++z) {
         if (z == kz) {
 #pragma unroll
           for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-            for (int n = 0; n < kBNW; ++n) sm[mi][n] += acc[m0 + mi][n];
+            for (int n = 0; n < NW; ++n) sm[mi][n] += acc[m0 + mi][n];
           continue;
         }
-        const float* zb = g.part + (((long)tile * g.kg + z) * kBWaves + w) * (kBM * kBNW * 256);
-        float2 lo[2][kBNW], hi[2][kBNW];
+        const float* zb = g.part + (((long)tile * g.kg + z) * kBWaves + w) * (kBM * NW * 256);
+        float2 lo[2][NW], hi[2][NW];
 #pragma unroll
         for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-          for (int n = 0; n < kBNW; ++n) {
-            const float* blk = zb + ((m0 + mi) * kBNW + n) * 256;
+          for (int n = 0; n < NW; ++n) {
+            const float* blk = zb + ((m0 + mi) * NW + n) * 256;
             lo[mi][n] = ld_coh2(blk + lane * 2);
             hi[mi][n] = ld_coh2(blk + 128 + lane * 2);
           }
 #pragma unroll
         for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-          for (int n = 0; n < kBNW; ++n) sm[mi][n] += f32x4{lo[mi][n].x, lo[mi][n].y, hi[mi][n].x, hi[mi][n].y};
+          for (int n = 0; n < NW; ++n) sm[mi][n] += f32x4{lo[mi][n].x, lo[mi][n].y, hi[mi][n].x, hi[mi][n].y};
       }
 #pragma unroll
       for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-        for (int n = 0; n < kBNW; ++n) acc[m0 + mi][n] = sm[mi][n];
+        for (int n = 0; n < NW; ++n) acc[m0 + mi][n] = sm[mi][n];
     }
   }
 
@@ -270,7 +270,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
     const int kvd = g.kv_tiles * 16;
     const float* kvb = g.bias ? g.bias + (long)(g.layer0 + layer) * 2 * kvd : nullptr;
 #pragma unroll
-    for (int n = 0; n < kBNW; ++n) {
+    for (int n = 0; n < NW; ++n) {
       const int nt = nt0 + n;
       if (nt >= g.Nt) continue;
       int region, tt;  // 0 = Q, 1 = K, 2 = V
@@ -323,7 +323,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
     }
   } else if constexpr (EPI == BEPI_RESID) {
 #pragma unroll
-    for (int n = 0; n < kBNW; ++n) {
+    for (int n = 0; n < NW; ++n) {
       const int nt = nt0 + n;
       if (nt >= g.Nt) continue;
       // every row of the m-tiles, those past M included (padding rows of X, never read),
@@ -343,7 +343,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
   } else if constexpr (EPI == BEPI_SWIGLU) {
     uint32_t* out = reinterpret_cast<uint32_t*>(g.out16);
 #pragma unroll
-    for (int n = 0; n < kBNW; ++n) {
+    for (int n = 0; n < NW; ++n) {
       const int nt = nt0 + n;
 #pragma unroll
       for (int m = 0; m < kBM; ++m)
@@ -361,7 +361,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
   } else if constexpr (EPI == BEPI_BIAS16) {
     uint32_t* out = reinterpret_cast<uint32_t*>(g.out16);
 #pragma unroll
-    for (int n = 0; n < kBNW; ++n) {
+    for (int n = 0; n < NW; ++n) {
       const int nt = nt0 + n;
       const float bcol = (g.bias && nt < g.Nt) ? g.bias[nt * 16 + col] : 0.f;
 #pragma unroll
@@ -388,7 +388,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
           bi[e] = 0x7FFFFFFF;
         }
 #pragma unroll
-        for (int n = 0; n < kBNW; ++n) {
+        for (int n = 0; n < NW; ++n) {
           const int vc = (nt0 + n) * 16 + col;
           const bool ok = vc < g.V;
 #pragma unroll
@@ -425,7 +425,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
       static_for<0, kBM>([&](auto mc) {
         constexpr int m = decltype(mc)::value;
 #pragma unroll
-        for (int n = 0; n < kBNW; ++n) {
+        for (int n = 0; n < NW; ++n) {
           const int vc = (nt0 + n) * 16 + col;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -439,7 +439,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
         // rows 4 q .. 4 q + 3 of one sequence share one Philox call, else one call per row
         const bool grouped = (s_pos[r0] & 3) == 0 && s_pos[r0 + 3] == s_pos[r0] + 3 && s_slot[r0 + 3] == s_slot[r0];
 #pragma unroll 1
-        for (int j = 0; j < kBNW * 4; ++j) {
+        for (int j = 0; j < NW * 4; ++j) {
           const int n = j >> 2, e = j & 3;
           if (e == 0 || !grouped) {
             const int pos = s_pos[r0 + e], slot = s_slot[r0 + e];
@@ -456,7 +456,7 @@ __global__ __launch_bounds__(kBT) __attribute__((amdgpu_waves_per_eu(kBWavesPerS
           bi[e] = 0x7FFFFFFF;
         }
 #pragma unroll
-        for (int n = 0; n < kBNW; ++n) {
+        for (int n = 0; n < NW; ++n) {
           const int vc = (nt0 + n) * 16 + col;
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -987,20 +987,32 @@ __global__ __launch_bounds__(64) void k_bcomb(BAttnArgs a, BRows rows, u32x4* ou
 // ------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------
-int bgemm_groups(int Nt, int Mt) { return ((Nt + kBN - 1) / kBN) * ((Mt + kBM - 1) / kBM); }
+int bgemm_groups(int Nt, int Mt, int nw) {
+  const int bn = kBWaves * nw;
+  return ((Nt + bn - 1) / bn) * ((Mt + kBM - 1) / kBM);
+}
 
 void launch_tiles_to_f16(hipStream_t s, u32x4* dst, const u32x4* src, long n) {
   hipLaunchKernelGGL(k_tiles_to_f16, dim3(2048), dim3(256), 0, s, dst, src, n);
 }
 
 void launch_bgemm(hipStream_t s, int epi, const BGemmArgs& g, const BRows& rows) {
-  const dim3 grid(bgemm_groups(g.Nt, g.Mt) * g.kg * g.layers);
+  const dim3 grid(bgemm_groups(g.Nt, g.Mt, g.nw) * g.kg * g.layers);
   switch (epi) {
-    case BEPI_QKV: hipLaunchKernelGGL(k_bgemm<BEPI_QKV>, grid, dim3(kBT), 0, s, g, rows); break;
-    case BEPI_RESID: hipLaunchKernelGGL(k_bgemm<BEPI_RESID>, grid, dim3(kBT), 0, s, g, rows); break;
-    case BEPI_SWIGLU: hipLaunchKernelGGL(k_bgemm<BEPI_SWIGLU>, grid, dim3(kBT), 0, s, g, rows); break;
-    case BEPI_BIAS16: hipLaunchKernelGGL(k_bgemm<BEPI_BIAS16>, grid, dim3(kBT), 0, s, g, rows); break;
-    default: hipLaunchKernelGGL(k_bgemm<BEPI_ARGMAX>, grid, dim3(kBT), 0, s, g, rows); break;
+    case BEPI_QKV:
+      if (g.nw == 3) hipLaunchKernelGGL((k_bgemm<BEPI_QKV, 3>), grid, dim3(kBT), 0, s, g, rows);
+      else hipLaunchKernelGGL((k_bgemm<BEPI_QKV, kBNW>), grid, dim3(kBT), 0, s, g, rows);
+      break;
+    case BEPI_RESID:
+      if (g.nw == 3) hipLaunchKernelGGL((k_bgemm<BEPI_RESID, 3>), grid, dim3(kBT), 0, s, g, rows);
+      else hipLaunchKernelGGL((k_bgemm<BEPI_RESID, kBNW>), grid, dim3(kBT), 0, s, g, rows);
+      break;
+    case BEPI_SWIGLU:
+      if (g.nw == 3) hipLaunchKernelGGL((k_bgemm<BEPI_SWIGLU, 3>), grid, dim3(kBT), 0, s, g, rows);
+      else hipLaunchKernelGGL((k_bgemm<BEPI_SWIGLU, kBNW>), grid, dim3(kBT), 0, s, g, rows);
+      break;
+    case BEPI_BIAS16: hipLaunchKernelGGL((k_bgemm<BEPI_BIAS16, kBNW>), grid, dim3(kBT), 0, s, g, rows); break;
+    default: hipLaunchKernelGGL((k_bgemm<BEPI_ARGMAX, kBNW>), grid, dim3(kBT), 0, s, g, rows); break;
   }
 }
 

@@ -375,8 +375,8 @@ GemmPlan choose_plan(const char* name, int Nt, int Kt, int blocks, bool allow_sp
 // gate/up 1, the 8-layer context K/V of a ~270-row append 1); an earlier cost fit in k-tiles
 // per work-group chose 3 for Q/K/V, 23% slower.
 // DFLARE_BSPLIT_<NAME>=kg overrides the choice (tuning).
-int bgemm_split(int cus, const char* name, int Nt, int Mt, int Kt, int layers, bool allow) {
-  const long tiles = (long)bgemm_groups(Nt, Mt) * layers;
+int bgemm_split(int cus, const char* name, int Nt, int Mt, int Kt, int layers, bool allow, int nw = kBNW) {
+  const long tiles = (long)bgemm_groups(Nt, Mt, nw) * layers;
   if (!allow || tiles > kBCounters) return 1;
   int best = 1;
   for (int kg : {2, 3, 4, 6, 8})
@@ -388,6 +388,27 @@ int bgemm_split(int cus, const char* name, int Nt, int Mt, int Kt, int layers, b
     if (v >= 1 && v <= kBSplitMax && v <= Kt) best = v;
   }
   return best;
+}
+
+// Output-tile width of a batched GEMM (n-tiles per wave, 4 or 3): 3 where its work-groups
+// (with their K split) fill whole rounds of two per CU better, e.g. gate/up at 512 rows
+// (384 work-groups of 4 leave half the CUs with one, 512 of 3 give every CU two) and Q/K/V
+// (192 vs 256 work-groups on 256 CUs).  The LM head keeps 4 (its partial maxima are laid
+// out per 256 columns).  DFLARE_BNW_<NAME>=3|4 overrides the choice (tuning).
+int bgemm_nw(int cus, const char* name, int Nt, int Mt, int Kt, int layers, bool allow) {
+  auto fill = [&](int nw) {
+    const long wgs = (long)bgemm_groups(Nt, Mt, nw) * layers * bgemm_split(cus, name, Nt, Mt, Kt, layers, allow, nw);
+    const long slots = 2L * cus;
+    return (double)wgs / (double)(((wgs + slots - 1) / slots) * slots);
+  };
+  int nw = allow && fill(3) > fill(kBNW) + 1e-9 ? 3 : kBNW;
+  char key[64];
+  snprintf(key, sizeof key, "DFLARE_BNW_%s", name);
+  if (const char* env = getenv(key)) {
+    const int v = atoi(env);
+    if (allow && (v == 3 || v == kBNW)) nw = v;
+  }
+  return nw;
 }
 
 DraftArgs draft_args(const dflare_handle* h);
@@ -599,8 +620,10 @@ int build(dflare_handle* h, const dflare_weights* w) {
     // partial tiles of the largest split of any call shape
     long part = 0;
     auto need = [&](const char* name, int Nt, int mt, int Kt, int layers) {
-      const int kg = bgemm_split(h->cus, name, Nt, mt, Kt, layers, true);
-      if (kg > 1) part = std::max(part, (long)bgemm_groups(Nt, mt) * layers * kg * kBPartFloats);
+      for (int nw : {kBNW, 3}) {  // either tile width (the per-tile partial scales with it)
+        const int kg = bgemm_split(h->cus, name, Nt, mt, Kt, layers, true, nw);
+        if (kg > 1) part = std::max(part, (long)bgemm_groups(Nt, mt, nw) * layers * kg * kBPartFloats);
+      }
     };
     for (int mt = 1; mt <= h->b_mt; ++mt) {
       need("QKV", Nt_qkv, mt, Kt_H, 1);
@@ -863,7 +886,8 @@ int ensure_f16_weights(dflare_handle* h) {
 
 // one batched GEMM with its fused epilogue; the K split is chosen per shape
 void bgemm(dflare_handle* h, int kind, const char* name, int epi, BGemmArgs g, const BRows& rows) {
-  g.kg = bgemm_split(h->cus, name, g.Nt, g.Mt, g.Kt, g.layers, epi != BEPI_ARGMAX);
+  g.nw = bgemm_nw(h->cus, name, g.Nt, g.Mt, g.Kt, g.layers, epi != BEPI_ARGMAX && epi != BEPI_BIAS16);
+  g.kg = bgemm_split(h->cus, name, g.Nt, g.Mt, g.Kt, g.layers, epi != BEPI_ARGMAX, g.nw);
   g.zero = h->zero_tile;
   g.part = h->bpart;
   g.cnt = h->bcnt;
