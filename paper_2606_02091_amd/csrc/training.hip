@@ -48,6 +48,7 @@ struct AttnT {
   float2* st;                       // [n_kv][n_blocks][Rp] (lse * log2 e, rowsum(dO O)); (+inf, 0) past R
   float* dsum;                      // [M][n_q] rowsum(dO * O)
   float* part;                      // [nch][T][n_kv][hd] x2 (dK, dV)
+  int* order;                       // [n_blocks] blocks by decreasing anchor (work order)
   int nch;
   // outputs
   float *out, *lse;
@@ -189,7 +190,28 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t* q, const float
   }
 }
 
-// ---- forward and dQ: work-group (block i, KV head g); its 4 waves take the 16-row query
+// ---- work order of the row kernels: the blocks by decreasing anchor (ties by index), so that
+// the work-groups with the longest contexts start first and the short ones fill the tail.
+// Thread i counts the blocks that go before block i. ----
+__global__ __launch_bounds__(256) void k_anchor_order(const int32_t* anchors, int n, int T, int* order) {
+  __shared__ int sa[256];
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  const int ai = i < n ? min(max(anchors[i], 0), T) : 0;
+  int rank = 0;
+  for (int j0 = 0; j0 < n; j0 += 256) {
+    __syncthreads();
+    sa[threadIdx.x] = j0 + (int)threadIdx.x < n ? min(max(anchors[j0 + threadIdx.x], 0), T) : -1;
+    __syncthreads();
+    const int m = min(256, n - j0);
+    for (int k = 0; k < m; ++k) {
+      const int aj = sa[k];
+      rank += (aj > ai || (aj == ai && j0 + k < i)) ? 1 : 0;
+    }
+  }
+  if (i < n) order[rank] = i;
+}
+
+// ---- forward and dQ: work-group (block i, KV head g), blocks taken in the order above; its 4 waves take the 16-row query
 // tiles w, w + 4 (TPW tiles each).  Key tiles of 32 (the context before the anchor, then the
 // block's own keys) are shared through LDS, double-buffered: LDS-direct loads fill the next
 // tile while the current one goes through the matrix cores.  Per stage: K rows (and for dQ
@@ -204,7 +226,7 @@ __global__ __launch_bounds__(kTrT) void k_aatt_rows(AttnT a) {
   static_assert(NP % 64 == 0, "whole wave loads");
   __shared__ u32x4 lds[2][NP];
   const AttnShapeT& s = a.s;
-  const int i = blockIdx.x, g = blockIdx.y;
+  const int i = a.order[blockIdx.x], g = blockIdx.y;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = lane & 15, q4 = lane >> 4;
   const int QT = (s.R + 15) / 16;
@@ -1006,7 +1028,7 @@ static int att_check(int n_blocks, int B, int T, int n_q, int n_kv, int hd) {
 }
 
 struct WsLayout {
-  size_t kct, vct, kbt, vbt, qt, dot, qr, dor, st, dob, dsum, part, total;
+  size_t kct, vct, kbt, vbt, qt, dot, qr, dor, st, dob, dsum, part, order, total;
   int nch;
 };
 
@@ -1030,6 +1052,7 @@ static WsLayout ws_layout(const AttnShapeT& s) {
   L.dob = o; o = al(o + rows * s.hd * 2);
   L.dsum = o; o = al(o + rows * 4);
   L.part = o; o = al(o + (size_t)2 * L.nch * s.T * s.n_kv * s.hd * 4);
+  L.order = o; o = al(o + (size_t)s.n_blocks * 4);
   L.total = o;
   return L;
 }
@@ -1058,6 +1081,7 @@ static AttnT att_args(const AttnShapeT& s, const void* q, const void* kc, const 
   a.st = (float2*)(w + L.st);
   a.dsum = (float*)(w + L.dsum);
   a.part = (float*)(w + L.part);
+  a.order = (int*)(w + L.order);
   a.nch = L.nch;
   a.scale = 1.0f / sqrtf((float)s.hd);
   return a;
@@ -1103,6 +1127,7 @@ int dflare_anchor_attention_fwd(const void* q, const void* k_ctx, const void* v_
   const uint16_t* zero_src = a.kb;  // with T = 0 the context copies are all zeros
   transpose_kv(st, T > 0 ? a.vc : zero_src, T, cols, s.Tp, a.vct);
   hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks, (cols + 255) / 256), dim3(256), 0, st, a.vb, n_blocks, B, cols, a.vbt);
+  hipLaunchKernelGGL(k_anchor_order, dim3((n_blocks + 255) / 256), dim3(256), 0, st, anchors, n_blocks, T, a.order);
   const bool two = (s.R + 15) / 16 > 4;
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
@@ -1138,6 +1163,7 @@ int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_
   const uint16_t* zero_src = a.kb;
   transpose_kv(st, T > 0 ? a.kc : zero_src, T, cols, s.Tp, a.kct);
   hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks, (cols + 255) / 256), dim3(256), 0, st, a.kb, n_blocks, B, cols, a.kbt);
+  hipLaunchKernelGGL(k_anchor_order, dim3((n_blocks + 255) / 256), dim3(256), 0, st, anchors, n_blocks, T, a.order);
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
     hipLaunchKernelGGL((k_bwd_prep<HD>), dim3(n_blocks, n_kv), dim3(256), (size_t)4 * HD * s.Rp, st, a.q, dout, out,
