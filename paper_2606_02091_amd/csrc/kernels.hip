@@ -78,8 +78,8 @@ __global__ void k_bf16_to_f32(float* dst, const uint16_t* src, long n) {
 // Writes the A fragments of u^(i) * g_fuse^(i) and per-16-column sums of squares of u^(i);
 // the 1/rms of Eq. 3 is applied in the K/V projection.  The D blocks of one (512 columns,
 // row) pair read the same target row pieces; consecutive block ids are dealt to the 8 XCDs
-// in turn, so the pair's D blocks get ids 8 apart (one XCD, one L2) and the pieces come
-// from HBM once per pair.  Ids past the last pair are idle.
+// in turn, so the pair's D blocks get ids 8 apart (one XCD, one L2), where they can share
+// the pieces.  Ids past the last pair are idle.
 // ------------------------------------------------------------------------------------------
 constexpr int kFuseBatch = 40;  // target layers whose loads are in flight together
 constexpr int kXcds = 8;
