@@ -763,7 +763,8 @@ __global__ __launch_bounds__(256, 2) void k_battn(BAttnArgs a, BRows rows) {
 
   // loads of key block b into registers.  Every lane loads (pieces past kend repeat the
   // last key row or the last 8-key group), so that no load sits in a branch; those pieces
-  // are zeroed when they are stored to LDS.
+  // are zeroed when they are stored to LDS.  The cache is read once per step: nontemporal
+  // loads (115 -> 107 us per layer at 32 sequences).
   // blocks loaded ahead of the one being computed: two, or one where the query tiles of a
   // wave already fill the registers (set b % PF holds block b)
   constexpr int PF = (NBUF == 1 || (HD == 128 && TPW == 2)) ? 1 : 2;
@@ -775,10 +776,10 @@ __global__ __launch_bounds__(256, 2) void k_battn(BAttnArgs a, BRows rows) {
       const int p = k * NT + tid;  // the K / V^T split is static per k (KP is a multiple of NT)
       if (k * NT < KP) {
         const int r = p / KC, c = p % KC;
-        dst[k] = *reinterpret_cast<const u32x4*>(kc + (long)min(k0 + r, kend - 1) * HD + c * 8);
+        dst[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kc + (long)min(k0 + r, kend - 1) * HD + c * 8));
       } else {
         const int pv = p - KP, d = pv / VC, c = pv % VC;
-        dst[k] = *reinterpret_cast<const u32x4*>(vt + (long)d * a.Lcap + min(k0 + c * 8, (kend - 1) & ~7));
+        dst[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vt + (long)d * a.Lcap + min(k0 + c * 8, (kend - 1) & ~7)));
       }
     }
   };
