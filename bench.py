@@ -182,22 +182,25 @@ def summarize_counters(fetch_dir: str, write_dir: str, workload: str, context: i
     fetch_rows, write_rows = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
     out = {"kernels": {}}
     if workload == "batched":
-        # the batched GEMMs by epilogue template and grid: Q/K/V is the most frequent grid of
-        # k_bgemm<0> (8 per step; the append's context K/V GEMM runs once), the output
-        # projection the smaller and the down projection the larger grid of k_bgemm<1>
+        # the batched GEMMs by epilogue template (k_bgemm<epilogue, tile width>) and grid: Q/K/V
+        # is the most frequent grid of k_bgemm<0, ...> (8 per step; the append's context K/V GEMM
+        # runs once); the residual GEMMs k_bgemm<1, ...> alternate, output projection then down
+        # projection, in every layer, so they are told apart by their order of dispatch
         def grids(frag):
             from collections import Counter
             return Counter(g for _, n, g, _ in fetch_rows if frag in n)
-        g0, g1 = grids("k_bgemm<0>"), grids("k_bgemm<1>")
-        sel = {"gate_up": ("k_bgemm<2>", None), "lm_head": ("k_bgemm<3>", None), "attn": ("k_battn", None)}
+        g0 = grids("k_bgemm<0,")
+        sel = {"gate_up": ("k_bgemm<2,", None, None), "lm_head": ("k_bgemm<3,", None, None),
+               "attn": ("k_battn", None, None), "o": ("k_bgemm<1,", None, 0), "down": ("k_bgemm<1,", None, 1)}
         if g0:
-            sel["qkv"] = ("k_bgemm<0>", g0.most_common(1)[0][0])
-        if len(g1) >= 2:
-            top = sorted(g for g, _ in g1.most_common(2))
-            sel["o"], sel["down"] = ("k_bgemm<1>", top[0]), ("k_bgemm<1>", top[1])
-        for kname, (frag, grid) in sel.items():
-            fr = [v for _, n, g, v in fetch_rows if frag in n and (grid is None or g == grid)]
-            wr = [v for _, n, g, v in write_rows if frag in n and (grid is None or g == grid)]
+            sel["qkv"] = ("k_bgemm<0,", g0.most_common(1)[0][0], None)
+
+        def pick(rows_, frag, grid, parity):
+            r = sorted((d, v) for d, n, g, v in rows_ if frag in n and (grid is None or g == grid))
+            return [v for i, (_, v) in enumerate(r) if parity is None or i % 2 == parity]
+        for kname, (frag, grid, parity) in sel.items():
+            fr = pick(fetch_rows, frag, grid, parity)
+            wr = pick(write_rows, frag, grid, parity)
             if fr and len(fr) == len(wr):
                 out["kernels"][kname] = {"fetch_kib": int(statistics.median(fr)), "write_kib": int(statistics.median(wr)),
                                          "dispatches": len(fr)}

@@ -194,18 +194,21 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t* q, const float
 // the work-groups with the longest contexts start first and the short ones fill the tail.
 // Thread i counts the blocks that go before block i. ----
 __global__ __launch_bounds__(256) void k_anchor_order(const int32_t* anchors, int n, int T, int* order) {
-  __shared__ int sa[256];
+  __shared__ int4 sa[64];  // 256 anchors of the current tile; -1 past n (never counted)
   const int i = blockIdx.x * 256 + threadIdx.x;
   const int ai = i < n ? min(max(anchors[i], 0), T) : 0;
   int rank = 0;
   for (int j0 = 0; j0 < n; j0 += 256) {
     __syncthreads();
-    sa[threadIdx.x] = j0 + (int)threadIdx.x < n ? min(max(anchors[j0 + threadIdx.x], 0), T) : -1;
+    reinterpret_cast<int*>(sa)[threadIdx.x] = j0 + (int)threadIdx.x < n ? min(max(anchors[j0 + threadIdx.x], 0), T) : -1;
     __syncthreads();
-    const int m = min(256, n - j0);
-    for (int k = 0; k < m; ++k) {
-      const int aj = sa[k];
-      rank += (aj > ai || (aj == ai && j0 + k < i)) ? 1 : 0;
+    // four anchors per LDS read, many reads in flight (the sum has no order dependence)
+#pragma unroll 16
+    for (int k = 0; k < 64; ++k) {
+      const int4 v = sa[k];
+      const int j = j0 + 4 * k;
+      rank += (v.x > ai || (v.x == ai && j < i)) + (v.y > ai || (v.y == ai && j + 1 < i)) +
+              (v.z > ai || (v.z == ai && j + 2 < i)) + (v.w > ai || (v.w == ai && j + 3 < i));
     }
   }
   if (i < n) order[rank] = i;
