@@ -193,25 +193,24 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t* q, const float
 // ---- work order of the row kernels: the blocks by decreasing anchor (ties by index), so that
 // the work-groups with the longest contexts start first and the short ones fill the tail.
 // Thread i counts the blocks that go before block i. ----
-__global__ __launch_bounds__(256) void k_anchor_order(const int32_t* anchors, int n, int T, int* order) {
-  __shared__ int4 sa[64];  // 256 anchors of the current tile; -1 past n (never counted)
-  const int i = blockIdx.x * 256 + threadIdx.x;
+__global__ __launch_bounds__(256) void k_anchor_order(const int32_t* __restrict__ anchors, int n, int T,
+                                                      int* __restrict__ order) {
+  __shared__ int part[4][64];
+  // lane l of wave q: block i = 64 * blockIdx.x + l against the q-th quarter of the blocks; the
+  // quarter's anchors are the same for the whole wave (scalar loads)
+  const int l = threadIdx.x & 63, q = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int i = blockIdx.x * 64 + l;
   const int ai = i < n ? min(max(anchors[i], 0), T) : 0;
+  const int per = (n + 3) / 4, jb = q * per, je = min(n, jb + per);
   int rank = 0;
-  for (int j0 = 0; j0 < n; j0 += 256) {
-    __syncthreads();
-    reinterpret_cast<int*>(sa)[threadIdx.x] = j0 + (int)threadIdx.x < n ? min(max(anchors[j0 + threadIdx.x], 0), T) : -1;
-    __syncthreads();
-    // four anchors per LDS read, many reads in flight (the sum has no order dependence)
-#pragma unroll 16
-    for (int k = 0; k < 64; ++k) {
-      const int4 v = sa[k];
-      const int j = j0 + 4 * k;
-      rank += (v.x > ai || (v.x == ai && j < i)) + (v.y > ai || (v.y == ai && j + 1 < i)) +
-              (v.z > ai || (v.z == ai && j + 2 < i)) + (v.w > ai || (v.w == ai && j + 3 < i));
-    }
+#pragma unroll 8
+  for (int j = jb; j < je; ++j) {
+    const int aj = min(max(anchors[j], 0), T);
+    rank += (aj > ai || (aj == ai && j < i)) ? 1 : 0;
   }
-  if (i < n) order[rank] = i;
+  part[q][l] = rank;
+  __syncthreads();
+  if (q == 0 && i < n) order[part[0][l] + part[1][l] + part[2][l] + part[3][l]] = i;
 }
 
 // ---- forward and dQ: work-group (block i, KV head g), blocks taken in the order above; its 4 waves take the 16-row query
@@ -1130,7 +1129,7 @@ int dflare_anchor_attention_fwd(const void* q, const void* k_ctx, const void* v_
   const uint16_t* zero_src = a.kb;  // with T = 0 the context copies are all zeros
   transpose_kv(st, T > 0 ? a.vc : zero_src, T, cols, s.Tp, a.vct);
   hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks, (cols + 255) / 256), dim3(256), 0, st, a.vb, n_blocks, B, cols, a.vbt);
-  hipLaunchKernelGGL(k_anchor_order, dim3((n_blocks + 255) / 256), dim3(256), 0, st, anchors, n_blocks, T, a.order);
+  hipLaunchKernelGGL(k_anchor_order, dim3((n_blocks + 63) / 64), dim3(256), 0, st, anchors, n_blocks, T, a.order);
   const bool two = (s.R + 15) / 16 > 4;
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
@@ -1166,7 +1165,7 @@ int dflare_anchor_attention_bwd(const void* q, const void* k_ctx, const void* v_
   const uint16_t* zero_src = a.kb;
   transpose_kv(st, T > 0 ? a.kc : zero_src, T, cols, s.Tp, a.kct);
   hipLaunchKernelGGL(k_tr_blk_t, dim3(n_blocks, (cols + 255) / 256), dim3(256), 0, st, a.kb, n_blocks, B, cols, a.kbt);
-  hipLaunchKernelGGL(k_anchor_order, dim3((n_blocks + 255) / 256), dim3(256), 0, st, anchors, n_blocks, T, a.order);
+  hipLaunchKernelGGL(k_anchor_order, dim3((n_blocks + 63) / 64), dim3(256), 0, st, anchors, n_blocks, T, a.order);
   by_hd(hd, [&](auto h) {
     constexpr int HD = decltype(h)::value;
     hipLaunchKernelGGL((k_bwd_prep<HD>), dim3(n_blocks, n_kv), dim3(256), (size_t)4 * HD * s.Rp, st, a.q, dout, out,
