@@ -441,7 +441,7 @@ __device__ __forceinline__ int ctx_len(Call c) { return c->Lp ? *c->Lp : c->L; }
 // Run by wave 0.  Item = 8 columns of one row; items 2m and 2m + 1 (one 16-column tile) go to
 // lanes 2k and 2k + 1 of work-group m % blocks, so the work spreads over every work-group and
 // the two halves of a tile meet in one shuffle.
-__device__ void phase_embed(Args a, Call c) {
+__device__ __forceinline__ void phase_embed(Args a, Call c) {
   const int H = a->H, Kt = H / 32, per_row = H / 8;
   const int pairs = a->B * per_row / 2;
   const float* gain = a->g_attn;
@@ -1370,7 +1370,7 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
 // runs over S waves (S = 4 / rows per work-group), which meet in LDS in run order.  Waves
 // 4-7 meanwhile stream the context of the next layer's attention item into LDS (stage).
 template <int HD>
-__device__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, Failed failed, u32x4* smem,
+__device__ __forceinline__ void phase_comb(Args a, Call dc, int layer, const PhaseCtl& pc, Failed failed, u32x4* smem,
                            bool stage) {
   using A = AttnShape<HD>;
   constexpr int DPL = HD / 64;                 // dims per lane
