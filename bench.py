@@ -714,7 +714,7 @@ def phase_trace(dfl, h, step, cfg, kb, steps):
     epilogues, split-K combine and final epilogue; attention: key staging, scores and
     values, merge and stores).  "GBs" relates "us" to the phase's algorithmic bytes."""
     import numpy as np
-    n_launch, _, blocks, n_phase, _ = dfl.dflare_kernel_stats(h)
+    n_launch, _, blocks, n_phase = dfl.dflare_kernel_stats(h)[:4]
     if n_launch != 1:
         return None
     dfl.dflare_set_option(h, dfl.OPT_TRACE, 1)

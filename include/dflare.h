@@ -352,7 +352,11 @@ int dflare_debug_read_seq(dflare_handle* h, int what, int seq, int layer, float*
  *   [2] work-groups of the draft-block kernel
  *   [3] phases of a draft block (embedding; per layer QKV, attention, combine,
  *       output projection, gate/up, down; LM head)
- *   [4] grid barriers one draft_block waits at (0 with one launch per phase)
+ *   [4] grid barriers one draft_block waits at (0 with one launch per phase; the
+ *       combine phases wait for their KV head's attention items instead)
+ *   [5] plan signature of the draft-block kernel that runs: the chunk widths of
+ *       the Q/K/V, output, gate/up and down GEMMs in 4 bits each (Q/K/V lowest) for
+ *       a kernel built for the handle's plans, 0 for the generic kernel
  */
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count);
 
@@ -411,8 +415,20 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches);
  *                          layer (DFLARE_DBG_LOGITS, DFLARE_DBG_HIDDEN) in the launch
  *                          configuration that is timed; 0 (default): debug capture runs
  *                          one launch per phase.
+ *   DFLARE_OPT_GENERIC_KERNEL
+ *                          0 (default): where the library holds a draft-block kernel built
+ *                          for the handle's GEMM plans (the plans chosen for the Qwen3-8B,
+ *                          Qwen3-4B and GPT-OSS-20B shapes on 256 CUs), that kernel runs;
+ *                          1: the generic kernel, which reads the plans at run time.  Both
+ *                          compute the same results bit for bit.
  */
-enum { DFLARE_OPT_PERSISTENT = 1, DFLARE_OPT_TRACE = 2, DFLARE_OPT_CAPTURE_PERSISTENT = 3, DFLARE_OPT_COOPERATIVE = 4 };
+enum {
+  DFLARE_OPT_PERSISTENT = 1,
+  DFLARE_OPT_TRACE = 2,
+  DFLARE_OPT_CAPTURE_PERSISTENT = 3,
+  DFLARE_OPT_COOPERATIVE = 4,
+  DFLARE_OPT_GENERIC_KERNEL = 5
+};
 int dflare_set_option(dflare_handle* h, int option, int value);
 
 /*

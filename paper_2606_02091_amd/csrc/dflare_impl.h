@@ -194,10 +194,16 @@ void launch_kvt(hipStream_t s, int nt_per_block, int waves, const KvtArgs& a, in
 // Phases [p0, p1) of a draft block on `blocks` work-groups of kThreads threads, which wait at
 // grid barriers between phases (p1 > p0 + 1 needs all of them resident: one per CU, placed
 // at once when no other stream holds CUs).  cooperative = true asks the runtime to
-// guarantee that co-residency.
-hipError_t launch_draft(hipStream_t s, const DraftArgs* a_dev, const DraftCall& c, int hd, int blocks, int p0,
-                        int p1, bool cooperative);
-int draft_blocks_per_cu(int hd);
+// guarantee that co-residency.  sig is the plans' signature (chunk widths of Q/K/V, output,
+// gate/up and down, 4 bits each, draft_plan_sig): a kernel built for those plans runs if
+// there is one, else the generic kernel (sig 0), with the same results.
+hipError_t launch_draft(hipStream_t s, const DraftArgs* a_dev, const DraftCall& c, int hd, int sig, int blocks,
+                        int p0, int p1, bool cooperative);
+bool draft_specialized(int hd, int sig);
+int draft_blocks_per_cu(int hd, int sig);
+inline int draft_plan_sig(int tn_qkv, int tn_o, int tn_gu, int tn_down) {
+  return tn_qkv | tn_o << 4 | tn_gu << 8 | tn_down << 12;
+}
 // measurement: streaming read of `bytes` (a multiple of 16) on `blocks` work-groups of 256
 void launch_read_probe(hipStream_t s, const void* buf, long bytes, uint32_t* sink, int blocks);
 

@@ -1505,8 +1505,13 @@ __device__ __forceinline__ void phase_comb(Args a, Call dc, int layer, const Pha
   }
 }
 
-// GEMM phase with the plan's chunk width (the LM head always uses 8)
-template <int EPI>
+// Chunk width of phase kind slot s (Q/K/V 0, output 1, gate/up 2, down 3) in a kernel's plan
+// signature: 4 bits per slot; signature 0 leaves every width to the plan read at run time.
+constexpr int sig_tn(int sig, int s) { return (sig >> (4 * s)) & 15; }
+
+// GEMM phase with the plan's chunk width: TNF when the kernel is built for its plan, else the
+// plan's width read at run time (the LM head always uses 8)
+template <int EPI, int TNF>
 __device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int layer, const PhaseCtl& pc, Failed failed,
                                               u32x4* smem) {
   GemmJob g = make_job(a, c, kind, layer);
@@ -1516,6 +1521,8 @@ __device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int laye
   g.tag = (c->done_epoch * (unsigned)a->D + (unsigned)layer + 1u) & 1u;
   if constexpr (EPI == EPI_ARGMAX) {
     gemm_phase<EPI, 8>(a, c, g, kind, 1, pc, failed, smem);
+  } else if constexpr (TNF != 0) {
+    gemm_phase<EPI, TNF>(a, c, g, kind, kg, pc, failed, smem);
   } else {
     switch (a->tn[kind]) {
       case 2: gemm_phase<EPI, 2>(a, c, g, kind, kg, pc, failed, smem); break;
@@ -1529,7 +1536,13 @@ __device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int laye
 // The single kernel argument is read in place through the kernel-argument pointer, so each
 // field is loaded where it is used instead of being held in scalar registers (or copied to
 // scratch memory, as a by-reference use of a parameter would) for the whole launch.
-template <int HD>
+//
+// SIG != 0 builds the kernel for one set of GEMM plans (chunk widths per phase kind, see
+// sig_tn): only those GEMM bodies are instantiated, 100 KiB of code instead of 265 KiB.  The
+// phases of a layer then run from a smaller code footprint (each phase's epilogue runs once
+// per layer, so its instructions are fetched anew every layer); results are the same as the
+// generic kernel's (SIG = 0), which serves every other plan.
+template <int HD, int SIG>
 __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
   __shared__ u32x4 smem[kLdsBytes / 16];
   const CONSTANT DraftKernArgs* ka = (const CONSTANT DraftKernArgs*)__builtin_amdgcn_kernarg_segment_ptr();
@@ -1557,7 +1570,7 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
         attn_stage<HD>(a, c, 0, blockIdx.x, smem, 1);
         break;
       case PH_QKV:
-        gemm_dispatch<EPI_QKV>(a, c, kind, layer, pc, failed, smem);
+        gemm_dispatch<EPI_QKV, sig_tn(SIG, 0)>(a, c, kind, layer, pc, failed, smem);
         break;
       case PH_ATTN:  // staged by the embedding phase (layer 0) or the previous layer's combine phase
         phase_attn<HD>(a, c, layer, pc, failed, smem, layer == 0 ? p - 2 >= p0 : p - 5 >= p0);
@@ -1566,16 +1579,16 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
         phase_comb<HD>(a, c, layer, pc, failed, smem, layer + 1 < a->D && p + 5 < p1);
         break;
       case PH_O:
-        gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem);
+        gemm_dispatch<EPI_RESID, sig_tn(SIG, 1)>(a, c, kind, layer, pc, failed, smem);
         break;
       case PH_GU:
-        gemm_dispatch<EPI_SWIGLU>(a, c, kind, layer, pc, failed, smem);
+        gemm_dispatch<EPI_SWIGLU, sig_tn(SIG, 2)>(a, c, kind, layer, pc, failed, smem);
         break;
       case PH_DOWN:
-        gemm_dispatch<EPI_RESID>(a, c, kind, layer, pc, failed, smem);
+        gemm_dispatch<EPI_RESID, sig_tn(SIG, 3)>(a, c, kind, layer, pc, failed, smem);
         break;
       default:  // PH_LM
-        gemm_dispatch<EPI_ARGMAX>(a, c, kind, layer, pc, failed, smem);
+        gemm_dispatch<EPI_ARGMAX, 0>(a, c, kind, layer, pc, failed, smem);
         break;
     }
     // the attention phase hands over to the combine phase through the per-KV-head counters
@@ -1692,25 +1705,38 @@ void launch_read_probe(hipStream_t s, const void* buf, long bytes, uint32_t* sin
                      sink);
 }
 
-static const void* draft_kernel(int hd) {
-  return hd == 64 ? reinterpret_cast<const void*>(&k_draft<64>) : reinterpret_cast<const void*>(&k_draft<128>);
+// Kernels built for one set of plans: those the plan chooser picks on 256 work-groups for the
+// Qwen3-8B, Qwen3-4B and GPT-OSS-20B shapes (signature: Q/K/V | output << 4 | gate/up << 8 |
+// down << 12).  Any other head size and plan runs the generic kernel.
+constexpr int kSigQwen3_8B = 6 | 2 << 4 | 6 << 8 | 4 << 12;
+constexpr int kSigQwen3_4B = 4 | 4 << 4 | 6 << 8 | 6 << 12;
+constexpr int kSigGptOss = 6 | 4 << 4 | 4 << 8 | 4 << 12;
+
+static const void* draft_kernel(int hd, int sig) {
+  if (hd == 128 && sig == kSigQwen3_8B) return reinterpret_cast<const void*>(&k_draft<128, kSigQwen3_8B>);
+  if (hd == 128 && sig == kSigQwen3_4B) return reinterpret_cast<const void*>(&k_draft<128, kSigQwen3_4B>);
+  if (hd == 64 && sig == kSigGptOss) return reinterpret_cast<const void*>(&k_draft<64, kSigGptOss>);
+  return hd == 64 ? reinterpret_cast<const void*>(&k_draft<64, 0>) : reinterpret_cast<const void*>(&k_draft<128, 0>);
 }
 
-hipError_t launch_draft(hipStream_t s, const DraftArgs* a_dev, const DraftCall& c, int hd, int blocks, int p0,
-                        int p1, bool cooperative) {
+bool draft_specialized(int hd, int sig) { return draft_kernel(hd, sig) != draft_kernel(hd, 0); }
+
+hipError_t launch_draft(hipStream_t s, const DraftArgs* a_dev, const DraftCall& c, int hd, int sig, int blocks,
+                        int p0, int p1, bool cooperative) {
   DraftKernArgs ka;
   ka.a = a_dev;
   ka.c = c;
   ka.p0 = p0;
   ka.p1 = p1;
   void* kargs[] = {&ka};
-  if (cooperative) return hipLaunchCooperativeKernel(draft_kernel(hd), dim3(blocks), dim3(kThreads), kargs, 0, s);
-  return hipLaunchKernel(draft_kernel(hd), dim3(blocks), dim3(kThreads), kargs, 0, s);
+  const void* fn = draft_kernel(hd, sig);
+  if (cooperative) return hipLaunchCooperativeKernel(fn, dim3(blocks), dim3(kThreads), kargs, 0, s);
+  return hipLaunchKernel(fn, dim3(blocks), dim3(kThreads), kargs, 0, s);
 }
 
-int draft_blocks_per_cu(int hd) {
+int draft_blocks_per_cu(int hd, int sig) {
   int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, draft_kernel(hd), kThreads, 0) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, draft_kernel(hd, sig), kThreads, 0) != hipSuccess) return 0;
   return n;
 }
 

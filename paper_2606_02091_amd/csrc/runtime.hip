@@ -91,6 +91,8 @@ struct dflare_handle {
   bool persistent = true;
   bool coop_ok = false;    // the device keeps one work-group per CU resident
   bool coop_launch = false;  // DFLARE_OPT_COOPERATIVE: the persistent kernel through the cooperative launch
+  int draft_sig = 0;         // signature of the GEMM plans (draft_plan_sig) when a kernel is built for them
+  bool generic_draft = false;  // DFLARE_OPT_GENERIC_KERNEL: the generic draft kernel whatever the plans
   GemmPlan plan[PH_COUNT];
   int attn_nch = 1;
   int attn_chunk = 128;
@@ -438,7 +440,7 @@ int build(dflare_handle* h, const dflare_weights* w) {
   h->cus = cus;
   int coop = 0;
   HIP_OR_FAIL(h, hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, h->device));
-  const int per_cu = draft_blocks_per_cu(hd);
+  const int per_cu = draft_blocks_per_cu(hd, 0);
   h->coop_ok = coop != 0 && per_cu >= 1;
   h->blocks = cus;
   if (const char* env = getenv("DFLARE_BLOCKS")) {
@@ -455,6 +457,10 @@ int build(dflare_handle* h, const dflare_weights* w) {
   h->plan[PH_GU] = choose_plan("GU", Nt_gu, Kt_H, h->blocks, true);
   h->plan[PH_DOWN] = choose_plan("DOWN", Nt_down, Kt_F, h->blocks, true);
   h->plan[PH_LM] = choose_plan("LM", Nt_lm, Kt_H, h->blocks, false);
+  {
+    const int sig = draft_plan_sig(h->plan[PH_QKV].tn, h->plan[PH_O].tn, h->plan[PH_GU].tn, h->plan[PH_DOWN].tn);
+    if (draft_specialized(hd, sig) && draft_blocks_per_cu(hd, sig) >= 1) h->draft_sig = sig;
+  }
   if (getenv("DFLARE_VERBOSE"))
     fprintf(stderr, "dflare: %d work-groups; GEMM plans (tn,kg) qkv %d,%d o %d,%d gate/up %d,%d down %d,%d lm %d,%d\n",
             h->blocks, h->plan[PH_QKV].tn, h->plan[PH_QKV].kg, h->plan[PH_O].tn, h->plan[PH_O].kg,
@@ -801,12 +807,12 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   if (h->trace && !h->trace_buf) TRY(dev_zalloc(h, &h->trace_buf, (size_t)h->blocks * kTraceSlots * P * 8));
   if (h->trace) HIP_OR_FAIL(h, hipMemsetAsync(h->trace_buf, 0, (size_t)h->blocks * kTraceSlots * P * 8, s));
   const DraftCall dc = draft_call(h, ids, positions_host, out);
-  const int hd = c.head_dim;
+  const int hd = c.head_dim, sig = h->generic_draft ? 0 : h->draft_sig;
   const bool split = !h->persistent || (h->debug && !h->capture_persistent) ||
                      (h->prof_kind >= DFLARE_K_QKV && h->prof_kind <= DFLARE_K_LM_HEAD);
   prof_mark(h, DFLARE_K_DRAFT, true);
   if (!split) {
-    HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, h->blocks, 0, P, h->coop_launch));
+    HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, sig, h->blocks, 0, P, h->coop_launch));
     // a grid barrier before every phase but the first and the combine phases
     h->bar_epoch += (unsigned)(P - 1 - c.n_draft_layers);
   } else {
@@ -816,7 +822,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
       const int pk = prof_kind_of(kind);
       const bool open = pk && (kind != PH_COMB);  // attention + combine are timed together
       if (open) prof_mark(h, pk, true);
-      HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, h->blocks, p, p + 1, false));
+      HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, sig, h->blocks, p, p + 1, false));
       if (pk && kind != PH_ATTN) prof_mark(h, pk, false);
       if (h->debug && kind == PH_DOWN)
         HIP_OR_FAIL(h, hipMemcpyAsync(h->dbg_hidden + (long)layer * c.block_size * c.hidden, h->X,
@@ -1531,8 +1537,10 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches) {
 
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count) {
   if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
-  const int32_t v[5] = {h->persistent ? 1 : h->phases, 2, h->blocks, h->phases, h->persistent ? h->phases - 1 : 0};
-  for (int i = 0; i < count && i < 5; ++i) out[i] = v[i];
+  const int32_t v[6] = {h->persistent ? 1 : h->phases, 2, h->blocks, h->phases,
+                        h->persistent ? h->phases - 1 - h->cfg.n_draft_layers : 0,
+                        h->generic_draft ? 0 : h->draft_sig};
+  for (int i = 0; i < count && i < 6; ++i) out[i] = v[i];
   return DFLARE_OK;
 }
 
@@ -1562,6 +1570,9 @@ int dflare_set_option(dflare_handle* h, int option, int value) {
       return DFLARE_OK;
     case DFLARE_OPT_COOPERATIVE:
       h->coop_launch = value != 0;
+      return DFLARE_OK;
+    case DFLARE_OPT_GENERIC_KERNEL:
+      h->generic_draft = value != 0;
       return DFLARE_OK;
     default: return fail(h, DFLARE_ERR_INVALID_ARG, "unknown option");
   }

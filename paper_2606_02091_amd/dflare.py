@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "lib
 
 OK, ERR_INVALID_ARG, ERR_OUT_OF_MEMORY, ERR_CONTEXT_FULL, ERR_HIP, ERR_UNSUPPORTED = 0, -1, -2, -3, -4, -5
 DBG_FUSED, DBG_KCACHE, DBG_VCACHE, DBG_HIDDEN, DBG_LOGITS, DBG_ALPHA, DBG_TRACE, DBG_BLOGITS = range(8)
-OPT_PERSISTENT, OPT_TRACE, OPT_CAPTURE_PERSISTENT, OPT_COOPERATIVE = 1, 2, 3, 4
+OPT_PERSISTENT, OPT_TRACE, OPT_CAPTURE_PERSISTENT, OPT_COOPERATIVE, OPT_GENERIC_KERNEL = 1, 2, 3, 4, 5
 
 EXPORTED = (
     "dflare_init", "dflare_fuse_append", "dflare_draft_block", "dflare_draft_block_pos",
@@ -349,9 +349,10 @@ def dflare_debug_read(h: int, what: int, layer: int, shape) -> np.ndarray:
 
 
 def dflare_kernel_stats(h: int) -> tuple[int, ...]:
-    """(kernels per draft_block, kernels per fuse_append, work-groups, phases, grid barriers)."""
-    out = (ctypes.c_int32 * 5)()
-    _check(lib().dflare_kernel_stats(h, out, 5), h)
+    """(kernels per draft_block, kernels per fuse_append, work-groups, phases, grid barriers,
+    plan signature of the draft-block kernel, 0 for the generic one)."""
+    out = (ctypes.c_int32 * 6)()
+    _check(lib().dflare_kernel_stats(h, out, 6), h)
     return tuple(out)
 
 

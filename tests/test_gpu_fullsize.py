@@ -7,7 +7,8 @@ context K/V cache of every draft layer, the block rows after every layer, the lo
 and the draft tokens (the bar of tests/parity.py).  The bench's configuration -- a
 non-default stream, the draft block as one persistent launch whose phases wait at grid
 barriers -- must produce the very same tokens, bitwise, as the debug run with one
-launch per phase.
+launch per phase, and the kernel built for the shape's GEMM plans the very same logits
+and rows as the generic kernel.
 """
 import os
 
@@ -70,6 +71,22 @@ def test_fullsize_parity(name):
             p_logits = dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0, (cfg.block_size, cfg.vocab))
             p_hidden = [dfl.dflare_debug_read(model.h, dfl.DBG_HIDDEN, i, (cfg.block_size, cfg.hidden))
                         for i in range(cfg.n_draft_layers)]
+            # these shapes' plans on 256 CUs have a kernel built for them; the generic kernel
+            # (plans read at run time) gives the same logits and rows bitwise
+            stats = dfl.dflare_kernel_stats(model.h)
+            if stats[2] == 256:
+                assert stats[5] != 0, (name, stats)
+            dfl.dflare_set_option(model.h, dfl.OPT_GENERIC_KERNEL, 1)
+            assert dfl.dflare_kernel_stats(model.h)[5] == 0
+            model.draft_block(ids_t, out)
+            side.synchronize()
+            dfl.dflare_set_option(model.h, dfl.OPT_GENERIC_KERNEL, 0)
+            assert np.array_equal(out.cpu().numpy(), persistent_tokens), (name, step, "generic kernel")
+            assert np.array_equal(p_logits, dfl.dflare_debug_read(model.h, dfl.DBG_LOGITS, 0,
+                                                                  (cfg.block_size, cfg.vocab))), (name, step)
+            for i in range(cfg.n_draft_layers):
+                g = dfl.dflare_debug_read(model.h, dfl.DBG_HIDDEN, i, (cfg.block_size, cfg.hidden))
+                assert np.array_equal(p_hidden[i], g), (name, step, "generic kernel", i)
             dfl.dflare_set_option(model.h, dfl.OPT_CAPTURE_PERSISTENT, 0)
             eager = model.draft_block(ids_t).cpu().numpy()
             side.synchronize()
