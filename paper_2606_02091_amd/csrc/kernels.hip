@@ -1578,14 +1578,17 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
       case PH_COMB:  // stages the next layer's first attention item when that phase runs in this launch
         phase_comb<HD>(a, c, layer, pc, failed, smem, layer + 1 < a->D && p + 5 < p1);
         break;
-      case PH_O:
-        gemm_dispatch<EPI_RESID, sig_tn(SIG, 1)>(a, c, kind, layer, pc, failed, smem);
-        break;
       case PH_GU:
         gemm_dispatch<EPI_SWIGLU, sig_tn(SIG, 2)>(a, c, kind, layer, pc, failed, smem);
         break;
+      case PH_O:  // one call site for both residual GEMMs: one copy of each body they use
       case PH_DOWN:
-        gemm_dispatch<EPI_RESID, sig_tn(SIG, 3)>(a, c, kind, layer, pc, failed, smem);
+        if constexpr (sig_tn(SIG, 1) == sig_tn(SIG, 3))
+          gemm_dispatch<EPI_RESID, sig_tn(SIG, 1)>(a, c, kind, layer, pc, failed, smem);
+        else if (kind == PH_O)
+          gemm_dispatch<EPI_RESID, sig_tn(SIG, 1)>(a, c, kind, layer, pc, failed, smem);
+        else
+          gemm_dispatch<EPI_RESID, sig_tn(SIG, 3)>(a, c, kind, layer, pc, failed, smem);
         break;
       default:  // PH_LM
         gemm_dispatch<EPI_ARGMAX, 0>(a, c, kind, layer, pc, failed, smem);
@@ -1708,8 +1711,8 @@ void launch_read_probe(hipStream_t s, const void* buf, long bytes, uint32_t* sin
 // Kernels built for one set of plans: those the plan chooser picks on 256 work-groups for the
 // Qwen3-8B, Qwen3-4B and GPT-OSS-20B shapes (signature: Q/K/V | output << 4 | gate/up << 8 |
 // down << 12).  Any other head size and plan runs the generic kernel.
-constexpr int kSigQwen3_8B = 6 | 2 << 4 | 6 << 8 | 4 << 12;
-constexpr int kSigQwen3_4B = 4 | 4 << 4 | 6 << 8 | 6 << 12;
+constexpr int kSigQwen3_8B = 6 | 4 << 4 | 6 << 8 | 4 << 12;
+constexpr int kSigQwen3_4B = 4 | 4 << 4 | 6 << 8 | 4 << 12;
 constexpr int kSigGptOss = 6 | 4 << 4 | 4 << 8 | 4 << 12;
 
 static const void* draft_kernel(int hd, int sig) {
