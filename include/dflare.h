@@ -353,7 +353,8 @@ int dflare_debug_read_seq(dflare_handle* h, int what, int seq, int layer, float*
  *   [3] phases of a draft block (embedding; per layer QKV, attention, combine,
  *       output projection, gate/up, down; LM head)
  *   [4] grid barriers one draft_block waits at (0 with one launch per phase; the
- *       combine phases wait for their KV head's attention items instead)
+ *       attention and combine phases wait for their KV head's Q/K/V tiles and
+ *       attention items instead)
  *   [5] plan signature of the draft-block kernel that runs: the chunk widths of
  *       the Q/K/V, output, gate/up and down GEMMs in 4 bits each (Q/K/V lowest) for
  *       a kernel built for the handle's plans, 0 for the generic kernel

@@ -37,10 +37,12 @@ constexpr int kMaxBlocks = 1024;  // work-groups of the draft-block kernel
 // kSplitKinds x kMaxBlocks counter lines follows the grid-barrier counters and the LM-head
 // completion counter in the synchronisation area.
 constexpr int kSplitKinds = 4;    // QKV, O, gate/up, down
-// Attention arrival counters: one per KV head, each on its own 128 B line, after the split-K ones.
+// Attention arrival counters, then Q/K/V tile counters: one per KV head each, each on its own
+// 128 B line, after the split-K ones.
 constexpr int kMaxKvHeads = 128;
 constexpr long kAttnCntOff = 4096 + (long)kSplitKinds * kMaxBlocks * 128;  // bytes
-constexpr long kSyncBytes = kAttnCntOff + (long)kMaxKvHeads * 128;
+constexpr long kQkvCntOff = kAttnCntOff + (long)kMaxKvHeads * 128;         // bytes
+constexpr long kSyncBytes = kQkvCntOff + (long)kMaxKvHeads * 128;
 // Zero k-tiles after the K real ones in every draft-block activation (A-fragment) plane:
 // a GEMM wave's run of k-tiles may reach past K, by less than 2 * 8 + 1 batches of 4.
 constexpr int kKtPad = 72;
@@ -77,6 +79,7 @@ struct DraftCall {
   unsigned bar_epoch;   // grid barriers completed by earlier launches
   unsigned done_epoch;  // launches that ran the LM phase before this one
   unsigned acnt_base;   // value of every attention arrival counter before this launch
+  unsigned qcnt_base;   // value of every Q/K/V tile counter before this launch
   unsigned long long* trace;  // optional [blocks][phases][kTraceSlots] wall clock at marks of each phase
   // candidate selection: inv_temp = 0 greedy argmax; otherwise argmax of z * inv_temp plus
   // Gumbel noise of draw `draw` under `seed` (sequence slot 0)
@@ -135,6 +138,7 @@ struct DraftArgs {
   float* part;           // split-K partial sums [kSplitKinds][blocks][kTNMax][64 lanes][4], tagged per use
   unsigned* kcnt;        // spare counters [kSplitKinds][kMaxBlocks], 32 words apart (unused by the draft block)
   unsigned* acnt;        // attention arrival counters [n_kv], 32 words apart, monotonic across launches
+  unsigned* qcnt;        // Q/K/V tile counters [n_kv], 32 words apart, monotonic across launches
   // synchronisation
   unsigned* bar;          // kBarCounters counters, 32 words apart, monotonic across launches
   unsigned* done;         // LM-head completion counter, monotonic across launches

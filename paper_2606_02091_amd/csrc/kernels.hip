@@ -433,6 +433,57 @@ __device__ __forceinline__ void phase_begin(Args a, Call c, const PhaseCtl& pc,
   trace_mark(c, pc.slot, pc.nslots);
 }
 
+// Q/K/V -> attention hand-over without a grid barrier.  An attention item of KV head g needs
+// only the Q tiles of g's query heads and g's K and V tiles (its block keys), (G + 2) hd / 16
+// tiles per layer.  Each work-group that finishes Q/K/V tiles (a range's first work-group, or
+// every one without a K split) adds, once every wave's stores are complete, the number it
+// finished of each head to that head's counter; an item waits until its head's counter holds
+// this layer's count (counters are monotonic across launches, from qcnt_base).
+__device__ __forceinline__ void qkv_arrive(Args a) {
+  wait_vm();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int kg = a->kg[PH_QKV];
+    if (blockIdx.x % kg == 0) {
+      const int rg = blockIdx.x / kg, nq = a->nq[PH_QKV], nr = a->nr[PH_QKV];
+      const int t0 = rg * nq + min(rg, nr), t1 = t0 + nq + (rg < nr ? 1 : 0);
+      const int tph = a->hd / 16, G = a->n_q / a->n_kv, nqt = a->n_q * tph, nkt = a->n_kv * tph;
+      int head = -1;
+      unsigned n = 0;
+      for (int t = t0; t < t1; ++t) {
+        const int hq = t < nqt ? t / (G * tph) : (t - nqt < nkt ? (t - nqt) / tph : (t - nqt - nkt) / tph);
+        if (hq != head) {
+          if (n) __hip_atomic_fetch_add(a->qcnt + head * 32, n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          head = hq;
+          n = 0;
+        }
+        ++n;
+      }
+      if (n) __hip_atomic_fetch_add(a->qcnt + head * 32, n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+__device__ __forceinline__ void qkv_wait(Args a, Call c, int layer, int g, Failed failed) {
+  if (threadIdx.x < 64 && !*failed) {
+    const unsigned* cnt = a->qcnt + g * 32;
+    const unsigned target =
+        c->qcnt_base + (unsigned)(layer + 1) * (unsigned)((a->n_q / a->n_kv + 2) * (a->hd / 16));
+    const long long t0 = wall_clock64();
+    while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      __builtin_amdgcn_s_sleep(1);
+      if (wall_clock64() - t0 > kBarrierTimeout) {
+        if (threadIdx.x == 0) {
+          *failed = 1;
+          __hip_atomic_store(a->err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+        break;
+      }
+    }
+  }
+  __syncthreads();
+}
+
 // Context length of the call: the host's value or, when the length is kept on the device
 // (after a verification step that did not wait), the word written by that step.
 __device__ __forceinline__ int ctx_len(Call c) { return c->Lp ? *c->Lp : c->L; }
@@ -1361,8 +1412,15 @@ __device__ __forceinline__ void phase_attn(Args a, Call dc, int layer, const Pha
   };
 
   // One call site for the item body keeps the phase's code small.
-  phase_begin(a, dc, pc, failed);
-  for (int j = blockIdx.x; j < items; j += gridDim.x) item(j, staged && j == (int)blockIdx.x);
+  // no grid barrier before this phase: each item waits for its KV head's Q/K/V tiles
+  if (!pc.wait || (int)blockIdx.x >= items) trace_mark(dc, pc.slot, pc.nslots);
+  for (int j = blockIdx.x; j < items; j += gridDim.x) {
+    if (pc.wait) {
+      qkv_wait(a, dc, layer, j % nkv, failed);
+      if (j == (int)blockIdx.x) trace_mark(dc, pc.slot, pc.nslots);
+    }
+    item(j, staged && j == (int)blockIdx.x);
+  }
 }
 
 // COMB: work-groups b < W * n_kv (W = work-groups per KV head) merge the chunks of KV head
@@ -1558,8 +1616,10 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
     int kind, layer;
     phase_of(p, a->D, kind, layer);
     PhaseCtl pc;
-    pc.wait = p > p0;  // the combine phase waits for its KV head's items, every other phase at a grid barrier
-    if (pc.wait && kind != PH_COMB) ++epoch;
+    // the attention and combine phases wait for their KV head's Q/K/V tiles and attention
+    // items, every other phase at a grid barrier
+    pc.wait = p > p0;
+    if (pc.wait && kind != PH_ATTN && kind != PH_COMB) ++epoch;
     pc.epoch = epoch;
     pc.slot = kTraceSlots * p;
     pc.nslots = nslots;
@@ -1594,9 +1654,11 @@ __global__ __launch_bounds__(kThreads) void k_draft(DraftKernArgs) {
         gemm_dispatch<EPI_ARGMAX, 0>(a, c, kind, layer, pc, failed, smem);
         break;
     }
-    // the attention phase hands over to the combine phase through the per-KV-head counters
+    // the Q/K/V and attention phases hand over through the per-KV-head counters (the Q/K/V
+    // counts are added in every launch: the host's count of them does not depend on the mode);
     // the staging waves of the embedding phase issued loads only: they need not wait for them
-    if (p + 1 < p1 && kind != PH_ATTN) grid_arrive(a, kind != PH_EMBED || threadIdx.x < 64);
+    if (kind == PH_QKV) qkv_arrive(a);
+    else if (p + 1 < p1 && kind != PH_ATTN) grid_arrive(a, kind != PH_EMBED || threadIdx.x < 64);
     else wait_vm();
     trace_mark(c, kTraceSlots * p + kTraceSlots - 1, nslots);
   }

@@ -116,6 +116,7 @@ struct dflare_handle {
   unsigned* sync = nullptr;  // barrier counters, the LM-head completion counter, split-K counters
   unsigned bar_epoch = 0, done_epoch = 0;
   unsigned acnt_epoch = 0;  // value of every attention arrival counter (grows by D * chunks per draft block)
+  unsigned qcnt_epoch = 0;  // value of every Q/K/V tile counter (grows by D * (G + 2) * hd / 16 per draft block)
   int* err_host = nullptr;   // host-mapped barrier time-out flag
   int* err_dev = nullptr;
   // Context length of slot 0 kept on the device (after dflare_accept_async): two words used
@@ -775,6 +776,7 @@ DraftArgs draft_args(const dflare_handle* h) {
   a.part = h->part;
   a.kcnt = h->sync + 1024;
   a.acnt = h->sync + kAttnCntOff / 4;
+  a.qcnt = h->sync + kQkvCntOff / 4;
   a.err = h->err_dev;
   return a;
 }
@@ -793,6 +795,7 @@ DraftCall draft_call(const dflare_handle* h, const int32_t* ids, const int32_t* 
   d.bar_epoch = h->bar_epoch;
   d.done_epoch = h->done_epoch;
   d.acnt_base = h->acnt_epoch;
+  d.qcnt_base = h->qcnt_epoch;
   d.trace = h->trace ? h->trace_buf : nullptr;
   d.inv_temp = h->temperature > 0.f ? 1.0f / h->temperature : 0.f;
   d.draw = h->draw;
@@ -821,7 +824,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
     HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
     HIP_OR_FAIL(h, hipMemsetAsync(h->part, 0, (size_t)kSplitKinds * h->blocks * kTNMax * 1024, s));
     HIP_OR_FAIL(h, hipStreamSynchronize(s));
-    h->bar_epoch = h->done_epoch = h->acnt_epoch = 0;
+    h->bar_epoch = h->done_epoch = h->acnt_epoch = h->qcnt_epoch = 0;
     *(volatile int*)h->err_host = 0;
     h->persistent = false;
     return fail(h, DFLARE_ERR_HIP,
@@ -832,14 +835,17 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   // counters are monotonic across launches; start again from zero long before they wrap
   // (split-K counters reach (done_epoch + 1) * D * kg <= (done_epoch + 1) * D * 8)
   // (every layer adds the chunk capacity to each attention counter, whatever the length)
+  // (every layer's Q/K/V phase adds each KV head's tile count, (G + 2) * hd / 16, to its counter)
   const unsigned attn_adds = (unsigned)c.n_draft_layers * (unsigned)h->attn_nch;
+  const unsigned qkv_adds =
+      (unsigned)c.n_draft_layers * (unsigned)(c.n_q_heads / c.n_kv_heads + 2) * (unsigned)(c.head_dim / 16);
   if (h->bar_epoch + (unsigned)P > (1u << 24) || h->done_epoch + 1u > (1u << 22) ||
       ((uint64_t)h->done_epoch + 1u) * (uint64_t)c.n_draft_layers * kMaxSplit >= (1ull << 31) ||
-      (uint64_t)h->acnt_epoch + attn_adds >= (1ull << 31)) {
+      (uint64_t)h->acnt_epoch + attn_adds >= (1ull << 31) || (uint64_t)h->qcnt_epoch + qkv_adds >= (1ull << 31)) {
     // the split-K partial tags follow done_epoch: start them again from cleared areas
     HIP_OR_FAIL(h, hipMemsetAsync(h->sync, 0, kSyncBytes, s));
     HIP_OR_FAIL(h, hipMemsetAsync(h->part, 0, (size_t)kSplitKinds * h->blocks * kTNMax * 1024, s));
-    h->bar_epoch = h->done_epoch = h->acnt_epoch = 0;
+    h->bar_epoch = h->done_epoch = h->acnt_epoch = h->qcnt_epoch = 0;
   }
   if (h->trace && !h->trace_buf) TRY(dev_zalloc(h, &h->trace_buf, (size_t)h->blocks * kTraceSlots * P * 8));
   if (h->trace) HIP_OR_FAIL(h, hipMemsetAsync(h->trace_buf, 0, (size_t)h->blocks * kTraceSlots * P * 8, s));
@@ -850,8 +856,8 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   prof_mark(h, DFLARE_K_DRAFT, true);
   if (!split) {
     HIP_OR_FAIL(h, launch_draft(s, h->args_dev, dc, hd, sig, h->blocks, 0, P, h->coop_launch));
-    // a grid barrier before every phase but the first and the combine phases
-    h->bar_epoch += (unsigned)(P - 1 - c.n_draft_layers);
+    // a grid barrier before every phase but the first and the attention and combine phases
+    h->bar_epoch += (unsigned)(P - 1 - 2 * c.n_draft_layers);
   } else {
     for (int p = 0; p < P; ++p) {
       int kind, layer;
@@ -868,6 +874,7 @@ int run_draft_block(dflare_handle* h, const int32_t* ids, const int32_t* positio
   }
   h->done_epoch += 1;
   h->acnt_epoch += attn_adds;  // every attention item of every layer counted once
+  h->qcnt_epoch += qkv_adds;   // every Q/K/V tile of every layer counted once
   if (h->temperature > 0.f) ++h->draw;
   prof_mark(h, DFLARE_K_DRAFT, false);
   return check_launch(h, "draft_block");
@@ -1575,7 +1582,7 @@ int dflare_profile_end(dflare_handle* h, double* total_ms, int32_t* launches) {
 int dflare_kernel_stats(const dflare_handle* h, int32_t* out, int32_t count) {
   if (!live(h) || !out) return DFLARE_ERR_INVALID_ARG;
   const int32_t v[6] = {h->persistent ? 1 : h->phases, 2, h->blocks, h->phases,
-                        h->persistent ? h->phases - 1 - h->cfg.n_draft_layers : 0,
+                        h->persistent ? h->phases - 1 - 2 * h->cfg.n_draft_layers : 0,
                         h->generic_draft ? 0 : h->draft_sig};
   for (int i = 0; i < count && i < 6; ++i) out[i] = v[i];
   return DFLARE_OK;
