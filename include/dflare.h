@@ -221,8 +221,9 @@ int dflare_accept_async(dflare_handle* h, const int32_t* block_ids, const int32_
  * Block row b sits at position L + b.  The context cache is not modified, so the
  * call can be repeated.  An empty context (L = 0) is allowed.
  * By default the whole pass is one launch of one work-group per CU whose phases
- * are separated by grid barriers (see DFLARE_OPT_PERSISTENT); the barriers need
- * every work-group resident at once (DFLARE_OPT_COOPERATIVE).  If a grid barrier
+ * are separated by grid barriers or per-KV-head counters (see
+ * DFLARE_OPT_PERSISTENT); these waits need every work-group resident at once
+ * (DFLARE_OPT_COOPERATIVE).  If a grid barrier
  * of an earlier call timed out (the work-groups were not all resident within
  * 0.25 s), this call returns DFLARE_ERR_HIP without enqueuing work and the handle
  * switches to one launch per phase.
