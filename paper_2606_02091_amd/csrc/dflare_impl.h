@@ -103,7 +103,7 @@ struct DraftArgs {
   float eps, qscale;
   // GEMM plan of each phase kind: the work-groups form blocks / kg output ranges of
   // consecutive n-tiles, kg work-groups per range each taking 1/kg of K; a work-group
-  // accumulates up to tn (2, 3, 4, 6 or 8) n-tiles at once.
+  // accumulates up to tn (2, 3, 4, 5, 6 or 8) n-tiles at once.
   int tn[PH_COUNT], kg[PH_COUNT];
   // the partition, precomputed: output range r holds nq + (r < nr) n-tiles starting at
   // r * nq + min(r, nr); K part k holds kq + (k < kr) k-tiles starting at k * kq + min(k, kr)

@@ -1586,6 +1586,7 @@ __device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int laye
       case 2: gemm_phase<EPI, 2>(a, c, g, kind, kg, pc, failed, smem); break;
       case 3: gemm_phase<EPI, 3>(a, c, g, kind, kg, pc, failed, smem); break;
       case 4: gemm_phase<EPI, 4>(a, c, g, kind, kg, pc, failed, smem); break;
+      case 5: gemm_phase<EPI, 5>(a, c, g, kind, kg, pc, failed, smem); break;
       case 6: gemm_phase<EPI, 6>(a, c, g, kind, kg, pc, failed, smem); break;
       default: gemm_phase<EPI, 8>(a, c, g, kind, kg, pc, failed, smem); break;
     }
@@ -1775,8 +1776,8 @@ void launch_read_probe(hipStream_t s, const void* buf, long bytes, uint32_t* sin
 // Qwen3-8B, Qwen3-4B and GPT-OSS-20B shapes (signature: Q/K/V | output << 4 | gate/up << 8 |
 // down << 12).  Any other head size and plan runs the generic kernel.
 constexpr int kSigQwen3_8B = 3 | 4 << 4 | 6 << 8 | 4 << 12;
-constexpr int kSigQwen3_4B = 3 | 3 << 4 | 6 << 8 | 3 << 12;
-constexpr int kSigGptOss = 6 | 3 << 4 | 3 << 8 | 3 << 12;
+constexpr int kSigQwen3_4B = 3 | 3 << 4 | 5 << 8 | 3 << 12;
+constexpr int kSigGptOss = 5 | 3 << 4 | 3 << 8 | 3 << 12;
 
 static const void* draft_kernel(int hd, int sig) {
   if (hd == 128 && sig == kSigQwen3_8B) return reinterpret_cast<const void*>(&k_draft<128, kSigQwen3_8B>);

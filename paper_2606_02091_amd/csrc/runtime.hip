@@ -324,13 +324,13 @@ int validate_config(const dflare_config* c) {
 
 // GEMM plan of a phase kind (see DraftArgs::tn / kg).  Candidates: kg in {1, 2, 4, 8}
 // dividing the work-group count (kg > 1 only where the epilogue is linear in the sum and
-// a range fits one chunk of <= 8 tiles), tn the smallest of 2, 3, 4, 6, 8 that holds a range
+// a range fits one chunk of <= 8 tiles), tn the smallest of 2, 3, 4, 5, 6, 8 that holds a range
 // (8 when a range needs several chunks).  Cost, in KiB streamed by the busiest work-group:
 // its weight tiles, plus a quarter of its A-fragment and padding re-reads (L2 hits), plus
 // for a split the partial tiles the last work-group reads back and a fixed 16 for the
 // extra round trip.  DFLARE_PLAN_<NAME>=tn,kg overrides the choice (tuning, tests).
 bool plan_ok(int tn, int kg, int Nt, int blocks, bool allow_split) {
-  if (tn != 2 && tn != 3 && tn != 4 && tn != 6 && tn != 8) return false;
+  if (tn < 2 || tn > 8 || tn == 7) return false;
   if (kg < 1 || kg > kMaxSplit || (kg & (kg - 1)) || blocks % kg) return false;
   if (kg > 1 && (!allow_split || ceil_div(Nt, blocks / kg) > tn)) return false;
   return true;
@@ -347,7 +347,7 @@ GemmPlan choose_plan(const char* name, int Nt, int Kt, int blocks, bool allow_sp
     const int T = ceil_div(Nt, blocks / kg);
     if (kg > 1 && T > kTNMax) continue;
     int tn = kTNMax;
-    for (int c : {2, 3, 4, 6, 8})
+    for (int c : {2, 3, 4, 5, 6, 8})
       if (c >= T) {
         tn = c;
         break;
@@ -391,7 +391,7 @@ void share_resid_width(GemmPlan& po, GemmPlan& pd, int Nt_o, int Kt_o, int Nt_d,
   if (po.tn == pd.tn) return;
   double best = 1e300;
   GemmPlan bo = po, bd = pd;
-  for (int tn : {2, 3, 4, 6, 8}) {
+  for (int tn : {2, 3, 4, 5, 6, 8}) {
     double xo = 0, xd = 0;
     const GemmPlan qo = choose_plan("O", Nt_o, Kt_o, blocks, true, tn, &xo);
     const GemmPlan qd = choose_plan("DOWN", Nt_d, Kt_d, blocks, true, tn, &xd);
