@@ -1598,7 +1598,7 @@ __device__ __forceinline__ void gemm_dispatch(Args a, Call c, int kind, int laye
 // scratch memory, as a by-reference use of a parameter would) for the whole launch.
 //
 // SIG != 0 builds the kernel for one set of GEMM plans (chunk widths per phase kind, see
-// sig_tn): only those GEMM bodies are instantiated, 100 KiB of code instead of 265 KiB.  The
+// sig_tn): only those GEMM bodies are instantiated, ~90 KiB of code instead of ~320 KiB.  The
 // phases of a layer then run from a smaller code footprint (each phase's epilogue runs once
 // per layer, so its instructions are fetched anew every layer); results are the same as the
 // generic kernel's (SIG = 0), which serves every other plan.
